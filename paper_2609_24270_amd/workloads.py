@@ -1,0 +1,120 @@
+"""Seeded synthetic workloads shared by the tests, the benchmark and the oracle.
+
+This module only draws inputs: it holds none of the method's arithmetic (no
+product, no rounding beyond torch's own fp32->bf16 conversion of the draws, no
+scheduling), so the HIP path and the CPU oracle can both consume its output
+without sharing code.
+
+Recipe (one torch CPU generator per GEMM problem, seeded as listed):
+  * A is drawn first, then B, each in fp32 in its storage shape and converted
+    to bf16 with torch's round-to-nearest-even;
+  * uniform[-1,1]: torch.rand(...) * 2 - 1;  normal(0, s): torch.randn(...) * s;
+  * B is stored [N, K] (the K-contiguous weight layout); a [K, N] copy is the
+    transpose of the same logical matrix.
+The shapes are those of the paper's workload classes transplanted to a bf16
+GEMM: square GEMMs, and the three projection shapes of an 8B-class decoder
+layer (hidden 4096, FFN 14336, fused QKV 6144) with 4096 tokens.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import torch
+
+
+@dataclass(frozen=True)
+class GemmProblem:
+    name: str
+    M: int
+    N: int
+    K: int
+    seed: int
+    dist: str = "uniform"      # "uniform" | "llm" | "int"
+    a_sigma: float = 1.0       # llm: activation std
+    b_sigma: float = 0.02      # llm: weight std
+
+    @property
+    def flops(self) -> float:
+        return 2.0 * self.M * self.N * self.K
+
+
+# Square GEMM, 512^3, the small parity case (the oracle finishes in seconds).
+SQUARE_512 = GemmProblem("square_512", 512, 512, 512, seed=0)
+# Square GEMM, 8192^3, the headline full-GPU case.
+SQUARE_8192 = GemmProblem("square_8192", 8192, 8192, 8192, seed=1)
+# 8B-class decoder projections at 4096 tokens (FFN up, FFN down, fused QKV).
+LLM_SHAPES = (
+    GemmProblem("llm_ffn_up", 4096, 14336, 4096, seed=2, dist="llm"),
+    GemmProblem("llm_ffn_down", 4096, 4096, 14336, seed=2, dist="llm"),
+    GemmProblem("llm_qkv", 4096, 6144, 4096, seed=2, dist="llm"),
+)
+# Prefill / decode GEMMs multiplexed on two CU partitions (seed 3, one generator:
+# prefill A, B then decode A, B).
+PREFILL = GemmProblem("prefill", 8192, 4096, 4096, seed=3, dist="llm")
+DECODE = GemmProblem("decode", 32, 14336, 4096, seed=3, dist="llm")
+# Co-location sweep GEMM (seed 4), uniform inputs.
+COLOC = GemmProblem("coloc_4096", 4096, 4096, 4096, seed=4)
+COPY_BYTES = 64 << 20
+
+
+def _draw(g: torch.Generator, shape, dist: str, sigma: float) -> torch.Tensor:
+    if dist == "uniform":
+        x = torch.rand(shape, generator=g, dtype=torch.float32) * 2.0 - 1.0
+    elif dist == "normal":
+        x = torch.randn(shape, generator=g, dtype=torch.float32) * sigma
+    elif dist == "int":
+        # integers in {-2,...,2}: every partial sum of a K <= 2^20 dot product
+        # is an integer below 2^24, so fp32 accumulation is exact in any order
+        x = torch.randint(-2, 3, shape, generator=g).to(torch.float32)
+    else:
+        raise ValueError(dist)
+    return x.to(torch.bfloat16)
+
+
+def make_inputs_from(g: torch.Generator, p: GemmProblem):
+    """Draw (A [M,K], B [N,K]) bf16 CPU tensors for problem p from generator g."""
+    if p.dist == "llm":
+        A = _draw(g, (p.M, p.K), "normal", p.a_sigma)
+        B = _draw(g, (p.N, p.K), "normal", p.b_sigma)
+    else:
+        A = _draw(g, (p.M, p.K), p.dist, 1.0)
+        B = _draw(g, (p.N, p.K), p.dist, 1.0)
+    return A, B
+
+
+def make_inputs(p: GemmProblem):
+    """(A [M,K], B [N,K]) bf16 CPU tensors for p from a fresh generator."""
+    g = torch.Generator(device="cpu").manual_seed(p.seed)
+    return make_inputs_from(g, p)
+
+
+def make_pd_inputs():
+    """Prefill then decode inputs from one generator seeded 3."""
+    g = torch.Generator(device="cpu").manual_seed(PREFILL.seed)
+    pa, pb = make_inputs_from(g, PREFILL)
+    da, db = make_inputs_from(g, DECODE)
+    return (pa, pb), (da, db)
+
+
+def make_problem(M: int, N: int, K: int, seed: int, dist: str = "uniform") -> GemmProblem:
+    return GemmProblem(f"gemm_{M}x{N}x{K}", M, N, K, seed=seed, dist=dist)
+
+
+def random_mask_bits(seed: int, n_masks: int, n_bits: int, total: int = 256):
+    """n_masks seeded random subsets of n_bits CU-mask bit positions out of total.
+
+    Each subset is the first n_bits entries of a seeded permutation, drawn the
+    way a topology-oblivious user would pick CUs: over mask bits, by count.
+    """
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    out = []
+    for _ in range(n_masks):
+        perm = torch.randperm(total, generator=g)
+        out.append(sorted(int(b) for b in perm[:n_bits]))
+    return out
+
+
+def copy_source(n_elems: int, seed: int = COLOC.seed + 1000) -> torch.Tensor:
+    """Arbitrary bf16 bit patterns (finite) for the streaming-copy source."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    return (torch.rand(n_elems, generator=g) * 2 - 1).to(torch.bfloat16)
