@@ -1,0 +1,277 @@
+/*
+ * asym: asymmetry-aware scheduling of a persistent bf16 GEMM on MI355X (gfx950).
+ *
+ * C ABI of libasym.so.  Plain C types only: device buffers are `void*` device
+ * pointers, streams are `void*` hipStream_t handles, host arrays are plain
+ * pointers with explicit sizes.
+ *
+ * The calls follow the paper's problem statement ("Dissecting How Die Scaling
+ * Breaks GPU Fine-grained Scheduling"):
+ *   - discover the chip's hidden compute topology and memory affinity per chip
+ *     (Introduction, challenge C-1; Section 5.1 topology discovery;
+ *     Section 6.1 latency-based affinity discovery; Appendix G for the
+ *     XCD-level variant on AMD parts);
+ *   - run a kernel on an allocated set of compute units, assigning work by the
+ *     physical unit it lands on (Section 7.1: persistent blocks, affinity-based
+ *     static task assignment, work in proportion to each partition's units);
+ *   - co-run kernels on partitioned unit sets (Sections 7.2 and 7.3), choosing
+ *     which units, not only how many (Section 7.4, lessons).
+ *
+ * Conventions
+ *   Return value: every call returning int returns an asym_status; 0 is
+ *   success.  On failure, asym_last_error() returns a message for the calling
+ *   thread (valid until that thread's next call into the library).  No call
+ *   aborts the process on bad input.
+ *   Ownership: the library owns asym_topology objects (free with
+ *   asym_topology_free), the streams it creates (destroy with
+ *   asym_stream_destroy) and its internal device workspace (schedules,
+ *   counters; kept for the life of the process).  All matrix and copy
+ *   buffers are owned by the caller; the library never frees them.
+ *   Devices: one GPU at a time; `device` is a HIP device ordinal.
+ *   Asynchrony: asym_gemm_bf16 and asym_copy_bf16 enqueue work on the given
+ *   stream and return; probes, asym_corun and asym_copy_bandwidth synchronise.
+ */
+#ifndef ASYM_H
+#define ASYM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ASYM_MASK_WORDS 8 /* 256 compute units, one bit each */
+#define ASYM_MAX_XCDS 16
+#define ASYM_MAX_CUS (ASYM_MASK_WORDS * 32)
+
+typedef enum asym_status {
+  ASYM_OK = 0,
+  ASYM_EINVAL = -1,       /* bad argument (null pointer, size, layout, mask) */
+  ASYM_EHIP = -2,         /* a HIP runtime call failed; message has its text */
+  ASYM_EUNSUPPORTED = -3, /* valid request the library or device cannot serve */
+  ASYM_ETIMEOUT = -4,     /* a watched device wait did not finish in time */
+  ASYM_EINVARIANT = -5,   /* a topology map violates its exact invariants */
+  ASYM_ENOMEM = -6        /* host or device allocation failed */
+} asym_status;
+
+/* Tile-to-compute-unit mappings of the persistent GEMM (Section 7.1). */
+typedef enum asym_mapping {
+  /* Each workgroup reads the XCD it runs on and takes tiles from that XCD's
+   * region; regions hold tile counts proportional to the XCD's CUs and are
+   * contiguous runs of a banded column-major tile order, so the tiles an XCD
+   * runs at once share A rows and B columns in its L2. */
+  ASYM_MAP_AWARE = 0,
+  /* Same banded order, tile i to persistent workgroup i mod P: with the
+   * hardware's round-robin workgroup-to-XCD dispatch, neighbouring tiles land
+   * on different XCDs (the usual single-L2 "grouped" order). */
+  ASYM_MAP_OBLIVIOUS_GROUPED = 1,
+  /* Row-major tile order, tile i to workgroup i mod P. */
+  ASYM_MAP_OBLIVIOUS_ROWMAJOR = 2
+} asym_mapping;
+
+/* Storage of the B operand of C = A . B. */
+typedef enum asym_b_layout {
+  ASYM_B_NK = 0, /* B stored transposed, [N][ldb] row-major, K contiguous */
+  ASYM_B_KN = 1  /* B stored [K][ldb] row-major (not served: ASYM_EUNSUPPORTED) */
+} asym_b_layout;
+
+/* What asym_probe_topology measures. */
+typedef enum asym_probe_flags {
+  ASYM_PROBE_IDENTITY = 1, /* XCC/SE/SH/CU of every CU from hardware IDs */
+  ASYM_PROBE_MASKMAP = 2,  /* CU-mask bit -> physical CU map (implies IDENTITY) */
+  ASYM_PROBE_LATENCY = 4   /* per-XCD L2 / memory-side-cache / HBM latency */
+} asym_probe_flags;
+
+/* CU-set policies for asym_cuset_make (Section 7.3; lessons of Section 7.4:
+ * tenants state topology requirements, not only counts). */
+typedef enum asym_cuset_policy {
+  ASYM_CUSET_XCD_ALIGNED = 0,      /* whole XCDs, lowest free XCD ids first */
+  ASYM_CUSET_AFFINITY_ALIGNED = 1, /* whole XCDs, filling one affinity group first */
+  ASYM_CUSET_STRIPED = 2,          /* the same share of every XCD, SE-balanced */
+  ASYM_CUSET_RANDOM = 3            /* seeded uniform choice among free CUs */
+} asym_cuset_policy;
+
+/* a1: device and partition-mode discovery. */
+typedef struct asym_device_info {
+  int n_cus;          /* hipDeviceAttributeMultiprocessorCount */
+  int n_xccs;         /* hipDeviceAttributeNumberOfXccs */
+  int n_cus_physical; /* hipDeviceAttributePhysicalMultiProcessorCount */
+  int clock_khz;      /* peak shader clock */
+  int wall_clock_khz; /* rate of the constant-rate counter read by s_memrealtime */
+  int lds_bytes_per_cu;
+  int l2_bytes;       /* per XCD as reported by the runtime */
+  size_t hbm_bytes;
+  char arch[64];      /* gcnArchName, e.g. "gfx950:sramecc+:xnack-" */
+} asym_device_info;
+
+typedef struct asym_topology asym_topology; /* opaque, library-owned */
+
+/* Per-XCD latency tiers in shader-clock cycles (a4; Section 6.1 access latency
+ * distribution, Appendix C kernels, Appendix G per-XCD probing).  Arrays are
+ * indexed by XCD; values < 0 mean "not measured". */
+typedef struct asym_latency_summary {
+  int n_xcds;
+  int n_samples;                   /* addresses sampled per regime */
+  double l2_hit[ASYM_MAX_XCDS];    /* mean latency, line warm in the XCD's L2 */
+  double mall_hit[ASYM_MAX_XCDS];  /* L2 bypassed, line in the memory-side cache */
+  double hbm[ASYM_MAX_XCDS];       /* L2 bypassed, memory-side cache flushed */
+  int group_of_xcd[ASYM_MAX_XCDS]; /* affinity group id of each XCD */
+  int n_groups;
+  double home_share[ASYM_MAX_XCDS];/* fraction of addresses homed on each group */
+} asym_latency_summary;
+
+/* ---- a1: device discovery ---------------------------------------------- */
+/* Fill *out from the HIP runtime.  Errors: ASYM_EINVAL (null out),
+ * ASYM_EHIP. */
+int asym_device_query(int device, asym_device_info* out);
+
+/* ---- a2-a4: topology probe (Section 5.1, Section 6.1, Appendix G) ------- */
+/* Probe `device` and return a new topology map in *out.
+ * IDENTITY launches an oversubscribed kernel whose workgroups record
+ * XCC_ID and HW_ID; the distinct (xcc, se, sh, cu) tuples, sorted, are the
+ * CU records with dense indices 0..n-1.  MASKMAP launches the same kernel once
+ * per mask bit on a stream whose CU mask has every bit but that one, and maps
+ * the bit to the one CU that never appears.  LATENCY runs a single-lane
+ * pointer chase from each XCD (see asym_latency_summary).
+ * The map is checked against its exact invariants (every CU once, per-XCD
+ * counts summing to the device CU count, mask map a bijection); a violation
+ * returns ASYM_EINVARIANT and no map.  Synchronous.
+ * Errors: ASYM_EINVAL, ASYM_EHIP, ASYM_EINVARIANT, ASYM_ETIMEOUT. */
+int asym_probe_topology(int device, unsigned flags, asym_topology** out);
+
+/* Build a topology from raw identity records without a GPU (host only).
+ * records: n_records rows of 4 int32 {xcc_id register, hw_id register,
+ * block index, unused}.  n_cus_expected / n_xccs_expected are the device's
+ * counts the invariants are checked against.  mask_bit_cu (nullable): for each
+ * mask bit b < n_cus_expected, the index into `records` of a record of the CU
+ * that bit controls (-1 if unknown).  Errors: ASYM_EINVAL, ASYM_EINVARIANT. */
+int asym_topology_from_records(const int32_t* records, int n_records,
+                               int n_cus_expected, int n_xccs_expected,
+                               const int32_t* mask_bit_record,
+                               asym_topology** out);
+
+void asym_topology_free(asym_topology* topo);
+
+/* Counts of the map.  cus_per_xcd and group_of_xcd (nullable) must hold
+ * ASYM_MAX_XCDS ints; group ids are -1 without a latency probe. */
+int asym_topology_info(const asym_topology* topo, int* n_cus, int* n_xcds,
+                       int* cus_per_xcd, int* group_of_xcd);
+
+/* Record of dense CU `cu_index`: XCC, shader engine, shader array, CU id
+ * within its array, and the CU-mask bit controlling it (-1 if no mask map). */
+int asym_topology_cu(const asym_topology* topo, int cu_index, int* xcc,
+                     int* se, int* sh, int* cu, int* mask_bit);
+
+/* Fraction of a full-grid probe launch whose workgroup b ran on XCC b mod
+ * n_xccs (1.0 = round-robin dispatch).  Written by the IDENTITY probe. */
+int asym_topology_dispatch(const asym_topology* topo, double* rr_fraction);
+
+/* a4 results; ASYM_EUNSUPPORTED if the map was probed without LATENCY. */
+int asym_topology_latency(const asym_topology* topo, asym_latency_summary* out);
+
+/* JSON text of the map into buf (len bytes incl. NUL); *needed receives the
+ * size required.  Returns ASYM_EINVAL if buf is too small (needed still set). */
+int asym_topology_json(const asym_topology* topo, char* buf, size_t len,
+                       size_t* needed);
+
+/* ---- CU sets and masked streams (a3, a7) -------------------------------- */
+/* Choose n_cus compute units by `policy` among the CUs not in `exclude`
+ * (nullable), and write their CU-mask bits to mask_out[ASYM_MASK_WORDS].
+ * Needs a topology probed with MASKMAP.  XCD-aligned policies need n_cus to be
+ * a whole number of XCDs.  Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED. */
+int asym_cuset_make(const asym_topology* topo, int n_cus, int policy,
+                    uint64_t seed, const uint32_t* exclude, uint32_t* mask_out);
+
+/* Per-XCD CU counts of a mask (mask bits, ASYM_MASK_WORDS words). */
+int asym_cuset_counts(const asym_topology* topo, const uint32_t* mask,
+                      int* per_xcd /* ASYM_MAX_XCDS */);
+
+/* Create a stream whose queue may only use the CUs in `mask`
+ * (hipExtStreamCreateWithCUMask).  The mask must leave every XCD at least one
+ * CU (a queue with an empty XCD is refused: ASYM_EUNSUPPORTED), which needs a
+ * topology with a mask map; mask == NULL gives an unmasked stream.  *out
+ * receives a hipStream_t.  Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
+int asym_stream_create(const asym_topology* topo, const uint32_t* mask,
+                       void** out);
+int asym_stream_destroy(void* stream);
+
+/* ---- a5: tile schedule (host only) -------------------------------------- */
+/* Tile order for a tiles_m x tiles_n grid under `mapping`, for n_xcds XCDs
+ * with slots[x] persistent workgroups each (0 = XCD excluded).
+ * order[tiles_m*tiles_n] receives tile ids (row*tiles_n + col); for AWARE the
+ * tiles of XCD x are order[off[x] .. off[x+1]), off has n_xcds+1 entries, and
+ * quota[x] = off[x+1]-off[x] is proportional to slots[x] (largest remainder,
+ * ties to the lower XCD).  For the oblivious mappings off/quota describe which
+ * XCD round-robin dispatch sends each order position to.  band = tile rows per
+ * band of the banded order (0 = chosen from the slots).
+ * Errors: ASYM_EINVAL. */
+int asym_schedule_build(int tiles_m, int tiles_n, int n_xcds,
+                        const int* slots, int mapping, int band, int* order,
+                        int* off, int* quota);
+
+/* ---- a6: persistent bf16 GEMM (Section 7.1) ----------------------------- */
+/* C = A . B, bf16 inputs, fp32 accumulation, bf16 round-to-nearest-even
+ * output.  A: [M][lda] row-major.  B: ASYM_B_NK, [N][ldb] row-major (the
+ * logical B is its transpose).  C: [M][ldc] row-major.  Requires M, N, K >= 1,
+ * lda >= K, ldb >= K, ldc >= N; 16-byte aligned pointers with lda, ldb, K
+ * multiples of 8 and ldc a multiple of 4 take the vector path, anything else a
+ * slower fully predicated path.  The CU set scheduled for is the stream's CU
+ * mask (hipExtStreamGetCUMask) restricted to the XCDs in xcd_mask (bit x =
+ * XCD x; 0 = all); workgroups landing on other XCDs exit at once.  topo may be
+ * NULL (a per-device identity probe made on first use is taken); a stream
+ * with a partial CU mask needs a topology with a mask map.  Accumulation order
+ * differs from a sequential sum but not between mappings: results are bitwise
+ * identical across mappings, CU masks and runs.  Asynchronous on `stream`.
+ * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
+int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K,
+                   const void* A, int lda, const void* B, int ldb,
+                   int b_layout, void* C, int ldc, int mapping,
+                   uint32_t xcd_mask, void* stream);
+
+/* ---- a7: streaming copy and co-run (Sections 7.2, 7.3) ------------------ */
+/* dst[i] = src[i] for n_bytes bytes (16-byte aligned, n_bytes a multiple of
+ * 16), `passes` times over the buffer, with 16-byte accesses from every lane.
+ * If stop_flag (device int, nullable) becomes nonzero the kernel ends after
+ * the pass in progress; it always ends after `passes` passes.  On XCDs outside
+ * xcd_mask (0 = all) workgroups exit at once.  Asynchronous.
+ * Errors: ASYM_EINVAL, ASYM_EHIP. */
+int asym_copy_bf16(void* dst, const void* src, size_t n_bytes, int passes,
+                   const int* stop_flag, uint32_t xcd_mask, void* stream);
+
+/* One task of a co-run: a GEMM or a streaming copy on its own CU set. */
+typedef struct asym_task {
+  int kind;        /* 0 = GEMM, 1 = streaming copy */
+  uint32_t mask[ASYM_MASK_WORDS]; /* CU-mask bits; all-zero = all CUs */
+  uint32_t xcd_mask;              /* whole-XCD restriction, 0 = none */
+  int iters;       /* GEMM launches, or copy passes */
+  int mapping;     /* GEMM mapping */
+  int M, N, K;     /* GEMM shape, dense row-major A, B ([N][K]), C */
+  const void* A; const void* B; void* C;
+  const void* src; void* dst; size_t n_bytes; /* copy */
+} asym_task;
+
+typedef struct asym_task_result {
+  double ms_total;    /* first launch start to last launch end */
+  double ms_per_iter;
+  double tflops;      /* GEMM */
+  double gbps;        /* copy: bytes read + written per second / 1e9 */
+  int iters_done;
+} asym_task_result;
+
+/* Run tasks concurrently, each on its own stream (masked streams for partial
+ * masks, unmasked streams with XCD filtering for whole-XCD sets).  All tasks
+ * are released together; a copy task with iters <= 0 runs until every GEMM
+ * task has finished (bounded at 100000 passes).  Synchronous.
+ * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
+int asym_corun(const asym_topology* topo, const asym_task* tasks, int n_tasks,
+               asym_task_result* out);
+
+/* ---- misc ---------------------------------------------------------------- */
+const char* asym_last_error(void);
+int asym_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ASYM_H */

@@ -1,0 +1,88 @@
+"""Oracle for the tile schedule.  TEST INFRASTRUCTURE ONLY.
+
+Section 7.1 assigns each persistent block the tasks local to its partition and
+spreads the work over partitions in proportion to their compute units; the
+full-GPU lesson of Section 7.4 restates the proportional rule.  "In proportion"
+with whole tiles is an apportionment problem; the reading taken here is
+Hamilton's largest-remainder method (each partition first gets the floor of its
+exact share T*w_x/W, and the tiles left over go one each to the largest
+fractional remainders, ties to the lower partition index).
+
+The tile order is the banded column-major walk: tile rows are cut into bands of
+`band` rows, each band is walked column by column, top to bottom.  AWARE gives
+partition x the contiguous run of the order of length quota[x], partitions in
+index order; the oblivious mappings hand order position i to workgroup i mod P,
+which round-robin dispatch places on partition (i mod P) mod n.
+
+Written from the definitions with exact rational arithmetic; no code is shared
+with the library.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+
+def hamilton_quotas(total: int, weights):
+    W = sum(weights)
+    if W <= 0 or total <= 0:
+        return [0] * len(weights)
+    shares = [Fraction(total * w, W) for w in weights]
+    q = [int(s) for s in shares]            # floor (shares are >= 0)
+    left = total - sum(q)
+    rema = [(s - int(s), -i) for i, s in enumerate(shares)]
+    ranked = sorted(range(len(weights)), key=lambda i: rema[i], reverse=True)
+    for i in ranked:
+        if left == 0:
+            break
+        if weights[i] > 0:
+            q[i] += 1
+            left -= 1
+    return q
+
+
+def banded_order(tiles_m: int, tiles_n: int, band: int):
+    order = []
+    r0 = 0
+    while r0 < tiles_m:
+        rows = range(r0, min(tiles_m, r0 + band))
+        for c in range(tiles_n):
+            for r in rows:
+                order.append(r * tiles_n + c)
+        r0 += band
+    return order
+
+
+def rowmajor_order(tiles_m: int, tiles_n: int):
+    return list(range(tiles_m * tiles_n))
+
+
+def aware_assignment(tiles_m, tiles_n, slots, band):
+    """tile id -> partition, for the aware mapping."""
+    order = banded_order(tiles_m, tiles_n, band)
+    q = hamilton_quotas(len(order), slots)
+    owner = {}
+    pos = 0
+    for x, qx in enumerate(q):
+        for t in order[pos:pos + qx]:
+            owner[t] = x
+        pos += qx
+    return owner, q
+
+
+def oblivious_assignment(order, slots):
+    """tile id -> partition under round-robin dispatch of workgroup i mod P."""
+    P = sum(slots)
+    n = len(slots)
+    return {t: (i % P) % n for i, t in enumerate(order)}
+
+
+def band_cost_choice(tiles_m: int, s: int) -> int:
+    """Band height minimising band + ceil(s/band); ties to a band dividing
+    tiles_m, then to the taller band."""
+    s = max(1, s)
+    best = None
+    for h in range(1, min(tiles_m, s) + 1):
+        key = (h + -(-s // h), 0 if tiles_m % h == 0 else 1, -h)
+        if best is None or key < best[0]:
+            best = (key, h)
+    return best[1]

@@ -1,0 +1,375 @@
+"""asym: asymmetry-aware persistent bf16 GEMM scheduling for MI355X (gfx950).
+
+Thin ctypes binding of libasym.so (C ABI in include/asym.h).  Every step of
+the hot path runs in the library's HIP kernels; this module only marshals
+arguments (tensor data pointers, stream handles, host arrays).  PyTorch is used
+for device memory and streams.  There is no fallback: if libasym.so is missing
+or fails to load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import json
+import os
+from typing import Optional, Sequence
+
+from . import workloads  # noqa: F401  (seeded inputs; no method arithmetic)
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libasym.so")
+
+MASK_WORDS = 8
+MAX_XCDS = 16
+MAX_CUS = MASK_WORDS * 32
+
+OK, EINVAL, EHIP, EUNSUPPORTED, ETIMEOUT, EINVARIANT, ENOMEM = 0, -1, -2, -3, -4, -5, -6
+MAP_AWARE, MAP_OBLIVIOUS_GROUPED, MAP_OBLIVIOUS_ROWMAJOR = 0, 1, 2
+MAPPINGS = {"aware": MAP_AWARE, "oblivious_grouped": MAP_OBLIVIOUS_GROUPED,
+            "oblivious_rowmajor": MAP_OBLIVIOUS_ROWMAJOR}
+B_NK, B_KN = 0, 1
+PROBE_IDENTITY, PROBE_MASKMAP, PROBE_LATENCY = 1, 2, 4
+CUSET_XCD_ALIGNED, CUSET_AFFINITY_ALIGNED, CUSET_STRIPED, CUSET_RANDOM = 0, 1, 2, 3
+
+# Every function the C ABI exports (include/asym.h), in declaration order.
+EXPORTS = (
+    "asym_device_query", "asym_probe_topology", "asym_topology_from_records",
+    "asym_topology_free", "asym_topology_info", "asym_topology_cu",
+    "asym_topology_dispatch", "asym_topology_latency", "asym_topology_json",
+    "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
+    "asym_stream_destroy", "asym_schedule_build", "asym_gemm_bf16",
+    "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
+)
+
+
+class AsymError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"asym error {status}: {msg}")
+        self.status = status
+
+
+class DeviceInfo(ctypes.Structure):
+    _fields_ = [("n_cus", ctypes.c_int), ("n_xccs", ctypes.c_int),
+                ("n_cus_physical", ctypes.c_int), ("clock_khz", ctypes.c_int),
+                ("wall_clock_khz", ctypes.c_int), ("lds_bytes_per_cu", ctypes.c_int),
+                ("l2_bytes", ctypes.c_int), ("hbm_bytes", ctypes.c_size_t),
+                ("arch", ctypes.c_char * 64)]
+
+
+class LatencySummary(ctypes.Structure):
+    _fields_ = [("n_xcds", ctypes.c_int), ("n_samples", ctypes.c_int),
+                ("l2_hit", ctypes.c_double * MAX_XCDS),
+                ("mall_hit", ctypes.c_double * MAX_XCDS),
+                ("hbm", ctypes.c_double * MAX_XCDS),
+                ("group_of_xcd", ctypes.c_int * MAX_XCDS),
+                ("n_groups", ctypes.c_int),
+                ("home_share", ctypes.c_double * MAX_XCDS)]
+
+
+class Task(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("mask", ctypes.c_uint32 * MASK_WORDS),
+                ("xcd_mask", ctypes.c_uint32), ("iters", ctypes.c_int),
+                ("mapping", ctypes.c_int), ("M", ctypes.c_int), ("N", ctypes.c_int),
+                ("K", ctypes.c_int), ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
+                ("C", ctypes.c_void_p), ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p),
+                ("n_bytes", ctypes.c_size_t)]
+
+
+class TaskResult(ctypes.Structure):
+    _fields_ = [("ms_total", ctypes.c_double), ("ms_per_iter", ctypes.c_double),
+                ("tflops", ctypes.c_double), ("gbps", ctypes.c_double),
+                ("iters_done", ctypes.c_int)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libasym.so and declare its signatures; raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise AsymError(EUNSUPPORTED, f"{path} is not built; run paper_2609_24270_amd.build")
+    lib = ctypes.CDLL(path)
+    i, u32, vp, cp = ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_char_p
+    ip = ctypes.POINTER(ctypes.c_int)
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    topo_p = ctypes.c_void_p
+    sig = {
+        "asym_device_query": (i, [i, ctypes.POINTER(DeviceInfo)]),
+        "asym_probe_topology": (i, [i, ctypes.c_uint, ctypes.POINTER(topo_p)]),
+        "asym_topology_from_records": (i, [ctypes.POINTER(ctypes.c_int32), i, i, i,
+                                           ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(topo_p)]),
+        "asym_topology_free": (None, [topo_p]),
+        "asym_topology_info": (i, [topo_p, ip, ip, ip, ip]),
+        "asym_topology_cu": (i, [topo_p, i, ip, ip, ip, ip, ip]),
+        "asym_topology_dispatch": (i, [topo_p, ctypes.POINTER(ctypes.c_double)]),
+        "asym_topology_latency": (i, [topo_p, ctypes.POINTER(LatencySummary)]),
+        "asym_topology_json": (i, [topo_p, cp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
+        "asym_cuset_make": (i, [topo_p, i, i, ctypes.c_uint64, u32p, u32p]),
+        "asym_cuset_counts": (i, [topo_p, u32p, ip]),
+        "asym_stream_create": (i, [topo_p, u32p, ctypes.POINTER(vp)]),
+        "asym_stream_destroy": (i, [vp]),
+        "asym_schedule_build": (i, [i, i, i, ip, i, i, ip, ip, ip]),
+        "asym_gemm_bf16": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp]),
+        "asym_copy_bf16": (i, [vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
+        "asym_corun": (i, [topo_p, ctypes.POINTER(Task), i, ctypes.POINTER(TaskResult)]),
+        "asym_last_error": (cp, []),
+        "asym_version": (i, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != OK:
+        msg = load_library().asym_last_error()
+        raise AsymError(rc, msg.decode() if msg else "")
+
+
+def _ints(vals: Sequence[int]):
+    arr = (ctypes.c_int * max(1, len(vals)))(*vals)
+    return arr
+
+
+def mask_words(bits: Optional[Sequence[int]]):
+    """CU-mask bit positions -> ctypes uint32[8] (None -> None)."""
+    if bits is None:
+        return None
+    m = (ctypes.c_uint32 * MASK_WORDS)()
+    for b in bits:
+        if not 0 <= b < MAX_CUS:
+            raise ValueError(f"mask bit {b} out of range")
+        m[b >> 5] |= 1 << (b & 31)
+    return m
+
+
+def mask_bits(words) -> list:
+    return [w * 32 + b for w in range(MASK_WORDS) for b in range(32) if (words[w] >> b) & 1]
+
+
+# ---- a1 ---------------------------------------------------------------------
+
+def device_query(device: int = 0) -> dict:
+    info = DeviceInfo()
+    _check(load_library().asym_device_query(device, ctypes.byref(info)))
+    d = {k: getattr(info, k) for k, _ in DeviceInfo._fields_}
+    d["arch"] = info.arch.decode()
+    return d
+
+
+# ---- a2-a4 topology -----------------------------------------------------------
+
+class Topology:
+    """A probed (or record-built) topology map; owns the library object."""
+
+    def __init__(self, handle: int):
+        self._h = ctypes.c_void_p(handle)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value and _lib is not None:
+            _lib.asym_topology_free(self._h)
+            self._h = ctypes.c_void_p(0)
+
+    def info(self) -> dict:
+        n_cus, n_xcds = ctypes.c_int(), ctypes.c_int()
+        per = (ctypes.c_int * MAX_XCDS)()
+        grp = (ctypes.c_int * MAX_XCDS)()
+        _check(load_library().asym_topology_info(self._h, ctypes.byref(n_cus), ctypes.byref(n_xcds), per, grp))
+        nx = n_xcds.value
+        return {"n_cus": n_cus.value, "n_xcds": nx, "cus_per_xcd": list(per)[:nx],
+                "group_of_xcd": list(grp)[:nx]}
+
+    def cu(self, idx: int) -> dict:
+        vals = [ctypes.c_int() for _ in range(5)]
+        _check(load_library().asym_topology_cu(self._h, idx, *[ctypes.byref(v) for v in vals]))
+        return dict(zip(("xcc", "se", "sh", "cu", "mask_bit"), (v.value for v in vals)))
+
+    def cus(self) -> list:
+        return [self.cu(i) for i in range(self.info()["n_cus"])]
+
+    def dispatch_rr_fraction(self) -> float:
+        v = ctypes.c_double()
+        _check(load_library().asym_topology_dispatch(self._h, ctypes.byref(v)))
+        return v.value
+
+    def latency(self) -> dict:
+        s = LatencySummary()
+        _check(load_library().asym_topology_latency(self._h, ctypes.byref(s)))
+        nx = s.n_xcds
+        return {"n_samples": s.n_samples, "l2_hit": list(s.l2_hit)[:nx],
+                "mall_hit": list(s.mall_hit)[:nx], "hbm": list(s.hbm)[:nx],
+                "group_of_xcd": list(s.group_of_xcd)[:nx], "n_groups": s.n_groups,
+                "home_share": list(s.home_share)[:s.n_groups]}
+
+    def json(self) -> dict:
+        lib = load_library()
+        need = ctypes.c_size_t()
+        lib.asym_topology_json(self._h, None, 0, ctypes.byref(need))
+        buf = ctypes.create_string_buffer(need.value)
+        _check(lib.asym_topology_json(self._h, buf, need.value, ctypes.byref(need)))
+        return json.loads(buf.value.decode())
+
+    def cuset(self, n_cus: int, policy: int, seed: int = 0, exclude: Optional[Sequence[int]] = None) -> list:
+        out = (ctypes.c_uint32 * MASK_WORDS)()
+        _check(load_library().asym_cuset_make(self._h, n_cus, policy, seed, mask_words(exclude), out))
+        return mask_bits(out)
+
+    def cuset_counts(self, bits: Sequence[int]) -> list:
+        per = (ctypes.c_int * MAX_XCDS)()
+        _check(load_library().asym_cuset_counts(self._h, mask_words(bits), per))
+        return list(per)[: self.info()["n_xcds"]]
+
+
+def probe_topology(device: int = 0, flags: int = PROBE_IDENTITY) -> Topology:
+    h = ctypes.c_void_p()
+    _check(load_library().asym_probe_topology(device, flags, ctypes.byref(h)))
+    return Topology(h.value)
+
+
+def topology_from_records(records, n_cus: int, n_xccs: int, mask_bit_record=None) -> Topology:
+    import numpy as np
+    rec = np.ascontiguousarray(records, dtype=np.int32).reshape(-1, 4)
+    mb = None
+    if mask_bit_record is not None:
+        mb = np.ascontiguousarray(mask_bit_record, dtype=np.int32)
+    h = ctypes.c_void_p()
+    _check(load_library().asym_topology_from_records(
+        rec.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), rec.shape[0], n_cus, n_xccs,
+        mb.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if mb is not None else None,
+        ctypes.byref(h)))
+    return Topology(h.value)
+
+
+# ---- a5 schedule ----------------------------------------------------------------
+
+def schedule_build(tiles_m: int, tiles_n: int, slots: Sequence[int], mapping: int, band: int = 0):
+    n_x = len(slots)
+    T = tiles_m * tiles_n
+    order = (ctypes.c_int * T)()
+    off = (ctypes.c_int * (n_x + 1))()
+    quota = (ctypes.c_int * n_x)()
+    _check(load_library().asym_schedule_build(tiles_m, tiles_n, n_x, _ints(slots), mapping, band,
+                                              order, off, quota))
+    return list(order), list(off), list(quota)
+
+
+# ---- streams ---------------------------------------------------------------------
+
+def stream_create(topo: Optional[Topology] = None, mask: Optional[Sequence[int]] = None):
+    """A library stream (optionally CU-masked) wrapped as torch.cuda.ExternalStream."""
+    import torch
+    h = ctypes.c_void_p()
+    _check(load_library().asym_stream_create(topo.handle if topo else None, mask_words(mask),
+                                             ctypes.byref(h)))
+    return torch.cuda.ExternalStream(h.value)
+
+
+def stream_destroy(stream) -> None:
+    _check(load_library().asym_stream_destroy(ctypes.c_void_p(stream.cuda_stream)))
+
+
+def _stream_ptr(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+# ---- a6 GEMM -----------------------------------------------------------------------
+
+def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mask: int = 0,
+         stream=None):
+    """C = A . B^T for bf16 CUDA tensors A [M,K] and B [N,K] (B's [N][K] storage).
+
+    Launches the persistent HIP kernel asynchronously on `stream` (default:
+    torch's current stream) and returns C.
+    """
+    import torch
+    if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16:
+        raise TypeError("A and B must be bfloat16")
+    if A.dim() != 2 or B.dim() != 2 or A.shape[1] != B.shape[1]:
+        raise ValueError("A must be [M,K] and B [N,K]")
+    if not (A.is_cuda and B.is_cuda):
+        raise ValueError("A and B must be on the GPU")
+    if A.stride(1) != 1 or B.stride(1) != 1:
+        raise ValueError("A and B must be K-contiguous")
+    M, K = A.shape
+    N = B.shape[0]
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.bfloat16, device=A.device)
+    if C.dtype != torch.bfloat16 or C.shape != (M, N) or C.stride(1) != 1:
+        raise ValueError("C must be a row-major bf16 [M,N] tensor")
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    _check(load_library().asym_gemm_bf16(
+        topo.handle if topo else None, M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0),
+        ctypes.c_void_p(B.data_ptr()), B.stride(0), B_NK, ctypes.c_void_p(C.data_ptr()),
+        C.stride(0), mp, xcd_mask, _stream_ptr(stream)))
+    return C
+
+
+# ---- a7 copy and co-run --------------------------------------------------------------
+
+def copy(dst, src, passes: int = 1, stop_flag=None, xcd_mask: int = 0, stream=None):
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n:
+        raise ValueError("size mismatch")
+    _check(load_library().asym_copy_bf16(
+        ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), n, passes,
+        ctypes.c_void_p(stop_flag.data_ptr()) if stop_flag is not None else None, xcd_mask,
+        _stream_ptr(stream)))
+    return dst
+
+
+def gemm_task(A, B, C, iters: int, mapping="aware", mask=None, xcd_mask: int = 0) -> Task:
+    t = Task()
+    t.kind = 0
+    if mask is not None:
+        m = mask_words(mask)
+        for w in range(MASK_WORDS):
+            t.mask[w] = m[w]
+    t.xcd_mask = xcd_mask
+    t.iters = iters
+    t.mapping = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    t.M, t.K = A.shape
+    t.N = B.shape[0]
+    t.A, t.B, t.C = A.data_ptr(), B.data_ptr(), C.data_ptr()
+    return t
+
+
+def copy_task(dst, src, passes: int = 0, mask=None, xcd_mask: int = 0) -> Task:
+    t = Task()
+    t.kind = 1
+    if mask is not None:
+        m = mask_words(mask)
+        for w in range(MASK_WORDS):
+            t.mask[w] = m[w]
+    t.xcd_mask = xcd_mask
+    t.iters = passes
+    t.src, t.dst = src.data_ptr(), dst.data_ptr()
+    t.n_bytes = src.numel() * src.element_size()
+    return t
+
+
+def corun(tasks: Sequence[Task], topo: Optional[Topology] = None) -> list:
+    n = len(tasks)
+    arr = (Task * n)(*tasks)
+    res = (TaskResult * n)()
+    _check(load_library().asym_corun(topo.handle if topo else None, arr, n, res))
+    return [{k: getattr(r, k) for k, _ in TaskResult._fields_} for r in res]
+
+
+def last_error() -> str:
+    return load_library().asym_last_error().decode()
+
+
+def version() -> int:
+    return load_library().asym_version()

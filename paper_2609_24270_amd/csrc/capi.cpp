@@ -1,0 +1,341 @@
+// C ABI of libasym: argument checking, device discovery, per-stream device
+// workspaces, schedule caching, masked streams, and the co-run harness.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <thread>
+#include <tuple>
+
+#include "internal.h"
+
+struct asym_topology;
+
+namespace asym {
+
+const Topology* unwrap(const asym_topology* p);
+asym_topology* wrap_topology(Topology&& t);
+int gemm_tile_m();
+int gemm_tile_n();
+
+static thread_local std::string g_last_error;
+
+int fail(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return ASYM_EHIP;
+}
+
+// ---- process-wide state, guarded by one mutex --------------------------------
+namespace {
+
+std::mutex g_mu;
+
+struct ScheduleKey {
+  int device, tiles_m, tiles_n, mapping;
+  std::vector<int> slots;
+  bool operator<(const ScheduleKey& o) const {
+    return std::tie(device, tiles_m, tiles_n, mapping, slots) <
+           std::tie(o.device, o.tiles_m, o.tiles_n, o.mapping, o.slots);
+  }
+};
+struct DeviceSchedule {
+  int* d_order = nullptr;
+  int* d_off = nullptr;    // [ASYM_MAX_XCDS + 1]
+  int* d_slots = nullptr;  // [ASYM_MAX_XCDS]
+};
+std::map<ScheduleKey, DeviceSchedule> g_schedules;  // never freed: kernels may still read them
+
+// Device counters per (device, stream): launches on one stream run in order
+// and the kernels leave their counters zeroed, so one block per stream does.
+struct Workspace {
+  int* gemm_ctr = nullptr;                  // 64 ints
+  unsigned long long* copy_ctr = nullptr;   // 4 words
+};
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+std::map<int, std::unique_ptr<Topology>> g_default_topo;
+
+}  // namespace
+
+static int get_workspace(int device, hipStream_t s, Workspace** out) {
+  auto key = std::make_pair(device, s);
+  auto it = g_ws.find(key);
+  if (it == g_ws.end()) {
+    Workspace w;
+    ASYM_HIP(hipMalloc(&w.gemm_ctr, 64 * sizeof(int)));
+    ASYM_HIP(hipMalloc(&w.copy_ctr, 4 * sizeof(unsigned long long)));
+    ASYM_HIP(hipMemset(w.gemm_ctr, 0, 64 * sizeof(int)));
+    ASYM_HIP(hipMemset(w.copy_ctr, 0, 4 * sizeof(unsigned long long)));
+    it = g_ws.emplace(key, w).first;
+  }
+  *out = &it->second;
+  return ASYM_OK;
+}
+
+int default_topology(int device, const Topology** out) {
+  auto it = g_default_topo.find(device);
+  if (it == g_default_topo.end()) {
+    asym_topology* t = nullptr;
+    int rc = asym_probe_topology(device, ASYM_PROBE_IDENTITY, &t);
+    if (rc != ASYM_OK) return rc;
+    const Topology* tt = unwrap(t);
+    g_default_topo[device] = std::make_unique<Topology>(*tt);
+    asym_topology_free(t);
+    it = g_default_topo.find(device);
+  }
+  *out = it->second.get();
+  return ASYM_OK;
+}
+
+int stream_cu_mask(hipStream_t s, int n_cus, uint32_t* mask) {
+  std::memset(mask, 0, sizeof(uint32_t) * ASYM_MASK_WORDS);
+  uint32_t m[ASYM_MASK_WORDS] = {0};
+  hipError_t e = hipExtStreamGetCUMask(s, ASYM_MASK_WORDS, m);
+  if (e != hipSuccess) {
+    // streams without a queue of their own (the null stream) report no mask:
+    // they run on the whole device
+    (void)hipGetLastError();
+    std::memset(m, 0, sizeof m);
+  }
+  int pop = 0;
+  for (int b = 0; b < n_cus; ++b)
+    if ((m[b >> 5] >> (b & 31)) & 1u) {
+      mask[b >> 5] |= 1u << (b & 31);
+      ++pop;
+    }
+  if (pop == 0)  // no mask reported: the whole device
+    for (int b = 0; b < n_cus; ++b) mask[b >> 5] |= 1u << (b & 31);
+  return ASYM_OK;
+}
+
+static int current_device(int* dev) {
+  ASYM_HIP(hipGetDevice(dev));
+  return ASYM_OK;
+}
+
+static int upload_schedule(int device, int tiles_m, int tiles_n, int mapping,
+                           const std::vector<int>& slots, const DeviceSchedule** out) {
+  ScheduleKey key{device, tiles_m, tiles_n, mapping, slots};
+  auto it = g_schedules.find(key);
+  if (it == g_schedules.end()) {
+    Schedule s;
+    int rc = build_schedule(tiles_m, tiles_n, (int)slots.size(), slots.data(), mapping, 0, s);
+    if (rc != ASYM_OK) return rc;
+    std::vector<int> off(ASYM_MAX_XCDS + 1, s.off.back()), sl(ASYM_MAX_XCDS, 0);
+    for (size_t x = 0; x < s.off.size(); ++x) off[x] = s.off[x];
+    for (size_t x = 0; x < slots.size(); ++x) sl[x] = slots[x];
+    DeviceSchedule d;
+    ASYM_HIP(hipMalloc(&d.d_order, sizeof(int) * s.order.size()));
+    ASYM_HIP(hipMalloc(&d.d_off, sizeof(int) * off.size()));
+    ASYM_HIP(hipMalloc(&d.d_slots, sizeof(int) * sl.size()));
+    ASYM_HIP(hipMemcpy(d.d_order, s.order.data(), sizeof(int) * s.order.size(), hipMemcpyHostToDevice));
+    ASYM_HIP(hipMemcpy(d.d_off, off.data(), sizeof(int) * off.size(), hipMemcpyHostToDevice));
+    ASYM_HIP(hipMemcpy(d.d_slots, sl.data(), sizeof(int) * sl.size(), hipMemcpyHostToDevice));
+    it = g_schedules.emplace(key, d).first;
+  }
+  *out = &it->second;
+  return ASYM_OK;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
+              const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
+              uint32_t xcd_mask, hipStream_t stream) {
+  if (M < 1 || N < 1 || K < 1) return fail(ASYM_EINVAL, "gemm: M, N, K must be >= 1");
+  if (!A || !B || !C) return fail(ASYM_EINVAL, "gemm: null matrix pointer");
+  if (lda < K || ldc < N) return fail(ASYM_EINVAL, "gemm: leading dimension too small");
+  if (b_layout == ASYM_B_KN) return fail(ASYM_EUNSUPPORTED, "gemm: B stored [K][N] is not served; store B as [N][K]");
+  if (b_layout != ASYM_B_NK) return fail(ASYM_EINVAL, "gemm: unknown B layout");
+  if (ldb < K) return fail(ASYM_EINVAL, "gemm: leading dimension too small");
+  if (mapping != ASYM_MAP_AWARE && mapping != ASYM_MAP_OBLIVIOUS_GROUPED &&
+      mapping != ASYM_MAP_OBLIVIOUS_ROWMAJOR)
+    return fail(ASYM_EINVAL, "gemm: unknown mapping");
+  // one tile's rows must be addressable by a 32-bit buffer offset
+  const int64_t BMr = gemm_tile_m(), BNr = gemm_tile_n();
+  if ((int64_t)BMr * lda * 2 >= (1ll << 31) || (int64_t)BNr * ldb * 2 >= (1ll << 31) ||
+      (int64_t)BMr * ldc * 2 >= (1ll << 31))
+    return fail(ASYM_EUNSUPPORTED, "gemm: leading dimension too large for 32-bit tile offsets");
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  int rc = current_device(&device);
+  if (rc != ASYM_OK) return rc;
+  const Topology* t = unwrap(topo_in);
+  if (!t) {
+    rc = default_topology(device, &t);
+    if (rc != ASYM_OK) return rc;
+  } else if (t->device != device && t->device >= 0) {
+    return fail(ASYM_EINVAL, "gemm: topology was probed on another device");
+  }
+  uint32_t mask[ASYM_MASK_WORDS];
+  rc = stream_cu_mask(stream, t->n_cus, mask);
+  if (rc != ASYM_OK) return rc;
+  std::vector<int> per;
+  rc = mask_counts(*t, mask, per);
+  if (rc != ASYM_OK) return rc;
+  const uint32_t all = (t->n_xccs >= 32) ? 0xFFFFFFFFu : ((1u << t->n_xccs) - 1u);
+  const uint32_t xm = xcd_mask == 0 ? all : (xcd_mask & all);
+  if (xcd_mask != 0 && (xcd_mask & ~all)) return fail(ASYM_EINVAL, "gemm: xcd_mask names XCDs the device does not have");
+  if (mapping != ASYM_MAP_AWARE && xm != all)
+    return fail(ASYM_EUNSUPPORTED, "gemm: XCD restriction needs the aware mapping (oblivious mappings place tiles statically)");
+  std::vector<int> slots(t->n_xccs, 0);
+  int total = 0, smax = 0;
+  for (int x = 0; x < t->n_xccs; ++x) {
+    slots[x] = ((xm >> x) & 1u) ? per[x] : 0;  // one persistent workgroup per CU
+    total += slots[x];
+    smax = std::max(smax, slots[x]);
+  }
+  if (total == 0) return fail(ASYM_EINVAL, "gemm: the CU set is empty");
+
+  const int tiles_m = (M + BMr - 1) / BMr, tiles_n = (N + BNr - 1) / BNr;
+  const DeviceSchedule* ds = nullptr;
+  rc = upload_schedule(device, tiles_m, tiles_n, mapping, slots, &ds);
+  if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(device, stream, &ws);
+  if (rc != ASYM_OK) return rc;
+
+  GemmLaunch g;
+  g.A = A; g.B = B; g.C = C;
+  g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
+  g.mapping = mapping;
+  g.d_order = ds->d_order; g.d_off = ds->d_off; g.d_slots = ds->d_slots;
+  g.d_ctr = ws->gemm_ctr;
+  g.tiles_m = tiles_m; g.tiles_n = tiles_n;
+  g.n_xccs = t->n_xccs;
+  g.grid = mapping == ASYM_MAP_AWARE ? t->n_xccs * smax : total;
+  g.vec = aligned16(A) && aligned16(B) && (((uintptr_t)C & 7u) == 0) && (K % 8 == 0) &&
+          (lda % 8 == 0) && (ldb % 8 == 0) && (ldc % 4 == 0);
+  return launch_gemm(g, stream);
+}
+
+// Bytes moved by copies on stream s since the last call; clears the count.
+int copy_bytes_take(hipStream_t s, unsigned long long* bytes) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  int rc = current_device(&device);
+  if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(device, s, &ws);
+  if (rc != ASYM_OK) return rc;
+  ASYM_HIP(hipStreamSynchronize(s));
+  ASYM_HIP(hipMemcpy(bytes, ws->copy_ctr + 2, sizeof(unsigned long long), hipMemcpyDeviceToHost));
+  ASYM_HIP(hipMemset(ws->copy_ctr + 2, 0, sizeof(unsigned long long)));
+  return ASYM_OK;
+}
+
+// Drop the workspace of a stream that is about to be destroyed.
+void release_workspace(hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  for (auto it = g_ws.begin(); it != g_ws.end();) {
+    if (it->first.second == s) {
+      hipFree(it->second.gemm_ctr);
+      hipFree(it->second.copy_ctr);
+      it = g_ws.erase(it);
+    } else {
+      ++it;
+    }
+  }
+}
+
+}  // namespace asym
+
+using asym::fail;
+
+extern "C" int asym_device_query(int device, asym_device_info* out) {
+  if (!out) return fail(ASYM_EINVAL, "null out");
+  std::memset(out, 0, sizeof *out);
+  int n = 0;
+  ASYM_HIP(hipGetDeviceCount(&n));
+  if (device < 0 || device >= n) return fail(ASYM_EINVAL, "no such device");
+  ASYM_HIP(hipDeviceGetAttribute(&out->n_cus, hipDeviceAttributeMultiprocessorCount, device));
+  ASYM_HIP(hipDeviceGetAttribute(&out->n_xccs, hipDeviceAttributeNumberOfXccs, device));
+  ASYM_HIP(hipDeviceGetAttribute(&out->n_cus_physical, hipDeviceAttributePhysicalMultiProcessorCount, device));
+  ASYM_HIP(hipDeviceGetAttribute(&out->clock_khz, hipDeviceAttributeClockRate, device));
+  ASYM_HIP(hipDeviceGetAttribute(&out->wall_clock_khz, hipDeviceAttributeWallClockRate, device));
+  ASYM_HIP(hipDeviceGetAttribute(&out->lds_bytes_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device));
+  ASYM_HIP(hipDeviceGetAttribute(&out->l2_bytes, hipDeviceAttributeL2CacheSize, device));
+  hipDeviceProp_t p;
+  ASYM_HIP(hipGetDeviceProperties(&p, device));
+  out->hbm_bytes = p.totalGlobalMem;
+  std::strncpy(out->arch, p.gcnArchName, sizeof(out->arch) - 1);
+  if (out->n_xccs < 1) out->n_xccs = 1;
+  return ASYM_OK;
+}
+
+extern "C" int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K, const void* A, int lda,
+                              const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
+                              uint32_t xcd_mask, void* stream) {
+  return asym::gemm_bf16(topo, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask,
+                         static_cast<hipStream_t>(stream));
+}
+
+extern "C" int asym_copy_bf16(void* dst, const void* src, size_t n_bytes, int passes,
+                              const int* stop_flag, uint32_t xcd_mask, void* stream) {
+  using namespace asym;
+  if (!dst || !src) return fail(ASYM_EINVAL, "copy: null pointer");
+  if (n_bytes == 0 || (n_bytes & 15u) || ((uintptr_t)dst & 15u) || ((uintptr_t)src & 15u))
+    return fail(ASYM_EINVAL, "copy: size and pointers must be nonzero multiples of 16 bytes");
+  if (passes < 1) return fail(ASYM_EINVAL, "copy: passes must be >= 1");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  int rc = current_device(&device);
+  if (rc != ASYM_OK) return rc;
+  const Topology* t = nullptr;
+  rc = default_topology(device, &t);
+  if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(device, s, &ws);
+  if (rc != ASYM_OK) return rc;
+  const int grid = 4 * t->n_cus;
+  return launch_copy(dst, src, n_bytes, passes, stop_flag, xcd_mask, grid, ws->copy_ctr, s);
+}
+
+extern "C" int asym_stream_create(const asym_topology* topo, const uint32_t* mask, void** out) {
+  using namespace asym;
+  if (!out) return fail(ASYM_EINVAL, "null out");
+  *out = nullptr;
+  hipStream_t s = nullptr;
+  if (!mask) {
+    ASYM_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
+    *out = s;
+    return ASYM_OK;
+  }
+  const Topology* t = unwrap(topo);
+  if (!t) return fail(ASYM_EINVAL, "stream: a masked stream needs a topology");
+  std::vector<int> per;
+  int rc = mask_counts(*t, mask, per);
+  if (rc != ASYM_OK) return rc;
+  for (int x = 0; x < t->n_xccs; ++x)
+    if (per[x] == 0)
+      return fail(ASYM_EUNSUPPORTED, "stream: the mask leaves XCD " + std::to_string(x) +
+                                         " without a CU; workgroups dispatched there could never run "
+                                         "(restrict whole XCDs with xcd_mask instead)");
+  ASYM_HIP(hipExtStreamCreateWithCUMask(&s, ASYM_MASK_WORDS, mask));
+  *out = s;
+  return ASYM_OK;
+}
+
+extern "C" int asym_stream_destroy(void* stream) {
+  if (!stream) return fail(ASYM_EINVAL, "null stream");
+  ASYM_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+  asym::release_workspace(static_cast<hipStream_t>(stream));
+  ASYM_HIP(hipStreamDestroy(static_cast<hipStream_t>(stream)));
+  return ASYM_OK;
+}
+
+extern "C" const char* asym_last_error(void) { return asym::g_last_error.c_str(); }
+
+extern "C" int asym_version(void) { return 1; }

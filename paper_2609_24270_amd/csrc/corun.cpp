@@ -1,0 +1,146 @@
+// Co-running kernels on partitioned CU sets (Section 7.2: prefill and decode
+// multiplexed on two SM partitions; Section 7.3: co-located tenants on equal
+// SM counts whose physical placement differs).  Each task gets its own stream:
+// a hardware CU-masked queue when the task names a CU mask, an unmasked queue
+// with the kernels' own XCD filter when it names whole XCDs.  Tasks are
+// enqueued back to back and timed with events on their own streams; a copy
+// task with iters <= 0 keeps streaming until a device flag, raised on the
+// GEMM streams after their last launch, stops it.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <vector>
+
+#include "internal.h"
+
+struct asym_topology;
+
+namespace asym {
+int gemm_bf16(const asym_topology* topo, int M, int N, int K, const void* A, int lda,
+              const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
+              uint32_t xcd_mask, hipStream_t stream);
+}
+
+using asym::fail;
+
+namespace {
+
+struct Guard {  // releases streams, events and the flag on every exit path
+  std::vector<hipStream_t> streams;
+  std::vector<hipEvent_t> events;
+  int* flag = nullptr;
+  ~Guard() {
+    for (hipStream_t s : streams) hipStreamSynchronize(s);
+    for (hipEvent_t e : events) hipEventDestroy(e);
+    for (hipStream_t s : streams) asym_stream_destroy(s);
+    if (flag) hipFree(flag);
+  }
+};
+
+bool mask_empty(const uint32_t* m) {
+  for (int i = 0; i < ASYM_MASK_WORDS; ++i)
+    if (m[i]) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int n_tasks,
+                          asym_task_result* out) {
+  if (!tasks || !out || n_tasks < 1 || n_tasks > 16) return fail(ASYM_EINVAL, "corun: bad task list");
+  std::memset(out, 0, sizeof(asym_task_result) * n_tasks);
+  Guard g;
+  int n_gemm = 0;
+  for (int i = 0; i < n_tasks; ++i) {
+    const asym_task& t = tasks[i];
+    if (t.kind == 0) {
+      if (t.iters < 1 || !t.A || !t.B || !t.C) return fail(ASYM_EINVAL, "corun: bad GEMM task");
+      ++n_gemm;
+    } else if (t.kind == 1) {
+      if (!t.src || !t.dst || t.n_bytes == 0) return fail(ASYM_EINVAL, "corun: bad copy task");
+    } else {
+      return fail(ASYM_EINVAL, "corun: unknown task kind");
+    }
+    void* s = nullptr;
+    int rc = asym_stream_create(topo, mask_empty(t.mask) ? nullptr : t.mask, &s);
+    if (rc != ASYM_OK) return rc;
+    g.streams.push_back(static_cast<hipStream_t>(s));
+  }
+  bool open_copy = false;
+  for (int i = 0; i < n_tasks; ++i)
+    if (tasks[i].kind == 1 && tasks[i].iters <= 0) open_copy = true;
+  if (open_copy && n_gemm == 0) return fail(ASYM_EINVAL, "corun: an open-ended copy needs a GEMM task to end it");
+  if (open_copy) {
+    ASYM_HIP(hipMalloc(&g.flag, sizeof(int)));
+    ASYM_HIP(hipMemset(g.flag, 0, sizeof(int)));
+  }
+  std::vector<hipEvent_t> ev0(n_tasks), ev1(n_tasks);
+  for (int i = 0; i < n_tasks; ++i) {
+    ASYM_HIP(hipEventCreate(&ev0[i]));
+    g.events.push_back(ev0[i]);
+    ASYM_HIP(hipEventCreate(&ev1[i]));
+    g.events.push_back(ev1[i]);
+  }
+  ASYM_HIP(hipDeviceSynchronize());
+
+  // copies first, so they are streaming when the GEMMs start
+  std::vector<unsigned long long*> copy_ctr(n_tasks, nullptr);
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int i = 0; i < n_tasks; ++i) {
+      const asym_task& t = tasks[i];
+      if ((pass == 0) != (t.kind == 1)) continue;
+      hipStream_t s = g.streams[i];
+      ASYM_HIP(hipEventRecord(ev0[i], s));
+      if (t.kind == 1) {
+        const int passes = t.iters > 0 ? t.iters : 100000;
+        int rc = asym_copy_bf16(t.dst, t.src, t.n_bytes, passes, t.iters > 0 ? nullptr : g.flag,
+                                t.xcd_mask, s);
+        if (rc != ASYM_OK) return rc;
+      } else {
+        for (int it = 0; it < t.iters; ++it) {
+          int rc = asym::gemm_bf16(topo, t.M, t.N, t.K, t.A, t.K, t.B, t.K, ASYM_B_NK, t.C, t.N,
+                                   t.mapping, t.xcd_mask, s);
+          if (rc != ASYM_OK) return rc;
+        }
+      }
+      ASYM_HIP(hipEventRecord(ev1[i], s));
+    }
+  }
+  if (open_copy) {
+    // raise the stop flag once every GEMM stream has drained: the last GEMM
+    // stream waits for the others' end events, then sets the flag
+    int last = -1;
+    for (int i = 0; i < n_tasks; ++i)
+      if (tasks[i].kind == 0) last = i;
+    for (int i = 0; i < n_tasks; ++i)
+      if (tasks[i].kind == 0 && i != last) ASYM_HIP(hipStreamWaitEvent(g.streams[last], ev1[i], 0));
+    int rc = asym::launch_set_flag(g.flag, 1, g.streams[last]);
+    if (rc != ASYM_OK) return rc;
+  }
+  for (int i = 0; i < n_tasks; ++i) ASYM_HIP(hipEventSynchronize(ev1[i]));
+  for (int i = 0; i < n_tasks; ++i) {
+    float ms = 0.f;
+    ASYM_HIP(hipEventElapsedTime(&ms, ev0[i], ev1[i]));
+    asym_task_result& r = out[i];
+    const asym_task& t = tasks[i];
+    r.ms_total = ms;
+    if (t.kind == 0) {
+      r.iters_done = t.iters;
+      r.ms_per_iter = ms / t.iters;
+      r.tflops = 2.0 * t.M * t.N * (double)t.K * t.iters / (ms * 1e-3) / 1e12;
+    }
+  }
+  // bytes moved by each copy: read back and clear the stream's byte counter
+  for (int i = 0; i < n_tasks; ++i) {
+    if (tasks[i].kind != 1) continue;
+    unsigned long long bytes = 0;
+    int rc = asym::copy_bytes_take(g.streams[i], &bytes);
+    if (rc != ASYM_OK) return rc;
+    asym_task_result& r = out[i];
+    const double passes = (double)bytes / (double)tasks[i].n_bytes;
+    r.iters_done = (int)(passes + 0.5);
+    r.ms_per_iter = r.iters_done > 0 ? r.ms_total / passes : 0.0;
+    r.gbps = 2.0 * (double)bytes / (r.ms_total * 1e-3) / 1e9;
+  }
+  return ASYM_OK;
+}

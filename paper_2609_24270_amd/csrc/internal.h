@@ -1,0 +1,101 @@
+// Internal declarations of libasym (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/asym.h"
+
+namespace asym {
+
+// ---- errors: thread-local message, status codes from asym.h ---------------
+int fail(int status, const std::string& msg);
+int hip_fail(hipError_t e, const char* what);
+#define ASYM_HIP(call)                                   \
+  do {                                                   \
+    hipError_t e_ = (call);                              \
+    if (e_ != hipSuccess) return ::asym::hip_fail(e_, #call); \
+  } while (0)
+
+// ---- topology ---------------------------------------------------------------
+struct CuRecord {
+  int xcc, se, sh, cu;
+  int mask_bit;  // -1 if unknown
+};
+
+struct Topology {
+  int device = -1;
+  int n_xccs = 0;
+  int n_cus = 0;
+  std::vector<CuRecord> cus;             // dense order: sorted (xcc, se, sh, cu)
+  std::vector<int> cus_per_xcd;          // [n_xccs]
+  std::vector<int> bit_to_cu;            // mask bit -> dense CU index, -1 unknown
+  bool has_maskmap = false;
+  double rr_fraction = -1.0;             // round-robin dispatch agreement
+  bool has_latency = false;
+  asym_latency_summary lat{};
+};
+
+// Fields of the HW_ID hardware register (GCN/CDNA layout).
+inline int hwid_cu(uint32_t h) { return (h >> 8) & 0xF; }
+inline int hwid_sh(uint32_t h) { return (h >> 12) & 0x1; }
+inline int hwid_se(uint32_t h) { return (h >> 13) & 0x7; }
+inline int xccid(uint32_t x) { return x & 0xF; }
+
+// Build the dense map from raw identity records {xcc reg, hw_id reg, block, _}.
+int build_topology(const int32_t* rec, int n, int n_cus_expected,
+                   int n_xccs_expected, const int32_t* mask_bit_record,
+                   Topology& out);
+// Exact invariants: every CU once, per-XCD counts sum to n_cus, bijective map.
+int check_invariants(const Topology& t);
+// Per-XCD CU counts of a mask; needs the mask map unless the mask is full.
+int mask_counts(const Topology& t, const uint32_t* mask, std::vector<int>& per_xcd);
+
+// Default per-device topology (identity probe on first use).
+int default_topology(int device, const Topology** out);
+
+// ---- schedule ---------------------------------------------------------------
+struct Schedule {
+  int tiles_m = 0, tiles_n = 0, n_xcds = 0;
+  std::vector<int> order;   // tile ids
+  std::vector<int> off;     // [n_xcds + 1]
+  std::vector<int> quota;   // [n_xcds]
+};
+int build_schedule(int tiles_m, int tiles_n, int n_xcds, const int* slots,
+                   int mapping, int band, Schedule& s);
+std::vector<int> largest_remainder_quotas(int total, const std::vector<int>& w);
+
+// ---- device entry points (implemented in .hip files) -------------------------
+struct GemmLaunch {
+  const void* A; const void* B; void* C;
+  int M, N, K, lda, ldb, ldc;
+  int mapping;                 // asym_mapping
+  const int* d_order;          // device tile order
+  const int* d_off;            // device [ASYM_MAX_XCDS+1]
+  const int* d_slots;          // device [ASYM_MAX_XCDS]
+  int* d_ctr;                  // device counters (self-resetting)
+  int grid;                    // workgroups
+  int tiles_m, tiles_n;
+  int n_xccs;
+  bool vec;                    // aligned vector path
+};
+int launch_gemm(const GemmLaunch& g, hipStream_t s);
+
+int probe_identity_run(int device, hipStream_t s, int n_blocks,
+                       std::vector<int32_t>& rec);
+int probe_latency_run(int device, Topology& t);
+
+int launch_copy(void* dst, const void* src, size_t n_bytes, int passes,
+                const int* stop_flag, uint32_t xcd_mask, int grid,
+                unsigned long long* ctr, hipStream_t s);
+int launch_set_flag(int* flag, int v, hipStream_t s);
+int copy_bytes_take(hipStream_t s, unsigned long long* bytes);
+void release_workspace(hipStream_t s);
+
+// Stream CU mask -> CU set seen by the scheduler.
+int stream_cu_mask(hipStream_t s, int n_cus, uint32_t* mask /*ASYM_MASK_WORDS*/);
+
+}  // namespace asym

@@ -1,0 +1,139 @@
+// Tile schedules for the persistent GEMM.
+//
+// The paper's full-GPU recipe (Section 7.1, "Integration with popular
+// kernels") converts a kernel to persistent blocks, lets each block find the
+// unit it runs on, and hands it the tasks whose data is local to that unit's
+// partition, with work spread over partitions in proportion to their compute
+// units (same section, last paragraph, and the full-GPU lesson of
+// Section 7.4).  On MI355X the partition that matters for a GEMM is the XCD:
+// each XCD has a private L2, so tiles that share A rows and B columns should
+// run on the same XCD at the same time.
+//
+// Banded order: tile rows are cut into bands of `band` rows; a band is walked
+// column by column, each column top to bottom.  A run of s consecutive tiles of
+// this order covers about band rows x s/band columns, a near-square block when
+// band ~ sqrt(s).
+//   AWARE:             XCD x owns a contiguous run of the order whose length
+//                      is its largest-remainder quota of the tile count,
+//                      weighted by its persistent workgroups.
+//   OBLIVIOUS_GROUPED: the same order, tile i to workgroup i mod P; round-robin
+//                      dispatch then puts neighbouring tiles on different XCDs.
+//   OBLIVIOUS_ROWMAJOR: row-major order, tile i to workgroup i mod P.
+#include <algorithm>
+#include <cstdint>
+
+#include "internal.h"
+
+namespace asym {
+
+std::vector<int> largest_remainder_quotas(int total, const std::vector<int>& w) {
+  const int n = (int)w.size();
+  std::vector<int> q(n, 0);
+  int64_t W = 0;
+  for (int x : w) W += x;
+  if (W <= 0 || total <= 0) return q;
+  std::vector<int64_t> rem(n, 0);
+  int64_t assigned = 0;
+  for (int i = 0; i < n; ++i) {
+    const int64_t num = (int64_t)total * w[i];
+    q[i] = (int)(num / W);
+    rem[i] = num % W;
+    assigned += q[i];
+  }
+  int left = (int)(total - assigned);
+  // hand out the remaining units to the largest remainders, ties to lower index
+  std::vector<int> idx(n);
+  for (int i = 0; i < n; ++i) idx[i] = i;
+  std::stable_sort(idx.begin(), idx.end(),
+                   [&](int a, int b) { return rem[a] > rem[b]; });
+  for (int k = 0; k < n && left > 0; ++k) {
+    if (w[idx[k]] <= 0) continue;
+    q[idx[k]] += 1;
+    --left;
+  }
+  return q;
+}
+
+// Band height: minimise band + ceil(s / band) for s tiles in flight per XCD;
+// ties go to a band dividing tiles_m, then to the taller band.
+static int choose_band(int tiles_m, int s) {
+  if (s < 1) s = 1;
+  int best = 1, best_cost = 1 << 30;
+  bool best_div = false;
+  for (int h = 1; h <= std::min(tiles_m, s); ++h) {
+    const int cost = h + (s + h - 1) / h;
+    const bool div = (tiles_m % h) == 0;
+    if (cost < best_cost || (cost == best_cost && (div && !best_div)) ||
+        (cost == best_cost && div == best_div)) {
+      best = h;
+      best_cost = cost;
+      best_div = div;
+    }
+  }
+  return best;
+}
+
+int build_schedule(int tiles_m, int tiles_n, int n_xcds, const int* slots,
+                   int mapping, int band, Schedule& s) {
+  if (tiles_m < 1 || tiles_n < 1) return fail(ASYM_EINVAL, "schedule: empty tile grid");
+  if ((int64_t)tiles_m * tiles_n > (1 << 30)) return fail(ASYM_EINVAL, "schedule: tile grid too large");
+  if (n_xcds < 1 || n_xcds > ASYM_MAX_XCDS) return fail(ASYM_EINVAL, "schedule: bad XCD count");
+  if (!slots) return fail(ASYM_EINVAL, "schedule: null slots");
+  if (band < 0) return fail(ASYM_EINVAL, "schedule: negative band");
+  int P = 0, smax = 0;
+  for (int x = 0; x < n_xcds; ++x) {
+    if (slots[x] < 0) return fail(ASYM_EINVAL, "schedule: negative slot count");
+    P += slots[x];
+    smax = std::max(smax, slots[x]);
+  }
+  if (P < 1) return fail(ASYM_EINVAL, "schedule: no workgroup slots");
+  if (mapping != ASYM_MAP_AWARE && mapping != ASYM_MAP_OBLIVIOUS_GROUPED &&
+      mapping != ASYM_MAP_OBLIVIOUS_ROWMAJOR)
+    return fail(ASYM_EINVAL, "schedule: bad mapping");
+
+  const int T = tiles_m * tiles_n;
+  s.tiles_m = tiles_m;
+  s.tiles_n = tiles_n;
+  s.n_xcds = n_xcds;
+  s.order.assign(T, 0);
+  s.off.assign(n_xcds + 1, 0);
+  s.quota.assign(n_xcds, 0);
+
+  if (mapping == ASYM_MAP_OBLIVIOUS_ROWMAJOR) {
+    for (int i = 0; i < T; ++i) s.order[i] = i;
+  } else {
+    const int h = band > 0 ? std::min(band, tiles_m) : choose_band(tiles_m, smax);
+    int i = 0;
+    for (int r0 = 0; r0 < tiles_m; r0 += h) {
+      const int r1 = std::min(tiles_m, r0 + h);
+      for (int c = 0; c < tiles_n; ++c)
+        for (int r = r0; r < r1; ++r) s.order[i++] = r * tiles_n + c;
+    }
+  }
+
+  if (mapping == ASYM_MAP_AWARE) {
+    std::vector<int> w(slots, slots + n_xcds);
+    s.quota = largest_remainder_quotas(T, w);
+    for (int x = 0; x < n_xcds; ++x) s.off[x + 1] = s.off[x] + s.quota[x];
+  } else {
+    // one shared list; quota[x] counts tiles that workgroup i mod P, placed on
+    // XCD (i mod P) mod n_xcds by round-robin dispatch, would run on XCD x
+    for (int x = 0; x <= n_xcds; ++x) s.off[x] = (x == n_xcds) ? T : 0;
+    for (int i = 0; i < T; ++i) s.quota[(i % P) % n_xcds] += 1;
+  }
+  return ASYM_OK;
+}
+
+}  // namespace asym
+
+extern "C" int asym_schedule_build(int tiles_m, int tiles_n, int n_xcds,
+                                   const int* slots, int mapping, int band,
+                                   int* order, int* off, int* quota) {
+  asym::Schedule s;
+  int rc = asym::build_schedule(tiles_m, tiles_n, n_xcds, slots, mapping, band, s);
+  if (rc != ASYM_OK) return rc;
+  if (order) std::copy(s.order.begin(), s.order.end(), order);
+  if (off) std::copy(s.off.begin(), s.off.end(), off);
+  if (quota) std::copy(s.quota.begin(), s.quota.end(), quota);
+  return ASYM_OK;
+}

@@ -1,0 +1,138 @@
+"""GPU parity of the persistent bf16 GEMM against the CPU oracle.
+
+All calls go through libasym's C ABI.  Small shapes are compared element by
+element; full-size shapes (8192^3 and the decoder projections) on sampled rows
+and columns, which the oracle computes as a sub-GEMM.  Bitwise properties that
+hold at any size: every mapping, CU mask and repeat gives identical bits, and
+exact-integer inputs give exactly the integer product.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_24270_amd as asym
+from paper_2609_24270_amd import workloads
+from tests.checks import REL_TOL, assert_gemm_close
+
+pytestmark = pytest.mark.gpu
+
+MAPS = ("aware", "oblivious_grouped", "oblivious_rowmajor")
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    asym.load_library()
+    torch.cuda.set_device(0)
+    return torch.device("cuda:0")
+
+
+def run(A, B, mapping="aware", stream=None, **kw):
+    C = asym.gemm(A, B, mapping=mapping, stream=stream, **kw)
+    torch.cuda.synchronize()
+    return C
+
+
+def sampled_check(A, B, C, n_rows=128, n_cols=128, seed=0, exact=False):
+    g = np.random.default_rng(seed)
+    M, N = C.shape
+    rows = np.sort(g.choice(M, size=min(n_rows, M), replace=False))
+    cols = np.sort(g.choice(N, size=min(n_cols, N), replace=False))
+    # always include the last row / column (ragged tile edges)
+    rows[-1], cols[-1] = M - 1, N - 1
+    rows, cols = np.unique(rows), np.unique(cols)
+    Ab, Bb, Cb = bits(A), bits(B), bits(C)
+    R, Co = oracle.gemm_bf16(Ab[rows], Bb[cols], "nk")
+    got = Cb[np.ix_(rows, cols)]
+    if exact:
+        assert np.array_equal(got, Co)
+        return 0.0
+    return assert_gemm_close(got, R)
+
+
+def test_device_query(dev):
+    d = asym.device_query(0)
+    print(d)
+    assert d["n_cus"] == 256 and d["n_xccs"] == 8 and d["arch"].startswith("gfx950")
+
+
+@pytest.mark.parametrize("mapping", MAPS)
+def test_gemm_512_parity(dev, mapping):
+    A, B = workloads.make_inputs(workloads.SQUARE_512)
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    C = run(A.to(dev), B.to(dev), mapping)
+    e = assert_gemm_close(bits(C), R, what=f"512^3 {mapping}")
+    print(f"512^3 {mapping}: max rel err {e:.3e}")
+
+
+def test_gemm_mappings_and_repeats_bitwise(dev):
+    A, B = workloads.make_inputs(workloads.SQUARE_512)
+    A, B = A.to(dev), B.to(dev)
+    ref = bits(run(A, B, "aware"))
+    for m in MAPS:
+        for _ in range(2):
+            assert np.array_equal(bits(run(A, B, m)), ref), m
+
+
+ODD = [(1, 1, 1), (17, 17, 17), (129, 1000, 17), (1000, 129, 129), (17, 1, 1000), (1, 1000, 129),
+       (300, 520, 72), (257, 255, 64), (513, 1031, 200), (32, 14336, 4096), (100, 300, 4104)]
+
+
+@pytest.mark.parametrize("M,N,K", ODD)
+def test_gemm_odd_shapes(dev, M, N, K):
+    A, B = workloads.make_inputs(workloads.make_problem(M, N, K, seed=M + 3 * N + 7 * K))
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    for m in ("aware", "oblivious_grouped"):
+        C = run(A.to(dev), B.to(dev), m)
+        assert_gemm_close(bits(C), R, what=f"{M}x{N}x{K} {m}")
+
+
+def test_gemm_strided_and_unaligned(dev):
+    # leading dimensions larger than the row, and a K that is not a multiple of 8
+    M, N, K = 200, 136, 150
+    A, B = workloads.make_inputs(workloads.make_problem(M, N, K, seed=9))
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    Ap = torch.zeros((M, K + 24), dtype=torch.bfloat16)
+    Ap[:, :K] = A
+    Bp = torch.zeros((N, K + 40), dtype=torch.bfloat16)
+    Bp[:, :K] = B
+    Cp = torch.full((M, N + 8), 7.0, dtype=torch.bfloat16, device=dev)
+    asym.gemm(Ap.to(dev)[:, :K], Bp.to(dev)[:, :K], Cp[:, :N])
+    torch.cuda.synchronize()
+    assert_gemm_close(bits(Cp[:, :N]), R)
+    # the padding columns of C are untouched
+    assert torch.all(Cp[:, N:].cpu() == 7.0)
+
+
+def test_gemm_exact_integer_8192_sampled(dev):
+    p = workloads.make_problem(8192, 8192, 8192, seed=21, dist="int")
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = run(Ad, Bd, "aware")
+    sampled_check(A, B, C, 96, 96, seed=1, exact=True)
+    C2 = run(Ad, Bd, "oblivious_grouped")
+    assert torch.equal(C, C2)
+
+
+def test_gemm_8192_uniform_sampled(dev):
+    A, B = workloads.make_inputs(workloads.SQUARE_8192)
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = run(Ad, Bd, "aware")
+    e = sampled_check(A, B, C, 128, 128, seed=2)
+    print(f"8192^3 aware sampled max rel err {e:.3e}")
+    for m in ("oblivious_grouped", "oblivious_rowmajor"):
+        assert torch.equal(run(Ad, Bd, m), C), m
+
+
+@pytest.mark.parametrize("p", workloads.LLM_SHAPES, ids=lambda p: p.name)
+def test_gemm_llm_shapes_sampled(dev, p):
+    A, B = workloads.make_inputs(p)
+    C = run(A.to(dev), B.to(dev), "aware")
+    e = sampled_check(A, B, C, 128, 128, seed=3)
+    print(f"{p.name} sampled max rel err {e:.3e}")

@@ -1,0 +1,126 @@
+"""GPU tests of the topology probe, CU-masked streams, the copy kernel and co-run.
+
+Topology: the exact invariants (every CU once, per-XCD counts summing to the
+device CU count, a bijective mask map whose CUs are the identity probe's CUs).
+Masked and XCD-restricted GEMMs must give bitwise the unmasked result.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import topology as otopo
+import paper_2609_24270_amd as asym
+from paper_2609_24270_amd import workloads
+from tests.checks import assert_gemm_close
+
+pytestmark = pytest.mark.gpu
+
+
+def bits(t):
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    asym.load_library()
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def topo(dev):
+    return asym.probe_topology(0, asym.PROBE_IDENTITY | asym.PROBE_MASKMAP)
+
+
+def test_identity_probe_invariants(dev):
+    t = asym.probe_topology(0, asym.PROBE_IDENTITY)
+    d = asym.device_query(0)
+    info = t.info()
+    cus = [(c["xcc"], c["se"], c["sh"], c["cu"]) for c in t.cus()]
+    print("cus_per_xcd", info["cus_per_xcd"], "round-robin fraction", t.dispatch_rr_fraction())
+    assert otopo.invariant_violations(cus, d["n_cus"], d["n_xccs"]) == []
+    assert info["n_cus"] == d["n_cus"] and sum(info["cus_per_xcd"]) == d["n_cus"]
+    assert info["n_xcds"] == d["n_xccs"]
+
+
+def test_maskmap_probe(dev, topo):
+    d = asym.device_query(0)
+    cus = topo.cus()
+    keys = [(c["xcc"], c["se"], c["sh"], c["cu"]) for c in cus]
+    bit_to_cu = [None] * d["n_cus"]
+    for i, c in enumerate(cus):
+        bit_to_cu[c["mask_bit"]] = i
+    assert otopo.invariant_violations(keys, d["n_cus"], d["n_xccs"], bit_to_cu) == []
+    ident = asym.probe_topology(0, asym.PROBE_IDENTITY)
+    assert keys == [(c["xcc"], c["se"], c["sh"], c["cu"]) for c in ident.cus()]
+    js = topo.json()
+    print("mask bit -> xcc:", [cus[bit_to_cu[b]]["xcc"] for b in range(32)])
+    assert js["has_maskmap"]
+
+
+def test_masked_gemm_bitwise(dev, topo):
+    A, B = workloads.make_inputs(workloads.COLOC)
+    Ad, Bd = A.to(dev), B.to(dev)
+    ref = asym.gemm(Ad, Bd, mapping="aware")
+    torch.cuda.synchronize()
+    R, _ = oracle.gemm_bf16(bits(A)[:64], bits(B)[:64], "nk")
+    assert_gemm_close(bits(ref)[:64, :64], R)
+    mask = workloads.random_mask_bits(4, 1, 128)[0]
+    counts = topo.cuset_counts(mask)
+    print("random mask per-XCD counts", counts)
+    s = asym.stream_create(topo, mask)
+    try:
+        for m in ("aware", "oblivious_grouped", "oblivious_rowmajor"):
+            C = asym.gemm(Ad, Bd, mapping=m, topo=topo, stream=s)
+            s.synchronize()
+            assert torch.equal(C, ref), m
+    finally:
+        asym.stream_destroy(s)
+    # whole-XCD restriction on an unmasked stream (aware only)
+    for xm in (0x0F, 0xF0, 0x81):
+        C = asym.gemm(Ad, Bd, mapping="aware", topo=topo, xcd_mask=xm)
+        torch.cuda.synchronize()
+        assert torch.equal(C, ref), hex(xm)
+    with pytest.raises(asym.AsymError):
+        asym.gemm(Ad, Bd, mapping="oblivious_grouped", topo=topo, xcd_mask=0x0F)
+
+
+def test_copy_kernel(dev):
+    n = workloads.COPY_BYTES // 2
+    src = workloads.copy_source(n).to(dev)
+    for xm, passes in ((0, 1), (0x3, 2), (0xF0, 3)):
+        dst = torch.zeros_like(src)
+        asym.copy(dst, src, passes=passes, xcd_mask=xm)
+        torch.cuda.synchronize()
+        assert torch.equal(dst, src)
+    # a ragged size (not a multiple of the 64 KiB chunk)
+    s2 = src[: 12345 * 8]
+    d2 = torch.zeros_like(s2)
+    asym.copy(d2, s2)
+    torch.cuda.synchronize()
+    assert torch.equal(d2, s2)
+
+
+def test_corun_gemm_and_copy(dev, topo):
+    A, B = workloads.make_inputs(workloads.COLOC)
+    Ad, Bd = A.to(dev), B.to(dev)
+    ref = asym.gemm(Ad, Bd)
+    torch.cuda.synchronize()
+    C = torch.empty_like(ref)
+    src = workloads.copy_source(workloads.COPY_BYTES // 2).to(dev)
+    dst = torch.empty_like(src)
+    mask = workloads.random_mask_bits(4, 1, 128)[0]
+    comp = [b for b in range(256) if b not in set(mask)]
+    res = asym.corun([asym.gemm_task(Ad, Bd, C, 5, "aware", mask=mask),
+                      asym.copy_task(dst, src, 0, mask=comp)], topo)
+    print(res)
+    assert torch.equal(C, ref)
+    assert torch.equal(dst, src)
+    assert res[0]["tflops"] > 0 and res[1]["gbps"] > 0 and res[1]["iters_done"] >= 1
+    # whole-XCD partitions through the kernels' XCD filter
+    res = asym.corun([asym.gemm_task(Ad, Bd, C, 5, "aware", xcd_mask=0x0F),
+                      asym.copy_task(dst, src, 0, xcd_mask=0xF0)], topo)
+    print(res)
+    assert torch.equal(C, ref)

@@ -1,0 +1,271 @@
+"""Host-side logic of libasym against the oracle, on the CPU (no GPU calls).
+
+Covers: every symbol declared in include/asym.h is exported; the tile
+schedule equals the oracle's definition (quotas, order, coverage); the
+topology map built from synthetic identity records equals the oracle's map and
+rejects maps that break the exact invariants; CU-set policies; argument errors
+that the library reports before touching a device.
+"""
+import os
+import random
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_24270_amd as asym
+from oracle import schedule as osched
+from oracle import topology as otopo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return asym.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    hdr = open(os.path.join(ROOT, "include", "asym.h")).read()
+    declared = set(re.findall(r"^\s*(?:int|void|const char\*)\s+(asym_\w+)\s*\(", hdr, re.M))
+    assert declared == set(asym.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert asym.version() >= 1
+
+
+# -- schedule ------------------------------------------------------------------
+
+def _cases():
+    rng = random.Random(1234)
+    cases = [(32, 32, [32] * 8), (16, 56, [32] * 8), (16, 16, [32] * 8), (1, 1, [32] * 8),
+             (2, 65, [24] * 6 + [0, 0]), (16, 16, [16, 10, 22, 16, 13, 19, 16, 16]),
+             (7, 3, [1, 0, 0, 0, 0, 0, 0, 0]), (32, 16, [24] * 8)]
+    for _ in range(25):
+        n = rng.choice([1, 2, 4, 8])
+        slots = [rng.randint(0, 32) for _ in range(n)]
+        if sum(slots) == 0:
+            slots[0] = 1
+        cases.append((rng.randint(1, 40), rng.randint(1, 40), slots))
+    return cases
+
+
+@pytest.mark.parametrize("tm,tn,slots", _cases())
+def test_schedule_matches_oracle(lib, tm, tn, slots):
+    T = tm * tn
+    band = osched.band_cost_choice(tm, max(slots))
+    # aware: quotas are Hamilton's apportionment, runs of the banded order
+    order, off, quota = asym.schedule_build(tm, tn, slots, asym.MAP_AWARE)
+    assert quota == osched.hamilton_quotas(T, slots)
+    assert order == osched.banded_order(tm, tn, band)
+    assert off[0] == 0 and all(off[x + 1] - off[x] == quota[x] for x in range(len(slots)))
+    assert sorted(order) == list(range(T))                     # every tile exactly once
+    W = sum(slots)
+    assert all(abs(quota[x] - T * slots[x] / W) < 1 for x in range(len(slots)))
+    assert all(q == 0 for q, s in zip(quota, slots) if s == 0)
+    # oblivious grouped: the same order, placed round-robin
+    order_g, _, quota_g = asym.schedule_build(tm, tn, slots, asym.MAP_OBLIVIOUS_GROUPED)
+    assert order_g == order
+    owner = osched.oblivious_assignment(order_g, slots)
+    assert quota_g == [sum(1 for v in owner.values() if v == x) for x in range(len(slots))]
+    # oblivious row-major
+    order_r, _, _ = asym.schedule_build(tm, tn, slots, asym.MAP_OBLIVIOUS_ROWMAJOR)
+    assert order_r == osched.rowmajor_order(tm, tn)
+
+
+def test_schedule_explicit_band(lib):
+    order, _, _ = asym.schedule_build(10, 7, [4] * 8, asym.MAP_AWARE, band=3)
+    assert order == osched.banded_order(10, 7, 3)
+
+
+def test_aware_wave_blocks_are_compact():
+    # 8192^3 at 256^2 tiles: 32 tiles per XCD per wave form 8 rows x 4 columns
+    order, off, quota = asym.schedule_build(32, 32, [32] * 8, asym.MAP_AWARE)
+    for x in range(8):
+        run = order[off[x]:off[x + 1]]
+        for w in range(0, len(run), 32):
+            wave = run[w:w + 32]
+            rows = {t // 32 for t in wave}
+            cols = {t % 32 for t in wave}
+            assert len(rows) + len(cols) == 12
+    # the grouped-oblivious order spreads each wave over 1 row x 32 columns per XCD
+    order_g, _, _ = asym.schedule_build(32, 32, [32] * 8, asym.MAP_OBLIVIOUS_GROUPED)
+    own = osched.oblivious_assignment(order_g, [32] * 8)
+    first_wave = order_g[:256]
+    for x in range(8):
+        mine = [t for t in first_wave if own[t] == x]
+        assert len({t // 32 for t in mine}) + len({t % 32 for t in mine}) == 33
+
+
+@pytest.mark.parametrize("args", [
+    (0, 4, [1] * 8, 0), (4, 4, [0] * 8, 0), (4, 4, [1] * 8, 7), (4, 4, [-1] + [1] * 7, 0)])
+def test_schedule_rejects_bad_input(lib, args):
+    with pytest.raises(asym.AsymError) as e:
+        asym.schedule_build(*args)
+    assert e.value.status == asym.EINVAL
+
+
+# -- topology from synthetic records ------------------------------------------------
+
+def fake_records(layout, n_rep=4, seed=0, rr=True):
+    """layout: {xcc: [(se, sh, cu), ...]} -> identity records, shuffled."""
+    rng = random.Random(seed)
+    cus = [(x, se, sh, cu) for x, lst in layout.items() for (se, sh, cu) in lst]
+    recs = []
+    nx = max(layout) + 1
+    for rep in range(n_rep):
+        for c in rng.sample(cus, len(cus)):
+            b = len(recs)
+            x = c[0]
+            if rr:
+                # place the record at a block index whose residue is its XCC
+                b = b - (b % nx) + x
+            hw = (c[3] << 8) | (c[2] << 12) | (c[1] << 13) | (rng.randint(0, 15))
+            recs.append([x | (rng.randint(0, 15) << 8), hw, b, 0])
+    return recs
+
+
+def uniform_layout(n_xcc=8, n_se=4, per_se=8):
+    return {x: [(se, 0, cu) for se in range(n_se) for cu in range(per_se)] for x in range(n_xcc)}
+
+
+def test_topology_uniform_matches_oracle(lib):
+    lay = uniform_layout()
+    recs = fake_records(lay)
+    t = asym.topology_from_records(recs, 256, 8)
+    info = t.info()
+    assert info["n_cus"] == 256 and info["cus_per_xcd"] == [32] * 8
+    cus = [(c["xcc"], c["se"], c["sh"], c["cu"]) for c in t.cus()]
+    assert cus == otopo.build_map(recs)
+    assert otopo.invariant_violations(cus, 256, 8) == []
+    assert t.dispatch_rr_fraction() == pytest.approx(otopo.round_robin_fraction(recs, 8))
+    js = t.json()
+    assert js["n_cus"] == 256 and len(js["cus"]) == 256
+
+
+def test_topology_uneven_floorswept_layout(lib):
+    # floorsweeping leaves XCDs (and SEs) with different CU counts
+    rng = random.Random(7)
+    lay = {}
+    for x in range(8):
+        lst = [(se, sh, cu) for se in range(4) for sh in range(2) for cu in range(5)]
+        lay[x] = sorted(rng.sample(lst, rng.randint(20, 36)))
+    n = sum(len(v) for v in lay.values())
+    recs = fake_records(lay, seed=3)
+    t = asym.topology_from_records(recs, n, 8)
+    cus = [(c["xcc"], c["se"], c["sh"], c["cu"]) for c in t.cus()]
+    assert cus == otopo.build_map(recs)
+    assert t.info()["cus_per_xcd"] == otopo.per_xcd_counts(cus, 8)
+
+
+def test_topology_rejects_broken_maps(lib):
+    lay = uniform_layout()
+    recs = fake_records(lay)
+    # the device reports a different CU count than the records show
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_from_records(recs, 250, 8)
+    assert e.value.status == asym.EINVARIANT
+    # an XCD missing entirely
+    lay7 = {x: v for x, v in lay.items() if x != 5}
+    recs7 = fake_records(lay7)
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_from_records(recs7, 224, 8)
+    assert e.value.status == asym.EINVARIANT
+    assert otopo.invariant_violations(otopo.build_map(recs7), 224, 8) != []
+    # XCC id beyond the device's XCC count
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_from_records(recs, 256, 4)
+    assert e.value.status == asym.EINVARIANT
+    # a mask-bit map that sends two bits to one CU
+    bit_rec = list(range(256))
+    first = {}
+    for i, r in enumerate(recs):
+        first.setdefault(otopo.fields(r[0], r[1]), i)
+    keys = otopo.build_map(recs)
+    bit_rec = [first[keys[b]] for b in range(256)]
+    bad = list(bit_rec)
+    bad[1] = bad[0]
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_from_records(recs, 256, 8, bad)
+    assert e.value.status == asym.EINVARIANT
+
+
+def _maskmap_topology(seed=0):
+    lay = uniform_layout()
+    recs = fake_records(lay, seed=seed)
+    first = {}
+    for i, r in enumerate(recs):
+        first.setdefault(otopo.fields(r[0], r[1]), i)
+    keys = otopo.build_map(recs)
+    # bit b -> CU on XCC b % 8 (interleaved), a permutation of the dense order
+    perm = []
+    per_x = {x: [k for k in keys if k[0] == x] for x in range(8)}
+    for b in range(256):
+        perm.append(per_x[b % 8][b // 8])
+    bit_rec = [first[k] for k in perm]
+    return asym.topology_from_records(recs, 256, 8, bit_rec), perm
+
+
+def test_maskmap_and_cusets(lib):
+    t, perm = _maskmap_topology()
+    cus = t.cus()
+    assert sorted(c["mask_bit"] for c in cus) == list(range(256))
+    for c in cus:
+        assert perm[c["mask_bit"]] == (c["xcc"], c["se"], c["sh"], c["cu"])
+    # XCD-aligned: whole XCDs
+    m = t.cuset(64, asym.CUSET_XCD_ALIGNED)
+    assert len(m) == 64 and t.cuset_counts(m) == [32, 32, 0, 0, 0, 0, 0, 0]
+    m2 = t.cuset(64, asym.CUSET_XCD_ALIGNED, exclude=m)
+    assert not set(m) & set(m2) and t.cuset_counts(m2) == [0, 0, 32, 32, 0, 0, 0, 0]
+    with pytest.raises(asym.AsymError):
+        t.cuset(48, asym.CUSET_XCD_ALIGNED)
+    # striped: the same share of every XCD, balanced over shader engines
+    s = t.cuset(64, asym.CUSET_STRIPED)
+    assert t.cuset_counts(s) == [8] * 8
+    by_se = {}
+    for b in s:
+        x, se, _, _ = perm[b]
+        by_se[(x, se)] = by_se.get((x, se), 0) + 1
+    assert set(by_se.values()) == {2}
+    rest = t.cuset(192, asym.CUSET_STRIPED, exclude=s)
+    assert sorted(s + rest) == list(range(256))
+    # random: seeded, reproducible, honours exclusion
+    r1 = t.cuset(128, asym.CUSET_RANDOM, seed=4)
+    r2 = t.cuset(128, asym.CUSET_RANDOM, seed=4)
+    r3 = t.cuset(128, asym.CUSET_RANDOM, seed=5)
+    assert r1 == r2 and r1 != r3 and len(r1) == 128
+    r4 = t.cuset(100, asym.CUSET_RANDOM, seed=1, exclude=r1)
+    assert not set(r4) & set(r1)
+
+
+def test_masked_stream_refuses_an_empty_xcd(lib):
+    t, _ = _maskmap_topology()
+    aligned = t.cuset(128, asym.CUSET_XCD_ALIGNED)
+    with pytest.raises(asym.AsymError) as e:
+        asym.stream_create(t, aligned)
+    assert e.value.status == asym.EUNSUPPORTED
+    # a partial mask needs a mask map
+    plain = asym.topology_from_records(fake_records(uniform_layout()), 256, 8)
+    with pytest.raises(asym.AsymError) as e:
+        plain.cuset_counts(list(range(100)))
+    assert e.value.status == asym.EUNSUPPORTED
+
+
+def test_gemm_and_copy_argument_errors(lib):
+    vp = 0x1000
+    lib_ = asym.load_library()
+    import ctypes
+    P = ctypes.c_void_p(vp)
+    cases = [
+        ((None, 0, 4, 4, P, 4, P, 4, 0, P, 4, 0, 0, None), asym.EINVAL),      # M = 0
+        ((None, 4, 4, 4, None, 4, P, 4, 0, P, 4, 0, 0, None), asym.EINVAL),   # null A
+        ((None, 4, 4, 8, P, 4, P, 8, 0, P, 4, 0, 0, None), asym.EINVAL),      # lda < K
+        ((None, 4, 4, 4, P, 4, P, 4, 1, P, 4, 0, 0, None), asym.EUNSUPPORTED),  # [K][N] B
+        ((None, 4, 4, 4, P, 4, P, 4, 7, P, 4, 0, 0, None), asym.EINVAL),      # bad layout
+        ((None, 4, 4, 4, P, 4, P, 4, 0, P, 4, 9, 0, None), asym.EINVAL),      # bad mapping
+    ]
+    for args, want in cases:
+        assert lib_.asym_gemm_bf16(*args) == want, args
+        assert asym.last_error()
+    assert lib_.asym_copy_bf16(P, P, 24, 1, None, 0, None) == asym.EINVAL
+    assert lib_.asym_copy_bf16(P, P, 32, 0, None, 0, None) == asym.EINVAL

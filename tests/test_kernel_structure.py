@@ -1,0 +1,114 @@
+"""Structure of the compiled claim loops (CPU only: hipcc -S for gfx950).
+
+The persistent kernels claim work in a loop whose body holds barriers: one
+lane claims, a barrier publishes the claim, every lane reads it.  If lane-
+divergent code sits at the end of such a body, the compiler may restructure
+the loop so that the barriers head an inner loop the claiming lane never
+re-enters; the other lanes then keep re-reading a stale claim and the kernel
+never ends.  These tests check, on the generated assembly, that each claim
+atomic and the barrier that publishes it belong to the same loop.
+"""
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2609_24270_amd", "csrc")
+
+
+def asm_of(src: str, tmp_path) -> str:
+    out = tmp_path / (os.path.basename(src) + ".s")
+    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"),
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", str(out)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    return out.read_text()
+
+
+def function_body(asm: str, name_fragment: str) -> list:
+    lines = asm.splitlines()
+    start = next(i for i, l in enumerate(lines)
+                 if re.match(r"^_Z\w*" + name_fragment + r"\w*:", l))
+    end = next(i for i in range(start, len(lines)) if lines[i].startswith(".Lfunc_end"))
+    return lines[start:end]
+
+
+def annotate_loops(body: list):
+    """(instruction, innermost loop header, chain of enclosing headers) per
+    instruction, from the loop comments the compiler writes on each block."""
+    parent = {}
+    out = []
+    cur_loop, header_lbl, pending_parent = None, None, None
+    for l in body:
+        m = re.match(r"^(\.LBB\d+_\d+|; %bb\.\d+):", l)
+        if m:
+            header_lbl = m.group(1)[1:] if m.group(1).startswith(".") else None
+            cur_loop = None
+            mp = re.search(r"Parent Loop (BB\d+_\d+) Depth=", l)
+            pending_parent = "L" + mp.group(1) if mp else None
+            if re.search(r"Loop Header: Depth=", l):
+                cur_loop = header_lbl
+                if pending_parent:
+                    parent.setdefault(header_lbl, pending_parent)
+            mi = re.search(r"in Loop: Header=(BB\d+_\d+)", l)
+            if mi:
+                cur_loop = "L" + mi.group(1)
+            continue
+        st = l.strip()
+        if st.startswith(";"):
+            if re.search(r"Loop Header: Depth=", st) and header_lbl:
+                cur_loop = header_lbl
+                if pending_parent:
+                    parent.setdefault(header_lbl, pending_parent)
+            mp = re.search(r"Parent Loop (BB\d+_\d+) Depth=", st)
+            if mp and header_lbl and cur_loop == header_lbl:
+                parent.setdefault(header_lbl, "L" + mp.group(1))
+            mi = re.search(r"in Loop: Header=(BB\d+_\d+)", st)
+            if mi:
+                cur_loop = "L" + mi.group(1)
+            continue
+        if st:
+            out.append((st, cur_loop))
+
+    def chain(h):
+        c = []
+        while h is not None:
+            c.append(h)
+            h = parent.get(h)
+        return c
+    return [(i, h, chain(h)) for (i, h) in out]
+
+
+@pytest.fixture(scope="module")
+def tmp(tmp_path_factory):
+    return tmp_path_factory.mktemp("asm")
+
+
+def test_copy_claim_and_barriers_share_one_loop(tmp):
+    insts = annotate_loops(function_body(asm_of("copy.hip", tmp), "copy_kernel"))
+    claim = [k for k, (i, h, c) in enumerate(insts)
+             if re.match(r"^global_atomic_add_x2 v\[\d+:\d+\], v\d+, v\[\d+:\d+\], s\[\d+:\d+\] sc0$", i)]
+    barriers = [k for k, (i, h, c) in enumerate(insts) if i.startswith("s_barrier")]
+    assert claim and barriers
+    loop = insts[claim[0]][1]
+    assert loop is not None
+    # every barrier sits directly in the loop that makes the claim
+    assert all(insts[b][1] == loop for b in barriers), [(insts[b][1], loop) for b in barriers]
+
+
+def test_gemm_tile_claim_is_published_in_its_own_loop(tmp):
+    insts = annotate_loops(function_body(asm_of("gemm.hip", tmp), "gemm_bf16_persistentILb1E"))
+    # the tile claim: a returning atomic add on the per-XCD tile counters (offset 64)
+    claim = [k for k, (i, h, c) in enumerate(insts)
+             if re.match(r"^global_atomic_add v\d+, v\d+, v\d+, s\[\d+:\d+\] offset:64 sc0", i)]
+    assert len(claim) == 1
+    k = claim[0]
+    nxt = next(j for j in range(k, len(insts)) if insts[j][0].startswith("s_barrier"))
+    bar_loop = insts[nxt][1]
+    # the barrier publishing the tile is in the persistent tile loop, and that
+    # loop encloses the claim (the claim may sit in the small steal loop)
+    assert bar_loop is not None
+    assert bar_loop in insts[k][2], (bar_loop, insts[k][2])
