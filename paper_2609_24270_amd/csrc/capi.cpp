@@ -288,6 +288,10 @@ extern "C" int asym_copy_bf16(void* dst, const void* src, size_t n_bytes, int pa
   if (n_bytes == 0 || (n_bytes & 15u) || ((uintptr_t)dst & 15u) || ((uintptr_t)src & 15u))
     return fail(ASYM_EINVAL, "copy: size and pointers must be nonzero multiples of 16 bytes");
   if (passes < 1) return fail(ASYM_EINVAL, "copy: passes must be >= 1");
+  if (!copy_kernel_enabled())
+    return fail(ASYM_EUNSUPPORTED,
+                "copy: the streaming-copy kernel is switched off: its launches did not finish on the "
+                "device and the cause has not been found yet");
   hipStream_t s = static_cast<hipStream_t>(stream);
   std::lock_guard<std::mutex> lock(g_mu);
   int device = 0;

@@ -100,6 +100,10 @@ int launch_copy(void* dst, const void* src, size_t n_bytes, int passes, const in
   return ASYM_OK;
 }
 
+// The claim-loop copy kernel did not finish in two device runs whose cause is
+// not understood; it stays unreachable until the cause is shown.
+bool copy_kernel_enabled() { return false; }
+
 int launch_set_flag(int* flag, int v, hipStream_t s) {
   hipLaunchKernelGGL(set_flag_kernel, dim3(1), dim3(64), 0, s, flag, v);
   ASYM_HIP(hipGetLastError());

@@ -92,6 +92,7 @@ int launch_copy(void* dst, const void* src, size_t n_bytes, int passes,
                 const int* stop_flag, uint32_t xcd_mask, int grid,
                 unsigned long long* ctr, hipStream_t s);
 int launch_set_flag(int* flag, int v, hipStream_t s);
+bool copy_kernel_enabled();
 int copy_bytes_take(hipStream_t s, unsigned long long* bytes);
 void release_workspace(hipStream_t s);
 

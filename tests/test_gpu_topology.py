@@ -87,6 +87,11 @@ def test_masked_gemm_bitwise(dev, topo):
         asym.gemm(Ad, Bd, mapping="oblivious_grouped", topo=topo, xcd_mask=0x0F)
 
 
+COPY_OFF = ("the streaming-copy kernel is switched off in libasym: two device runs of this test "
+            "did not finish and the cause has not been found; it stays off the GPU until it is")
+
+
+@pytest.mark.skip(reason=COPY_OFF)
 def test_copy_kernel(dev):
     n = workloads.COPY_BYTES // 2
     src = workloads.copy_source(n).to(dev)
@@ -103,6 +108,7 @@ def test_copy_kernel(dev):
     assert torch.equal(d2, s2)
 
 
+@pytest.mark.skip(reason=COPY_OFF)
 def test_corun_gemm_and_copy(dev, topo):
     A, B = workloads.make_inputs(workloads.COLOC)
     Ad, Bd = A.to(dev), B.to(dev)
@@ -124,3 +130,37 @@ def test_corun_gemm_and_copy(dev, topo):
                       asym.copy_task(dst, src, 0, xcd_mask=0xF0)], topo)
     print(res)
     assert torch.equal(C, ref)
+
+
+def test_copy_reports_switched_off(dev):
+    src = torch.zeros(1024, dtype=torch.bfloat16, device=dev)
+    with pytest.raises(asym.AsymError) as e:
+        asym.copy(torch.empty_like(src), src)
+    assert e.value.status == asym.EUNSUPPORTED
+
+
+def test_corun_prefill_decode(dev, topo):
+    """Prefill and decode GEMMs co-running on CU-striped masks (every XCD split
+    24/8) and on whole-XCD partitions (6 XCDs / 2 XCDs) give bitwise the
+    results of the GEMMs run alone."""
+    (pa, pb), (da, db) = workloads.make_pd_inputs()
+    pa, pb, da, db = pa.to(dev), pb.to(dev), da.to(dev), db.to(dev)
+    ref_p = asym.gemm(pa, pb)
+    ref_d = asym.gemm(da, db)
+    torch.cuda.synchronize()
+    R, _ = oracle.gemm_bf16(bits(da)[:, :], bits(db)[:256], "nk")
+    assert_gemm_close(bits(ref_d)[:, :256], R)
+    cp = torch.empty_like(ref_p)
+    cd = torch.empty_like(ref_d)
+    prefill = topo.cuset(192, asym.CUSET_STRIPED)
+    decode = [b for b in range(256) if b not in set(prefill)]
+    assert topo.cuset_counts(prefill) == [24] * 8 and topo.cuset_counts(decode) == [8] * 8
+    res = asym.corun([asym.gemm_task(pa, pb, cp, 3, "aware", mask=prefill),
+                      asym.gemm_task(da, db, cd, 20, "aware", mask=decode)], topo)
+    print("striped", res)
+    assert torch.equal(cp, ref_p) and torch.equal(cd, ref_d)
+    assert res[0]["tflops"] > 0 and res[1]["tflops"] > 0
+    res = asym.corun([asym.gemm_task(pa, pb, cp, 3, "aware", xcd_mask=0x3F),
+                      asym.gemm_task(da, db, cd, 20, "aware", xcd_mask=0xC0)], topo)
+    print("xcd-aligned", res)
+    assert torch.equal(cp, ref_p) and torch.equal(cd, ref_d)
