@@ -9,10 +9,12 @@ exact share T*w_x/W, and the tiles left over go one each to the largest
 fractional remainders, ties to the lower partition index).
 
 The tile order is the banded column-major walk: tile rows are cut into bands of
-`band` rows, each band is walked column by column, top to bottom.  AWARE gives
-partition x the contiguous run of the order of length quota[x], partitions in
-index order; the oblivious mappings hand order position i to workgroup i mod P,
-which round-robin dispatch places on partition (i mod P) mod n.
+`band` rows, each band is walked column by column, top to bottom.  AWARE shares
+every band out among the partitions: the band's walk is cut into contiguous
+runs of Hamilton-apportioned lengths, one per partition in index order, and a
+partition's list is its run of band 0, then of band 1, and so on.  The
+oblivious mappings hand order position i of the whole walk to workgroup
+i mod P, which round-robin dispatch places on partition (i mod P) mod n.
 
 Written from the definitions with exact rational arithmetic; no code is shared
 with the library.
@@ -56,17 +58,34 @@ def rowmajor_order(tiles_m: int, tiles_n: int):
     return list(range(tiles_m * tiles_n))
 
 
+def band_walks(tiles_m: int, tiles_n: int, band: int):
+    """The banded walk, one list per band."""
+    walks = []
+    r0 = 0
+    while r0 < tiles_m:
+        rows = range(r0, min(tiles_m, r0 + band))
+        walks.append([r * tiles_n + c for c in range(tiles_n) for r in rows])
+        r0 += band
+    return walks
+
+
+def aware_lists(tiles_m, tiles_n, slots, band):
+    """Per-partition tile lists of the aware mapping."""
+    lists = [[] for _ in slots]
+    for walk in band_walks(tiles_m, tiles_n, band):
+        q = hamilton_quotas(len(walk), slots)
+        pos = 0
+        for x, qx in enumerate(q):
+            lists[x].extend(walk[pos:pos + qx])
+            pos += qx
+    return lists
+
+
 def aware_assignment(tiles_m, tiles_n, slots, band):
-    """tile id -> partition, for the aware mapping."""
-    order = banded_order(tiles_m, tiles_n, band)
-    q = hamilton_quotas(len(order), slots)
-    owner = {}
-    pos = 0
-    for x, qx in enumerate(q):
-        for t in order[pos:pos + qx]:
-            owner[t] = x
-        pos += qx
-    return owner, q
+    """tile id -> partition, and the per-partition tile counts."""
+    lists = aware_lists(tiles_m, tiles_n, slots, band)
+    owner = {t: x for x, lst in enumerate(lists) for t in lst}
+    return owner, [len(lst) for lst in lists]
 
 
 def oblivious_assignment(order, slots):

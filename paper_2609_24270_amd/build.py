@@ -26,6 +26,10 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-function"]
 # Packed fp32 VALU forms are kept out of the device code.
 DEVICE_ONLY = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Per-source extras.  gemm.hip: let the MFMA accumulators take the VGPR form, so
+# that the register allocator can keep 256 fp32 accumulators and two sets of
+# operand fragments without spilling (the AGPR-only form spills in the k-loop).
+EXTRA = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:
@@ -38,7 +42,7 @@ def hipcc() -> str:
 def _compile(src: str) -> str:
     out = os.path.join(OBJ, os.path.splitext(src)[0] + ".o")
     cmd = [hipcc()] + COMMON + (DEVICE_ONLY if src.endswith(".hip") else []) + \
-        ["-c", os.path.join(CSRC, src), "-o", out]
+        EXTRA.get(src, []) + ["-c", os.path.join(CSRC, src), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

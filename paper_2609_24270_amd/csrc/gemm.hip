@@ -18,17 +18,23 @@
 // bf16; fp32 accumulation in the matrix cores (v_mfma_f32_16x16x32_bf16);
 // bf16 round-to-nearest-even output (v_cvt_pk_bf16_f32).
 //
-// Tile 256x256x64, 256 threads = 4 waves in a 2x2 grid, 128x128 per wave
-// (8x8 MFMA blocks, 256 fp32 accumulators per lane).  LDS: two stages of A and
-// B, rows padded to 72 bf16 (144 B) so that the 16-byte reads of 16 different
-// rows fall in distinct banks; 144 KiB in all, one workgroup per CU.
-// Global->LDS staging goes through registers with 16-byte loads: the next
-// k-step's loads are issued before the current step's MFMAs and written to the
-// other LDS stage after them, with one barrier per k-step.
+// Tile 256x256, 256 threads = 4 waves in a 2x2 grid, 128x128 per wave (8x8
+// MFMA blocks, 256 fp32 accumulators per lane in AGPRs).
 //
-// The MFMA's first operand is taken from B and its second from A, so each
-// lane's four accumulators are four consecutive columns of one C row: the
-// epilogue stores 8 contiguous bytes per lane.
+// Vector path (16-byte aligned operands, K a multiple of 8): k advances in
+// stages of 32 through a ring of four LDS slots (A and B, 256 rows x 64 bytes
+// each, 32 KiB per slot).  Operands go from HBM straight into LDS with
+// buffer_load_dwordx4 ... lds (no staging registers, no LDS write
+// instructions); the loads for stage t+4 are issued when stage t starts, so
+// three stages of MFMA work cover their latency.  Inside a row the four
+// 16-byte chunks are stored XOR-swizzled by (row >> 1) & 3, which keeps the
+// 16 rows read by one ds_read_b128 free of bank conflicts.  MFMA fragments are
+// double-buffered: stage t+1's fragments are read while stage t's 64 MFMAs
+// run.  One barrier per stage publishes the next slot; waits on the loads are
+// explicit, so the barrier does not drain the prefetch.
+//
+// Generic path (any alignment or K): 256x256x64 tiles, register-staged
+// element loads into two padded LDS stages.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -210,53 +216,372 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
   }
 }
 
+// ---- vector path: direct-to-LDS four-slot ring ---------------------------------
+constexpr int KS = 32;                 // k per stage
+constexpr int SLOTS = 4;
+constexpr int SLOT_BYTES = 32768;      // A (16 KiB) then B (16 KiB)
+constexpr int RING_BYTES = SLOTS * SLOT_BYTES;
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
+  const unsigned long long a = (unsigned long long)base;
+  return i32x4{(int)(uint32_t)a, (int)(uint32_t)(a >> 32), (int)bytes, 0x00020000};
+}
+
+// Direct-to-LDS load of 16 tile rows (1 KiB): lane L lands at M0 + 16 L, i.e.
+// row L/4 of the 16, physical chunk L%4; `vo` already selects the logical
+// chunk that belongs there, `so` the row block and k (uniform).
+__device__ __forceinline__ void dma_1k(uint32_t lds_dst, i32x4 rs, uint32_t vo, int so) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_dst);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(m0), "v"(vo), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(so)) : "memory");
+}
+
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// acc += A . B on the matrix cores, with the accumulator pinned to AGPRs and
+// the fragments to VGPRs.  Issued as inline asm so the register files and the
+// issue order are exactly as written; the compiler does not see these MFMAs,
+// so the hazard padding around them is explicit (mfma_fence()).
+__device__ __forceinline__ void mfma_acc(f32x4& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+// Wait states between VALU accesses of accumulators and the MFMAs that use
+// them (covers the longest MFMA-to-VALU dependency of the 16x16x32 shape).
+__device__ __forceinline__ void mfma_fence() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+
+// 16-byte LDS read of one MFMA fragment into VGPRs.  Issued as inline asm so
+// the compiler neither tracks nor waits on it: the stage that consumes the
+// fragment starts with lds_barrier(), whose lgkmcnt(0) is the wait, and the
+// fragment's registers are not touched before that (checked in the ISA).
+template <int OFF>
+__device__ __forceinline__ void lds_read_frag(bf16x8& f, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(f) : "v"(addr), "i"(OFF) : "memory");
+}
+
+struct RingCtx {
+  i32x4 rsa, rsb;
+  uint32_t voa, vob, dst_a, dst_b;
+  int lda, ldb, K, lchunk;
+};
+
+// Lane 0's fetch of the workgroup's next tile, issued from inside the k-loop
+// at stage KT - 4, so that its latency, including the contention of an XCD's
+// workgroups on one counter, overlaps the last stages' MFMA work: vector
+// memory operations complete in order, and a claim issued before a tile's
+// first loads would hold up the waits on them.  Issuing it late keeps the
+// fetched values live for only a few stages (an early fetch's result, live
+// across the whole k-loop, ends up spilled, and the spill waits on memory).
+constexpr int CLAIM_FROM_END = 4;
+struct NextTile {
+  const int* order;
+  int* counter;      // aware: the own XCD's tile counter; null for oblivious
+  int own_off, own_q;
+  int pend;          // aware: own-region index claimed one tile ahead (observed)
+  int claimed;       // aware: the claim issued during this tile (in flight)
+  int i_next;        // oblivious: next position of the shared order
+  int n_tiles;
+  int raw;           // order entry loaded during this tile (in flight)
+  int result;        // finish_next's answer, kept (scalar) across the epilogue
+  bool fetched;
+  bool finished;
+};
+
+// Issue the fetch (lane 0).  Only loads are issued here, and their results
+// are first touched at the end of the tile (finish_next), so nothing in the
+// k-loop waits on them.  The order entry read is always in bounds; whether it
+// is the next tile is decided at the end.
+__device__ __forceinline__ void fetch_next(NextTile& n) {
+  if (n.fetched) return;
+  n.fetched = true;
+  if (threadIdx.x != 0) return;
+  if (n.counter) {
+    const int i = n.own_off + (n.pend < n.own_q ? n.pend : 0);
+    n.raw = n.order[i];
+    if (n.pend < n.own_q) n.claimed = atomicAdd(n.counter, 1);
+  } else {
+    n.raw = n.order[n.i_next < n.n_tiles ? n.i_next : 0];
+  }
+}
+
+// End of a tile (lane 0): the next tile (-1 none, -2 own region exhausted),
+// and the claim issued during the tile becomes `pend`.  The readfirstlanes are
+// real instructions on the loaded values, so the compiler's waits land here.
+// Called right after the tile's k-loop has drained its loads, before the
+// epilogue: the epilogue needs every VGPR for the accumulators, so nothing of
+// the fetch may stay live across it except the scalar `result`.
+__device__ __forceinline__ void finish_next(NextTile& n) {
+  if (n.finished) return;
+  n.finished = true;
+  if (threadIdx.x != 0) return;
+  const int raw = __builtin_amdgcn_readfirstlane(n.raw);
+  if (n.counter) {
+    const bool mine = n.pend < n.own_q;
+    if (mine) n.pend = __builtin_amdgcn_readfirstlane(n.claimed);
+    n.result = mine ? raw : -2;
+  } else {
+    n.result = n.i_next < n.n_tiles ? raw : -1;
+  }
+}
+
+// g-th of the 8 loads of stage t into slot t % SLOTS: g < 4 are A's, g >= 4
+// B's; each wave owns rows w*64 .. w*64+63 of both operands.  Stages at or past
+// the end of K are sent out of range and fill the slot with zeros.
+__device__ __forceinline__ void ring_load(const RingCtx& c, int t, int g) {
+  const int k0 = t * KS;
+  const uint32_t slot = (uint32_t)(t & (SLOTS - 1)) * SLOT_BYTES;
+  const bool in_k = k0 + c.lchunk * 8 < c.K;
+  const int i = g & 3;
+  if (g < 4)
+    dma_1k(c.dst_a + slot + i * 1024, c.rsa, in_k ? c.voa : kOOB, (16 * i * c.lda + k0) * 2);
+  else
+    dma_1k(c.dst_b + slot + i * 1024, c.rsb, in_k ? c.vob : kOOB, (16 * i * c.ldb + k0) * 2);
+}
+
+// One group of a stage: refill slot t with load G of stage t+4, run stage t's
+// 8 MFMAs that use B fragment G, then read stage t+1's A fragment G into `an`
+// and its B fragment G into `b` (B fragment G has no later use in this stage,
+// so it is replaced in place; the A fragments feed every group and are double
+// buffered).  `sa`/`sb` are the LDS addresses of stage t+1's fragment 0.
+template <int G>
+__device__ __forceinline__ void ring_group(const RingCtx& c, int t, f32x4 (&acc)[8][8],
+                                           const bf16x8 (&ac)[8], bf16x8 (&an)[8], bf16x8 (&b)[8],
+                                           uint32_t sa, uint32_t sb) {
+  ring_load(c, t + SLOTS, G);
+#pragma unroll
+  for (int mb = 0; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
+  lds_read_frag<G * 1024>(an[G], sa);
+  lds_read_frag<G * 1024>(b[G], sb);
+  if constexpr (G + 1 < 8) ring_group<G + 1>(c, t, acc, ac, an, b, sa, sb);
+}
+
+// One stage, branch-free: wait for this wave's loads of stage t+1 (stages t+2
+// and t+3 stay in flight), publish slot t+1 to all waves, then the 8 groups.
+// Every instruction of the stage is inline asm, so the issue order is exactly
+// the program order: no MFMA waits on a read issued in the same stage.
+__device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)[8][8],
+                                           const bf16x8 (&ac)[8], bf16x8 (&an)[8], bf16x8 (&b)[8],
+                                           uint32_t ra0, uint32_t rb0, NextTile& nt, int claim_t) {
+  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  lds_barrier();
+  const uint32_t s = (uint32_t)((t + 1) & (SLOTS - 1)) * SLOT_BYTES;
+  ring_group<0>(c, t, acc, ac, an, b, ra0 + s, rb0 + s);
+  if (t == claim_t) fetch_next(nt);
+}
+
+__device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, unsigned char* lds,
+                                                  NextTile& nt) {
+  // Everything the tile needs passes through an opaque move first, so that no
+  // per-lane setup is hoisted out of the tile loop and kept live (and spilled)
+  // across the k-loop; recomputing it per tile costs a few instructions.
+  Params p = pin;
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid), "+s"(p.K), "+s"(p.lda), "+s"(p.ldb), "+s"(p.ldc), "+s"(p.M), "+s"(p.N));
+  const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int KT = (p.K + KS - 1) / KS;
+
+  f32x4 acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  mfma_fence();
+  const int rows_a = min(BM, p.M - m0), rows_b = min(BN, p.N - n0);
+  const i32x4 rsa = rsrc_words(p.A + (size_t)m0 * p.lda, (uint32_t)rows_a * p.lda * 2u);
+  const i32x4 rsb = rsrc_words(p.B + (size_t)n0 * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
+  // load side: lane -> (row in its 16-row group, logical chunk)
+  const int lrow = lane >> 2;
+  const int lchunk = (lane & 3) ^ ((lrow >> 1) & 3);
+  const uint32_t voa = (uint32_t)((wave * 64 + lrow) * p.lda + lchunk * 8) * 2u;
+  const uint32_t vob = (uint32_t)((wave * 64 + lrow) * p.ldb + lchunk * 8) * 2u;
+  const uint32_t lds0 = (uint32_t)(size_t)lds;
+  const uint32_t dst_a = lds0 + wave * 64 * 64, dst_b = lds0 + 16384 + wave * 64 * 64;
+  // read side: lane -> (row l%16 of a 16-row block, physical chunk of logical chunk l/16)
+  const int rrow = lane & 15;
+  const int pchunk = (lane >> 4) ^ ((rrow >> 1) & 3);
+  const uint32_t ra0 = lds0 + (uint32_t)((wm * 128 + rrow) * 64 + pchunk * 16);
+  const uint32_t rb0 = lds0 + (uint32_t)(16384 + (wn * 128 + rrow) * 64 + pchunk * 16);
+
+  RingCtx c{rsa, rsb, voa, vob, dst_a, dst_b, p.lda, p.ldb, p.K, lchunk};
+  // prologue: stages 0..3 in flight (stages past K load zeros), stage 0 published
+#pragma unroll
+  for (int t = 0; t < SLOTS; ++t)
+#pragma unroll
+    for (int g = 0; g < 8; ++g) ring_load(c, t, g);
+  asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+  lds_barrier();
+  bf16x8 a0[8], a1[8], bf[8];
+  lds_read_frag<0>(a0[0], ra0); lds_read_frag<1024>(a0[1], ra0);
+  lds_read_frag<2048>(a0[2], ra0); lds_read_frag<3072>(a0[3], ra0);
+  lds_read_frag<4096>(a0[4], ra0); lds_read_frag<5120>(a0[5], ra0);
+  lds_read_frag<6144>(a0[6], ra0); lds_read_frag<7168>(a0[7], ra0);
+  lds_read_frag<0>(bf[0], rb0); lds_read_frag<1024>(bf[1], rb0);
+  lds_read_frag<2048>(bf[2], rb0); lds_read_frag<3072>(bf[3], rb0);
+  lds_read_frag<4096>(bf[4], rb0); lds_read_frag<5120>(bf[5], rb0);
+  lds_read_frag<6144>(bf[6], rb0); lds_read_frag<7168>(bf[7], rb0);
+  const int claim_t = KT > CLAIM_FROM_END ? KT - CLAIM_FROM_END : 0;
+  for (int t = 0; t < KT; t += 2) {
+    ring_stage(c, t, acc, a0, a1, bf, ra0, rb0, nt, claim_t);
+    if (t + 1 < KT) ring_stage(c, t + 1, acc, a1, a0, bf, ra0, rb0, nt, claim_t);
+  }
+  // drain the loads still in flight (zero fills past K) before the slots
+  // are reused, and make sure every wave is past its last LDS read
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  fetch_next(nt);   // for a K too short to reach the claim stage
+  finish_next(nt);
+  mfma_fence();
+  // every wave is past its last LDS read before the slots are reused
+  lds_barrier();
+
+  // epilogue: lane holds C[m][n..n+3] for each (nb, mb) block.  The lane's
+  // own offset is one VGPR; the block's offset is uniform and goes in the
+  // scalar offset.  Rows past M fall outside the resource: stores dropped.
+  // (the inputs pass through an opaque move so that nothing below is hoisted
+  // out of the tile loop and kept live across the k-loop)
+  int ldc = p.ldc, nN = p.N, lid = lane;
+  const int rows_c = min(BM, p.M - m0);
+  const __amdgpu_buffer_rsrc_t rsc = make_rsrc(p.C + (size_t)m0 * ldc + n0, (uint32_t)rows_c * ldc * 2u);
+  const int ncol = wn * WN + (lid >> 4) * 4;  // lane's first column within the tile
+  const uint32_t vc = (uint32_t)((wm * WM + (lid & 15)) * ldc + ncol) * 2u;
+#pragma unroll
+  for (int nb = 0; nb < 8; ++nb) {
+    const int n = n0 + ncol + nb * 16;
+    // keep this block's accumulators in AGPRs up to here, so that they are
+    // copied to VGPRs one block at a time (not all 256 at the loop exit)
+    asm volatile("" :: "a"(acc[nb][0]), "a"(acc[nb][1]), "a"(acc[nb][2]), "a"(acc[nb][3]),
+                 "a"(acc[nb][4]), "a"(acc[nb][5]), "a"(acc[nb][6]), "a"(acc[nb][7]));
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const f32x4 v = acc[nb][mb];
+      const int so = (mb * 16 * ldc + nb * 16) * 2;
+      if (n + 3 < nN) {
+        v2u w;
+        w.x = pack_bf16x2(v[0], v[1]);
+        w.y = pack_bf16x2(v[2], v[3]);
+        __builtin_amdgcn_raw_buffer_store_b64(w, rsc, vc, so, 0);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const __bf16 h = (__bf16)v[r];
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), rsc,
+                                                n + r < nN ? vc + 2u * r : kOOB, so, 0);
+        }
+      }
+    }
+    // one column block of accumulators at a time, so their VGPR copies stay few
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Claim the next tile for a workgroup on XCD `xcc` (aware mapping): its own
+// XCD's region first, then the other regions (work stealing), so every tile is
+// computed whatever the hardware's placement of workgroups.  Returns -1 when
+// all regions are exhausted.  Called by one lane.
+__device__ __forceinline__ int claim_aware(const Params& p, int xcc) {
+  int tile = -1;
+  for (int d = 0; d < p.n_xccs && tile < 0; ++d) {
+    const int y = (xcc + d) % p.n_xccs;
+    const int q = p.off[y + 1] - p.off[y];
+    if (q <= 0) continue;
+    // a cheap read first, so exhausted regions are not hammered
+    if (__hip_atomic_load(&p.ctr[16 + y], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= q) continue;
+    const int t = atomicAdd(&p.ctr[16 + y], 1);
+    if (t < q) tile = p.order[p.off[y] + t];
+  }
+  return tile;
+}
+
+template <bool VEC>
+__device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned char* lds, NextTile& nt) {
+  if constexpr (VEC)
+    compute_tile_ring(p, tile, lds, nt);
+  else
+    compute_tile<false>(p, tile, reinterpret_cast<uint16_t*>(lds),
+                        reinterpret_cast<uint16_t*>(lds) + 2 * BM * LDP);
+  fetch_next(nt);   // no-ops if the tile routine already did them
+  finish_next(nt);
+}
+
+constexpr int LDS_BYTES = RING_BYTES > 2 * (BM + BN) * LDP * 2 ? RING_BYTES : 2 * (BM + BN) * LDP * 2;
+
 template <bool VEC>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 gemm_bf16_persistent(Params p) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2 * BM * LDP];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2 * BN * LDP];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[VEC ? RING_BYTES : 2 * (BM + BN) * LDP * 2];
   __shared__ int s_info[2];
 
-  if (p.mapping == ASYM_MAP_AWARE) {
-    const int xcc = (int)read_xcc_id();
-    if (threadIdx.x == 0) {
+  // Aware: a rank ticket per XCD; workgroups beyond the XCD's scheduled CU
+  // count leave at once.  Oblivious: every workgroup is a persistent worker.
+  const int xcc = (int)read_xcc_id();
+  const bool aware = p.mapping == ASYM_MAP_AWARE;
+  const int own = xcc < p.n_xccs ? xcc : 0;
+  // read (and observed) before the tile loop, so that no first use inside the
+  // k-loop makes the compiler wait there on these loads
+  const int own_off = __builtin_amdgcn_readfirstlane(aware ? p.off[own] : 0);
+  const int own_q = __builtin_amdgcn_readfirstlane(aware ? p.off[own + 1] - p.off[own] : 0);
+  NextTile nt;
+  nt.order = p.order;
+  nt.counter = aware ? &p.ctr[16 + own] : nullptr;
+  nt.own_off = own_off;
+  nt.own_q = own_q;
+  nt.pend = 0;
+  nt.claimed = 0;
+  nt.raw = 0;
+  nt.result = -1;
+  nt.i_next = blockIdx.x;
+  nt.n_tiles = p.n_tiles;
+  if (threadIdx.x == 0) {
+    int active = 1, first;
+    if (aware) {
       int r = -1;
       if (xcc < p.n_xccs) r = atomicAdd(&p.ctr[xcc], 1);
-      s_info[0] = (xcc < p.n_xccs && r < p.slots[xcc]) ? 1 : 0;
+      active = (xcc < p.n_xccs && r < p.slots[xcc]) ? 1 : 0;
+      first = active ? claim_aware(p, xcc) : -1;
+      if (active) nt.pend = atomicAdd(nt.counter, 1);
+      // observe the claim here (a wait before the tile loop) so the first
+      // fetch inside the k-loop finds it complete and waits on nothing
+      nt.pend = __builtin_amdgcn_readfirstlane(nt.pend);
+    } else {
+      first = (int)blockIdx.x < p.n_tiles ? p.order[blockIdx.x] : -1;
+    }
+    s_info[1] = first;
+  }
+  __syncthreads();
+  int tile = s_info[1];
+  while (tile >= 0) {
+    // lane 0 fetches the following tile during this tile (fetch_next): the
+    // order entry of the index claimed one tile ago and the aware claim of the
+    // tile after that, or position i + grid of the shared order (oblivious)
+    nt.i_next += gridDim.x;
+    nt.fetched = false;
+    nt.finished = false;
+    run_tile<VEC>(p, tile, lds, nt);
+    if (threadIdx.x == 0) {
+      int nxt = nt.result;
+      if (nxt == -2) nxt = claim_aware(p, xcc);
+      s_info[1] = nxt;
     }
     __syncthreads();
-    if (s_info[0]) {
-      for (;;) {
-        if (threadIdx.x == 0) {
-          int tile = -1;
-          for (int d = 0; d < p.n_xccs && tile < 0; ++d) {
-            const int y = (xcc + d) % p.n_xccs;
-            const int q = p.off[y + 1] - p.off[y];
-            if (q <= 0) continue;
-            // a cheap read first, so exhausted regions are not hammered
-            if (__hip_atomic_load(&p.ctr[16 + y], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= q) continue;
-            const int t = atomicAdd(&p.ctr[16 + y], 1);
-            if (t < q) tile = p.order[p.off[y] + t];
-          }
-          s_info[1] = tile;
-        }
-        __syncthreads();
-        const int tile = s_info[1];
-        if (tile < 0) break;
-        compute_tile<VEC>(p, tile, sA, sB);
-      }
-    }
+    tile = s_info[1];
+  }
+  if (aware && threadIdx.x == 0) {
     // the last workgroup to leave resets the counters for the next launch
-    if (threadIdx.x == 0) {
+    __threadfence();
+    const int done = atomicAdd(&p.ctr[32], 1);
+    if (done == (int)gridDim.x - 1) {
+      for (int c = 0; c < 33; ++c) atomicExch(&p.ctr[c], 0);
       __threadfence();
-      const int done = atomicAdd(&p.ctr[32], 1);
-      if (done == (int)gridDim.x - 1) {
-        for (int i = 0; i < 33; ++i) atomicExch(&p.ctr[i], 0);
-        __threadfence();
-      }
     }
-  } else {
-    for (int i = blockIdx.x; i < p.n_tiles; i += gridDim.x) compute_tile<VEC>(p, p.order[i], sA, sB);
   }
 }
 

@@ -13,10 +13,16 @@
 // column by column, each column top to bottom.  A run of s consecutive tiles of
 // this order covers about band rows x s/band columns, a near-square block when
 // band ~ sqrt(s).
-//   AWARE:             XCD x owns a contiguous run of the order whose length
-//                      is its largest-remainder quota of the tile count,
-//                      weighted by its persistent workgroups.
-//   OBLIVIOUS_GROUPED: the same order, tile i to workgroup i mod P; round-robin
+//   AWARE:             every band is shared out among the XCDs: the band's
+//                      tiles, in the banded order, are cut into contiguous runs
+//                      whose lengths are the largest-remainder apportionment of
+//                      the band's tile count by the XCDs' persistent
+//                      workgroups, and an XCD's list is its run of band 0, then
+//                      of band 1, and so on.  Each XCD's concurrent tiles then
+//                      form a compact block in its own L2, and all XCDs work in
+//                      the same band at the same time, so the band's A rows are
+//                      fetched from HBM once for all of them (memory-side cache).
+//   OBLIVIOUS_GROUPED: the banded order, tile i to workgroup i mod P; round-robin
 //                      dispatch then puts neighbouring tiles on different XCDs.
 //   OBLIVIOUS_ROWMAJOR: row-major order, tile i to workgroup i mod P.
 #include <algorithm>
@@ -112,9 +118,29 @@ int build_schedule(int tiles_m, int tiles_n, int n_xcds, const int* slots,
   }
 
   if (mapping == ASYM_MAP_AWARE) {
+    // per band: apportion the band's tiles, cut the band's banded order into
+    // one contiguous run per XCD; then concatenate each XCD's runs band by band
+    const int h = band > 0 ? std::min(band, tiles_m) : choose_band(tiles_m, smax);
     std::vector<int> w(slots, slots + n_xcds);
-    s.quota = largest_remainder_quotas(T, w);
-    for (int x = 0; x < n_xcds; ++x) s.off[x + 1] = s.off[x] + s.quota[x];
+    std::vector<std::vector<int>> lists(n_xcds);
+    int i = 0;
+    for (int r0 = 0; r0 < tiles_m; r0 += h) {
+      const int len = (std::min(tiles_m, r0 + h) - r0) * tiles_n;
+      const std::vector<int> q = largest_remainder_quotas(len, w);
+      int pos = i;
+      for (int x = 0; x < n_xcds; ++x) {
+        lists[x].insert(lists[x].end(), s.order.begin() + pos, s.order.begin() + pos + q[x]);
+        pos += q[x];
+      }
+      i += len;
+    }
+    int o = 0;
+    for (int x = 0; x < n_xcds; ++x) {
+      std::copy(lists[x].begin(), lists[x].end(), s.order.begin() + o);
+      s.quota[x] = (int)lists[x].size();
+      o += s.quota[x];
+      s.off[x + 1] = o;
+    }
   } else {
     // one shared list; quota[x] counts tiles that workgroup i mod P, placed on
     // XCD (i mod P) mod n_xcds by round-robin dispatch, would run on XCD x

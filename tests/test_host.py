@@ -54,18 +54,21 @@ def _cases():
 def test_schedule_matches_oracle(lib, tm, tn, slots):
     T = tm * tn
     band = osched.band_cost_choice(tm, max(slots))
-    # aware: quotas are Hamilton's apportionment, runs of the banded order
+    # aware: every band apportioned by Hamilton's method, lists band by band
     order, off, quota = asym.schedule_build(tm, tn, slots, asym.MAP_AWARE)
-    assert quota == osched.hamilton_quotas(T, slots)
-    assert order == osched.banded_order(tm, tn, band)
+    lists = osched.aware_lists(tm, tn, slots, band)
+    assert quota == [len(lst) for lst in lists]
+    assert order == [t for lst in lists for t in lst]
     assert off[0] == 0 and all(off[x + 1] - off[x] == quota[x] for x in range(len(slots)))
     assert sorted(order) == list(range(T))                     # every tile exactly once
     W = sum(slots)
-    assert all(abs(quota[x] - T * slots[x] / W) < 1 for x in range(len(slots)))
+    n_bands = -(-tm // band)
+    # each band's share is within one tile of exact, so the total within n_bands
+    assert all(abs(quota[x] - T * slots[x] / W) < n_bands for x in range(len(slots)))
     assert all(q == 0 for q, s in zip(quota, slots) if s == 0)
-    # oblivious grouped: the same order, placed round-robin
+    # oblivious grouped: the whole banded walk, placed round-robin
     order_g, _, quota_g = asym.schedule_build(tm, tn, slots, asym.MAP_OBLIVIOUS_GROUPED)
-    assert order_g == order
+    assert order_g == osched.banded_order(tm, tn, band)
     owner = osched.oblivious_assignment(order_g, slots)
     assert quota_g == [sum(1 for v in owner.values() if v == x) for x in range(len(slots))]
     # oblivious row-major
@@ -74,20 +77,33 @@ def test_schedule_matches_oracle(lib, tm, tn, slots):
 
 
 def test_schedule_explicit_band(lib):
-    order, _, _ = asym.schedule_build(10, 7, [4] * 8, asym.MAP_AWARE, band=3)
+    order, _, _ = asym.schedule_build(10, 7, [4] * 8, asym.MAP_OBLIVIOUS_GROUPED, band=3)
     assert order == osched.banded_order(10, 7, 3)
+    order, _, _ = asym.schedule_build(10, 7, [4] * 8, asym.MAP_AWARE, band=3)
+    assert order == [t for lst in osched.aware_lists(10, 7, [4] * 8, 3) for t in lst]
+
+
+def test_hamilton_pins():
+    # textbook cases of the largest-remainder method
+    assert osched.hamilton_quotas(10, [1, 1, 1]) == [4, 3, 3]      # tie to the lowest index
+    assert osched.hamilton_quotas(7, [5, 3, 2]) == [4, 2, 1]       # 3.5, 2.1, 1.4 -> 3,2,1 + 1 to the .5
+    assert osched.hamilton_quotas(100, [1, 0, 3]) == [25, 0, 75]
+    assert osched.hamilton_quotas(5, [0, 0, 2]) == [0, 0, 5]
 
 
 def test_aware_wave_blocks_are_compact():
-    # 8192^3 at 256^2 tiles: 32 tiles per XCD per wave form 8 rows x 4 columns
+    # 8192^3 at 256^2 tiles: 32 tiles per XCD per wave form 8 rows x 4 columns,
+    # and in each wave all XCDs share the same 8 rows of A
     order, off, quota = asym.schedule_build(32, 32, [32] * 8, asym.MAP_AWARE)
-    for x in range(8):
-        run = order[off[x]:off[x + 1]]
-        for w in range(0, len(run), 32):
-            wave = run[w:w + 32]
+    for w in range(4):
+        band_rows = set()
+        for x in range(8):
+            wave = order[off[x] + 32 * w: off[x] + 32 * (w + 1)]
             rows = {t // 32 for t in wave}
             cols = {t % 32 for t in wave}
             assert len(rows) + len(cols) == 12
+            band_rows |= rows
+        assert len(band_rows) == 8
     # the grouped-oblivious order spreads each wave over 1 row x 32 columns per XCD
     order_g, _, _ = asym.schedule_build(32, 32, [32] * 8, asym.MAP_OBLIVIOUS_GROUPED)
     own = osched.oblivious_assignment(order_g, [32] * 8)

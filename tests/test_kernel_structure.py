@@ -22,6 +22,7 @@ def asm_of(src: str, tmp_path) -> str:
     out = tmp_path / (os.path.basename(src) + ".s")
     cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"),
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           *(["-mllvm", "-amdgpu-mfma-vgpr-form=1"] if src == "gemm.hip" else []),
            "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", str(out)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
@@ -99,16 +100,36 @@ def test_copy_claim_and_barriers_share_one_loop(tmp):
     assert all(insts[b][1] == loop for b in barriers), [(insts[b][1], loop) for b in barriers]
 
 
+def claims_published_in_their_loop(insts, claim_re):
+    """For every claim atomic: if a loop enclosing it contains barriers, the
+    outermost such loop must hold a barrier directly, not only inside a nested
+    loop that the claim is not part of (the shape that never finishes)."""
+    bar_chains = [c for (i, h, c) in insts if i.startswith("s_barrier")]
+    bar_inner = {h for (i, h, c) in insts if i.startswith("s_barrier")}
+    claims = [k for k, (i, h, c) in enumerate(insts) if re.match(claim_re, i)]
+    assert claims
+    checked = 0
+    for k in claims:
+        chain = insts[k][2]
+        with_bars = [L for L in chain if any(L in bc for bc in bar_chains)]
+        if not with_bars:
+            continue            # a lane-local loop with no barrier anywhere in it
+        outer = with_bars[-1]   # chains list loops innermost first
+        assert outer in bar_inner, (k, chain, outer)
+        checked += 1
+    return checked
+
+
 def test_gemm_tile_claim_is_published_in_its_own_loop(tmp):
     insts = annotate_loops(function_body(asm_of("gemm.hip", tmp), "gemm_bf16_persistentILb1E"))
-    # the tile claim: a returning atomic add on the per-XCD tile counters (offset 64)
-    claim = [k for k, (i, h, c) in enumerate(insts)
-             if re.match(r"^global_atomic_add v\d+, v\d+, v\d+, s\[\d+:\d+\] offset:64 sc0", i)]
-    assert len(claim) == 1
-    k = claim[0]
-    nxt = next(j for j in range(k, len(insts)) if insts[j][0].startswith("s_barrier"))
-    bar_loop = insts[nxt][1]
-    # the barrier publishing the tile is in the persistent tile loop, and that
-    # loop encloses the claim (the claim may sit in the small steal loop)
-    assert bar_loop is not None
-    assert bar_loop in insts[k][2], (bar_loop, insts[k][2])
+    # tile claims: returning atomic adds on the per-XCD tile counters (offset 64)
+    n = claims_published_in_their_loop(
+        insts, r"^global_atomic_add v\d+, v\d+, v\d+, s\[\d+:\d+\] offset:64 sc0")
+    assert n >= 1
+
+
+def test_copy_claim_checked_by_the_general_rule(tmp):
+    insts = annotate_loops(function_body(asm_of("copy.hip", tmp), "copy_kernel"))
+    n = claims_published_in_their_loop(
+        insts, r"^global_atomic_add_x2 v\[\d+:\d+\], v\d+, v\[\d+:\d+\], s\[\d+:\d+\] sc0$")
+    assert n >= 1
