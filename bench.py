@@ -1,14 +1,19 @@
 #!/usr/bin/env python3
 """Benchmark of the hot path: persistent XCD-aware bf16 GEMM on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--spread]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--studies ...]
 
 Workload: square bf16 GEMM M = N = K = 8192, inputs uniform[-1,1] from seed 1,
 B stored [N][K], fp32 accumulation, bf16 output, on the whole GPU; the
 topology probe runs first (untimed).  One step is one launch of the
 persistent GEMM with the XCD-aware mapping (the schedule is cached after the
-first launch).  The same K steps are then timed for the two oblivious
-mappings, for comparison.
+first launch).  W warm-up launches and a few seconds of untimed launches
+(the clock and power state settle) precede the K timed steps.
+
+Studies added to the same line (all on synthetic inputs): the three mappings
+timed interleaved at 8192^3; the decoder-layer shapes; prefill || decode on
+XCD-aligned and CU-striped partitions; the GEMM 4096^3 on 32 random and 2
+XCD-aligned 128-CU sets beside a second tenant, with the max/min spread.
 
 Prints one JSON line with the metric, the roofline of the GEMM kernel
 (achieved TFLOP/s from HIP events around every launch, against the 2516.6
@@ -89,10 +94,125 @@ def cpu_baseline(A, B, rows: int):
                       f"{flops / 1e9:.1f} GFLOP"}
 
 
-def spread_study(topo, dev, n_masks: int, iters: int):
-    """GEMM 4096^3 on 128-CU masks (seeded random over mask bits, and the two
-    XCD-aligned halves through the XCD filter) with a streaming copy on the
-    complementary CUs; per-mask TFLOP/s for the aware and oblivious kernels."""
+def settle(fns, seconds: float):
+    """Untimed launches, round-robin over fns, for `seconds` of wall time: the
+    chip's clock and power state move for a second or more after a burst of
+    GEMMs starts, and a measurement taken earlier would favour whichever
+    variant runs last."""
+    import torch
+    t0 = time.perf_counter()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        for f in fns:
+            f()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+
+
+def interleaved(fns: dict, rounds: int, stream) -> dict:
+    """Mean per-launch ms of each fn, timed with HIP events on `stream`, the
+    variants launched in turn within every round so that all of them see the
+    same clock and power state."""
+    import torch
+    names = list(fns)
+    evs = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(rounds)] for k in names}
+    torch.cuda.synchronize()
+    for r in range(rounds):
+        for k in names:
+            evs[k][r][0].record(stream)
+            fns[k]()
+            evs[k][r][1].record(stream)
+    torch.cuda.synchronize()
+    return {k: sum(a.elapsed_time(b) for a, b in evs[k]) / rounds for k in names}
+
+
+MAPPINGS = ("aware", "oblivious_grouped", "oblivious_rowmajor")
+
+
+def affinity_halves(topo, n_xcds: int):
+    """Two whole-XCD sets of equal size: the two measured affinity groups when the
+    latency probe found exactly two of equal size, else the lower and upper XCDs."""
+    g = topo.info()["group_of_xcd"]
+    if g and min(g) >= 0 and sorted(set(g)) == [0, 1] and g.count(0) == g.count(1):
+        a = sum(1 << x for x in range(n_xcds) if g[x] == 0)
+    else:
+        a = (1 << (n_xcds // 2)) - 1
+    return a, ((1 << n_xcds) - 1) & ~a
+
+
+def affinity_summary(topo):
+    L = topo.latency()
+    r = lambda v: [round(x, 1) for x in v]
+    return {"n_samples": L["n_samples"], "passes": L["passes"], "clock_mhz": round(L["clock_mhz"], 1),
+            "timer_overhead_cycles": L["timer_overhead"], "l2_hit_cycles": r(L["l2_hit"]),
+            "mall_hit_cycles": r(L["mall_hit"]), "hbm_cycles": r(L["hbm"]),
+            "group_of_xcd": L["group_of_xcd"], "home_share": [round(x, 4) for x in L["home_share"]],
+            "unclassified_share": round(L["unclassified_share"], 4),
+            "hbm_by_home_cycles": [r(v) for v in L["hbm_by_home"]]}
+
+
+def llm_shapes(dev, stream, rounds: int):
+    """Decoder-layer GEMMs M=4096 x (N,K) in {(14336,4096),(4096,14336),(6144,4096)},
+    N(0,0.02) weights and N(0,1) activations, full GPU, the three mappings."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    out = {}
+    for p in workloads.LLM_SHAPES:
+        A, B = workloads.make_inputs(p)
+        Ad, Bd = A.to(dev), B.to(dev)
+        C = torch.empty((p.M, p.N), dtype=torch.bfloat16, device=dev)
+        fns = {m: (lambda m=m: asym.gemm(Ad, Bd, C, mapping=m, stream=stream)) for m in MAPPINGS}
+        settle(list(fns.values()), 0.3)
+        ms = interleaved(fns, rounds, stream)
+        out[p.name] = {"M": p.M, "N": p.N, "K": p.K,
+                       **{m: round(p.flops / (ms[m] * 1e-3) / 1e12, 2) for m in MAPPINGS}}
+    return out
+
+
+def prefill_decode(topo, dev, iters: int, halves):
+    """Prefill GEMM 8192x4096x4096 on 192 CUs co-running with decode GEMM
+    32x14336x4096 on the other 64, on XCD-aligned sets (6 XCDs / 2 XCDs, the
+    decode pair taken from one affinity group) and on CU-striped sets (24 / 8
+    CUs of every XCD); aware mapping."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    (pa, pb), (da, db) = workloads.make_pd_inputs()
+    pa, pb, da, db = pa.to(dev), pb.to(dev), da.to(dev), db.to(dev)
+    cp = torch.empty((pa.shape[0], pb.shape[0]), dtype=torch.bfloat16, device=dev)
+    cd = torch.empty((da.shape[0], db.shape[0]), dtype=torch.bfloat16, device=dev)
+    prefill = topo.cuset(192, asym.CUSET_STRIPED)
+    decode = [b for b in range(256) if b not in set(prefill)]
+    grp = [x for x in range(8) if (halves[1] >> x) & 1]
+    dec_x = (1 << grp[-1]) | (1 << grp[-2])
+    pre_x = 0xFF & ~dec_x
+    runs = {"xcd_aligned": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", xcd_mask=pre_x),
+                                               asym.gemm_task(da, db, cd, 3 * iters, "aware", xcd_mask=dec_x)], topo),
+            "cu_striped": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=prefill),
+                                              asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=decode)], topo)}
+    out = {}
+    for _ in range(2):  # first round settles the clock; the second is kept
+        for k, fn in runs.items():
+            r = fn()
+            out[k] = {"prefill_ms": round(r[0]["ms_per_iter"], 4), "prefill_tflops": round(r[0]["tflops"], 2),
+                      "decode_ms": round(r[1]["ms_per_iter"], 4), "decode_tflops": round(r[1]["tflops"], 2)}
+    return out
+
+
+def spread_study(topo, dev, n_masks: int, iters: int, halves):
+    """GEMM 4096^3 (uniform[-1,1], seed 4) on 128-CU sets: n_masks seeded random
+    choices of 128 mask bits (what a topology-oblivious allocator hands out) and
+    the two whole-XCD halves (the measured affinity groups, through the XCD
+    filter).  A second
+    tenant, the same GEMM, runs on the complementary 128 CUs for the whole
+    measurement.  Per-set TFLOP/s of the measured GEMM for each mapping, and the
+    max/min spread over the random sets."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -100,26 +220,32 @@ def spread_study(topo, dev, n_masks: int, iters: int):
     A, B = workloads.make_inputs(workloads.COLOC)
     Ad, Bd = A.to(dev), B.to(dev)
     C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
-    src = workloads.copy_source(workloads.COPY_BYTES // 2).to(dev)
-    dst = torch.empty_like(src)
-    out = {"random": {"aware": [], "oblivious_grouped": []}, "aligned": {"aware": []}}
+    C2 = torch.empty_like(C)
     masks = workloads.random_mask_bits(workloads.COLOC.seed, n_masks, 128)
-    for m in masks:
+    per = {m: [] for m in MAPPINGS}
+    counts = []
+    for i, m in enumerate(masks):
         comp = [b for b in range(256) if b not in set(m)]
-        for mapping in ("aware", "oblivious_grouped"):
+        counts.append(topo.cuset_counts(m))
+        for mapping in MAPPINGS:
             r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m),
-                            asym.copy_task(dst, src, 0, mask=comp)], topo)
-            out["random"][mapping].append(r[0]["tflops"])
-    for xm in (0x0F, 0xF0):
+                            asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=comp)], topo)
+            if i == 0 and not per[mapping]:
+                # the first set is run twice: its first run settles the clock
+                r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m),
+                                asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=comp)], topo)
+            per[mapping].append(r[0]["tflops"])
+    aligned = []
+    for xm in halves:
         r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", xcd_mask=xm),
-                        asym.copy_task(dst, src, 0, xcd_mask=0xFF & ~xm)], topo)
-        out["aligned"]["aware"].append(r[0]["tflops"])
-    summ = {}
-    for kind, d in out.items():
-        for mapping, v in d.items():
-            if v:
-                summ[f"{kind}_{mapping}"] = {"min": min(v), "max": max(v), "spread": max(v) / min(v),
-                                             "median": sorted(v)[len(v) // 2]}
+                        asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", xcd_mask=0xFF & ~xm)], topo)
+        aligned.append(round(r[0]["tflops"], 2))
+    summ = {"n_random_sets": n_masks, "iters": iters, "aligned_aware_tflops": aligned,
+            "random_set_min_max_cus_per_xcd": [min(min(c) for c in counts), max(max(c) for c in counts)]}
+    for mapping, v in per.items():
+        summ[f"random_{mapping}"] = {"min": round(min(v), 2), "max": round(max(v), 2),
+                                     "spread": round(max(v) / min(v), 4),
+                                     "median": round(sorted(v)[len(v) // 2], 2)}
     return summ
 
 
@@ -128,21 +254,29 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--settle", type=float, default=2.0,
+                    help="seconds of untimed launches before timing (clock and power settle)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-rows", type=int, default=8192,
                     help="rows of A in the CPU oracle sample (8192 = the whole problem)")
-    ap.add_argument("--probe", choices=("maskmap", "identity"), default="maskmap",
-                    help="topology probe run first; profiling runs use 'identity' (the profiler's "
+    ap.add_argument("--probe", choices=("full", "maskmap", "identity"), default="full",
+                    help="topology probe run first: full = identity, mask map and the per-XCD "
+                         "latency / affinity probe; profiling runs use 'identity' (the profiler's "
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--spread", action="store_true", help="also run the CU-mask spread study")
+    ap.add_argument("--studies", default="compare,llm,pd,spread",
+                    help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
+                         "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets); "
+                         "'none' for the headline only")
     ap.add_argument("--spread-masks", type=int, default=32)
-    ap.add_argument("--mapping-only", default=None, help="time only this mapping (profiling runs)")
+    ap.add_argument("--mapping-only", default=None,
+                    help="time only this mapping, no studies (profiling runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the GEMM shards by output columns with no exchange, see the design notes", file=sys.stderr)
+              "the GEMM would shard by output columns with no exchange, see the design notes",
+              file=sys.stderr)
         return 2
 
     import torch
@@ -164,73 +298,80 @@ def main() -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_each_way": src.numel() * 2, "launches": 10}))
         return 0
+    studies = set() if args.mapping_only or args.studies == "none" else set(args.studies.split(","))
+    if args.probe == "identity":
+        studies -= {"pd", "spread"}  # CU-masked sets need the mask map
     p = workloads.SQUARE_8192
     A, B = workloads.make_inputs(p)
     Ad, Bd = A.to(dev), B.to(dev)
     C = torch.empty((p.M, p.N), dtype=torch.bfloat16, device=dev)
     t0 = time.perf_counter()
-    flags = asym.PROBE_IDENTITY | (asym.PROBE_MASKMAP if args.probe == "maskmap" else 0)
+    flags = asym.PROBE_IDENTITY
+    if args.probe in ("full", "maskmap"):
+        flags |= asym.PROBE_MASKMAP
+    if args.probe == "full":
+        flags |= asym.PROBE_LATENCY
     topo = asym.probe_topology(0, flags)
     probe_s = time.perf_counter() - t0
     info = topo.info()
+    halves = affinity_halves(topo, info["n_xcds"])
     stream = torch.cuda.current_stream()
 
-    results = {}
-    mappings = [args.mapping_only] if args.mapping_only else ["aware", "oblivious_grouped", "oblivious_rowmajor"]
-    for mapping in mappings:
-        fn = lambda m=mapping: asym.gemm(Ad, Bd, C, mapping=m, topo=topo, stream=stream)
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        total_ms, per_launch_ms = time_launches(fn, args.steps, stream)
-        results[mapping] = {"ms_per_step": total_ms / args.steps, "per_launch_ms": per_launch_ms,
-                            "tflops": p.flops / (total_ms / args.steps * 1e-3) / 1e12}
+    head_mapping = args.mapping_only or "aware"
+    fns = {m: (lambda m=m: asym.gemm(Ad, Bd, C, mapping=m, topo=topo, stream=stream)) for m in MAPPINGS}
+    head = fns[head_mapping]
+    for _ in range(args.warmup):
+        head()
+    settle([head], args.settle)
+    total_ms, per_launch_ms = time_launches(head, args.steps, stream)
+    ms_per_step = total_ms / args.steps
+    tflops = p.flops / (ms_per_step * 1e-3) / 1e12
+    achieved = p.flops / (per_launch_ms * 1e-3) / 1e12
 
-    # context: the vendor library on the same operands (not the product path)
-    ctx = None
-    if not args.mapping_only:
-        Bt = Bd.t().contiguous()
-        mm = lambda: torch.mm(Ad, Bt)
-        for _ in range(3):
-            mm()
-        tot, per = time_launches(mm, 10, stream)
-        ctx = {"torch_matmul_tflops": p.flops / (tot / 10 * 1e-3) / 1e12}
-
-    head = results[mappings[0]]
-    achieved = p.flops / (head["per_launch_ms"] * 1e-3) / 1e12
     line = {
         "metric": METRIC,
-        "value": round(head["tflops"], 2),
+        "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(head["ms_per_step"], 5),
+        "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": "square bf16 GEMM M=N=K=8192, uniform[-1,1] seed 1, B [N,K], "
-                               "full GPU, XCD-aware persistent mapping, topology probe first",
-                   "M": p.M, "N": p.N, "K": p.K, "mapping": mappings[0], "tile": "256x256x64"},
-        "pct_peak": round(100.0 * head["tflops"] / PEAK_BF16_TFLOPS, 2),
+                               f"full GPU, {head_mapping} persistent mapping, topology probe first",
+                   "M": p.M, "N": p.N, "K": p.K, "mapping": head_mapping, "tile": "256x256, k-step 32"},
+        "pct_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic()},
-        "mappings": {k: {kk: round(vv, 5) for kk, vv in v.items()} for k, v in results.items()},
         "topology": {"cus_per_xcd": info["cus_per_xcd"], "probe_s": round(probe_s, 3),
-                     "round_robin_dispatch": topo.dispatch_rr_fraction()},
+                     "round_robin_dispatch": topo.dispatch_rr_fraction(),
+                     "affinity": affinity_summary(topo) if args.probe == "full" else None},
     }
-    if "oblivious_grouped" in results and "aware" in results:
-        line["aware_speedup_vs_oblivious_grouped"] = round(
-            results["oblivious_grouped"]["ms_per_step"] / results["aware"]["ms_per_step"], 4)
-        line["aware_speedup_vs_oblivious_rowmajor"] = round(
-            results["oblivious_rowmajor"]["ms_per_step"] / results["aware"]["ms_per_step"], 4)
-    if ctx:
-        line["context"] = {k: round(v, 2) for k, v in ctx.items()}
-    if args.spread:
-        line["cu_mask_spread"] = spread_study(topo, dev, args.spread_masks, 20)
+    if "compare" in studies:
+        ms = interleaved(fns, args.steps, stream)
+        line["mappings_interleaved"] = {m: {"per_launch_ms": round(ms[m], 5),
+                                            "tflops": round(p.flops / (ms[m] * 1e-3) / 1e12, 2)}
+                                        for m in MAPPINGS}
+        line["aware_speedup_vs_oblivious_grouped"] = round(ms["oblivious_grouped"] / ms["aware"], 4)
+        line["aware_speedup_vs_oblivious_rowmajor"] = round(ms["oblivious_rowmajor"] / ms["aware"], 4)
+        # context: the vendor library on the same operands (not the product path)
+        Bt = Bd.t().contiguous()
+        mm = lambda: torch.mm(Ad, Bt)
+        settle([mm], 0.3)
+        tot, per = time_launches(mm, 10, stream)
+        line["context"] = {"torch_matmul_tflops": round(p.flops / (tot / 10 * 1e-3) / 1e12, 2)}
+        del Bt
+    if "llm" in studies:
+        line["llm_shapes_tflops"] = llm_shapes(dev, stream, 20)
+    if "pd" in studies:
+        line["prefill_decode"] = prefill_decode(topo, dev, 10, halves)
+    if "spread" in studies:
+        line["cu_set_spread"] = spread_study(topo, dev, args.spread_masks, 20, halves)
     line["cpu_baseline"] = None if args.no_cpu else cpu_baseline(A, B, args.cpu_rows)
     if line["cpu_baseline"]:
         line["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)

@@ -29,7 +29,7 @@
  *   buffers are owned by the caller; the library never frees them.
  *   Devices: one GPU at a time; `device` is a HIP device ordinal.
  *   Asynchrony: asym_gemm_bf16 and asym_copy_bf16 enqueue work on the given
- *   stream and return; probes, asym_corun and asym_copy_bandwidth synchronise.
+ *   stream and return; probes and asym_corun synchronise.
  */
 #ifndef ASYM_H
 #define ASYM_H
@@ -92,7 +92,7 @@ typedef enum asym_cuset_policy {
   ASYM_CUSET_RANDOM = 3            /* seeded uniform choice among free CUs */
 } asym_cuset_policy;
 
-/* a1: device and partition-mode discovery. */
+/* Device and partition-mode discovery. */
 typedef struct asym_device_info {
   int n_cus;          /* hipDeviceAttributeMultiprocessorCount */
   int n_xccs;         /* hipDeviceAttributeNumberOfXccs */
@@ -107,33 +107,73 @@ typedef struct asym_device_info {
 
 typedef struct asym_topology asym_topology; /* opaque, library-owned */
 
-/* Per-XCD latency tiers in shader-clock cycles (a4; Section 6.1 access latency
- * distribution, Appendix C kernels, Appendix G per-XCD probing).  Arrays are
- * indexed by XCD; values < 0 mean "not measured". */
+/* Per-XCD memory latency and affinity (Section 6.1, access latency
+ * distribution; Appendix C, the latency kernels; Appendix G, XCD-level probing
+ * and XCD grouping on an AMD part).  One lane on one XCD times dependent
+ * loads of sampled 128-byte lines, one at a time, with the shader clock
+ * (s_memtime).  Three regimes per XCD x:
+ *   L2:   the lines were just loaded by x (in x's L2; the sample is far larger
+ *         than the per-CU vector cache, so that cache misses);
+ *   MALL: all caches flushed, then the lines loaded by another XCD, so they sit
+ *         in the memory-side cache but not in x's L2;
+ *   HBM:  all caches flushed before every pass.
+ * A flush writes a buffer four times the memory-side cache through every XCD.
+ * Before each timed load the lane touches another line of the same 2 MiB page,
+ * so a translation miss does not enter the timed window.  Every figure is the
+ * minimum over `passes` passes per (XCD, address). */
+typedef struct asym_latency_params {
+  size_t alloc_bytes;     /* sampled allocation; 0 = 32 GiB (less if memory is short);
+                             rounded down to a multiple of 2 MiB, at least 64 MiB */
+  int n_samples;          /* addresses, uniform 128-byte-aligned lines (<= 1<<22) */
+  int passes;             /* 1..64 */
+  int l2_samples;         /* the first l2_samples addresses are timed in the L2
+                             regime (<= n_samples, <= 8192) */
+  uint64_t seed;          /* address sample (splitmix64) */
+  double group_threshold; /* XCDs whose HBM latency vectors correlate above this
+                             (Pearson) are joined into one affinity group */
+  double tie_cycles;      /* an address whose two lowest group means differ by
+                             less is left unclassified */
+} asym_latency_params;
+
+/* Fill *p with the defaults: 32 GiB, 16384 samples, 8 passes, 4096 L2
+ * samples, seed 0, threshold 0.5, tie 20 cycles. */
+void asym_latency_params_default(asym_latency_params* p);
+
+/* Results of the latency probe.  Latencies are shader-clock cycles including the timer's
+ * own overhead (timer_overhead, reported separately); < 0 = not measured. */
 typedef struct asym_latency_summary {
   int n_xcds;
-  int n_samples;                   /* addresses sampled per regime */
-  double l2_hit[ASYM_MAX_XCDS];    /* mean latency, line warm in the XCD's L2 */
-  double mall_hit[ASYM_MAX_XCDS];  /* L2 bypassed, line in the memory-side cache */
-  double hbm[ASYM_MAX_XCDS];       /* L2 bypassed, memory-side cache flushed */
-  int group_of_xcd[ASYM_MAX_XCDS]; /* affinity group id of each XCD */
+  int n_samples;                   /* addresses per regime (L2: l2_samples) */
+  int passes;
+  int l2_samples;
+  double timer_overhead;           /* cycles of an empty timed window (min) */
+  double clock_mhz;                /* shader-clock ticks per microsecond seen by the probe */
+  double l2_hit[ASYM_MAX_XCDS];    /* mean latency per XCD, L2 regime */
+  double mall_hit[ASYM_MAX_XCDS];  /* mean latency per XCD, memory-side-cache regime */
+  double hbm[ASYM_MAX_XCDS];       /* mean latency per XCD, HBM regime */
+  int group_of_xcd[ASYM_MAX_XCDS]; /* affinity group of each XCD (0 .. n_groups-1,
+                                      numbered by lowest member XCD) */
   int n_groups;
-  double home_share[ASYM_MAX_XCDS];/* fraction of addresses homed on each group */
+  double home_share[ASYM_MAX_XCDS];/* fraction of addresses whose home is group g */
+  double unclassified_share;       /* fraction left unclassified (tie) */
+  double corr[ASYM_MAX_XCDS][ASYM_MAX_XCDS];        /* Pearson, HBM regime */
+  double hbm_by_home[ASYM_MAX_XCDS][ASYM_MAX_XCDS]; /* [x][g]: mean HBM latency from
+                                      XCD x to addresses homed in group g (-1: none) */
 } asym_latency_summary;
 
-/* ---- a1: device discovery ---------------------------------------------- */
+/* ---- device discovery -------------------------------------------------- */
 /* Fill *out from the HIP runtime.  Errors: ASYM_EINVAL (null out),
  * ASYM_EHIP. */
 int asym_device_query(int device, asym_device_info* out);
 
-/* ---- a2-a4: topology probe (Section 5.1, Section 6.1, Appendix G) ------- */
+/* ---- topology probe (Section 5.1, Section 6.1, Appendix G) -------------- */
 /* Probe `device` and return a new topology map in *out.
  * IDENTITY launches an oversubscribed kernel whose workgroups record
  * XCC_ID and HW_ID; the distinct (xcc, se, sh, cu) tuples, sorted, are the
  * CU records with dense indices 0..n-1.  MASKMAP launches the same kernel once
  * per mask bit on a stream whose CU mask has every bit but that one, and maps
- * the bit to the one CU that never appears.  LATENCY runs a single-lane
- * pointer chase from each XCD (see asym_latency_summary).
+ * the bit to the one CU that never appears.  LATENCY runs asym_latency_probe
+ * with default parameters and keeps its summary (affinity groups).
  * The map is checked against its exact invariants (every CU once, per-XCD
  * counts summing to the device CU count, mask map a bijection); a violation
  * returns ASYM_EINVARIANT and no map.  Synchronous.
@@ -167,7 +207,7 @@ int asym_topology_cu(const asym_topology* topo, int cu_index, int* xcc,
  * n_xccs (1.0 = round-robin dispatch).  Written by the IDENTITY probe. */
 int asym_topology_dispatch(const asym_topology* topo, double* rr_fraction);
 
-/* a4 results; ASYM_EUNSUPPORTED if the map was probed without LATENCY. */
+/* Latency-probe results; ASYM_EUNSUPPORTED if the map was probed without LATENCY. */
 int asym_topology_latency(const asym_topology* topo, asym_latency_summary* out);
 
 /* JSON text of the map into buf (len bytes incl. NUL); *needed receives the
@@ -175,7 +215,34 @@ int asym_topology_latency(const asym_topology* topo, asym_latency_summary* out);
 int asym_topology_json(const asym_topology* topo, char* buf, size_t len,
                        size_t* needed);
 
-/* ---- CU sets and masked streams (a3, a7) -------------------------------- */
+/* ---- latency / affinity probe (Section 6.1, Appendices C and G) -------- */
+/* Run the probe on `device` with params p (NULL = defaults).  lat (nullable)
+ * receives the per-address minima, uint32 [3][n_xcds][n_samples] in regime
+ * order L2, MALL, HBM (L2 rows hold l2_samples values, the rest 0).  The
+ * summary is asym_latency_analyze of the HBM regime plus the per-regime
+ * means.  Allocates alloc_bytes plus a 1 GiB flush buffer for the duration
+ * of the call.  Synchronous; takes seconds at the defaults.
+ * Errors: ASYM_EINVAL, ASYM_ENOMEM, ASYM_EHIP, ASYM_ETIMEOUT (no workgroup
+ * reached an XCD). */
+int asym_latency_probe(int device, const asym_latency_params* p, uint32_t* lat,
+                       asym_latency_summary* out);
+
+/* Affinity analysis of HBM-regime latencies (host only, no GPU):
+ * hbm_lat is uint32 [n_xcds][n_samples].  corr[x][y] is the Pearson
+ * correlation of rows x and y (0 when either row is constant; 1 on the
+ * diagonal).  XCDs are joined into a group when their correlation exceeds
+ * group_threshold, transitively (connected components).  An address's home is
+ * the group with the lowest mean latency over its XCDs (ties to the lower
+ * group); it is unclassified when the second-lowest group mean is less than
+ * tie_cycles above it (never with a single group).  Fills n_xcds, n_samples,
+ * hbm, group_of_xcd, n_groups, home_share, unclassified_share, corr and
+ * hbm_by_home of *out; other fields are set to -1.
+ * Errors: ASYM_EINVAL. */
+int asym_latency_analyze(const uint32_t* hbm_lat, int n_xcds, int n_samples,
+                         double group_threshold, double tie_cycles,
+                         asym_latency_summary* out);
+
+/* ---- CU sets and masked streams ----------------------------------------- */
 /* Choose n_cus compute units by `policy` among the CUs not in `exclude`
  * (nullable), and write their CU-mask bits to mask_out[ASYM_MASK_WORDS].
  * Needs a topology probed with MASKMAP.  XCD-aligned policies need n_cus to be
@@ -196,7 +263,7 @@ int asym_stream_create(const asym_topology* topo, const uint32_t* mask,
                        void** out);
 int asym_stream_destroy(void* stream);
 
-/* ---- a5: tile schedule (host only) -------------------------------------- */
+/* ---- tile schedule (host only) ------------------------------------------ */
 /* Tile order for a tiles_m x tiles_n grid under `mapping`, for n_xcds XCDs
  * with slots[x] persistent workgroups each (0 = XCD excluded).
  * order[tiles_m*tiles_n] receives tile ids (row*tiles_n + col); for AWARE the
@@ -210,7 +277,7 @@ int asym_schedule_build(int tiles_m, int tiles_n, int n_xcds,
                         const int* slots, int mapping, int band, int* order,
                         int* off, int* quota);
 
-/* ---- a6: persistent bf16 GEMM (Section 7.1) ----------------------------- */
+/* ---- persistent bf16 GEMM (Section 7.1) --------------------------------- */
 /* C = A . B, bf16 inputs, fp32 accumulation, bf16 round-to-nearest-even
  * output.  A: [M][lda] row-major.  B: ASYM_B_NK, [N][ldb] row-major (the
  * logical B is its transpose).  C: [M][ldc] row-major.  Requires M, N, K >= 1,
@@ -229,7 +296,7 @@ int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K,
                    int b_layout, void* C, int ldc, int mapping,
                    uint32_t xcd_mask, void* stream);
 
-/* ---- a7: streaming copy and co-run (Sections 7.2, 7.3) ------------------ */
+/* ---- streaming copy and co-run (Sections 7.2, 7.3) ---------------------- */
 /* dst[i] = src[i] for n_bytes bytes (16-byte aligned, n_bytes a multiple of
  * 16), `passes` times over the buffer, with 16-byte accesses from every lane.
  * If stop_flag (device int, nullable) becomes nonzero the kernel ends after

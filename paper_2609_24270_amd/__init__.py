@@ -35,6 +35,7 @@ EXPORTS = (
     "asym_device_query", "asym_probe_topology", "asym_topology_from_records",
     "asym_topology_free", "asym_topology_info", "asym_topology_cu",
     "asym_topology_dispatch", "asym_topology_latency", "asym_topology_json",
+    "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_gemm_bf16",
     "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
@@ -55,14 +56,38 @@ class DeviceInfo(ctypes.Structure):
                 ("arch", ctypes.c_char * 64)]
 
 
+class LatencyParams(ctypes.Structure):
+    _fields_ = [("alloc_bytes", ctypes.c_size_t), ("n_samples", ctypes.c_int),
+                ("passes", ctypes.c_int), ("l2_samples", ctypes.c_int),
+                ("seed", ctypes.c_uint64), ("group_threshold", ctypes.c_double),
+                ("tie_cycles", ctypes.c_double)]
+
+
 class LatencySummary(ctypes.Structure):
     _fields_ = [("n_xcds", ctypes.c_int), ("n_samples", ctypes.c_int),
+                ("passes", ctypes.c_int), ("l2_samples", ctypes.c_int),
+                ("timer_overhead", ctypes.c_double), ("clock_mhz", ctypes.c_double),
                 ("l2_hit", ctypes.c_double * MAX_XCDS),
                 ("mall_hit", ctypes.c_double * MAX_XCDS),
                 ("hbm", ctypes.c_double * MAX_XCDS),
                 ("group_of_xcd", ctypes.c_int * MAX_XCDS),
                 ("n_groups", ctypes.c_int),
-                ("home_share", ctypes.c_double * MAX_XCDS)]
+                ("home_share", ctypes.c_double * MAX_XCDS),
+                ("unclassified_share", ctypes.c_double),
+                ("corr", (ctypes.c_double * MAX_XCDS) * MAX_XCDS),
+                ("hbm_by_home", (ctypes.c_double * MAX_XCDS) * MAX_XCDS)]
+
+    def to_dict(self) -> dict:
+        nx, ng = self.n_xcds, self.n_groups
+        return {"n_xcds": nx, "n_samples": self.n_samples, "passes": self.passes,
+                "l2_samples": self.l2_samples, "timer_overhead": self.timer_overhead,
+                "clock_mhz": self.clock_mhz, "l2_hit": list(self.l2_hit)[:nx],
+                "mall_hit": list(self.mall_hit)[:nx], "hbm": list(self.hbm)[:nx],
+                "group_of_xcd": list(self.group_of_xcd)[:nx], "n_groups": ng,
+                "home_share": list(self.home_share)[:ng],
+                "unclassified_share": self.unclassified_share,
+                "corr": [list(self.corr[x])[:nx] for x in range(nx)],
+                "hbm_by_home": [list(self.hbm_by_home[x])[:ng] for x in range(nx)]}
 
 
 class Task(ctypes.Structure):
@@ -105,6 +130,10 @@ def load_library(path: str = LIB_PATH):
         "asym_topology_cu": (i, [topo_p, i, ip, ip, ip, ip, ip]),
         "asym_topology_dispatch": (i, [topo_p, ctypes.POINTER(ctypes.c_double)]),
         "asym_topology_latency": (i, [topo_p, ctypes.POINTER(LatencySummary)]),
+        "asym_latency_params_default": (None, [ctypes.POINTER(LatencyParams)]),
+        "asym_latency_probe": (i, [i, ctypes.POINTER(LatencyParams), u32p, ctypes.POINTER(LatencySummary)]),
+        "asym_latency_analyze": (i, [u32p, i, i, ctypes.c_double, ctypes.c_double,
+                                     ctypes.POINTER(LatencySummary)]),
         "asym_topology_json": (i, [topo_p, cp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_cuset_make": (i, [topo_p, i, i, ctypes.c_uint64, u32p, u32p]),
         "asym_cuset_counts": (i, [topo_p, u32p, ip]),
@@ -152,7 +181,7 @@ def mask_bits(words) -> list:
     return [w * 32 + b for w in range(MASK_WORDS) for b in range(32) if (words[w] >> b) & 1]
 
 
-# ---- a1 ---------------------------------------------------------------------
+# ---- device -----------------------------------------------------------------
 
 def device_query(device: int = 0) -> dict:
     info = DeviceInfo()
@@ -162,7 +191,7 @@ def device_query(device: int = 0) -> dict:
     return d
 
 
-# ---- a2-a4 topology -----------------------------------------------------------
+# ---- topology -----------------------------------------------------------
 
 class Topology:
     """A probed (or record-built) topology map; owns the library object."""
@@ -204,11 +233,7 @@ class Topology:
     def latency(self) -> dict:
         s = LatencySummary()
         _check(load_library().asym_topology_latency(self._h, ctypes.byref(s)))
-        nx = s.n_xcds
-        return {"n_samples": s.n_samples, "l2_hit": list(s.l2_hit)[:nx],
-                "mall_hit": list(s.mall_hit)[:nx], "hbm": list(s.hbm)[:nx],
-                "group_of_xcd": list(s.group_of_xcd)[:nx], "n_groups": s.n_groups,
-                "home_share": list(s.home_share)[:s.n_groups]}
+        return s.to_dict()
 
     def json(self) -> dict:
         lib = load_library()
@@ -235,6 +260,48 @@ def probe_topology(device: int = 0, flags: int = PROBE_IDENTITY) -> Topology:
     return Topology(h.value)
 
 
+def latency_params(**kw) -> LatencyParams:
+    """Library defaults, with any field overridden by keyword."""
+    p = LatencyParams()
+    load_library().asym_latency_params_default(ctypes.byref(p))
+    for k, v in kw.items():
+        if not hasattr(p, k):
+            raise TypeError(f"unknown latency parameter {k}")
+        setattr(p, k, v)
+    return p
+
+
+def latency_probe(device: int = 0, want_raw: bool = False, **kw):
+    """Run the per-XCD latency / affinity probe; returns the summary dict, and
+    with want_raw the per-address minima as uint32 [3, n_xcds, n_samples]
+    (regimes L2, memory-side cache, HBM)."""
+    import numpy as np
+    p = latency_params(**kw)
+    s = LatencySummary()
+    raw = None
+    ptr = None
+    if want_raw:
+        n_x = device_query(device)["n_xccs"]
+        raw = np.zeros((3, n_x, p.n_samples), dtype=np.uint32)
+        ptr = raw.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+    _check(load_library().asym_latency_probe(device, ctypes.byref(p), ptr, ctypes.byref(s)))
+    d = s.to_dict()
+    return (d, raw) if want_raw else d
+
+
+def latency_analyze(hbm_lat, group_threshold: float = 0.5, tie_cycles: float = 20.0) -> dict:
+    """Affinity analysis of uint32 [n_xcds, n_samples] HBM latencies (host only)."""
+    import numpy as np
+    L = np.ascontiguousarray(hbm_lat, dtype=np.uint32)
+    if L.ndim != 2:
+        raise ValueError("latencies must be [n_xcds, n_samples]")
+    s = LatencySummary()
+    _check(load_library().asym_latency_analyze(L.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+                                               L.shape[0], L.shape[1], group_threshold, tie_cycles,
+                                               ctypes.byref(s)))
+    return s.to_dict()
+
+
 def topology_from_records(records, n_cus: int, n_xccs: int, mask_bit_record=None) -> Topology:
     import numpy as np
     rec = np.ascontiguousarray(records, dtype=np.int32).reshape(-1, 4)
@@ -249,7 +316,7 @@ def topology_from_records(records, n_cus: int, n_xccs: int, mask_bit_record=None
     return Topology(h.value)
 
 
-# ---- a5 schedule ----------------------------------------------------------------
+# ---- schedule ----------------------------------------------------------------
 
 def schedule_build(tiles_m: int, tiles_n: int, slots: Sequence[int], mapping: int, band: int = 0):
     n_x = len(slots)
@@ -284,7 +351,7 @@ def _stream_ptr(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-# ---- a6 GEMM -----------------------------------------------------------------------
+# ---- GEMM -----------------------------------------------------------------------
 
 def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mask: int = 0,
          stream=None):
@@ -316,7 +383,7 @@ def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mas
     return C
 
 
-# ---- a7 copy and co-run --------------------------------------------------------------
+# ---- copy and co-run --------------------------------------------------------------
 
 def copy(dst, src, passes: int = 1, stop_flag=None, xcd_mask: int = 0, stream=None):
     n = src.numel() * src.element_size()

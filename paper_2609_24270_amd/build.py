@@ -19,7 +19,7 @@ OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libasym.so")
 ARCH = "gfx950"
 
-SOURCES = ["capi.cpp", "topology.cpp", "schedule.cpp", "corun.cpp",
+SOURCES = ["capi.cpp", "topology.cpp", "schedule.cpp", "corun.cpp", "affinity.cpp",
            "gemm.hip", "probe.hip", "latency.hip", "copy.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

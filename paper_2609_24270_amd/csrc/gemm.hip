@@ -271,63 +271,44 @@ struct RingCtx {
   int lda, ldb, K, lchunk;
 };
 
-// Lane 0's fetch of the workgroup's next tile, issued from inside the k-loop
-// at stage KT - 4, so that its latency, including the contention of an XCD's
-// workgroups on one counter, overlaps the last stages' MFMA work: vector
-// memory operations complete in order, and a claim issued before a tile's
-// first loads would hold up the waits on them.  Issuing it late keeps the
-// fetched values live for only a few stages (an early fetch's result, live
-// across the whole k-loop, ends up spilled, and the spill waits on memory).
-constexpr int CLAIM_FROM_END = 4;
+// The workgroup's next tile.  Lane 0 issues the fetch right after a tile's
+// k-loop has drained (issue_next): the aware claim on its XCD's counter, or
+// the order entry at position i + grid (oblivious).  Nothing waits on it until
+// the epilogue's stores are issued (take_next); by then the fetch has
+// returned.  Issuing it inside the k-loop instead would hold up the ring: the
+// result must stay live across the remaining stages, where every VGPR is
+// taken, so it is spilled, and the spill waits on memory.  Every aware claim
+// is made at the end of a tile, never ahead: a workgroup that took a second
+// tile before the others had their first would leave some of them idle and
+// run two tiles in a row (one tile per workgroup is the common case for
+// decoder shapes).
 struct NextTile {
   const int* order;
   int* counter;      // aware: the own XCD's tile counter; null for oblivious
   int own_off, own_q;
-  int pend;          // aware: own-region index claimed one tile ahead (observed)
-  int claimed;       // aware: the claim issued during this tile (in flight)
   int i_next;        // oblivious: next position of the shared order
   int n_tiles;
-  int raw;           // order entry loaded during this tile (in flight)
-  int result;        // finish_next's answer, kept (scalar) across the epilogue
-  bool fetched;
-  bool finished;
+  int v;             // lane 0: the claim (aware) or order entry (oblivious) in flight
 };
 
-// Issue the fetch (lane 0).  Only loads are issued here, and their results
-// are first touched at the end of the tile (finish_next), so nothing in the
-// k-loop waits on them.  The order entry read is always in bounds; whether it
-// is the next tile is decided at the end.
-__device__ __forceinline__ void fetch_next(NextTile& n) {
-  if (n.fetched) return;
-  n.fetched = true;
+__device__ __forceinline__ void issue_next(NextTile& n) {
   if (threadIdx.x != 0) return;
-  if (n.counter) {
-    const int i = n.own_off + (n.pend < n.own_q ? n.pend : 0);
-    n.raw = n.order[i];
-    if (n.pend < n.own_q) n.claimed = atomicAdd(n.counter, 1);
-  } else {
-    n.raw = n.order[n.i_next < n.n_tiles ? n.i_next : 0];
-  }
+  if (n.counter)
+    n.v = atomicAdd(n.counter, 1);
+  else
+    n.v = n.order[n.i_next < n.n_tiles ? n.i_next : 0];
 }
 
-// End of a tile (lane 0): the next tile (-1 none, -2 own region exhausted),
-// and the claim issued during the tile becomes `pend`.  The readfirstlanes are
-// real instructions on the loaded values, so the compiler's waits land here.
-// Called right after the tile's k-loop has drained its loads, before the
-// epilogue: the epilogue needs every VGPR for the accumulators, so nothing of
-// the fetch may stay live across it except the scalar `result`.
-__device__ __forceinline__ void finish_next(NextTile& n) {
-  if (n.finished) return;
-  n.finished = true;
-  if (threadIdx.x != 0) return;
-  const int raw = __builtin_amdgcn_readfirstlane(n.raw);
+__device__ __forceinline__ int claim_aware(const Params& p, int xcc);
+
+// Lane 0: the next tile, or -1.  Aware: the claimed index is looked up in the
+// XCD's list; once the own region is exhausted, other regions are tried.
+__device__ __forceinline__ int take_next(const Params& p, const NextTile& n, int xcc) {
   if (n.counter) {
-    const bool mine = n.pend < n.own_q;
-    if (mine) n.pend = __builtin_amdgcn_readfirstlane(n.claimed);
-    n.result = mine ? raw : -2;
-  } else {
-    n.result = n.i_next < n.n_tiles ? raw : -1;
+    const int idx = n.v;
+    return idx < n.own_q ? n.order[n.own_off + idx] : claim_aware(p, xcc);
   }
+  return n.i_next < n.n_tiles ? n.v : -1;
 }
 
 // g-th of the 8 loads of stage t into slot t % SLOTS: g < 4 are A's, g >= 4
@@ -367,12 +348,11 @@ __device__ __forceinline__ void ring_group(const RingCtx& c, int t, f32x4 (&acc)
 // the program order: no MFMA waits on a read issued in the same stage.
 __device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)[8][8],
                                            const bf16x8 (&ac)[8], bf16x8 (&an)[8], bf16x8 (&b)[8],
-                                           uint32_t ra0, uint32_t rb0, NextTile& nt, int claim_t) {
+                                           uint32_t ra0, uint32_t rb0) {
   asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
   lds_barrier();
   const uint32_t s = (uint32_t)((t + 1) & (SLOTS - 1)) * SLOT_BYTES;
   ring_group<0>(c, t, acc, ac, an, b, ra0 + s, rb0 + s);
-  if (t == claim_t) fetch_next(nt);
 }
 
 __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, unsigned char* lds,
@@ -429,16 +409,14 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   lds_read_frag<2048>(bf[2], rb0); lds_read_frag<3072>(bf[3], rb0);
   lds_read_frag<4096>(bf[4], rb0); lds_read_frag<5120>(bf[5], rb0);
   lds_read_frag<6144>(bf[6], rb0); lds_read_frag<7168>(bf[7], rb0);
-  const int claim_t = KT > CLAIM_FROM_END ? KT - CLAIM_FROM_END : 0;
   for (int t = 0; t < KT; t += 2) {
-    ring_stage(c, t, acc, a0, a1, bf, ra0, rb0, nt, claim_t);
-    if (t + 1 < KT) ring_stage(c, t + 1, acc, a1, a0, bf, ra0, rb0, nt, claim_t);
+    ring_stage(c, t, acc, a0, a1, bf, ra0, rb0);
+    if (t + 1 < KT) ring_stage(c, t + 1, acc, a1, a0, bf, ra0, rb0);
   }
   // drain the loads still in flight (zero fills past K) before the slots
   // are reused, and make sure every wave is past its last LDS read
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  fetch_next(nt);   // for a K too short to reach the claim stage
-  finish_next(nt);
+  issue_next(nt);
   mfma_fence();
   // every wave is past its last LDS read before the slots are reused
   lds_barrier();
@@ -503,13 +481,13 @@ __device__ __forceinline__ int claim_aware(const Params& p, int xcc) {
 
 template <bool VEC>
 __device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned char* lds, NextTile& nt) {
-  if constexpr (VEC)
+  if constexpr (VEC) {
     compute_tile_ring(p, tile, lds, nt);
-  else
+  } else {
     compute_tile<false>(p, tile, reinterpret_cast<uint16_t*>(lds),
                         reinterpret_cast<uint16_t*>(lds) + 2 * BM * LDP);
-  fetch_next(nt);   // no-ops if the tile routine already did them
-  finish_next(nt);
+    issue_next(nt);
+  }
 }
 
 constexpr int LDS_BYTES = RING_BYTES > 2 * (BM + BN) * LDP * 2 ? RING_BYTES : 2 * (BM + BN) * LDP * 2;
@@ -534,10 +512,7 @@ gemm_bf16_persistent(Params p) {
   nt.counter = aware ? &p.ctr[16 + own] : nullptr;
   nt.own_off = own_off;
   nt.own_q = own_q;
-  nt.pend = 0;
-  nt.claimed = 0;
-  nt.raw = 0;
-  nt.result = -1;
+  nt.v = -1;
   nt.i_next = blockIdx.x;
   nt.n_tiles = p.n_tiles;
   if (threadIdx.x == 0) {
@@ -547,10 +522,6 @@ gemm_bf16_persistent(Params p) {
       if (xcc < p.n_xccs) r = atomicAdd(&p.ctr[xcc], 1);
       active = (xcc < p.n_xccs && r < p.slots[xcc]) ? 1 : 0;
       first = active ? claim_aware(p, xcc) : -1;
-      if (active) nt.pend = atomicAdd(nt.counter, 1);
-      // observe the claim here (a wait before the tile loop) so the first
-      // fetch inside the k-loop finds it complete and waits on nothing
-      nt.pend = __builtin_amdgcn_readfirstlane(nt.pend);
     } else {
       first = (int)blockIdx.x < p.n_tiles ? p.order[blockIdx.x] : -1;
     }
@@ -559,18 +530,9 @@ gemm_bf16_persistent(Params p) {
   __syncthreads();
   int tile = s_info[1];
   while (tile >= 0) {
-    // lane 0 fetches the following tile during this tile (fetch_next): the
-    // order entry of the index claimed one tile ago and the aware claim of the
-    // tile after that, or position i + grid of the shared order (oblivious)
     nt.i_next += gridDim.x;
-    nt.fetched = false;
-    nt.finished = false;
     run_tile<VEC>(p, tile, lds, nt);
-    if (threadIdx.x == 0) {
-      int nxt = nt.result;
-      if (nxt == -2) nxt = claim_aware(p, xcc);
-      s_info[1] = nxt;
-    }
+    if (threadIdx.x == 0) s_info[1] = take_next(p, nt, xcc);
     __syncthreads();
     tile = s_info[1];
   }

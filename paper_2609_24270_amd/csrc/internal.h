@@ -87,6 +87,11 @@ int launch_gemm(const GemmLaunch& g, hipStream_t s);
 int probe_identity_run(int device, hipStream_t s, int n_blocks,
                        std::vector<int32_t>& rec);
 int probe_latency_run(int device, Topology& t);
+int latency_probe(int device, const asym_latency_params& p, uint32_t* lat_out,
+                  asym_latency_summary& out);
+// Affinity groups and home groups from HBM latencies [n_x][n_s] (host only).
+int analyze_latency(const uint32_t* lat, int n_x, int n_s, double threshold, double tie,
+                    asym_latency_summary& out);
 
 int launch_copy(void* dst, const void* src, size_t n_bytes, int passes,
                 const int* stop_flag, uint32_t xcd_mask, int grid,

@@ -239,7 +239,11 @@ static std::string topology_json(const Topology& t) {
       }
       return a + "]";
     };
-    s += ", \"latency\": {\"n_samples\": " + std::to_string(L.n_samples);
+    s += ", \"latency\": {\"n_samples\": " + std::to_string(L.n_samples) +
+         ", \"passes\": " + std::to_string(L.passes) + ", \"l2_samples\": " + std::to_string(L.l2_samples);
+    std::snprintf(buf, sizeof buf, ", \"timer_overhead\": %.1f, \"clock_mhz\": %.1f, \"unclassified_share\": %.4f",
+                  L.timer_overhead, L.clock_mhz, L.unclassified_share);
+    s += buf;
     s += ", \"l2_hit\": " + arr(L.l2_hit) + ", \"mall_hit\": " + arr(L.mall_hit) + ", \"hbm\": " + arr(L.hbm);
     s += ", \"group_of_xcd\": [";
     for (int x = 0; x < L.n_xcds; ++x) s += (x ? ", " : "") + std::to_string(L.group_of_xcd[x]);
@@ -248,6 +252,15 @@ static std::string topology_json(const Topology& t) {
     for (int g = 0; g < L.n_groups; ++g) {
       std::snprintf(buf, sizeof buf, "%s%.4f", g ? ", " : "", L.home_share[g]);
       s += buf;
+    }
+    s += "], \"hbm_by_home\": [";
+    for (int x = 0; x < L.n_xcds; ++x) {
+      s += x ? ", [" : "[";
+      for (int g = 0; g < L.n_groups; ++g) {
+        std::snprintf(buf, sizeof buf, "%s%.2f", g ? ", " : "", L.hbm_by_home[x][g]);
+        s += buf;
+      }
+      s += "]";
     }
     s += "]}";
   }

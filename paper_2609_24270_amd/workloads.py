@@ -118,3 +118,29 @@ def copy_source(n_elems: int, seed: int = COLOC.seed + 1000) -> torch.Tensor:
     """Arbitrary bf16 bit patterns (finite) for the streaming-copy source."""
     g = torch.Generator(device="cpu").manual_seed(seed)
     return (torch.rand(n_elems, generator=g) * 2 - 1).to(torch.bfloat16)
+
+
+# Synthetic per-address latencies with a planted affinity structure, input to
+# the affinity analysis in host-only tests.  XCD x belongs to group grp[x];
+# each address gets a uniformly drawn home group h; its latency from x is
+# tier[dist[grp[x]][h]] plus a per-address offset shared by all XCDs (uniform in
+# [0, common)) plus per-(XCD, address) jitter (uniform in [0, jitter)).
+# Appendix G's MI300X picture: four XCD pairs on four I/O dies in a 2x2 grid,
+# tiers about 707 / 817 / 926 cycles for local / adjacent / opposite.
+MI300X_GROUPS = (0, 0, 1, 1, 2, 2, 3, 3)
+MI300X_DIST = ((0, 1, 1, 2), (1, 0, 2, 1), (1, 2, 0, 1), (2, 1, 1, 0))
+MI300X_TIERS = (707, 817, 926)
+
+
+def planted_latency(seed: int, n_samples: int, grp=MI300X_GROUPS, dist=MI300X_DIST,
+                    tiers=MI300X_TIERS, common: int = 40, jitter: int = 12):
+    """Returns (lat uint32 [n_xcds, n_samples], home int64 [n_samples])."""
+    import numpy as np
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    n_g = len(dist)
+    home = torch.randint(0, n_g, (n_samples,), generator=g)
+    off = torch.randint(0, max(1, common), (n_samples,), generator=g)
+    jit = torch.randint(0, max(1, jitter), (len(grp), n_samples), generator=g)
+    tier_t = torch.tensor([[tiers[dist[a][b]] for b in range(n_g)] for a in range(n_g)])
+    lat = torch.stack([tier_t[grp[x]][home] for x in range(len(grp))]) + off + jit
+    return lat.numpy().astype(np.uint32), home.numpy()
