@@ -72,8 +72,15 @@ __device__ __forceinline__ uint32_t read_xcc_id() {
 
 // Buffer resource over `bytes` bytes at `base`: loads beyond the range return
 // zero and stores beyond it are dropped, so tile edges need no branches.
+// Every argument here is the same in all lanes; reading it from the first lane
+// tells the compiler so, and the resource stays in SGPRs (a resource it takes
+// for lane-varying is re-checked lane by lane around every access).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+  const unsigned long long a = (unsigned long long)base;
+  const unsigned long long u = ((unsigned long long)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+                               (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0,
+                                           (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 constexpr uint32_t kOOB = 0x80000000u;  // an offset past any range used here
 
@@ -217,10 +224,11 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
 }
 
 // ---- vector path: direct-to-LDS four-slot ring ---------------------------------
-constexpr int KS = 32;                 // k per stage
-constexpr int SLOTS = 4;
-constexpr int SLOT_BYTES = 32768;      // A (16 KiB) then B (16 KiB)
+constexpr int KS = 64;                 // k per stage: one 128-byte line of every row
+constexpr int SLOTS = 2;
+constexpr int SLOT_BYTES = 65536;      // A (256 rows x 128 B) then B (256 rows x 128 B)
 constexpr int RING_BYTES = SLOTS * SLOT_BYTES;
+constexpr int ROW_BYTES = KS * 2;
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -229,9 +237,11 @@ __device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
   return i32x4{(int)(uint32_t)a, (int)(uint32_t)(a >> 32), (int)bytes, 0x00020000};
 }
 
-// Direct-to-LDS load of 16 tile rows (1 KiB): lane L lands at M0 + 16 L, i.e.
-// row L/4 of the 16, physical chunk L%4; `vo` already selects the logical
-// chunk that belongs there, `so` the row block and k (uniform).
+// Direct-to-LDS load of 8 tile rows x 128 bytes (1 KiB): lane L lands at
+// M0 + 16 L, i.e. row L/8 of the 8, physical chunk L%8; `vo` already selects
+// the logical chunk that belongs there, `so` the row block and k (uniform).
+// Eight lanes read one whole 128-byte line of a row: loads of half lines (a
+// 32-wide k stage) reach barely 60% of this rate through the vector cache.
 __device__ __forceinline__ void dma_1k(uint32_t lds_dst, i32x4 rs, uint32_t vo, int so) {
   const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_dst);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
@@ -267,8 +277,10 @@ __device__ __forceinline__ void lds_read_frag(bf16x8& f, uint32_t addr) {
 
 struct RingCtx {
   i32x4 rsa, rsb;
-  uint32_t voa, vob, dst_a, dst_b;
-  int lda, ldb, K, lchunk;
+  uint32_t voa[2], vob[2];  // per-lane offsets for even / odd 8-row blocks
+  uint32_t dst_a, dst_b;
+  int lda, ldb, K;
+  int lchunk[2];            // the lane's logical chunk for even / odd blocks
 };
 
 // The workgroup's next tile.  Lane 0 issues the fetch right after a tile's
@@ -299,60 +311,76 @@ __device__ __forceinline__ void issue_next(NextTile& n) {
     n.v = n.order[n.i_next < n.n_tiles ? n.i_next : 0];
 }
 
-__device__ __forceinline__ int claim_aware(const Params& p, int xcc);
+__device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane);
 
-// Lane 0: the next tile, or -1.  Aware: the claimed index is looked up in the
-// XCD's list; once the own region is exhausted, other regions are tried.
-__device__ __forceinline__ int take_next(const Params& p, const NextTile& n, int xcc) {
+// Wave 0 (all lanes): the next tile, or -1.  Aware: the index claimed by lane
+// 0 is looked up in the XCD's list; once the own region is exhausted, other
+// regions are tried.
+__device__ __forceinline__ int take_next(const Params& p, const NextTile& n, int xcc, int q_lane) {
   if (n.counter) {
-    const int idx = n.v;
-    return idx < n.own_q ? n.order[n.own_off + idx] : claim_aware(p, xcc);
+    const int idx = __builtin_amdgcn_readfirstlane(n.v);
+    if (idx < n.own_q) return __builtin_amdgcn_readfirstlane(n.order[n.own_off + idx]);
+    return steal_aware(p, xcc, q_lane);
   }
-  return n.i_next < n.n_tiles ? n.v : -1;
+  const int v = __builtin_amdgcn_readfirstlane(n.v);
+  return n.i_next < n.n_tiles ? v : -1;
 }
 
-// g-th of the 8 loads of stage t into slot t % SLOTS: g < 4 are A's, g >= 4
-// B's; each wave owns rows w*64 .. w*64+63 of both operands.  Stages at or past
-// the end of K are sent out of range and fill the slot with zeros.
-__device__ __forceinline__ void ring_load(const RingCtx& c, int t, int g) {
+// j-th of the 16 loads of stage t into slot t % SLOTS: j < 8 are A's, j >= 8
+// B's; each wave owns rows w*64 .. w*64+63 of both operands, load i covering
+// rows w*64 + 8i .. +7.  Stages at or past the end of K are sent out of range
+// and fill the slot with zeros.
+__device__ __forceinline__ void ring_load(const RingCtx& c, int t, int j) {
   const int k0 = t * KS;
   const uint32_t slot = (uint32_t)(t & (SLOTS - 1)) * SLOT_BYTES;
-  const bool in_k = k0 + c.lchunk * 8 < c.K;
-  const int i = g & 3;
-  if (g < 4)
-    dma_1k(c.dst_a + slot + i * 1024, c.rsa, in_k ? c.voa : kOOB, (16 * i * c.lda + k0) * 2);
+  const int i = j & 7, par = i & 1;
+  const bool in_k = k0 + c.lchunk[par] * 8 < c.K;
+  if (j < 8)
+    dma_1k(c.dst_a + slot + i * 1024, c.rsa, in_k ? c.voa[par] : kOOB, (8 * i * c.lda + k0) * 2);
   else
-    dma_1k(c.dst_b + slot + i * 1024, c.rsb, in_k ? c.vob : kOOB, (16 * i * c.ldb + k0) * 2);
+    dma_1k(c.dst_b + slot + i * 1024, c.rsb, in_k ? c.vob[par] : kOOB, (8 * i * c.ldb + k0) * 2);
 }
 
-// One group of a stage: refill slot t with load G of stage t+4, run stage t's
-// 8 MFMAs that use B fragment G, then read stage t+1's A fragment G into `an`
-// and its B fragment G into `b` (B fragment G has no later use in this stage,
-// so it is replaced in place; the A fragments feed every group and are double
-// buffered).  `sa`/`sb` are the LDS addresses of stage t+1's fragment 0.
-template <int G>
+// One group of a half-stage (32 of the stage's 64 k): with LOADS, issue loads
+// 2G and 2G+1 of stage t+2 first (spread over the 8 groups, the loads keep the
+// MFMAs fed better than in bursts); run the 8 MFMAs that use B
+// fragment G; then read the next half-stage's A fragment G into `an` and its B
+// fragment G into `b` (B fragment G has no later use in this half-stage, so it
+// is replaced in place; the A fragments feed every group and are double
+// buffered).  `sa`/`sb` are the LDS addresses of the next half-stage's
+// fragment 0.
+template <int G, bool LOADS>
 __device__ __forceinline__ void ring_group(const RingCtx& c, int t, f32x4 (&acc)[8][8],
                                            const bf16x8 (&ac)[8], bf16x8 (&an)[8], bf16x8 (&b)[8],
                                            uint32_t sa, uint32_t sb) {
-  ring_load(c, t + SLOTS, G);
+  if constexpr (LOADS) {
+    ring_load(c, t + SLOTS, 2 * G);
+    ring_load(c, t + SLOTS, 2 * G + 1);
+  }
 #pragma unroll
   for (int mb = 0; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
-  lds_read_frag<G * 1024>(an[G], sa);
-  lds_read_frag<G * 1024>(b[G], sb);
-  if constexpr (G + 1 < 8) ring_group<G + 1>(c, t, acc, ac, an, b, sa, sb);
+  lds_read_frag<G * 2048>(an[G], sa);
+  lds_read_frag<G * 2048>(b[G], sb);
+  if constexpr (G + 1 < 8) ring_group<G + 1, LOADS>(c, t, acc, ac, an, b, sa, sb);
 }
 
-// One stage, branch-free: wait for this wave's loads of stage t+1 (stages t+2
-// and t+3 stay in flight), publish slot t+1 to all waves, then the 8 groups.
-// Every instruction of the stage is inline asm, so the issue order is exactly
-// the program order: no MFMA waits on a read issued in the same stage.
+// Stage t in two halves, branch-free.  First half (k 0..31): its fragments
+// were read during the previous half; wait for those reads, compute, and read
+// the second half's fragments from slot t.  Second half (k 32..63): wait for
+// this wave's loads of stage t+1, publish slot t+1 to all waves (the barrier
+// also tells every wave that slot t has been read completely), refill slot t
+// with stage t+2 while computing, and read the first half of stage t+1.  Every
+// instruction is inline asm, so the issue order is the program order.
 __device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)[8][8],
-                                           const bf16x8 (&ac)[8], bf16x8 (&an)[8], bf16x8 (&b)[8],
-                                           uint32_t ra0, uint32_t rb0) {
-  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+                                           bf16x8 (&a0)[8], bf16x8 (&a1)[8], bf16x8 (&b)[8],
+                                           const uint32_t (&ra)[2], const uint32_t (&rb)[2]) {
+  const uint32_t s0 = (uint32_t)(t & (SLOTS - 1)) * SLOT_BYTES;
+  const uint32_t s1 = (uint32_t)((t + 1) & (SLOTS - 1)) * SLOT_BYTES;
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  ring_group<0, false>(c, t, acc, a0, a1, b, ra[1] + s0, rb[1] + s0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   lds_barrier();
-  const uint32_t s = (uint32_t)((t + 1) & (SLOTS - 1)) * SLOT_BYTES;
-  ring_group<0>(c, t, acc, ac, an, b, ra0 + s, rb0 + s);
+  ring_group<0, true>(c, t, acc, a1, a0, b, ra[0] + s1, rb[0] + s1);
 }
 
 __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, unsigned char* lds,
@@ -379,40 +407,51 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   const int rows_a = min(BM, p.M - m0), rows_b = min(BN, p.N - n0);
   const i32x4 rsa = rsrc_words(p.A + (size_t)m0 * p.lda, (uint32_t)rows_a * p.lda * 2u);
   const i32x4 rsb = rsrc_words(p.B + (size_t)n0 * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
-  // load side: lane -> (row in its 16-row group, logical chunk)
-  const int lrow = lane >> 2;
-  const int lchunk = (lane & 3) ^ ((lrow >> 1) & 3);
-  const uint32_t voa = (uint32_t)((wave * 64 + lrow) * p.lda + lchunk * 8) * 2u;
-  const uint32_t vob = (uint32_t)((wave * 64 + lrow) * p.ldb + lchunk * 8) * 2u;
+  // load side: lane -> (row in its 8-row block, physical chunk L%8); the
+  // logical chunk stored there is the physical one XOR (row/2)%8, which for a
+  // row w*64 + 8i + r is (r/2) | 4*(i%2): one offset for even blocks, one for odd
+  const int lrow = lane >> 3;
+  int lchunk[2], voa[2], vob[2];
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    lchunk[par] = (lane & 7) ^ ((lrow >> 1) | (par << 2));
+    voa[par] = ((wave * 64 + lrow) * p.lda + lchunk[par] * 8) * 2;
+    vob[par] = ((wave * 64 + lrow) * p.ldb + lchunk[par] * 8) * 2;
+  }
   const uint32_t lds0 = (uint32_t)(size_t)lds;
-  const uint32_t dst_a = lds0 + wave * 64 * 64, dst_b = lds0 + 16384 + wave * 64 * 64;
-  // read side: lane -> (row l%16 of a 16-row block, physical chunk of logical chunk l/16)
+  const uint32_t dst_a = lds0 + wave * 64 * ROW_BYTES, dst_b = lds0 + SLOT_BYTES / 2 + wave * 64 * ROW_BYTES;
+  // read side: lane -> row l%16 of a 16-row block, logical chunk l/16 (+4 for
+  // the second half-stage), stored at that chunk XOR (row/2)%8: conflict-free
+  // 16-byte reads across every 16 lanes
   const int rrow = lane & 15;
-  const int pchunk = (lane >> 4) ^ ((rrow >> 1) & 3);
-  const uint32_t ra0 = lds0 + (uint32_t)((wm * 128 + rrow) * 64 + pchunk * 16);
-  const uint32_t rb0 = lds0 + (uint32_t)(16384 + (wn * 128 + rrow) * 64 + pchunk * 16);
+  uint32_t ra[2], rb[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int pchunk = ((lane >> 4) | (h << 2)) ^ ((rrow >> 1) & 7);
+    ra[h] = lds0 + (uint32_t)((wm * 128 + rrow) * ROW_BYTES + pchunk * 16);
+    rb[h] = lds0 + (uint32_t)(SLOT_BYTES / 2 + (wn * 128 + rrow) * ROW_BYTES + pchunk * 16);
+  }
 
-  RingCtx c{rsa, rsb, voa, vob, dst_a, dst_b, p.lda, p.ldb, p.K, lchunk};
-  // prologue: stages 0..3 in flight (stages past K load zeros), stage 0 published
+  RingCtx c{rsa, rsb, {(uint32_t)voa[0], (uint32_t)voa[1]}, {(uint32_t)vob[0], (uint32_t)vob[1]},
+            dst_a, dst_b, p.lda, p.ldb, p.K, {lchunk[0], lchunk[1]}};
+  // prologue: stages 0 and 1 in flight (a stage past K loads zeros); stage 0
+  // published and its first half's fragments read
 #pragma unroll
   for (int t = 0; t < SLOTS; ++t)
 #pragma unroll
-    for (int g = 0; g < 8; ++g) ring_load(c, t, g);
-  asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+    for (int j = 0; j < 16; ++j) ring_load(c, t, j);
+  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
   lds_barrier();
   bf16x8 a0[8], a1[8], bf[8];
-  lds_read_frag<0>(a0[0], ra0); lds_read_frag<1024>(a0[1], ra0);
-  lds_read_frag<2048>(a0[2], ra0); lds_read_frag<3072>(a0[3], ra0);
-  lds_read_frag<4096>(a0[4], ra0); lds_read_frag<5120>(a0[5], ra0);
-  lds_read_frag<6144>(a0[6], ra0); lds_read_frag<7168>(a0[7], ra0);
-  lds_read_frag<0>(bf[0], rb0); lds_read_frag<1024>(bf[1], rb0);
-  lds_read_frag<2048>(bf[2], rb0); lds_read_frag<3072>(bf[3], rb0);
-  lds_read_frag<4096>(bf[4], rb0); lds_read_frag<5120>(bf[5], rb0);
-  lds_read_frag<6144>(bf[6], rb0); lds_read_frag<7168>(bf[7], rb0);
-  for (int t = 0; t < KT; t += 2) {
-    ring_stage(c, t, acc, a0, a1, bf, ra0, rb0);
-    if (t + 1 < KT) ring_stage(c, t + 1, acc, a1, a0, bf, ra0, rb0);
-  }
+  lds_read_frag<0>(a0[0], ra[0]); lds_read_frag<2048>(a0[1], ra[0]);
+  lds_read_frag<4096>(a0[2], ra[0]); lds_read_frag<6144>(a0[3], ra[0]);
+  lds_read_frag<8192>(a0[4], ra[0]); lds_read_frag<10240>(a0[5], ra[0]);
+  lds_read_frag<12288>(a0[6], ra[0]); lds_read_frag<14336>(a0[7], ra[0]);
+  lds_read_frag<0>(bf[0], rb[0]); lds_read_frag<2048>(bf[1], rb[0]);
+  lds_read_frag<4096>(bf[2], rb[0]); lds_read_frag<6144>(bf[3], rb[0]);
+  lds_read_frag<8192>(bf[4], rb[0]); lds_read_frag<10240>(bf[5], rb[0]);
+  lds_read_frag<12288>(bf[6], rb[0]); lds_read_frag<14336>(bf[7], rb[0]);
+  for (int t = 0; t < KT; ++t) ring_stage(c, t, acc, a0, a1, bf, ra, rb);
   // drain the loads still in flight (zero fills past K) before the slots
   // are reused, and make sure every wave is past its last LDS read
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -461,22 +500,29 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   }
 }
 
-// Claim the next tile for a workgroup on XCD `xcc` (aware mapping): its own
-// XCD's region first, then the other regions (work stealing), so every tile is
-// computed whatever the hardware's placement of workgroups.  Returns -1 when
-// all regions are exhausted.  Called by one lane.
-__device__ __forceinline__ int claim_aware(const Params& p, int xcc) {
-  int tile = -1;
-  for (int d = 0; d < p.n_xccs && tile < 0; ++d) {
+// Another XCD's tile for a workgroup whose own region is exhausted (aware
+// mapping), so every tile is computed whatever the hardware's placement of
+// workgroups.  Run by all 64 lanes of wave 0: lane y reads XCD y's counter, so
+// one round trip shows which regions still have tiles; those are then claimed
+// from in turn, starting after the own XCD.  `q_lane` is region y's tile count
+// in lane y.  Returns -1 when every region is exhausted.
+__device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane) {
+  const int lane = threadIdx.x & 63;
+  int left = 0;
+  if (lane < p.n_xccs)
+    left = q_lane - __hip_atomic_load(&p.ctr[16 + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  unsigned long long open = __ballot(left > 0);
+  for (int d = 1; d <= p.n_xccs && open; ++d) {
     const int y = (xcc + d) % p.n_xccs;
-    const int q = p.off[y + 1] - p.off[y];
-    if (q <= 0) continue;
-    // a cheap read first, so exhausted regions are not hammered
-    if (__hip_atomic_load(&p.ctr[16 + y], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= q) continue;
-    const int t = atomicAdd(&p.ctr[16 + y], 1);
-    if (t < q) tile = p.order[p.off[y] + t];
+    if (!((open >> y) & 1ull)) continue;
+    int t = 0;
+    if (lane == 0) t = atomicAdd(&p.ctr[16 + y], 1);
+    t = __builtin_amdgcn_readfirstlane(t);
+    const int q = __builtin_amdgcn_readfirstlane(__shfl(q_lane, y));
+    if (t < q) return __builtin_amdgcn_readfirstlane(p.order[p.off[y] + t]);
+    open &= ~(1ull << y);
   }
-  return tile;
+  return -1;
 }
 
 template <bool VEC>
@@ -498,15 +544,19 @@ gemm_bf16_persistent(Params p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[VEC ? RING_BYTES : 2 * (BM + BN) * LDP * 2];
   __shared__ int s_info[2];
 
-  // Aware: a rank ticket per XCD; workgroups beyond the XCD's scheduled CU
-  // count leave at once.  Oblivious: every workgroup is a persistent worker.
+  // Aware: workgroups take tiles of the region of the XCD they run on; where
+  // an XCD is scheduled fewer workgroups than land on it (a partial CU set), a
+  // rank ticket lets the first slots[x] stay and the rest leave at once.
+  // Oblivious: every workgroup is a persistent worker.
   const int xcc = (int)read_xcc_id();
   const bool aware = p.mapping == ASYM_MAP_AWARE;
   const int own = xcc < p.n_xccs ? xcc : 0;
+  const int lane = threadIdx.x & 63;
   // read (and observed) before the tile loop, so that no first use inside the
   // k-loop makes the compiler wait there on these loads
   const int own_off = __builtin_amdgcn_readfirstlane(aware ? p.off[own] : 0);
   const int own_q = __builtin_amdgcn_readfirstlane(aware ? p.off[own + 1] - p.off[own] : 0);
+  const int q_lane = (aware && lane < p.n_xccs) ? p.off[lane + 1] - p.off[lane] : 0;
   NextTile nt;
   nt.order = p.order;
   nt.counter = aware ? &p.ctr[16 + own] : nullptr;
@@ -515,26 +565,38 @@ gemm_bf16_persistent(Params p) {
   nt.v = -1;
   nt.i_next = blockIdx.x;
   nt.n_tiles = p.n_tiles;
-  if (threadIdx.x == 0) {
-    int active = 1, first;
+  if (threadIdx.x < 64) {
+    int first = -1;
     if (aware) {
-      int r = -1;
-      if (xcc < p.n_xccs) r = atomicAdd(&p.ctr[xcc], 1);
-      active = (xcc < p.n_xccs && r < p.slots[xcc]) ? 1 : 0;
-      first = active ? claim_aware(p, xcc) : -1;
+      bool active = xcc < p.n_xccs;
+      if (active && p.slots[xcc] < (int)gridDim.x / p.n_xccs) {
+        int r = 0;
+        if (lane == 0) r = atomicAdd(&p.ctr[xcc], 1);
+        active = __builtin_amdgcn_readfirstlane(r) < p.slots[xcc];
+      }
+      if (active) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(nt.counter, 1);
+        idx = __builtin_amdgcn_readfirstlane(idx);
+        first = idx < own_q ? __builtin_amdgcn_readfirstlane(p.order[own_off + idx])
+                            : steal_aware(p, xcc, q_lane);
+      }
     } else {
       first = (int)blockIdx.x < p.n_tiles ? p.order[blockIdx.x] : -1;
     }
-    s_info[1] = first;
+    if (lane == 0) s_info[1] = first;
   }
   __syncthreads();
-  int tile = s_info[1];
+  int tile = __builtin_amdgcn_readfirstlane(s_info[1]);
   while (tile >= 0) {
     nt.i_next += gridDim.x;
     run_tile<VEC>(p, tile, lds, nt);
-    if (threadIdx.x == 0) s_info[1] = take_next(p, nt, xcc);
+    if (threadIdx.x < 64) {
+      const int nxt = take_next(p, nt, xcc, q_lane);
+      if (lane == 0) s_info[1] = nxt;
+    }
     __syncthreads();
-    tile = s_info[1];
+    tile = __builtin_amdgcn_readfirstlane(s_info[1]);
   }
   if (aware && threadIdx.x == 0) {
     // the last workgroup to leave resets the counters for the next launch
