@@ -57,10 +57,13 @@ typedef enum asym_status {
 
 /* Tile-to-compute-unit mappings of the persistent GEMM (Section 7.1). */
 typedef enum asym_mapping {
-  /* Each workgroup reads the XCD it runs on and takes tiles from that XCD's
-   * region; regions hold tile counts proportional to the XCD's CUs and are
-   * contiguous runs of a banded column-major tile order, so the tiles an XCD
-   * runs at once share A rows and B columns in its L2. */
+  /* Every XCD gets a region of the tile grid: in each band of tile rows, a
+   * contiguous run of the band's column-major walk whose length is
+   * proportional to the XCD's CUs in the set (largest remainder), so the
+   * tiles an XCD runs at once share A rows and B columns in its L2.
+   * Workgroup b is XCD (b mod n)'s (b / n)-th worker (the hardware's
+   * round-robin dispatch, measured by the identity probe) and runs that
+   * region with a stride of the XCD's CU count. */
   ASYM_MAP_AWARE = 0,
   /* Same banded order, tile i to persistent workgroup i mod P: with the
    * hardware's round-robin workgroup-to-XCD dispatch, neighbouring tiles land
@@ -267,11 +270,14 @@ int asym_stream_destroy(void* stream);
 /* Tile order for a tiles_m x tiles_n grid under `mapping`, for n_xcds XCDs
  * with slots[x] persistent workgroups each (0 = XCD excluded).
  * order[tiles_m*tiles_n] receives tile ids (row*tiles_n + col); for AWARE the
- * tiles of XCD x are order[off[x] .. off[x+1]), off has n_xcds+1 entries, and
- * quota[x] = off[x+1]-off[x] is proportional to slots[x] (largest remainder,
- * ties to the lower XCD).  For the oblivious mappings off/quota describe which
- * XCD round-robin dispatch sends each order position to.  band = tile rows per
- * band of the banded order (0 = chosen from the slots).
+ * tiles of XCD x are order[off[x] .. off[x+1]), off has n_xcds+1 entries:
+ * every band of `band` tile rows is walked column by column and cut into one
+ * contiguous run per XCD, of length proportional to slots[x] (largest
+ * remainder, ties to the lower XCD), and XCD x's list is its run of band 0,
+ * then of band 1, and so on; quota[x] = off[x+1]-off[x].  For the oblivious
+ * mappings off/quota describe which XCD round-robin dispatch sends each order
+ * position to.  band = tile rows per band (0 = the height h minimising
+ * h + ceil(max slots / h), ties to a divisor of tiles_m, then the taller).
  * Errors: ASYM_EINVAL. */
 int asym_schedule_build(int tiles_m, int tiles_n, int n_xcds,
                         const int* slots, int mapping, int band, int* order,

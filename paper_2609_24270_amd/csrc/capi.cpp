@@ -58,7 +58,6 @@ std::map<ScheduleKey, DeviceSchedule> g_schedules;  // never freed: kernels may 
 // Device counters per (device, stream): launches on one stream run in order
 // and the kernels leave their counters zeroed, so one block per stream does.
 struct Workspace {
-  int* gemm_ctr = nullptr;                  // 64 ints
   unsigned long long* copy_ctr = nullptr;   // 4 words
 };
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
@@ -72,9 +71,7 @@ static int get_workspace(int device, hipStream_t s, Workspace** out) {
   auto it = g_ws.find(key);
   if (it == g_ws.end()) {
     Workspace w;
-    ASYM_HIP(hipMalloc(&w.gemm_ctr, 64 * sizeof(int)));
     ASYM_HIP(hipMalloc(&w.copy_ctr, 4 * sizeof(unsigned long long)));
-    ASYM_HIP(hipMemset(w.gemm_ctr, 0, 64 * sizeof(int)));
     ASYM_HIP(hipMemset(w.copy_ctr, 0, 4 * sizeof(unsigned long long)));
     it = g_ws.emplace(key, w).first;
   }
@@ -202,16 +199,11 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   const DeviceSchedule* ds = nullptr;
   rc = upload_schedule(device, tiles_m, tiles_n, mapping, slots, &ds);
   if (rc != ASYM_OK) return rc;
-  Workspace* ws = nullptr;
-  rc = get_workspace(device, stream, &ws);
-  if (rc != ASYM_OK) return rc;
-
   GemmLaunch g;
   g.A = A; g.B = B; g.C = C;
   g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
   g.mapping = mapping;
   g.d_order = ds->d_order; g.d_off = ds->d_off; g.d_slots = ds->d_slots;
-  g.d_ctr = ws->gemm_ctr;
   g.tiles_m = tiles_m; g.tiles_n = tiles_n;
   g.n_xccs = t->n_xccs;
   g.grid = mapping == ASYM_MAP_AWARE ? t->n_xccs * smax : total;
@@ -240,7 +232,6 @@ void release_workspace(hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_mu);
   for (auto it = g_ws.begin(); it != g_ws.end();) {
     if (it->first.second == s) {
-      hipFree(it->second.gemm_ctr);
       hipFree(it->second.copy_ctr);
       it = g_ws.erase(it);
     } else {

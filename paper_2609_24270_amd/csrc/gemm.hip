@@ -1,18 +1,21 @@
 // Persistent bf16 GEMM for gfx950 with XCD-aware tile placement.
 //
 // Section 7.1 ("Integration with popular kernels") makes a kernel
-// asymmetry-aware by running one persistent block per compute unit, letting
-// each block look up the unit it landed on, and giving it the tasks whose data
-// is local to that unit's partition, with work in proportion to each
-// partition's units.  Here a task is a 256x256 output tile, the partition is
-// the XCD (private 4 MB L2), and the lookup is one read of the XCC_ID hardware
-// register.  In AWARE mode a workgroup takes a rank ticket on its XCD, exits if
-// the XCD already has as many persistent workgroups as it has scheduled CUs,
-// and then claims tiles from its XCD's region of the schedule with a per-XCD
-// atomic counter (then from other XCDs' regions once its own is empty, so the
-// result never depends on where the hardware placed workgroups).  The
-// OBLIVIOUS modes walk one shared order statically (tile i on workgroup i mod
-// P), which is how a persistent GEMM without topology knowledge runs.
+// asymmetry-aware by running one persistent block per compute unit, finding
+// the unit each block runs on, and giving it the tasks whose data is local to
+// that unit's partition, with work in proportion to each partition's units.
+// Here a task is a 256x256 output tile and the partition is the XCD (private
+// 4 MB L2).  On gfx950 the XCD a workgroup lands on is fixed by its launch
+// index: workgroups are dealt to the XCDs round-robin, which the identity
+// probe measures (every workgroup of a full-grid launch reports XCC_ID =
+// block index mod 8).  So the lookup costs nothing at run time: in AWARE mode
+// workgroup b is XCD (b mod n)'s (b / n)-th worker and runs that XCD's region
+// of the schedule with a stride of the XCD's worker count; workers beyond the
+// XCD's scheduled CU count leave at once.  No counters or atomics are
+// involved, and every tile is computed whatever the actual placement (which
+// decides only the L2 a tile is served from).  The OBLIVIOUS modes walk one
+// shared order (tile i on workgroup i mod P), which is how a persistent GEMM
+// without topology knowledge runs.
 //
 // C = A . B with A [M][lda], B stored [N][ldb] (K contiguous), C [M][ldc], all
 // bf16; fp32 accumulation in the matrix cores (v_mfma_f32_16x16x32_bf16);
@@ -22,16 +25,17 @@
 // MFMA blocks, 256 fp32 accumulators per lane in AGPRs).
 //
 // Vector path (16-byte aligned operands, K a multiple of 8): k advances in
-// stages of 32 through a ring of four LDS slots (A and B, 256 rows x 64 bytes
-// each, 32 KiB per slot).  Operands go from HBM straight into LDS with
+// stages of 64 through a ring of two LDS slots (A and B, 256 rows x 128 bytes
+// each, 64 KiB per slot).  Operands go from HBM straight into LDS with
 // buffer_load_dwordx4 ... lds (no staging registers, no LDS write
-// instructions); the loads for stage t+4 are issued when stage t starts, so
-// three stages of MFMA work cover their latency.  Inside a row the four
-// 16-byte chunks are stored XOR-swizzled by (row >> 1) & 3, which keeps the
-// 16 rows read by one ds_read_b128 free of bank conflicts.  MFMA fragments are
-// double-buffered: stage t+1's fragments are read while stage t's 64 MFMAs
-// run.  One barrier per stage publishes the next slot; waits on the loads are
-// explicit, so the barrier does not drain the prefetch.
+// instructions), eight lanes per whole 128-byte line; the loads for stage t+2
+// are issued during the second half of stage t, so a full stage of MFMA work
+// covers their latency.  Inside a row the eight 16-byte chunks are stored
+// XOR-swizzled by (row >> 1) & 7, which keeps the 16 rows read by one
+// ds_read_b128 free of bank conflicts.  MFMA fragments are double-buffered:
+// the next half-stage's fragments are read while the current half-stage's 64
+// MFMAs run.  One barrier per stage publishes the next slot; waits on the
+// loads are explicit, so the barrier does not drain the prefetch.
 //
 // Generic path (any alignment or K): 256x256x64 tiles, register-staged
 // element loads into two padded LDS stages.
@@ -61,14 +65,7 @@ struct Params {
   const int* order;
   const int* off;    // [ASYM_MAX_XCDS + 1]
   const int* slots;  // [ASYM_MAX_XCDS]
-  int* ctr;          // [0,16) rank tickets, [16,32) tile counters, [32] exits
 };
-
-__device__ __forceinline__ uint32_t read_xcc_id() {
-  uint32_t v;
-  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
-  return v & 0xFu;
-}
 
 // Buffer resource over `bytes` bytes at `base`: loads beyond the range return
 // zero and stores beyond it are dropped, so tile edges need no branches.
@@ -283,47 +280,29 @@ struct RingCtx {
   int lchunk[2];            // the lane's logical chunk for even / odd blocks
 };
 
-// The workgroup's next tile.  Lane 0 issues the fetch right after a tile's
-// k-loop has drained (issue_next): the aware claim on its XCD's counter, or
-// the order entry at position i + grid (oblivious).  Nothing waits on it until
-// the epilogue's stores are issued (take_next); by then the fetch has
-// returned.  Issuing it inside the k-loop instead would hold up the ring: the
-// result must stay live across the remaining stages, where every VGPR is
-// taken, so it is spilled, and the spill waits on memory.  Every aware claim
-// is made at the end of a tile, never ahead: a workgroup that took a second
-// tile before the others had their first would leave some of them idle and
-// run two tiles in a row (one tile per workgroup is the common case for
-// decoder shapes).
+// The workgroup's tiles are positions i, i + step, i + 2 step, ... (< end) of
+// the tile order: for the oblivious mappings the whole order with step = the
+// grid; for the aware mapping the region of the workgroup's XCD with step = the
+// XCD's workgroup count.  Lane 0 loads the next order entry right after a
+// tile's k-loop has drained (issue_next); nothing reads it until the
+// epilogue's stores are issued (take_next).  Issuing it inside the k-loop
+// instead would hold up the ring: the value must stay live across the
+// remaining stages, where every VGPR is taken, so it is spilled, and the
+// spill waits on memory.
 struct NextTile {
   const int* order;
-  int* counter;      // aware: the own XCD's tile counter; null for oblivious
-  int own_off, own_q;
-  int i_next;        // oblivious: next position of the shared order
-  int n_tiles;
-  int v;             // lane 0: the claim (aware) or order entry (oblivious) in flight
+  int i_next, step, end;
+  int v;             // lane 0: the order entry in flight
 };
 
 __device__ __forceinline__ void issue_next(NextTile& n) {
   if (threadIdx.x != 0) return;
-  if (n.counter)
-    n.v = atomicAdd(n.counter, 1);
-  else
-    n.v = n.order[n.i_next < n.n_tiles ? n.i_next : 0];
+  n.v = n.order[n.i_next < n.end ? n.i_next : 0];
 }
 
-__device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane);
-
-// Wave 0 (all lanes): the next tile, or -1.  Aware: the index claimed by lane
-// 0 is looked up in the XCD's list; once the own region is exhausted, other
-// regions are tried.
-__device__ __forceinline__ int take_next(const Params& p, const NextTile& n, int xcc, int q_lane) {
-  if (n.counter) {
-    const int idx = __builtin_amdgcn_readfirstlane(n.v);
-    if (idx < n.own_q) return __builtin_amdgcn_readfirstlane(n.order[n.own_off + idx]);
-    return steal_aware(p, xcc, q_lane);
-  }
+__device__ __forceinline__ int take_next(const NextTile& n) {
   const int v = __builtin_amdgcn_readfirstlane(n.v);
-  return n.i_next < n.n_tiles ? v : -1;
+  return n.i_next < n.end ? v : -1;
 }
 
 // j-th of the 16 loads of stage t into slot t % SLOTS: j < 8 are A's, j >= 8
@@ -500,31 +479,6 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   }
 }
 
-// Another XCD's tile for a workgroup whose own region is exhausted (aware
-// mapping), so every tile is computed whatever the hardware's placement of
-// workgroups.  Run by all 64 lanes of wave 0: lane y reads XCD y's counter, so
-// one round trip shows which regions still have tiles; those are then claimed
-// from in turn, starting after the own XCD.  `q_lane` is region y's tile count
-// in lane y.  Returns -1 when every region is exhausted.
-__device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane) {
-  const int lane = threadIdx.x & 63;
-  int left = 0;
-  if (lane < p.n_xccs)
-    left = q_lane - __hip_atomic_load(&p.ctr[16 + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  unsigned long long open = __ballot(left > 0);
-  for (int d = 1; d <= p.n_xccs && open; ++d) {
-    const int y = (xcc + d) % p.n_xccs;
-    if (!((open >> y) & 1ull)) continue;
-    int t = 0;
-    if (lane == 0) t = atomicAdd(&p.ctr[16 + y], 1);
-    t = __builtin_amdgcn_readfirstlane(t);
-    const int q = __builtin_amdgcn_readfirstlane(__shfl(q_lane, y));
-    if (t < q) return __builtin_amdgcn_readfirstlane(p.order[p.off[y] + t]);
-    open &= ~(1ull << y);
-  }
-  return -1;
-}
-
 template <bool VEC>
 __device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned char* lds, NextTile& nt) {
   if constexpr (VEC) {
@@ -544,68 +498,35 @@ gemm_bf16_persistent(Params p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[VEC ? RING_BYTES : 2 * (BM + BN) * LDP * 2];
   __shared__ int s_info[2];
 
-  // Aware: workgroups take tiles of the region of the XCD they run on; where
-  // an XCD is scheduled fewer workgroups than land on it (a partial CU set), a
-  // rank ticket lets the first slots[x] stay and the rest leave at once.
-  // Oblivious: every workgroup is a persistent worker.
-  const int xcc = (int)read_xcc_id();
-  const bool aware = p.mapping == ASYM_MAP_AWARE;
-  const int own = xcc < p.n_xccs ? xcc : 0;
-  const int lane = threadIdx.x & 63;
-  // read (and observed) before the tile loop, so that no first use inside the
-  // k-loop makes the compiler wait there on these loads
-  const int own_off = __builtin_amdgcn_readfirstlane(aware ? p.off[own] : 0);
-  const int own_q = __builtin_amdgcn_readfirstlane(aware ? p.off[own + 1] - p.off[own] : 0);
-  const int q_lane = (aware && lane < p.n_xccs) ? p.off[lane + 1] - p.off[lane] : 0;
+  // Workgroup b belongs to XCD b mod n and is that XCD's (b / n)-th
+  // persistent worker: the hardware deals workgroups to XCDs round-robin in
+  // launch order, the rule the identity probe measures.  Aware: worker r of XCD
+  // x runs positions r, r + s_x, ... of x's region, and workers r >= s_x (CUs
+  // outside the set) leave at once.  The assignment covers every tile whatever
+  // the actual placement; the placement decides only which L2 serves a tile.
+  // Oblivious: every workgroup is a persistent worker over the whole order.
   NextTile nt;
   nt.order = p.order;
-  nt.counter = aware ? &p.ctr[16 + own] : nullptr;
-  nt.own_off = own_off;
-  nt.own_q = own_q;
   nt.v = -1;
-  nt.i_next = blockIdx.x;
-  nt.n_tiles = p.n_tiles;
-  if (threadIdx.x < 64) {
-    int first = -1;
-    if (aware) {
-      bool active = xcc < p.n_xccs;
-      if (active && p.slots[xcc] < (int)gridDim.x / p.n_xccs) {
-        int r = 0;
-        if (lane == 0) r = atomicAdd(&p.ctr[xcc], 1);
-        active = __builtin_amdgcn_readfirstlane(r) < p.slots[xcc];
-      }
-      if (active) {
-        int idx = 0;
-        if (lane == 0) idx = atomicAdd(nt.counter, 1);
-        idx = __builtin_amdgcn_readfirstlane(idx);
-        first = idx < own_q ? __builtin_amdgcn_readfirstlane(p.order[own_off + idx])
-                            : steal_aware(p, xcc, q_lane);
-      }
-    } else {
-      first = (int)blockIdx.x < p.n_tiles ? p.order[blockIdx.x] : -1;
-    }
-    if (lane == 0) s_info[1] = first;
+  if (p.mapping == ASYM_MAP_AWARE) {
+    const int x = (int)blockIdx.x % p.n_xccs, r = (int)blockIdx.x / p.n_xccs;
+    const int s_x = p.slots[x];
+    if (r >= s_x) return;  // the whole workgroup, before any barrier
+    nt.i_next = p.off[x] + r;
+    nt.step = s_x;
+    nt.end = p.off[x + 1];
+  } else {
+    nt.i_next = blockIdx.x;
+    nt.step = gridDim.x;
+    nt.end = p.n_tiles;
   }
-  __syncthreads();
-  int tile = __builtin_amdgcn_readfirstlane(s_info[1]);
+  int tile = nt.i_next < nt.end ? __builtin_amdgcn_readfirstlane(p.order[nt.i_next]) : -1;
   while (tile >= 0) {
-    nt.i_next += gridDim.x;
+    nt.i_next += nt.step;
     run_tile<VEC>(p, tile, lds, nt);
-    if (threadIdx.x < 64) {
-      const int nxt = take_next(p, nt, xcc, q_lane);
-      if (lane == 0) s_info[1] = nxt;
-    }
+    if (threadIdx.x == 0) s_info[1] = take_next(nt);
     __syncthreads();
     tile = __builtin_amdgcn_readfirstlane(s_info[1]);
-  }
-  if (aware && threadIdx.x == 0) {
-    // the last workgroup to leave resets the counters for the next launch
-    __threadfence();
-    const int done = atomicAdd(&p.ctr[32], 1);
-    if (done == (int)gridDim.x - 1) {
-      for (int c = 0; c < 33; ++c) atomicExch(&p.ctr[c], 0);
-      __threadfence();
-    }
   }
 }
 
@@ -621,7 +542,7 @@ int launch_gemm(const GemmLaunch& g, hipStream_t s) {
   p.tiles_m = g.tiles_m; p.tiles_n = g.tiles_n; p.n_tiles = g.tiles_m * g.tiles_n;
   p.mapping = g.mapping;
   p.n_xccs = g.n_xccs;
-  p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots; p.ctr = g.d_ctr;
+  p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots;
   if (g.vec)
     hipLaunchKernelGGL(gemm_bf16_persistent<true>, dim3(g.grid), dim3(NT), 0, s, p);
   else

@@ -76,7 +76,6 @@ struct GemmLaunch {
   const int* d_order;          // device tile order
   const int* d_off;            // device [ASYM_MAX_XCDS+1]
   const int* d_slots;          // device [ASYM_MAX_XCDS]
-  int* d_ctr;                  // device counters (self-resetting)
   int grid;                    // workgroups
   int tiles_m, tiles_n;
   int n_xccs;
