@@ -239,10 +239,15 @@ __device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
 // the logical chunk that belongs there, `so` the row block and k (uniform).
 // Eight lanes read one whole 128-byte line of a row: loads of half lines (a
 // 32-wide k stage) reach barely 60% of this rate through the vector cache.
-__device__ __forceinline__ void dma_1k(uint32_t lds_dst, i32x4 rs, uint32_t vo, int so) {
-  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_dst);
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(m0), "v"(vo), "s"(rs), "s"(__builtin_amdgcn_readfirstlane(so)) : "memory");
+// `row` (the row block's byte offset) and `kb` (the stage's k byte offset)
+// are added in the scalar unit inside the asm, so no part of the address
+// passes through vector registers.
+__device__ __forceinline__ void dma_1k(uint32_t lds_dst, i32x4 rs, uint32_t vo, int row, int kb) {
+  int so;
+  asm volatile("s_add_u32 %0, %1, %2\n\ts_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %4, %5, %0 offen lds"
+               : "=&s"(so)
+               : "s"(row), "s"(kb), "s"(lds_dst), "v"(vo), "s"(rs)
+               : "memory");
 }
 
 __device__ __forceinline__ void lds_barrier() {
@@ -276,7 +281,8 @@ struct RingCtx {
   i32x4 rsa, rsb;
   uint32_t voa[2], vob[2];  // per-lane offsets for even / odd 8-row blocks
   uint32_t dst_a, dst_b;
-  int lda, ldb, K;
+  int row_a[8], row_b[8];   // byte offsets of the wave's eight 8-row blocks
+  int K;
   int lchunk[2];            // the lane's logical chunk for even / odd blocks
 };
 
@@ -305,19 +311,37 @@ __device__ __forceinline__ int take_next(const NextTile& n) {
   return n.i_next < n.end ? v : -1;
 }
 
+// The per-lane load offsets of one stage: the lane's chunk of its row, or an
+// offset past the range (a zero fill) where that chunk starts at or beyond K.
+// Computed once per stage, so the loads themselves need no vector arithmetic.
+struct StageOffsets {
+  uint32_t a[2], b[2];  // even / odd 8-row blocks
+};
+
+__device__ __forceinline__ StageOffsets stage_offsets(const RingCtx& c, int t) {
+  const int k0 = t * KS;
+  StageOffsets o;
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    const bool in_k = k0 + c.lchunk[par] * 8 < c.K;
+    o.a[par] = in_k ? c.voa[par] : kOOB;
+    o.b[par] = in_k ? c.vob[par] : kOOB;
+  }
+  return o;
+}
+
 // j-th of the 16 loads of stage t into slot t % SLOTS: j < 8 are A's, j >= 8
 // B's; each wave owns rows w*64 .. w*64+63 of both operands, load i covering
-// rows w*64 + 8i .. +7.  Stages at or past the end of K are sent out of range
-// and fill the slot with zeros.
-__device__ __forceinline__ void ring_load(const RingCtx& c, int t, int j) {
-  const int k0 = t * KS;
+// rows w*64 + 8i .. +7.  The LDS address and the row/k offset are uniform
+// (scalar registers); stages past the end of K read zeros or go unused.
+__device__ __forceinline__ void ring_load(const RingCtx& c, const StageOffsets& o, int t, int j) {
+  const int kb = __builtin_amdgcn_readfirstlane(t * KS * 2);
   const uint32_t slot = (uint32_t)(t & (SLOTS - 1)) * SLOT_BYTES;
   const int i = j & 7, par = i & 1;
-  const bool in_k = k0 + c.lchunk[par] * 8 < c.K;
   if (j < 8)
-    dma_1k(c.dst_a + slot + i * 1024, c.rsa, in_k ? c.voa[par] : kOOB, (8 * i * c.lda + k0) * 2);
+    dma_1k(c.dst_a + slot + i * 1024, c.rsa, o.a[par], c.row_a[i], kb);
   else
-    dma_1k(c.dst_b + slot + i * 1024, c.rsb, in_k ? c.vob[par] : kOOB, (8 * i * c.ldb + k0) * 2);
+    dma_1k(c.dst_b + slot + i * 1024, c.rsb, o.b[par], c.row_b[i], kb);
 }
 
 // One group of a half-stage (32 of the stage's 64 k): with LOADS, issue loads
@@ -329,18 +353,18 @@ __device__ __forceinline__ void ring_load(const RingCtx& c, int t, int j) {
 // buffered).  `sa`/`sb` are the LDS addresses of the next half-stage's
 // fragment 0.
 template <int G, bool LOADS>
-__device__ __forceinline__ void ring_group(const RingCtx& c, int t, f32x4 (&acc)[8][8],
-                                           const bf16x8 (&ac)[8], bf16x8 (&an)[8], bf16x8 (&b)[8],
-                                           uint32_t sa, uint32_t sb) {
+__device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets& o, int t,
+                                           f32x4 (&acc)[8][8], const bf16x8 (&ac)[8],
+                                           bf16x8 (&an)[8], bf16x8 (&b)[8], uint32_t sa, uint32_t sb) {
   if constexpr (LOADS) {
-    ring_load(c, t + SLOTS, 2 * G);
-    ring_load(c, t + SLOTS, 2 * G + 1);
+    ring_load(c, o, t + SLOTS, 2 * G);
+    ring_load(c, o, t + SLOTS, 2 * G + 1);
   }
 #pragma unroll
   for (int mb = 0; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
   lds_read_frag<G * 2048>(an[G], sa);
   lds_read_frag<G * 2048>(b[G], sb);
-  if constexpr (G + 1 < 8) ring_group<G + 1, LOADS>(c, t, acc, ac, an, b, sa, sb);
+  if constexpr (G + 1 < 8) ring_group<G + 1, LOADS>(c, o, t, acc, ac, an, b, sa, sb);
 }
 
 // Stage t in two halves, branch-free.  First half (k 0..31): its fragments
@@ -355,11 +379,12 @@ __device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)
                                            const uint32_t (&ra)[2], const uint32_t (&rb)[2]) {
   const uint32_t s0 = (uint32_t)(t & (SLOTS - 1)) * SLOT_BYTES;
   const uint32_t s1 = (uint32_t)((t + 1) & (SLOTS - 1)) * SLOT_BYTES;
+  const StageOffsets o = stage_offsets(c, t + SLOTS);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  ring_group<0, false>(c, t, acc, a0, a1, b, ra[1] + s0, rb[1] + s0);
+  ring_group<0, false>(c, o, t, acc, a0, a1, b, ra[1] + s0, rb[1] + s0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   lds_barrier();
-  ring_group<0, true>(c, t, acc, a1, a0, b, ra[0] + s1, rb[0] + s1);
+  ring_group<0, true>(c, o, t, acc, a1, a0, b, ra[0] + s1, rb[0] + s1);
 }
 
 __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, unsigned char* lds,
@@ -370,6 +395,14 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   Params p = pin;
   int tid = threadIdx.x;
   asm volatile("" : "+v"(tid), "+s"(p.K), "+s"(p.lda), "+s"(p.ldb), "+s"(p.ldc), "+s"(p.M), "+s"(p.N));
+  // (and is then read from the first lane, which marks it uniform: address
+  // arithmetic on it stays scalar instead of going through vector registers)
+  p.K = __builtin_amdgcn_readfirstlane(p.K);
+  p.lda = __builtin_amdgcn_readfirstlane(p.lda);
+  p.ldb = __builtin_amdgcn_readfirstlane(p.ldb);
+  p.ldc = __builtin_amdgcn_readfirstlane(p.ldc);
+  p.M = __builtin_amdgcn_readfirstlane(p.M);
+  p.N = __builtin_amdgcn_readfirstlane(p.N);
   const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
   const int lane = tid & 63, wave = tid >> 6;
@@ -398,7 +431,8 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
     vob[par] = ((wave * 64 + lrow) * p.ldb + lchunk[par] * 8) * 2;
   }
   const uint32_t lds0 = (uint32_t)(size_t)lds;
-  const uint32_t dst_a = lds0 + wave * 64 * ROW_BYTES, dst_b = lds0 + SLOT_BYTES / 2 + wave * 64 * ROW_BYTES;
+  const uint32_t dst_a = __builtin_amdgcn_readfirstlane(lds0 + wave * 64 * ROW_BYTES);
+  const uint32_t dst_b = __builtin_amdgcn_readfirstlane(lds0 + SLOT_BYTES / 2 + wave * 64 * ROW_BYTES);
   // read side: lane -> row l%16 of a 16-row block, logical chunk l/16 (+4 for
   // the second half-stage), stored at that chunk XOR (row/2)%8: conflict-free
   // 16-byte reads across every 16 lanes
@@ -412,13 +446,20 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   }
 
   RingCtx c{rsa, rsb, {(uint32_t)voa[0], (uint32_t)voa[1]}, {(uint32_t)vob[0], (uint32_t)vob[1]},
-            dst_a, dst_b, p.lda, p.ldb, p.K, {lchunk[0], lchunk[1]}};
+            dst_a, dst_b, {}, {}, p.K, {lchunk[0], lchunk[1]}};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    c.row_a[i] = __builtin_amdgcn_readfirstlane(8 * i * p.lda * 2);
+    c.row_b[i] = __builtin_amdgcn_readfirstlane(8 * i * p.ldb * 2);
+  }
   // prologue: stages 0 and 1 in flight (a stage past K loads zeros); stage 0
   // published and its first half's fragments read
 #pragma unroll
-  for (int t = 0; t < SLOTS; ++t)
+  for (int t = 0; t < SLOTS; ++t) {
+    const StageOffsets o = stage_offsets(c, t);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) ring_load(c, t, j);
+    for (int j = 0; j < 16; ++j) ring_load(c, o, t, j);
+  }
   asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
   lds_barrier();
   bf16x8 a0[8], a1[8], bf[8];
