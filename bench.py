@@ -192,8 +192,10 @@ def prefill_decode(topo, dev, iters: int, halves):
     grp = [x for x in range(8) if (halves[1] >> x) & 1]
     dec_x = (1 << grp[-1]) | (1 << grp[-2])
     pre_x = 0xFF & ~dec_x
-    runs = {"xcd_aligned": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", xcd_mask=pre_x),
-                                               asym.gemm_task(da, db, cd, 3 * iters, "aware", xcd_mask=dec_x)], topo),
+    pre_m, dec_m = topo.cuset_split_xcds(pre_x)
+    runs = {"xcd_aligned": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=pre_m, xcd_mask=pre_x),
+                                               asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=dec_m, xcd_mask=dec_x)],
+                                              topo),
             "cu_striped": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=prefill),
                                               asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=decode)], topo)}
     out = {}
@@ -208,8 +210,8 @@ def prefill_decode(topo, dev, iters: int, halves):
 def spread_study(topo, dev, n_masks: int, iters: int, halves):
     """GEMM 4096^3 (uniform[-1,1], seed 4) on 128-CU sets: n_masks seeded random
     choices of 128 mask bits (what a topology-oblivious allocator hands out) and
-    the two whole-XCD halves (the measured affinity groups, through the XCD
-    filter).  A second
+    the two whole-XCD halves (the measured affinity groups; each side lends the
+    other one CU per XCD and works only on its own XCDs).  A second
     tenant, the same GEMM, runs on the complementary 128 CUs for the whole
     measurement.  Per-set TFLOP/s of the measured GEMM for each mapping, and the
     max/min spread over the random sets."""
@@ -237,8 +239,10 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves):
             per[mapping].append(r[0]["tflops"])
     aligned = []
     for xm in halves:
-        r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", xcd_mask=xm),
-                        asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", xcd_mask=0xFF & ~xm)], topo)
+        ma, mb = topo.cuset_split_xcds(xm)
+        r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
+                        asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=mb, xcd_mask=0xFF & ~xm)],
+                       topo)
         aligned.append(round(r[0]["tflops"], 2))
     summ = {"n_random_sets": n_masks, "iters": iters, "aligned_aware_tflops": aligned,
             "random_set_min_max_cus_per_xcd": [min(min(c) for c in counts), max(max(c) for c in counts)]}

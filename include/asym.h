@@ -210,6 +210,16 @@ int asym_topology_cu(const asym_topology* topo, int cu_index, int* xcc,
  * n_xccs (1.0 = round-robin dispatch).  Written by the IDENTITY probe. */
 int asym_topology_dispatch(const asym_topology* topo, double* rr_fraction);
 
+/* Where launches land on a CU set: runs 4 x n_cus workgroups of the identity
+ * kernel on a stream restricted to `mask` (CU-mask bits, ASYM_MASK_WORDS
+ * words; NULL = every CU; the same rules as asym_stream_create) and reports
+ * the fraction whose XCC is their block index mod the XCD count, and
+ * (nullable, ASYM_MAX_XCDS ints) how many workgroups each XCD ran.  The aware
+ * GEMM assumes that rule for locality only.  Synchronous.
+ * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
+int asym_dispatch_check(const asym_topology* topo, const uint32_t* mask,
+                        double* rr_fraction, int* blocks_per_xcd);
+
 /* Latency-probe results; ASYM_EUNSUPPORTED if the map was probed without LATENCY. */
 int asym_topology_latency(const asym_topology* topo, asym_latency_summary* out);
 
@@ -252,6 +262,15 @@ int asym_latency_analyze(const uint32_t* hbm_lat, int n_xcds, int n_samples,
  * a whole number of XCDs.  Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED. */
 int asym_cuset_make(const asym_topology* topo, int n_cus, int policy,
                     uint64_t seed, const uint32_t* exclude, uint32_t* mask_out);
+
+/* Two CU sets on disjoint whole-XCD sides: A works on the XCDs in
+ * xcd_mask_a, B on the others.  Each side gives the other its lowest CU on
+ * each of its XCDs, so that neither mask leaves an XCD empty and workgroups a
+ * kernel deals to the other side's XCDs find a free CU there and leave at once
+ * (run A with xcd_mask = xcd_mask_a and B with the complement).  Needs a
+ * topology with a mask map.  Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED. */
+int asym_cuset_split_xcds(const asym_topology* topo, uint32_t xcd_mask_a,
+                          uint32_t* mask_a, uint32_t* mask_b);
 
 /* Per-XCD CU counts of a mask (mask bits, ASYM_MASK_WORDS words). */
 int asym_cuset_counts(const asym_topology* topo, const uint32_t* mask,

@@ -36,6 +36,7 @@ EXPORTS = (
     "asym_topology_free", "asym_topology_info", "asym_topology_cu",
     "asym_topology_dispatch", "asym_topology_latency", "asym_topology_json",
     "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
+    "asym_dispatch_check", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_gemm_bf16",
     "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
@@ -131,6 +132,8 @@ def load_library(path: str = LIB_PATH):
         "asym_topology_dispatch": (i, [topo_p, ctypes.POINTER(ctypes.c_double)]),
         "asym_topology_latency": (i, [topo_p, ctypes.POINTER(LatencySummary)]),
         "asym_latency_params_default": (None, [ctypes.POINTER(LatencyParams)]),
+        "asym_dispatch_check": (i, [topo_p, u32p, ctypes.POINTER(ctypes.c_double), ip]),
+        "asym_cuset_split_xcds": (i, [topo_p, u32, u32p, u32p]),
         "asym_latency_probe": (i, [i, ctypes.POINTER(LatencyParams), u32p, ctypes.POINTER(LatencySummary)]),
         "asym_latency_analyze": (i, [u32p, i, i, ctypes.c_double, ctypes.c_double,
                                      ctypes.POINTER(LatencySummary)]),
@@ -243,10 +246,26 @@ class Topology:
         _check(lib.asym_topology_json(self._h, buf, need.value, ctypes.byref(need)))
         return json.loads(buf.value.decode())
 
+    def dispatch_check(self, mask: Optional[Sequence[int]] = None):
+        """(fraction of workgroups on XCC block mod n, workgroups per XCD) for a
+        launch on the CU set `mask` (None = all CUs)."""
+        rr = ctypes.c_double()
+        per = (ctypes.c_int * MAX_XCDS)()
+        _check(load_library().asym_dispatch_check(self._h, mask_words(mask), ctypes.byref(rr), per))
+        return rr.value, list(per)[: self.info()["n_xcds"]]
+
     def cuset(self, n_cus: int, policy: int, seed: int = 0, exclude: Optional[Sequence[int]] = None) -> list:
         out = (ctypes.c_uint32 * MASK_WORDS)()
         _check(load_library().asym_cuset_make(self._h, n_cus, policy, seed, mask_words(exclude), out))
         return mask_bits(out)
+
+    def cuset_split_xcds(self, xcd_mask_a: int):
+        """(bits of side A, bits of side B): A works on the XCDs in xcd_mask_a,
+        B on the rest; each side lends the other one CU per XCD."""
+        a = (ctypes.c_uint32 * MASK_WORDS)()
+        b = (ctypes.c_uint32 * MASK_WORDS)()
+        _check(load_library().asym_cuset_split_xcds(self._h, xcd_mask_a, a, b))
+        return mask_bits(a), mask_bits(b)
 
     def cuset_counts(self, bits: Sequence[int]) -> list:
         per = (ctypes.c_int * MAX_XCDS)()

@@ -58,6 +58,7 @@ std::map<ScheduleKey, DeviceSchedule> g_schedules;  // never freed: kernels may 
 // Device counters per (device, stream): launches on one stream run in order
 // and the kernels leave their counters zeroed, so one block per stream does.
 struct Workspace {
+  int* gemm_ctr = nullptr;                  // 64 ints (dynamic aware GEMM)
   unsigned long long* copy_ctr = nullptr;   // 4 words
 };
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
@@ -71,6 +72,8 @@ static int get_workspace(int device, hipStream_t s, Workspace** out) {
   auto it = g_ws.find(key);
   if (it == g_ws.end()) {
     Workspace w;
+    ASYM_HIP(hipMalloc(&w.gemm_ctr, 64 * sizeof(int)));
+    ASYM_HIP(hipMemset(w.gemm_ctr, 0, 64 * sizeof(int)));
     ASYM_HIP(hipMalloc(&w.copy_ctr, 4 * sizeof(unsigned long long)));
     ASYM_HIP(hipMemset(w.copy_ctr, 0, 4 * sizeof(unsigned long long)));
     it = g_ws.emplace(key, w).first;
@@ -186,6 +189,10 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   if (xcd_mask != 0 && (xcd_mask & ~all)) return fail(ASYM_EINVAL, "gemm: xcd_mask names XCDs the device does not have");
   if (mapping != ASYM_MAP_AWARE && xm != all)
     return fail(ASYM_EUNSUPPORTED, "gemm: XCD restriction needs the aware mapping (oblivious mappings place tiles statically)");
+  for (int x = 0; x < t->n_xccs; ++x)
+    if (per[x] == 0)
+      return fail(ASYM_EUNSUPPORTED, "gemm: the stream's CU mask leaves XCD " + std::to_string(x) +
+                                         " without a CU; workgroups dealt to it could never run");
   std::vector<int> slots(t->n_xccs, 0);
   int total = 0, smax = 0;
   for (int x = 0; x < t->n_xccs; ++x) {
@@ -199,6 +206,10 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   const DeviceSchedule* ds = nullptr;
   rc = upload_schedule(device, tiles_m, tiles_n, mapping, slots, &ds);
   if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(device, stream, &ws);
+  if (rc != ASYM_OK) return rc;
+
   GemmLaunch g;
   g.A = A; g.B = B; g.C = C;
   g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
@@ -207,6 +218,14 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   g.tiles_m = tiles_m; g.tiles_n = tiles_n;
   g.n_xccs = t->n_xccs;
   g.grid = mapping == ASYM_MAP_AWARE ? t->n_xccs * smax : total;
+  g.d_ctr = ws->gemm_ctr;
+  // The aware grid deals smax workgroups to every XCD.  Where an XCD has fewer
+  // CUs in the stream's set, the surplus there waits for a CU and holds up the
+  // dispatch behind it, so the static assignment (which needs every worker to
+  // run) gives way to claims.
+  g.dynamic = false;
+  for (int x = 0; x < t->n_xccs; ++x)
+    if (per[x] < smax) g.dynamic = true;
   g.vec = aligned16(A) && aligned16(B) && (((uintptr_t)C & 7u) == 0) && (K % 8 == 0) &&
           (lda % 8 == 0) && (ldb % 8 == 0) && (ldc % 4 == 0);
   return launch_gemm(g, stream);
@@ -232,6 +251,7 @@ void release_workspace(hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_mu);
   for (auto it = g_ws.begin(); it != g_ws.end();) {
     if (it->first.second == s) {
+      hipFree(it->second.gemm_ctr);
       hipFree(it->second.copy_ctr);
       it = g_ws.erase(it);
     } else {

@@ -65,6 +65,8 @@ struct Params {
   const int* order;
   const int* off;    // [ASYM_MAX_XCDS + 1]
   const int* slots;  // [ASYM_MAX_XCDS]
+  int* ctr;          // dynamic aware: [0,16) rank tickets, [16,32) tile counters, [32] exits
+  int dynamic;       // aware mapping with claims instead of the static assignment
 };
 
 // Buffer resource over `bytes` bytes at `base`: loads beyond the range return
@@ -286,27 +288,43 @@ struct RingCtx {
   int lchunk[2];            // the lane's logical chunk for even / odd blocks
 };
 
-// The workgroup's tiles are positions i, i + step, i + 2 step, ... (< end) of
-// the tile order: for the oblivious mappings the whole order with step = the
-// grid; for the aware mapping the region of the workgroup's XCD with step = the
-// XCD's workgroup count.  Lane 0 loads the next order entry right after a
-// tile's k-loop has drained (issue_next); nothing reads it until the
+// The workgroup's next tile.  Static assignment: positions i, i + step,
+// i + 2 step, ... (< end) of the tile order: for the oblivious mappings the
+// whole order with step = the grid; for the aware mapping the region of the
+// workgroup's XCD with step = the XCD's workgroup count.  Dynamic (aware on an
+// uneven CU set): claims on a per-XCD counter.  Lane 0 issues the fetch right
+// after a tile's k-loop has drained (issue_next); nothing reads it until the
 // epilogue's stores are issued (take_next).  Issuing it inside the k-loop
 // instead would hold up the ring: the value must stay live across the
 // remaining stages, where every VGPR is taken, so it is spilled, and the
 // spill waits on memory.
 struct NextTile {
   const int* order;
+  int* counter;      // dynamic: the own XCD's tile counter; null for static
+  int own_off, own_q;
   int i_next, step, end;
-  int v;             // lane 0: the order entry in flight
+  int v;             // lane 0: the claim or the order entry in flight
 };
 
 __device__ __forceinline__ void issue_next(NextTile& n) {
   if (threadIdx.x != 0) return;
-  n.v = n.order[n.i_next < n.end ? n.i_next : 0];
+  if (n.counter)
+    n.v = atomicAdd(n.counter, 1);
+  else
+    n.v = n.order[n.i_next < n.end ? n.i_next : 0];
 }
 
-__device__ __forceinline__ int take_next(const NextTile& n) {
+__device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane);
+
+// Wave 0 (all lanes): the next tile, or -1.  Dynamic: the index claimed by
+// lane 0 is looked up in the XCD's list; once the own region is exhausted,
+// other regions are tried.
+__device__ __forceinline__ int take_next(const Params& p, const NextTile& n, int xcc, int q_lane) {
+  if (n.counter) {
+    const int idx = __builtin_amdgcn_readfirstlane(n.v);
+    if (idx < n.own_q) return __builtin_amdgcn_readfirstlane(n.order[n.own_off + idx]);
+    return steal_aware(p, xcc, q_lane);
+  }
   const int v = __builtin_amdgcn_readfirstlane(n.v);
   return n.i_next < n.end ? v : -1;
 }
@@ -520,6 +538,31 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   }
 }
 
+// Another XCD's tile for a workgroup whose own region is exhausted (dynamic
+// aware mapping), so every tile is computed whatever the hardware's placement
+// of workgroups.  Run by all 64 lanes of wave 0: lane y reads XCD y's counter,
+// so one round trip shows which regions still have tiles; those are then
+// claimed from in turn, starting after the own XCD.  `q_lane` is region y's
+// tile count in lane y.  Returns -1 when every region is exhausted.
+__device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane) {
+  const int lane = threadIdx.x & 63;
+  int left = 0;
+  if (lane < p.n_xccs)
+    left = q_lane - __hip_atomic_load(&p.ctr[16 + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  unsigned long long open = __ballot(left > 0);
+  for (int d = 1; d <= p.n_xccs && open; ++d) {
+    const int y = (xcc + d) % p.n_xccs;
+    if (!((open >> y) & 1ull)) continue;
+    int t = 0;
+    if (lane == 0) t = atomicAdd(&p.ctr[16 + y], 1);
+    t = __builtin_amdgcn_readfirstlane(t);
+    const int q = __builtin_amdgcn_readfirstlane(__shfl(q_lane, y));
+    if (t < q) return __builtin_amdgcn_readfirstlane(p.order[p.off[y] + t]);
+    open &= ~(1ull << y);
+  }
+  return -1;
+}
+
 template <bool VEC>
 __device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned char* lds, NextTile& nt) {
   if constexpr (VEC) {
@@ -539,17 +582,41 @@ gemm_bf16_persistent(Params p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[VEC ? RING_BYTES : 2 * (BM + BN) * LDP * 2];
   __shared__ int s_info[2];
 
-  // Workgroup b belongs to XCD b mod n and is that XCD's (b / n)-th
-  // persistent worker: the hardware deals workgroups to XCDs round-robin in
-  // launch order, the rule the identity probe measures.  Aware: worker r of XCD
-  // x runs positions r, r + s_x, ... of x's region, and workers r >= s_x (CUs
-  // outside the set) leave at once.  The assignment covers every tile whatever
-  // the actual placement; the placement decides only which L2 serves a tile.
-  // Oblivious: every workgroup is a persistent worker over the whole order.
+  // Static aware assignment: workgroup b belongs to XCD b mod n and is that
+  // XCD's (b / n)-th persistent worker (the hardware deals workgroups to XCDs
+  // round-robin in launch order, the rule the identity probe measures); worker
+  // r of XCD x runs positions r, r + s_x, ... of x's region, and workers
+  // r >= s_x leave at once.  It covers every tile whatever the actual
+  // placement, which decides only the L2 a tile is served from.  It is used
+  // when every XCD has at least as many CUs in the stream's set as workgroups
+  // are dealt to it, so no workgroup waits behind a full XCD.  Otherwise
+  // (uneven CU sets) the dynamic form: a workgroup reads the XCD it runs on,
+  // takes a rank ticket there (ranks past the XCD's CU count leave), and
+  // claims tiles of that XCD's region from a counter, then of other regions.
+  // Oblivious: every workgroup walks the whole order statically.
+  const int lane = threadIdx.x & 63;
+  const bool aware = p.mapping == ASYM_MAP_AWARE;
+  const bool dyn = aware && p.dynamic;
+  int xcc = 0, q_lane = 0;
   NextTile nt;
   nt.order = p.order;
+  nt.counter = nullptr;
+  nt.own_off = 0;
+  nt.own_q = 0;
   nt.v = -1;
-  if (p.mapping == ASYM_MAP_AWARE) {
+  if (dyn) {
+    uint32_t xr;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xr));
+    xcc = (int)(xr & 0xFu);
+    const int own = xcc < p.n_xccs ? xcc : 0;
+    nt.own_off = __builtin_amdgcn_readfirstlane(p.off[own]);
+    nt.own_q = __builtin_amdgcn_readfirstlane(p.off[own + 1] - p.off[own]);
+    nt.counter = &p.ctr[16 + own];
+    q_lane = lane < p.n_xccs ? p.off[lane + 1] - p.off[lane] : 0;
+    nt.i_next = 0;
+    nt.step = 0;
+    nt.end = 0;
+  } else if (aware) {
     const int x = (int)blockIdx.x % p.n_xccs, r = (int)blockIdx.x / p.n_xccs;
     const int s_x = p.slots[x];
     if (r >= s_x) return;  // the whole workgroup, before any barrier
@@ -561,13 +628,48 @@ gemm_bf16_persistent(Params p) {
     nt.step = gridDim.x;
     nt.end = p.n_tiles;
   }
-  int tile = nt.i_next < nt.end ? __builtin_amdgcn_readfirstlane(p.order[nt.i_next]) : -1;
+  int tile;
+  if (dyn) {
+    if (threadIdx.x < 64) {
+      int first = -1;
+      bool active = xcc < p.n_xccs && p.slots[xcc] > 0;  // no ticket on an XCD outside the set
+      if (active) {
+        int r = 0;
+        if (lane == 0) r = atomicAdd(&p.ctr[xcc], 1);
+        active = __builtin_amdgcn_readfirstlane(r) < p.slots[xcc];
+      }
+      if (active) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(nt.counter, 1);
+        idx = __builtin_amdgcn_readfirstlane(idx);
+        first = idx < nt.own_q ? __builtin_amdgcn_readfirstlane(p.order[nt.own_off + idx])
+                               : steal_aware(p, xcc, q_lane);
+      }
+      if (lane == 0) s_info[1] = first;
+    }
+    __syncthreads();
+    tile = __builtin_amdgcn_readfirstlane(s_info[1]);
+  } else {
+    tile = nt.i_next < nt.end ? __builtin_amdgcn_readfirstlane(p.order[nt.i_next]) : -1;
+  }
   while (tile >= 0) {
     nt.i_next += nt.step;
     run_tile<VEC>(p, tile, lds, nt);
-    if (threadIdx.x == 0) s_info[1] = take_next(nt);
+    if (threadIdx.x < 64) {
+      const int nxt = take_next(p, nt, xcc, q_lane);
+      if (lane == 0) s_info[1] = nxt;
+    }
     __syncthreads();
     tile = __builtin_amdgcn_readfirstlane(s_info[1]);
+  }
+  if (dyn && threadIdx.x == 0) {
+    // the last workgroup to leave resets the counters for the next launch
+    __threadfence();
+    const int done = atomicAdd(&p.ctr[32], 1);
+    if (done == (int)gridDim.x - 1) {
+      for (int c = 0; c < 33; ++c) atomicExch(&p.ctr[c], 0);
+      __threadfence();
+    }
   }
 }
 
@@ -583,7 +685,8 @@ int launch_gemm(const GemmLaunch& g, hipStream_t s) {
   p.tiles_m = g.tiles_m; p.tiles_n = g.tiles_n; p.n_tiles = g.tiles_m * g.tiles_n;
   p.mapping = g.mapping;
   p.n_xccs = g.n_xccs;
-  p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots;
+  p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots; p.ctr = g.d_ctr;
+  p.dynamic = g.dynamic ? 1 : 0;
   if (g.vec)
     hipLaunchKernelGGL(gemm_bf16_persistent<true>, dim3(g.grid), dim3(NT), 0, s, p);
   else

@@ -76,6 +76,8 @@ struct GemmLaunch {
   const int* d_order;          // device tile order
   const int* d_off;            // device [ASYM_MAX_XCDS+1]
   const int* d_slots;          // device [ASYM_MAX_XCDS]
+  int* d_ctr;                  // device counters of the dynamic form (self-resetting)
+  bool dynamic;                // aware mapping on an uneven CU set: claims, not static
   int grid;                    // workgroups
   int tiles_m, tiles_n;
   int n_xccs;

@@ -118,6 +118,7 @@ static int probe_maskmap(int device, const Topology& t, const std::vector<int32_
 struct asym_topology;
 namespace asym {
 asym_topology* wrap_topology(Topology&& t);
+const Topology* unwrap(const asym_topology* p);
 }
 
 extern "C" int asym_probe_topology(int device, unsigned flags, asym_topology** out) {
@@ -159,5 +160,42 @@ extern "C" int asym_probe_topology(int device, unsigned flags, asym_topology** o
     if (rc != ASYM_OK) return rc;
   }
   *out = wrap_topology(std::move(t));
+  return ASYM_OK;
+}
+
+// Where a launch on a CU set lands: the identity kernel is run on a stream
+// restricted to `mask` (NULL = every CU) and each workgroup's XCC is compared
+// with its block index mod the XCD count.  The aware GEMM relies on that rule
+// only for locality (its tile assignment covers every tile whatever the
+// placement), so this is the check of a performance assumption, not of
+// correctness.
+extern "C" int asym_dispatch_check(const asym_topology* topo, const uint32_t* mask,
+                                   double* rr_fraction, int* blocks_per_xcd) {
+  using namespace asym;
+  const Topology* t = unwrap(topo);
+  if (!t || !rr_fraction) return fail(ASYM_EINVAL, "dispatch check: null argument");
+  int device = 0;
+  ASYM_HIP(hipGetDevice(&device));
+  if (t->device >= 0 && t->device != device)
+    return fail(ASYM_EINVAL, "dispatch check: topology was probed on another device");
+  void* sv = nullptr;
+  int rc = asym_stream_create(topo, mask, &sv);
+  if (rc != ASYM_OK) return rc;
+  hipStream_t s = static_cast<hipStream_t>(sv);
+  const int n_blocks = 4 * t->n_cus;
+  std::vector<int32_t> rec;
+  rc = probe_identity_run(device, s, n_blocks, rec);
+  asym_stream_destroy(sv);
+  if (rc != ASYM_OK) return rc;
+  std::vector<int> per(ASYM_MAX_XCDS, 0);
+  int agree = 0;
+  for (int b = 0; b < n_blocks; ++b) {
+    const int x = xccid((uint32_t)rec[4 * b]);
+    if (x < ASYM_MAX_XCDS) per[x] += 1;
+    if (x == b % t->n_xccs) ++agree;
+  }
+  *rr_fraction = (double)agree / n_blocks;
+  if (blocks_per_xcd)
+    for (int x = 0; x < ASYM_MAX_XCDS; ++x) blocks_per_xcd[x] = per[x];
   return ASYM_OK;
 }

@@ -361,3 +361,38 @@ extern "C" int asym_cuset_counts(const asym_topology* topo, const uint32_t* mask
   for (int x = 0; x < ASYM_MAX_XCDS; ++x) per_xcd[x] = x < (int)per.size() ? per[x] : 0;
   return ASYM_OK;
 }
+
+// Two tenants on disjoint whole-XCD sides.  Workgroups are dealt to every XCD
+// in turn whatever the stream's CU mask, so a tenant whose mask left an XCD
+// empty could never run the workgroups dealt there, and a tenant whose
+// workgroups had to wait for a CU held by the other side's persistent kernel
+// would stall its own dispatch.  So each side gives the other one CU (its
+// lowest) on each of its XCDs: the other tenant's workgroups that land there
+// find a free CU and leave at once (xcd_mask restricts the work to the
+// tenant's own XCDs).
+extern "C" int asym_cuset_split_xcds(const asym_topology* topo, uint32_t xcd_mask_a,
+                                     uint32_t* mask_a, uint32_t* mask_b) {
+  using namespace asym;
+  if (!topo || !mask_a || !mask_b) return fail(ASYM_EINVAL, "null argument");
+  const Topology& t = topo->t;
+  if (!t.has_maskmap) return fail(ASYM_EUNSUPPORTED, "cuset split: needs a topology with a mask map");
+  const uint32_t all = t.n_xccs >= 32 ? 0xFFFFFFFFu : ((1u << t.n_xccs) - 1u);
+  if ((xcd_mask_a & ~all) || (xcd_mask_a & all) == 0 || (xcd_mask_a & all) == all)
+    return fail(ASYM_EINVAL, "cuset split: side A must name some but not all XCDs");
+  std::memset(mask_a, 0, sizeof(uint32_t) * ASYM_MASK_WORDS);
+  std::memset(mask_b, 0, sizeof(uint32_t) * ASYM_MASK_WORDS);
+  std::vector<int> bit_of(t.n_cus, -1);
+  for (int b = 0; b < (int)t.bit_to_cu.size(); ++b)
+    if (t.bit_to_cu[b] >= 0) bit_of[t.bit_to_cu[b]] = b;
+  std::vector<bool> first_seen(t.n_xccs, false);
+  for (int c = 0; c < t.n_cus; ++c) {  // dense order: each XCD's lowest CU comes first
+    const int x = t.cus[c].xcc, b = bit_of[c];
+    if (b < 0) return fail(ASYM_EINVAL, "cuset split: mask map incomplete");
+    const bool side_a = (xcd_mask_a >> x) & 1u;
+    const bool give = !first_seen[x];
+    first_seen[x] = true;
+    uint32_t* m = (side_a != give) ? mask_a : mask_b;
+    m[b >> 5] |= 1u << (b & 31);
+  }
+  return ASYM_OK;
+}

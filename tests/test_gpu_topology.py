@@ -60,6 +60,21 @@ def test_maskmap_probe(dev, topo):
     assert js["has_maskmap"]
 
 
+def test_dispatch_rule_on_cu_sets(dev, topo):
+    """Launches are dealt to XCDs round-robin by block index on the whole chip;
+    the same check on a random 128-CU set and on a striped set reports where
+    masked launches land (the aware GEMM relies on the rule for locality only)."""
+    n = asym.device_query(0)["n_cus"]
+    rr, per = topo.dispatch_check(None)
+    print("full", rr, per)
+    assert rr == 1.0 and sum(per) == 4 * n
+    for name, m in (("random", workloads.random_mask_bits(4, 1, 128)[0]),
+                    ("striped", topo.cuset(128, asym.CUSET_STRIPED))):
+        rr, per = topo.dispatch_check(m)
+        print(name, rr, per, topo.cuset_counts(m))
+        assert 0.0 <= rr <= 1.0 and sum(per) == 4 * n
+
+
 def test_masked_gemm_bitwise(dev, topo):
     A, B = workloads.make_inputs(workloads.COLOC)
     Ad, Bd = A.to(dev), B.to(dev)
@@ -160,7 +175,8 @@ def test_corun_prefill_decode(dev, topo):
     print("striped", res)
     assert torch.equal(cp, ref_p) and torch.equal(cd, ref_d)
     assert res[0]["tflops"] > 0 and res[1]["tflops"] > 0
-    res = asym.corun([asym.gemm_task(pa, pb, cp, 3, "aware", xcd_mask=0x3F),
-                      asym.gemm_task(da, db, cd, 20, "aware", xcd_mask=0xC0)], topo)
+    pm, dm = topo.cuset_split_xcds(0x3F)
+    res = asym.corun([asym.gemm_task(pa, pb, cp, 3, "aware", mask=pm, xcd_mask=0x3F),
+                      asym.gemm_task(da, db, cd, 20, "aware", mask=dm, xcd_mask=0xC0)], topo)
     print("xcd-aligned", res)
     assert torch.equal(cp, ref_p) and torch.equal(cd, ref_d)

@@ -254,6 +254,30 @@ def test_maskmap_and_cusets(lib):
     assert not set(r4) & set(r1)
 
 
+def test_xcd_split_lends_one_cu_per_foreign_xcd(lib):
+    t, perm = _maskmap_topology()
+    a, b = t.cuset_split_xcds(0x0F)
+    assert not set(a) & set(b) and sorted(a + b) == list(range(256))
+    assert t.cuset_counts(a) == [31, 31, 31, 31, 1, 1, 1, 1]
+    assert t.cuset_counts(b) == [1, 1, 1, 1, 31, 31, 31, 31]
+    # the lent CU is the lowest CU of its XCD in the dense order
+    lowest = {}
+    for c in t.cus():
+        lowest.setdefault(c["xcc"], c["mask_bit"])
+    for x in range(8):
+        owner, other = (a, b) if x < 4 else (b, a)
+        assert lowest[x] in other and lowest[x] not in owner
+    a6, b2 = t.cuset_split_xcds(0x3F)
+    assert t.cuset_counts(a6) == [31] * 6 + [1, 1] and t.cuset_counts(b2) == [1] * 6 + [31, 31]
+    for bad in (0, 0xFF, 0x100):
+        with pytest.raises(asym.AsymError):
+            t.cuset_split_xcds(bad)
+    plain = asym.topology_from_records(fake_records(uniform_layout()), 256, 8)
+    with pytest.raises(asym.AsymError) as e:
+        plain.cuset_split_xcds(0x0F)
+    assert e.value.status == asym.EUNSUPPORTED
+
+
 def test_masked_stream_refuses_an_empty_xcd(lib):
     t, _ = _maskmap_topology()
     aligned = t.cuset(128, asym.CUSET_XCD_ALIGNED)

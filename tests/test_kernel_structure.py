@@ -120,14 +120,15 @@ def claims_published_in_their_loop(insts, claim_re):
     return checked
 
 
-def test_gemm_workers_share_no_state(tmp):
-    """The persistent GEMM assigns tiles statically (worker r of XCD x runs its
-    region with a stride): no atomics, so no lost claim can keep a workgroup
-    waiting, and no scalar-cache writes of any kind."""
+def test_gemm_tile_claim_is_published_in_its_own_loop(tmp):
+    """The dynamic aware form claims tiles on per-XCD counters (offset 64 and
+    up) inside the tile loop; every such claim must sit in the loop whose
+    barrier publishes it.  No scalar-cache writes of any kind."""
     body = function_body(asm_of("gemm.hip", tmp), "gemm_bf16_persistentILb1E")
+    insts = annotate_loops(body)
+    n = claims_published_in_their_loop(insts, r"^global_atomic_add v\d+, v\d+, v\d+, s\[\d+:\d+\]( offset:\d+)? sc0")
+    assert n >= 1
     text = "\n".join(body)
-    assert "v_mfma_f32_16x16x32_bf16" in text
-    assert not re.search(r"\b(global|buffer|flat)_atomic", text)
     assert not re.search(r"\bs_(store|atomic|buffer_store|dcache_wb|scratch_store)", text)
 
 
