@@ -149,6 +149,30 @@ static int upload_schedule(int device, int tiles_m, int tiles_n, int mapping,
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Tile width of the vector path (the height is always 256): the one with the
+// least time per launch in the model  ceil(tiles / workers) x width / eff,
+// i.e. whole waves of tiles, each as long as its width, with eff the measured
+// relative MFMA efficiency of the narrower tiles.  Decoder shapes gain most:
+// 4096 x 6144 is 1.5 waves of 256-wide tiles on 256 CUs but 2 waves of
+// 192-wide ones; 4096 x 14336 is 3.5 waves at 256 but 4 at 224.
+static int choose_tile_width(int M, int N, int workers) {
+  static const int widths[3] = {256, 224, 192};
+  static const double eff[3] = {1.0, 0.97, 0.94};
+  const int64_t tm = (M + 255) / 256;
+  int best = 256;
+  double best_cost = 0;
+  for (int i = 0; i < 3; ++i) {
+    const int64_t tiles = tm * ((N + widths[i] - 1) / widths[i]);
+    const int64_t waves = (tiles + workers - 1) / workers;
+    const double cost = (double)waves * widths[i] / eff[i];
+    if (i == 0 || cost < best_cost * (1.0 - 1e-9)) {
+      best = widths[i];
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
 int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
               const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
               uint32_t xcd_mask, hipStream_t stream) {
@@ -202,7 +226,10 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   }
   if (total == 0) return fail(ASYM_EINVAL, "gemm: the CU set is empty");
 
-  const int tiles_m = (M + BMr - 1) / BMr, tiles_n = (N + BNr - 1) / BNr;
+  const bool vec = aligned16(A) && aligned16(B) && (((uintptr_t)C & 7u) == 0) && (K % 8 == 0) &&
+                   (lda % 8 == 0) && (ldb % 8 == 0) && (ldc % 4 == 0);
+  const int bn = vec ? choose_tile_width(M, N, total) : (int)BNr;
+  const int tiles_m = (M + BMr - 1) / BMr, tiles_n = (N + bn - 1) / bn;
   const DeviceSchedule* ds = nullptr;
   rc = upload_schedule(device, tiles_m, tiles_n, mapping, slots, &ds);
   if (rc != ASYM_OK) return rc;
@@ -226,8 +253,8 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   g.dynamic = false;
   for (int x = 0; x < t->n_xccs; ++x)
     if (per[x] < smax) g.dynamic = true;
-  g.vec = aligned16(A) && aligned16(B) && (((uintptr_t)C & 7u) == 0) && (K % 8 == 0) &&
-          (lda % 8 == 0) && (ldb % 8 == 0) && (ldc % 4 == 0);
+  g.vec = vec;
+  g.bn = bn;
   return launch_gemm(g, stream);
 }
 

@@ -225,9 +225,12 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
 // ---- vector path: direct-to-LDS four-slot ring ---------------------------------
 constexpr int KS = 64;                 // k per stage: one 128-byte line of every row
 constexpr int SLOTS = 2;
-constexpr int SLOT_BYTES = 65536;      // A (256 rows x 128 B) then B (256 rows x 128 B)
-constexpr int RING_BYTES = SLOTS * SLOT_BYTES;
 constexpr int ROW_BYTES = KS * 2;
+constexpr int A_BYTES = BM * ROW_BYTES;                 // a slot's A part (32 KiB)
+// A slot holds A (256 rows) then B (16 * nbf * 2 rows, nbf = 16-column B
+// fragments per wave: 8, 7 or 6 for 256-, 224- and 192-wide tiles).
+template <int NBF> constexpr int slot_bytes() { return A_BYTES + 32 * NBF * ROW_BYTES; }
+constexpr int RING_BYTES = SLOTS * (A_BYTES + 32 * 8 * ROW_BYTES);  // the widest tile
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -278,14 +281,22 @@ template <int OFF>
 __device__ __forceinline__ void lds_read_frag(bf16x8& f, uint32_t addr) {
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(f) : "v"(addr), "i"(OFF) : "memory");
 }
+// A fragments G .. 7 (after the last B group of a tile narrower than 256)
+template <int G>
+__device__ __forceinline__ void lds_read_frags_from(bf16x8 (&f)[8], uint32_t addr) {
+  if constexpr (G < 8) {
+    lds_read_frag<G * 2048>(f[G], addr);
+    lds_read_frags_from<G + 1>(f, addr);
+  }
+}
 
 struct RingCtx {
   i32x4 rsa, rsb;
   uint32_t voa[2], vob[2];  // per-lane offsets for even / odd 8-row blocks
   uint32_t dst_a, dst_b;
-  int row_a[8], row_b[8];   // byte offsets of the wave's eight 8-row blocks
+  int row_a[8], row_b[8];   // byte offsets of the wave's 8-row blocks
   int K;
-  int lchunk[2];            // the lane's logical chunk for even / odd blocks
+  int lca[2], lcb[2];       // the lane's logical chunk for even / odd blocks of A, B
 };
 
 // The workgroup's next tile.  Static assignment: positions i, i + step,
@@ -341,48 +352,58 @@ __device__ __forceinline__ StageOffsets stage_offsets(const RingCtx& c, int t) {
   StageOffsets o;
 #pragma unroll
   for (int par = 0; par < 2; ++par) {
-    const bool in_k = k0 + c.lchunk[par] * 8 < c.K;
-    o.a[par] = in_k ? c.voa[par] : kOOB;
-    o.b[par] = in_k ? c.vob[par] : kOOB;
+    o.a[par] = k0 + c.lca[par] * 8 < c.K ? c.voa[par] : kOOB;
+    o.b[par] = k0 + c.lcb[par] * 8 < c.K ? c.vob[par] : kOOB;
   }
   return o;
 }
 
-// j-th of the 16 loads of stage t into slot t % SLOTS: j < 8 are A's, j >= 8
-// B's; each wave owns rows w*64 .. w*64+63 of both operands, load i covering
-// rows w*64 + 8i .. +7.  The LDS address and the row/k offset are uniform
+// j-th of the 8 + NBF loads of stage t into slot t % SLOTS: j < 8 are A's,
+// the rest B's; each wave owns 64 rows of A and 8 * NBF rows of B, load i
+// covering 8 of them.  The LDS address and the row/k offset are uniform
 // (scalar registers); stages past the end of K read zeros or go unused.
+template <int NBF>
 __device__ __forceinline__ void ring_load(const RingCtx& c, const StageOffsets& o, int t, int j) {
   const int kb = __builtin_amdgcn_readfirstlane(t * KS * 2);
-  const uint32_t slot = (uint32_t)(t & (SLOTS - 1)) * SLOT_BYTES;
-  const int i = j & 7, par = i & 1;
+  const uint32_t slot = (uint32_t)(t & (SLOTS - 1)) * slot_bytes<NBF>();
   if (j < 8)
-    dma_1k(c.dst_a + slot + i * 1024, c.rsa, o.a[par], c.row_a[i], kb);
+    dma_1k(c.dst_a + slot + j * 1024, c.rsa, o.a[j & 1], c.row_a[j], kb);
   else
-    dma_1k(c.dst_b + slot + i * 1024, c.rsb, o.b[par], c.row_b[i], kb);
+    dma_1k(c.dst_b + slot + (j - 8) * 1024, c.rsb, o.b[(j - 8) & 1], c.row_b[j - 8], kb);
 }
 
-// One group of a half-stage (32 of the stage's 64 k): with LOADS, issue loads
-// 2G and 2G+1 of stage t+2 first (spread over the 8 groups, the loads keep the
-// MFMAs fed better than in bursts); run the 8 MFMAs that use B
-// fragment G; then read the next half-stage's A fragment G into `an` and its B
-// fragment G into `b` (B fragment G has no later use in this half-stage, so it
-// is replaced in place; the A fragments feed every group and are double
-// buffered).  `sa`/`sb` are the LDS addresses of the next half-stage's
-// fragment 0.
-template <int G, bool LOADS>
+// One group of a half-stage (32 of the stage's 64 k): the 8 MFMAs that use B
+// fragment G, with the group's other work spread between them: with LOADS,
+// the group's share of stage t+2's loads (the first before the MFMAs, the rest
+// after the first four), then the next half-stage's A fragment G (for G < 8)
+// into `an`, and after the last four MFMAs its B fragment G into `b` (B
+// fragment G has no later use in this half-stage, so it is replaced in place;
+// the A fragments feed every group and are double buffered).  Spreading the
+// loads and reads keeps the MFMAs fed better than bursts do.  `sa`/`sb` are
+// the LDS addresses of the next half-stage's fragment 0.
+template <int NBF, int G, bool LOADS>
 __device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets& o, int t,
-                                           f32x4 (&acc)[8][8], const bf16x8 (&ac)[8],
-                                           bf16x8 (&an)[8], bf16x8 (&b)[8], uint32_t sa, uint32_t sb) {
-  if constexpr (LOADS) {
-    ring_load(c, o, t + SLOTS, 2 * G);
-    ring_load(c, o, t + SLOTS, 2 * G + 1);
-  }
+                                           f32x4 (&acc)[NBF][8], const bf16x8 (&ac)[8],
+                                           bf16x8 (&an)[8], bf16x8 (&b)[NBF], uint32_t sa,
+                                           uint32_t sb) {
+  constexpr int L = 8 + NBF, lo = G * L / NBF, hi = (G + 1) * L / NBF;
+  if constexpr (LOADS) ring_load<NBF>(c, o, t + SLOTS, lo);
 #pragma unroll
-  for (int mb = 0; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
-  lds_read_frag<G * 2048>(an[G], sa);
+  for (int mb = 0; mb < 4; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
+  if constexpr (LOADS) {
+#pragma unroll
+    for (int j = lo + 1; j < hi; ++j) ring_load<NBF>(c, o, t + SLOTS, j);
+  }
+  if constexpr (G < 8) lds_read_frag<G * 2048>(an[G], sa);
+#pragma unroll
+  for (int mb = 4; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
   lds_read_frag<G * 2048>(b[G], sb);
-  if constexpr (G + 1 < 8) ring_group<G + 1, LOADS>(c, o, t, acc, ac, an, b, sa, sb);
+  if constexpr (G + 1 == NBF) {
+    // fewer B fragments than A fragments: read the remaining A fragments
+    lds_read_frags_from<NBF>(an, sa);
+  } else {
+    ring_group<NBF, G + 1, LOADS>(c, o, t, acc, ac, an, b, sa, sb);
+  }
 }
 
 // Stage t in two halves, branch-free.  First half (k 0..31): its fragments
@@ -392,21 +413,24 @@ __device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets&
 // also tells every wave that slot t has been read completely), refill slot t
 // with stage t+2 while computing, and read the first half of stage t+1.  Every
 // instruction is inline asm, so the issue order is the program order.
-__device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)[8][8],
-                                           bf16x8 (&a0)[8], bf16x8 (&a1)[8], bf16x8 (&b)[8],
+template <int NBF>
+__device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)[NBF][8],
+                                           bf16x8 (&a0)[8], bf16x8 (&a1)[8], bf16x8 (&b)[NBF],
                                            const uint32_t (&ra)[2], const uint32_t (&rb)[2]) {
-  const uint32_t s0 = (uint32_t)(t & (SLOTS - 1)) * SLOT_BYTES;
-  const uint32_t s1 = (uint32_t)((t + 1) & (SLOTS - 1)) * SLOT_BYTES;
+  const uint32_t s0 = (uint32_t)(t & (SLOTS - 1)) * slot_bytes<NBF>();
+  const uint32_t s1 = (uint32_t)((t + 1) & (SLOTS - 1)) * slot_bytes<NBF>();
   const StageOffsets o = stage_offsets(c, t + SLOTS);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  ring_group<0, false>(c, o, t, acc, a0, a1, b, ra[1] + s0, rb[1] + s0);
+  ring_group<NBF, 0, false>(c, o, t, acc, a0, a1, b, ra[1] + s0, rb[1] + s0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   lds_barrier();
-  ring_group<0, true>(c, o, t, acc, a1, a0, b, ra[0] + s1, rb[0] + s1);
+  ring_group<NBF, 0, true>(c, o, t, acc, a1, a0, b, ra[0] + s1, rb[0] + s1);
 }
 
+template <int NBF>
 __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, unsigned char* lds,
                                                   NextTile& nt) {
+  constexpr int WNT = 16 * NBF, BNT = 2 * WNT;  // per-wave and per-tile B width
   // Everything the tile needs passes through an opaque move first, so that no
   // per-lane setup is hoisted out of the tile loop and kept live (and spilled)
   // across the k-loop; recomputing it per tile costs a few instructions.
@@ -422,35 +446,40 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   p.M = __builtin_amdgcn_readfirstlane(p.M);
   p.N = __builtin_amdgcn_readfirstlane(p.N);
   const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * BM, n0 = tn * BNT;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int KT = (p.K + KS - 1) / KS;
 
-  f32x4 acc[8][8];
+  f32x4 acc[NBF][8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < NBF; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   mfma_fence();
-  const int rows_a = min(BM, p.M - m0), rows_b = min(BN, p.N - n0);
+  const int rows_a = min(BM, p.M - m0), rows_b = min(BNT, p.N - n0);
   const i32x4 rsa = rsrc_words(p.A + (size_t)m0 * p.lda, (uint32_t)rows_a * p.lda * 2u);
   const i32x4 rsb = rsrc_words(p.B + (size_t)n0 * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
   // load side: lane -> (row in its 8-row block, physical chunk L%8); the
   // logical chunk stored there is the physical one XOR (row/2)%8, which for a
-  // row w*64 + 8i + r is (r/2) | 4*(i%2): one offset for even blocks, one for odd
+  // row 8b + r (b the block's index in the tile) is (r/2) | 4*(b%2): one
+  // offset for even blocks, one for odd.  A wave's A blocks start at block
+  // 8w (even); its B blocks start at block NBF*w, odd for odd NBF and w.
   const int lrow = lane >> 3;
-  int lchunk[2], voa[2], vob[2];
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int bsw = (wv * NBF) & 1;
+  int lca[2], lcb[2], voa[2], vob[2];
 #pragma unroll
   for (int par = 0; par < 2; ++par) {
-    lchunk[par] = (lane & 7) ^ ((lrow >> 1) | (par << 2));
-    voa[par] = ((wave * 64 + lrow) * p.lda + lchunk[par] * 8) * 2;
-    vob[par] = ((wave * 64 + lrow) * p.ldb + lchunk[par] * 8) * 2;
+    lca[par] = (lane & 7) ^ ((lrow >> 1) | (par << 2));
+    lcb[par] = (lane & 7) ^ ((lrow >> 1) | ((par ^ bsw) << 2));
+    voa[par] = ((wv * 64 + lrow) * p.lda + lca[par] * 8) * 2;
+    vob[par] = ((wv * 8 * NBF + lrow) * p.ldb + lcb[par] * 8) * 2;
   }
   const uint32_t lds0 = (uint32_t)(size_t)lds;
-  const uint32_t dst_a = __builtin_amdgcn_readfirstlane(lds0 + wave * 64 * ROW_BYTES);
-  const uint32_t dst_b = __builtin_amdgcn_readfirstlane(lds0 + SLOT_BYTES / 2 + wave * 64 * ROW_BYTES);
+  const uint32_t dst_a = __builtin_amdgcn_readfirstlane(lds0 + wv * 64 * ROW_BYTES);
+  const uint32_t dst_b = __builtin_amdgcn_readfirstlane(lds0 + A_BYTES + wv * 8 * NBF * ROW_BYTES);
   // read side: lane -> row l%16 of a 16-row block, logical chunk l/16 (+4 for
   // the second half-stage), stored at that chunk XOR (row/2)%8: conflict-free
   // 16-byte reads across every 16 lanes
@@ -460,11 +489,11 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   for (int h = 0; h < 2; ++h) {
     const int pchunk = ((lane >> 4) | (h << 2)) ^ ((rrow >> 1) & 7);
     ra[h] = lds0 + (uint32_t)((wm * 128 + rrow) * ROW_BYTES + pchunk * 16);
-    rb[h] = lds0 + (uint32_t)(SLOT_BYTES / 2 + (wn * 128 + rrow) * ROW_BYTES + pchunk * 16);
+    rb[h] = lds0 + (uint32_t)(A_BYTES + (wn * WNT + rrow) * ROW_BYTES + pchunk * 16);
   }
 
   RingCtx c{rsa, rsb, {(uint32_t)voa[0], (uint32_t)voa[1]}, {(uint32_t)vob[0], (uint32_t)vob[1]},
-            dst_a, dst_b, {}, {}, p.K, {lchunk[0], lchunk[1]}};
+            dst_a, dst_b, {}, {}, p.K, {lca[0], lca[1]}, {lcb[0], lcb[1]}};
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     c.row_a[i] = __builtin_amdgcn_readfirstlane(8 * i * p.lda * 2);
@@ -476,20 +505,18 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   for (int t = 0; t < SLOTS; ++t) {
     const StageOffsets o = stage_offsets(c, t);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) ring_load(c, o, t, j);
+    for (int j = 0; j < 8 + NBF; ++j) ring_load<NBF>(c, o, t, j);
   }
-  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(8 + NBF) : "memory");
   lds_barrier();
-  bf16x8 a0[8], a1[8], bf[8];
-  lds_read_frag<0>(a0[0], ra[0]); lds_read_frag<2048>(a0[1], ra[0]);
-  lds_read_frag<4096>(a0[2], ra[0]); lds_read_frag<6144>(a0[3], ra[0]);
-  lds_read_frag<8192>(a0[4], ra[0]); lds_read_frag<10240>(a0[5], ra[0]);
-  lds_read_frag<12288>(a0[6], ra[0]); lds_read_frag<14336>(a0[7], ra[0]);
+  bf16x8 a0[8], a1[8], bf[NBF];
+  lds_read_frags_from<0>(a0, ra[0]);
   lds_read_frag<0>(bf[0], rb[0]); lds_read_frag<2048>(bf[1], rb[0]);
   lds_read_frag<4096>(bf[2], rb[0]); lds_read_frag<6144>(bf[3], rb[0]);
   lds_read_frag<8192>(bf[4], rb[0]); lds_read_frag<10240>(bf[5], rb[0]);
-  lds_read_frag<12288>(bf[6], rb[0]); lds_read_frag<14336>(bf[7], rb[0]);
-  for (int t = 0; t < KT; ++t) ring_stage(c, t, acc, a0, a1, bf, ra, rb);
+  if constexpr (NBF > 6) lds_read_frag<12288>(bf[6 % NBF], rb[0]);
+  if constexpr (NBF > 7) lds_read_frag<14336>(bf[7 % NBF], rb[0]);
+  for (int t = 0; t < KT; ++t) ring_stage<NBF>(c, t, acc, a0, a1, bf, ra, rb);
   // drain the loads still in flight (zero fills past K) before the slots
   // are reused, and make sure every wave is past its last LDS read
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -506,10 +533,10 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   int ldc = p.ldc, nN = p.N, lid = lane;
   const int rows_c = min(BM, p.M - m0);
   const __amdgpu_buffer_rsrc_t rsc = make_rsrc(p.C + (size_t)m0 * ldc + n0, (uint32_t)rows_c * ldc * 2u);
-  const int ncol = wn * WN + (lid >> 4) * 4;  // lane's first column within the tile
+  const int ncol = wn * WNT + (lid >> 4) * 4;  // lane's first column within the tile
   const uint32_t vc = (uint32_t)((wm * WM + (lid & 15)) * ldc + ncol) * 2u;
 #pragma unroll
-  for (int nb = 0; nb < 8; ++nb) {
+  for (int nb = 0; nb < NBF; ++nb) {
     const int n = n0 + ncol + nb * 16;
     // keep this block's accumulators in AGPRs up to here, so that they are
     // copied to VGPRs one block at a time (not all 256 at the loop exit)
@@ -563,10 +590,10 @@ __device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane)
   return -1;
 }
 
-template <bool VEC>
+template <bool VEC, int NBF>
 __device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned char* lds, NextTile& nt) {
   if constexpr (VEC) {
-    compute_tile_ring(p, tile, lds, nt);
+    compute_tile_ring<NBF>(p, tile, lds, nt);
   } else {
     compute_tile<false>(p, tile, reinterpret_cast<uint16_t*>(lds),
                         reinterpret_cast<uint16_t*>(lds) + 2 * BM * LDP);
@@ -576,7 +603,7 @@ __device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned cha
 
 constexpr int LDS_BYTES = RING_BYTES > 2 * (BM + BN) * LDP * 2 ? RING_BYTES : 2 * (BM + BN) * LDP * 2;
 
-template <bool VEC>
+template <bool VEC, int NBF>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 gemm_bf16_persistent(Params p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[VEC ? RING_BYTES : 2 * (BM + BN) * LDP * 2];
@@ -654,7 +681,7 @@ gemm_bf16_persistent(Params p) {
   }
   while (tile >= 0) {
     nt.i_next += nt.step;
-    run_tile<VEC>(p, tile, lds, nt);
+    run_tile<VEC, NBF>(p, tile, lds, nt);
     if (threadIdx.x < 64) {
       const int nxt = take_next(p, nt, xcc, q_lane);
       if (lane == 0) s_info[1] = nxt;
@@ -687,10 +714,16 @@ int launch_gemm(const GemmLaunch& g, hipStream_t s) {
   p.n_xccs = g.n_xccs;
   p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots; p.ctr = g.d_ctr;
   p.dynamic = g.dynamic ? 1 : 0;
-  if (g.vec)
-    hipLaunchKernelGGL(gemm_bf16_persistent<true>, dim3(g.grid), dim3(NT), 0, s, p);
+  if (!g.vec)
+    hipLaunchKernelGGL((gemm_bf16_persistent<false, 8>), dim3(g.grid), dim3(NT), 0, s, p);
+  else if (g.bn == 256)
+    hipLaunchKernelGGL((gemm_bf16_persistent<true, 8>), dim3(g.grid), dim3(NT), 0, s, p);
+  else if (g.bn == 224)
+    hipLaunchKernelGGL((gemm_bf16_persistent<true, 7>), dim3(g.grid), dim3(NT), 0, s, p);
+  else if (g.bn == 192)
+    hipLaunchKernelGGL((gemm_bf16_persistent<true, 6>), dim3(g.grid), dim3(NT), 0, s, p);
   else
-    hipLaunchKernelGGL(gemm_bf16_persistent<false>, dim3(g.grid), dim3(NT), 0, s, p);
+    return fail(ASYM_EINVAL, "gemm: unsupported tile width");
   ASYM_HIP(hipGetLastError());
   return ASYM_OK;
 }

@@ -82,6 +82,7 @@ struct GemmLaunch {
   int tiles_m, tiles_n;
   int n_xccs;
   bool vec;                    // aligned vector path
+  int bn;                      // tile width: 256, or 224 / 192 on the vector path
 };
 int launch_gemm(const GemmLaunch& g, hipStream_t s);
 
