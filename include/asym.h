@@ -321,6 +321,32 @@ int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K,
                    int b_layout, void* C, int ldc, int mapping,
                    uint32_t xcd_mask, void* stream);
 
+/* What asym_gemm_bf16 with the same arguments would launch, without
+ * launching it or touching the matrices: the same checks and errors, the
+ * output tile (tile_m x tile_n; the width is taken from 256, 224 and 192 to
+ * minimise the rounds of tiles the persistent workers run, Section 7.1's wave
+ * quantization), the tile grid, the workgroups launched and the workers that
+ * take tiles, per XCD and in all.  claims = 1 when the aware mapping hands
+ * tiles out through per-XCD counters (CU sets with unequal XCD counts),
+ * 0 when every worker walks a fixed list.  vector_path = 1 for 16-byte loads
+ * into LDS, 0 for the predicated path.  Synchronous, host only.
+ * Errors: as asym_gemm_bf16. */
+typedef struct asym_gemm_plan_info {
+  int tile_m, tile_n;
+  int tiles_m, tiles_n;
+  int grid;
+  int workers;
+  int claims;
+  int vector_path;
+  int n_xcds;
+  int workers_per_xcd[ASYM_MAX_XCDS];
+} asym_gemm_plan_info;
+
+int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
+                   const void* A, int lda, const void* B, int ldb,
+                   int b_layout, const void* C, int ldc, int mapping,
+                   uint32_t xcd_mask, void* stream, asym_gemm_plan_info* out);
+
 /* ---- streaming copy and co-run (Sections 7.2, 7.3) ---------------------- */
 /* dst[i] = src[i] for n_bytes bytes (16-byte aligned, n_bytes a multiple of
  * 16), `passes` times over the buffer, with 16-byte accesses from every lane.

@@ -39,7 +39,7 @@ EXPORTS = (
     "asym_dispatch_check", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_gemm_bf16",
-    "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
+    "asym_gemm_plan", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
 
@@ -100,6 +100,19 @@ class Task(ctypes.Structure):
                 ("n_bytes", ctypes.c_size_t)]
 
 
+class GemmPlanInfo(ctypes.Structure):
+    _fields_ = [("tile_m", ctypes.c_int), ("tile_n", ctypes.c_int),
+                ("tiles_m", ctypes.c_int), ("tiles_n", ctypes.c_int),
+                ("grid", ctypes.c_int), ("workers", ctypes.c_int),
+                ("claims", ctypes.c_int), ("vector_path", ctypes.c_int),
+                ("n_xcds", ctypes.c_int), ("workers_per_xcd", ctypes.c_int * MAX_XCDS)]
+
+    def to_dict(self) -> dict:
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "workers_per_xcd"}
+        d["workers_per_xcd"] = list(self.workers_per_xcd)[:self.n_xcds]
+        return d
+
+
 class TaskResult(ctypes.Structure):
     _fields_ = [("ms_total", ctypes.c_double), ("ms_per_iter", ctypes.c_double),
                 ("tflops", ctypes.c_double), ("gbps", ctypes.c_double),
@@ -144,6 +157,8 @@ def load_library(path: str = LIB_PATH):
         "asym_stream_destroy": (i, [vp]),
         "asym_schedule_build": (i, [i, i, i, ip, i, i, ip, ip, ip]),
         "asym_gemm_bf16": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp]),
+        "asym_gemm_plan": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp,
+                               ctypes.POINTER(GemmPlanInfo)]),
         "asym_copy_bf16": (i, [vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
         "asym_corun": (i, [topo_p, ctypes.POINTER(Task), i, ctypes.POINTER(TaskResult)]),
         "asym_last_error": (cp, []),
@@ -400,6 +415,34 @@ def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mas
         ctypes.c_void_p(B.data_ptr()), B.stride(0), B_NK, ctypes.c_void_p(C.data_ptr()),
         C.stride(0), mp, xcd_mask, _stream_ptr(stream)))
     return C
+
+
+def gemm_plan(A=None, B=None, C=None, mapping="aware", topo: Optional[Topology] = None,
+              xcd_mask: int = 0, stream=None, M: Optional[int] = None, N: Optional[int] = None,
+              K: Optional[int] = None) -> dict:
+    """What gemm() would launch for these operands (or, given M, N, K alone,
+    for dense 256-byte-aligned operands of that shape): tile shape and grid,
+    workers in all and per XCD, static or claiming aware form, vector or
+    predicated path.  Launches nothing."""
+    if A is not None:
+        M, K = A.shape
+        N = B.shape[0]
+        pa, lda = A.data_ptr(), A.stride(0)
+        pb, ldb = B.data_ptr(), B.stride(0)
+        if C is not None:
+            pc, ldc = C.data_ptr(), C.stride(0)
+        else:
+            pc, ldc = 256, N
+    else:
+        if M is None or N is None or K is None:
+            raise ValueError("give A and B, or M, N and K")
+        pa, lda, pb, ldb, pc, ldc = 256, K, 256, K, 256, N
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    out = GemmPlanInfo()
+    _check(load_library().asym_gemm_plan(
+        topo.handle if topo else None, M, N, K, ctypes.c_void_p(pa), lda, ctypes.c_void_p(pb),
+        ldb, B_NK, ctypes.c_void_p(pc), ldc, mp, xcd_mask, _stream_ptr(stream), ctypes.byref(out)))
+    return out.to_dict()
 
 
 # ---- copy and co-run --------------------------------------------------------------

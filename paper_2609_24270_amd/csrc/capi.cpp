@@ -173,9 +173,21 @@ static int choose_tile_width(int M, int N, int workers) {
   return best;
 }
 
-int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
-              const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
-              uint32_t xcd_mask, hipStream_t stream) {
+// Everything a launch decides before it touches the device: arguments checked,
+// the CU set read off the stream, the tile width and the aware form chosen.
+// Called with g_mu held.
+struct GemmPlan {
+  const Topology* t = nullptr;
+  int device = 0;
+  std::vector<int> per, slots;
+  int total = 0, smax = 0;
+  bool vec = false, dynamic = false;
+  int bn = 0, tiles_m = 0, tiles_n = 0, grid = 0;
+};
+
+static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
+                     const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
+                     uint32_t xcd_mask, hipStream_t stream, GemmPlan* P) {
   if (M < 1 || N < 1 || K < 1) return fail(ASYM_EINVAL, "gemm: M, N, K must be >= 1");
   if (!A || !B || !C) return fail(ASYM_EINVAL, "gemm: null matrix pointer");
   if (lda < K || ldc < N) return fail(ASYM_EINVAL, "gemm: leading dimension too small");
@@ -191,7 +203,6 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
       (int64_t)BMr * ldc * 2 >= (1ll << 31))
     return fail(ASYM_EUNSUPPORTED, "gemm: leading dimension too large for 32-bit tile offsets");
 
-  std::lock_guard<std::mutex> lock(g_mu);
   int device = 0;
   int rc = current_device(&device);
   if (rc != ASYM_OK) return rc;
@@ -228,13 +239,39 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
 
   const bool vec = aligned16(A) && aligned16(B) && (((uintptr_t)C & 7u) == 0) && (K % 8 == 0) &&
                    (lda % 8 == 0) && (ldb % 8 == 0) && (ldc % 4 == 0);
-  const int bn = vec ? choose_tile_width(M, N, total) : (int)BNr;
-  const int tiles_m = (M + BMr - 1) / BMr, tiles_n = (N + bn - 1) / bn;
+  P->t = t;
+  P->device = device;
+  P->total = total;
+  P->smax = smax;
+  P->vec = vec;
+  P->bn = vec ? choose_tile_width(M, N, total) : (int)BNr;
+  P->tiles_m = (int)((M + BMr - 1) / BMr);
+  P->tiles_n = (N + P->bn - 1) / P->bn;
+  P->grid = mapping == ASYM_MAP_AWARE ? t->n_xccs * smax : total;
+  // The aware grid deals smax workgroups to every XCD.  Where an XCD has fewer
+  // CUs in the stream's set, the surplus there waits for a CU and holds up the
+  // dispatch behind it, so the static assignment (which needs every worker to
+  // run) gives way to claims.
+  P->dynamic = false;
+  for (int x = 0; x < t->n_xccs; ++x)
+    if (per[x] < smax) P->dynamic = true;
+  P->per = std::move(per);
+  P->slots = std::move(slots);
+  return ASYM_OK;
+}
+
+int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
+              const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
+              uint32_t xcd_mask, hipStream_t stream) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  GemmPlan P;
+  int rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
+  if (rc != ASYM_OK) return rc;
   const DeviceSchedule* ds = nullptr;
-  rc = upload_schedule(device, tiles_m, tiles_n, mapping, slots, &ds);
+  rc = upload_schedule(P.device, P.tiles_m, P.tiles_n, mapping, P.slots, &ds);
   if (rc != ASYM_OK) return rc;
   Workspace* ws = nullptr;
-  rc = get_workspace(device, stream, &ws);
+  rc = get_workspace(P.device, stream, &ws);
   if (rc != ASYM_OK) return rc;
 
   GemmLaunch g;
@@ -242,20 +279,36 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
   g.mapping = mapping;
   g.d_order = ds->d_order; g.d_off = ds->d_off; g.d_slots = ds->d_slots;
-  g.tiles_m = tiles_m; g.tiles_n = tiles_n;
-  g.n_xccs = t->n_xccs;
-  g.grid = mapping == ASYM_MAP_AWARE ? t->n_xccs * smax : total;
+  g.tiles_m = P.tiles_m; g.tiles_n = P.tiles_n;
+  g.n_xccs = P.t->n_xccs;
+  g.grid = P.grid;
   g.d_ctr = ws->gemm_ctr;
-  // The aware grid deals smax workgroups to every XCD.  Where an XCD has fewer
-  // CUs in the stream's set, the surplus there waits for a CU and holds up the
-  // dispatch behind it, so the static assignment (which needs every worker to
-  // run) gives way to claims.
-  g.dynamic = false;
-  for (int x = 0; x < t->n_xccs; ++x)
-    if (per[x] < smax) g.dynamic = true;
-  g.vec = vec;
-  g.bn = bn;
+  g.dynamic = P.dynamic;
+  g.vec = P.vec;
+  g.bn = P.bn;
   return launch_gemm(g, stream);
+}
+
+int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
+              const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
+              uint32_t xcd_mask, hipStream_t stream, asym_gemm_plan_info* out) {
+  if (!out) return fail(ASYM_EINVAL, "gemm_plan: null output");
+  std::lock_guard<std::mutex> lock(g_mu);
+  GemmPlan P;
+  const int rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
+  if (rc != ASYM_OK) return rc;
+  *out = asym_gemm_plan_info{};
+  out->tile_m = gemm_tile_m();
+  out->tile_n = P.bn;
+  out->tiles_m = P.tiles_m;
+  out->tiles_n = P.tiles_n;
+  out->grid = P.grid;
+  out->workers = P.total;
+  out->claims = (mapping == ASYM_MAP_AWARE && P.dynamic) ? 1 : 0;
+  out->vector_path = P.vec ? 1 : 0;
+  out->n_xcds = P.t->n_xccs;
+  for (int x = 0; x < P.t->n_xccs && x < ASYM_MAX_XCDS; ++x) out->workers_per_xcd[x] = P.slots[x];
+  return ASYM_OK;
 }
 
 // Bytes moved by copies on stream s since the last call; clears the count.
@@ -317,6 +370,13 @@ extern "C" int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K, co
                               uint32_t xcd_mask, void* stream) {
   return asym::gemm_bf16(topo, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask,
                          static_cast<hipStream_t>(stream));
+}
+
+extern "C" int asym_gemm_plan(const asym_topology* topo, int M, int N, int K, const void* A, int lda,
+                              const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
+                              uint32_t xcd_mask, void* stream, asym_gemm_plan_info* out) {
+  return asym::gemm_plan(topo, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask,
+                         static_cast<hipStream_t>(stream), out);
 }
 
 extern "C" int asym_copy_bf16(void* dst, const void* src, size_t n_bytes, int passes,

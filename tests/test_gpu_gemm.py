@@ -136,3 +136,53 @@ def test_gemm_llm_shapes_sampled(dev, p):
     C = run(A.to(dev), B.to(dev), "aware")
     e = sampled_check(A, B, C, 128, 128, seed=3)
     print(f"{p.name} sampled max rel err {e:.3e}")
+
+
+# Tile widths: the launch takes 256, 224 or 192 columns per tile, whichever
+# leaves the persistent workers the fewest rounds of tiles.  With the aware
+# grid kept to XCD 0 (32 workers) and two tile rows, each width is the choice
+# for one of these shapes, every one with ragged M, N and K tails.
+WIDTH_CASES = [(256, 500, 4092, 328), (224, 500, 3548, 328), (192, 500, 700, 328)]
+
+
+@pytest.mark.parametrize("width,M,N,K", WIDTH_CASES, ids=lambda v: str(v))
+def test_gemm_tile_widths_elementwise(dev, width, M, N, K):
+    A, B = workloads.make_inputs(workloads.make_problem(M, N, K, seed=width + N))
+    Ad, Bd = A.to(dev), B.to(dev)
+    plan = asym.gemm_plan(Ad, Bd, mapping="aware", xcd_mask=1)
+    assert plan["tile_n"] == width and plan["vector_path"] == 1, plan
+    assert plan["workers"] == 32 and plan["workers_per_xcd"][1:] == [0] * 7, plan
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    C = run(Ad, Bd, "aware", xcd_mask=1)
+    e = assert_gemm_close(bits(C), R, what=f"width {width} {M}x{N}x{K}")
+    print(f"width {width} {M}x{N}x{K}: max rel err {e:.3e}")
+    # a different width over the whole chip gives the same bits
+    full = asym.gemm_plan(Ad, Bd, mapping="aware")
+    assert full["tile_n"] == 192 and full["workers"] == 256, full
+    assert torch.equal(run(Ad, Bd, "aware"), C)
+
+
+def test_gemm_plan_full_sizes(dev):
+    """The widths and forms the full-size workloads launch with."""
+    want = {(8192, 8192, 8192): 256, (4096, 14336, 4096): 224, (4096, 4096, 14336): 256,
+            (4096, 6144, 4096): 192}
+    for (M, N, K), w in want.items():
+        for m in MAPS:
+            p = asym.gemm_plan(mapping=m, M=M, N=N, K=K)
+            assert p["tile_m"] == 256 and p["tile_n"] == w, (M, N, K, m, p)
+            assert p["tiles_m"] == -(-M // 256) and p["tiles_n"] == -(-N // w)
+            assert p["workers"] == 256 and p["workers_per_xcd"] == [32] * 8
+            assert p["claims"] == 0
+            assert p["grid"] == 256
+    # the predicated path keeps the 256-wide tile
+    p = asym.gemm_plan(mapping="aware", M=300, N=700, K=150)
+    assert p["vector_path"] == 0 and p["tile_n"] == 256
+
+
+def test_gemm_plan_rejects_like_launch(dev):
+    with pytest.raises(asym.AsymError) as e:
+        asym.gemm_plan(M=0, N=8, K=8)
+    assert e.value.status == asym.EINVAL
+    with pytest.raises(asym.AsymError) as e:
+        asym.gemm_plan(mapping="oblivious_grouped", M=64, N=64, K=64, xcd_mask=1)
+    assert e.value.status == asym.EUNSUPPORTED
