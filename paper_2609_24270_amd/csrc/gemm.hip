@@ -427,6 +427,14 @@ __device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)
   ring_group<NBF, 0, true>(c, o, t, acc, a1, a0, b, ra[0] + s1, rb[0] + s1);
 }
 
+// An empty asm that redefines one column block's accumulators in AGPRs: the
+// values read after it exist only from here on, so their copies to VGPRs
+// cannot be scheduled above it (an input-only operand would leave the compiler
+// free to copy all 256 accumulators out at the loop exit, and spill).
+__device__ __forceinline__ void keep_agprs(f32x4 (&a)[8]) {
+  asm volatile("" : "+a"(a[0]), "+a"(a[1]), "+a"(a[2]), "+a"(a[3]), "+a"(a[4]), "+a"(a[5]), "+a"(a[6]), "+a"(a[7]));
+}
+
 template <int NBF>
 __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, unsigned char* lds,
                                                   NextTile& nt) {
@@ -525,43 +533,82 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   // every wave is past its last LDS read before the slots are reused
   lds_barrier();
 
-  // epilogue: lane holds C[m][n..n+3] for each (nb, mb) block.  The lane's
-  // own offset is one VGPR; the block's offset is uniform and goes in the
-  // scalar offset.  Rows past M fall outside the resource: stores dropped.
+  // epilogue.  In a 16x16 block the lane with row r = lane % 16 holds columns
+  // 4c .. 4c+3, c = lane / 16.  Blocks 2q and 2q+1 are paired by one
+  // v_permlane16_swap per packed word, after which lane (r, c) holds 8
+  // consecutive columns, 8 (c >> 1) .. +7 of block 2q + (c & 1): one 16-byte
+  // store per lane covers 16 rows x 32 columns, and the pairs of a 16-row block
+  // go out back to back, so every 128-byte line of C is written by four
+  // consecutive stores.  An odd last block (224-wide tiles) keeps the 8-byte
+  // layout.  Offsets: the lane's own one is a VGPR, the block's is uniform
+  // (scalar offset).  Rows past M fall outside the resource: stores dropped.
   // (the inputs pass through an opaque move so that nothing below is hoisted
   // out of the tile loop and kept live across the k-loop)
   int ldc = p.ldc, nN = p.N, lid = lane;
   const int rows_c = min(BM, p.M - m0);
   const __amdgpu_buffer_rsrc_t rsc = make_rsrc(p.C + (size_t)m0 * ldc + n0, (uint32_t)rows_c * ldc * 2u);
-  const int ncol = wn * WNT + (lid >> 4) * 4;  // lane's first column within the tile
-  const uint32_t vc = (uint32_t)((wm * WM + (lid & 15)) * ldc + ncol) * 2u;
+  // 16-byte stores need 16-byte aligned rows; otherwise two 8-byte halves
+  const bool c16 = (((uintptr_t)p.C & 15u) == 0) && ((ldc & 7) == 0);
+  const int r16 = lid & 15, c4 = lid >> 4;
+  const int pcol = wn * WNT + (c4 & 1) * 16 + (c4 >> 1) * 8;  // paired layout, first column
+  const uint32_t vp = (uint32_t)((wm * WM + r16) * ldc + pcol) * 2u;
 #pragma unroll
-  for (int nb = 0; nb < NBF; ++nb) {
-    const int n = n0 + ncol + nb * 16;
-    // keep this block's accumulators in AGPRs up to here, so that they are
-    // copied to VGPRs one block at a time (not all 256 at the loop exit)
-    asm volatile("" :: "a"(acc[nb][0]), "a"(acc[nb][1]), "a"(acc[nb][2]), "a"(acc[nb][3]),
-                 "a"(acc[nb][4]), "a"(acc[nb][5]), "a"(acc[nb][6]), "a"(acc[nb][7]));
+  for (int q = 0; q < NBF / 2; ++q) {
+    // keep this pair's accumulators in AGPRs up to here, so that they are
+    // copied to VGPRs one pair at a time (not all 256 at the loop exit)
+    keep_agprs(acc[2 * q]);
+    keep_agprs(acc[2 * q + 1]);
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const f32x4 v = acc[2 * q][mb], u = acc[2 * q + 1][mb];
+      uint32_t w0 = pack_bf16x2(v[0], v[1]), w1 = pack_bf16x2(v[2], v[3]);
+      uint32_t u0 = pack_bf16x2(u[0], u[1]), u1 = pack_bf16x2(u[2], u[3]);
+      const auto s0 = __builtin_amdgcn_permlane16_swap(w0, u0, false, false);
+      const auto s1 = __builtin_amdgcn_permlane16_swap(w1, u1, false, false);
+      w0 = s0[0]; u0 = s0[1];
+      w1 = s1[0]; u1 = s1[1];
+      const int col = n0 + pcol + 32 * q;
+      const int so = (mb * 16 * ldc + 32 * q) * 2;
+      if (col + 7 < nN) {
+        if (c16) {
+          __builtin_amdgcn_raw_buffer_store_b128(v4u{w0, w1, u0, u1}, rsc, vp, so, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b64(v2u{w0, w1}, rsc, vp, so, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(v2u{u0, u1}, rsc, vp + 8u, so, 0);
+        }
+      } else {
+        const uint32_t wd[4] = {w0, w1, u0, u1};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const unsigned short h = (unsigned short)(wd[e >> 1] >> (16 * (e & 1)));
+          __builtin_amdgcn_raw_buffer_store_b16(h, rsc, col + e < nN ? vp + 2u * e : kOOB, so, 0);
+        }
+      }
+    }
+    // one pair of column blocks at a time, so their VGPR copies stay few
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if constexpr (NBF & 1) {
+    constexpr int nb = NBF - 1;
+    keep_agprs(acc[nb]);
+    const int scol = wn * WNT + nb * 16 + c4 * 4;
+    const uint32_t vs = (uint32_t)((wm * WM + r16) * ldc + scol) * 2u;
+    const int n = n0 + scol;
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
       const f32x4 v = acc[nb][mb];
-      const int so = (mb * 16 * ldc + nb * 16) * 2;
+      const int so = mb * 16 * ldc * 2;
       if (n + 3 < nN) {
-        v2u w;
-        w.x = pack_bf16x2(v[0], v[1]);
-        w.y = pack_bf16x2(v[2], v[3]);
-        __builtin_amdgcn_raw_buffer_store_b64(w, rsc, vc, so, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(v2u{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])}, rsc, vs, so, 0);
       } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const __bf16 h = (__bf16)v[r];
           __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, h), rsc,
-                                                n + r < nN ? vc + 2u * r : kOOB, so, 0);
+                                                n + r < nN ? vs + 2u * r : kOOB, so, 0);
         }
       }
     }
-    // one column block of accumulators at a time, so their VGPR copies stay few
-    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
