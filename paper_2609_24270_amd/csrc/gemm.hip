@@ -222,15 +222,21 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
   }
 }
 
-// ---- vector path: direct-to-LDS four-slot ring ---------------------------------
+// ---- vector path: direct-to-LDS rings ---------------------------------------------
+// k advances in stages of 64.  A stage of A (256 rows) and one of B (16 * nbf * 2
+// rows, nbf = 16-column B fragments per wave: 8, 7 or 6 for 256-, 224- and
+// 192-wide tiles) each hold one 128-byte line of every row.  A has three ring
+// slots and B two: A's loads for stage t+2 go out during the first half of
+// stage t and B's during the second half, so the load path is busy evenly
+// instead of in bursts (a load that cannot issue holds up the MFMAs behind it).
+// 3 x 32 KiB + 2 x 32 KiB fill the 160 KiB of LDS at the 256-wide tile.
 constexpr int KS = 64;                 // k per stage: one 128-byte line of every row
-constexpr int SLOTS = 2;
+constexpr int A_SLOTS = 3, B_SLOTS = 2;
 constexpr int ROW_BYTES = KS * 2;
-constexpr int A_BYTES = BM * ROW_BYTES;                 // a slot's A part (32 KiB)
-// A slot holds A (256 rows) then B (16 * nbf * 2 rows, nbf = 16-column B
-// fragments per wave: 8, 7 or 6 for 256-, 224- and 192-wide tiles).
-template <int NBF> constexpr int slot_bytes() { return A_BYTES + 32 * NBF * ROW_BYTES; }
-constexpr int RING_BYTES = SLOTS * (A_BYTES + 32 * 8 * ROW_BYTES);  // the widest tile
+constexpr int A_BYTES = BM * ROW_BYTES;                 // one stage of A (32 KiB)
+constexpr int A_RING = A_SLOTS * A_BYTES;
+template <int NBF> constexpr int b_bytes() { return 32 * NBF * ROW_BYTES; }  // one stage of B
+constexpr int RING_BYTES = A_RING + B_SLOTS * b_bytes<8>();  // the widest tile
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -246,13 +252,14 @@ __device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
 // 32-wide k stage) reach barely 60% of this rate through the vector cache.
 // `row` (the row block's byte offset) and `kb` (the stage's k byte offset)
 // are added in the scalar unit inside the asm, so no part of the address
-// passes through vector registers.
+// passes through vector registers.  The add writes SCC, which the compiler
+// must not keep a value in across the asm (declared clobbered), and M0.
 __device__ __forceinline__ void dma_1k(uint32_t lds_dst, i32x4 rs, uint32_t vo, int row, int kb) {
   int so;
   asm volatile("s_add_u32 %0, %1, %2\n\ts_mov_b32 m0, %3\n\tbuffer_load_dwordx4 %4, %5, %0 offen lds"
                : "=&s"(so)
                : "s"(row), "s"(kb), "s"(lds_dst), "v"(vo), "s"(rs)
-               : "memory");
+               : "memory", "scc", "m0");
 }
 
 __device__ __forceinline__ void lds_barrier() {
@@ -358,42 +365,43 @@ __device__ __forceinline__ StageOffsets stage_offsets(const RingCtx& c, int t) {
   return o;
 }
 
-// j-th of the 8 + NBF loads of stage t into slot t % SLOTS: j < 8 are A's,
-// the rest B's; each wave owns 64 rows of A and 8 * NBF rows of B, load i
-// covering 8 of them.  The LDS address and the row/k offset are uniform
-// (scalar registers); stages past the end of K read zeros or go unused.
+// j-th of the 8 + NBF loads of stage t: j < 8 are A's, into A slot t % 3, the
+// rest B's, into B slot t % 2; each wave owns 64 rows of A and 8 * NBF rows of
+// B, load i covering 8 of them.  `sa_t` is A slot t's byte offset.  The LDS
+// address and the row/k offset are uniform (scalar registers); stages past
+// the end of K read zeros or go unused.
 template <int NBF>
-__device__ __forceinline__ void ring_load(const RingCtx& c, const StageOffsets& o, int t, int j) {
+__device__ __forceinline__ void ring_load(const RingCtx& c, const StageOffsets& o, int t, uint32_t sa_t,
+                                          int j) {
   const int kb = __builtin_amdgcn_readfirstlane(t * KS * 2);
-  const uint32_t slot = (uint32_t)(t & (SLOTS - 1)) * slot_bytes<NBF>();
   if (j < 8)
-    dma_1k(c.dst_a + slot + j * 1024, c.rsa, o.a[j & 1], c.row_a[j], kb);
+    dma_1k(c.dst_a + sa_t + j * 1024, c.rsa, o.a[j & 1], c.row_a[j], kb);
   else
-    dma_1k(c.dst_b + slot + (j - 8) * 1024, c.rsb, o.b[(j - 8) & 1], c.row_b[j - 8], kb);
+    dma_1k(c.dst_b + (uint32_t)(t & 1) * b_bytes<NBF>() + (j - 8) * 1024, c.rsb, o.b[(j - 8) & 1],
+           c.row_b[j - 8], kb);
 }
 
 // One group of a half-stage (32 of the stage's 64 k): the 8 MFMAs that use B
-// fragment G, with the group's other work spread between them: with LOADS,
-// the group's share of stage t+2's loads (the first before the MFMAs, the rest
-// after the first four), then the next half-stage's A fragment G (for G < 8)
-// into `an`, and after the last four MFMAs its B fragment G into `b` (B
-// fragment G has no later use in this half-stage, so it is replaced in place;
-// the A fragments feed every group and are double buffered).  Spreading the
-// loads and reads keeps the MFMAs fed better than bursts do.  `sa`/`sb` are
-// the LDS addresses of the next half-stage's fragment 0.
-template <int NBF, int G, bool LOADS>
-__device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets& o, int t,
+// fragment G, with the group's other work spread between them: the group's
+// share of stage t+2's loads (HALF 0: A's 8, HALF 1: B's NBF; the first before
+// the MFMAs, the rest after the first four), then the next half-stage's A
+// fragment G (for G < 8) into `an`, and after the last four MFMAs its B
+// fragment G into `b` (B fragment G has no later use in this half-stage, so it
+// is replaced in place; the A fragments feed every group and are double
+// buffered).  Spreading the loads and reads keeps the MFMAs fed better than
+// bursts do.  `sa`/`sb` are the LDS addresses of the next half-stage's
+// fragment 0; `sa2` is A slot (t+2)'s byte offset.
+template <int NBF, int G, int HALF>
+__device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets& o, int t, uint32_t sa2,
                                            f32x4 (&acc)[NBF][8], const bf16x8 (&ac)[8],
                                            bf16x8 (&an)[8], bf16x8 (&b)[NBF], uint32_t sa,
                                            uint32_t sb) {
-  constexpr int L = 8 + NBF, lo = G * L / NBF, hi = (G + 1) * L / NBF;
-  if constexpr (LOADS) ring_load<NBF>(c, o, t + SLOTS, lo);
+  constexpr int lo = HALF == 0 ? G * 8 / NBF : 8 + G, hi = HALF == 0 ? (G + 1) * 8 / NBF : 9 + G;
+  if constexpr (lo < hi) ring_load<NBF>(c, o, t + 2, sa2, lo);
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
-  if constexpr (LOADS) {
 #pragma unroll
-    for (int j = lo + 1; j < hi; ++j) ring_load<NBF>(c, o, t + SLOTS, j);
-  }
+  for (int j = lo + 1; j < hi; ++j) ring_load<NBF>(c, o, t + 2, sa2, j);
   if constexpr (G < 8) lds_read_frag<G * 2048>(an[G], sa);
 #pragma unroll
   for (int mb = 4; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
@@ -402,29 +410,34 @@ __device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets&
     // fewer B fragments than A fragments: read the remaining A fragments
     lds_read_frags_from<NBF>(an, sa);
   } else {
-    ring_group<NBF, G + 1, LOADS>(c, o, t, acc, ac, an, b, sa, sb);
+    ring_group<NBF, G + 1, HALF>(c, o, t, sa2, acc, ac, an, b, sa, sb);
   }
 }
 
 // Stage t in two halves, branch-free.  First half (k 0..31): its fragments
-// were read during the previous half; wait for those reads, compute, and read
-// the second half's fragments from slot t.  Second half (k 32..63): wait for
-// this wave's loads of stage t+1, publish slot t+1 to all waves (the barrier
-// also tells every wave that slot t has been read completely), refill slot t
-// with stage t+2 while computing, and read the first half of stage t+1.  Every
+// were read during the previous half; wait for those reads, compute, load A of
+// stage t+2 into A slot (t+2) % 3 (last read in the first half of stage t-1,
+// which every wave has left: the barrier of stage t-1), and read the second
+// half's fragments from the slots of stage t.  Second half (k 32..63): wait
+// for this wave's loads of stage t+1 (all but the 8 A loads just issued; loads
+// complete in order), publish stage t+1 to all waves (the barrier also tells
+// every wave that B slot t % 2 has been read completely), load B of stage t+2
+// into it while computing, and read the first half of stage t+1.  Every
 // instruction is inline asm, so the issue order is the program order.
+// `sa` holds A slot offsets of stages t, t+1, t+2.
 template <int NBF>
-__device__ __forceinline__ void ring_stage(const RingCtx& c, int t, f32x4 (&acc)[NBF][8],
-                                           bf16x8 (&a0)[8], bf16x8 (&a1)[8], bf16x8 (&b)[NBF],
-                                           const uint32_t (&ra)[2], const uint32_t (&rb)[2]) {
-  const uint32_t s0 = (uint32_t)(t & (SLOTS - 1)) * slot_bytes<NBF>();
-  const uint32_t s1 = (uint32_t)((t + 1) & (SLOTS - 1)) * slot_bytes<NBF>();
-  const StageOffsets o = stage_offsets(c, t + SLOTS);
+__device__ __forceinline__ void ring_stage(const RingCtx& c, int t, const uint32_t (&sa)[3],
+                                           f32x4 (&acc)[NBF][8], bf16x8 (&a0)[8], bf16x8 (&a1)[8],
+                                           bf16x8 (&b)[NBF], const uint32_t (&ra)[2],
+                                           const uint32_t (&rb)[2]) {
+  const uint32_t sb0 = (uint32_t)(t & 1) * b_bytes<NBF>();
+  const uint32_t sb1 = (uint32_t)((t + 1) & 1) * b_bytes<NBF>();
+  const StageOffsets o = stage_offsets(c, t + 2);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  ring_group<NBF, 0, false>(c, o, t, acc, a0, a1, b, ra[1] + s0, rb[1] + s0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  ring_group<NBF, 0, 0>(c, o, t, sa[2], acc, a0, a1, b, ra[1] + sa[0], rb[1] + sb0);
+  asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
   lds_barrier();
-  ring_group<NBF, 0, true>(c, o, t, acc, a1, a0, b, ra[0] + s1, rb[0] + s1);
+  ring_group<NBF, 0, 1>(c, o, t, sa[2], acc, a1, a0, b, ra[0] + sa[1], rb[0] + sb1);
 }
 
 // An empty asm that redefines one column block's accumulators in AGPRs: the
@@ -487,7 +500,7 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   }
   const uint32_t lds0 = (uint32_t)(size_t)lds;
   const uint32_t dst_a = __builtin_amdgcn_readfirstlane(lds0 + wv * 64 * ROW_BYTES);
-  const uint32_t dst_b = __builtin_amdgcn_readfirstlane(lds0 + A_BYTES + wv * 8 * NBF * ROW_BYTES);
+  const uint32_t dst_b = __builtin_amdgcn_readfirstlane(lds0 + A_RING + wv * 8 * NBF * ROW_BYTES);
   // read side: lane -> row l%16 of a 16-row block, logical chunk l/16 (+4 for
   // the second half-stage), stored at that chunk XOR (row/2)%8: conflict-free
   // 16-byte reads across every 16 lanes
@@ -497,7 +510,7 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   for (int h = 0; h < 2; ++h) {
     const int pchunk = ((lane >> 4) | (h << 2)) ^ ((rrow >> 1) & 7);
     ra[h] = lds0 + (uint32_t)((wm * 128 + rrow) * ROW_BYTES + pchunk * 16);
-    rb[h] = lds0 + (uint32_t)(A_BYTES + (wn * WNT + rrow) * ROW_BYTES + pchunk * 16);
+    rb[h] = lds0 + (uint32_t)(A_RING + (wn * WNT + rrow) * ROW_BYTES + pchunk * 16);
   }
 
   RingCtx c{rsa, rsb, {(uint32_t)voa[0], (uint32_t)voa[1]}, {(uint32_t)vob[0], (uint32_t)vob[1]},
@@ -510,10 +523,10 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   // prologue: stages 0 and 1 in flight (a stage past K loads zeros); stage 0
   // published and its first half's fragments read
 #pragma unroll
-  for (int t = 0; t < SLOTS; ++t) {
+  for (int t = 0; t < 2; ++t) {
     const StageOffsets o = stage_offsets(c, t);
 #pragma unroll
-    for (int j = 0; j < 8 + NBF; ++j) ring_load<NBF>(c, o, t, j);
+    for (int j = 0; j < 8 + NBF; ++j) ring_load<NBF>(c, o, t, (uint32_t)t * A_BYTES, j);
   }
   asm volatile("s_waitcnt vmcnt(%0)" :: "n"(8 + NBF) : "memory");
   lds_barrier();
@@ -524,7 +537,15 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   lds_read_frag<8192>(bf[4], rb[0]); lds_read_frag<10240>(bf[5], rb[0]);
   if constexpr (NBF > 6) lds_read_frag<12288>(bf[6 % NBF], rb[0]);
   if constexpr (NBF > 7) lds_read_frag<14336>(bf[7 % NBF], rb[0]);
-  for (int t = 0; t < KT; ++t) ring_stage<NBF>(c, t, acc, a0, a1, bf, ra, rb);
+  // A slot offsets of stages t, t+1, t+2 (uniform, rotated each stage)
+  uint32_t sa[3] = {0u, (uint32_t)A_BYTES, 2u * A_BYTES};
+  for (int t = 0; t < KT; ++t) {
+    ring_stage<NBF>(c, t, sa, acc, a0, a1, bf, ra, rb);
+    const uint32_t s0 = sa[0];
+    sa[0] = sa[1];
+    sa[1] = sa[2];
+    sa[2] = s0;
+  }
   // drain the loads still in flight (zero fills past K) before the slots
   // are reused, and make sure every wave is past its last LDS read
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -648,13 +669,22 @@ __device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned cha
   }
 }
 
-constexpr int LDS_BYTES = RING_BYTES > 2 * (BM + BN) * LDP * 2 ? RING_BYTES : 2 * (BM + BN) * LDP * 2;
+// Wave 0's value in box[0] (the first word of LDS) to every wave.  Between
+// tiles no load into LDS is in flight and no wave reads it, so the word is
+// free; the second barrier keeps the next tile's loads from overwriting it
+// before every wave has read it.
+__device__ __forceinline__ int read_box(const int* box) {
+  __syncthreads();
+  const int v = __builtin_amdgcn_readfirstlane(box[0]);
+  __syncthreads();
+  return v;
+}
 
 template <bool VEC, int NBF>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 gemm_bf16_persistent(Params p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[VEC ? RING_BYTES : 2 * (BM + BN) * LDP * 2];
-  __shared__ int s_info[2];
+  int* const box = reinterpret_cast<int*>(lds);  // tile broadcast, used between tiles only
 
   // Static aware assignment: workgroup b belongs to XCD b mod n and is that
   // XCD's (b / n)-th persistent worker (the hardware deals workgroups to XCDs
@@ -719,10 +749,9 @@ gemm_bf16_persistent(Params p) {
         first = idx < nt.own_q ? __builtin_amdgcn_readfirstlane(p.order[nt.own_off + idx])
                                : steal_aware(p, xcc, q_lane);
       }
-      if (lane == 0) s_info[1] = first;
+      if (lane == 0) box[0] = first;
     }
-    __syncthreads();
-    tile = __builtin_amdgcn_readfirstlane(s_info[1]);
+    tile = read_box(box);
   } else {
     tile = nt.i_next < nt.end ? __builtin_amdgcn_readfirstlane(p.order[nt.i_next]) : -1;
   }
@@ -731,10 +760,9 @@ gemm_bf16_persistent(Params p) {
     run_tile<VEC, NBF>(p, tile, lds, nt);
     if (threadIdx.x < 64) {
       const int nxt = take_next(p, nt, xcc, q_lane);
-      if (lane == 0) s_info[1] = nxt;
+      if (lane == 0) box[0] = nxt;
     }
-    __syncthreads();
-    tile = __builtin_amdgcn_readfirstlane(s_info[1]);
+    tile = read_box(box);
   }
   if (dyn && threadIdx.x == 0) {
     // the last workgroup to leave resets the counters for the next launch

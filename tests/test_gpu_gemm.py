@@ -186,3 +186,32 @@ def test_gemm_plan_rejects_like_launch(dev):
     with pytest.raises(asym.AsymError) as e:
         asym.gemm_plan(mapping="oblivious_grouped", M=64, N=64, K=64, xcd_mask=1)
     assert e.value.status == asym.EUNSUPPORTED
+
+
+# k-stage isolation: with A (or B) zero outside one 64-wide k stage, C is that
+# stage's product alone, so a stage read from the wrong ring slot, or data
+# landing in the wrong slot, shows up as a wrong stage.  Small integers make
+# the fp32 sums exact, so the output must equal the oracle's bit for bit.
+# Each tile width, with stage counts that are not multiples of the ring's
+# three A slots; XCD 0 only (32 workers) so that the widths are the chosen ones.
+STAGE_CASES = [(256, 500, 4092, 7), (224, 500, 3548, 5), (192, 500, 700, 8)]
+
+
+@pytest.mark.parametrize("width,M,N,KT", STAGE_CASES, ids=lambda v: str(v))
+def test_gemm_ring_stage_isolation(dev, width, M, N, KT):
+    K = 64 * KT
+    g = np.random.default_rng(width + KT)
+    A = g.integers(-3, 4, size=(M, K)).astype(np.float32)
+    B = g.integers(-3, 4, size=(N, K)).astype(np.float32)
+    assert asym.gemm_plan(M=M, N=N, K=K, xcd_mask=1)["tile_n"] == width
+    for which in ("A", "B"):
+        for s in range(KT):
+            a, b = A.copy(), B.copy()
+            x = a if which == "A" else b
+            x[:, :64 * s] = 0
+            x[:, 64 * s + 64:] = 0
+            ta = torch.tensor(a, dtype=torch.bfloat16)
+            tb = torch.tensor(b, dtype=torch.bfloat16)
+            _, ref = oracle.gemm_bf16(bits(ta), bits(tb), "nk")
+            C = run(ta.to(dev), tb.to(dev), "aware", xcd_mask=1)
+            assert np.array_equal(bits(C), ref), f"width {width}: {which} stage {s} of {KT}"
