@@ -546,11 +546,13 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
     sa[1] = sa[2];
     sa[2] = s0;
   }
-  // drain the loads still in flight (zero fills past K) before the slots
-  // are reused, and make sure every wave is past its last LDS read
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // Right after the k-loop, in one asm statement (nothing the compiler places
+  // after the loop can come before it): drain the loads still in flight (zero
+  // fills past K) before the slots are reused, let this wave's last fragment
+  // reads land, and give the last MFMAs their wait states before anything
+  // reads the accumulators.
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
   issue_next(nt);
-  mfma_fence();
   // every wave is past its last LDS read before the slots are reused
   lds_barrier();
 

@@ -194,7 +194,11 @@ def test_gemm_plan_rejects_like_launch(dev):
 # the fp32 sums exact, so the output must equal the oracle's bit for bit.
 # Each tile width, with stage counts that are not multiples of the ring's
 # three A slots; XCD 0 only (32 workers) so that the widths are the chosen ones.
-STAGE_CASES = [(256, 500, 4092, 7), (224, 500, 3548, 5), (192, 500, 700, 8)]
+# The last three give each of the 32 workgroups two tiles (the rings run on
+# from one tile into the next), with K of 7 stages, of 2 (the fewest that run
+# on) and of 1 (each tile starts with its own prologue).
+STAGE_CASES = [(256, 500, 4092, 7), (224, 500, 3548, 5), (192, 500, 700, 8),
+               (256, 1000, 4092, 7), (256, 1000, 4092, 2), (256, 1000, 4092, 1)]
 
 
 @pytest.mark.parametrize("width,M,N,KT", STAGE_CASES, ids=lambda v: str(v))

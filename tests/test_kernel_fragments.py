@@ -1,0 +1,215 @@
+"""In-flight fragment registers in the compiled GEMM (CPU only: hipcc -S for gfx950).
+
+The ring's MFMA fragments are read from LDS by inline-asm ds_read_b128: the
+compiler does not know that the destination registers are written later, when
+the read completes, and the kernel's own `s_waitcnt lgkmcnt(0)` is the wait.
+If the compiler copies, reads or reuses such a register before that wait
+(for instance to reconcile register assignments where two paths join), the
+copy takes the stale value and the product is wrong; this went wrong once
+when a loop body got two paths.  The test runs a dataflow pass over the
+control-flow graph of each vector-path kernel and requires that no
+instruction touches a fragment register between the read that fills it and
+the next lgkmcnt(0).  The accumulators have the same problem with the
+inline-asm MFMAs that write them: reading them needs the wait states of the
+kernel's MFMA fence (`s_nop 7` x 3), which the compiler does not know about, so
+no instruction the compiler places may touch an accumulator register between
+an MFMA and the fence.
+"""
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2609_24270_amd", "csrc")
+
+_VREG = re.compile(r"\bv(?:\[(\d+):(\d+)\]|(\d+)\b)")
+# instructions whose first operand is read, not written
+_NO_DEST = re.compile(r"^(buffer_store|global_store|flat_store|scratch_store|ds_write|ds_store|"
+                      r"buffer_load\w*.*\blds\b|s_\w+|v_cmpx)")
+
+
+def _vregs(text: str):
+    out = set()
+    for m in _VREG.finditer(text):
+        if m.group(3) is not None:
+            out.add(int(m.group(3)))
+        else:
+            out.update(range(int(m.group(1)), int(m.group(2)) + 1))
+    return out
+
+
+def _split(inst: str):
+    """(mnemonic, written VGPRs, read VGPRs) of one instruction."""
+    inst = inst.split(";")[0].strip()
+    parts = inst.split(None, 1)
+    mn = parts[0]
+    ops = parts[1] if len(parts) > 1 else ""
+    args = [a.strip() for a in ops.split(",")]
+    if _NO_DEST.match(inst) or not args or not args[0]:
+        return mn, set(), _vregs(ops)
+    dst, srcs = args[0], ",".join(args[1:])
+    reads = _vregs(srcs)
+    writes = _vregs(dst)
+    if mn.startswith(("v_permlane16_swap", "v_permlane32_swap", "v_writelane")):
+        reads |= writes  # swaps and lane writes also read their first operand
+    return mn, writes, reads
+
+
+def blocks_of(asm: str, kernel: str):
+    lines = asm.splitlines()
+    start = next(i for i, l in enumerate(lines) if re.match(r"^" + re.escape(kernel) + r":", l))
+    end = next(i for i in range(start, len(lines)) if lines[i].startswith(".Lfunc_end"))
+    blocks, cur, in_asm = [], {"label": None, "insts": []}, False
+    for l in lines[start + 1:end]:
+        st = l.strip()
+        m = re.match(r"^(\.LBB\d+_\d+):", st)
+        if m or re.match(r"^; %bb\.\d+:", st):
+            if cur["insts"] or cur["label"]:
+                blocks.append(cur)
+            cur = {"label": m.group(1) if m else None, "insts": []}
+            continue
+        if st.startswith(";;#ASMSTART"):
+            in_asm = True
+            continue
+        if st.startswith(";;#ASMEND"):
+            in_asm = False
+            continue
+        if not st or st.startswith(";") or st.startswith("."):
+            continue
+        for piece in st.split("\n"):
+            cur["insts"].append((piece.strip(), in_asm))
+    blocks.append(cur)
+    return blocks
+
+
+def successors(blocks):
+    label_at = {b["label"]: i for i, b in enumerate(blocks) if b["label"]}
+    succ = []
+    for i, b in enumerate(blocks):
+        last = b["insts"][-1][0] if b["insts"] else ""
+        m = re.match(r"^s_(c?branch\w*)\s+(\.LBB\d+_\d+)", last)
+        s = []
+        if last.startswith("s_endpgm"):
+            pass
+        elif m and m.group(1) == "branch":
+            s = [label_at[m.group(2)]]
+        elif m:
+            s = [label_at[m.group(2)]] + ([i + 1] if i + 1 < len(blocks) else [])
+        elif i + 1 < len(blocks):
+            s = [i + 1]
+        succ.append(s)
+    return succ
+
+
+_AGPR_TOUCH = re.compile(r"^v_accvgpr_(read|write|mov)")
+
+
+def transfer(block, state, violations=None):
+    """state: (VGPRs whose fragment read is in flight, MFMA results pending)."""
+    cur, mfma = set(state[0]), state[1]
+    nops = 0
+    for inst, is_asm in block["insts"]:
+        mn, writes, reads = _split(inst)
+        if is_asm and mn == "s_nop" and inst.split()[-1] == "7":
+            nops += 1
+            if nops >= 3:
+                mfma = False
+            continue
+        nops = 0
+        if mn == "s_waitcnt":
+            m = re.search(r"lgkmcnt\((\d+)\)", inst)
+            if m and int(m.group(1)) == 0:
+                cur.clear()
+            continue
+        if is_asm and mn == "ds_read_b128":
+            cur |= writes
+            continue
+        if is_asm and mn.startswith("v_mfma"):
+            mfma = True
+        elif mfma and not is_asm and _AGPR_TOUCH.match(mn) and violations is not None:
+            violations.append((block["label"], inst, "accumulator touched before the MFMA fence"))
+        bad = (reads | writes) & cur
+        if bad and violations is not None:
+            violations.append((block["label"], inst, sorted(bad)))
+    return cur, mfma
+
+
+def inflight_violations(asm: str, kernel: str):
+    blocks = blocks_of(asm, kernel)
+    succ = successors(blocks)
+    ins = [(set(), False) for _ in blocks]
+    changed = True
+    while changed:
+        changed = False
+        for i, b in enumerate(blocks):
+            out = transfer(b, ins[i])
+            for j in succ[i]:
+                merged = (ins[j][0] | out[0], ins[j][1] or out[1])
+                if merged != ins[j]:
+                    ins[j] = merged
+                    changed = True
+    v = []
+    for i, b in enumerate(blocks):
+        transfer(b, ins[i], v)
+    return v
+
+
+@pytest.fixture(scope="module")
+def gemm_asm(tmp_path_factory):
+    out = tmp_path_factory.mktemp("asm") / "gemm.s"
+    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"),
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+           "--cuda-device-only", "-S", os.path.join(CSRC, "gemm.hip"), "-o", str(out)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    return out.read_text()
+
+
+@pytest.mark.parametrize("nbf", [8, 7, 6])
+def test_no_use_of_fragments_in_flight(gemm_asm, nbf):
+    kernel = f"_ZN4asym12_GLOBAL__N_120gemm_bf16_persistentILb1ELi{nbf}EEEvNS0_6ParamsE"
+    v = inflight_violations(gemm_asm, kernel)
+    assert not v, f"{len(v)} instructions touch fragment registers still being read, e.g. {v[:4]}"
+
+
+def test_checker_sees_a_planted_copy():
+    """The pass flags a copy of a register whose read is in flight, across a
+    branch, and accepts the same code with the wait in between."""
+    bad = """k:
+\t;;#ASMSTART
+\tds_read_b128 v[10:13], v1 offset:0
+\t;;#ASMEND
+\ts_cbranch_scc1 .LBB0_2
+.LBB0_1:
+\tv_mov_b64_e32 v[20:21], v[12:13]
+.LBB0_2:
+\t;;#ASMSTART
+\ts_waitcnt lgkmcnt(0)
+\t;;#ASMEND
+\ts_endpgm
+.Lfunc_end0:
+"""
+    v = inflight_violations(bad, "k")
+    assert len(v) == 1 and v[0][2] == [12, 13]
+    # an accumulator read between an MFMA and the fence is flagged; after it, not
+    mf = """k:
+\t;;#ASMSTART
+\tv_mfma_f32_16x16x32_bf16 a[0:3], v[0:3], v[4:7], a[0:3]
+\t;;#ASMEND
+\tv_accvgpr_read_b32 v9, a1
+\t;;#ASMSTART
+\ts_nop 7
+\ts_nop 7
+\ts_nop 7
+\t;;#ASMEND
+\tv_accvgpr_read_b32 v8, a0
+\ts_endpgm
+.Lfunc_end0:
+"""
+    v = inflight_violations(mf, "k")
+    assert len(v) == 1 and "v9" in v[0][1]
+    good = bad.replace("\ts_cbranch_scc1 .LBB0_2\n", "\ts_waitcnt lgkmcnt(0)\n\ts_cbranch_scc1 .LBB0_2\n")
+    assert inflight_violations(good, "k") == []
