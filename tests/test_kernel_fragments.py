@@ -213,3 +213,44 @@ def test_checker_sees_a_planted_copy():
     assert len(v) == 1 and "v9" in v[0][1]
     good = bad.replace("\ts_cbranch_scc1 .LBB0_2\n", "\ts_waitcnt lgkmcnt(0)\n\ts_cbranch_scc1 .LBB0_2\n")
     assert inflight_violations(good, "k") == []
+
+
+# Scalar ALU instructions that write SCC (the add/sub/logic/shift/compare
+# families); an inline asm that contains one must declare SCC clobbered, or
+# the compiler may keep a live compare result in SCC across it.  (A missing
+# clobber once turned a uniform select after a load into a select on the
+# load's carry: the wrong B slot, wrong products.)
+_SCC_WRITERS = re.compile(r"\bs_(add|addc|sub|subb|and|or|xor|andn2|orn2|nand|nor|xnor|lshl|lshr|ashr|bfe|"
+                          r"min|max|cmp|bitcmp|abs|not)\w*\b")
+
+
+def _asm_statements(src: str):
+    """(template text, clobber text) of each `asm volatile(...)` / `asm(...)`."""
+    out = []
+    for m in re.finditer(r"\basm\s+(?:volatile\s*)?\(", src):
+        i, depth = m.end(), 1
+        while depth:
+            depth += {"(": 1, ")": -1}.get(src[i], 0)
+            i += 1
+        body = src[m.end():i - 1]
+        parts = re.split(r"(?<!:):(?!:)", body)
+        template = "".join(re.findall(r'"((?:[^"\\]|\\.)*)"', parts[0]))
+        clobbers = parts[3] if len(parts) > 3 else ""
+        out.append((template, clobbers))
+    return out
+
+
+@pytest.mark.parametrize("src", sorted(f for f in os.listdir(CSRC) if f.endswith(".hip")))
+def test_asm_that_writes_scc_declares_it(src):
+    text = open(os.path.join(CSRC, src)).read()
+    bad = [t for t, clob in _asm_statements(text) if _SCC_WRITERS.search(t) and '"scc"' not in clob]
+    assert not bad, f"{src}: asm writing SCC without an scc clobber: {bad}"
+
+
+def test_scc_rule_sees_a_missing_clobber():
+    src = 'asm volatile("s_add_u32 %0, %1, %2" : "=s"(x) : "s"(a), "s"(b) : "memory");\n' \
+          'asm volatile("s_add_u32 %0, %1, %2" : "=s"(x) : "s"(a), "s"(b) : "memory", "scc");\n' \
+          'asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");\n'
+    st = _asm_statements(src)
+    flagged = [t for t, c in st if _SCC_WRITERS.search(t) and '"scc"' not in c]
+    assert len(st) == 3 and len(flagged) == 1
