@@ -302,6 +302,20 @@ int asym_schedule_build(int tiles_m, int tiles_n, int n_xcds,
                         const int* slots, int mapping, int band, int* order,
                         int* off, int* quota);
 
+/* Grouped form of the tile schedule (the expert layer of mixture-of-experts
+ * models, to which Section 7.1 applies the same recipe): group g has
+ * tiles_m[g] >= 0 tile rows of tiles_n columns; tile ids number the tiles in
+ * group order, row-major inside a group (base_g + r * tiles_n + c).  Each group
+ * is one band, walked column by column, top to bottom.  AWARE shares every
+ * group out among the XCDs in contiguous runs of its walk, largest-remainder
+ * lengths by slots[x], ties to the lower XCD; XCD x's list is its runs, group
+ * after group.  OBLIVIOUS_GROUPED: the walk; OBLIVIOUS_ROWMAJOR: ids in order;
+ * both with off/quota as in asym_schedule_build.  order receives
+ * sum(tiles_m) * tiles_n ids.  Errors: ASYM_EINVAL. */
+int asym_grouped_schedule_build(int G, const int* tiles_m, int tiles_n, int n_xcds,
+                                const int* slots, int mapping, int* order, int* off,
+                                int* quota);
+
 /* ---- persistent bf16 GEMM (Section 7.1) --------------------------------- */
 /* C = A . B, bf16 inputs, fp32 accumulation, bf16 round-to-nearest-even
  * output.  A: [M][lda] row-major.  B: ASYM_B_NK, [N][ldb] row-major (the
@@ -320,6 +334,26 @@ int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K,
                    const void* A, int lda, const void* B, int ldb,
                    int b_layout, void* C, int ldc, int mapping,
                    uint32_t xcd_mask, void* stream);
+
+/* Grouped GEMM, one launch (Section 7.1 applies the persistent, partition-
+ * aware recipe to grouped GEMM, the mixture-of-experts expert layer): for each
+ * group g = 0 .. G-1, C_g = A_g . B_g with the numerics of asym_gemm_bf16.
+ * M: host array of G row counts (>= 0; zero-row groups are skipped).  A:
+ * the groups' rows packed in group order, [sum M][lda]; group g's rows start
+ * at row M_0 + ... + M_(g-1).  B: the groups' weights, each stored [N][K] as
+ * in ASYM_B_NK, one after the other: [G * N][ldb], group g's at row g * N.
+ * C: packed like A, [sum M][ldc].  Tiles never cross a group boundary; rows
+ * of other groups are neither read nor written by a group's tiles.  The tile
+ * schedule is asym_grouped_schedule_build's, over the stream's CU set as in
+ * asym_gemm_bf16; the tile table and schedule are rebuilt on the host and
+ * copied to the device on `stream` at every call (the library keeps the
+ * device buffers per stream).  Bitwise identical across mappings and CU sets.
+ * Asynchronous on `stream`.  Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED,
+ * ASYM_EHIP. */
+int asym_gemm_grouped_bf16(const asym_topology* topo, int G, const int* M, int N, int K,
+                           const void* A, int lda, const void* B, int ldb,
+                           void* C, int ldc, int mapping, uint32_t xcd_mask,
+                           void* stream);
 
 /* What asym_gemm_bf16 with the same arguments would launch, without
  * launching it or touching the matrices: the same checks and errors, the

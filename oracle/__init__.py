@@ -9,6 +9,8 @@ Contents
   gemm_bf16          plain C GEMM, fp32 k-ordered accumulation, bf16 RNE output
                      (the full-GPU kernel case of Section 7.1 computes this
                      product; placement changes only who computes each tile)
+  grouped_gemm_bf16  one gemm_bf16 per group of packed rows (the grouped GEMM
+                     of Section 7.1, the mixture-of-experts expert layer)
   f32_to_bf16        the oracle's own round-to-nearest-even conversion
   schedule           per-partition work quotas proportional to compute units
                      (Section 7.1 and the full-GPU lesson of Section 7.4)
@@ -99,6 +101,33 @@ def gemm_bf16(A_bits: np.ndarray, B_bits: np.ndarray, b_layout: str = "nk",
         _u16(C))
     if rc != 0:
         raise RuntimeError("oracle_gemm_bf16 failed")
+    return R, C
+
+
+def grouped_gemm_bf16(A_bits: np.ndarray, B_bits: np.ndarray, M, want_r32: bool = True):
+    """Grouped GEMM, by definition one gemm_bf16 per group.
+
+    A_bits: uint16 [sum(M), K], the groups' rows packed in group order.
+    B_bits: uint16 [G, N, K], group g's weights stored [N, K].
+    M:      the G row counts (>= 0).
+    Returns (R32 float32 [sum(M), N] or None, C uint16 [sum(M), N]), packed
+    like A: group g's rows start at M[0] + ... + M[g-1].
+    """
+    A = np.asarray(A_bits, dtype=np.uint16)
+    B = np.asarray(B_bits, dtype=np.uint16)
+    G, N, K = B.shape
+    if len(M) != G or A.shape != (sum(M), K):
+        raise ValueError("A must be [sum(M), K] and B [len(M), N, K]")
+    R = np.zeros((A.shape[0], N), dtype=np.float32) if want_r32 else None
+    C = np.zeros((A.shape[0], N), dtype=np.uint16)
+    row = 0
+    for g, m in enumerate(M):
+        if m:
+            Rg, Cg = gemm_bf16(A[row:row + m], B[g], "nk", want_r32)
+            C[row:row + m] = Cg
+            if want_r32:
+                R[row:row + m] = Rg
+        row += m
     return R, C
 
 

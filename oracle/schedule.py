@@ -105,3 +105,48 @@ def band_cost_choice(tiles_m: int, s: int) -> int:
         if best is None or key < best[0]:
             best = (key, h)
     return best[1]
+
+
+# ---- grouped GEMM -------------------------------------------------------------
+# The same recipe applied to grouped GEMM (Section 7.1: the expert layer of
+# mixture-of-experts models).  Group g owns rows_g tile rows of tiles_n
+# columns.  A tile is named (g, r, c); the tiles are numbered group after
+# group, row-major inside a group.  Reading taken here: each group is one band
+# of the plain schedule, so the aware mapping shares every group out among the
+# partitions exactly as it shares out a band.
+
+def grouped_tile_ids(rows_per_group, tiles_n):
+    """(g, r, c) -> tile id, numbering groups in order, row-major inside each."""
+    ids, nxt = {}, 0
+    for g, rows in enumerate(rows_per_group):
+        for r in range(rows):
+            for c in range(tiles_n):
+                ids[(g, r, c)] = nxt
+                nxt += 1
+    return ids
+
+
+def grouped_walks(rows_per_group, tiles_n):
+    """One walk per group: column by column, each column top to bottom."""
+    ids = grouped_tile_ids(rows_per_group, tiles_n)
+    return [[ids[(g, r, c)] for c in range(tiles_n) for r in range(rows)]
+            for g, rows in enumerate(rows_per_group)]
+
+
+def grouped_aware_lists(rows_per_group, tiles_n, slots):
+    lists = [[] for _ in slots]
+    for walk in grouped_walks(rows_per_group, tiles_n):
+        if not walk:
+            continue
+        q = hamilton_quotas(len(walk), slots)
+        pos = 0
+        for x, qx in enumerate(q):
+            lists[x].extend(walk[pos:pos + qx])
+            pos += qx
+    return lists
+
+
+def grouped_oblivious_order(rows_per_group, tiles_n, grouped_walk: bool):
+    if grouped_walk:
+        return [t for walk in grouped_walks(rows_per_group, tiles_n) for t in walk]
+    return list(range(sum(rows_per_group) * tiles_n))

@@ -38,8 +38,8 @@ EXPORTS = (
     "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
     "asym_dispatch_check", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
-    "asym_stream_destroy", "asym_schedule_build", "asym_gemm_bf16",
-    "asym_gemm_plan", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
+    "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
+    "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_plan", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
 
@@ -157,6 +157,8 @@ def load_library(path: str = LIB_PATH):
         "asym_stream_destroy": (i, [vp]),
         "asym_schedule_build": (i, [i, i, i, ip, i, i, ip, ip, ip]),
         "asym_gemm_bf16": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp]),
+        "asym_grouped_schedule_build": (i, [i, ip, i, i, ip, i, ip, ip, ip]),
+        "asym_gemm_grouped_bf16": (i, [topo_p, i, ip, i, i, vp, i, vp, i, vp, i, i, u32, vp]),
         "asym_gemm_plan": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp,
                                ctypes.POINTER(GemmPlanInfo)]),
         "asym_copy_bf16": (i, [vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
@@ -363,6 +365,17 @@ def schedule_build(tiles_m: int, tiles_n: int, slots: Sequence[int], mapping: in
     return list(order), list(off), list(quota)
 
 
+def grouped_schedule_build(tiles_m: Sequence[int], tiles_n: int, slots: Sequence[int], mapping: int):
+    n_x = len(slots)
+    T = sum(tiles_m) * tiles_n
+    order = (ctypes.c_int * max(1, T))()
+    off = (ctypes.c_int * (n_x + 1))()
+    quota = (ctypes.c_int * n_x)()
+    _check(load_library().asym_grouped_schedule_build(len(tiles_m), _ints(tiles_m), tiles_n, n_x,
+                                                      _ints(slots), mapping, order, off, quota))
+    return list(order)[:T], list(off), list(quota)
+
+
 # ---- streams ---------------------------------------------------------------------
 
 def stream_create(topo: Optional[Topology] = None, mask: Optional[Sequence[int]] = None):
@@ -414,6 +427,51 @@ def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mas
         topo.handle if topo else None, M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0),
         ctypes.c_void_p(B.data_ptr()), B.stride(0), B_NK, ctypes.c_void_p(C.data_ptr()),
         C.stride(0), mp, xcd_mask, _stream_ptr(stream)))
+    return C
+
+
+def gemm_grouped(A, B, M: Sequence[int], C=None, mapping="aware", topo: Optional[Topology] = None,
+                 xcd_mask: int = 0, stream=None):
+    """Grouped GEMM: C_g = A_g . B_g^T for every group g, one launch.
+
+    A: bf16 CUDA tensor [sum(M), K], the groups' rows packed in group order.
+    B: bf16 CUDA tensor [G, N, K] (or [G * N, K]), group g's weights [N, K].
+    M: the G row counts.  Returns C [sum(M), N], packed like A.
+    """
+    import torch
+    G = len(M)
+    if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16:
+        raise TypeError("A and B must be bfloat16")
+    if not (A.is_cuda and B.is_cuda):
+        raise ValueError("A and B must be on the GPU")
+    if B.dim() == 3:
+        if B.shape[0] != G:
+            raise ValueError("B must be [G, N, K]")
+        N, K = B.shape[1], B.shape[2]
+        if not B.is_contiguous():
+            raise ValueError("B [G, N, K] must be contiguous")
+        ldb = K
+    elif B.dim() == 2:
+        if B.shape[0] % G:
+            raise ValueError("B [G * N, K]: rows not a multiple of G")
+        N, K = B.shape[0] // G, B.shape[1]
+        if B.stride(1) != 1:
+            raise ValueError("B must be K-contiguous")
+        ldb = B.stride(0)
+    else:
+        raise ValueError("B must be [G, N, K] or [G * N, K]")
+    rows = int(sum(M))
+    if A.dim() != 2 or A.shape[0] != rows or A.shape[1] != K or A.stride(1) != 1:
+        raise ValueError("A must be a K-contiguous [sum(M), K] tensor")
+    if C is None:
+        C = torch.empty((rows, N), dtype=torch.bfloat16, device=A.device)
+    if C.dtype != torch.bfloat16 or tuple(C.shape) != (rows, N) or C.stride(1) != 1:
+        raise ValueError("C must be a row-major bf16 [sum(M), N] tensor")
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    _check(load_library().asym_gemm_grouped_bf16(
+        topo.handle if topo else None, G, _ints([int(m) for m in M]), N, K,
+        ctypes.c_void_p(A.data_ptr()), max(A.stride(0), K), ctypes.c_void_p(B.data_ptr()), ldb,
+        ctypes.c_void_p(C.data_ptr()), max(C.stride(0), N), mp, xcd_mask, _stream_ptr(stream)))
     return C
 
 

@@ -60,6 +60,16 @@ std::map<ScheduleKey, DeviceSchedule> g_schedules;  // never freed: kernels may 
 struct Workspace {
   int* gemm_ctr = nullptr;                  // 64 ints (dynamic aware GEMM)
   unsigned long long* copy_ctr = nullptr;   // 4 words
+  // grouped GEMM: the tile table and schedule of the latest call on the
+  // stream (each call's copies are ordered after the previous call's kernel)
+  int4* g_desc = nullptr;
+  int* g_sched = nullptr;                   // order [cap], off [MAX_XCDS + 1], slots [MAX_XCDS]
+  int g_cap = 0;
+  // pinned host staging of the same, and an event recorded after the copies
+  // out of it: the next call waits for it before writing the staging again
+  void* g_host = nullptr;
+  hipEvent_t g_copied = nullptr;
+  bool g_pending = false;
 };
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
@@ -289,6 +299,115 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   return launch_gemm(g, stream);
 }
 
+int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N, int K, const void* A,
+                      int lda, const void* B, int ldb, void* C, int ldc, int mapping, uint32_t xcd_mask,
+                      hipStream_t stream) {
+  if (G < 1) return fail(ASYM_EINVAL, "grouped gemm: G must be >= 1");
+  if (!Ms) return fail(ASYM_EINVAL, "grouped gemm: null row counts");
+  int64_t rows = 0;
+  for (int g = 0; g < G; ++g) {
+    if (Ms[g] < 0) return fail(ASYM_EINVAL, "grouped gemm: negative row count");
+    rows += Ms[g];
+  }
+  if (rows > (1ll << 30)) return fail(ASYM_EINVAL, "grouped gemm: too many rows");
+  if ((int64_t)G * N > (1ll << 31) - 1) return fail(ASYM_EINVAL, "grouped gemm: G * N too large");
+  std::vector<int> tm(G);
+  int64_t trows = 0;
+  for (int g = 0; g < G; ++g) {
+    tm[g] = (Ms[g] + gemm_tile_m() - 1) / gemm_tile_m();
+    trows += tm[g];
+  }
+  if (rows == 0) {
+    // nothing to compute; A and C may be empty (null) buffers
+    if (N < 1 || K < 1) return fail(ASYM_EINVAL, "grouped gemm: N, K must be >= 1");
+    if (!B) return fail(ASYM_EINVAL, "grouped gemm: null weights");
+    if (mapping != ASYM_MAP_AWARE && mapping != ASYM_MAP_OBLIVIOUS_GROUPED &&
+        mapping != ASYM_MAP_OBLIVIOUS_ROWMAJOR)
+      return fail(ASYM_EINVAL, "grouped gemm: unknown mapping");
+    return ASYM_OK;
+  }
+  std::lock_guard<std::mutex> lock(g_mu);
+  // the checks, CU set, path and tile width of a GEMM with as many tile rows
+  // (the weights: G * N rows of B)
+  GemmPlan P;
+  const int virt_m = (int)std::max<int64_t>(1, trows * gemm_tile_m());
+  int rc = plan_gemm(topo_in, virt_m, N, K, A, lda, B, ldb, ASYM_B_NK, C, ldc, mapping, xcd_mask, stream, &P);
+  if (rc != ASYM_OK) return rc;
+  const int tiles_n = (N + P.bn - 1) / P.bn;
+  Schedule sch;
+  rc = build_grouped_schedule(G, tm.data(), tiles_n, P.t->n_xccs, P.slots.data(), mapping, sch);
+  if (rc != ASYM_OK) return rc;
+  const int T = (int)sch.order.size();
+  std::vector<int4> desc(T);
+  {
+    int id = 0, row0 = 0;
+    for (int g = 0; g < G; ++g) {
+      for (int r = 0; r < tm[g]; ++r)
+        for (int c = 0; c < tiles_n; ++c)
+          desc[id++] = int4{row0 + r * gemm_tile_m(), std::min(gemm_tile_m(), Ms[g] - r * gemm_tile_m()),
+                            g * N, c * P.bn};
+      row0 += Ms[g];
+    }
+  }
+  Workspace* ws = nullptr;
+  rc = get_workspace(P.device, stream, &ws);
+  if (rc != ASYM_OK) return rc;
+  const size_t desc_bytes = (size_t)T * sizeof(int4);
+  const size_t sched_ints = (size_t)T + 2 * ASYM_MAX_XCDS + 1;
+  // the staging buffer is free once the previous call's copies have run
+  if (ws->g_pending) {
+    ASYM_HIP(hipEventSynchronize(ws->g_copied));
+    ws->g_pending = false;
+  }
+  if (ws->g_cap < T) {
+    // earlier launches on this stream may still read the old device buffers
+    ASYM_HIP(hipStreamSynchronize(stream));
+    if (ws->g_desc) ASYM_HIP(hipFree(ws->g_desc));
+    if (ws->g_sched) ASYM_HIP(hipFree(ws->g_sched));
+    if (ws->g_host) ASYM_HIP(hipHostFree(ws->g_host));
+    ws->g_desc = nullptr;
+    ws->g_sched = nullptr;
+    ws->g_host = nullptr;
+    ws->g_cap = 0;
+    const int cap = std::max(T, 1024);
+    const size_t bytes = (size_t)cap * sizeof(int4) + ((size_t)cap + 2 * ASYM_MAX_XCDS + 1) * sizeof(int);
+    ASYM_HIP(hipMalloc(&ws->g_desc, (size_t)cap * sizeof(int4)));
+    ASYM_HIP(hipMalloc(&ws->g_sched, ((size_t)cap + 2 * ASYM_MAX_XCDS + 1) * sizeof(int)));
+    ASYM_HIP(hipHostMalloc(&ws->g_host, bytes));
+    ws->g_cap = cap;
+  }
+  if (!ws->g_copied) ASYM_HIP(hipEventCreateWithFlags(&ws->g_copied, hipEventDisableTiming));
+  int4* h_desc = static_cast<int4*>(ws->g_host);
+  int* h_sched = reinterpret_cast<int*>(static_cast<char*>(ws->g_host) + (size_t)ws->g_cap * sizeof(int4));
+  std::copy(desc.begin(), desc.end(), h_desc);
+  std::fill(h_sched, h_sched + sched_ints, 0);
+  std::copy(sch.order.begin(), sch.order.end(), h_sched);
+  for (int x = 0; x <= P.t->n_xccs; ++x) h_sched[T + x] = sch.off[x];
+  for (int x = 0; x < P.t->n_xccs; ++x) h_sched[T + ASYM_MAX_XCDS + 1 + x] = P.slots[x];
+  ASYM_HIP(hipMemcpyAsync(ws->g_desc, h_desc, desc_bytes, hipMemcpyHostToDevice, stream));
+  ASYM_HIP(hipMemcpyAsync(ws->g_sched, h_sched, sched_ints * sizeof(int), hipMemcpyHostToDevice, stream));
+  ASYM_HIP(hipEventRecord(ws->g_copied, stream));
+  ws->g_pending = true;
+
+  GemmLaunch gl;
+  gl.A = A; gl.B = B; gl.C = C;
+  gl.M = virt_m; gl.N = N; gl.K = K; gl.lda = lda; gl.ldb = ldb; gl.ldc = ldc;
+  gl.mapping = mapping;
+  gl.d_order = ws->g_sched;
+  gl.d_off = ws->g_sched + T;
+  gl.d_slots = ws->g_sched + T + ASYM_MAX_XCDS + 1;
+  gl.tiles_m = (int)trows;
+  gl.tiles_n = tiles_n;
+  gl.n_xccs = P.t->n_xccs;
+  gl.grid = P.grid;
+  gl.d_ctr = ws->gemm_ctr;
+  gl.dynamic = P.dynamic;
+  gl.vec = P.vec;
+  gl.bn = P.bn;
+  gl.d_desc = ws->g_desc;
+  return launch_gemm(gl, stream);
+}
+
 int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
               const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
               uint32_t xcd_mask, hipStream_t stream, asym_gemm_plan_info* out) {
@@ -333,6 +452,10 @@ void release_workspace(hipStream_t s) {
     if (it->first.second == s) {
       hipFree(it->second.gemm_ctr);
       hipFree(it->second.copy_ctr);
+      if (it->second.g_desc) hipFree(it->second.g_desc);
+      if (it->second.g_sched) hipFree(it->second.g_sched);
+      if (it->second.g_host) hipHostFree(it->second.g_host);
+      if (it->second.g_copied) hipEventDestroy(it->second.g_copied);
       it = g_ws.erase(it);
     } else {
       ++it;
@@ -370,6 +493,13 @@ extern "C" int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K, co
                               uint32_t xcd_mask, void* stream) {
   return asym::gemm_bf16(topo, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask,
                          static_cast<hipStream_t>(stream));
+}
+
+extern "C" int asym_gemm_grouped_bf16(const asym_topology* topo, int G, const int* M, int N, int K,
+                                      const void* A, int lda, const void* B, int ldb, void* C, int ldc,
+                                      int mapping, uint32_t xcd_mask, void* stream) {
+  return asym::gemm_grouped_bf16(topo, G, M, N, K, A, lda, B, ldb, C, ldc, mapping, xcd_mask,
+                                 static_cast<hipStream_t>(stream));
 }
 
 extern "C" int asym_gemm_plan(const asym_topology* topo, int M, int N, int K, const void* A, int lda,

@@ -67,7 +67,35 @@ struct Params {
   const int* slots;  // [ASYM_MAX_XCDS]
   int* ctr;          // dynamic aware: [0,16) rank tickets, [16,32) tile counters, [32] exits
   int dynamic;       // aware mapping with claims instead of the static assignment
+  const int4* desc;  // grouped GEMM: per tile {first row, rows, group's first B row, first column}
 };
+
+// Where a tile lies.  Plain GEMM: tile = row-major index in the tile grid.
+// Grouped GEMM (Section 7.1 applies the recipe to grouped GEMM, the expert
+// layer of mixture-of-experts models): tile = index into `desc`; its rows are
+// rows [m0, m0 + rows) of the packed A and C (the group's rows, at most BM),
+// and its B rows are the group's weight rows b0 + [n0, n0 + width).
+struct TileGeom {
+  int m0, rows, b0, n0;
+};
+
+__device__ __forceinline__ TileGeom tile_geom(const Params& p, int tile, int width) {
+  TileGeom g;
+  if (p.desc) {
+    const int4 d = p.desc[tile];
+    g.m0 = __builtin_amdgcn_readfirstlane(d.x);
+    g.rows = __builtin_amdgcn_readfirstlane(d.y);
+    g.b0 = __builtin_amdgcn_readfirstlane(d.z);
+    g.n0 = __builtin_amdgcn_readfirstlane(d.w);
+  } else {
+    const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
+    g.m0 = tm * BM;
+    g.rows = min(BM, p.M - g.m0);
+    g.b0 = 0;
+    g.n0 = tn * width;
+  }
+  return g;
+}
 
 // Buffer resource over `bytes` bytes at `base`: loads beyond the range return
 // zero and stores beyond it are dropped, so tile edges need no branches.
@@ -138,8 +166,8 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 template <bool VEC>
 __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t* sA, uint16_t* sB) {
-  const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const TileGeom tg = tile_geom(p, tile, BN);
+  const int m0 = tg.m0, n0 = tg.n0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int KT = (p.K + BK - 1) / BK;
@@ -150,9 +178,10 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int rows_a = min(BM, p.M - m0), rows_b = min(BN, p.N - n0);
+  const int rows_a = tg.rows, rows_b = min(BN, p.N - n0);
   const __amdgpu_buffer_rsrc_t rsa = make_rsrc(p.A + (size_t)m0 * p.lda, (uint32_t)rows_a * p.lda * 2u);
-  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(p.B + (size_t)n0 * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
+  const __amdgpu_buffer_rsrc_t rsb =
+      make_rsrc(p.B + (size_t)(tg.b0 + n0) * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
   const uint32_t voa = (uint32_t)((threadIdx.x >> 3) * p.lda + (threadIdx.x & 7) * 8) * 2u;
   const uint32_t vob = (uint32_t)((threadIdx.x >> 3) * p.ldb + (threadIdx.x & 7) * 8) * 2u;
   uint4 ra[8], rb[8];
@@ -195,7 +224,7 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
 
   // epilogue: lane holds C[m][n..n+3] for each (nb, mb) block; rows past M
   // fall outside the resource and their stores are dropped
-  const int rows_c = min(BM, p.M - m0);
+  const int rows_c = tg.rows;
   const __amdgpu_buffer_rsrc_t rsc = make_rsrc(p.C + (size_t)m0 * p.ldc, (uint32_t)rows_c * p.ldc * 2u);
 #pragma unroll
   for (int nb = 0; nb < 8; ++nb) {
@@ -466,8 +495,8 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   p.ldc = __builtin_amdgcn_readfirstlane(p.ldc);
   p.M = __builtin_amdgcn_readfirstlane(p.M);
   p.N = __builtin_amdgcn_readfirstlane(p.N);
-  const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
-  const int m0 = tm * BM, n0 = tn * BNT;
+  const TileGeom tg = tile_geom(p, tile, BNT);
+  const int m0 = tg.m0, n0 = tg.n0;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int KT = (p.K + KS - 1) / KS;
@@ -479,9 +508,9 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   mfma_fence();
-  const int rows_a = min(BM, p.M - m0), rows_b = min(BNT, p.N - n0);
+  const int rows_a = tg.rows, rows_b = min(BNT, p.N - n0);
   const i32x4 rsa = rsrc_words(p.A + (size_t)m0 * p.lda, (uint32_t)rows_a * p.lda * 2u);
-  const i32x4 rsb = rsrc_words(p.B + (size_t)n0 * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
+  const i32x4 rsb = rsrc_words(p.B + (size_t)(tg.b0 + n0) * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
   // load side: lane -> (row in its 8-row block, physical chunk L%8); the
   // logical chunk stored there is the physical one XOR (row/2)%8, which for a
   // row 8b + r (b the block's index in the tile) is (r/2) | 4*(b%2): one
@@ -568,7 +597,7 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   // (the inputs pass through an opaque move so that nothing below is hoisted
   // out of the tile loop and kept live across the k-loop)
   int ldc = p.ldc, nN = p.N, lid = lane;
-  const int rows_c = min(BM, p.M - m0);
+  const int rows_c = rows_a;
   const __amdgpu_buffer_rsrc_t rsc = make_rsrc(p.C + (size_t)m0 * ldc + n0, (uint32_t)rows_c * ldc * 2u);
   // 16-byte stores need 16-byte aligned rows; otherwise two 8-byte halves
   const bool c16 = (((uintptr_t)p.C & 15u) == 0) && ((ldc & 7) == 0);
@@ -791,6 +820,7 @@ int launch_gemm(const GemmLaunch& g, hipStream_t s) {
   p.n_xccs = g.n_xccs;
   p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots; p.ctr = g.d_ctr;
   p.dynamic = g.dynamic ? 1 : 0;
+  p.desc = static_cast<const int4*>(g.d_desc);
   if (!g.vec)
     hipLaunchKernelGGL((gemm_bf16_persistent<false, 8>), dim3(g.grid), dim3(NT), 0, s, p);
   else if (g.bn == 256)

@@ -67,6 +67,8 @@ struct Schedule {
 int build_schedule(int tiles_m, int tiles_n, int n_xcds, const int* slots,
                    int mapping, int band, Schedule& s);
 std::vector<int> largest_remainder_quotas(int total, const std::vector<int>& w);
+int build_grouped_schedule(int G, const int* tiles_m, int tiles_n, int n_xcds, const int* slots,
+                           int mapping, Schedule& s);
 
 // ---- device entry points (implemented in .hip files) -------------------------
 struct GemmLaunch {
@@ -83,6 +85,7 @@ struct GemmLaunch {
   int n_xccs;
   bool vec;                    // aligned vector path
   int bn;                      // tile width: 256, or 224 / 192 on the vector path
+  const void* d_desc = nullptr; // grouped GEMM: device int4 per tile {row, rows, group B row, column}
 };
 int launch_gemm(const GemmLaunch& g, hipStream_t s);
 

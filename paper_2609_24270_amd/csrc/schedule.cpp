@@ -150,7 +150,106 @@ int build_schedule(int tiles_m, int tiles_n, int n_xcds, const int* slots,
   return ASYM_OK;
 }
 
+// Grouped GEMM (the same recipe applied to grouped GEMM, Section 7.1: the
+// expert layer of mixture-of-experts models).  Group g has tiles_m[g] tile rows
+// of tiles_n columns; tile ids number the groups' tiles in group order,
+// row-major inside a group (id = base_g + r * tiles_n + c).  Every group is one
+// band: walked column by column, top to bottom, so the tiles that share a
+// column panel of the group's weights follow each other.
+//   AWARE:             every group is shared out among the XCDs as a band of
+//                      the plain schedule is: contiguous runs of its walk, of
+//                      largest-remainder lengths by the XCDs' workgroups; an
+//                      XCD's list is its runs, group after group.  An XCD's
+//                      concurrent tiles then hold few column panels of few
+//                      groups, each panel fetched into its L2 once.
+//   OBLIVIOUS_GROUPED: the same walk, tile i to workgroup i mod P.
+//   OBLIVIOUS_ROWMAJOR: tile ids in order, tile i to workgroup i mod P.
+int build_grouped_schedule(int G, const int* tiles_m, int tiles_n, int n_xcds, const int* slots,
+                           int mapping, Schedule& s) {
+  if (G < 1) return fail(ASYM_EINVAL, "grouped schedule: no groups");
+  if (!tiles_m || !slots) return fail(ASYM_EINVAL, "grouped schedule: null argument");
+  if (tiles_n < 1) return fail(ASYM_EINVAL, "grouped schedule: no tile columns");
+  if (n_xcds < 1 || n_xcds > ASYM_MAX_XCDS) return fail(ASYM_EINVAL, "grouped schedule: bad XCD count");
+  if (mapping != ASYM_MAP_AWARE && mapping != ASYM_MAP_OBLIVIOUS_GROUPED &&
+      mapping != ASYM_MAP_OBLIVIOUS_ROWMAJOR)
+    return fail(ASYM_EINVAL, "grouped schedule: bad mapping");
+  int P = 0;
+  for (int x = 0; x < n_xcds; ++x) {
+    if (slots[x] < 0) return fail(ASYM_EINVAL, "grouped schedule: negative slot count");
+    P += slots[x];
+  }
+  if (P < 1) return fail(ASYM_EINVAL, "grouped schedule: no workgroup slots");
+  int64_t rows = 0;
+  for (int g = 0; g < G; ++g) {
+    if (tiles_m[g] < 0) return fail(ASYM_EINVAL, "grouped schedule: negative tile rows");
+    rows += tiles_m[g];
+  }
+  if (rows * tiles_n > (1 << 30)) return fail(ASYM_EINVAL, "grouped schedule: too many tiles");
+  const int T = (int)(rows * tiles_n);
+  s.tiles_m = (int)rows;
+  s.tiles_n = tiles_n;
+  s.n_xcds = n_xcds;
+  s.order.assign(T, 0);
+  s.off.assign(n_xcds + 1, 0);
+  s.quota.assign(n_xcds, 0);
+  if (T == 0) return ASYM_OK;
+
+  // the walk, one band per group
+  std::vector<int> walk(T), band_start(G + 1, 0);
+  {
+    int i = 0, base = 0;
+    for (int g = 0; g < G; ++g) {
+      band_start[g] = i;
+      for (int c = 0; c < tiles_n; ++c)
+        for (int r = 0; r < tiles_m[g]; ++r) walk[i++] = base + r * tiles_n + c;
+      base += tiles_m[g] * tiles_n;
+    }
+    band_start[G] = i;
+  }
+  if (mapping == ASYM_MAP_AWARE) {
+    std::vector<int> w(slots, slots + n_xcds);
+    std::vector<std::vector<int>> lists(n_xcds);
+    for (int g = 0; g < G; ++g) {
+      const int len = band_start[g + 1] - band_start[g];
+      if (len == 0) continue;
+      const std::vector<int> q = largest_remainder_quotas(len, w);
+      int pos = band_start[g];
+      for (int x = 0; x < n_xcds; ++x) {
+        lists[x].insert(lists[x].end(), walk.begin() + pos, walk.begin() + pos + q[x]);
+        pos += q[x];
+      }
+    }
+    int o = 0;
+    for (int x = 0; x < n_xcds; ++x) {
+      std::copy(lists[x].begin(), lists[x].end(), s.order.begin() + o);
+      s.quota[x] = (int)lists[x].size();
+      o += s.quota[x];
+      s.off[x + 1] = o;
+    }
+  } else {
+    if (mapping == ASYM_MAP_OBLIVIOUS_GROUPED)
+      s.order = walk;
+    else
+      for (int i = 0; i < T; ++i) s.order[i] = i;
+    for (int x = 0; x <= n_xcds; ++x) s.off[x] = (x == n_xcds) ? T : 0;
+    for (int i = 0; i < T; ++i) s.quota[(i % P) % n_xcds] += 1;
+  }
+  return ASYM_OK;
+}
+
 }  // namespace asym
+
+extern "C" int asym_grouped_schedule_build(int G, const int* tiles_m, int tiles_n, int n_xcds,
+                                           const int* slots, int mapping, int* order, int* off,
+                                           int* quota) {
+  asym::Schedule s;
+  int rc = asym::build_grouped_schedule(G, tiles_m, tiles_n, n_xcds, slots, mapping, s);
+  if (rc != ASYM_OK) return rc;
+  if (order) std::copy(s.order.begin(), s.order.end(), order);
+  if (off) std::copy(s.off.begin(), s.off.end(), off);
+  if (quota) std::copy(s.quota.begin(), s.quota.end(), quota);
+  return ASYM_OK;
+}
 
 extern "C" int asym_schedule_build(int tiles_m, int tiles_n, int n_xcds,
                                    const int* slots, int mapping, int band,

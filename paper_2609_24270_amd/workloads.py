@@ -17,6 +17,7 @@ layer (hidden 4096, FFN 14336, fused QKV 6144) with 4096 tokens.
 """
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass, field
 
 import torch
@@ -98,6 +99,70 @@ def make_pd_inputs():
 
 def make_problem(M: int, N: int, K: int, seed: int, dist: str = "uniform") -> GemmProblem:
     return GemmProblem(f"gemm_{M}x{N}x{K}", M, N, K, seed=seed, dist=dist)
+
+
+# Grouped GEMM, the mixture-of-experts expert layer (Section 7.1 and its
+# appendix): G groups with expected row count M; group i has
+# M_i = floor(M * U_i) rows, U_i ~ Uniform(0.7, 1.3), drawn per shape seed.
+# The configurations are every (G, M) in GROUPED_GM with every (N, K) in
+# GROUPED_NK.  Recipe: one torch CPU generator per problem, seeded with
+# `seed`; the G values U_i are drawn first (float64), then A [sum M_i, K] ~
+# normal(0, 1) and B [G, N, K] ~ normal(0, 0.02), converted to bf16.
+GROUPED_GM = ((32, 192), (6, 1024), (32, 20), (6, 20))
+GROUPED_NK = ((6144, 7168), (7168, 3072), (4096, 4096), (4096, 2048))
+
+
+@dataclass(frozen=True)
+class GroupedProblem:
+    name: str
+    G: int
+    M: int          # expected rows per group
+    N: int
+    K: int
+    seed: int
+    dist: str = "llm"    # "llm" | "uniform" | "int"
+
+    def rows(self):
+        g = torch.Generator(device="cpu").manual_seed(self.seed)
+        return _group_rows(g, self.G, self.M)
+
+    @property
+    def flops(self) -> float:
+        return 2.0 * sum(self.rows()) * self.N * self.K
+
+    @property
+    def working_set_bytes(self) -> int:
+        """Logical bytes of inputs and output: 2 (sum M_i (K + N) + G N K)."""
+        return 2 * (sum(self.rows()) * (self.K + self.N) + self.G * self.N * self.K)
+
+
+def _group_rows(g: torch.Generator, G: int, M: int):
+    u = torch.rand(G, generator=g, dtype=torch.float64) * 0.6 + 0.7
+    return [int(math.floor(M * float(x))) for x in u]
+
+
+def grouped_problem(G: int, M: int, N: int, K: int, seed: int = 5, dist: str = "llm") -> GroupedProblem:
+    return GroupedProblem(f"group_G{G}_M{M}_N{N}_K{K}_s{seed}", G, M, N, K, seed=seed, dist=dist)
+
+
+GROUPED = tuple(grouped_problem(G, M, N, K) for (G, M) in GROUPED_GM for (N, K) in GROUPED_NK)
+
+
+def make_grouped_inputs(p: GroupedProblem, rows=None):
+    """(row counts, A [sum M_i, K], B [G, N, K]) bf16 CPU tensors for p.  `rows`
+    overrides the sampled row counts (the generator still draws them first)."""
+    g = torch.Generator(device="cpu").manual_seed(p.seed)
+    Ms = _group_rows(g, p.G, p.M)
+    if rows is not None:
+        Ms = list(rows)
+    total = sum(Ms)
+    if p.dist == "llm":
+        A = _draw(g, (total, p.K), "normal", 1.0)
+        B = _draw(g, (p.G, p.N, p.K), "normal", 0.02)
+    else:
+        A = _draw(g, (total, p.K), p.dist, 1.0)
+        B = _draw(g, (p.G, p.N, p.K), p.dist, 1.0)
+    return Ms, A, B
 
 
 def random_mask_bits(seed: int, n_masks: int, n_bits: int, total: int = 256):

@@ -309,3 +309,61 @@ def test_gemm_and_copy_argument_errors(lib):
         assert asym.last_error()
     assert lib_.asym_copy_bf16(P, P, 24, 1, None, 0, None) == asym.EINVAL
     assert lib_.asym_copy_bf16(P, P, 32, 0, None, 0, None) == asym.EINVAL
+
+
+def _grouped_cases():
+    rng = random.Random(99)
+    cases = [([1] * 32, 16, [32] * 8), ([5, 4, 4, 5, 4, 5], 16, [32] * 8), ([0, 3, 0, 1], 7, [32] * 8),
+             ([2, 1], 28, [16, 10, 22, 16, 13, 19, 16, 16]), ([4], 1, [1, 0, 0, 0, 0, 0, 0, 0])]
+    for _ in range(20):
+        G = rng.randint(1, 12)
+        n = rng.choice([1, 2, 4, 8])
+        slots = [rng.randint(0, 32) for _ in range(n)]
+        if sum(slots) == 0:
+            slots[0] = 1
+        cases.append(([rng.randint(0, 6) for _ in range(G)], rng.randint(1, 30), slots))
+    return cases
+
+
+@pytest.mark.parametrize("rows,tn,slots", _grouped_cases())
+def test_grouped_schedule_matches_oracle(lib, rows, tn, slots):
+    T = sum(rows) * tn
+    order, off, quota = asym.grouped_schedule_build(rows, tn, slots, asym.MAP_AWARE)
+    lists = osched.grouped_aware_lists(rows, tn, slots)
+    assert quota == [len(lst) for lst in lists]
+    assert order == [t for lst in lists for t in lst]
+    assert off[0] == 0 and all(off[x + 1] - off[x] == quota[x] for x in range(len(slots)))
+    assert sorted(order) == list(range(T))                     # every tile exactly once
+    W = sum(slots)
+    n_groups = sum(1 for r in rows if r)
+    assert all(abs(quota[x] - T * slots[x] / W) < max(1, n_groups) for x in range(len(slots)))
+    assert all(q == 0 for q, s in zip(quota, slots) if s == 0)
+    order_g, _, quota_g = asym.grouped_schedule_build(rows, tn, slots, asym.MAP_OBLIVIOUS_GROUPED)
+    assert order_g == osched.grouped_oblivious_order(rows, tn, True)
+    owner = osched.oblivious_assignment(order_g, slots)
+    assert quota_g == [sum(1 for v in owner.values() if v == x) for x in range(len(slots))]
+    order_r, _, _ = asym.grouped_schedule_build(rows, tn, slots, asym.MAP_OBLIVIOUS_ROWMAJOR)
+    assert order_r == osched.grouped_oblivious_order(rows, tn, False)
+
+
+def test_grouped_aware_keeps_a_column_panel_on_one_xcd():
+    """Six groups of 4-5 tile rows on 8 XCDs of 32: every column panel of a
+    group (its tile rows of one column) lands on at most two XCDs."""
+    rows, tn, slots = [5, 4, 4, 4, 4, 5], 16, [32] * 8
+    order, off, _ = asym.grouped_schedule_build(rows, tn, slots, asym.MAP_AWARE)
+    owner = {t: x for x in range(8) for t in order[off[x]:off[x + 1]]}
+    ids = osched.grouped_tile_ids(rows, tn)
+    for g, r_g in enumerate(rows):
+        for c in range(tn):
+            assert len({owner[ids[(g, r, c)]] for r in range(r_g)}) <= 2
+
+
+def test_grouped_schedule_rejects_bad_input(lib):
+    with pytest.raises(asym.AsymError):
+        asym.grouped_schedule_build([], 4, [32] * 8, asym.MAP_AWARE)
+    with pytest.raises(asym.AsymError):
+        asym.grouped_schedule_build([1, -1], 4, [32] * 8, asym.MAP_AWARE)
+    with pytest.raises(asym.AsymError):
+        asym.grouped_schedule_build([1, 1], 0, [32] * 8, asym.MAP_AWARE)
+    with pytest.raises(asym.AsymError):
+        asym.grouped_schedule_build([1, 1], 4, [0] * 8, asym.MAP_AWARE)

@@ -162,3 +162,70 @@ def test_row_permutation_equivariant():
     perm = np.random.default_rng(0).permutation(M)
     R2, C2 = oracle.gemm_bf16(bits(A)[perm], bits(B), "nk")
     assert np.array_equal(R1[perm], R2) and np.array_equal(C1[perm], C2)
+
+
+# ---- grouped GEMM oracle ------------------------------------------------------
+
+def _grouped_case(rows, N, K, seed, dist="uniform"):
+    p = workloads.GroupedProblem("t", len(rows), 1, N, K, seed=seed, dist=dist)
+    Ms, A, B = workloads.make_grouped_inputs(p, rows=rows)
+    return Ms, bits(A), bits(B.reshape(len(rows) * N, K)).reshape(len(rows), N, K)
+
+
+def test_grouped_one_group_is_the_plain_gemm():
+    Ms, A, B = _grouped_case([77], 40, 130, seed=11)
+    R, C = oracle.grouped_gemm_bf16(A, B, Ms)
+    R1, C1 = oracle.gemm_bf16(A, B[0], "nk")
+    assert np.array_equal(C, C1) and np.array_equal(R, R1)
+
+
+def test_grouped_shared_weights_are_one_gemm_of_the_packed_rows():
+    """With every group's weights equal, the grouped product of the packed rows
+    is one plain product of all of them: row offsets and packing are pinned."""
+    Ms, A, B = _grouped_case([5, 0, 33, 1, 17], 24, 72, seed=12)
+    Bs = np.repeat(B[:1], len(Ms), axis=0)
+    R, C = oracle.grouped_gemm_bf16(A, Bs, Ms)
+    R1, C1 = oracle.gemm_bf16(A, B[0], "nk")
+    assert np.array_equal(C, C1) and np.array_equal(R, R1)
+
+
+def test_grouped_permuting_groups_permutes_row_blocks():
+    """Reordering the groups (rows and weights together) reorders the output
+    blocks and changes nothing else: each group meets its own weights."""
+    Ms, A, B = _grouped_case([9, 4, 0, 21, 13], 16, 96, seed=13)
+    R, C = oracle.grouped_gemm_bf16(A, B, Ms)
+    starts = np.cumsum([0] + Ms)
+    perm = [3, 0, 4, 2, 1]
+    A2 = np.concatenate([A[starts[g]:starts[g + 1]] for g in perm])
+    C_expect = np.concatenate([C[starts[g]:starts[g + 1]] for g in perm])
+    R2, C2 = oracle.grouped_gemm_bf16(A2, B[perm], [Ms[g] for g in perm])
+    assert np.array_equal(C2, C_expect)
+    # and the weights matter: pairing every group with group 0's weights differs
+    _, C3 = oracle.grouped_gemm_bf16(A, np.repeat(B[:1], len(Ms), axis=0), Ms)
+    assert not np.array_equal(C3, C)
+
+
+def test_grouped_exact_integer_closed_form():
+    """Integer inputs: every product and partial sum is exact, so each group's
+    block equals the integer product, converted once."""
+    Ms, A, B = _grouped_case([3, 7, 2], 12, 40, seed=14, dist="int")
+    R, C = oracle.grouped_gemm_bf16(A, B, Ms)
+    Af = oracle.bf16_bits_to_f32(A).astype(np.int64)
+    Bf = oracle.bf16_bits_to_f32(B).astype(np.int64)
+    row = 0
+    for g, m in enumerate(Ms):
+        exact = Af[row:row + m] @ Bf[g].T
+        assert np.array_equal(R[row:row + m], exact.astype(np.float32))
+        row += m
+
+
+def test_grouped_row_sampling_follows_the_definition():
+    """M_i = floor(M U_i), U_i in [0.7, 1.3): every count within the range,
+    reproducible from the seed."""
+    for G, M in workloads.GROUPED_GM:
+        p = workloads.grouped_problem(G, M, 64, 64)
+        rows = p.rows()
+        assert len(rows) == G and rows == p.rows()
+        assert all(int(0.7 * M) <= r <= int(1.3 * M) for r in rows)
+    p = workloads.GROUPED[0]
+    assert p.working_set_bytes == 2 * (sum(p.rows()) * (p.K + p.N) + p.G * p.N * p.K)
