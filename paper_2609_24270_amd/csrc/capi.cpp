@@ -55,22 +55,32 @@ struct DeviceSchedule {
 };
 std::map<ScheduleKey, DeviceSchedule> g_schedules;  // never freed: kernels may still read them
 
+// One grouped problem's device tables: tile descriptors, and the schedule
+// (order [T], off [MAX_XCDS + 1], slots [MAX_XCDS]).
+struct GroupedTables {
+  std::vector<int> key;   // row counts, N, tile width, mapping, slots
+  int4* desc = nullptr;
+  int* sched = nullptr;
+  int T = 0;
+};
+constexpr size_t kGroupedCache = 8;
+
 // Device counters per (device, stream): launches on one stream run in order
 // and the kernels leave their counters zeroed, so one block per stream does.
 struct Workspace {
   int* gemm_ctr = nullptr;                  // 64 ints (dynamic aware GEMM)
   unsigned long long* copy_ctr = nullptr;   // 4 words
-  // grouped GEMM: the tile table and schedule of the latest call on the
-  // stream (each call's copies are ordered after the previous call's kernel)
-  int4* g_desc = nullptr;
-  int* g_sched = nullptr;                   // order [cap], off [MAX_XCDS + 1], slots [MAX_XCDS]
-  int g_cap = 0;
-  // pinned host staging of the same, and an event recorded after the copies
-  // out of it: the next call waits for it before writing the staging again
+  // grouped GEMM: device copies of recent tile tables and schedules, most
+  // recent first (a repeated call reuses its tables), and a pinned host
+  // staging buffer with an event recorded after the copies out of it: the
+  // next upload waits for it before writing the staging again
+  std::vector<GroupedTables> g_tables;
   void* g_host = nullptr;
+  size_t g_host_bytes = 0;
   hipEvent_t g_copied = nullptr;
   bool g_pending = false;
 };
+
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
 std::map<int, std::unique_ptr<Topology>> g_default_topo;
@@ -334,68 +344,83 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   int rc = plan_gemm(topo_in, virt_m, N, K, A, lda, B, ldb, ASYM_B_NK, C, ldc, mapping, xcd_mask, stream, &P);
   if (rc != ASYM_OK) return rc;
   const int tiles_n = (N + P.bn - 1) / P.bn;
-  Schedule sch;
-  rc = build_grouped_schedule(G, tm.data(), tiles_n, P.t->n_xccs, P.slots.data(), mapping, sch);
-  if (rc != ASYM_OK) return rc;
-  const int T = (int)sch.order.size();
-  std::vector<int4> desc(T);
-  {
-    int id = 0, row0 = 0;
-    for (int g = 0; g < G; ++g) {
-      for (int r = 0; r < tm[g]; ++r)
-        for (int c = 0; c < tiles_n; ++c)
-          desc[id++] = int4{row0 + r * gemm_tile_m(), std::min(gemm_tile_m(), Ms[g] - r * gemm_tile_m()),
-                            g * N, c * P.bn};
-      row0 += Ms[g];
-    }
-  }
   Workspace* ws = nullptr;
   rc = get_workspace(P.device, stream, &ws);
   if (rc != ASYM_OK) return rc;
-  const size_t desc_bytes = (size_t)T * sizeof(int4);
-  const size_t sched_ints = (size_t)T + 2 * ASYM_MAX_XCDS + 1;
-  // the staging buffer is free once the previous call's copies have run
-  if (ws->g_pending) {
-    ASYM_HIP(hipEventSynchronize(ws->g_copied));
-    ws->g_pending = false;
+  std::vector<int> key(Ms, Ms + G);
+  key.push_back(N);
+  key.push_back(P.bn);
+  key.push_back(mapping);
+  key.insert(key.end(), P.slots.begin(), P.slots.end());
+  auto hit = std::find_if(ws->g_tables.begin(), ws->g_tables.end(),
+                          [&](const GroupedTables& t) { return t.key == key; });
+  if (hit != ws->g_tables.end()) {
+    std::rotate(ws->g_tables.begin(), hit, hit + 1);  // most recent first
+  } else {
+    Schedule sch;
+    rc = build_grouped_schedule(G, tm.data(), tiles_n, P.t->n_xccs, P.slots.data(), mapping, sch);
+    if (rc != ASYM_OK) return rc;
+    GroupedTables tb;
+    tb.key = std::move(key);
+    tb.T = (int)sch.order.size();
+    const size_t desc_bytes = (size_t)tb.T * sizeof(int4);
+    const size_t sched_bytes = ((size_t)tb.T + 2 * ASYM_MAX_XCDS + 1) * sizeof(int);
+    if (ws->g_tables.size() >= kGroupedCache) {
+      // the oldest tables may still be read by launches on this stream
+      ASYM_HIP(hipStreamSynchronize(stream));
+      GroupedTables& old = ws->g_tables.back();
+      ASYM_HIP(hipFree(old.desc));
+      ASYM_HIP(hipFree(old.sched));
+      ws->g_tables.pop_back();
+    }
+    ASYM_HIP(hipMalloc(&tb.desc, desc_bytes));
+    ASYM_HIP(hipMalloc(&tb.sched, sched_bytes));
+    // the staging buffer is free once the previous upload's copies have run
+    if (ws->g_pending) {
+      ASYM_HIP(hipEventSynchronize(ws->g_copied));
+      ws->g_pending = false;
+    }
+    if (ws->g_host_bytes < desc_bytes + sched_bytes) {
+      if (ws->g_host) ASYM_HIP(hipHostFree(ws->g_host));
+      ws->g_host = nullptr;
+      ws->g_host_bytes = 0;
+      const size_t bytes = std::max<size_t>(desc_bytes + sched_bytes, 64 << 10);
+      ASYM_HIP(hipHostMalloc(&ws->g_host, bytes));
+      ws->g_host_bytes = bytes;
+    }
+    if (!ws->g_copied) ASYM_HIP(hipEventCreateWithFlags(&ws->g_copied, hipEventDisableTiming));
+    int4* h_desc = static_cast<int4*>(ws->g_host);
+    int* h_sched = reinterpret_cast<int*>(static_cast<char*>(ws->g_host) + desc_bytes);
+    {
+      int id = 0, row0 = 0;
+      for (int g = 0; g < G; ++g) {
+        for (int r = 0; r < tm[g]; ++r)
+          for (int c = 0; c < tiles_n; ++c)
+            h_desc[id++] = int4{row0 + r * gemm_tile_m(), std::min(gemm_tile_m(), Ms[g] - r * gemm_tile_m()),
+                                g * N, c * P.bn};
+        row0 += Ms[g];
+      }
+    }
+    std::fill(h_sched, h_sched + sched_bytes / sizeof(int), 0);
+    std::copy(sch.order.begin(), sch.order.end(), h_sched);
+    for (int x = 0; x <= P.t->n_xccs; ++x) h_sched[tb.T + x] = sch.off[x];
+    for (int x = 0; x < P.t->n_xccs; ++x) h_sched[tb.T + ASYM_MAX_XCDS + 1 + x] = P.slots[x];
+    ASYM_HIP(hipMemcpyAsync(tb.desc, h_desc, desc_bytes, hipMemcpyHostToDevice, stream));
+    ASYM_HIP(hipMemcpyAsync(tb.sched, h_sched, sched_bytes, hipMemcpyHostToDevice, stream));
+    ASYM_HIP(hipEventRecord(ws->g_copied, stream));
+    ws->g_pending = true;
+    ws->g_tables.insert(ws->g_tables.begin(), std::move(tb));
   }
-  if (ws->g_cap < T) {
-    // earlier launches on this stream may still read the old device buffers
-    ASYM_HIP(hipStreamSynchronize(stream));
-    if (ws->g_desc) ASYM_HIP(hipFree(ws->g_desc));
-    if (ws->g_sched) ASYM_HIP(hipFree(ws->g_sched));
-    if (ws->g_host) ASYM_HIP(hipHostFree(ws->g_host));
-    ws->g_desc = nullptr;
-    ws->g_sched = nullptr;
-    ws->g_host = nullptr;
-    ws->g_cap = 0;
-    const int cap = std::max(T, 1024);
-    const size_t bytes = (size_t)cap * sizeof(int4) + ((size_t)cap + 2 * ASYM_MAX_XCDS + 1) * sizeof(int);
-    ASYM_HIP(hipMalloc(&ws->g_desc, (size_t)cap * sizeof(int4)));
-    ASYM_HIP(hipMalloc(&ws->g_sched, ((size_t)cap + 2 * ASYM_MAX_XCDS + 1) * sizeof(int)));
-    ASYM_HIP(hipHostMalloc(&ws->g_host, bytes));
-    ws->g_cap = cap;
-  }
-  if (!ws->g_copied) ASYM_HIP(hipEventCreateWithFlags(&ws->g_copied, hipEventDisableTiming));
-  int4* h_desc = static_cast<int4*>(ws->g_host);
-  int* h_sched = reinterpret_cast<int*>(static_cast<char*>(ws->g_host) + (size_t)ws->g_cap * sizeof(int4));
-  std::copy(desc.begin(), desc.end(), h_desc);
-  std::fill(h_sched, h_sched + sched_ints, 0);
-  std::copy(sch.order.begin(), sch.order.end(), h_sched);
-  for (int x = 0; x <= P.t->n_xccs; ++x) h_sched[T + x] = sch.off[x];
-  for (int x = 0; x < P.t->n_xccs; ++x) h_sched[T + ASYM_MAX_XCDS + 1 + x] = P.slots[x];
-  ASYM_HIP(hipMemcpyAsync(ws->g_desc, h_desc, desc_bytes, hipMemcpyHostToDevice, stream));
-  ASYM_HIP(hipMemcpyAsync(ws->g_sched, h_sched, sched_ints * sizeof(int), hipMemcpyHostToDevice, stream));
-  ASYM_HIP(hipEventRecord(ws->g_copied, stream));
-  ws->g_pending = true;
+  const GroupedTables& tb = ws->g_tables.front();
+  const int T = tb.T;
 
   GemmLaunch gl;
   gl.A = A; gl.B = B; gl.C = C;
   gl.M = virt_m; gl.N = N; gl.K = K; gl.lda = lda; gl.ldb = ldb; gl.ldc = ldc;
   gl.mapping = mapping;
-  gl.d_order = ws->g_sched;
-  gl.d_off = ws->g_sched + T;
-  gl.d_slots = ws->g_sched + T + ASYM_MAX_XCDS + 1;
+  gl.d_order = tb.sched;
+  gl.d_off = tb.sched + T;
+  gl.d_slots = tb.sched + T + ASYM_MAX_XCDS + 1;
   gl.tiles_m = (int)trows;
   gl.tiles_n = tiles_n;
   gl.n_xccs = P.t->n_xccs;
@@ -404,7 +429,7 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   gl.dynamic = P.dynamic;
   gl.vec = P.vec;
   gl.bn = P.bn;
-  gl.d_desc = ws->g_desc;
+  gl.d_desc = tb.desc;
   return launch_gemm(gl, stream);
 }
 
@@ -452,8 +477,10 @@ void release_workspace(hipStream_t s) {
     if (it->first.second == s) {
       hipFree(it->second.gemm_ctr);
       hipFree(it->second.copy_ctr);
-      if (it->second.g_desc) hipFree(it->second.g_desc);
-      if (it->second.g_sched) hipFree(it->second.g_sched);
+      for (auto& t : it->second.g_tables) {
+        hipFree(t.desc);
+        hipFree(t.sched);
+      }
       if (it->second.g_host) hipHostFree(it->second.g_host);
       if (it->second.g_copied) hipEventDestroy(it->second.g_copied);
       it = g_ws.erase(it);
