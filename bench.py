@@ -253,6 +253,81 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves):
     return summ
 
 
+def queued(fns: dict, launches: int, rounds: int, stream) -> dict:
+    """Mean per-launch ms of each fn for kernels too short to time one launch
+    at a time: each round first parks the stream on a spin kernel (about
+    3 ms), then queues `launches` back-to-back launches of every variant in
+    turn, each run bracketed by HIP events; the host finishes queueing before
+    the spin ends, so the events time the GPU alone, not the launch calls."""
+    import torch
+    names = list(fns)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    torch.cuda._sleep(1 << 20)
+    b.record(stream)
+    torch.cuda.synchronize()
+    spin = int((1 << 20) * 3.0 / max(a.elapsed_time(b), 1e-3))
+    evs = {k: [] for k in names}
+    for _ in range(rounds):
+        torch.cuda._sleep(spin)
+        for k in names:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(launches):
+                fns[k]()
+            e1.record(stream)
+            evs[k].append((e0, e1))
+        torch.cuda.synchronize()
+    return {k: sum(x.elapsed_time(y) for x, y in evs[k]) / (rounds * launches) for k in names}
+
+
+def grouped_study(dev, stream, seeds, launches: int, rounds: int):
+    """Grouped GEMM over the 16 expert-layer configurations, (G, M) x (N, K),
+    five row-count seeds each (M_i = floor(M U_i), U_i ~ U(0.7, 1.3)): per
+    instance, the three mappings timed in turn; reported per configuration
+    (seed means) with the logical working set W = 2 (sum M_i (K + N) + G N K)
+    bytes, and the aware speedups over all instances."""
+    import math
+
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    per, sp_g, sp_r = {}, [], []
+    for base in workloads.GROUPED:
+        rows = []
+        for seed in seeds:
+            p = workloads.grouped_problem(base.G, base.M, base.N, base.K, seed=seed)
+            Ms, A, B = workloads.make_grouped_inputs_on(p, dev)
+            C = torch.empty((sum(Ms), p.N), dtype=torch.bfloat16, device=dev)
+            fns = {m: (lambda m=m: asym.gemm_grouped(A, B, Ms, C, mapping=m, stream=stream)) for m in MAPPINGS}
+            for f in fns.values():
+                f()
+            ms = queued(fns, launches, rounds, stream)
+            rows.append((p.flops, p.working_set_bytes, ms))
+            sp_g.append(ms["oblivious_grouped"] / ms["aware"])
+            sp_r.append(ms["oblivious_rowmajor"] / ms["aware"])
+            del A, B, C
+        n = len(rows)
+        gm = lambda v: math.exp(sum(math.log(x) for x in v) / len(v))
+        per[f"G{base.G}_M{base.M}_N{base.N}_K{base.K}"] = {
+            "W_GB": round(sum(r[1] for r in rows) / n / 1e9, 4),
+            **{f"{m}_us": round(1e3 * sum(r[2][m] for r in rows) / n, 2) for m in MAPPINGS},
+            "aware_tflops": round(sum(r[0] / (r[2]["aware"] * 1e-3) for r in rows) / n / 1e12, 1),
+            "aware_TBps_W": round(sum(r[1] / (r[2]["aware"] * 1e-3) for r in rows) / n / 1e12, 3),
+            "speedup_vs_oblivious_grouped": round(gm([r[2]["oblivious_grouped"] / r[2]["aware"] for r in rows]), 4),
+            "speedup_vs_oblivious_rowmajor": round(gm([r[2]["oblivious_rowmajor"] / r[2]["aware"] for r in rows]), 4)}
+    torch.cuda.empty_cache()
+
+    def summ(v):
+        v = sorted(v)
+        return {"min": round(v[0], 4), "median": round(v[len(v) // 2], 4), "max": round(v[-1], 4),
+                "geomean": round(math.exp(sum(math.log(x) for x in v) / len(v)), 4)}
+    return {"seeds": list(seeds), "launches_per_run": launches, "rounds": rounds, "instances": len(sp_g),
+            "aware_speedup_vs_oblivious_grouped": summ(sp_g),
+            "aware_speedup_vs_oblivious_rowmajor": summ(sp_r), "per_config": per}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -269,10 +344,10 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,spread",
+    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
-                         "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets); "
-                         "'none' for the headline only")
+                         "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
+                         "grouped (expert-layer grouped GEMMs); 'none' for the headline only")
     ap.add_argument("--spread-masks", type=int, default=32)
     ap.add_argument("--mapping-only", default=None,
                     help="time only this mapping, no studies (profiling runs)")
@@ -376,6 +451,8 @@ def main() -> int:
         line["prefill_decode"] = prefill_decode(topo, dev, 10, halves)
     if "spread" in studies:
         line["cu_set_spread"] = spread_study(topo, dev, args.spread_masks, 20, halves)
+    if "grouped" in studies:
+        line["grouped_gemm"] = grouped_study(dev, stream, range(1, 6), 8, 5)
     line["cpu_baseline"] = None if args.no_cpu else cpu_baseline(A, B, args.cpu_rows)
     if line["cpu_baseline"]:
         line["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)

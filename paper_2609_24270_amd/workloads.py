@@ -165,6 +165,23 @@ def make_grouped_inputs(p: GroupedProblem, rows=None):
     return Ms, A, B
 
 
+def make_grouped_inputs_on(p: GroupedProblem, device):
+    """(row counts, A, B) like make_grouped_inputs, with A and B drawn on
+    `device` by a generator there seeded with p.seed (same distributions,
+    different streams of numbers; for timing runs at the full sizes, where
+    drawing gigabytes on the CPU would take minutes).  The row counts are the
+    CPU draw, identical to make_grouped_inputs."""
+    Ms = p.rows()
+    g = torch.Generator(device=device).manual_seed(p.seed)
+    if p.dist != "llm":
+        raise ValueError("device draws support the llm recipe only")
+    A = torch.randn((sum(Ms), p.K), generator=g, device=device).to(torch.bfloat16)
+    B = torch.empty((p.G, p.N, p.K), dtype=torch.bfloat16, device=device)
+    for i in range(p.G):  # one group at a time keeps the fp32 draw small
+        B[i] = (torch.randn((p.N, p.K), generator=g, device=device) * 0.02).to(torch.bfloat16)
+    return Ms, A, B
+
+
 def random_mask_bits(seed: int, n_masks: int, n_bits: int, total: int = 256):
     """n_masks seeded random subsets of n_bits CU-mask bit positions out of total.
 
