@@ -226,3 +226,59 @@ def planted_latency(seed: int, n_samples: int, grp=MI300X_GROUPS, dist=MI300X_DI
     tier_t = torch.tensor([[tiers[dist[a][b]] for b in range(n_g)] for a in range(n_g)])
     lat = torch.stack([tier_t[grp[x]][home] for x in range(len(grp))]) + off + jit
     return lat.numpy().astype(np.uint32), home.numpy()
+
+
+# Synthetic inputs for the partition-hash (interleave) discovery, host-only
+# tests.  interleave_layout draws the probe's address blocks: a base line
+# uniform among the 128-byte lines below 2^hi_bit, the base with each bit in
+# [lo_bit, hi_bit) flipped, then n_pairs variants with two distinct such bits
+# flipped.  planted_interleave_latency gives every address a home partition
+# from a planted rule and the per-XCD latencies that go with it (two XCD halves,
+# local / remote tiers as measured on MI355X, shared per-address offset and
+# per-(XCD, address) jitter as in planted_latency).  Rules:
+#   "xor": parity of (offset & mask & (2^page_bits - 1)), XOR a seeded bit per
+#          2^page_bits page (the page's unknown physical bits);
+#   "mixed": bit m0 XOR (bit m1 AND bit m2) of the three lowest mask bits, XOR
+#          the page bit (not one parity: flips of m1, m2 change the home for
+#          half of the addresses).
+def interleave_layout(seed: int, n_bases: int, lo_bit: int, hi_bit: int, n_pairs: int):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    nb = hi_bit - lo_bit
+    offs = []
+    for _ in range(n_bases):
+        base = int(torch.randint(0, 1 << (hi_bit - 7), (1,), generator=g)) << 7
+        offs.append(base)
+        offs.extend(base ^ (1 << b) for b in range(lo_bit, hi_bit))
+        for _ in range(n_pairs):
+            i, j = (int(v) + lo_bit for v in torch.randperm(nb, generator=g)[:2])
+            offs.append(base ^ (1 << i) ^ (1 << j))
+    return offs, 1 + nb + n_pairs
+
+
+def planted_interleave_latency(seed: int, offs, mask: int, page_bits: int = 21, rule: str = "xor",
+                               grp=(0, 0, 0, 0, 1, 1, 1, 1), tiers=(735, 950), common: int = 40,
+                               jitter: int = 12):
+    """Returns (lat uint32 [n_xcds, n_addr], home list)."""
+    import numpy as np
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    page_bit = {}
+    home = []
+    low = mask & ((1 << page_bits) - 1)
+    mb = [b for b in range(64) if (mask >> b) & 1]
+    for o in offs:
+        p = o >> page_bits
+        if p not in page_bit:
+            page_bit[p] = int(torch.randint(0, 2, (1,), generator=g))
+        if rule == "xor":
+            h = bin(o & low).count("1") & 1
+        elif rule == "mixed":
+            h = ((o >> mb[0]) & 1) ^ (((o >> mb[1]) & 1) & ((o >> mb[2]) & 1))
+        else:
+            raise ValueError(rule)
+        home.append(h ^ page_bit[p])
+    n = len(offs)
+    off = torch.randint(0, max(1, common), (n,), generator=g)
+    jit = torch.randint(0, max(1, jitter), (len(grp), n), generator=g)
+    h = torch.tensor(home)
+    lat = torch.stack([torch.where(h == grp[x], tiers[0], tiers[1]) for x in range(len(grp))]) + off + jit
+    return lat.numpy().astype(np.uint32), home
