@@ -255,6 +255,98 @@ int asym_latency_analyze(const uint32_t* hbm_lat, int n_xcds, int n_samples,
                          double group_threshold, double tie_cycles,
                          asym_latency_summary* out);
 
+/* ---- partition-hash discovery (Section 6.1, NUMA partition identification) */
+/* Which address bits decide an address's memory partition.  The partition of
+ * an address is its home affinity group, classified from HBM-regime latencies
+ * as in asym_latency_analyze.  On the GPUs the paper dissects the partition is
+ * one parity (XOR) over some physical address bits; flipping one bit of an
+ * address and seeing whether the partition changes tells whether the bit takes
+ * part, and the lowest bit that takes part sets the granularity.
+ *
+ * The probe allocates max(2^hi_bit, 2 MiB) bytes starting on a 2 MiB boundary
+ * and times, from every XCD (HBM regime, minimum over passes), n_bases blocks
+ * of lines.  Block b is, in order: a base line (uniform among the 128-byte
+ * lines below 2^hi_bit), the base with offset bit k flipped for each k in
+ * [lo_bit, hi_bit), then n_pairs variants with two distinct such bits flipped.
+ * Bases and pairs come from splitmix64 seeded with `seed`.  The translation
+ * warm-up load before each timed load goes to offset ^ 0x1F0000 (bits 16-20,
+ * same 2 MiB page), which is never another line of the same block.  Offsets
+ * below the base alignment equal virtual-address bits; bits below the
+ * translation page (2 MiB assumed) equal physical bits; flips above it land on
+ * other physical pages, whose contribution shows as undetermined bits unless
+ * the allocation is physically contiguous there. */
+typedef struct asym_interleave_params {
+  int n_bases;            /* blocks, 1..4096 */
+  int lo_bit;             /* lowest flipped bit, 7..hi_bit-1 (7: 128-byte lines) */
+  int hi_bit;             /* one past the highest flipped bit, lo_bit+1..36 */
+  int n_pairs;            /* two-bit variants per block, 0..64 (0 if one bit is flipped) */
+  int passes;             /* 1..64 */
+  uint64_t seed;
+  double group_threshold; /* as asym_latency_params */
+  double tie_cycles;      /* as asym_latency_params */
+  double decide;          /* verdict margin, in (0, 0.5) */
+} asym_interleave_params;
+
+/* Defaults: 128 bases, bits 7..31, 4 pairs, 8 passes, seed 1, threshold 0.5,
+ * tie 20 cycles, margin 0.1. */
+void asym_interleave_params_default(asym_interleave_params* p);
+
+enum { ASYM_BIT_UNDETERMINED = -1, ASYM_BIT_NOT_TESTED = -2 };
+
+typedef struct asym_interleave_result {
+  int n_xcds;
+  int n_groups;
+  int group_of_xcd[ASYM_MAX_XCDS];
+  int n_addresses;
+  int block;                 /* addresses per block */
+  double flip_fraction[64];  /* per bit: share of usable blocks whose base and one-bit
+                                variant have different homes; -1 if none usable */
+  int usable[64];            /* blocks where both homes were classified */
+  int verdict[64];           /* 1 takes part (fraction >= 1 - decide), 0 does not
+                                (<= decide), ASYM_BIT_UNDETERMINED (between, or no
+                                usable block), ASYM_BIT_NOT_TESTED (never flipped) */
+  uint64_t hash_mask;        /* bits with verdict 1 */
+  int lowest_bit;            /* lowest bit with verdict 1, -1 if none */
+  int determined_below;      /* lowest tested bit that is undetermined (one past the
+                                highest tested bit if none): every tested bit below
+                                it has a verdict */
+  int64_t granularity;       /* 2^lowest_bit bytes when lowest_bit < determined_below,
+                                else -1 */
+  int pair_checks;           /* two-bit variants whose bits both have verdicts and whose
+                                homes (and the base's) are classified */
+  int pair_agree;            /* of those, variants whose home differs from the base's
+                                exactly when one of the two bits takes part */
+  double linear_consistency; /* pair_agree / pair_checks, -1 without checks */
+  double unclassified_share; /* addresses with no home (tie) */
+  double local_cycles;       /* mean HBM latency from an XCD to lines homed in its own
+                                group, over (XCD, line) pairs; -1 if none */
+  double remote_cycles;      /* same, lines homed in another group */
+  uint64_t base_align;       /* probe only (0 from the analysis): the largest power of
+                                two dividing the walked range's start address */
+} asym_interleave_result;
+
+/* Run the probe on `device` with params p (NULL = defaults).  With
+ * n = n_bases * (1 + hi_bit - lo_bit + n_pairs) addresses: offs (nullable)
+ * receives their byte offsets [n], lat (nullable) the HBM latencies
+ * uint32 [n_xcds][n] (n_xcds <= ASYM_MAX_XCDS), home (nullable) each address's
+ * home group or -1 [n].  The result is asym_interleave_analyze of the
+ * measurement plus base_align.  Allocates max(2^hi_bit, 2 MiB) + 2 MiB and a
+ * 1 GiB flush buffer for the duration of the call.  Synchronous.
+ * Errors: ASYM_EINVAL, ASYM_ENOMEM, ASYM_EHIP, ASYM_ETIMEOUT. */
+int asym_interleave_probe(int device, const asym_interleave_params* p, uint64_t* offs,
+                          uint32_t* lat, int8_t* home, asym_interleave_result* out);
+
+/* Analysis alone (host only, no GPU).  hbm_lat uint32 [n_xcds][n_addr],
+ * offs [n_addr] in blocks of `block` (base first; a variant's flipped bits are
+ * its offset XOR its base's: one bit = a flip test, two = a pair check, other
+ * counts are ignored).  Homes as asym_latency_analyze with group_threshold and
+ * tie_cycles; home (nullable) receives them.  Errors: ASYM_EINVAL (sizes, a
+ * partial block, decide outside (0, 0.5)). */
+int asym_interleave_analyze(const uint32_t* hbm_lat, int n_xcds, int n_addr,
+                            const uint64_t* offs, int block, double group_threshold,
+                            double tie_cycles, double decide, int8_t* home,
+                            asym_interleave_result* out);
+
 /* ---- CU sets and masked streams ----------------------------------------- */
 /* Choose n_cus compute units by `policy` among the CUs not in `exclude`
  * (nullable), and write their CU-mask bits to mask_out[ASYM_MASK_WORDS].

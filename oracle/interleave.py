@@ -26,7 +26,9 @@ where the paper gives no rule:
     the base's exactly when one of the two bits takes part.  Only pairs whose
     two bits have verdict 0 or 1 and whose two homes exist are counted;
   * the granularity is 2 to the lowest participating bit, when every tested bit
-    below it has a verdict; else unknown.
+    below it has a verdict; else unknown;
+  * the local and remote tiers are the mean latencies over (XCD, address) pairs
+    whose address has a home in the XCD's own group, or in another group.
 Plain Python; no code shared with the library.
 """
 from __future__ import annotations
@@ -94,7 +96,12 @@ def analyze(lat, offs, block: int, threshold: float = 0.5, tie: float = 20.0,
     undet = [i for i in tested_bits if verdict[i] == UNDETERMINED]
     determined_below = min(undet) if undet else (max(tested_bits) + 1 if tested_bits else 0)
     gran = (1 << lowest) if 0 <= lowest < determined_below else -1
-    return {"n_groups": a["n_groups"], "group_of_xcd": a["group_of_xcd"], "home": home,
+    grp = a["group_of_xcd"]
+    loc = [lat[x][i] for x in range(len(lat)) for i in range(n_addr) if home[i] >= 0 and home[i] == grp[x]]
+    rem = [lat[x][i] for x in range(len(lat)) for i in range(n_addr) if home[i] >= 0 and home[i] != grp[x]]
+    return {"local_cycles": sum(loc) / len(loc) if loc else -1.0,
+            "remote_cycles": sum(rem) / len(rem) if rem else -1.0,
+            "n_groups": a["n_groups"], "group_of_xcd": a["group_of_xcd"], "home": home,
             "unclassified_share": a["unclassified_share"],
             "flip_fraction": frac, "usable": usable, "verdict": verdict,
             "hash_mask": mask, "lowest_bit": lowest, "determined_below": determined_below,

@@ -36,6 +36,7 @@ EXPORTS = (
     "asym_topology_free", "asym_topology_info", "asym_topology_cu",
     "asym_topology_dispatch", "asym_topology_latency", "asym_topology_json",
     "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
+    "asym_interleave_params_default", "asym_interleave_probe", "asym_interleave_analyze",
     "asym_dispatch_check", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
@@ -89,6 +90,35 @@ class LatencySummary(ctypes.Structure):
                 "unclassified_share": self.unclassified_share,
                 "corr": [list(self.corr[x])[:nx] for x in range(nx)],
                 "hbm_by_home": [list(self.hbm_by_home[x])[:ng] for x in range(nx)]}
+
+
+class InterleaveParams(ctypes.Structure):
+    _fields_ = [("n_bases", ctypes.c_int), ("lo_bit", ctypes.c_int), ("hi_bit", ctypes.c_int),
+                ("n_pairs", ctypes.c_int), ("passes", ctypes.c_int), ("seed", ctypes.c_uint64),
+                ("group_threshold", ctypes.c_double), ("tie_cycles", ctypes.c_double),
+                ("decide", ctypes.c_double)]
+
+
+class InterleaveResult(ctypes.Structure):
+    _fields_ = [("n_xcds", ctypes.c_int), ("n_groups", ctypes.c_int),
+                ("group_of_xcd", ctypes.c_int * MAX_XCDS), ("n_addresses", ctypes.c_int),
+                ("block", ctypes.c_int), ("flip_fraction", ctypes.c_double * 64),
+                ("usable", ctypes.c_int * 64), ("verdict", ctypes.c_int * 64),
+                ("hash_mask", ctypes.c_uint64), ("lowest_bit", ctypes.c_int),
+                ("determined_below", ctypes.c_int), ("granularity", ctypes.c_int64),
+                ("pair_checks", ctypes.c_int), ("pair_agree", ctypes.c_int),
+                ("linear_consistency", ctypes.c_double), ("unclassified_share", ctypes.c_double),
+                ("local_cycles", ctypes.c_double), ("remote_cycles", ctypes.c_double),
+                ("base_align", ctypes.c_uint64)]
+
+    def to_dict(self) -> dict:
+        d = {k: getattr(self, k) for k, _ in self._fields_
+             if k not in ("group_of_xcd", "flip_fraction", "usable", "verdict")}
+        d["group_of_xcd"] = list(self.group_of_xcd)[:self.n_xcds]
+        d["flip_fraction"] = list(self.flip_fraction)
+        d["usable"] = list(self.usable)
+        d["verdict"] = list(self.verdict)
+        return d
 
 
 class Task(ctypes.Structure):
@@ -150,6 +180,12 @@ def load_library(path: str = LIB_PATH):
         "asym_latency_probe": (i, [i, ctypes.POINTER(LatencyParams), u32p, ctypes.POINTER(LatencySummary)]),
         "asym_latency_analyze": (i, [u32p, i, i, ctypes.c_double, ctypes.c_double,
                                      ctypes.POINTER(LatencySummary)]),
+        "asym_interleave_params_default": (None, [ctypes.POINTER(InterleaveParams)]),
+        "asym_interleave_probe": (i, [i, ctypes.POINTER(InterleaveParams), ctypes.POINTER(ctypes.c_uint64),
+                                      u32p, ctypes.POINTER(ctypes.c_int8), ctypes.POINTER(InterleaveResult)]),
+        "asym_interleave_analyze": (i, [u32p, i, i, ctypes.POINTER(ctypes.c_uint64), i, ctypes.c_double,
+                                        ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_int8),
+                                        ctypes.POINTER(InterleaveResult)]),
         "asym_topology_json": (i, [topo_p, cp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_cuset_make": (i, [topo_p, i, i, ctypes.c_uint64, u32p, u32p]),
         "asym_cuset_counts": (i, [topo_p, u32p, ip]),
@@ -336,6 +372,57 @@ def latency_analyze(hbm_lat, group_threshold: float = 0.5, tie_cycles: float = 2
                                                L.shape[0], L.shape[1], group_threshold, tie_cycles,
                                                ctypes.byref(s)))
     return s.to_dict()
+
+
+def interleave_params_default() -> dict:
+    p = InterleaveParams()
+    load_library().asym_interleave_params_default(ctypes.byref(p))
+    return {k: getattr(p, k) for k, _ in p._fields_}
+
+
+def interleave_probe(device: int = 0, **kw):
+    """Run the partition-hash probe; returns (result dict, offsets uint64 [n],
+    HBM latencies uint32 [n_xcds, n], homes int8 [n])."""
+    import numpy as np
+    p = InterleaveParams()
+    load_library().asym_interleave_params_default(ctypes.byref(p))
+    for k, v in kw.items():
+        if not hasattr(p, k):
+            raise TypeError(f"unknown interleave parameter {k}")
+        setattr(p, k, v)
+    n = p.n_bases * (1 + p.hi_bit - p.lo_bit + p.n_pairs)
+    n_x = device_query(device)["n_xccs"]
+    offs = np.zeros(n, dtype=np.uint64)
+    lat = np.zeros((n_x, n), dtype=np.uint32)
+    home = np.zeros(n, dtype=np.int8)
+    r = InterleaveResult()
+    _check(load_library().asym_interleave_probe(
+        device, ctypes.byref(p), offs.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
+        lat.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+        home.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)), ctypes.byref(r)))
+    return r.to_dict(), offs, lat, home
+
+
+def interleave_analyze(hbm_lat, offs, block: int, group_threshold: float = 0.5,
+                       tie_cycles: float = 20.0, decide: float = 0.1) -> dict:
+    """Partition-hash analysis of uint32 [n_xcds, n] HBM latencies over byte
+    offsets [n] in blocks of `block` (host only); the dict carries the homes."""
+    import numpy as np
+    L = np.ascontiguousarray(hbm_lat, dtype=np.uint32)
+    o = np.ascontiguousarray(offs, dtype=np.uint64)
+    if L.ndim != 2 or o.ndim != 1:
+        raise ValueError("latencies must be [n_xcds, n] and offsets [n]")
+    if L.shape[1] != o.shape[0]:
+        raise ValueError("latency columns and offsets differ in count")
+    home = np.zeros(o.shape[0], dtype=np.int8)
+    r = InterleaveResult()
+    _check(load_library().asym_interleave_analyze(
+        L.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), L.shape[0], o.shape[0],
+        o.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), block, group_threshold, tie_cycles, decide,
+        home.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)), ctypes.byref(r)))
+    d = r.to_dict()
+    d["home"] = [int(h) for h in home]
+    return d
 
 
 def topology_from_records(records, n_cus: int, n_xccs: int, mask_bit_record=None) -> Topology:

@@ -20,6 +20,7 @@ LIB = os.path.join(PKG, "libasym.so")
 ARCH = "gfx950"
 
 SOURCES = ["capi.cpp", "topology.cpp", "schedule.cpp", "corun.cpp", "affinity.cpp",
+           "interleave.cpp",
            "gemm.hip", "probe.hip", "latency.hip", "copy.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -17,7 +17,7 @@
 namespace asym {
 
 int analyze_latency(const uint32_t* L, int n_x, int n_s, double threshold, double tie,
-                    asym_latency_summary& out) {
+                    asym_latency_summary& out, int8_t* home) {
   if (!L || n_x < 1 || n_x > ASYM_MAX_XCDS || n_s < 1)
     return fail(ASYM_EINVAL, "latency analysis: bad sizes");
   if (!std::isfinite(threshold) || !std::isfinite(tie) || tie < 0)
@@ -109,6 +109,7 @@ int analyze_latency(const uint32_t* L, int n_x, int n_s, double threshold, doubl
     bool tied = false;
     for (int g = 0; g < n_g; ++g)
       if (g != best && gsum[g] / gsize[g] - b1 < tie) tied = true;
+    if (home) home[i] = (int8_t)(tied ? -1 : best);
     if (tied) {
       ++unclassified;
       continue;

@@ -94,9 +94,36 @@ int probe_identity_run(int device, hipStream_t s, int n_blocks,
 int probe_latency_run(int device, Topology& t);
 int latency_probe(int device, const asym_latency_params& p, uint32_t* lat_out,
                   asym_latency_summary& out);
-// Affinity groups and home groups from HBM latencies [n_x][n_s] (host only).
+// One latency measurement over explicit line offsets of a fresh allocation of
+// `alloc` bytes (2 MiB aligned): per XCD and pass, the HBM regime over every
+// offset, the L2 regime over the first l2_samples and (if mall) the
+// memory-side-cache regime over every offset; best = per-(regime, XCD,
+// offset) minima, [3][n_x][offs.size()], regimes L2, MALL, HBM (UINT32_MAX
+// where not timed).  Each timed load is preceded by a load of the line at
+// offset ^ touch_delta (translation warm-up; must stay in the allocation).
+struct LatencyMeasure {
+  size_t alloc = 0;
+  std::vector<uint64_t> offs;
+  int passes = 8;
+  int l2_samples = 0;
+  bool mall = true;
+  uint64_t touch_delta = 1ull << 20;
+  int n_x = 0;                     // out
+  std::vector<uint32_t> best;      // out
+  double timer_overhead = -1.0;    // out
+  double clock_mhz = -1.0;         // out
+  uint64_t base_align = 0;         // out: largest power of two dividing the base address
+};
+int latency_measure(int device, LatencyMeasure& m);
+// Affinity groups and home groups from HBM latencies [n_x][n_s] (host only);
+// home (nullable, n_s entries) receives each address's home group, -1 if tied.
 int analyze_latency(const uint32_t* lat, int n_x, int n_s, double threshold, double tie,
-                    asym_latency_summary& out);
+                    asym_latency_summary& out, int8_t* home = nullptr);
+
+// Partition-hash analysis of HBM latencies [n_x][n_a] over offsets in blocks (host only).
+int analyze_interleave(const uint32_t* L, int n_x, int n_a, const uint64_t* offs, int block,
+                       double threshold, double tie, double decide, int8_t* home_out,
+                       asym_interleave_result& r);
 
 int launch_copy(void* dst, const void* src, size_t n_bytes, int passes,
                 const int* stop_flag, uint32_t xcd_mask, int grid,

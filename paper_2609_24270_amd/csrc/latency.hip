@@ -8,7 +8,9 @@
 // its XCD from the XCC_ID register; the launch has several workgroups per XCD
 // and the first one on the wanted XCD to take a ticket does the walk, the
 // rest exit at once.  Before each timed load the lane loads another line of
-// the same 2 MiB page (translation warm-up, outside the window).
+// the same 2 MiB page (translation warm-up, outside the window); the host
+// picks that line's distance so that it is never a line timed later in the
+// same walk.
 //
 // Regimes are set up around the walk by the host: an untimed walk by the same
 // XCD first (L2), or a cache flush followed by an untimed walk on another XCD
@@ -40,6 +42,7 @@ struct LatArgs {
   uint64_t* info;         // [8]: sink, memtime0, memtime1, realtime0, realtime1,
                           //      min empty window, done, xcc
   int* ticket;            // zero before the launch
+  uint64_t touch;         // translation warm-up: the line at offset ^ touch
   int n;
   int target;             // XCC that runs the walk
   int mode;
@@ -70,7 +73,7 @@ __global__ void __launch_bounds__(64) latency_kernel(LatArgs a) {
     const uint64_t off = a.offs[i];
     const uint32_t* p = reinterpret_cast<const uint32_t*>(a.base + off);
     if (a.mode == kModeTimed) {
-      const uint32_t* q = reinterpret_cast<const uint32_t*>(a.base + (off ^ kTouchDelta));
+      const uint32_t* q = reinterpret_cast<const uint32_t*>(a.base + (off ^ a.touch));
       uint32_t w, v;
       uint64_t t0, t1;
       asm volatile(
@@ -149,51 +152,45 @@ int validate(const asym_latency_params& p) {
 
 }  // namespace
 
-int latency_probe(int device, const asym_latency_params& p, uint32_t* lat_out,
-                  asym_latency_summary& out) {
-  int rc = validate(p);
-  if (rc != ASYM_OK) return rc;
+int latency_measure(int device, LatencyMeasure& m) {
   ASYM_HIP(hipSetDevice(device));
   int n_x = 0, wall_khz = 0;
   ASYM_HIP(hipDeviceGetAttribute(&n_x, hipDeviceAttributeNumberOfXccs, device));
   ASYM_HIP(hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, device));
   if (n_x < 1 || n_x > ASYM_MAX_XCDS) return fail(ASYM_EUNSUPPORTED, "latency probe: XCD count");
-  size_t free_b = 0, total_b = 0;
-  ASYM_HIP(hipMemGetInfo(&free_b, &total_b));
-  size_t alloc = p.alloc_bytes ? p.alloc_bytes : (32ull << 30);
-  const size_t room = free_b > kFlushBytes + (1ull << 30) ? free_b - kFlushBytes - (1ull << 30) : 0;
-  if (alloc > room) {
-    if (p.alloc_bytes) return fail(ASYM_ENOMEM, "latency probe: allocation larger than free memory");
-    alloc = room / 2;
-  }
-  alloc -= alloc % kPage;
-  if (alloc < (64ull << 20)) return fail(ASYM_ENOMEM, "latency probe: not enough free device memory");
-
-  const int n_s = p.n_samples;
-  std::vector<uint64_t> offs(n_s);
-  uint64_t st = p.seed;
-  const uint64_t lines = alloc / 128;
-  for (int i = 0; i < n_s; ++i) offs[i] = (splitmix64(st) % lines) * 128;
+  const int n_s = (int)m.offs.size();
+  if (n_s < 1 || m.alloc % kPage || m.alloc == 0 || m.passes < 1 || m.l2_samples < 0 ||
+      m.l2_samples > n_s)
+    return fail(ASYM_EINVAL, "latency probe: bad measurement set-up");
+  for (uint64_t o : m.offs)
+    if (o % 128 || o >= m.alloc || (o ^ m.touch_delta) >= m.alloc || ((o ^ m.touch_delta) % 128))
+      return fail(ASYM_EINVAL, "latency probe: offset or its translation touch outside the allocation");
 
   DevBufs b;
   ASYM_HIP(hipStreamCreateWithFlags(&b.s, hipStreamNonBlocking));
-  ASYM_HIP(hipMalloc(&b.p[0], alloc));
+  // one page more than asked, so the walked range can start on a 2 MiB boundary
+  ASYM_HIP(hipMalloc(&b.p[0], m.alloc + kPage));
   ASYM_HIP(hipMalloc(&b.p[1], kFlushBytes));
   ASYM_HIP(hipMalloc(&b.p[2], sizeof(uint64_t) * n_s));
   ASYM_HIP(hipMalloc(&b.p[3], sizeof(uint32_t) * n_s));
   ASYM_HIP(hipMalloc(&b.p[4], sizeof(uint64_t) * 8));
   ASYM_HIP(hipMalloc(&b.p[5], sizeof(int) * 4));
-  ASYM_HIP(hipMemcpy(b.p[2], offs.data(), sizeof(uint64_t) * n_s, hipMemcpyHostToDevice));
-  ASYM_HIP(hipMemset(b.p[0], 0, alloc));
+  ASYM_HIP(hipMemcpy(b.p[2], m.offs.data(), sizeof(uint64_t) * n_s, hipMemcpyHostToDevice));
+  ASYM_HIP(hipMemset(b.p[0], 0, m.alloc + kPage));
+  const uintptr_t raw = reinterpret_cast<uintptr_t>(b.p[0]);
+  const uintptr_t base = (raw + kPage - 1) & ~(uintptr_t)(kPage - 1);
+  m.base_align = base & (~base + 1);
 
   LatArgs a;
-  a.base = static_cast<const char*>(b.p[0]);
+  a.base = reinterpret_cast<const char*>(base);
   a.offs = static_cast<const uint64_t*>(b.p[2]);
   a.lat = static_cast<uint32_t*>(b.p[3]);
   a.info = static_cast<uint64_t*>(b.p[4]);
   a.ticket = static_cast<int*>(b.p[5]);
+  a.touch = m.touch_delta;
 
-  std::vector<uint32_t> best((size_t)3 * n_x * n_s, UINT32_MAX);
+  m.n_x = n_x;
+  m.best.assign((size_t)3 * n_x * n_s, UINT32_MAX);
   std::vector<uint32_t> host(n_s);
   uint64_t ov_min = ~0ull, d_mt = 0, d_rt = 0;
   int flush_value = 1;
@@ -226,23 +223,59 @@ int latency_probe(int device, const asym_latency_params& p, uint32_t* lat_out,
     return ASYM_OK;
   };
 
-  for (int pass = 0; pass < p.passes; ++pass) {
+  int rc = ASYM_OK;
+  for (int pass = 0; pass < m.passes; ++pass) {
     for (int x = 0; x < n_x; ++x) {
-      uint32_t* l2 = &best[((size_t)0 * n_x + x) * n_s];
-      uint32_t* mall = &best[((size_t)1 * n_x + x) * n_s];
-      uint32_t* hbm = &best[((size_t)2 * n_x + x) * n_s];
+      uint32_t* l2 = &m.best[((size_t)0 * n_x + x) * n_s];
+      uint32_t* mall = &m.best[((size_t)1 * n_x + x) * n_s];
+      uint32_t* hbm = &m.best[((size_t)2 * n_x + x) * n_s];
       // L2: the same XCD loads the lines, then times them
-      if ((rc = flush()) || (rc = walk(x, kModeWarm, p.l2_samples, nullptr)) ||
-          (rc = walk(x, kModeTimed, p.l2_samples, l2)))
+      if (m.l2_samples > 0 && ((rc = flush()) || (rc = walk(x, kModeWarm, m.l2_samples, nullptr)) ||
+                               (rc = walk(x, kModeTimed, m.l2_samples, l2))))
         return rc;
       // memory-side cache: flush, another XCD loads the lines, x times them
-      if ((rc = flush()) || (rc = walk((x + 1) % n_x, kModeWarm, n_s, nullptr)) ||
-          (rc = walk(x, kModeTimed, n_s, mall)))
+      if (m.mall && ((rc = flush()) || (rc = walk((x + 1) % n_x, kModeWarm, n_s, nullptr)) ||
+                     (rc = walk(x, kModeTimed, n_s, mall))))
         return rc;
       // HBM: flush, x times the lines
       if ((rc = flush()) || (rc = walk(x, kModeTimed, n_s, hbm))) return rc;
     }
   }
+  m.timer_overhead = (double)ov_min;
+  m.clock_mhz = d_rt > 0 ? (double)d_mt / (double)d_rt * (wall_khz / 1000.0) : -1.0;
+  return ASYM_OK;
+}
+
+int latency_probe(int device, const asym_latency_params& p, uint32_t* lat_out,
+                  asym_latency_summary& out) {
+  int rc = validate(p);
+  if (rc != ASYM_OK) return rc;
+  ASYM_HIP(hipSetDevice(device));
+  size_t free_b = 0, total_b = 0;
+  ASYM_HIP(hipMemGetInfo(&free_b, &total_b));
+  size_t alloc = p.alloc_bytes ? p.alloc_bytes : (32ull << 30);
+  const size_t room = free_b > kFlushBytes + (1ull << 30) ? free_b - kFlushBytes - (1ull << 30) : 0;
+  if (alloc > room) {
+    if (p.alloc_bytes) return fail(ASYM_ENOMEM, "latency probe: allocation larger than free memory");
+    alloc = room / 2;
+  }
+  alloc -= alloc % kPage;
+  if (alloc < (64ull << 20)) return fail(ASYM_ENOMEM, "latency probe: not enough free device memory");
+
+  LatencyMeasure m;
+  m.alloc = alloc;
+  m.passes = p.passes;
+  m.l2_samples = p.l2_samples;
+  m.mall = true;
+  m.touch_delta = kTouchDelta;
+  const int n_s = p.n_samples;
+  m.offs.resize(n_s);
+  uint64_t st = p.seed;
+  const uint64_t lines = alloc / 128;
+  for (int i = 0; i < n_s; ++i) m.offs[i] = (splitmix64(st) % lines) * 128;
+  if ((rc = latency_measure(device, m)) != ASYM_OK) return rc;
+  const int n_x = m.n_x;
+  std::vector<uint32_t>& best = m.best;
 
   rc = analyze_latency(&best[(size_t)2 * n_x * n_s], n_x, n_s, p.group_threshold, p.tie_cycles, out);
   if (rc != ASYM_OK) return rc;
@@ -255,8 +288,8 @@ int latency_probe(int device, const asym_latency_params& p, uint32_t* lat_out,
   }
   out.passes = p.passes;
   out.l2_samples = p.l2_samples;
-  out.timer_overhead = (double)ov_min;
-  out.clock_mhz = d_rt > 0 ? (double)d_mt / (double)d_rt * (wall_khz / 1000.0) : -1.0;
+  out.timer_overhead = m.timer_overhead;
+  out.clock_mhz = m.clock_mhz;
   if (lat_out) {
     for (int x = 0; x < n_x; ++x)
       for (int i = p.l2_samples; i < n_s; ++i) best[((size_t)0 * n_x + x) * n_s + i] = 0;

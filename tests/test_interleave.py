@@ -39,6 +39,8 @@ def test_oracle_recovers_a_planted_parity_inside_the_page():
     assert r["determined_below"] == 21
     assert r["pair_checks"] > 0 and r["linear_consistency"] == 1.0
     assert all(r["verdict"][b] == oil.NOT_TESTED for b in list(range(LO)) + list(range(HI, 64)))
+    # planted tiers 735 / 950 plus offsets in [0, 40) and jitter in [0, 12)
+    assert 735 <= r["local_cycles"] < 735 + 51 and 950 <= r["remote_cycles"] < 950 + 51
 
 
 def test_oracle_with_contiguous_pages_sees_every_bit():
@@ -95,3 +97,56 @@ def test_oracle_without_homes_decides_nothing():
 def test_oracle_rejects_partial_blocks():
     with pytest.raises(ValueError):
         oil.analyze([[1, 2, 3]] * 8, [0, 128, 256], 2)
+
+
+def _lib_result(L, offs, block, threshold=0.5, tie=20.0, decide=0.1):
+    lib = asym.load_library()
+    return asym.interleave_analyze(np.asarray(L, dtype=np.uint32), offs, block, threshold, tie, decide)
+
+
+def _compare(res, ref):
+    for k in ("n_groups", "group_of_xcd", "home", "usable", "verdict", "hash_mask", "lowest_bit",
+              "determined_below", "granularity", "pair_checks", "pair_agree"):
+        assert res[k] == ref[k], k
+    for k in ("flip_fraction",):
+        assert all(abs(a - b) < 1e-12 for a, b in zip(res[k], ref[k])), k
+    for k in ("linear_consistency", "unclassified_share", "local_cycles", "remote_cycles"):
+        assert abs(res[k] - ref[k]) < 1e-9 * max(1.0, abs(ref[k])), k
+
+
+@pytest.mark.parametrize("case", ["xor_page", "contiguous", "mixed", "no_homes", "one_bit"])
+def test_library_analysis_matches_oracle(case):
+    if case == "xor_page":
+        offs, block = workloads.interleave_layout(3, 64, LO, HI, 4)
+        L, _ = workloads.planted_interleave_latency(4, offs, (1 << 12) | (1 << 15) | (1 << 24))
+    elif case == "contiguous":
+        offs, block = workloads.interleave_layout(5, 32, LO, 24, 6)
+        L, _ = workloads.planted_interleave_latency(6, offs, (1 << 8) | (1 << 22), page_bits=40)
+    elif case == "mixed":
+        offs, block = workloads.interleave_layout(7, 100, LO, 20, 3)
+        L, _ = workloads.planted_interleave_latency(8, offs, (1 << 12) | (1 << 13) | (1 << 14), rule="mixed")
+    elif case == "no_homes":
+        offs, block = workloads.interleave_layout(9, 8, LO, 12, 1)
+        L = np.full((8, len(offs)), 800, dtype=np.uint32)
+    else:
+        offs, block = workloads.interleave_layout(10, 16, 12, 13, 0)
+        L, _ = workloads.planted_interleave_latency(11, offs, 1 << 12)
+    ref = oil.analyze(np.asarray(L).tolist(), offs, block)
+    _compare(_lib_result(L, offs, block), ref)
+
+
+def test_library_analysis_rejects_bad_input():
+    offs, block = workloads.interleave_layout(3, 4, LO, 10, 1)
+    L = np.full((8, len(offs)), 800, dtype=np.uint32)
+    with pytest.raises(asym.AsymError):
+        asym.interleave_analyze(L[:, :-1], offs[:-1], block)     # partial block
+    with pytest.raises(asym.AsymError):
+        asym.interleave_analyze(L, offs, block, decide=0.5)      # margin out of range
+    with pytest.raises(asym.AsymError):
+        asym.interleave_analyze(np.full((17, len(offs)), 800, dtype=np.uint32), offs, block)
+
+
+def test_interleave_params_defaults():
+    p = asym.interleave_params_default()
+    assert (p["n_bases"], p["lo_bit"], p["hi_bit"], p["n_pairs"], p["passes"]) == (128, 7, 32, 4, 8)
+    assert p["decide"] == 0.1 and p["tie_cycles"] == 20.0 and p["group_threshold"] == 0.5
