@@ -328,6 +328,55 @@ def grouped_study(dev, stream, seeds, launches: int, rounds: int):
             "aware_speedup_vs_oblivious_rowmajor": summ(sp_r), "per_config": per}
 
 
+def interleave_summary(dev):
+    """Partition-hash discovery over offset bits 7..33 of a 16 GiB allocation."""
+    import paper_2609_24270_amd as asym
+    r, *_ = asym.interleave_probe(0, n_bases=128, lo_bit=7, hi_bit=34, n_pairs=4, passes=4)
+    bits = "".join({1: "1", 0: "0", -1: "?", -2: "."}[r["verdict"][b]] for b in range(7, 34))
+    return {"hash_mask": hex(r["hash_mask"]), "lowest_bit": r["lowest_bit"], "granularity": r["granularity"],
+            "determined_below": r["determined_below"], "verdicts_bits_7_to_33": bits,
+            "pair_checks": r["pair_checks"], "pair_agree": r["pair_agree"],
+            "unclassified_share": round(r["unclassified_share"], 4),
+            "local_cycles": round(r["local_cycles"], 1), "remote_cycles": round(r["remote_cycles"], 1),
+            "group_of_xcd": r["group_of_xcd"]}, r
+
+
+def numa_bw_study(dev, hash_res, rounds: int = 3, gib: int = 16):
+    """Read bandwidth of a 16 GiB region by chunk home: every chunk read once per
+    iteration, each XCD reading chunks homed on its own group (local), on the
+    other group (remote), or chunks in address order whatever their home (all);
+    on the whole chip and on one group's XCDs alone."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    nbytes = gib << 30
+    page = 2 << 20
+    raw = torch.empty(nbytes + page, dtype=torch.uint8, device=dev)
+    shift = (-raw.data_ptr()) % page
+    ptr = raw.data_ptr() + shift
+    raw.fill_(1)
+    chunk_log2 = max(12, hash_res["lowest_bit"])
+    info, homes = asym.home_map(ptr, nbytes, hash_res["hash_mask"], chunk_log2,
+                                group_of_xcd=hash_res["group_of_xcd"], passes=2, n_verify=4096, seed=7)
+    grp = info["group_of_xcd"]
+    g0 = sum(1 << x for x, g in enumerate(grp) if g == 0)
+    cases = {}
+    for where, xm in (("chip", 0), ("group0_xcds", g0)):
+        for name, mode in (("all", asym.CHUNKS_ALL), ("local", asym.CHUNKS_LOCAL), ("remote", asym.CHUNKS_REMOTE)):
+            cases[f"{where}_{name}"] = asym.chunk_lists(homes, len(grp), grp, mode, xm)
+    acc = {k: 0.0 for k in cases}
+    for _ in range(rounds):
+        for k, (chunks, off) in cases.items():
+            ms, _ = asym.chunk_read_bw(ptr, nbytes, chunk_log2, chunks, off, iters=5)
+            acc[k] += len(chunks) * (1 << chunk_log2) / (ms * 1e-3) / 1e9
+    del raw
+    torch.cuda.empty_cache()
+    return {"region_gib": gib, "chunk_bytes": 1 << chunk_log2, "rounds": rounds,
+            "map": {k: info[k] for k in ("n_pages", "unclassified_pages", "chunk_share", "verify_classified",
+                                         "verify_agree", "local_cycles", "remote_cycles")},
+            "GBps": {k: round(v / rounds, 1) for k, v in acc.items()}}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -344,10 +393,11 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped",
+    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
-                         "grouped (expert-layer grouped GEMMs); 'none' for the headline only")
+                         "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
+                         "remote read bandwidth); 'none' for the headline only")
     ap.add_argument("--spread-masks", type=int, default=32)
     ap.add_argument("--mapping-only", default=None,
                     help="time only this mapping, no studies (profiling runs)")
@@ -453,6 +503,11 @@ def main() -> int:
         line["cu_set_spread"] = spread_study(topo, dev, args.spread_masks, 20, halves)
     if "grouped" in studies:
         line["grouped_gemm"] = grouped_study(dev, stream, range(1, 6), 8, 5)
+    if "numa" in studies:
+        summ, hres = interleave_summary(dev)
+        line["partition_hash"] = summ
+        if hres["n_groups"] == 2:
+            line["numa_read_bw"] = numa_bw_study(dev, hres)
     line["cpu_baseline"] = None if args.no_cpu else cpu_baseline(A, B, args.cpu_rows)
     if line["cpu_baseline"]:
         line["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)

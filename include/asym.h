@@ -347,6 +347,83 @@ int asym_interleave_analyze(const uint32_t* hbm_lat, int n_xcds, int n_addr,
                             double tie_cycles, double decide, int8_t* home,
                             asym_interleave_result* out);
 
+/* ---- home map of an allocation, local / remote reads (Section 6.1 local
+ *      and remote bandwidth; Appendix on NUMA-aware address remapping) ---- */
+/* Home group (0 or 1) of every 2^chunk_log2-byte chunk of the caller's device
+ * range [ptr, ptr + bytes).  The first line of every 2 MiB page is timed from
+ * every XCD (HBM regime, minimum over `passes`, translation touch 1 MiB away in
+ * the same page), giving the page's home; a chunk's home is its page's home
+ * XOR the parity of (chunk offset in the page & hash_mask), the partition
+ * hash from asym_interleave_probe restricted to bits below 2 MiB.  Chunks of a
+ * page whose first line has no home (tie) get -1.  group_of_xcd (nullable,
+ * n_xcds ints) gives the XCD groups; NULL = found from the timed lines by
+ * correlation as in asym_latency_analyze.  n_verify random lines (seeded) are
+ * also timed and their measured homes compared with the map.  The range is
+ * only read.
+ * Requirements: ptr and bytes multiples of 2 MiB, 12 <= chunk_log2 <= 21,
+ * hash_mask without bits below chunk_log2 inside the page (a chunk must have
+ * one home), exactly two groups, at least 16 pages when the groups are found
+ * here.  chunk_home receives bytes >> chunk_log2 entries.  Synchronous;
+ * allocates a 1 GiB flush buffer for the call.
+ * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED (not two groups), ASYM_EHIP,
+ * ASYM_ETIMEOUT. */
+typedef struct asym_home_map_info {
+  int n_pages;
+  int n_chunks;
+  int n_groups;
+  int group_of_xcd[ASYM_MAX_XCDS];
+  int unclassified_pages;
+  double chunk_share[2];     /* chunks homed on group 0 / group 1 */
+  int n_verify;
+  int verify_classified;     /* verification lines with a measured home */
+  int verify_agree;          /* of those, lines whose measured home equals the map's */
+  double local_cycles;       /* page lines: mean HBM latency from an XCD to lines of
+                                its own group / of the other group */
+  double remote_cycles;
+} asym_home_map_info;
+
+int asym_home_map(int device, const void* ptr, size_t bytes, uint64_t hash_mask, int chunk_log2,
+                  const int* group_of_xcd, int passes, int n_verify, uint64_t seed,
+                  double tie_cycles, int8_t* chunk_home, asym_home_map_info* info);
+
+/* The map's host analysis alone (no GPU): lat uint32 [n_xcds][n_pages +
+ * n_verify] holds the HBM latencies of each page's first line, then of the
+ * verification lines at byte offsets verify_offs[n_verify] (below n_pages *
+ * 2 MiB); group_of_xcd (required) the two groups.  Same outputs and rules as
+ * asym_home_map.  Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED. */
+int asym_home_map_analyze(const uint32_t* lat, int n_xcds, int n_pages, const uint64_t* verify_offs,
+                          int n_verify, const int* group_of_xcd, uint64_t hash_mask, int chunk_log2,
+                          double tie_cycles, int8_t* chunk_home, asym_home_map_info* info);
+
+/* Which chunks each XCD reads, for the read-bandwidth kernel (host only).
+ * Active XCDs: bits of xcd_mask (0 = all n_xcds).  Modes:
+ *   ALL:    every chunk, dealt round-robin over the active XCDs in chunk order;
+ *   LOCAL:  the chunks homed on group g, dealt round-robin over g's active XCDs;
+ *   REMOTE: the chunks homed on g, dealt over the other group's active XCDs.
+ * LOCAL and REMOTE skip chunks with no home and chunks whose readers have no
+ * active XCD.  chunks_out receives the chunk indices XCD by XCD (at most
+ * n_chunks), off_out[n_xcds + 1] the start of each XCD's list, *n_listed the
+ * total.  Errors: ASYM_EINVAL (sizes, a group id outside 0..1, no active XCD). */
+enum asym_chunk_mode { ASYM_CHUNKS_ALL = 0, ASYM_CHUNKS_LOCAL = 1, ASYM_CHUNKS_REMOTE = 2 };
+int asym_chunk_lists(const int8_t* chunk_home, int n_chunks, int n_xcds, const int* group_of_xcd,
+                     uint32_t xcd_mask, int mode, uint32_t* chunks_out, int* off_out, int* n_listed);
+
+/* Read-bandwidth kernel: every XCD x reads the 2^chunk_log2-byte chunks
+ * chunks[off[x] .. off[x+1]) of the device range [base, base + bytes) (chunk
+ * c at base + c << chunk_log2; every index must lie below bytes >> chunk_log2,
+ * checked on the host), 16 bytes per lane, with 256 workgroups of 256 threads per
+ * XCD (workgroup b runs on XCD b mod n_xcds: the dispatch rule the identity
+ * probe checks).  Runs `iters` times on `stream` (NULL = null stream) between
+ * two events and reports ms per iteration; checksum_out (nullable, 4 words)
+ * receives the XOR of every 16-byte word read by one iteration.  chunks and
+ * off are host arrays, copied to the device for the call; n_xcds must be the
+ * device's XCD count; 12 <= chunk_log2 <= 21; base 16-byte aligned.  Synchronous.
+ * Errors: ASYM_EINVAL, ASYM_EHIP. */
+int asym_chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uint32_t* chunks,
+                       const int* off,
+                       int n_xcds, int iters, void* stream, uint32_t* checksum_out,
+                       double* ms_per_iter);
+
 /* ---- CU sets and masked streams ----------------------------------------- */
 /* Choose n_cus compute units by `policy` among the CUs not in `exclude`
  * (nullable), and write their CU-mask bits to mask_out[ASYM_MASK_WORDS].

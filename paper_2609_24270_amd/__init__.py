@@ -37,6 +37,7 @@ EXPORTS = (
     "asym_topology_dispatch", "asym_topology_latency", "asym_topology_json",
     "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
     "asym_interleave_params_default", "asym_interleave_probe", "asym_interleave_analyze",
+    "asym_home_map", "asym_home_map_analyze", "asym_chunk_lists", "asym_chunk_read_bw",
     "asym_dispatch_check", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
@@ -121,6 +122,23 @@ class InterleaveResult(ctypes.Structure):
         return d
 
 
+class HomeMapInfo(ctypes.Structure):
+    _fields_ = [("n_pages", ctypes.c_int), ("n_chunks", ctypes.c_int), ("n_groups", ctypes.c_int),
+                ("group_of_xcd", ctypes.c_int * MAX_XCDS), ("unclassified_pages", ctypes.c_int),
+                ("chunk_share", ctypes.c_double * 2), ("n_verify", ctypes.c_int),
+                ("verify_classified", ctypes.c_int), ("verify_agree", ctypes.c_int),
+                ("local_cycles", ctypes.c_double), ("remote_cycles", ctypes.c_double)]
+
+    def to_dict(self, n_xcds: int) -> dict:
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k not in ("group_of_xcd", "chunk_share")}
+        d["group_of_xcd"] = list(self.group_of_xcd)[:n_xcds]
+        d["chunk_share"] = list(self.chunk_share)
+        return d
+
+
+CHUNKS_ALL, CHUNKS_LOCAL, CHUNKS_REMOTE = 0, 1, 2
+
+
 class Task(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int), ("mask", ctypes.c_uint32 * MASK_WORDS),
                 ("xcd_mask", ctypes.c_uint32), ("iters", ctypes.c_int),
@@ -186,6 +204,14 @@ def load_library(path: str = LIB_PATH):
         "asym_interleave_analyze": (i, [u32p, i, i, ctypes.POINTER(ctypes.c_uint64), i, ctypes.c_double,
                                         ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_int8),
                                         ctypes.POINTER(InterleaveResult)]),
+        "asym_home_map": (i, [i, vp, ctypes.c_size_t, ctypes.c_uint64, i, ip, i, i, ctypes.c_uint64,
+                              ctypes.c_double, ctypes.POINTER(ctypes.c_int8), ctypes.POINTER(HomeMapInfo)]),
+        "asym_home_map_analyze": (i, [u32p, i, i, ctypes.POINTER(ctypes.c_uint64), i, ip, ctypes.c_uint64, i,
+                                      ctypes.c_double, ctypes.POINTER(ctypes.c_int8),
+                                      ctypes.POINTER(HomeMapInfo)]),
+        "asym_chunk_lists": (i, [ctypes.POINTER(ctypes.c_int8), i, i, ip, u32, i, u32p, ip, ip]),
+        "asym_chunk_read_bw": (i, [vp, ctypes.c_size_t, i, u32p, ip, i, i, vp, u32p,
+                                   ctypes.POINTER(ctypes.c_double)]),
         "asym_topology_json": (i, [topo_p, cp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_cuset_make": (i, [topo_p, i, i, ctypes.c_uint64, u32p, u32p]),
         "asym_cuset_counts": (i, [topo_p, u32p, ip]),
@@ -423,6 +449,71 @@ def interleave_analyze(hbm_lat, offs, block: int, group_threshold: float = 0.5,
     d = r.to_dict()
     d["home"] = [int(h) for h in home]
     return d
+
+
+def home_map(ptr: int, nbytes: int, hash_mask: int, chunk_log2: int, group_of_xcd=None,
+             passes: int = 4, n_verify: int = 1024, seed: int = 1, tie_cycles: float = 20.0,
+             device: int = 0):
+    """Home group of every 2^chunk_log2-byte chunk of the device range [ptr,
+    ptr + nbytes) (both multiples of 2 MiB); returns (info dict, int8 homes)."""
+    import numpy as np
+    homes = np.zeros(nbytes >> chunk_log2, dtype=np.int8)
+    info = HomeMapInfo()
+    g = _ints(group_of_xcd) if group_of_xcd is not None else None
+    _check(load_library().asym_home_map(device, ctypes.c_void_p(ptr), nbytes, hash_mask, chunk_log2, g,
+                                        passes, n_verify, seed, tie_cycles,
+                                        homes.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)),
+                                        ctypes.byref(info)))
+    n_x = len(group_of_xcd) if group_of_xcd is not None else device_query(device)["n_xccs"]
+    return info.to_dict(n_x), homes
+
+
+def home_map_analyze(lat, n_pages: int, verify_offs, group_of_xcd, hash_mask: int, chunk_log2: int,
+                     tie_cycles: float = 20.0):
+    """Host analysis of page-line and verification-line latencies [n_xcds,
+    n_pages + n_verify]; returns (info dict, int8 homes)."""
+    import numpy as np
+    L = np.ascontiguousarray(lat, dtype=np.uint32)
+    vo = np.ascontiguousarray(verify_offs, dtype=np.uint64)
+    if L.ndim != 2 or L.shape[1] != n_pages + vo.shape[0]:
+        raise ValueError("latencies must be [n_xcds, n_pages + n_verify]")
+    homes = np.zeros((n_pages << 21) >> chunk_log2, dtype=np.int8)
+    info = HomeMapInfo()
+    _check(load_library().asym_home_map_analyze(
+        L.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), L.shape[0], n_pages,
+        vo.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), vo.shape[0], _ints(group_of_xcd), hash_mask,
+        chunk_log2, tie_cycles, homes.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)), ctypes.byref(info)))
+    return info.to_dict(L.shape[0]), homes
+
+
+def chunk_lists(homes, n_xcds: int, group_of_xcd, mode: int, xcd_mask: int = 0):
+    """(chunk indices XCD by XCD as uint32, offsets [n_xcds + 1] as int32)."""
+    import numpy as np
+    h = np.ascontiguousarray(homes, dtype=np.int8)
+    out = np.zeros(max(1, h.shape[0]), dtype=np.uint32)
+    off = np.zeros(n_xcds + 1, dtype=np.int32)
+    n = ctypes.c_int()
+    g = _ints(group_of_xcd) if group_of_xcd is not None else None
+    _check(load_library().asym_chunk_lists(
+        h.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)), h.shape[0], n_xcds, g, xcd_mask, mode,
+        out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+        off.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), ctypes.byref(n)))
+    return out[:n.value], off
+
+
+def chunk_read_bw(ptr: int, nbytes: int, chunk_log2: int, chunks, off, iters: int = 5, stream=None):
+    """Read the listed chunks of [ptr, ptr + nbytes) `iters` times; returns
+    (ms per iteration, XOR of every 16-byte word read as 4 uint32)."""
+    import numpy as np
+    c = np.ascontiguousarray(chunks, dtype=np.uint32)
+    o = np.ascontiguousarray(off, dtype=np.int32)
+    ms = ctypes.c_double()
+    ck = np.zeros(4, dtype=np.uint32)
+    _check(load_library().asym_chunk_read_bw(
+        ctypes.c_void_p(ptr), nbytes, chunk_log2, c.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+        o.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), o.shape[0] - 1, iters, _stream_ptr(stream),
+        ck.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), ctypes.byref(ms)))
+    return ms.value, ck
 
 
 def topology_from_records(records, n_cus: int, n_xccs: int, mask_bit_record=None) -> Topology:

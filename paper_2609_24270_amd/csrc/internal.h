@@ -108,6 +108,8 @@ struct LatencyMeasure {
   int l2_samples = 0;
   bool mall = true;
   uint64_t touch_delta = 1ull << 20;
+  const void* ext_base = nullptr;  // time lines of this caller allocation of `alloc`
+                                   // bytes (read only) instead of a fresh one
   int n_x = 0;                     // out
   std::vector<uint32_t> best;      // out
   double timer_overhead = -1.0;    // out

@@ -160,7 +160,7 @@ int latency_measure(int device, LatencyMeasure& m) {
   if (n_x < 1 || n_x > ASYM_MAX_XCDS) return fail(ASYM_EUNSUPPORTED, "latency probe: XCD count");
   const int n_s = (int)m.offs.size();
   if (n_s < 1 || m.alloc % kPage || m.alloc == 0 || m.passes < 1 || m.l2_samples < 0 ||
-      m.l2_samples > n_s)
+      m.l2_samples > n_s || (reinterpret_cast<uintptr_t>(m.ext_base) % kPage))
     return fail(ASYM_EINVAL, "latency probe: bad measurement set-up");
   for (uint64_t o : m.offs)
     if (o % 128 || o >= m.alloc || (o ^ m.touch_delta) >= m.alloc || ((o ^ m.touch_delta) % 128))
@@ -168,17 +168,22 @@ int latency_measure(int device, LatencyMeasure& m) {
 
   DevBufs b;
   ASYM_HIP(hipStreamCreateWithFlags(&b.s, hipStreamNonBlocking));
-  // one page more than asked, so the walked range can start on a 2 MiB boundary
-  ASYM_HIP(hipMalloc(&b.p[0], m.alloc + kPage));
+  uintptr_t base;
+  if (m.ext_base) {
+    base = reinterpret_cast<uintptr_t>(m.ext_base);
+  } else {
+    // one page more than asked, so the walked range can start on a 2 MiB boundary
+    ASYM_HIP(hipMalloc(&b.p[0], m.alloc + kPage));
+    ASYM_HIP(hipMemset(b.p[0], 0, m.alloc + kPage));
+    const uintptr_t raw = reinterpret_cast<uintptr_t>(b.p[0]);
+    base = (raw + kPage - 1) & ~(uintptr_t)(kPage - 1);
+  }
   ASYM_HIP(hipMalloc(&b.p[1], kFlushBytes));
   ASYM_HIP(hipMalloc(&b.p[2], sizeof(uint64_t) * n_s));
   ASYM_HIP(hipMalloc(&b.p[3], sizeof(uint32_t) * n_s));
   ASYM_HIP(hipMalloc(&b.p[4], sizeof(uint64_t) * 8));
   ASYM_HIP(hipMalloc(&b.p[5], sizeof(int) * 4));
   ASYM_HIP(hipMemcpy(b.p[2], m.offs.data(), sizeof(uint64_t) * n_s, hipMemcpyHostToDevice));
-  ASYM_HIP(hipMemset(b.p[0], 0, m.alloc + kPage));
-  const uintptr_t raw = reinterpret_cast<uintptr_t>(b.p[0]);
-  const uintptr_t base = (raw + kPage - 1) & ~(uintptr_t)(kPage - 1);
   m.base_align = base & (~base + 1);
 
   LatArgs a;

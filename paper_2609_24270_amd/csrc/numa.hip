@@ -1,0 +1,322 @@
+// Home map of an allocation and local / remote read bandwidth (Section 6.1:
+// pages classified by partition inside a contiguous region, then a read
+// kernel restricted to local or to remote pages; the appendix on NUMA-aware
+// address remapping places data by the same classification).
+//
+// On MI355X a partition is an affinity group of XCDs (an I/O die and its
+// memory).  The map times one line per 2 MiB page from every XCD and extends
+// the page's home to its chunks with the partition hash's in-page bits.  The
+// read kernel is a plain strided reader: workgroup b runs on XCD b mod n (the
+// hardware's round-robin dispatch) and walks that XCD's chunk list with a
+// fixed stride, so it has no atomics, no barriers and a bounded loop.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "internal.h"
+
+namespace asym {
+namespace {
+
+constexpr uint64_t kPage = 2ull << 20;
+constexpr int kReadThreads = 256;
+constexpr int kReadWorkersPerXcd = 256;  // 8 workgroups per CU at 32 CUs per XCD
+
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+
+// Each lane reads the 16-byte words at lane * 16 + j * 4096 of every chunk of
+// its workgroup's share; the XOR of what it read goes to sink[b * 256 + lane].
+__global__ void __launch_bounds__(kReadThreads)
+chunk_read_kernel(const char* __restrict__ base, int chunk_log2, const uint32_t* __restrict__ chunks,
+                  const int* __restrict__ off, int n_x, v4u* __restrict__ sink) {
+  const int b = blockIdx.x;
+  const int x = b % n_x;
+  const int r = b / n_x;
+  const int workers = gridDim.x / n_x;
+  const int i0 = off[x], i1 = off[x + 1];
+  const int words = 1 << (chunk_log2 - 12);  // 16-byte words per lane per chunk
+  v4u acc = {0u, 0u, 0u, 0u};
+  for (int i = i0 + r; i < i1; i += workers) {
+    const v4u* p = reinterpret_cast<const v4u*>(base + ((size_t)chunks[i] << chunk_log2)) + threadIdx.x;
+#pragma unroll 4
+    for (int j = 0; j < words; ++j) acc ^= p[(size_t)j * kReadThreads];
+  }
+  sink[(size_t)b * kReadThreads + threadIdx.x] = acc;
+}
+
+uint64_t mix64(uint64_t& s) {
+  uint64_t z = (s += 0x9E3779B97F4A7C15ull);
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+int parity64(uint64_t v) { return __builtin_popcountll(v) & 1; }
+
+struct Bufs {  // frees on every exit path
+  void* p[3] = {nullptr, nullptr, nullptr};
+  hipEvent_t e[2] = {nullptr, nullptr};
+  ~Bufs() {
+    for (void* q : p)
+      if (q) (void)hipFree(q);
+    for (hipEvent_t v : e)
+      if (v) (void)hipEventDestroy(v);
+  }
+};
+
+// Homes of lines [n_x][n] given the XCD groups (two): the group with the lower
+// mean latency, -1 when the two means are closer than `tie`.
+void homes_given_groups(const uint32_t* L, int n_x, int n, const int* grp, double tie, int8_t* home) {
+  int cnt[2] = {0, 0};
+  for (int x = 0; x < n_x; ++x) cnt[grp[x]] += 1;
+  for (int i = 0; i < n; ++i) {
+    double s[2] = {0.0, 0.0};
+    for (int x = 0; x < n_x; ++x) s[grp[x]] += L[(size_t)x * n + i];
+    const double m0 = s[0] / cnt[0], m1 = s[1] / cnt[1];
+    home[i] = std::fabs(m0 - m1) < tie ? -1 : (m0 < m1 ? 0 : 1);
+  }
+}
+
+}  // namespace
+
+int home_map_analyze(const uint32_t* L, int n_x, int n_pages, const uint64_t* voffs, int n_verify,
+                     const int* grp, uint64_t hash_mask, int chunk_log2, double tie, int8_t* chunk_home,
+                     asym_home_map_info& info) {
+  if (!L || !grp || !chunk_home || (n_verify > 0 && !voffs))
+    return fail(ASYM_EINVAL, "home map: null pointer");
+  if (n_x < 1 || n_x > ASYM_MAX_XCDS || n_pages < 1 || n_pages > (1 << 22) || n_verify < 0 ||
+      n_verify > (1 << 20) || !(tie >= 0.0))
+    return fail(ASYM_EINVAL, "home map: bad sizes or tie margin");
+  if (chunk_log2 < 12 || chunk_log2 > 21) return fail(ASYM_EINVAL, "home map: chunk_log2 must be in [12, 21]");
+  const uint64_t in_page = hash_mask & (kPage - 1);
+  if (in_page & ((1ull << chunk_log2) - 1))
+    return fail(ASYM_EINVAL, "home map: the hash has bits below the chunk size, a chunk would have two homes");
+  for (int x = 0; x < n_x; ++x)
+    if (grp[x] < 0 || grp[x] > 1) return fail(ASYM_EUNSUPPORTED, "home map: needs two XCD groups (0, 1)");
+  if (std::count(grp, grp + n_x, 0) == 0 || std::count(grp, grp + n_x, 1) == 0)
+    return fail(ASYM_EUNSUPPORTED, "home map: needs XCDs in both groups");
+  const uint64_t bytes = (uint64_t)n_pages * kPage;
+  for (int v = 0; v < n_verify; ++v)
+    if (voffs[v] >= bytes) return fail(ASYM_EINVAL, "home map: verification offset beyond the range");
+  const int n_s = n_pages + n_verify;
+  std::vector<int8_t> home(n_s);
+  homes_given_groups(L, n_x, n_s, grp, tie, home.data());
+
+  std::memset(&info, 0, sizeof info);
+  info.n_pages = n_pages;
+  info.n_chunks = (int)(bytes >> chunk_log2);
+  info.n_groups = 2;
+  for (int x = 0; x < ASYM_MAX_XCDS; ++x) info.group_of_xcd[x] = x < n_x ? grp[x] : -1;
+  long long c0 = 0, c1 = 0;
+  const size_t per_page = kPage >> chunk_log2;
+  for (int p = 0; p < n_pages; ++p) {
+    if (home[p] < 0) info.unclassified_pages += 1;
+    for (size_t c = 0; c < per_page; ++c) {
+      const uint64_t q = (uint64_t)c << chunk_log2;
+      const int8_t h = home[p] < 0 ? -1 : (int8_t)(home[p] ^ parity64(q & in_page));
+      chunk_home[(size_t)p * per_page + c] = h;
+      c0 += h == 0;
+      c1 += h == 1;
+    }
+  }
+  info.chunk_share[0] = (double)c0 / info.n_chunks;
+  info.chunk_share[1] = (double)c1 / info.n_chunks;
+  info.n_verify = n_verify;
+  for (int v = 0; v < n_verify; ++v) {
+    const int8_t got = home[n_pages + v];
+    const int8_t want = chunk_home[voffs[v] >> chunk_log2];
+    if (got < 0 || want < 0) continue;
+    info.verify_classified += 1;
+    info.verify_agree += got == want;
+  }
+  unsigned long long ls = 0, rs = 0, ln = 0, rn = 0;
+  for (int x = 0; x < n_x; ++x)
+    for (int p = 0; p < n_pages; ++p) {
+      if (home[p] < 0) continue;
+      const uint32_t v = L[(size_t)x * n_s + p];
+      if (home[p] == grp[x]) {
+        ls += v;
+        ln += 1;
+      } else {
+        rs += v;
+        rn += 1;
+      }
+    }
+  info.local_cycles = ln ? (double)ls / ln : -1.0;
+  info.remote_cycles = rn ? (double)rs / rn : -1.0;
+  return ASYM_OK;
+}
+
+int home_map(int device, const void* ptr, size_t bytes, uint64_t hash_mask, int chunk_log2,
+             const int* grp_in, int passes, int n_verify, uint64_t seed, double tie,
+             int8_t* chunk_home, asym_home_map_info& info) {
+  if (!ptr || !chunk_home) return fail(ASYM_EINVAL, "home map: null pointer");
+  if (reinterpret_cast<uintptr_t>(ptr) % kPage || bytes == 0 || bytes % kPage)
+    return fail(ASYM_EINVAL, "home map: ptr and bytes must be nonzero multiples of 2 MiB");
+  if (chunk_log2 < 12 || chunk_log2 > 21) return fail(ASYM_EINVAL, "home map: chunk_log2 must be in [12, 21]");
+  if ((hash_mask & (kPage - 1)) & ((1ull << chunk_log2) - 1))
+    return fail(ASYM_EINVAL, "home map: the hash has bits below the chunk size, a chunk would have two homes");
+  if (passes < 1 || passes > 64 || n_verify < 0 || n_verify > (1 << 20) || !(tie >= 0.0))
+    return fail(ASYM_EINVAL, "home map: passes in [1, 64], n_verify in [0, 2^20], tie >= 0");
+  const size_t n_pages = bytes / kPage;
+  if (n_pages > (1u << 22)) return fail(ASYM_EINVAL, "home map: range too large");
+  if (!grp_in && n_pages < 16) return fail(ASYM_EINVAL, "home map: at least 16 pages to find the groups");
+
+  LatencyMeasure m;
+  m.alloc = bytes;
+  m.ext_base = ptr;
+  m.passes = passes;
+  m.l2_samples = 0;
+  m.mall = false;
+  m.touch_delta = 1ull << 20;
+  for (size_t p = 0; p < n_pages; ++p) m.offs.push_back(p * kPage);
+  uint64_t st = seed;
+  for (int v = 0; v < n_verify; ++v) m.offs.push_back((mix64(st) % (bytes / 128)) * 128);
+  int rc = latency_measure(device, m);
+  if (rc != ASYM_OK) return rc;
+  const int n_x = m.n_x, n_s = (int)m.offs.size();
+  const uint32_t* L = &m.best[(size_t)2 * n_x * n_s];
+  std::vector<int> grp(n_x);
+  if (grp_in) {
+    std::copy(grp_in, grp_in + n_x, grp.begin());
+  } else {
+    asym_latency_summary s;
+    if ((rc = analyze_latency(L, n_x, n_s, 0.5, tie, s)) != ASYM_OK) return rc;
+    if (s.n_groups != 2)
+      return fail(ASYM_EUNSUPPORTED, "home map: the timed lines show " + std::to_string(s.n_groups) +
+                                         " XCD groups, not two");
+    for (int x = 0; x < n_x; ++x) grp[x] = s.group_of_xcd[x];
+  }
+  return home_map_analyze(L, n_x, (int)n_pages, m.offs.data() + n_pages, n_verify, grp.data(), hash_mask,
+                          chunk_log2, tie, chunk_home, info);
+}
+
+int chunk_lists(const int8_t* home, int n_chunks, int n_x, const int* grp, uint32_t xcd_mask, int mode,
+                uint32_t* out, int* off, int* n_listed) {
+  if (!home || !out || !off || !n_listed || n_chunks < 0 || n_x < 1 || n_x > ASYM_MAX_XCDS)
+    return fail(ASYM_EINVAL, "chunk lists: bad arguments");
+  if (mode < ASYM_CHUNKS_ALL || mode > ASYM_CHUNKS_REMOTE) return fail(ASYM_EINVAL, "chunk lists: unknown mode");
+  if (mode != ASYM_CHUNKS_ALL && !grp) return fail(ASYM_EINVAL, "chunk lists: LOCAL and REMOTE need the groups");
+  const uint32_t all = n_x >= 32 ? ~0u : ((1u << n_x) - 1);
+  const uint32_t act = xcd_mask ? (xcd_mask & all) : all;
+  if (!act) return fail(ASYM_EINVAL, "chunk lists: no active XCD");
+  if (grp)
+    for (int x = 0; x < n_x; ++x)
+      if (grp[x] < 0 || grp[x] > 1) return fail(ASYM_EINVAL, "chunk lists: group ids must be 0 or 1");
+  std::vector<std::vector<uint32_t>> per(n_x);
+  if (mode == ASYM_CHUNKS_ALL) {
+    std::vector<int> xs;
+    for (int x = 0; x < n_x; ++x)
+      if ((act >> x) & 1) xs.push_back(x);
+    for (int c = 0; c < n_chunks; ++c) per[xs[c % xs.size()]].push_back((uint32_t)c);
+  } else {
+    std::vector<int> readers[2];
+    for (int x = 0; x < n_x; ++x)
+      if ((act >> x) & 1) readers[mode == ASYM_CHUNKS_LOCAL ? grp[x] : 1 - grp[x]].push_back(x);
+    long long dealt[2] = {0, 0};
+    for (int c = 0; c < n_chunks; ++c) {
+      const int h = home[c];
+      if (h < 0 || h > 1 || readers[h].empty()) continue;
+      per[readers[h][dealt[h]++ % readers[h].size()]].push_back((uint32_t)c);
+    }
+  }
+  int k = 0;
+  for (int x = 0; x < n_x; ++x) {
+    off[x] = k;
+    for (uint32_t c : per[x]) out[k++] = c;
+  }
+  off[n_x] = k;
+  *n_listed = k;
+  return ASYM_OK;
+}
+
+int chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uint32_t* chunks, const int* off,
+                  int n_x, int iters, hipStream_t s, uint32_t* checksum, double* ms) {
+  if (!base || !chunks || !off || !ms) return fail(ASYM_EINVAL, "chunk read: null pointer");
+  if (reinterpret_cast<uintptr_t>(base) % 16) return fail(ASYM_EINVAL, "chunk read: base must be 16-byte aligned");
+  if (chunk_log2 < 12 || chunk_log2 > 21) return fail(ASYM_EINVAL, "chunk read: chunk_log2 must be in [12, 21]");
+  if (iters < 1 || iters > 10000) return fail(ASYM_EINVAL, "chunk read: iters must be in [1, 10000]");
+  int dev = 0, dev_x = 0;
+  ASYM_HIP(hipGetDevice(&dev));
+  ASYM_HIP(hipDeviceGetAttribute(&dev_x, hipDeviceAttributeNumberOfXccs, dev));
+  if (n_x != dev_x) return fail(ASYM_EINVAL, "chunk read: n_xcds must be the device's XCD count");
+  const uint64_t n_chunks = bytes >> chunk_log2;
+  if (off[0] != 0) return fail(ASYM_EINVAL, "chunk read: off[0] must be 0");
+  for (int x = 0; x < n_x; ++x)
+    if (off[x + 1] < off[x]) return fail(ASYM_EINVAL, "chunk read: off must not decrease");
+  const int n = off[n_x];
+  for (int i = 0; i < n; ++i)
+    if (chunks[i] >= n_chunks) return fail(ASYM_EINVAL, "chunk read: chunk index beyond the range");
+
+  const int grid = n_x * kReadWorkersPerXcd;
+  Bufs b;
+  ASYM_HIP(hipMalloc(&b.p[0], sizeof(uint32_t) * std::max(n, 1)));
+  ASYM_HIP(hipMalloc(&b.p[1], sizeof(int) * (n_x + 1)));
+  ASYM_HIP(hipMalloc(&b.p[2], sizeof(v4u) * (size_t)grid * kReadThreads));
+  if (n) ASYM_HIP(hipMemcpy(b.p[0], chunks, sizeof(uint32_t) * n, hipMemcpyHostToDevice));
+  ASYM_HIP(hipMemcpy(b.p[1], off, sizeof(int) * (n_x + 1), hipMemcpyHostToDevice));
+  ASYM_HIP(hipEventCreate(&b.e[0]));
+  ASYM_HIP(hipEventCreate(&b.e[1]));
+  const char* cb = static_cast<const char*>(base);
+  auto launch = [&]() -> int {
+    hipLaunchKernelGGL(chunk_read_kernel, dim3(grid), dim3(kReadThreads), 0, s, cb, chunk_log2,
+                       static_cast<const uint32_t*>(b.p[0]), static_cast<const int*>(b.p[1]), n_x,
+                       static_cast<v4u*>(b.p[2]));
+    ASYM_HIP(hipGetLastError());
+    return ASYM_OK;
+  };
+  int rc = launch();  // untimed first pass
+  if (rc != ASYM_OK) return rc;
+  ASYM_HIP(hipEventRecord(b.e[0], s));
+  for (int it = 0; it < iters; ++it)
+    if ((rc = launch()) != ASYM_OK) return rc;
+  ASYM_HIP(hipEventRecord(b.e[1], s));
+  ASYM_HIP(hipEventSynchronize(b.e[1]));
+  float t = 0.f;
+  ASYM_HIP(hipEventElapsedTime(&t, b.e[0], b.e[1]));
+  *ms = (double)t / iters;
+  if (checksum) {
+    std::vector<v4u> h((size_t)grid * kReadThreads);
+    ASYM_HIP(hipMemcpy(h.data(), b.p[2], sizeof(v4u) * h.size(), hipMemcpyDeviceToHost));
+    v4u acc = {0u, 0u, 0u, 0u};
+    for (const v4u& v : h) acc ^= v;
+    for (int w = 0; w < 4; ++w) checksum[w] = acc[w];
+  }
+  return ASYM_OK;
+}
+
+}  // namespace asym
+
+extern "C" int asym_home_map(int device, const void* ptr, size_t bytes, uint64_t hash_mask, int chunk_log2,
+                             const int* group_of_xcd, int passes, int n_verify, uint64_t seed,
+                             double tie_cycles, int8_t* chunk_home, asym_home_map_info* info) {
+  if (!info) return asym::fail(ASYM_EINVAL, "home map: null info");
+  return asym::home_map(device, ptr, bytes, hash_mask, chunk_log2, group_of_xcd, passes, n_verify, seed,
+                        tie_cycles, chunk_home, *info);
+}
+
+extern "C" int asym_home_map_analyze(const uint32_t* lat, int n_xcds, int n_pages,
+                                     const uint64_t* verify_offs, int n_verify, const int* group_of_xcd,
+                                     uint64_t hash_mask, int chunk_log2, double tie_cycles,
+                                     int8_t* chunk_home, asym_home_map_info* info) {
+  if (!info) return asym::fail(ASYM_EINVAL, "home map: null info");
+  return asym::home_map_analyze(lat, n_xcds, n_pages, verify_offs, n_verify, group_of_xcd, hash_mask,
+                                chunk_log2, tie_cycles, chunk_home, *info);
+}
+
+extern "C" int asym_chunk_lists(const int8_t* chunk_home, int n_chunks, int n_xcds, const int* group_of_xcd,
+                                uint32_t xcd_mask, int mode, uint32_t* chunks_out, int* off_out,
+                                int* n_listed) {
+  return asym::chunk_lists(chunk_home, n_chunks, n_xcds, group_of_xcd, xcd_mask, mode, chunks_out, off_out,
+                           n_listed);
+}
+
+extern "C" int asym_chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uint32_t* chunks,
+                                  const int* off, int n_xcds, int iters, void* stream,
+                                  uint32_t* checksum_out, double* ms_per_iter) {
+  return asym::chunk_read_bw(base, bytes, chunk_log2, chunks, off, n_xcds, iters,
+                             static_cast<hipStream_t>(stream), checksum_out, ms_per_iter);
+}
