@@ -542,13 +542,28 @@ typedef struct asym_gemm_plan_info {
   int claims;
   int vector_path;
   int n_xcds;
-  int workers_per_xcd[ASYM_MAX_XCDS];
+  int workers_per_xcd[ASYM_MAX_XCDS]; /* persistent kernel only (0 on the small-M path) */
+  int small_m;     /* 1: the small-M kernel (a plain launch of 32-column tiles,
+                      tile_m = 16, 32 or 64 rows, four waves splitting K per tile) */
 } asym_gemm_plan_info;
 
 int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
                    const void* A, int lda, const void* B, int ldb,
                    int b_layout, const void* C, int ldc, int mapping,
                    uint32_t xcd_mask, void* stream, asym_gemm_plan_info* out);
+
+/* Small-M path.  A GEMM with M <= 64 (a grouped GEMM whose groups all have at
+ * most 64 rows) on the vector path and on every XCD of its CU set (xcd_mask 0
+ * or all XCDs) runs a different kernel: with so few rows the product is bound
+ * by reading B once from HBM, no tile is reused, and a tile placement has
+ * nothing to gain, so every mapping gives the same launch and bitwise the same
+ * result.  Each workgroup computes 32 columns of C for all rows and all of K,
+ * its four waves streaming a quarter of K each straight into MFMA operands;
+ * the partial sums meet in LDS and are added in a fixed order.  This call
+ * switches the path on or off for the whole process (default on; off sends
+ * such products to the persistent kernel, for comparison) and returns the
+ * previous setting.  Not synchronised with launches in flight. */
+int asym_gemm_set_small_m(int enable);
 
 /* ---- streaming copy and co-run (Sections 7.2, 7.3) ---------------------- */
 /* dst[i] = src[i] for n_bytes bytes (16-byte aligned, n_bytes a multiple of

@@ -41,7 +41,7 @@ EXPORTS = (
     "asym_dispatch_check", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
-    "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_plan", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
+    "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_plan", "asym_gemm_set_small_m", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
 
@@ -153,7 +153,8 @@ class GemmPlanInfo(ctypes.Structure):
                 ("tiles_m", ctypes.c_int), ("tiles_n", ctypes.c_int),
                 ("grid", ctypes.c_int), ("workers", ctypes.c_int),
                 ("claims", ctypes.c_int), ("vector_path", ctypes.c_int),
-                ("n_xcds", ctypes.c_int), ("workers_per_xcd", ctypes.c_int * MAX_XCDS)]
+                ("n_xcds", ctypes.c_int), ("workers_per_xcd", ctypes.c_int * MAX_XCDS),
+                ("small_m", ctypes.c_int)]
 
     def to_dict(self) -> dict:
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "workers_per_xcd"}
@@ -223,6 +224,7 @@ def load_library(path: str = LIB_PATH):
         "asym_gemm_grouped_bf16": (i, [topo_p, i, ip, i, i, vp, i, vp, i, vp, i, i, u32, vp]),
         "asym_gemm_plan": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp,
                                ctypes.POINTER(GemmPlanInfo)]),
+        "asym_gemm_set_small_m": (i, [i]),
         "asym_copy_bf16": (i, [vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
         "asym_corun": (i, [topo_p, ctypes.POINTER(Task), i, ctypes.POINTER(TaskResult)]),
         "asym_last_error": (cp, []),
@@ -651,6 +653,11 @@ def gemm_grouped(A, B, M: Sequence[int], C=None, mapping="aware", topo: Optional
         ctypes.c_void_p(A.data_ptr()), max(A.stride(0), K), ctypes.c_void_p(B.data_ptr()), ldb,
         ctypes.c_void_p(C.data_ptr()), max(C.stride(0), N), mp, xcd_mask, _stream_ptr(stream)))
     return C
+
+
+def set_small_m(enable: bool) -> bool:
+    """Switch the small-M kernel on or off for the process; returns the previous setting."""
+    return bool(load_library().asym_gemm_set_small_m(1 if enable else 0))
 
 
 def gemm_plan(A=None, B=None, C=None, mapping="aware", topo: Optional[Topology] = None,

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cstring>
 #include <map>
@@ -201,9 +202,22 @@ struct GemmPlan {
   int device = 0;
   std::vector<int> per, slots;
   int total = 0, smax = 0;
-  bool vec = false, dynamic = false;
+  bool vec = false, dynamic = false, whole = true;
+  bool vec_ab = false;  // A and B alone meet the vector-path alignment
   int bn = 0, tiles_m = 0, tiles_n = 0, grid = 0;
+  int small_mb = 0;  // > 0: the small-M kernel with this many 16-row blocks
 };
+
+// The small-M kernel serves row tiles of at most 64 rows when A and B meet the
+// vector-path alignment (C may have any stride) and the GEMM runs on every XCD
+// of its CU set (a whole-XCD restriction needs
+// the persistent kernel, whose workers leave the excluded XCDs).
+std::atomic<bool> g_small_m{true};
+
+int small_m_for(const GemmPlan& P, int max_rows) {
+  if (!g_small_m.load() || !P.vec_ab || !P.whole) return 0;
+  return small_m_blocks(max_rows);
+}
 
 static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
                      const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
@@ -257,13 +271,14 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   }
   if (total == 0) return fail(ASYM_EINVAL, "gemm: the CU set is empty");
 
-  const bool vec = aligned16(A) && aligned16(B) && (((uintptr_t)C & 7u) == 0) && (K % 8 == 0) &&
-                   (lda % 8 == 0) && (ldb % 8 == 0) && (ldc % 4 == 0);
+  const bool vec_ab = aligned16(A) && aligned16(B) && (K % 8 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
+  const bool vec = vec_ab && (((uintptr_t)C & 7u) == 0) && (ldc % 4 == 0);
   P->t = t;
   P->device = device;
   P->total = total;
   P->smax = smax;
   P->vec = vec;
+  P->vec_ab = vec_ab;
   P->bn = vec ? choose_tile_width(M, N, total) : (int)BNr;
   P->tiles_m = (int)((M + BMr - 1) / BMr);
   P->tiles_n = (N + P->bn - 1) / P->bn;
@@ -275,8 +290,10 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   P->dynamic = false;
   for (int x = 0; x < t->n_xccs; ++x)
     if (per[x] < smax) P->dynamic = true;
+  P->whole = xm == all;
   P->per = std::move(per);
   P->slots = std::move(slots);
+  P->small_mb = small_m_for(*P, M);
   return ASYM_OK;
 }
 
@@ -287,6 +304,14 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   GemmPlan P;
   int rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
   if (rc != ASYM_OK) return rc;
+  if (P.small_mb) {
+    SmallMLaunch sm;
+    sm.A = A; sm.B = B; sm.C = C;
+    sm.M = M; sm.N = N; sm.K = K; sm.lda = lda; sm.ldb = ldb; sm.ldc = ldc;
+    sm.mb = P.small_mb;
+    sm.row_tiles = 1;
+    return launch_gemm_small_m(sm, stream);
+  }
   const DeviceSchedule* ds = nullptr;
   rc = upload_schedule(P.device, P.tiles_m, P.tiles_n, mapping, P.slots, &ds);
   if (rc != ASYM_OK) return rc;
@@ -343,13 +368,15 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   const int virt_m = (int)std::max<int64_t>(1, trows * gemm_tile_m());
   int rc = plan_gemm(topo_in, virt_m, N, K, A, lda, B, ldb, ASYM_B_NK, C, ldc, mapping, xcd_mask, stream, &P);
   if (rc != ASYM_OK) return rc;
-  const int tiles_n = (N + P.bn - 1) / P.bn;
+  const int max_rows = *std::max_element(Ms, Ms + G);
+  const int small_mb = small_m_for(P, max_rows);
+  const int tiles_n = small_mb ? (N + small_m_tile_cols() - 1) / small_m_tile_cols() : (N + P.bn - 1) / P.bn;
   Workspace* ws = nullptr;
   rc = get_workspace(P.device, stream, &ws);
   if (rc != ASYM_OK) return rc;
   std::vector<int> key(Ms, Ms + G);
   key.push_back(N);
-  key.push_back(P.bn);
+  key.push_back(small_mb ? -small_mb : P.bn);
   key.push_back(mapping);
   key.insert(key.end(), P.slots.begin(), P.slots.end());
   auto hit = std::find_if(ws->g_tables.begin(), ws->g_tables.end(),
@@ -358,8 +385,15 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
     std::rotate(ws->g_tables.begin(), hit, hit + 1);  // most recent first
   } else {
     Schedule sch;
-    rc = build_grouped_schedule(G, tm.data(), tiles_n, P.t->n_xccs, P.slots.data(), mapping, sch);
-    if (rc != ASYM_OK) return rc;
+    if (small_mb) {
+      // one row tile per nonempty group; the grid is a plain launch
+      for (int g = 0; g < G; ++g)
+        if (Ms[g] > 0) sch.order.push_back(g);
+      sch.off.assign(P.t->n_xccs + 1, 0);
+    } else {
+      rc = build_grouped_schedule(G, tm.data(), tiles_n, P.t->n_xccs, P.slots.data(), mapping, sch);
+      if (rc != ASYM_OK) return rc;
+    }
     GroupedTables tb;
     tb.key = std::move(key);
     tb.T = (int)sch.order.size();
@@ -391,7 +425,13 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
     if (!ws->g_copied) ASYM_HIP(hipEventCreateWithFlags(&ws->g_copied, hipEventDisableTiming));
     int4* h_desc = static_cast<int4*>(ws->g_host);
     int* h_sched = reinterpret_cast<int*>(static_cast<char*>(ws->g_host) + desc_bytes);
-    {
+    if (small_mb) {
+      int id = 0, row0 = 0;
+      for (int g = 0; g < G; ++g) {
+        if (Ms[g] > 0) h_desc[id++] = int4{row0, Ms[g], g * N, 0};
+        row0 += Ms[g];
+      }
+    } else {
       int id = 0, row0 = 0;
       for (int g = 0; g < G; ++g) {
         for (int r = 0; r < tm[g]; ++r)
@@ -413,6 +453,15 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   }
   const GroupedTables& tb = ws->g_tables.front();
   const int T = tb.T;
+  if (small_mb) {
+    SmallMLaunch sm;
+    sm.A = A; sm.B = B; sm.C = C;
+    sm.M = (int)rows; sm.N = N; sm.K = K; sm.lda = lda; sm.ldb = ldb; sm.ldc = ldc;
+    sm.mb = small_mb;
+    sm.row_tiles = T;
+    sm.d_desc = tb.desc;
+    return launch_gemm_small_m(sm, stream);
+  }
 
   GemmLaunch gl;
   gl.A = A; gl.B = B; gl.C = C;
@@ -442,6 +491,20 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   const int rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
   if (rc != ASYM_OK) return rc;
   *out = asym_gemm_plan_info{};
+  out->n_xcds = P.t->n_xccs;
+  out->vector_path = P.vec ? 1 : 0;
+  if (P.small_mb) {
+    out->vector_path = 1;
+    out->tile_m = 16 * P.small_mb;
+    out->tile_n = small_m_tile_cols();
+    out->tiles_m = 1;
+    out->tiles_n = (N + out->tile_n - 1) / out->tile_n;
+    out->grid = out->tiles_n;
+    out->workers = out->grid;
+    out->claims = 0;
+    out->small_m = 1;
+    return ASYM_OK;
+  }
   out->tile_m = gemm_tile_m();
   out->tile_n = P.bn;
   out->tiles_m = P.tiles_m;
@@ -449,9 +512,8 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   out->grid = P.grid;
   out->workers = P.total;
   out->claims = (mapping == ASYM_MAP_AWARE && P.dynamic) ? 1 : 0;
-  out->vector_path = P.vec ? 1 : 0;
-  out->n_xcds = P.t->n_xccs;
   for (int x = 0; x < P.t->n_xccs && x < ASYM_MAX_XCDS; ++x) out->workers_per_xcd[x] = P.slots[x];
+  out->small_m = 0;
   return ASYM_OK;
 }
 
@@ -598,3 +660,7 @@ extern "C" int asym_stream_destroy(void* stream) {
 extern "C" const char* asym_last_error(void) { return asym::g_last_error.c_str(); }
 
 extern "C" int asym_version(void) { return 1; }
+
+extern "C" int asym_gemm_set_small_m(int enable) {
+  return asym::g_small_m.exchange(enable != 0) ? 1 : 0;
+}

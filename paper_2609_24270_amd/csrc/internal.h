@@ -89,6 +89,18 @@ struct GemmLaunch {
 };
 int launch_gemm(const GemmLaunch& g, hipStream_t s);
 
+// Small-M path (at most 64 rows per row tile; vector-path alignment).
+struct SmallMLaunch {
+  const void* A; const void* B; void* C;
+  int M, N, K, lda, ldb, ldc;
+  int mb;                       // 16-row blocks per row tile: 1, 2 or 4
+  int row_tiles;                // 1 for a plain GEMM, nonempty groups for a grouped one
+  const void* d_desc = nullptr; // grouped: device int4 per row tile {row, rows, B row, 0}
+};
+int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s);
+int small_m_blocks(int max_rows);  // 1, 2, 4, or 0 above 64 rows
+int small_m_tile_cols();
+
 int probe_identity_run(int device, hipStream_t s, int n_blocks,
                        std::vector<int32_t>& rec);
 int probe_latency_run(int device, Topology& t);

@@ -1,0 +1,149 @@
+"""GPU parity of the small-M kernel (at most 64 rows per row tile) against the
+CPU oracle, through the C ABI.
+
+Element by element over row counts on both sides of every 16-row block
+boundary, ragged column counts and K not a multiple of the 32-wide k-step;
+the decode projection 32 x 14336 x 4096 on sampled columns; bitwise: every
+mapping, repeats and a CU-masked stream give the same bits, and on exact-integer
+inputs the small-M kernel and the persistent kernel (the path switched off)
+agree bit for bit with each other and with the integer product.  The plan says
+which kernel a shape takes.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_24270_amd as asym
+from paper_2609_24270_amd import workloads
+from tests.checks import assert_gemm_close
+
+pytestmark = pytest.mark.gpu
+
+MAPS = ("aware", "oblivious_grouped", "oblivious_rowmajor")
+
+
+def bits(t):
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    asym.load_library()
+    torch.cuda.set_device(0)
+    return torch.device("cuda:0")
+
+
+@pytest.mark.parametrize("M", [1, 5, 16, 17, 31, 32, 33, 48, 63, 64])
+@pytest.mark.parametrize("N,K", [(1000, 72), (96, 1000), (257, 4104)])
+def test_small_m_elementwise(dev, M, N, K):
+    p = workloads.make_problem(M, N, K, seed=100 + M)
+    A, B = workloads.make_inputs(p)
+    plan = asym.gemm_plan(A=A.to(dev), B=B.to(dev))
+    assert plan["small_m"] == 1 and plan["tile_m"] == (16 if M <= 16 else 32 if M <= 32 else 64)
+    C = asym.gemm(A.to(dev), B.to(dev))
+    torch.cuda.synchronize()
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    err = assert_gemm_close(bits(C), R, what=f"{M}x{N}x{K}")
+    assert err < 5e-3
+
+
+def test_plan_picks_the_kernel(dev):
+    def plan(M, K=4096, **kw):
+        A = torch.zeros((M, K), dtype=torch.bfloat16, device=dev)
+        B = torch.zeros((512, K), dtype=torch.bfloat16, device=dev)
+        return asym.gemm_plan(A=A, B=B, **kw)
+    assert plan(64)["small_m"] == 1 and plan(65)["small_m"] == 0
+    assert plan(32, K=4100)["small_m"] == 0                       # K not a multiple of 8
+    assert plan(32, xcd_mask=0x0F)["small_m"] == 0                # whole-XCD restriction
+    p = plan(32)
+    assert (p["tile_n"], p["tiles_n"], p["grid"], p["claims"]) == (32, 16, 16, 0)
+    prev = asym.set_small_m(False)
+    try:
+        assert plan(32)["small_m"] == 0
+    finally:
+        asym.set_small_m(prev)
+
+
+def test_decode_projection_sampled_and_bitwise(dev):
+    (_, _), (da, db) = workloads.make_pd_inputs()
+    A, B = da.to(dev), db.to(dev)
+    outs = []
+    for m in MAPS:
+        for _ in range(2):
+            outs.append(bits(asym.gemm(A, B, mapping=m)))
+    assert all(np.array_equal(outs[0], o) for o in outs[1:])
+    g = np.random.default_rng(3)
+    cols = np.unique(np.concatenate([g.choice(14336, 512, replace=False), [14335]]))
+    R, _ = oracle.gemm_bf16(bits(da), bits(db)[cols], "nk")
+    err = assert_gemm_close(outs[0][:, cols], R, what="decode 32x14336x4096")
+    print(f"decode 32x14336x4096 sampled max rel err {err:.3e}")
+
+
+def test_exact_integer_small_equals_persistent(dev):
+    p = workloads.make_problem(40, 3000, 2048, seed=7, dist="int")
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    small = bits(asym.gemm(Ad, Bd))
+    prev = asym.set_small_m(False)
+    try:
+        pers = bits(asym.gemm(Ad, Bd))
+    finally:
+        asym.set_small_m(prev)
+    _, Co = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    assert np.array_equal(small, Co) and np.array_equal(pers, Co)
+
+
+def test_strided_operands(dev):
+    M, N, K = 24, 700, 512
+    p = workloads.make_problem(M, N, K, seed=9)
+    A, B = workloads.make_inputs(p)
+    Abig = torch.zeros((M, K + 64), dtype=torch.bfloat16)
+    Abig[:, :K] = A
+    Bbig = torch.zeros((N, K + 128), dtype=torch.bfloat16)
+    Bbig[:, :K] = B
+    Cbig = torch.full((M, N + 36), 7.0, dtype=torch.bfloat16, device=dev)
+    Ad, Bd = Abig.to(dev)[:, :K], Bbig.to(dev)[:, :K]
+    C = Cbig[:, :N]
+    assert asym.gemm_plan(A=Ad, B=Bd, C=C)["small_m"] == 1
+    asym.gemm(Ad, Bd, C)
+    torch.cuda.synchronize()
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    assert_gemm_close(bits(C), R)
+    assert (Cbig[:, N:] == 7.0).all()   # columns past N untouched
+
+
+def test_cu_masked_stream_bitwise(dev):
+    topo = asym.probe_topology(0, asym.PROBE_IDENTITY | asym.PROBE_MASKMAP)
+    mask = workloads.random_mask_bits(11, 1, 128)[0]
+    p = workloads.make_problem(32, 5000, 4096, seed=12, dist="llm")
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    ref = bits(asym.gemm(Ad, Bd))
+    s = asym.stream_create(topo, mask)
+    try:
+        assert asym.gemm_plan(A=Ad, B=Bd, topo=topo, stream=s)["small_m"] == 1
+        C = asym.gemm(Ad, Bd, topo=topo, stream=s)
+        s.synchronize()
+        assert np.array_equal(bits(C), ref)
+    finally:
+        asym.stream_destroy(s)
+
+
+def test_grouped_small_groups_exact_integer_equals_persistent(dev):
+    p = workloads.grouped_problem(32, 20, 4096, 2048, seed=5, dist="int")
+    Ms, A, B = workloads.make_grouped_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    small = bits(asym.gemm_grouped(Ad, Bd, Ms))
+    prev = asym.set_small_m(False)
+    try:
+        pers = bits(asym.gemm_grouped(Ad, Bd, Ms))
+    finally:
+        asym.set_small_m(prev)
+    assert np.array_equal(small, pers)
+    rows = np.cumsum([0] + Ms)
+    for g in (0, 7, 31):
+        _, Co = oracle.grouped_gemm_bf16(bits(A)[rows[g]:rows[g + 1]], bits(B)[g:g + 1], [Ms[g]], False)
+        assert np.array_equal(small[rows[g]:rows[g + 1]], Co)
