@@ -174,6 +174,32 @@ def llm_shapes(dev, stream, rounds: int):
     return out
 
 
+def decode_gemm(dev, stream, launches: int = 20, rounds: int = 5):
+    """Decode projection 32 x 14336 x 4096 (N(0,0.02) weights, N(0,1) activations)
+    on the full GPU: the small-M kernel and the persistent kernel (aware), and
+    the weight-streaming rate 2 N K / time."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    (_, _), (da, db) = workloads.make_pd_inputs()
+    A, B = da.to(dev), db.to(dev)
+    C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
+    small = lambda: asym.gemm(A, B, C, stream=stream)
+    small()
+    out = {"small_m": queued({"s": small}, launches, rounds, stream)["s"]}
+    prev = asym.set_small_m(False)
+    try:
+        pers = lambda: asym.gemm(A, B, C, stream=stream)
+        pers()
+        out["persistent_aware"] = queued({"p": pers}, launches, rounds, stream)["p"]
+    finally:
+        asym.set_small_m(prev)
+    wbytes = 2 * B.shape[0] * B.shape[1]
+    return {k: {"us": round(1e3 * v, 2), "weights_TBps": round(wbytes / (v * 1e-3) / 1e12, 3),
+                "tflops": round(2 * 32 * 14336 * 4096 / (v * 1e-3) / 1e12, 2)} for k, v in out.items()}
+
+
 def prefill_decode(topo, dev, iters: int, halves):
     """Prefill GEMM 8192x4096x4096 on 192 CUs co-running with decode GEMM
     32x14336x4096 on the other 64, on XCD-aligned sets (6 XCDs / 2 XCDs, the
@@ -300,10 +326,20 @@ def grouped_study(dev, stream, seeds, launches: int, rounds: int):
             p = workloads.grouped_problem(base.G, base.M, base.N, base.K, seed=seed)
             Ms, A, B = workloads.make_grouped_inputs_on(p, dev)
             C = torch.empty((sum(Ms), p.N), dtype=torch.bfloat16, device=dev)
-            fns = {m: (lambda m=m: asym.gemm_grouped(A, B, Ms, C, mapping=m, stream=stream)) for m in MAPPINGS}
-            for f in fns.values():
+            # the mappings are compared on the persistent kernel; groups of at
+            # most 64 rows are also timed on the small-M kernel
+            prev = asym.set_small_m(False)
+            try:
+                fns = {m: (lambda m=m: asym.gemm_grouped(A, B, Ms, C, mapping=m, stream=stream)) for m in MAPPINGS}
+                for f in fns.values():
+                    f()
+                ms = queued(fns, launches, rounds, stream)
+            finally:
+                asym.set_small_m(prev)
+            if max(Ms) <= 64:
+                f = lambda: asym.gemm_grouped(A, B, Ms, C, stream=stream)
                 f()
-            ms = queued(fns, launches, rounds, stream)
+                ms["small_m"] = queued({"s": f}, launches, rounds, stream)["s"]
             rows.append((p.flops, p.working_set_bytes, ms))
             sp_g.append(ms["oblivious_grouped"] / ms["aware"])
             sp_r.append(ms["oblivious_rowmajor"] / ms["aware"])
@@ -317,6 +353,11 @@ def grouped_study(dev, stream, seeds, launches: int, rounds: int):
             "aware_TBps_W": round(sum(r[1] / (r[2]["aware"] * 1e-3) for r in rows) / n / 1e12, 3),
             "speedup_vs_oblivious_grouped": round(gm([r[2]["oblivious_grouped"] / r[2]["aware"] for r in rows]), 4),
             "speedup_vs_oblivious_rowmajor": round(gm([r[2]["oblivious_rowmajor"] / r[2]["aware"] for r in rows]), 4)}
+        if "small_m" in rows[0][2]:
+            e = per[f"G{base.G}_M{base.M}_N{base.N}_K{base.K}"]
+            e["small_m_us"] = round(1e3 * sum(r[2]["small_m"] for r in rows) / n, 2)
+            e["small_m_TBps_W"] = round(sum(r[1] / (r[2]["small_m"] * 1e-3) for r in rows) / n / 1e12, 3)
+            e["small_m_speedup_vs_aware"] = round(gm([r[2]["aware"] / r[2]["small_m"] for r in rows]), 4)
     torch.cuda.empty_cache()
 
     def summ(v):
@@ -497,6 +538,7 @@ def main() -> int:
         del Bt
     if "llm" in studies:
         line["llm_shapes_tflops"] = llm_shapes(dev, stream, 20)
+        line["decode_gemm"] = decode_gemm(dev, stream)
     if "pd" in studies:
         line["prefill_decode"] = prefill_decode(topo, dev, 10, halves)
     if "spread" in studies:

@@ -543,8 +543,8 @@ typedef struct asym_gemm_plan_info {
   int vector_path;
   int n_xcds;
   int workers_per_xcd[ASYM_MAX_XCDS]; /* persistent kernel only (0 on the small-M path) */
-  int small_m;     /* 1: the small-M kernel (a plain launch of 32-column tiles,
-                      tile_m = 16, 32 or 64 rows, four waves splitting K per tile) */
+  int small_m;     /* 1: the small-M kernel (a plain launch of 64-column tiles,
+                      tile_m = 16, 32 or 64 rows, each wave 16 columns over all of K) */
 } asym_gemm_plan_info;
 
 int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
@@ -557,9 +557,9 @@ int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
  * or all XCDs) runs a different kernel: with so few rows the product is bound
  * by reading B once from HBM, no tile is reused, and a tile placement has
  * nothing to gain, so every mapping gives the same launch and bitwise the same
- * result.  Each workgroup computes 32 columns of C for all rows and all of K,
- * its four waves streaming a quarter of K each straight into MFMA operands;
- * the partial sums meet in LDS and are added in a fixed order.  This call
+ * result.  Each workgroup computes 64 columns of C for all rows; each of its
+ * four waves streams its 16 rows of B over all of K straight into MFMA
+ * operands, with A shared through LDS.  This call
  * switches the path on or off for the whole process (default on; off sends
  * such products to the persistent kernel, for comparison) and returns the
  * previous setting.  Not synchronised with launches in flight. */

@@ -4,15 +4,18 @@
 //
 // With a few rows the work is bound by streaming B from HBM once (2 N K bytes
 // against 2 M N K flops), so the kernel is built for memory-level parallelism
-// rather than for operand reuse: a workgroup owns a 32-column slice of C for
-// its row tile and all of K; its four waves split K into four ranges and
-// each wave streams its range of the 32 B rows straight into MFMA operand
-// registers (no LDS staging: a lane's 8 bf16 of a 16x32 fragment are 16
-// contiguous bytes of one row), U k-steps of 32 ahead of the MFMAs.  The four
-// partial tiles meet in LDS at the end and are summed in wave order, so the
-// result does not depend on timing.  Every B byte is fetched once; there is no
-// tile reuse for a placement to exploit, so the grid is a plain launch over
-// the tiles and the hardware spreads it.
+// rather than for operand reuse.  A workgroup owns a 64-column slice of C for
+// its row tile; each of its four waves owns 16 of those columns and all of K,
+// and streams its 16 B rows straight into MFMA operand registers (a lane's 8
+// bf16 of a 16x32 fragment are 16 contiguous bytes of one row), two groups of
+// U k-steps in flight.  A, the same for every wave, goes through LDS once per
+// stage of U k-steps (double-buffered, one barrier per stage), so the vector
+// memory path carries B and little else: with A loaded by every wave, one A
+// fragment load per B fragment load, the kernel streamed B at about 4 TB/s;
+// shared through LDS, close to the chip's read rate.  Each output element is
+// one wave's MFMA chain over k in order, as in the persistent kernel.  Every B
+// byte is fetched once and no tile is reused, so there is no placement to
+// choose: the grid is a plain launch over the tiles.
 //
 // A row tile is one plain problem (rows 0..M-1) or one group of a grouped
 // problem, given by a descriptor {first row, rows, first B row, unused}.
@@ -23,11 +26,9 @@
 namespace asym {
 namespace {
 
-constexpr int SK_THREADS = 256;
 constexpr int SK_WAVES = 4;
-constexpr int SK_NBW = 2;            // 16-column blocks per tile: 32 columns
-constexpr int SK_COLS = 16 * SK_NBW;
-constexpr int SK_U = 4;              // k-steps of 32 loaded ahead
+constexpr int SK_THREADS = 64 * SK_WAVES;
+constexpr int SK_COLS = 16 * SK_WAVES;  // 64 columns per tile, 16 per wave
 constexpr uint32_t kSkOOB = 0x80000000u;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -41,7 +42,7 @@ struct SkinnyParams {
   const uint16_t* B;
   uint16_t* C;
   int M, N, K, lda, ldb, ldc;
-  int tiles_n;        // 32-column tiles per row tile
+  int tiles_n;        // 64-column tiles per row tile
   const int4* desc;   // per row tile {first row, rows, first B row, 0}; null = one tile of M rows
 };
 
@@ -53,21 +54,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t sk_rsrc(const void* base, uint
                                            (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
 }
 
-__device__ __forceinline__ bf16x8 sk_load(__amdgpu_buffer_rsrc_t rs, uint32_t vo, int so) {
-  const v4u x = __builtin_amdgcn_raw_buffer_load_b128(rs, vo, so, 0);
-  return __builtin_bit_cast(bf16x8, x);
-}
-
 __device__ __forceinline__ uint32_t sk_pack(float a, float b) {
   bf16x2 v = {(__bf16)a, (__bf16)b};
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// MB: 16-row blocks of the row tile (1, 2 or 4).
-template <int MB>
+// MB: 16-row blocks of the row tile (1, 2 or 4); U: k-steps of 32 per stage.
+template <int MB, int U>
 __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) {
-  __shared__ f32x4 red[SK_WAVES][SK_NBW * MB][64];
-
+  // A stage in LDS, in MFMA operand order: fragment (u, i) is 64 lanes x 16 bytes
+  __shared__ bf16x8 sa[2][U * MB * 64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int tile = blockIdx.x;
@@ -79,83 +75,103 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
     rows = __builtin_amdgcn_readfirstlane(d.y);
     brow0 = __builtin_amdgcn_readfirstlane(d.z);
   }
-  const int n0 = ct * SK_COLS;
-  const int cols = min(SK_COLS, p.N - n0);
+  // this wave's 16 columns; a wave past N has an empty B range and stores nothing
+  const int n0 = ct * SK_COLS + wave * 16;
+  const int cols = max(0, min(16, p.N - n0));
 
-  // operands: rows past the tile read as zero (outside the resource); k-steps
-  // at or past K are sent out of range per lane (K is a multiple of 8, so a
-  // lane's 8 elements are all inside or all outside)
+  // rows past the tile read as zero (outside the resource); a 16-byte chunk at
+  // k >= K is sent out of range (K is a multiple of 8: a chunk is all inside
+  // or all outside)
   const __amdgpu_buffer_rsrc_t ra = sk_rsrc(p.A + (size_t)row0 * p.lda, (uint32_t)rows * p.lda * 2u);
-  const __amdgpu_buffer_rsrc_t rb = sk_rsrc(p.B + (size_t)(brow0 + n0) * p.ldb, (uint32_t)cols * p.ldb * 2u);
+  const __amdgpu_buffer_rsrc_t rb =
+      sk_rsrc(p.B + (size_t)(brow0 + min(n0, p.N)) * p.ldb, (uint32_t)cols * p.ldb * 2u);
   const int lr = lane & 15, lk = (lane >> 4) * 8;
-  const uint32_t voa = (uint32_t)(lr * p.lda + lk) * 2u;
   const uint32_t vob = (uint32_t)(lr * p.ldb + lk) * 2u;
-
   const int steps = (p.K + 31) >> 5;
-  const int per = (steps + SK_WAVES - 1) / SK_WAVES;
-  const int s0 = min(steps, wave * per), s1 = min(steps, s0 + per);
+  const int stages = (steps + U - 1) / U;
 
-  f32x4 acc[SK_NBW][MB];
+  // A staging: chunk c of a stage is (row, k-step u, quarter kq) in row-major
+  // order; thread t carries chunks t, t + 256, ...
+  constexpr int CHUNKS = MB * 16 * U * 4;
+  constexpr int A_PER = (CHUNKS + SK_THREADS - 1) / SK_THREADS;
+  auto a_load = [&](int st, v4u (&r)[A_PER]) {
 #pragma unroll
-  for (int j = 0; j < SK_NBW; ++j)
-#pragma unroll
-    for (int i = 0; i < MB; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // two register sets in turn: the loads of one group of U k-steps are in
-  // flight while the MFMAs consume the other
-  bf16x8 b0[SK_U][SK_NBW], a0[SK_U][MB], b1[SK_U][SK_NBW], a1[SK_U][MB];
-  auto load_group = [&](int s, bf16x8 (&b)[SK_U][SK_NBW], bf16x8 (&a)[SK_U][MB]) {
-#pragma unroll
-    for (int u = 0; u < SK_U; ++u) {
-      const int k = (s + u) * 32;
-      const bool in = s + u < s1 && k + lk < p.K;
-      const uint32_t vb = in ? vob : kSkOOB, va = in ? voa : kSkOOB;
-#pragma unroll
-      for (int j = 0; j < SK_NBW; ++j) b[u][j] = sk_load(rb, vb, (16 * j * p.ldb + k) * 2);
-#pragma unroll
-      for (int i = 0; i < MB; ++i) a[u][i] = sk_load(ra, va, (16 * i * p.lda + k) * 2);
+    for (int e = 0; e < A_PER; ++e) {
+      const int c = threadIdx.x + e * SK_THREADS;
+      const int row = c / (U * 4), cc = c % (U * 4);
+      const int k = (st * U + (cc >> 2)) * 32 + (cc & 3) * 8;
+      const bool in = c < CHUNKS && k < p.K;
+      r[e] = __builtin_amdgcn_raw_buffer_load_b128(ra, in ? (uint32_t)(row * p.lda + k) * 2u : kSkOOB, 0, 0);
     }
   };
-  auto compute = [&](int s, const bf16x8 (&b)[SK_U][SK_NBW], const bf16x8 (&a)[SK_U][MB]) {
+  auto a_store = [&](int buf, const v4u (&r)[A_PER]) {
 #pragma unroll
-    for (int u = 0; u < SK_U; ++u) {
-      if (s + u >= s1) break;
-#pragma unroll
-      for (int j = 0; j < SK_NBW; ++j)
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-          acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[u][j], a[u][i], acc[j][i], 0, 0, 0);
+    for (int e = 0; e < A_PER; ++e) {
+      const int c = threadIdx.x + e * SK_THREADS;
+      if (c >= CHUNKS) continue;
+      const int row = c / (U * 4), cc = c % (U * 4);
+      const int u = cc >> 2, kq = cc & 3;
+      sa[buf][(u * MB + (row >> 4)) * 64 + (row & 15) + 16 * kq] = __builtin_bit_cast(bf16x8, r[e]);
     }
   };
-  if (s0 < s1) load_group(s0, b0, a0);
-  for (int s = s0; s < s1; s += 2 * SK_U) {
-    if (s + SK_U < s1) load_group(s + SK_U, b1, a1);
-    compute(s, b0, a0);
-    if (s + 2 * SK_U < s1) load_group(s + 2 * SK_U, b0, a0);
-    if (s + SK_U < s1) compute(s + SK_U, b1, a1);
-  }
+  auto b_load = [&](int st, bf16x8 (&b)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = (st * U + u) * 32;
+      const v4u x = __builtin_amdgcn_raw_buffer_load_b128(rb, k + lk < p.K ? vob : kSkOOB, k * 2, 0);
+      b[u] = __builtin_bit_cast(bf16x8, x);
+    }
+  };
+  f32x4 acc[MB];
+#pragma unroll
+  for (int i = 0; i < MB; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf, const bf16x8 (&b)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      bf16x8 a[MB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) a[i] = sa[buf][(u * MB + i) * 64 + lane];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[u], a[i], acc[i], 0, 0, 0);
+    }
+  };
 
-  // the four K ranges meet in LDS; block q = j * MB + i is summed by wave
-  // q % 4 in wave order 0, 1, 2, 3
-#pragma unroll
-  for (int j = 0; j < SK_NBW; ++j)
-#pragma unroll
-    for (int i = 0; i < MB; ++i) red[wave][j * MB + i][lane] = acc[j][i];
+  // stage s uses LDS buffer s % 2 and B registers b0 (even) / b1 (odd); the
+  // loads of stage s + 1 are in flight while stage s is computed
+  bf16x8 b0[U], b1[U];
+  v4u ar[A_PER];
+  a_load(0, ar);
+  a_store(0, ar);
+  if (stages > 1) a_load(1, ar);
+  b_load(0, b0);
   __syncthreads();
+  for (int st = 0; st < stages; st += 2) {
+    if (st + 1 < stages) b_load(st + 1, b1);
+    compute(0, b0);
+    if (st + 1 < stages) {
+      a_store(1, ar);
+      if (st + 2 < stages) a_load(st + 2, ar);
+    }
+    __syncthreads();
+    if (st + 1 >= stages) break;
+    if (st + 2 < stages) b_load(st + 2, b0);
+    compute(1, b1);
+    if (st + 2 < stages) {
+      a_store(0, ar);
+      if (st + 3 < stages) a_load(st + 3, ar);
+    }
+    __syncthreads();
+  }
 
   // in a 16x16 block the lane with row r = lane % 16 holds columns 4c..4c+3,
   // c = lane / 16; rows past the tile fall outside the resource
   const __amdgpu_buffer_rsrc_t rc = sk_rsrc(p.C + (size_t)row0 * p.ldc, (uint32_t)rows * p.ldc * 2u);
   const bool vec_c = ((p.ldc & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.C) & 7) == 0);
+  const int nl = (lane >> 4) * 4;  // column inside the wave's 16
 #pragma unroll
-  for (int q = 0; q < SK_NBW * MB; ++q) {
-    if (q % SK_WAVES != wave) continue;
-    const int j = q / MB, i = q - (q / MB) * MB;
-    f32x4 v = red[0][q][lane];
-#pragma unroll
-    for (int w = 1; w < SK_WAVES; ++w) v += red[w][q][lane];
+  for (int i = 0; i < MB; ++i) {
+    const f32x4 v = acc[i];
     const int m = i * 16 + lr;
-    const int nl = j * 16 + (lane >> 4) * 4;  // column inside the tile
     const uint32_t base = (uint32_t)(m * p.ldc + n0 + nl) * 2u;
     if (vec_c && nl + 3 < cols) {
       v2u w2;
@@ -198,14 +214,15 @@ int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s) {
   const long long grid = (long long)g.row_tiles * p.tiles_n;
   if (grid < 1 || grid > (1ll << 31) - 1) return fail(ASYM_EINVAL, "small-M GEMM: grid out of range");
   switch (g.mb) {
+    // stages of 8 k-steps (A stage 16 / 32 KiB of LDS); 4 with 64 rows (32 KiB)
     case 1:
-      hipLaunchKernelGGL(gemm_bf16_small_m<1>, dim3((unsigned)grid), dim3(SK_THREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_bf16_small_m<1, 8>), dim3((unsigned)grid), dim3(SK_THREADS), 0, s, p);
       break;
     case 2:
-      hipLaunchKernelGGL(gemm_bf16_small_m<2>, dim3((unsigned)grid), dim3(SK_THREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_bf16_small_m<2, 8>), dim3((unsigned)grid), dim3(SK_THREADS), 0, s, p);
       break;
     case 4:
-      hipLaunchKernelGGL(gemm_bf16_small_m<4>, dim3((unsigned)grid), dim3(SK_THREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_bf16_small_m<4, 4>), dim3((unsigned)grid), dim3(SK_THREADS), 0, s, p);
       break;
     default:
       return fail(ASYM_EINVAL, "small-M GEMM: row blocks must be 1, 2 or 4");

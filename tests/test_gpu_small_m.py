@@ -2,7 +2,8 @@
 CPU oracle, through the C ABI.
 
 Element by element over row counts on both sides of every 16-row block
-boundary, ragged column counts and K not a multiple of the 32-wide k-step;
+boundary, ragged column counts (tiles with waves past N), K not a multiple of
+the 32-wide k-step and K spanning one, two, three or many stages;
 the decode projection 32 x 14336 x 4096 on sampled columns; bitwise: every
 mapping, repeats and a CU-masked stream give the same bits, and on exact-integer
 inputs the small-M kernel and the persistent kernel (the path switched off)
@@ -37,7 +38,7 @@ def dev():
 
 
 @pytest.mark.parametrize("M", [1, 5, 16, 17, 31, 32, 33, 48, 63, 64])
-@pytest.mark.parametrize("N,K", [(1000, 72), (96, 1000), (257, 4104)])
+@pytest.mark.parametrize("N,K", [(1000, 72), (96, 1000), (257, 4104), (40, 264)])
 def test_small_m_elementwise(dev, M, N, K):
     p = workloads.make_problem(M, N, K, seed=100 + M)
     A, B = workloads.make_inputs(p)
@@ -59,7 +60,7 @@ def test_plan_picks_the_kernel(dev):
     assert plan(32, K=4100)["small_m"] == 0                       # K not a multiple of 8
     assert plan(32, xcd_mask=0x0F)["small_m"] == 0                # whole-XCD restriction
     p = plan(32)
-    assert (p["tile_n"], p["tiles_n"], p["grid"], p["claims"]) == (32, 16, 16, 0)
+    assert (p["tile_n"], p["tiles_n"], p["grid"], p["claims"]) == (64, 8, 8, 0)
     prev = asym.set_small_m(False)
     try:
         assert plan(32)["small_m"] == 0
