@@ -16,6 +16,14 @@ Contents
                      (Section 7.1 and the full-GPU lesson of Section 7.4)
   topology           the topology map's definition and exact invariants
                      (Section 5.1 topology discovery, Appendix G affinity)
+  affinity           XCD groups and home groups from per-address latencies
+                     (Section 6.1, Appendix G)
+  interleave         partition-hash bits from one- and two-bit address flips
+                     (Section 6.1, NUMA partition identification)
+  numa               chunk homes of an allocation and the local / remote read
+                     lists (Section 6.1 local and remote bandwidth)
+  attention          decode attention with grouped key/value heads, one
+                     float64 softmax per (request, head) (Section 7.1)
 """
 from __future__ import annotations
 

@@ -310,3 +310,52 @@ def planted_home_region(seed: int, n_pages: int, mask: int, n_verify: int = 64,
     pages = [p << 21 for p in range(n_pages)]
     vo = [int(v) * 128 for v in torch.randint(0, n_pages << 14, (n_verify,), generator=g)]
     return lat_of(pages), vo, lat_of(vo), home_of
+
+
+# Decode attention (Section 7.1 attention workloads; Appendix E): one query
+# token per request, head dimension 128, 32 query heads against 32 key/value
+# heads (multi-head) or 8 (grouped-query), batch 1..64, KV length from 512
+# doubling.  Recipe: one torch CPU generator per problem seeded `seed`, q then
+# K then V drawn N(0, 1) in fp32 in their storage shapes and rounded to bf16.
+# Layout: q [B, H_q, D], K and V [B, H_kv, S_k, D] (each request's head a
+# contiguous S_k x D slab).  The logical KV working set is 4 B S_k H_kv D bytes.
+@dataclass(frozen=True)
+class AttnProblem:
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    S: int
+    D: int = 128
+    seed: int = 6
+
+    @property
+    def kv_bytes(self) -> int:
+        return 4 * self.B * self.S * self.Hkv * self.D
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.D)
+
+
+def attn_problem(kind: str, B: int, S: int, seed: int = 6) -> AttnProblem:
+    Hkv = {"mha": 32, "gqa": 8}[kind]
+    return AttnProblem(f"decode_{kind}_B{B}_S{S}", B, 32, Hkv, S, seed=seed)
+
+
+def make_attn_inputs(p: AttnProblem):
+    """(q [B, H_q, D], K [B, H_kv, S, D], V [B, H_kv, S, D]) bf16 CPU tensors."""
+    g = torch.Generator(device="cpu").manual_seed(p.seed)
+    q = torch.randn((p.B, p.Hq, p.D), generator=g).to(torch.bfloat16)
+    k = torch.randn((p.B, p.Hkv, p.S, p.D), generator=g).to(torch.bfloat16)
+    v = torch.randn((p.B, p.Hkv, p.S, p.D), generator=g).to(torch.bfloat16)
+    return q, k, v
+
+
+def make_attn_inputs_on(p: AttnProblem, device):
+    """Same shapes and distribution drawn on `device` (timing runs at full size)."""
+    g = torch.Generator(device=device).manual_seed(p.seed)
+    q = torch.randn((p.B, p.Hq, p.D), generator=g, device=device).to(torch.bfloat16)
+    k = torch.randn((p.B, p.Hkv, p.S, p.D), generator=g, device=device).to(torch.bfloat16)
+    v = torch.randn((p.B, p.Hkv, p.S, p.D), generator=g, device=device).to(torch.bfloat16)
+    return q, k, v
