@@ -565,6 +565,48 @@ int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
  * previous setting.  Not synchronised with launches in flight. */
 int asym_gemm_set_small_m(int enable);
 
+/* ---- decode attention (Section 7.1 attention workloads, decode; Appendix E) */
+/* One query token per request against cached keys and values, with grouped
+ * key/value heads: for request b and query head h, with g = h / (H_q / H_kv),
+ *   O[b][h] = softmax_t(scale * q[b][h] . K[b][g][t]) . V[b][g][t]
+ *   lse[b][h] = log sum_t exp(scale * q[b][h] . K[b][g][t])   (nullable output)
+ * Layout (contiguous, caller-owned device memory): q [B][H_q][D], K and V
+ * [B][H_kv][S_k][D], O [B][H_q][D], all bf16; lse fp32 [B][H_q].  D must be
+ * 128 and H_q / H_kv one of 1, 2, 4, 8, 16.  q, K, V 16-byte aligned; O and
+ * lse 4-byte aligned.
+ * The sequence is cut into splits of split_tokens tokens (0 = automatic: the
+ * longest of 1024, 512, ... 64 giving at least 2048 tasks); a task is one
+ * (request, key/value head, split) and serves that head's query heads, so K
+ * and V are read once.  A second launch merges the splits of each (request,
+ * head) in split order.  Mapping: AWARE gives each XCD a share of the tasks
+ * proportional to its CU count in the stream's CU set (and honours a
+ * whole-XCD restriction); the oblivious mappings (both) hand out tasks
+ * round-robin by workgroup, an equal share per XCD.  Every mapping gives the
+ * same bits.  fp32 partials live in a per-stream library workspace, grown
+ * (after a stream synchronisation) when a call needs more.  Asynchronous.
+ * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
+int asym_attn_decode_bf16(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,
+                          const void* q, const void* k, const void* v, void* o, float* lse,
+                          float scale, int split_tokens, int mapping, uint32_t xcd_mask,
+                          void* stream);
+
+typedef struct asym_attn_plan_info {
+  int split_tokens;
+  int n_splits;
+  int tasks;               /* B * H_kv * n_splits */
+  int grid;                /* workgroups of the split launch */
+  int tasks_per_workgroup; /* one per wave */
+  int n_xcds;
+  int tasks_per_xcd[ASYM_MAX_XCDS];
+  size_t workspace_bytes;  /* fp32 partials: B * H_q * n_splits * 130 * 4 */
+} asym_attn_plan_info;
+
+/* What asym_attn_decode_bf16 would launch (no pointers needed; launches
+ * nothing).  Errors as asym_attn_decode_bf16. */
+int asym_attn_decode_plan(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,
+                          int split_tokens, int mapping, uint32_t xcd_mask, void* stream,
+                          asym_attn_plan_info* out);
+
 /* ---- streaming copy and co-run (Sections 7.2, 7.3) ---------------------- */
 /* dst[i] = src[i] for n_bytes bytes (16-byte aligned, n_bytes a multiple of
  * 16), `passes` times over the buffer, with 16-byte accesses from every lane.

@@ -41,7 +41,8 @@ EXPORTS = (
     "asym_dispatch_check", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
-    "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_plan", "asym_gemm_set_small_m", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
+    "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_plan", "asym_gemm_set_small_m",
+    "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
 
@@ -162,6 +163,17 @@ class GemmPlanInfo(ctypes.Structure):
         return d
 
 
+class AttnPlanInfo(ctypes.Structure):
+    _fields_ = [("split_tokens", ctypes.c_int), ("n_splits", ctypes.c_int), ("tasks", ctypes.c_int),
+                ("grid", ctypes.c_int), ("tasks_per_workgroup", ctypes.c_int), ("n_xcds", ctypes.c_int),
+                ("tasks_per_xcd", ctypes.c_int * MAX_XCDS), ("workspace_bytes", ctypes.c_size_t)]
+
+    def to_dict(self) -> dict:
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "tasks_per_xcd"}
+        d["tasks_per_xcd"] = list(self.tasks_per_xcd)[:self.n_xcds]
+        return d
+
+
 class TaskResult(ctypes.Structure):
     _fields_ = [("ms_total", ctypes.c_double), ("ms_per_iter", ctypes.c_double),
                 ("tflops", ctypes.c_double), ("gbps", ctypes.c_double),
@@ -225,6 +237,8 @@ def load_library(path: str = LIB_PATH):
         "asym_gemm_plan": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp,
                                ctypes.POINTER(GemmPlanInfo)]),
         "asym_gemm_set_small_m": (i, [i]),
+        "asym_attn_decode_bf16": (i, [topo_p, i, i, i, i, i, vp, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
+        "asym_attn_decode_plan": (i, [topo_p, i, i, i, i, i, i, i, u32, vp, ctypes.POINTER(AttnPlanInfo)]),
         "asym_copy_bf16": (i, [vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
         "asym_corun": (i, [topo_p, ctypes.POINTER(Task), i, ctypes.POINTER(TaskResult)]),
         "asym_last_error": (cp, []),
@@ -653,6 +667,51 @@ def gemm_grouped(A, B, M: Sequence[int], C=None, mapping="aware", topo: Optional
         ctypes.c_void_p(A.data_ptr()), max(A.stride(0), K), ctypes.c_void_p(B.data_ptr()), ldb,
         ctypes.c_void_p(C.data_ptr()), max(C.stride(0), N), mp, xcd_mask, _stream_ptr(stream)))
     return C
+
+
+def attn_decode(q, k, v, o=None, lse=None, scale: Optional[float] = None, split_tokens: int = 0,
+                mapping="aware", topo: Optional[Topology] = None, xcd_mask: int = 0, stream=None):
+    """Decode attention: q [B, H_q, D], k and v [B, H_kv, S_k, D] bf16 CUDA
+    tensors (contiguous); returns O [B, H_q, D] bf16 (and fills lse [B, H_q]
+    fp32 when given).  scale defaults to 1 / sqrt(D)."""
+    import math
+
+    import torch
+    if q.dtype != torch.bfloat16 or k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16:
+        raise TypeError("q, k, v must be bfloat16")
+    if not (q.is_cuda and k.is_cuda and v.is_cuda):
+        raise ValueError("q, k, v must be on the GPU")
+    if q.dim() != 3 or k.dim() != 4 or v.shape != k.shape:
+        raise ValueError("q must be [B, H_q, D] and k, v [B, H_kv, S_k, D]")
+    if not (q.is_contiguous() and k.is_contiguous() and v.is_contiguous()):
+        raise ValueError("q, k, v must be contiguous")
+    B, Hq, D = q.shape
+    Bk, Hkv, S, Dk = k.shape
+    if Bk != B or Dk != D:
+        raise ValueError("q and k disagree on B or D")
+    if o is None:
+        o = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=q.device)
+    if o.dtype != torch.bfloat16 or tuple(o.shape) != (B, Hq, D) or not o.is_contiguous():
+        raise ValueError("o must be a contiguous bf16 [B, H_q, D] tensor")
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hq) or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous fp32 [B, H_q] tensor")
+    sc = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    _check(load_library().asym_attn_decode_bf16(
+        topo.handle if topo else None, B, Hq, Hkv, S, D, ctypes.c_void_p(q.data_ptr()),
+        ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(o.data_ptr()),
+        ctypes.c_void_p(lse.data_ptr() if lse is not None else None), sc, split_tokens, mp, xcd_mask,
+        _stream_ptr(stream)))
+    return o
+
+
+def attn_decode_plan(B: int, Hq: int, Hkv: int, S: int, D: int = 128, split_tokens: int = 0,
+                     mapping="aware", topo: Optional[Topology] = None, xcd_mask: int = 0, stream=None) -> dict:
+    out = AttnPlanInfo()
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    _check(load_library().asym_attn_decode_plan(topo.handle if topo else None, B, Hq, Hkv, S, D, split_tokens,
+                                                mp, xcd_mask, _stream_ptr(stream), ctypes.byref(out)))
+    return out.to_dict()
 
 
 def set_small_m(enable: bool) -> bool:

@@ -1,0 +1,293 @@
+// Decode attention with grouped key/value heads (the attention workloads of
+// Section 7.1, decode case: one query token per request; Appendix E gives the
+// head dimension 128 and 32 or 8 key/value heads).
+//
+//   O[b, h] = softmax_t(scale * <q[b, h], K[b, g, t]>) . V[b, g, :],  g = h / G
+//
+// Work is split along the key/value sequence (flash-decoding): a task is one
+// (request, key/value head, sequence split) and serves the G query heads that
+// read that head, so every K and V byte is read once.  One wave runs one task:
+//   * scores of 16 tokens x 16 query-head rows come from four
+//     v_mfma_f32_16x16x32_bf16, K fragments loaded straight from HBM into
+//     operand registers (a lane's 8 bf16 are 16 contiguous bytes of one key);
+//   * an online softmax per head keeps the running max and sum;
+//   * P.V runs on the vector ALU: a lane owns 8 of the 128 dimensions and a
+//     quarter of the block's tokens, value rows are 16-byte loads, and the
+//     probabilities reach it through a per-wave LDS tile (V's layout puts the
+//     token index across rows, which an MFMA operand would need transposed);
+//   * the next block's K and V are in flight while a block is computed.
+// Each task writes its unnormalised output, max and sum (fp32); a second
+// kernel merges the splits of each (request, head) in split order, so the
+// result is the same for every assignment of tasks to workgroups.
+//
+// Assignment.  A task's bytes are read by exactly one wave, so there is no
+// cache reuse for a placement to exploit; what the topology decides is how
+// many tasks each XCD gets.  Workgroup i runs on XCD i mod n (round-robin
+// dispatch).  Oblivious: tasks 4i .. 4i+3 go to workgroup i, every XCD gets
+// the same share whatever its CU count.  Aware: each XCD's share of the task
+// list is proportional to its CU count in the stream's CU set, and XCD x's
+// workgroups i = x, x + n, ... take consecutive groups of 4 of its share.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace asym {
+namespace {
+
+constexpr int AD = 128;            // head dimension
+constexpr int AT_WAVES = 4;        // tasks per workgroup, one per wave
+constexpr uint32_t kAtOOB = 0x80000000u;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+
+struct AttnParams {
+  const uint16_t* q;   // [B][Hq][128]
+  const uint16_t* k;   // [B][Hkv][S][128]
+  const uint16_t* v;   // [B][Hkv][S][128]
+  float* part_o;       // [B][Hq][n_splits][128]
+  float* part_ml;      // [B][Hq][n_splits][2]: max, sum
+  const int* quota_off;  // aware: [n_x + 1] start of each XCD's share (tasks), null = oblivious
+  int B, Hq, Hkv, S, split, n_splits, tasks, n_x;
+  float scale;
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t at_rsrc(const void* base, uint32_t bytes) {
+  const unsigned long long a = (unsigned long long)base;
+  const unsigned long long u = ((unsigned long long)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+                               (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0,
+                                           (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// One task on one wave.  G: query heads per key/value head (1 .. 16).
+template <int G>
+__device__ void attn_task(const AttnParams& p, int task, float* __restrict__ sp) {
+  const int lane = threadIdx.x & 63;
+  const int split = task % p.n_splits;
+  const int bh = task / p.n_splits;          // b * Hkv + kv head
+  const int b = bh / p.Hkv, hk = bh - b * p.Hkv;
+  const int t0 = split * p.split;
+  const int t1 = min(p.S, t0 + p.split);
+  const int nblk = (t1 - t0 + 15) >> 4;
+
+  // q rows of the G heads; rows past G read as zero
+  const __amdgpu_buffer_rsrc_t rq = at_rsrc(p.q + ((size_t)b * p.Hq + (size_t)hk * G) * AD, G * AD * 2u);
+  const __amdgpu_buffer_rsrc_t rk = at_rsrc(p.k + (size_t)bh * p.S * AD, (uint32_t)p.S * AD * 2u);
+  const __amdgpu_buffer_rsrc_t rv = at_rsrc(p.v + (size_t)bh * p.S * AD, (uint32_t)p.S * AD * 2u);
+  const int lr = lane & 15, lq = lane >> 4;
+  bf16x8 qf[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    qf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rq, (uint32_t)(lr * AD + lq * 8 + 32 * c) * 2u, 0, 0));
+
+  // score lanes: head lr, tokens 4 lq .. 4 lq + 3 of a block;
+  // value lanes: dimensions 8 lr .. 8 lr + 7, tokens lq, lq + 4, lq + 8, lq + 12
+  float m_run = -INFINITY, l_part = 0.f;
+  float o[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+
+  auto load_k = [&](int blk, bf16x8 (&kf)[4]) {
+    const int tok = t0 + blk * 16 + lr;
+    const uint32_t base = tok < t1 ? (uint32_t)(tok * AD + lq * 8) * 2u : kAtOOB;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      kf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, base, 64 * c, 0));
+  };
+  auto load_v = [&](int blk, v4u (&vf)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tok = t0 + blk * 16 + 4 * i + lq;
+      vf[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, tok < t1 ? (uint32_t)(tok * AD + lr * 8) * 2u : kAtOOB,
+                                                    0, 0);
+    }
+  };
+
+  bf16x8 kc[4], kn[4];
+  v4u vc[4], vn[4];
+  load_k(0, kc);
+  load_v(0, vc);
+  for (int blk = 0; blk < nblk; ++blk) {
+    const bool more = blk + 1 < nblk;
+    if (more) {
+      load_k(blk + 1, kn);
+      load_v(blk + 1, vn);
+    }
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[c], qf[c], s, 0, 0, 0);
+    // mask tokens past the split, scale, block max per head
+    float bm = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int tok = t0 + blk * 16 + 4 * lq + r;
+      s[r] = tok < t1 ? s[r] * p.scale : -INFINITY;
+      bm = fmaxf(bm, s[r]);
+    }
+    bm = fmaxf(bm, __shfl_xor(bm, 16));
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    const float m_new = fmaxf(m_run, bm);   // finite: every block has a token
+    const float alpha = __expf(m_run - m_new);
+    m_run = m_new;
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float e = __expf(s[r] - m_new);
+      ps += e;
+      if (lr < G) sp[(4 * lq + r) * 16 + lr] = e;
+    }
+    l_part = l_part * alpha + ps;
+    if (lane < G) sp[256 + lane] = alpha;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // P.V on the value lanes
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float a = sp[256 + g];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] *= a;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 4 * i + lq;
+      float vx[8];
+      vx[0] = bf_lo(vc[i].x); vx[1] = bf_hi(vc[i].x);
+      vx[2] = bf_lo(vc[i].y); vx[3] = bf_hi(vc[i].y);
+      vx[4] = bf_lo(vc[i].z); vx[5] = bf_hi(vc[i].z);
+      vx[6] = bf_lo(vc[i].w); vx[7] = bf_hi(vc[i].w);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float pg = sp[t * 16 + g];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pg, vx[e], o[g][e]);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (more) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) kc[c] = kn[c];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) vc[i] = vn[i];
+    }
+  }
+  // the four token groups of a dimension chunk, and of a head's sum
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      o[g][e] += __shfl_xor(o[g][e], 16);
+      o[g][e] += __shfl_xor(o[g][e], 32);
+    }
+  l_part += __shfl_xor(l_part, 16);
+  l_part += __shfl_xor(l_part, 32);
+  const size_t row0 = ((size_t)b * p.Hq + (size_t)hk * G) * p.n_splits + split;  // (b, h = hk G, split)
+  if (lq == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float* dst = p.part_o + (row0 + (size_t)g * p.n_splits) * AD + lr * 8;
+      *reinterpret_cast<f32x4*>(dst) = f32x4{o[g][0], o[g][1], o[g][2], o[g][3]};
+      *reinterpret_cast<f32x4*>(dst + 4) = f32x4{o[g][4], o[g][5], o[g][6], o[g][7]};
+    }
+    if (lr < G) {
+      float* ml = p.part_ml + (row0 + (size_t)lr * p.n_splits) * 2;
+      ml[0] = m_run;
+      ml[1] = l_part;
+    }
+  }
+}
+
+template <int G>
+__global__ void __launch_bounds__(64 * AT_WAVES) attn_decode_split(AttnParams p) {
+  __shared__ float sp_all[AT_WAVES][256 + 16];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int task;
+  if (p.quota_off) {
+    const int x = blockIdx.x % p.n_x, j = blockIdx.x / p.n_x;
+    const int begin = p.quota_off[x], end = p.quota_off[x + 1];
+    task = begin + j * AT_WAVES + wave;
+    if (task >= end) return;
+  } else {
+    task = blockIdx.x * AT_WAVES + wave;
+    if (task >= p.tasks) return;
+  }
+  attn_task<G>(p, task, sp_all[wave]);
+}
+
+// Merge of the splits of one (request, head) per wave, in split order.
+__global__ void __launch_bounds__(256) attn_decode_merge(const float* __restrict__ part_o,
+                                                         const float* __restrict__ part_ml, int rows,
+                                                         int n_splits, uint16_t* __restrict__ o,
+                                                         float* __restrict__ lse) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const float* ml = part_ml + (size_t)row * n_splits * 2;
+  float M = -INFINITY;
+  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml[2 * s]);
+  float L = 0.f, a0 = 0.f, a1 = 0.f;
+  for (int s = 0; s < n_splits; ++s) {
+    const float w = __expf(ml[2 * s] - M);
+    L = fmaf(ml[2 * s + 1], w, L);
+    const float* src = part_o + ((size_t)row * n_splits + s) * AD + 2 * lane;
+    a0 = fmaf(src[0], w, a0);
+    a1 = fmaf(src[1], w, a1);
+  }
+  const float inv = 1.f / L;
+  const __bf16 h0 = (__bf16)(a0 * inv), h1 = (__bf16)(a1 * inv);
+  const uint32_t packed = (uint32_t)__builtin_bit_cast(unsigned short, h0) |
+                          ((uint32_t)__builtin_bit_cast(unsigned short, h1) << 16);
+  reinterpret_cast<uint32_t*>(o + (size_t)row * AD)[lane] = packed;
+  if (lse && lane == 0) lse[row] = M + __logf(L);
+}
+
+}  // namespace
+
+int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
+  AttnParams p;
+  p.q = static_cast<const uint16_t*>(a.q);
+  p.k = static_cast<const uint16_t*>(a.k);
+  p.v = static_cast<const uint16_t*>(a.v);
+  p.part_o = a.part_o;
+  p.part_ml = a.part_ml;
+  p.quota_off = a.d_quota_off;
+  p.B = a.B;
+  p.Hq = a.Hq;
+  p.Hkv = a.Hkv;
+  p.S = a.S;
+  p.split = a.split;
+  p.n_splits = a.n_splits;
+  p.tasks = a.B * a.Hkv * a.n_splits;
+  p.n_x = a.n_x;
+  p.scale = a.scale;
+  const int G = a.Hq / a.Hkv;
+  const dim3 grid((unsigned)a.grid), block(64 * AT_WAVES);
+  switch (G) {
+    case 1: hipLaunchKernelGGL(attn_decode_split<1>, grid, block, 0, s, p); break;
+    case 2: hipLaunchKernelGGL(attn_decode_split<2>, grid, block, 0, s, p); break;
+    case 4: hipLaunchKernelGGL(attn_decode_split<4>, grid, block, 0, s, p); break;
+    case 8: hipLaunchKernelGGL(attn_decode_split<8>, grid, block, 0, s, p); break;
+    case 16: hipLaunchKernelGGL(attn_decode_split<16>, grid, block, 0, s, p); break;
+    default: return fail(ASYM_EUNSUPPORTED, "attention: query heads per key/value head must be 1, 2, 4, 8 or 16");
+  }
+  ASYM_HIP(hipGetLastError());
+  const int rows = a.B * a.Hq;
+  hipLaunchKernelGGL(attn_decode_merge, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a.part_o, a.part_ml,
+                     rows, a.n_splits, static_cast<uint16_t*>(a.o), a.lse);
+  ASYM_HIP(hipGetLastError());
+  return ASYM_OK;
+}
+
+int attn_tasks_per_workgroup() { return AT_WAVES; }
+
+}  // namespace asym

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <atomic>
 #include <chrono>
 #include <cstring>
@@ -80,6 +81,11 @@ struct Workspace {
   size_t g_host_bytes = 0;
   hipEvent_t g_copied = nullptr;
   bool g_pending = false;
+  // decode attention: split partials (grown on demand) and the per-XCD task
+  // offsets of recent aware plans (key: tasks, per-XCD slots), most recent first
+  float* attn_buf = nullptr;
+  size_t attn_bytes = 0;
+  std::vector<std::pair<std::vector<int>, int*>> attn_off;
 };
 
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
@@ -219,6 +225,63 @@ int small_m_for(const GemmPlan& P, int max_rows) {
   return small_m_blocks(max_rows);
 }
 
+// The CU set a launch on `stream` may use: the device's topology (probed on
+// first use unless given), the stream's per-XCD CU counts, and the workers per
+// XCD after an optional whole-XCD restriction (one per CU).
+struct CuSet {
+  const Topology* t = nullptr;
+  int device = 0;
+  std::vector<int> per, slots;
+  int total = 0, smax = 0;
+  bool whole = true;
+};
+
+static int cu_set_for(const asym_topology* topo_in, int mapping, uint32_t xcd_mask, hipStream_t stream,
+                      const char* what, CuSet* cs) {
+  const std::string w(what);
+  int device = 0;
+  int rc = current_device(&device);
+  if (rc != ASYM_OK) return rc;
+  const Topology* t = unwrap(topo_in);
+  if (!t) {
+    rc = default_topology(device, &t);
+    if (rc != ASYM_OK) return rc;
+  } else if (t->device != device && t->device >= 0) {
+    return fail(ASYM_EINVAL, w + ": topology was probed on another device");
+  }
+  uint32_t mask[ASYM_MASK_WORDS];
+  rc = stream_cu_mask(stream, t->n_cus, mask);
+  if (rc != ASYM_OK) return rc;
+  std::vector<int> per;
+  rc = mask_counts(*t, mask, per);
+  if (rc != ASYM_OK) return rc;
+  const uint32_t all = (t->n_xccs >= 32) ? 0xFFFFFFFFu : ((1u << t->n_xccs) - 1u);
+  const uint32_t xm = xcd_mask == 0 ? all : (xcd_mask & all);
+  if (xcd_mask != 0 && (xcd_mask & ~all)) return fail(ASYM_EINVAL, w + ": xcd_mask names XCDs the device does not have");
+  if (mapping != ASYM_MAP_AWARE && xm != all)
+    return fail(ASYM_EUNSUPPORTED, w + ": XCD restriction needs the aware mapping (oblivious mappings place work statically)");
+  for (int x = 0; x < t->n_xccs; ++x)
+    if (per[x] == 0)
+      return fail(ASYM_EUNSUPPORTED, w + ": the stream's CU mask leaves XCD " + std::to_string(x) +
+                                         " without a CU; workgroups dealt to it could never run");
+  std::vector<int> slots(t->n_xccs, 0);
+  int total = 0, smax = 0;
+  for (int x = 0; x < t->n_xccs; ++x) {
+    slots[x] = ((xm >> x) & 1u) ? per[x] : 0;
+    total += slots[x];
+    smax = std::max(smax, slots[x]);
+  }
+  if (total == 0) return fail(ASYM_EINVAL, w + ": the CU set is empty");
+  cs->t = t;
+  cs->device = device;
+  cs->per = std::move(per);
+  cs->slots = std::move(slots);
+  cs->total = total;
+  cs->smax = smax;
+  cs->whole = xm == all;
+  return ASYM_OK;
+}
+
 static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
                      const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
                      uint32_t xcd_mask, hipStream_t stream, GemmPlan* P) {
@@ -237,39 +300,12 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
       (int64_t)BMr * ldc * 2 >= (1ll << 31))
     return fail(ASYM_EUNSUPPORTED, "gemm: leading dimension too large for 32-bit tile offsets");
 
-  int device = 0;
-  int rc = current_device(&device);
+  CuSet cs;
+  int rc = cu_set_for(topo_in, mapping, xcd_mask, stream, "gemm", &cs);
   if (rc != ASYM_OK) return rc;
-  const Topology* t = unwrap(topo_in);
-  if (!t) {
-    rc = default_topology(device, &t);
-    if (rc != ASYM_OK) return rc;
-  } else if (t->device != device && t->device >= 0) {
-    return fail(ASYM_EINVAL, "gemm: topology was probed on another device");
-  }
-  uint32_t mask[ASYM_MASK_WORDS];
-  rc = stream_cu_mask(stream, t->n_cus, mask);
-  if (rc != ASYM_OK) return rc;
-  std::vector<int> per;
-  rc = mask_counts(*t, mask, per);
-  if (rc != ASYM_OK) return rc;
-  const uint32_t all = (t->n_xccs >= 32) ? 0xFFFFFFFFu : ((1u << t->n_xccs) - 1u);
-  const uint32_t xm = xcd_mask == 0 ? all : (xcd_mask & all);
-  if (xcd_mask != 0 && (xcd_mask & ~all)) return fail(ASYM_EINVAL, "gemm: xcd_mask names XCDs the device does not have");
-  if (mapping != ASYM_MAP_AWARE && xm != all)
-    return fail(ASYM_EUNSUPPORTED, "gemm: XCD restriction needs the aware mapping (oblivious mappings place tiles statically)");
-  for (int x = 0; x < t->n_xccs; ++x)
-    if (per[x] == 0)
-      return fail(ASYM_EUNSUPPORTED, "gemm: the stream's CU mask leaves XCD " + std::to_string(x) +
-                                         " without a CU; workgroups dealt to it could never run");
-  std::vector<int> slots(t->n_xccs, 0);
-  int total = 0, smax = 0;
-  for (int x = 0; x < t->n_xccs; ++x) {
-    slots[x] = ((xm >> x) & 1u) ? per[x] : 0;  // one persistent workgroup per CU
-    total += slots[x];
-    smax = std::max(smax, slots[x]);
-  }
-  if (total == 0) return fail(ASYM_EINVAL, "gemm: the CU set is empty");
+  const Topology* t = cs.t;
+  const int device = cs.device, total = cs.total, smax = cs.smax;
+  std::vector<int> per = cs.per, slots = cs.slots;
 
   const bool vec_ab = aligned16(A) && aligned16(B) && (K % 8 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
   const bool vec = vec_ab && (((uintptr_t)C & 7u) == 0) && (ldc % 4 == 0);
@@ -290,7 +326,7 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   P->dynamic = false;
   for (int x = 0; x < t->n_xccs; ++x)
     if (per[x] < smax) P->dynamic = true;
-  P->whole = xm == all;
+  P->whole = cs.whole;
   P->per = std::move(per);
   P->slots = std::move(slots);
   P->small_mb = small_m_for(*P, M);
@@ -482,6 +518,160 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   return launch_gemm(gl, stream);
 }
 
+// ---- decode attention -------------------------------------------------------
+struct AttnPlan {
+  CuSet cs;
+  int split = 0, n_splits = 0, tasks = 0, grid = 0;
+  std::vector<int> quota;  // aware: tasks per XCD
+  size_t ws_bytes = 0;
+};
+
+static int attn_plan(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int D, int split_in,
+                     int mapping, uint32_t xcd_mask, hipStream_t stream, AttnPlan* P) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || S < 1) return fail(ASYM_EINVAL, "attention: B, H_q, H_kv, S_k must be >= 1");
+  if (Hq % Hkv) return fail(ASYM_EINVAL, "attention: H_kv must divide H_q");
+  const int G = Hq / Hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
+    return fail(ASYM_EUNSUPPORTED, "attention: query heads per key/value head must be 1, 2, 4, 8 or 16");
+  if (D != 128) return fail(ASYM_EUNSUPPORTED, "attention: the head dimension must be 128");
+  if (S >= (1 << 24)) return fail(ASYM_EUNSUPPORTED, "attention: S_k of 2^24 or more (32-bit offsets into a head's keys)");
+  if (split_in < 0 || split_in % 16 || split_in > (1 << 20))
+    return fail(ASYM_EINVAL, "attention: split_tokens must be 0 (automatic) or a positive multiple of 16");
+  if (mapping != ASYM_MAP_AWARE && mapping != ASYM_MAP_OBLIVIOUS_GROUPED && mapping != ASYM_MAP_OBLIVIOUS_ROWMAJOR)
+    return fail(ASYM_EINVAL, "attention: unknown mapping");
+  int rc = cu_set_for(topo_in, mapping, xcd_mask, stream, "attention", &P->cs);
+  if (rc != ASYM_OK) return rc;
+  const int64_t heads = (int64_t)B * Hkv;
+  int L = split_in;
+  if (!L) {
+    // the longest split (up to 1024 tokens) that still gives 2048 tasks
+    L = 1024;
+    while (L > 64 && heads * ((S + L - 1) / L) < 2048) L /= 2;
+  }
+  const int64_t n_splits = (S + L - 1) / L;
+  const int64_t tasks = heads * n_splits;
+  if (tasks > (1ll << 30)) return fail(ASYM_EINVAL, "attention: too many tasks");
+  P->split = L;
+  P->n_splits = (int)n_splits;
+  P->tasks = (int)tasks;
+  const int per_wg = attn_tasks_per_workgroup();
+  const int n_x = P->cs.t->n_xccs;
+  if (mapping == ASYM_MAP_AWARE) {
+    P->quota = largest_remainder_quotas(P->tasks, P->cs.slots);
+    int most = 0;
+    for (int x = 0; x < n_x; ++x) most = std::max(most, (P->quota[x] + per_wg - 1) / per_wg);
+    P->grid = std::max(1, most * n_x);
+  } else {
+    P->grid = (P->tasks + per_wg - 1) / per_wg;
+  }
+  P->ws_bytes = (size_t)B * Hq * n_splits * (128 + 2) * sizeof(float);
+  return ASYM_OK;
+}
+
+int attn_decode(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int D, const void* q, const void* k,
+                const void* v, void* o, float* lse, float scale, int split_in, int mapping, uint32_t xcd_mask,
+                hipStream_t stream) {
+  if (!q || !k || !v || !o) return fail(ASYM_EINVAL, "attention: null pointer");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || ((uintptr_t)o & 3u) || ((uintptr_t)lse & 3u))
+    return fail(ASYM_EINVAL, "attention: q, K, V must be 16-byte aligned, O and lse 4-byte aligned");
+  if (!std::isfinite(scale)) return fail(ASYM_EINVAL, "attention: scale must be finite");
+  std::lock_guard<std::mutex> lock(g_mu);
+  AttnPlan P;
+  int rc = attn_plan(topo_in, B, Hq, Hkv, S, D, split_in, mapping, xcd_mask, stream, &P);
+  if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(P.cs.device, stream, &ws);
+  if (rc != ASYM_OK) return rc;
+  if (ws->attn_bytes < P.ws_bytes) {
+    // the old buffer may still be read by launches on this stream
+    ASYM_HIP(hipStreamSynchronize(stream));
+    if (ws->attn_buf) ASYM_HIP(hipFree(ws->attn_buf));
+    ws->attn_buf = nullptr;
+    ws->attn_bytes = 0;
+    const size_t bytes = std::max<size_t>(P.ws_bytes, 1 << 20);
+    ASYM_HIP(hipMalloc(&ws->attn_buf, bytes));
+    ws->attn_bytes = bytes;
+  }
+  const int n_x = P.cs.t->n_xccs;
+  int* d_off = nullptr;
+  if (mapping == ASYM_MAP_AWARE) {
+    std::vector<int> key(P.cs.slots);
+    key.push_back(P.tasks);
+    auto hit = std::find_if(ws->attn_off.begin(), ws->attn_off.end(),
+                            [&](const std::pair<std::vector<int>, int*>& e) { return e.first == key; });
+    if (hit != ws->attn_off.end()) {
+      std::rotate(ws->attn_off.begin(), hit, hit + 1);
+    } else {
+      if (ws->attn_off.size() >= 8) {
+        ASYM_HIP(hipStreamSynchronize(stream));
+        ASYM_HIP(hipFree(ws->attn_off.back().second));
+        ws->attn_off.pop_back();
+      }
+      int* dev_off = nullptr;
+      ASYM_HIP(hipMalloc(&dev_off, (ASYM_MAX_XCDS + 1) * sizeof(int)));
+      if (ws->g_pending) {
+        ASYM_HIP(hipEventSynchronize(ws->g_copied));
+        ws->g_pending = false;
+      }
+      if (ws->g_host_bytes < (ASYM_MAX_XCDS + 1) * sizeof(int)) {
+        if (ws->g_host) ASYM_HIP(hipHostFree(ws->g_host));
+        ws->g_host = nullptr;
+        ws->g_host_bytes = 0;
+        ASYM_HIP(hipHostMalloc(&ws->g_host, 64 << 10));
+        ws->g_host_bytes = 64 << 10;
+      }
+      if (!ws->g_copied) ASYM_HIP(hipEventCreateWithFlags(&ws->g_copied, hipEventDisableTiming));
+      int* h = static_cast<int*>(ws->g_host);
+      h[0] = 0;
+      for (int x = 0; x < n_x; ++x) h[x + 1] = h[x] + P.quota[x];
+      ASYM_HIP(hipMemcpyAsync(dev_off, h, (n_x + 1) * sizeof(int), hipMemcpyHostToDevice, stream));
+      ASYM_HIP(hipEventRecord(ws->g_copied, stream));
+      ws->g_pending = true;
+      ws->attn_off.insert(ws->attn_off.begin(), std::make_pair(std::move(key), dev_off));
+    }
+    d_off = ws->attn_off.front().second;
+  }
+  AttnLaunch a;
+  a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse;
+  a.part_o = ws->attn_buf;
+  a.part_ml = ws->attn_buf + (size_t)B * Hq * P.n_splits * 128;
+  a.d_quota_off = d_off;
+  a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.S = S;
+  a.split = P.split; a.n_splits = P.n_splits;
+  a.n_x = n_x; a.grid = P.grid;
+  a.scale = scale;
+  return launch_attn_decode(a, stream);
+}
+
+int attn_decode_plan(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int D, int split_in,
+                     int mapping, uint32_t xcd_mask, hipStream_t stream, asym_attn_plan_info* out) {
+  if (!out) return fail(ASYM_EINVAL, "attention plan: null output");
+  std::lock_guard<std::mutex> lock(g_mu);
+  AttnPlan P;
+  const int rc = attn_plan(topo_in, B, Hq, Hkv, S, D, split_in, mapping, xcd_mask, stream, &P);
+  if (rc != ASYM_OK) return rc;
+  *out = asym_attn_plan_info{};
+  out->split_tokens = P.split;
+  out->n_splits = P.n_splits;
+  out->tasks = P.tasks;
+  out->grid = P.grid;
+  out->tasks_per_workgroup = attn_tasks_per_workgroup();
+  out->n_xcds = P.cs.t->n_xccs;
+  out->workspace_bytes = P.ws_bytes;
+  const int per_wg = attn_tasks_per_workgroup();
+  for (int x = 0; x < out->n_xcds && x < ASYM_MAX_XCDS; ++x) {
+    if (mapping == ASYM_MAP_AWARE) {
+      out->tasks_per_xcd[x] = P.quota[x];
+    } else {
+      // workgroup i lands on XCD i mod n and holds tasks per_wg i .. per_wg i + per_wg - 1
+      long long c = 0;
+      for (int i = x; i < P.grid; i += out->n_xcds) c += std::min(per_wg, P.tasks - i * per_wg);
+      out->tasks_per_xcd[x] = (int)c;
+    }
+  }
+  return ASYM_OK;
+}
+
 int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
               const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
               uint32_t xcd_mask, hipStream_t stream, asym_gemm_plan_info* out) {
@@ -539,6 +729,8 @@ void release_workspace(hipStream_t s) {
     if (it->first.second == s) {
       hipFree(it->second.gemm_ctr);
       hipFree(it->second.copy_ctr);
+      if (it->second.attn_buf) hipFree(it->second.attn_buf);
+      for (auto& t : it->second.attn_off) hipFree(t.second);
       for (auto& t : it->second.g_tables) {
         hipFree(t.desc);
         hipFree(t.sched);
@@ -663,4 +855,19 @@ extern "C" int asym_version(void) { return 1; }
 
 extern "C" int asym_gemm_set_small_m(int enable) {
   return asym::g_small_m.exchange(enable != 0) ? 1 : 0;
+}
+
+extern "C" int asym_attn_decode_bf16(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,
+                                     const void* q, const void* k, const void* v, void* o, float* lse,
+                                     float scale, int split_tokens, int mapping, uint32_t xcd_mask,
+                                     void* stream) {
+  return asym::attn_decode(topo, B, H_q, H_kv, S_k, D, q, k, v, o, lse, scale, split_tokens, mapping, xcd_mask,
+                           static_cast<hipStream_t>(stream));
+}
+
+extern "C" int asym_attn_decode_plan(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,
+                                     int split_tokens, int mapping, uint32_t xcd_mask, void* stream,
+                                     asym_attn_plan_info* out) {
+  return asym::attn_decode_plan(topo, B, H_q, H_kv, S_k, D, split_tokens, mapping, xcd_mask,
+                                static_cast<hipStream_t>(stream), out);
 }

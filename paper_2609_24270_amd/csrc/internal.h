@@ -101,6 +101,20 @@ int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s);
 int small_m_blocks(int max_rows);  // 1, 2, 4, or 0 above 64 rows
 int small_m_tile_cols();
 
+// Decode attention (head dimension 128).
+struct AttnLaunch {
+  const void *q, *k, *v;
+  void* o;
+  float* lse;                 // nullable
+  float* part_o;              // [B][Hq][n_splits][128]
+  float* part_ml;             // [B][Hq][n_splits][2]
+  const int* d_quota_off;     // aware: device [n_x + 1]; null = oblivious
+  int B, Hq, Hkv, S, split, n_splits, n_x, grid;
+  float scale;
+};
+int launch_attn_decode(const AttnLaunch& a, hipStream_t s);
+int attn_tasks_per_workgroup();
+
 int probe_identity_run(int device, hipStream_t s, int n_blocks,
                        std::vector<int32_t>& rec);
 int probe_latency_run(int device, Topology& t);
