@@ -418,6 +418,71 @@ def numa_bw_study(dev, hash_res, rounds: int = 3, gib: int = 16):
             "GBps": {k: round(v / rounds, 1) for k, v in acc.items()}}
 
 
+def attention_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 3):
+    """Decode attention (32 query heads, head dimension 128; grouped-query with
+    8 key/value heads and multi-head with 32) over batch and KV length: the
+    logical KV working set W = 4 B S_k H_kv D bytes per time, aware and
+    oblivious on the full GPU, and on one seeded random 128-CU set (unequal CUs
+    per XCD) with the same attention running on the complementary CUs."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    out = {}
+    for kind in ("gqa", "mha"):
+        for B in (1, 16, 64):
+            for S in (1024, 8192, 32768):
+                p = workloads.attn_problem(kind, B, S)
+                if p.kv_bytes > (16 << 30):
+                    continue
+                q, k, v = workloads.make_attn_inputs_on(p, dev)
+                o = torch.empty_like(q)
+                fns = {m: (lambda m=m: asym.attn_decode(q, k, v, o, mapping=m, stream=stream))
+                       for m in ("aware", "oblivious_rowmajor")}
+                for f in fns.values():
+                    f()
+                ms = queued(fns, launches, rounds, stream)
+                out[p.name] = {"W_GB": round(p.kv_bytes / 1e9, 4),
+                               **{f"{m}_us": round(1e3 * t, 2) for m, t in ms.items()},
+                               "aware_TBps_W": round(p.kv_bytes / (ms["aware"] * 1e-3) / 1e12, 3)}
+                del q, k, v, o
+    torch.cuda.empty_cache()
+    # unequal CU counts: a seeded random 128-CU set, the complement running the same work
+    res = {}
+    if masked:
+        p = workloads.attn_problem("gqa", 16, 8192)
+        q, k, v = workloads.make_attn_inputs_on(p, dev)
+        q2, k2, v2 = workloads.make_attn_inputs_on(p, dev)
+        o, o2 = torch.empty_like(q), torch.empty_like(q)
+        mask = workloads.random_mask_bits(workloads.COLOC.seed, 1, 128)[0]
+        comp = [b for b in range(256) if b not in set(mask)]
+        sa, sb = asym.stream_create(topo, mask), asym.stream_create(topo, comp)
+        try:
+            for m in ("aware", "oblivious_rowmajor"):
+                f = lambda: asym.attn_decode(q, k, v, o, mapping=m, topo=topo, stream=sa)
+                g = lambda: asym.attn_decode(q2, k2, v2, o2, mapping="aware", topo=topo, stream=sb)
+                for _ in range(3):
+                    f(), g()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(sa)
+                for _ in range(20):
+                    f()
+                    g()
+                e1.record(sa)
+                torch.cuda.synchronize()
+                t = e0.elapsed_time(e1) / 20
+                res[m] = {"us": round(1e3 * t, 2), "TBps_W": round(p.kv_bytes / (t * 1e-3) / 1e12, 3)}
+            res["cus_per_xcd"] = topo.cuset_counts(mask)
+            res["workload"] = p.name
+        finally:
+            asym.stream_destroy(sa)
+            asym.stream_destroy(sb)
+        del q, k, v, q2, k2, v2
+        torch.cuda.empty_cache()
+    return {"configs": out, "random_128_cu_set_with_tenant": res}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -434,11 +499,12 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa",
+    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa,attention",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
-                         "remote read bandwidth); 'none' for the headline only")
+                         "remote read bandwidth), attention (decode attention); 'none' for the "
+                         "headline only")
     ap.add_argument("--spread-masks", type=int, default=32)
     ap.add_argument("--mapping-only", default=None,
                     help="time only this mapping, no studies (profiling runs)")
@@ -545,6 +611,8 @@ def main() -> int:
         line["cu_set_spread"] = spread_study(topo, dev, args.spread_masks, 20, halves)
     if "grouped" in studies:
         line["grouped_gemm"] = grouped_study(dev, stream, range(1, 6), 8, 5)
+    if "attention" in studies:
+        line["decode_attention"] = attention_study(topo, dev, stream, args.probe != "identity")
     if "numa" in studies:
         summ, hres = interleave_summary(dev)
         line["partition_hash"] = summ
