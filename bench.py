@@ -483,6 +483,66 @@ def attention_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: 
     return {"configs": out, "random_128_cu_set_with_tenant": res}
 
 
+FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "chunk_read")
+
+
+def focus_run(name: str, dev, stream, launches: int) -> dict:
+    """One workload launched `launches` times after 3 warm-ups (for profiler runs):
+      decode_gemm      small-M GEMM 32 x 14336 x 4096 (decode projection)
+      grouped_small_m  grouped GEMM (32 groups of ~20 rows) x (6144, 7168), seed 5
+      attention_gqa    decode attention, grouped-query, B = 64, S_k = 32768
+      chunk_read       strided read of a 16 GiB region in 8 KiB chunks, address order
+    Reports the mean per launch (HIP events on the launch stream) and the
+    algorithmic bytes each launch must read or write."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    if name == "decode_gemm":
+        (_, _), (da, db) = workloads.make_pd_inputs()
+        A, B = da.to(dev), db.to(dev)
+        C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
+        fn = lambda: asym.gemm(A, B, C, stream=stream)
+        nbytes = 2 * (A.numel() + B.numel() + C.numel())
+        kernel = "gemm_bf16_small_m<2, 8>"
+    elif name == "grouped_small_m":
+        p = workloads.grouped_problem(32, 20, 6144, 7168)
+        Ms, A, B = workloads.make_grouped_inputs_on(p, dev)
+        C = torch.empty((sum(Ms), p.N), dtype=torch.bfloat16, device=dev)
+        fn = lambda: asym.gemm_grouped(A, B, Ms, C, stream=stream)
+        nbytes = p.working_set_bytes
+        kernel = "gemm_bf16_small_m<2, 8>"
+    elif name == "attention_gqa":
+        p = workloads.attn_problem("gqa", 64, 32768)
+        q, k, v = workloads.make_attn_inputs_on(p, dev)
+        o = torch.empty_like(q)
+        fn = lambda: asym.attn_decode(q, k, v, o, stream=stream)
+        nbytes = p.kv_bytes + 2 * 2 * q.numel()
+        kernel = "attn_decode_split<4> + attn_decode_merge"
+    elif name == "chunk_read":
+        nb = 16 << 30
+        raw = torch.empty(nb + (2 << 20), dtype=torch.uint8, device=dev)
+        ptr = raw.data_ptr() + ((-raw.data_ptr()) % (2 << 20))
+        raw.fill_(1)
+        import numpy as np
+        homes = np.zeros(nb >> 13, dtype=np.int8)
+        chunks, off = asym.chunk_lists(homes, 8, [0] * 4 + [1] * 4, asym.CHUNKS_ALL)
+        fn = lambda: asym.chunk_read_bw(ptr, nb, 13, chunks, off, iters=1, stream=stream)
+        nbytes = nb
+        kernel = "chunk_read_kernel"
+    else:
+        raise ValueError(name)
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    if name == "chunk_read":
+        ms = sum(fn()[0] for _ in range(launches)) / launches
+    else:
+        ms = queued({"f": fn}, launches, 1, stream)["f"]
+    return {"focus": name, "kernel": kernel, "launches": launches, "ms_per_launch": round(ms, 5),
+            "algorithmic_bytes": int(nbytes), "TBps": round(nbytes / (ms * 1e-3) / 1e12, 3)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -506,6 +566,8 @@ def main() -> int:
                          "remote read bandwidth), attention (decode attention); 'none' for the "
                          "headline only")
     ap.add_argument("--spread-masks", type=int, default=32)
+    ap.add_argument("--focus", choices=FOCUS, default=None,
+                    help="run only this workload (profiling runs); prints its own JSON line")
     ap.add_argument("--mapping-only", default=None,
                     help="time only this mapping, no studies (profiling runs)")
     args = ap.parse_args()
@@ -533,6 +595,9 @@ def main() -> int:
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_each_way": src.numel() * 2, "launches": 10}))
+        return 0
+    if args.focus:
+        print(json.dumps(focus_run(args.focus, dev, torch.cuda.current_stream(), args.steps)), flush=True)
         return 0
     studies = set() if args.mapping_only or args.studies == "none" else set(args.studies.split(","))
     if args.probe == "identity":
