@@ -544,7 +544,8 @@ typedef struct asym_gemm_plan_info {
   int n_xcds;
   int workers_per_xcd[ASYM_MAX_XCDS]; /* persistent kernel only (0 on the small-M path) */
   int small_m;     /* 1: the small-M kernel (a plain launch of 64-column tiles,
-                      tile_m = 16, 32 or 64 rows, each wave 16 columns over all of K) */
+                      tile_m = 16, 32 or 64 rows, each wave 16 columns over all of K;
+                      grid = workgroups in the mapping's order) */
 } asym_gemm_plan_info;
 
 int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
@@ -553,11 +554,15 @@ int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
                    uint32_t xcd_mask, void* stream, asym_gemm_plan_info* out);
 
 /* Small-M path.  A GEMM with M <= 64 (a grouped GEMM whose groups all have at
- * most 64 rows) on the vector path and on every XCD of its CU set (xcd_mask 0
- * or all XCDs) runs a different kernel: with so few rows the product is bound
- * by reading B once from HBM, no tile is reused, and a tile placement has
- * nothing to gain, so every mapping gives the same launch and bitwise the same
- * result.  Each workgroup computes 64 columns of C for all rows; each of its
+ * most 64 rows), or with at most 256 rows when its 64-row tiles number no more
+ * than two per CU of the set, on the vector path and on every XCD of its CU
+ * set (xcd_mask 0 or all XCDs) runs a different kernel, built for reading B
+ * at HBM rate.  With one row tile no B byte is reused and every mapping gives
+ * the same launch; with several, the mapping orders the workgroups: aware runs
+ * the row tiles that read one B panel one after another on one XCD (the panel
+ * crosses into its L2 once), the oblivious orders put them on neighbouring
+ * workgroups (column-major, different XCDs) or a row of tiles apart
+ * (row-major).  Every order gives bitwise the same result.  Each workgroup computes 64 columns of C for all rows; each of its
  * four waves streams its 16 rows of B over all of K straight into MFMA
  * operands, with A shared through LDS.  This call
  * switches the path on or off for the whole process (default on; off sends

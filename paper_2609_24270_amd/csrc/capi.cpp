@@ -220,9 +220,30 @@ struct GemmPlan {
 // the persistent kernel, whose workers leave the excluded XCDs).
 std::atomic<bool> g_small_m{true};
 
-int small_m_for(const GemmPlan& P, int max_rows) {
-  if (!g_small_m.load() || !P.vec_ab || !P.whole) return 0;
-  return small_m_blocks(max_rows);
+// Up to 64 rows (per group) the small-M kernel always wins (measured: decode
+// projections and 20-row expert groups).  From 65 to kSmallMMaxRows rows it
+// runs 64-row tiles, and each of them re-reads the shared A fragments from LDS
+// in every wave, so it only wins while its workgroups fit about two per CU
+// (where the persistent kernel's 256-row tiles leave most CUs idle); with more
+// work the persistent kernel is faster (measured: 4096- and 14336-column
+// products of 64 to 512 rows, the 192-row expert groups).
+constexpr int kSmallMMaxRows = 256;
+
+int small_m_for(const GemmPlan& P, int max_rows, long long wgs_at_64_rows) {
+  if (!g_small_m.load() || !P.vec_ab || !P.whole || max_rows > kSmallMMaxRows) return 0;
+  if (max_rows <= 64) return small_m_blocks(max_rows);
+  return wgs_at_64_rows <= 2ll * P.total ? 4 : 0;
+}
+
+// Workgroups of a plain small-M launch: the aware order pads the column tiles
+// to a multiple of the XCD count.
+long long small_m_grid(int row_tiles, int tiles_n, int order, int n_x) {
+  if (order == 0) return (long long)((tiles_n + n_x - 1) / n_x) * row_tiles * n_x;
+  return (long long)row_tiles * tiles_n;
+}
+
+int small_m_order(int mapping) {
+  return mapping == ASYM_MAP_AWARE ? 0 : mapping == ASYM_MAP_OBLIVIOUS_GROUPED ? 1 : 2;
 }
 
 // The CU set a launch on `stream` may use: the device's topology (probed on
@@ -329,7 +350,7 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   P->whole = cs.whole;
   P->per = std::move(per);
   P->slots = std::move(slots);
-  P->small_mb = small_m_for(*P, M);
+  P->small_mb = small_m_for(*P, M, (long long)((M + 63) / 64) * ((N + small_m_tile_cols() - 1) / small_m_tile_cols()));
   return ASYM_OK;
 }
 
@@ -345,7 +366,10 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
     sm.A = A; sm.B = B; sm.C = C;
     sm.M = M; sm.N = N; sm.K = K; sm.lda = lda; sm.ldb = ldb; sm.ldc = ldc;
     sm.mb = P.small_mb;
-    sm.row_tiles = 1;
+    sm.row_tiles = (M + 16 * P.small_mb - 1) / (16 * P.small_mb);
+    sm.order = small_m_order(mapping);
+    sm.n_x = P.t->n_xccs;
+    sm.grid = small_m_grid(sm.row_tiles, (N + small_m_tile_cols() - 1) / small_m_tile_cols(), sm.order, sm.n_x);
     return launch_gemm_small_m(sm, stream);
   }
   const DeviceSchedule* ds = nullptr;
@@ -405,7 +429,9 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   int rc = plan_gemm(topo_in, virt_m, N, K, A, lda, B, ldb, ASYM_B_NK, C, ldc, mapping, xcd_mask, stream, &P);
   if (rc != ASYM_OK) return rc;
   const int max_rows = *std::max_element(Ms, Ms + G);
-  const int small_mb = small_m_for(P, max_rows);
+  long long wgs64 = 0;
+  for (int g = 0; g < G; ++g) wgs64 += (long long)((Ms[g] + 63) / 64) * ((N + small_m_tile_cols() - 1) / small_m_tile_cols());
+  const int small_mb = small_m_for(P, max_rows, wgs64);
   const int tiles_n = small_mb ? (N + small_m_tile_cols() - 1) / small_m_tile_cols() : (N + P.bn - 1) / P.bn;
   Workspace* ws = nullptr;
   rc = get_workspace(P.device, stream, &ws);
@@ -421,10 +447,41 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
     std::rotate(ws->g_tables.begin(), hit, hit + 1);  // most recent first
   } else {
     Schedule sch;
+    std::vector<int4> small_desc;
     if (small_mb) {
-      // one row tile per nonempty group; the grid is a plain launch
-      for (int g = 0; g < G; ++g)
-        if (Ms[g] > 0) sch.order.push_back(g);
+      // one workgroup per (group, row tile, 64-column tile), in the mapping's
+      // order; the aware order runs a column's row tiles one after another on
+      // one XCD (each group's run padded to a multiple of the XCD count with
+      // empty entries, so the XCD of an entry is its column mod n)
+      const int n_x = P.t->n_xccs;
+      const int tr = 16 * small_mb;
+      const int order = small_m_order(mapping);
+      int row0 = 0;
+      for (int g = 0; g < G; ++g) {
+        const int R = (Ms[g] + tr - 1) / tr;
+        auto put = [&](int r, int c) {
+          if (c >= tiles_n) {
+            small_desc.push_back(int4{0, 0, 0, 0});
+            return;
+          }
+          small_desc.push_back(int4{row0 + r * tr, std::min(tr, Ms[g] - r * tr), g * N, c * small_m_tile_cols()});
+        };
+        if (R > 0) {
+          if (order == 0) {
+            for (int cb = 0; cb < (tiles_n + n_x - 1) / n_x; ++cb)
+              for (int r = 0; r < R; ++r)
+                for (int j = 0; j < n_x; ++j) put(r, cb * n_x + j);
+          } else if (order == 1) {
+            for (int c = 0; c < tiles_n; ++c)
+              for (int r = 0; r < R; ++r) put(r, c);
+          } else {
+            for (int r = 0; r < R; ++r)
+              for (int c = 0; c < tiles_n; ++c) put(r, c);
+          }
+        }
+        row0 += Ms[g];
+      }
+      for (size_t i = 0; i < small_desc.size(); ++i) sch.order.push_back((int)i);
       sch.off.assign(P.t->n_xccs + 1, 0);
     } else {
       rc = build_grouped_schedule(G, tm.data(), tiles_n, P.t->n_xccs, P.slots.data(), mapping, sch);
@@ -462,11 +519,7 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
     int4* h_desc = static_cast<int4*>(ws->g_host);
     int* h_sched = reinterpret_cast<int*>(static_cast<char*>(ws->g_host) + desc_bytes);
     if (small_mb) {
-      int id = 0, row0 = 0;
-      for (int g = 0; g < G; ++g) {
-        if (Ms[g] > 0) h_desc[id++] = int4{row0, Ms[g], g * N, 0};
-        row0 += Ms[g];
-      }
+      std::copy(small_desc.begin(), small_desc.end(), h_desc);
     } else {
       int id = 0, row0 = 0;
       for (int g = 0; g < G; ++g) {
@@ -494,7 +547,8 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
     sm.A = A; sm.B = B; sm.C = C;
     sm.M = (int)rows; sm.N = N; sm.K = K; sm.lda = lda; sm.ldb = ldb; sm.ldc = ldc;
     sm.mb = small_mb;
-    sm.row_tiles = T;
+    sm.n_x = P.t->n_xccs;
+    sm.grid = T;
     sm.d_desc = tb.desc;
     return launch_gemm_small_m(sm, stream);
   }
@@ -687,9 +741,9 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
     out->vector_path = 1;
     out->tile_m = 16 * P.small_mb;
     out->tile_n = small_m_tile_cols();
-    out->tiles_m = 1;
+    out->tiles_m = (M + out->tile_m - 1) / out->tile_m;
     out->tiles_n = (N + out->tile_n - 1) / out->tile_n;
-    out->grid = out->tiles_n;
+    out->grid = (int)small_m_grid(out->tiles_m, out->tiles_n, small_m_order(mapping), P.t->n_xccs);
     out->workers = out->grid;
     out->claims = 0;
     out->small_m = 1;

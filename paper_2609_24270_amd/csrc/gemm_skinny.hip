@@ -17,8 +17,13 @@
 // byte is fetched once and no tile is reused, so there is no placement to
 // choose: the grid is a plain launch over the tiles.
 //
-// A row tile is one plain problem (rows 0..M-1) or one group of a grouped
-// problem, given by a descriptor {first row, rows, first B row, unused}.
+// A plain problem is cut into row tiles of 16 MB rows (one tile up to 64
+// rows); a grouped problem's workgroups each read a descriptor {first row,
+// rows, first B row, first column}.  Where a B panel is read by several row
+// tiles, the aware order runs them one after another on one XCD, so the panel
+// crosses into that XCD's L2 once; the oblivious orders put them on
+// neighbouring workgroups (column-major, dealt to different XCDs) or a row of
+// tiles apart (row-major).
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -42,8 +47,11 @@ struct SkinnyParams {
   const uint16_t* B;
   uint16_t* C;
   int M, N, K, lda, ldb, ldc;
-  int tiles_n;        // 64-column tiles per row tile
-  const int4* desc;   // per row tile {first row, rows, first B row, 0}; null = one tile of M rows
+  int tiles_n;        // 64-column tiles
+  int row_tiles;      // plain GEMM: row tiles of 16 MB rows
+  int order;          // plain GEMM: 0 aware, 1 column-major, 2 row-major
+  int n_x;            // XCDs (workgroup i runs on XCD i mod n_x)
+  const int4* desc;   // grouped: per workgroup {first row, rows, first B row, first column}; rows 0 = none
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t sk_rsrc(const void* base, uint32_t bytes) {
@@ -66,17 +74,40 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
   __shared__ bf16x8 sa[2][U * MB * 64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int tile = blockIdx.x;
-  const int rt = tile / p.tiles_n, ct = tile - rt * p.tiles_n;
-  int row0 = 0, rows = p.M, brow0 = 0;
+  int row0, rows, brow0, ncol0;
   if (p.desc) {
-    const int4 d = p.desc[rt];
+    const int4 d = p.desc[blockIdx.x];
     row0 = __builtin_amdgcn_readfirstlane(d.x);
     rows = __builtin_amdgcn_readfirstlane(d.y);
     brow0 = __builtin_amdgcn_readfirstlane(d.z);
+    ncol0 = __builtin_amdgcn_readfirstlane(d.w);
+    if (rows <= 0) return;
+  } else {
+    // plain GEMM: which (row tile r, column tile c) this workgroup computes
+    const int i = blockIdx.x;
+    int r, c;
+    if (p.order == 0) {
+      // aware: the row tiles of column tile c run one after another on XCD
+      // c mod n_x, so the B panel they all read crosses into that XCD's L2 once
+      const int lane_x = i % p.n_x, q = i / p.n_x;
+      const int cb = q / p.row_tiles;
+      r = q - cb * p.row_tiles;
+      c = cb * p.n_x + lane_x;
+    } else if (p.order == 1) {
+      c = i / p.row_tiles;  // column-major: a column's row tiles on neighbouring workgroups
+      r = i - c * p.row_tiles;
+    } else {
+      r = i / p.tiles_n;    // row-major
+      c = i - r * p.tiles_n;
+    }
+    if (c >= p.tiles_n || r >= p.row_tiles) return;
+    row0 = r * 16 * MB;
+    rows = min(16 * MB, p.M - row0);
+    brow0 = 0;
+    ncol0 = c * SK_COLS;
   }
   // this wave's 16 columns; a wave past N has an empty B range and stores nothing
-  const int n0 = ct * SK_COLS + wave * 16;
+  const int n0 = ncol0 + wave * 16;
   const int cols = max(0, min(16, p.N - n0));
 
   // rows past the tile read as zero (outside the resource); a 16-byte chunk at
@@ -210,8 +241,11 @@ int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s) {
   p.ldb = g.ldb;
   p.ldc = g.ldc;
   p.tiles_n = (g.N + SK_COLS - 1) / SK_COLS;
+  p.row_tiles = g.row_tiles;
+  p.order = g.order;
+  p.n_x = g.n_x;
   p.desc = static_cast<const int4*>(g.d_desc);
-  const long long grid = (long long)g.row_tiles * p.tiles_n;
+  const long long grid = g.grid;
   if (grid < 1 || grid > (1ll << 31) - 1) return fail(ASYM_EINVAL, "small-M GEMM: grid out of range");
   switch (g.mb) {
     // stages of 8 k-steps (A stage 16 / 32 KiB of LDS); 4 with 64 rows (32 KiB)

@@ -94,8 +94,11 @@ struct SmallMLaunch {
   const void* A; const void* B; void* C;
   int M, N, K, lda, ldb, ldc;
   int mb;                       // 16-row blocks per row tile: 1, 2 or 4
-  int row_tiles;                // 1 for a plain GEMM, nonempty groups for a grouped one
-  const void* d_desc = nullptr; // grouped: device int4 per row tile {row, rows, B row, 0}
+  int row_tiles = 1;            // plain GEMM: row tiles of 16 mb rows
+  int order = 0;                // plain GEMM: 0 aware, 1 column-major, 2 row-major
+  int n_x = 8;                  // XCDs
+  long long grid = 0;           // workgroups
+  const void* d_desc = nullptr; // grouped: device int4 per workgroup {row, rows, B row, column}
 };
 int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s);
 int small_m_blocks(int max_rows);  // 1, 2, 4, or 0 above 64 rows

@@ -37,13 +37,14 @@ def dev():
     return torch.device("cuda:0")
 
 
-@pytest.mark.parametrize("M", [1, 5, 16, 17, 31, 32, 33, 48, 63, 64])
-@pytest.mark.parametrize("N,K", [(1000, 72), (96, 1000), (257, 4104), (40, 264)])
+@pytest.mark.parametrize("M", [1, 5, 16, 17, 31, 32, 33, 48, 63, 64, 65, 100, 128, 200, 256])
+@pytest.mark.parametrize("N,K", [(1000, 72), (96, 1000), (257, 4104), (40, 264)])  # <= 2 row-tile WGs per CU
 def test_small_m_elementwise(dev, M, N, K):
     p = workloads.make_problem(M, N, K, seed=100 + M)
     A, B = workloads.make_inputs(p)
     plan = asym.gemm_plan(A=A.to(dev), B=B.to(dev))
     assert plan["small_m"] == 1 and plan["tile_m"] == (16 if M <= 16 else 32 if M <= 32 else 64)
+    assert plan["tiles_m"] == (M + plan["tile_m"] - 1) // plan["tile_m"]
     C = asym.gemm(A.to(dev), B.to(dev))
     torch.cuda.synchronize()
     R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
@@ -56,11 +57,19 @@ def test_plan_picks_the_kernel(dev):
         A = torch.zeros((M, K), dtype=torch.bfloat16, device=dev)
         B = torch.zeros((512, K), dtype=torch.bfloat16, device=dev)
         return asym.gemm_plan(A=A, B=B, **kw)
-    assert plan(64)["small_m"] == 1 and plan(65)["small_m"] == 0
+    assert plan(64)["small_m"] == 1 and plan(256)["small_m"] == 1 and plan(257)["small_m"] == 0
+    # more than two 64-row workgroups per CU: the persistent kernel
+    A = torch.zeros((256, 4096), dtype=torch.bfloat16, device=dev)
+    B = torch.zeros((14336, 4096), dtype=torch.bfloat16, device=dev)
+    assert asym.gemm_plan(A=A, B=B)["small_m"] == 0 and asym.gemm_plan(A=A[:128], B=B)["small_m"] == 1
+    p65 = plan(65)
+    assert (p65["tile_m"], p65["tiles_m"], p65["grid"]) == (64, 2, 16)      # aware: 8 columns x 2 rows
+    assert plan(65, mapping="oblivious_rowmajor")["grid"] == 16
     assert plan(32, K=4100)["small_m"] == 0                       # K not a multiple of 8
     assert plan(32, xcd_mask=0x0F)["small_m"] == 0                # whole-XCD restriction
     p = plan(32)
     assert (p["tile_n"], p["tiles_n"], p["grid"], p["claims"]) == (64, 8, 8, 0)
+    assert plan(200, mapping="aware")["grid"] == 32 and plan(200, mapping="oblivious_grouped")["grid"] == 32
     prev = asym.set_small_m(False)
     try:
         assert plan(32)["small_m"] == 0
@@ -148,3 +157,41 @@ def test_grouped_small_groups_exact_integer_equals_persistent(dev):
     for g in (0, 7, 31):
         _, Co = oracle.grouped_gemm_bf16(bits(A)[rows[g]:rows[g + 1]], bits(B)[g:g + 1], [Ms[g]], False)
         assert np.array_equal(small[rows[g]:rows[g + 1]], Co)
+
+
+@pytest.mark.parametrize("M,N", [(200, 3000), (128, 14336), (130, 1000)])
+def test_row_tiles_every_order_bitwise(dev, M, N):
+    """Several 64-row tiles: the three placement orders give the same bits."""
+    p = workloads.make_problem(M, N, 4096, seed=M, dist="llm")
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    outs = [bits(asym.gemm(Ad, Bd, mapping=m)) for m in MAPS]
+    assert all(np.array_equal(outs[0], o) for o in outs[1:])
+    g = np.random.default_rng(M)
+    cols = np.unique(np.concatenate([g.choice(N, 256, replace=False), [N - 1]]))
+    R, _ = oracle.gemm_bf16(bits(A), bits(B)[cols], "nk")
+    assert_gemm_close(outs[0][:, cols], R, what=f"{M}x{N}x4096")
+
+
+def test_grouped_groups_up_to_256_rows(dev):
+    """Groups of 134..249 rows (the (32, 192) expert configuration's draw, 8
+    groups kept): element by element against the oracle, bitwise across the
+    orders, and bitwise equal to the persistent kernel on exact integers."""
+    p = workloads.grouped_problem(8, 192, 1000, 512, seed=5)
+    Ms, A, B = workloads.make_grouped_inputs(p)
+    assert max(Ms) > 64 and max(Ms) <= 256
+    Ad, Bd = A.to(dev), B.to(dev)
+    outs = [bits(asym.gemm_grouped(Ad, Bd, Ms, mapping=m)) for m in MAPS]
+    assert all(np.array_equal(outs[0], o) for o in outs[1:])
+    R, _ = oracle.grouped_gemm_bf16(bits(A), bits(B), Ms)
+    assert_gemm_close(outs[0], R, what="grouped up to 256 rows")
+    pi = workloads.grouped_problem(8, 192, 1000, 512, seed=5, dist="int")
+    Ms, A, B = workloads.make_grouped_inputs(pi)
+    Ad, Bd = A.to(dev), B.to(dev)
+    small = bits(asym.gemm_grouped(Ad, Bd, Ms))
+    prev = asym.set_small_m(False)
+    try:
+        pers = bits(asym.gemm_grouped(Ad, Bd, Ms))
+    finally:
+        asym.set_small_m(prev)
+    assert np.array_equal(small, pers)
