@@ -546,6 +546,10 @@ typedef struct asym_gemm_plan_info {
   int small_m;     /* 1: the small-M kernel (a plain launch of 64-column tiles,
                       tile_m = 16, 32 or 64 rows, each wave 16 columns over all of K;
                       grid = workgroups in the mapping's order) */
+  int k_splits;    /* small-M kernel with one row tile and fewer 64-column tiles
+                      than the device has CUs: K is cut into this many ranges, one
+                      workgroup each, and a second launch adds the fp32 partial
+                      tiles in range order (1 = no split) */
 } asym_gemm_plan_info;
 
 int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,

@@ -155,7 +155,7 @@ class GemmPlanInfo(ctypes.Structure):
                 ("grid", ctypes.c_int), ("workers", ctypes.c_int),
                 ("claims", ctypes.c_int), ("vector_path", ctypes.c_int),
                 ("n_xcds", ctypes.c_int), ("workers_per_xcd", ctypes.c_int * MAX_XCDS),
-                ("small_m", ctypes.c_int)]
+                ("small_m", ctypes.c_int), ("k_splits", ctypes.c_int)]
 
     def to_dict(self) -> dict:
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "workers_per_xcd"}

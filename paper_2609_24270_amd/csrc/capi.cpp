@@ -85,6 +85,9 @@ struct Workspace {
   // offsets of recent aware plans (key: tasks, per-XCD slots), most recent first
   float* attn_buf = nullptr;
   size_t attn_bytes = 0;
+  // small-M GEMM with a split K: fp32 partial tiles (grown on demand)
+  float* sm_part = nullptr;
+  size_t sm_part_bytes = 0;
   std::vector<std::pair<std::vector<int>, int*>> attn_off;
 };
 
@@ -246,6 +249,25 @@ int small_m_order(int mapping) {
   return mapping == ASYM_MAP_AWARE ? 0 : mapping == ASYM_MAP_OBLIVIOUS_GROUPED ? 1 : 2;
 }
 
+// A CU reads HBM at about 20-24 GB/s at most, so a single row tile with fewer
+// 64-column tiles than the device has CUs splits K into ranges, one workgroup
+// each (up to 8, each range at least two stages of k-steps); a second launch
+// adds the ranges' fp32 tiles in range order (the launch boundary makes the
+// partial tiles of every XCD visible; a hand-off inside the kernel needs
+// device-scope fences that write back and invalidate whole L2s, and measured
+// slower than no split).  The count
+// depends only on the shape and the device, not on the stream's CU set, so a
+// product has the same bits on every set.
+int small_m_ksplit(int M, int N, int K, int mb, int device_cus) {
+  if (M > 64) return 1;
+  const int tiles = (N + small_m_tile_cols() - 1) / small_m_tile_cols();
+  const int steps = (K + 31) / 32;
+  const int u = mb == 4 ? 4 : 8;
+  int ks = std::min(8, device_cus / std::max(1, tiles));
+  ks = std::min(ks, steps / (2 * u));
+  return std::max(1, ks);
+}
+
 // The CU set a launch on `stream` may use: the device's topology (probed on
 // first use unless given), the stream's per-XCD CU counts, and the workers per
 // XCD after an optional whole-XCD restriction (one per CU).
@@ -369,7 +391,27 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
     sm.row_tiles = (M + 16 * P.small_mb - 1) / (16 * P.small_mb);
     sm.order = small_m_order(mapping);
     sm.n_x = P.t->n_xccs;
-    sm.grid = small_m_grid(sm.row_tiles, (N + small_m_tile_cols() - 1) / small_m_tile_cols(), sm.order, sm.n_x);
+    const int tiles_n = (N + small_m_tile_cols() - 1) / small_m_tile_cols();
+    sm.grid = small_m_grid(sm.row_tiles, tiles_n, sm.order, sm.n_x);
+    sm.ksplit = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
+    if (sm.ksplit > 1) {
+      Workspace* ws = nullptr;
+      rc = get_workspace(P.device, stream, &ws);
+      if (rc != ASYM_OK) return rc;
+      const size_t part_bytes = (size_t)tiles_n * sm.ksplit * 16 * P.small_mb * 64 * sizeof(float);
+      if (ws->sm_part_bytes < part_bytes) {
+        // a buffer in use by launches on this stream is freed after they finish
+        ASYM_HIP(hipStreamSynchronize(stream));
+        if (ws->sm_part) ASYM_HIP(hipFree(ws->sm_part));
+        ws->sm_part = nullptr;
+        ws->sm_part_bytes = 0;
+        const size_t pb = std::max<size_t>(part_bytes, 4 << 20);
+        ASYM_HIP(hipMalloc(&ws->sm_part, pb));
+        ws->sm_part_bytes = pb;
+      }
+      sm.part = ws->sm_part;
+      sm.grid = (long long)tiles_n * sm.ksplit;
+    }
     return launch_gemm_small_m(sm, stream);
   }
   const DeviceSchedule* ds = nullptr;
@@ -744,6 +786,8 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
     out->tiles_m = (M + out->tile_m - 1) / out->tile_m;
     out->tiles_n = (N + out->tile_n - 1) / out->tile_n;
     out->grid = (int)small_m_grid(out->tiles_m, out->tiles_n, small_m_order(mapping), P.t->n_xccs);
+    out->k_splits = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
+    if (out->k_splits > 1) out->grid = out->tiles_n * out->k_splits;
     out->workers = out->grid;
     out->claims = 0;
     out->small_m = 1;
@@ -758,6 +802,7 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   out->claims = (mapping == ASYM_MAP_AWARE && P.dynamic) ? 1 : 0;
   for (int x = 0; x < P.t->n_xccs && x < ASYM_MAX_XCDS; ++x) out->workers_per_xcd[x] = P.slots[x];
   out->small_m = 0;
+  out->k_splits = 1;
   return ASYM_OK;
 }
 
@@ -784,6 +829,7 @@ void release_workspace(hipStream_t s) {
       hipFree(it->second.gemm_ctr);
       hipFree(it->second.copy_ctr);
       if (it->second.attn_buf) hipFree(it->second.attn_buf);
+      if (it->second.sm_part) hipFree(it->second.sm_part);
       for (auto& t : it->second.attn_off) hipFree(t.second);
       for (auto& t : it->second.g_tables) {
         hipFree(t.desc);

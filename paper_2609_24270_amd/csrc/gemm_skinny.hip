@@ -52,6 +52,8 @@ struct SkinnyParams {
   int order;          // plain GEMM: 0 aware, 1 column-major, 2 row-major
   int n_x;            // XCDs (workgroup i runs on XCD i mod n_x)
   const int4* desc;   // grouped: per workgroup {first row, rows, first B row, first column}; rows 0 = none
+  int ksplit;         // plain GEMM, one row tile: K ranges per column tile (1 = none)
+  float* part;        // ksplit > 1: fp32 partial tiles [column tile][range][16 MB][64]
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t sk_rsrc(const void* base, uint32_t bytes) {
@@ -74,7 +76,7 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
   __shared__ bf16x8 sa[2][U * MB * 64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  int row0, rows, brow0, ncol0;
+  int row0, rows, brow0, ncol0, kr = 0, ctile = 0;
   if (p.desc) {
     const int4 d = p.desc[blockIdx.x];
     row0 = __builtin_amdgcn_readfirstlane(d.x);
@@ -86,7 +88,12 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
     // plain GEMM: which (row tile r, column tile c) this workgroup computes
     const int i = blockIdx.x;
     int r, c;
-    if (p.order == 0) {
+    if (p.ksplit > 1) {
+      // one row tile; workgroups i = c * ksplit + range
+      c = i / p.ksplit;
+      kr = i - c * p.ksplit;
+      r = 0;
+    } else if (p.order == 0) {
       // aware: the row tiles of column tile c run one after another on XCD
       // c mod n_x, so the B panel they all read crosses into that XCD's L2 once
       const int lane_x = i % p.n_x, q = i / p.n_x;
@@ -105,6 +112,7 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
     rows = min(16 * MB, p.M - row0);
     brow0 = 0;
     ncol0 = c * SK_COLS;
+    ctile = c;
   }
   // this wave's 16 columns; a wave past N has an empty B range and stores nothing
   const int n0 = ncol0 + wave * 16;
@@ -118,8 +126,11 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
       sk_rsrc(p.B + (size_t)(brow0 + min(n0, p.N)) * p.ldb, (uint32_t)cols * p.ldb * 2u);
   const int lr = lane & 15, lk = (lane >> 4) * 8;
   const uint32_t vob = (uint32_t)(lr * p.ldb + lk) * 2u;
+  // this workgroup's k-steps of 32: all of K, or its range of a split K
   const int steps = (p.K + 31) >> 5;
-  const int stages = (steps + U - 1) / U;
+  const int per = (steps + p.ksplit - 1) / p.ksplit;
+  const int ks0 = min(steps, kr * per), ks1 = min(steps, ks0 + per);
+  const int stages = (ks1 - ks0 + U - 1) / U;
 
   // A staging: chunk c of a stage is (row, k-step u, quarter kq) in row-major
   // order; thread t carries chunks t, t + 256, ...
@@ -130,8 +141,9 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
     for (int e = 0; e < A_PER; ++e) {
       const int c = threadIdx.x + e * SK_THREADS;
       const int row = c / (U * 4), cc = c % (U * 4);
-      const int k = (st * U + (cc >> 2)) * 32 + (cc & 3) * 8;
-      const bool in = c < CHUNKS && k < p.K;
+      const int ks = ks0 + st * U + (cc >> 2);
+      const int k = ks * 32 + (cc & 3) * 8;
+      const bool in = c < CHUNKS && ks < ks1 && k < p.K;
       r[e] = __builtin_amdgcn_raw_buffer_load_b128(ra, in ? (uint32_t)(row * p.lda + k) * 2u : kSkOOB, 0, 0);
     }
   };
@@ -148,8 +160,9 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
   auto b_load = [&](int st, bf16x8 (&b)[U]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = (st * U + u) * 32;
-      const v4u x = __builtin_amdgcn_raw_buffer_load_b128(rb, k + lk < p.K ? vob : kSkOOB, k * 2, 0);
+      const int ks = ks0 + st * U + u;
+      const int k = ks * 32;
+      const v4u x = __builtin_amdgcn_raw_buffer_load_b128(rb, ks < ks1 && k + lk < p.K ? vob : kSkOOB, k * 2, 0);
       b[u] = __builtin_bit_cast(bf16x8, x);
     }
   };
@@ -196,9 +209,17 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
 
   // in a 16x16 block the lane with row r = lane % 16 holds columns 4c..4c+3,
   // c = lane / 16; rows past the tile fall outside the resource
+  const int nl = (lane >> 4) * 4;  // column inside the wave's 16
+  if (p.ksplit > 1) {
+    // split K: every range writes its fp32 tile; a second launch adds them
+    float* mine = p.part + ((size_t)ctile * p.ksplit + kr) * (16 * MB * 64);
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+      *reinterpret_cast<f32x4*>(mine + (i * 16 + lr) * 64 + wave * 16 + nl) = acc[i];
+    return;
+  }
   const __amdgpu_buffer_rsrc_t rc = sk_rsrc(p.C + (size_t)row0 * p.ldc, (uint32_t)rows * p.ldc * 2u);
   const bool vec_c = ((p.ldc & 3) == 0) && ((reinterpret_cast<uintptr_t>(p.C) & 7) == 0);
-  const int nl = (lane >> 4) * 4;  // column inside the wave's 16
 #pragma unroll
   for (int i = 0; i < MB; ++i) {
     const f32x4 v = acc[i];
@@ -218,6 +239,29 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
       }
     }
   }
+}
+
+// The sum of a split K: for each (column tile, row, 4 columns), the ranges'
+// partial tiles added in range order, rounded to bf16 and stored.  One thread
+// per 4 outputs.
+__global__ void __launch_bounds__(256) small_m_reduce(const float* __restrict__ part, int tiles_n, int ksplit,
+                                                      int tile_rows, int M, int N, uint16_t* __restrict__ C,
+                                                      int ldc) {
+  const long long id = (long long)blockIdx.x * 256 + threadIdx.x;
+  const long long per_tile = (long long)tile_rows * 16;   // 16 groups of 4 columns per row
+  if (id >= per_tile * tiles_n) return;
+  const int c = (int)(id / per_tile);
+  const int rem = (int)(id - (long long)c * per_tile);
+  const int m = rem / 16, q = rem % 16;
+  if (m >= M) return;
+  const float* src = part + (size_t)c * ksplit * tile_rows * 64 + m * 64 + 4 * q;
+  f32x4 v = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < ksplit; ++s) v += *reinterpret_cast<const f32x4*>(src + (size_t)s * tile_rows * 64);
+  const int n = c * SK_COLS + 4 * q;
+  uint16_t* dst = C + (size_t)m * ldc + n;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    if (n + r < N) dst[r] = __builtin_bit_cast(unsigned short, (__bf16)v[r]);
 }
 
 }  // namespace
@@ -245,6 +289,10 @@ int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s) {
   p.order = g.order;
   p.n_x = g.n_x;
   p.desc = static_cast<const int4*>(g.d_desc);
+  p.ksplit = g.ksplit;
+  p.part = g.part;
+  if (p.ksplit > 1 && (p.desc || p.row_tiles != 1 || !p.part))
+    return fail(ASYM_EINVAL, "small-M GEMM: a split K needs one row tile and a workspace");
   const long long grid = g.grid;
   if (grid < 1 || grid > (1ll << 31) - 1) return fail(ASYM_EINVAL, "small-M GEMM: grid out of range");
   switch (g.mb) {
@@ -262,6 +310,12 @@ int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s) {
       return fail(ASYM_EINVAL, "small-M GEMM: row blocks must be 1, 2 or 4");
   }
   ASYM_HIP(hipGetLastError());
+  if (p.ksplit > 1) {
+    const long long threads = (long long)p.tiles_n * 16 * g.mb * 16;
+    hipLaunchKernelGGL(small_m_reduce, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, g.part, p.tiles_n,
+                       p.ksplit, 16 * g.mb, g.M, g.N, static_cast<uint16_t*>(g.C), g.ldc);
+    ASYM_HIP(hipGetLastError());
+  }
   return ASYM_OK;
 }
 

@@ -99,6 +99,8 @@ struct SmallMLaunch {
   int n_x = 8;                  // XCDs
   long long grid = 0;           // workgroups
   const void* d_desc = nullptr; // grouped: device int4 per workgroup {row, rows, B row, column}
+  int ksplit = 1;               // plain, one row tile: K ranges per column tile
+  float* part = nullptr;        // ksplit > 1: [column tiles][ksplit][16 mb][64] fp32
 };
 int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s);
 int small_m_blocks(int max_rows);  // 1, 2, 4, or 0 above 64 rows

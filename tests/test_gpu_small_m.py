@@ -68,7 +68,9 @@ def test_plan_picks_the_kernel(dev):
     assert plan(32, K=4100)["small_m"] == 0                       # K not a multiple of 8
     assert plan(32, xcd_mask=0x0F)["small_m"] == 0                # whole-XCD restriction
     p = plan(32)
-    assert (p["tile_n"], p["tiles_n"], p["grid"], p["claims"]) == (64, 8, 8, 0)
+    # 8 column tiles on 256 CUs: K split into 8 ranges (128 k-steps, at least 16 per range)
+    assert (p["tile_n"], p["tiles_n"], p["k_splits"], p["grid"], p["claims"]) == (64, 8, 8, 64, 0)
+    assert plan(32, K=256)["k_splits"] == 1 and plan(65)["k_splits"] == 1
     assert plan(200, mapping="aware")["grid"] == 32 and plan(200, mapping="oblivious_grouped")["grid"] == 32
     prev = asym.set_small_m(False)
     try:
@@ -195,3 +197,35 @@ def test_grouped_groups_up_to_256_rows(dev):
     finally:
         asym.set_small_m(prev)
     assert np.array_equal(small, pers)
+
+
+@pytest.mark.parametrize("M,N,K", [(32, 4096, 4096), (16, 2000, 14336), (64, 1024, 8192), (5, 300, 1000)])
+def test_split_k_elementwise_and_repeatable(dev, M, N, K):
+    """Fewer column tiles than CUs: K is split across workgroups and a second
+    launch adds the partial tiles in range order.  Element by element against
+    the oracle; repeats and every mapping give the same bits."""
+    p = workloads.make_problem(M, N, K, seed=M + N, dist="llm")
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    plan = asym.gemm_plan(A=Ad, B=Bd)
+    assert plan["small_m"] == 1 and plan["k_splits"] > 1, plan
+    outs = [bits(asym.gemm(Ad, Bd, mapping=m)) for m in MAPS for _ in range(2)]
+    assert all(np.array_equal(outs[0], o) for o in outs[1:])
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    err = assert_gemm_close(outs[0], R, what=f"split K {M}x{N}x{K}")
+    print(f"{M}x{N}x{K}: {plan['k_splits']} K ranges, max rel err {err:.3e}")
+
+
+def test_split_k_exact_integer_equals_persistent(dev):
+    p = workloads.make_problem(32, 4096, 4096, seed=8, dist="int")
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    assert asym.gemm_plan(A=Ad, B=Bd)["k_splits"] > 1
+    small = bits(asym.gemm(Ad, Bd))
+    prev = asym.set_small_m(False)
+    try:
+        pers = bits(asym.gemm(Ad, Bd))
+    finally:
+        asym.set_small_m(prev)
+    _, Co = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    assert np.array_equal(small, Co) and np.array_equal(pers, Co)
