@@ -233,14 +233,16 @@ def prefill_decode(topo, dev, iters: int, halves):
     return out
 
 
-def spread_study(topo, dev, n_masks: int, iters: int, halves):
+def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gemm"):
     """GEMM 4096^3 (uniform[-1,1], seed 4) on 128-CU sets: n_masks seeded random
     choices of 128 mask bits (what a topology-oblivious allocator hands out) and
     the two whole-XCD halves (the measured affinity groups; each side lends the
     other one CU per XCD and works only on its own XCDs).  A second
     tenant, the same GEMM, runs on the complementary 128 CUs for the whole
-    measurement.  Per-set TFLOP/s of the measured GEMM for each mapping, and the
-    max/min spread over the random sets."""
+    measurement (tenant "gemm"), or the bandwidth-bound reader making 40 passes
+    of a 1 GiB buffer (tenant "read", longer than the GEMM).  Per-set TFLOP/s of
+    the measured GEMM for each mapping, and the max/min spread over the random
+    sets."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -249,28 +251,35 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves):
     Ad, Bd = A.to(dev), B.to(dev)
     C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
     C2 = torch.empty_like(C)
+    rbuf = torch.ones(256 << 20, dtype=torch.float32, device=dev) if tenant == "read" else None
     masks = workloads.random_mask_bits(workloads.COLOC.seed, n_masks, 128)
+
+    def other(cus, xm=0):
+        if tenant == "read":
+            return asym.read_task(rbuf, 40, mask=cus)
+        return asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=cus, xcd_mask=xm)
     per = {m: [] for m in MAPPINGS}
     counts = []
     for i, m in enumerate(masks):
         comp = [b for b in range(256) if b not in set(m)]
         counts.append(topo.cuset_counts(m))
         for mapping in MAPPINGS:
-            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m),
-                            asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=comp)], topo)
+            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m), other(comp)], topo)
             if i == 0 and not per[mapping]:
                 # the first set is run twice: its first run settles the clock
-                r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m),
-                                asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=comp)], topo)
+                r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m), other(comp)], topo)
             per[mapping].append(r[0]["tflops"])
     aligned = []
     for xm in halves:
         ma, mb = topo.cuset_split_xcds(xm)
-        r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
-                        asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=mb, xcd_mask=0xFF & ~xm)],
-                       topo)
+        if tenant == "read":
+            # the reader has no XCD filter: it runs on the other side's CUs only
+            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm), other(mb)], topo)
+        else:
+            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
+                            other(mb, 0xFF & ~xm)], topo)
         aligned.append(round(r[0]["tflops"], 2))
-    summ = {"n_random_sets": n_masks, "iters": iters, "aligned_aware_tflops": aligned,
+    summ = {"tenant": tenant, "n_random_sets": n_masks, "iters": iters, "aligned_aware_tflops": aligned,
             "random_set_min_max_cus_per_xcd": [min(min(c) for c in counts), max(max(c) for c in counts)]}
     for mapping, v in per.items():
         summ[f"random_{mapping}"] = {"min": round(min(v), 2), "max": round(max(v), 2),
@@ -674,6 +683,7 @@ def main() -> int:
         line["prefill_decode"] = prefill_decode(topo, dev, 10, halves)
     if "spread" in studies:
         line["cu_set_spread"] = spread_study(topo, dev, args.spread_masks, 20, halves)
+        line["cu_set_spread_read_tenant"] = spread_study(topo, dev, args.spread_masks, 20, halves, "read")
     if "grouped" in studies:
         line["grouped_gemm"] = grouped_study(dev, stream, range(1, 6), 8, 5)
     if "attention" in studies:

@@ -206,19 +206,30 @@ int asym_topology_info(const asym_topology* topo, int* n_cus, int* n_xcds,
 int asym_topology_cu(const asym_topology* topo, int cu_index, int* xcc,
                      int* se, int* sh, int* cu, int* mask_bit);
 
-/* Fraction of a full-grid probe launch whose workgroup b ran on XCC b mod
- * n_xccs (1.0 = round-robin dispatch).  Written by the IDENTITY probe. */
+/* Dispatch consistency of the IDENTITY probe's full-grid launch: the share of
+ * workgroups that ran on the XCC holding most of their residue class (block
+ * index mod n_xccs); 1.0 = every class on one XCC (round-robin dealing, up to
+ * which XCC the dealing starts on). */
 int asym_topology_dispatch(const asym_topology* topo, double* rr_fraction);
 
 /* Where launches land on a CU set: runs 4 x n_cus workgroups of the identity
  * kernel on a stream restricted to `mask` (CU-mask bits, ASYM_MASK_WORDS
  * words; NULL = every CU; the same rules as asym_stream_create) and reports
- * the fraction whose XCC is their block index mod the XCD count, and
- * (nullable, ASYM_MAX_XCDS ints) how many workgroups each XCD ran.  The aware
- * GEMM assumes that rule for locality only.  Synchronous.
+ * the share of workgroups on the XCC holding most of their residue class
+ * (block index mod the XCD count), and (nullable, ASYM_MAX_XCDS ints) how
+ * many workgroups each XCD ran.  The aware schedules assume each class stays
+ * on one XCD, for locality only.  Synchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_dispatch_check(const asym_topology* topo, const uint32_t* mask,
                         double* rr_fraction, int* blocks_per_xcd);
+
+/* The same probe, run right after a launch of pre_blocks workgroups on the
+ * same stream (0 = none), also reporting the rotation: the k for which
+ * workgroup b ran on XCC (b + k) mod n_xccs most often.  Shows whether the
+ * XCC that dealing starts on follows earlier launches.  Synchronous.
+ * Errors: as asym_dispatch_check. */
+int asym_dispatch_probe(const asym_topology* topo, const uint32_t* mask, int pre_blocks,
+                        double* class_fraction, int* rotation, int* blocks_per_xcd);
 
 /* Latency-probe results; ASYM_EUNSUPPORTED if the map was probed without LATENCY. */
 int asym_topology_latency(const asym_topology* topo, asym_latency_summary* out);
@@ -628,28 +639,32 @@ int asym_copy_bf16(void* dst, const void* src, size_t n_bytes, int passes,
 
 /* One task of a co-run: a GEMM or a streaming copy on its own CU set. */
 typedef struct asym_task {
-  int kind;        /* 0 = GEMM, 1 = streaming copy */
+  int kind;        /* 0 = GEMM, 1 = streaming copy, 2 = read (whole-buffer reader) */
   uint32_t mask[ASYM_MASK_WORDS]; /* CU-mask bits; all-zero = all CUs */
   uint32_t xcd_mask;              /* whole-XCD restriction, 0 = none */
-  int iters;       /* GEMM launches, or copy passes */
+  int iters;       /* GEMM launches, or copy / read passes (reads: >= 1) */
   int mapping;     /* GEMM mapping */
   int M, N, K;     /* GEMM shape, dense row-major A, B ([N][K]), C */
   const void* A; const void* B; void* C;
-  const void* src; void* dst; size_t n_bytes; /* copy */
+  const void* src; void* dst; size_t n_bytes; /* copy; read: src and n_bytes
+                                                 (a multiple of 16) */
 } asym_task;
 
 typedef struct asym_task_result {
   double ms_total;    /* first launch start to last launch end */
   double ms_per_iter;
   double tflops;      /* GEMM */
-  double gbps;        /* copy: bytes read + written per second / 1e9 */
+  double gbps;        /* copy: bytes read + written per second / 1e9; read: bytes read */
   int iters_done;
 } asym_task_result;
 
 /* Run tasks concurrently, each on its own stream (masked streams for partial
  * masks, unmasked streams with XCD filtering for whole-XCD sets).  All tasks
  * are released together; a copy task with iters <= 0 runs until every GEMM
- * task has finished (bounded at 100000 passes).  Synchronous.
+ * task has finished (bounded at 100000 passes).  A read task makes `iters`
+ * passes of a whole-buffer reader (256 workgroups per XCD, 16-byte loads,
+ * bounded, no atomics): the bandwidth-bound tenant of the co-location study.
+ * Synchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_corun(const asym_topology* topo, const asym_task* tasks, int n_tasks,
                asym_task_result* out);

@@ -54,6 +54,17 @@ def invariant_violations(cus, n_cus_device: int, n_xccs_device: int, bit_to_cu=N
 
 
 def round_robin_fraction(records, n_xccs: int) -> float:
+    """Share of records whose XCC (low 4 bits of the XCC_ID word) is the one
+    holding most records of their residue class, block index mod n_xccs.  The
+    dealing of workgroups to XCDs is round-robin by block index, but the XCD it
+    starts on can differ between launches; what the aware schedules need is
+    that each residue class sits on one XCD, which this measures."""
     recs = list(records)
-    agree = sum(1 for r in recs if (r[0] & 0xF) == r[2] % n_xccs)
-    return agree / len(recs)
+    counts = {}
+    for r in recs:
+        key = (r[2] % n_xccs, r[0] & 0xF)
+        counts[key] = counts.get(key, 0) + 1
+    best = {}
+    for (cls, x), c in counts.items():
+        best[cls] = max(best.get(cls, 0), c)
+    return sum(best.values()) / len(recs)

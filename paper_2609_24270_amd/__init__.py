@@ -38,7 +38,7 @@ EXPORTS = (
     "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
     "asym_interleave_params_default", "asym_interleave_probe", "asym_interleave_analyze",
     "asym_home_map", "asym_home_map_analyze", "asym_chunk_lists", "asym_chunk_read_bw",
-    "asym_dispatch_check", "asym_cuset_split_xcds",
+    "asym_dispatch_check", "asym_dispatch_probe", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
     "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_plan", "asym_gemm_set_small_m",
@@ -207,6 +207,7 @@ def load_library(path: str = LIB_PATH):
         "asym_topology_latency": (i, [topo_p, ctypes.POINTER(LatencySummary)]),
         "asym_latency_params_default": (None, [ctypes.POINTER(LatencyParams)]),
         "asym_dispatch_check": (i, [topo_p, u32p, ctypes.POINTER(ctypes.c_double), ip]),
+        "asym_dispatch_probe": (i, [topo_p, u32p, i, ctypes.POINTER(ctypes.c_double), ip, ip]),
         "asym_cuset_split_xcds": (i, [topo_p, u32, u32p, u32p]),
         "asym_latency_probe": (i, [i, ctypes.POINTER(LatencyParams), u32p, ctypes.POINTER(LatencySummary)]),
         "asym_latency_analyze": (i, [u32p, i, i, ctypes.c_double, ctypes.c_double,
@@ -342,12 +343,22 @@ class Topology:
         return json.loads(buf.value.decode())
 
     def dispatch_check(self, mask: Optional[Sequence[int]] = None):
-        """(fraction of workgroups on XCC block mod n, workgroups per XCD) for a
-        launch on the CU set `mask` (None = all CUs)."""
+        """(share of workgroups on their residue class's XCC, workgroups per XCD)
+        for a launch on the CU set `mask` (None = all CUs)."""
         rr = ctypes.c_double()
         per = (ctypes.c_int * MAX_XCDS)()
         _check(load_library().asym_dispatch_check(self._h, mask_words(mask), ctypes.byref(rr), per))
         return rr.value, list(per)[: self.info()["n_xcds"]]
+
+    def dispatch_probe(self, pre_blocks: int = 0, mask: Optional[Sequence[int]] = None):
+        """(class share, rotation, workgroups per XCD) of a launch right after a
+        launch of pre_blocks workgroups on the same stream."""
+        cf = ctypes.c_double()
+        rot = ctypes.c_int()
+        per = (ctypes.c_int * MAX_XCDS)()
+        _check(load_library().asym_dispatch_probe(self._h, mask_words(mask), pre_blocks, ctypes.byref(cf),
+                                                  ctypes.byref(rot), per))
+        return cf.value, rot.value, list(per)[: self.info()["n_xcds"]]
 
     def cuset(self, n_cus: int, policy: int, seed: int = 0, exclude: Optional[Sequence[int]] = None) -> list:
         out = (ctypes.c_uint32 * MASK_WORDS)()
@@ -786,6 +797,21 @@ def copy_task(dst, src, passes: int = 0, mask=None, xcd_mask: int = 0) -> Task:
     t.xcd_mask = xcd_mask
     t.iters = passes
     t.src, t.dst = src.data_ptr(), dst.data_ptr()
+    t.n_bytes = src.numel() * src.element_size()
+    return t
+
+
+def read_task(src, passes: int, mask=None, xcd_mask: int = 0) -> Task:
+    """A bandwidth-bound co-runner: `passes` whole reads of the CUDA tensor src."""
+    t = Task()
+    t.kind = 2
+    if mask is not None:
+        m = mask_words(mask)
+        for w in range(MASK_WORDS):
+            t.mask[w] = m[w]
+    t.xcd_mask = xcd_mask
+    t.iters = passes
+    t.src = src.data_ptr()
     t.n_bytes = src.numel() * src.element_size()
     return t
 

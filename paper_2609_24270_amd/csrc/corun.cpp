@@ -5,7 +5,9 @@
 // with the kernels' own XCD filter when it names whole XCDs.  Tasks are
 // enqueued back to back and timed with events on their own streams; a copy
 // task with iters <= 0 keeps streaming until a device flag, raised on the
-// GEMM streams after their last launch, stops it.
+// GEMM streams after their last launch, stops it.  A read task is the
+// bandwidth-bound co-runner that stays available while the copy kernel is
+// switched off: a fixed number of passes of a whole-buffer reader.
 #include <hip/hip_runtime.h>
 
 #include <cstring>
@@ -25,14 +27,16 @@ using asym::fail;
 
 namespace {
 
-struct Guard {  // releases streams, events and the flag on every exit path
+struct Guard {  // releases streams, events, the flag and sinks on every exit path
   std::vector<hipStream_t> streams;
   std::vector<hipEvent_t> events;
+  std::vector<void*> sinks;
   int* flag = nullptr;
   ~Guard() {
     for (hipStream_t s : streams) hipStreamSynchronize(s);
     for (hipEvent_t e : events) hipEventDestroy(e);
     for (hipStream_t s : streams) asym_stream_destroy(s);
+    for (void* p : sinks) hipFree(p);
     if (flag) hipFree(flag);
   }
 };
@@ -58,6 +62,10 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
       ++n_gemm;
     } else if (t.kind == 1) {
       if (!t.src || !t.dst || t.n_bytes == 0) return fail(ASYM_EINVAL, "corun: bad copy task");
+    } else if (t.kind == 2) {
+      if (!t.src || t.n_bytes < 16 || t.n_bytes % 16 || t.iters < 1)
+        return fail(ASYM_EINVAL, "corun: a read task needs a source of a multiple of 16 bytes and iters >= 1");
+      if (t.xcd_mask) return fail(ASYM_EUNSUPPORTED, "corun: a read task runs on a CU mask, not an XCD filter");
     } else {
       return fail(ASYM_EINVAL, "corun: unknown task kind");
     }
@@ -74,6 +82,16 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
     ASYM_HIP(hipMalloc(&g.flag, sizeof(int)));
     ASYM_HIP(hipMemset(g.flag, 0, sizeof(int)));
   }
+  int n_x = 0, dev = 0;
+  ASYM_HIP(hipGetDevice(&dev));
+  ASYM_HIP(hipDeviceGetAttribute(&n_x, hipDeviceAttributeNumberOfXccs, dev));
+  const int read_grid = asym::stream_read_grid(n_x);
+  std::vector<void*> sink(n_tasks, nullptr);
+  for (int i = 0; i < n_tasks; ++i)
+    if (tasks[i].kind == 2) {
+      ASYM_HIP(hipMalloc(&sink[i], (size_t)read_grid * 256 * 16));
+      g.sinks.push_back(sink[i]);
+    }
   std::vector<hipEvent_t> ev0(n_tasks), ev1(n_tasks);
   for (int i = 0; i < n_tasks; ++i) {
     ASYM_HIP(hipEventCreate(&ev0[i]));
@@ -83,15 +101,18 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
   }
   ASYM_HIP(hipDeviceSynchronize());
 
-  // copies first, so they are streaming when the GEMMs start
+  // copies and reads first, so they are streaming when the GEMMs start
   std::vector<unsigned long long*> copy_ctr(n_tasks, nullptr);
   for (int pass = 0; pass < 2; ++pass) {
     for (int i = 0; i < n_tasks; ++i) {
       const asym_task& t = tasks[i];
-      if ((pass == 0) != (t.kind == 1)) continue;
+      if ((pass == 0) != (t.kind != 0)) continue;
       hipStream_t s = g.streams[i];
       ASYM_HIP(hipEventRecord(ev0[i], s));
-      if (t.kind == 1) {
+      if (t.kind == 2) {
+        int rc = asym::launch_stream_read(t.src, t.n_bytes, t.iters, sink[i], read_grid, s);
+        if (rc != ASYM_OK) return rc;
+      } else if (t.kind == 1) {
         const int passes = t.iters > 0 ? t.iters : 100000;
         int rc = asym_copy_bf16(t.dst, t.src, t.n_bytes, passes, t.iters > 0 ? nullptr : g.flag,
                                 t.xcd_mask, s);
@@ -128,6 +149,10 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
       r.iters_done = t.iters;
       r.ms_per_iter = ms / t.iters;
       r.tflops = 2.0 * t.M * t.N * (double)t.K * t.iters / (ms * 1e-3) / 1e12;
+    } else if (t.kind == 2) {
+      r.iters_done = t.iters;
+      r.ms_per_iter = ms / t.iters;
+      r.gbps = (double)t.n_bytes * t.iters / (ms * 1e-3) / 1e9;
     }
   }
   // bytes moved by each copy: read back and clear the stream's byte counter

@@ -121,7 +121,11 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s);
 int attn_tasks_per_workgroup();
 
 int probe_identity_run(int device, hipStream_t s, int n_blocks,
-                       std::vector<int32_t>& rec);
+                       std::vector<int32_t>& rec, int pre_blocks = 0);
+// Dispatch of n workgroups (block index block[i] ran on XCC xcc[i]): the share
+// of workgroups on the XCC holding most of their residue class (block mod n_x),
+// and the rotation k for which xcc = (block + k) mod n_x fits most (host only).
+void dispatch_stats(const int* block, const int* xcc, int n, int n_x, double* class_fraction, int* rotation);
 int probe_latency_run(int device, Topology& t);
 int latency_probe(int device, const asym_latency_params& p, uint32_t* lat_out,
                   asym_latency_summary& out);
@@ -157,6 +161,11 @@ int analyze_latency(const uint32_t* lat, int n_x, int n_s, double threshold, dou
 int analyze_interleave(const uint32_t* L, int n_x, int n_a, const uint64_t* offs, int block,
                        double threshold, double tie, double decide, int8_t* home_out,
                        asym_interleave_result& r);
+
+// Bandwidth-bound co-runner: `passes` reads of a whole buffer (sink: grid x
+// 256 x 16 bytes).
+int stream_read_grid(int n_x);
+int launch_stream_read(const void* src, size_t n_bytes, int passes, void* sink, int grid, hipStream_t s);
 
 int launch_copy(void* dst, const void* src, size_t n_bytes, int passes,
                 const int* stop_flag, uint32_t xcd_mask, int grid,

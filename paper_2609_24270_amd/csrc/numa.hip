@@ -47,6 +47,18 @@ chunk_read_kernel(const char* __restrict__ base, int chunk_log2, const uint32_t*
   sink[(size_t)b * kReadThreads + threadIdx.x] = acc;
 }
 
+// Whole-buffer reader for a bandwidth-bound co-runner: `passes` passes over
+// n16 16-byte words, workgroup b taking words b * 256 + t, then a grid-wide
+// stride; bounded by the pass count, no atomics or barriers.
+__global__ void __launch_bounds__(kReadThreads)
+stream_read_kernel(const v4u* __restrict__ src, size_t n16, int passes, v4u* __restrict__ sink) {
+  v4u acc = {0u, 0u, 0u, 0u};
+  const size_t stride = (size_t)gridDim.x * kReadThreads;
+  for (int pass = 0; pass < passes; ++pass)
+    for (size_t i = (size_t)blockIdx.x * kReadThreads + threadIdx.x; i < n16; i += stride) acc ^= src[i];
+  sink[(size_t)blockIdx.x * kReadThreads + threadIdx.x] = acc;
+}
+
 uint64_t mix64(uint64_t& s) {
   uint64_t z = (s += 0x9E3779B97F4A7C15ull);
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -285,6 +297,17 @@ int chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uint32_t
     for (const v4u& v : h) acc ^= v;
     for (int w = 0; w < 4; ++w) checksum[w] = acc[w];
   }
+  return ASYM_OK;
+}
+
+int stream_read_grid(int n_x) { return n_x * kReadWorkersPerXcd; }
+
+int launch_stream_read(const void* src, size_t n_bytes, int passes, void* sink, int grid, hipStream_t s) {
+  if (!src || !sink || n_bytes < 16 || n_bytes % 16 || passes < 1 || grid < 1)
+    return fail(ASYM_EINVAL, "stream read: bad arguments");
+  hipLaunchKernelGGL(stream_read_kernel, dim3(grid), dim3(kReadThreads), 0, s, static_cast<const v4u*>(src),
+                     n_bytes / 16, passes, static_cast<v4u*>(sink));
+  ASYM_HIP(hipGetLastError());
   return ASYM_OK;
 }
 

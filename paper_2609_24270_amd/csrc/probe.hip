@@ -49,20 +49,26 @@ __global__ void __launch_bounds__(64) probe_identity_kernel(int32_t* rec, long s
 
 }  // namespace
 
-int probe_identity_run(int device, hipStream_t s, int n_blocks, std::vector<int32_t>& rec) {
+int probe_identity_run(int device, hipStream_t s, int n_blocks, std::vector<int32_t>& rec, int pre_blocks) {
   (void)device;
-  if (n_blocks < 1) return fail(ASYM_EINVAL, "probe: no blocks");
+  if (n_blocks < 1 || pre_blocks < 0) return fail(ASYM_EINVAL, "probe: no blocks");
   int32_t* d = nullptr;
-  const size_t bytes = sizeof(int32_t) * 4 * (size_t)n_blocks;
+  const size_t bytes = sizeof(int32_t) * 4 * (size_t)(n_blocks + pre_blocks);
   ASYM_HIP(hipMalloc(&d, bytes));
   hipError_t e = hipMemsetAsync(d, 0xFF, bytes, s);
+  if (e == hipSuccess && pre_blocks > 0) {
+    // a launch of pre_blocks workgroups right before the probed one, on the same stream
+    hipLaunchKernelGGL(probe_identity_kernel, dim3(pre_blocks), dim3(64), kProbeLds, s, d + 4 * (size_t)n_blocks,
+                       20000L);
+    e = hipGetLastError();
+  }
   if (e == hipSuccess) {
     hipLaunchKernelGGL(probe_identity_kernel, dim3(n_blocks), dim3(64), kProbeLds, s, d, 20000L);
     e = hipGetLastError();
   }
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   rec.assign(4 * (size_t)n_blocks, -1);
-  if (e == hipSuccess) e = hipMemcpy(rec.data(), d, bytes, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(rec.data(), d, sizeof(int32_t) * 4 * (size_t)n_blocks, hipMemcpyDeviceToHost);
   hipFree(d);
   if (e != hipSuccess) return hip_fail(e, "identity probe");
   for (int i = 0; i < n_blocks; ++i)
@@ -164,16 +170,19 @@ extern "C" int asym_probe_topology(int device, unsigned flags, asym_topology** o
 }
 
 // Where a launch on a CU set lands: the identity kernel is run on a stream
-// restricted to `mask` (NULL = every CU) and each workgroup's XCC is compared
-// with its block index mod the XCD count.  The aware GEMM relies on that rule
-// only for locality (its tile assignment covers every tile whatever the
-// placement), so this is the check of a performance assumption, not of
-// correctness.
-extern "C" int asym_dispatch_check(const asym_topology* topo, const uint32_t* mask,
-                                   double* rr_fraction, int* blocks_per_xcd) {
+// restricted to `mask` (NULL = every CU), optionally right after a launch of
+// pre_blocks workgroups, and each workgroup's XCC is compared with its block
+// index mod the XCD count.  The measure is per residue class: the share of
+// workgroups that sit on the XCD holding most of their class (block index mod
+// n), and the rotation k for which XCC = (b + k) mod n fits most workgroups.
+// The aware schedules need each class on one XCD; which XCD a class lands on
+// (the rotation) matters only where XCDs differ in CU count.  All of this is a
+// performance assumption: no kernel's correctness depends on it.
+static int dispatch_run(const asym_topology* topo, const uint32_t* mask, int pre_blocks, double* class_fraction,
+                        int* rotation, int* blocks_per_xcd) {
   using namespace asym;
   const Topology* t = unwrap(topo);
-  if (!t || !rr_fraction) return fail(ASYM_EINVAL, "dispatch check: null argument");
+  if (!t || !class_fraction || !rotation) return fail(ASYM_EINVAL, "dispatch check: null argument");
   int device = 0;
   ASYM_HIP(hipGetDevice(&device));
   if (t->device >= 0 && t->device != device)
@@ -184,18 +193,31 @@ extern "C" int asym_dispatch_check(const asym_topology* topo, const uint32_t* ma
   hipStream_t s = static_cast<hipStream_t>(sv);
   const int n_blocks = 4 * t->n_cus;
   std::vector<int32_t> rec;
-  rc = probe_identity_run(device, s, n_blocks, rec);
+  rc = probe_identity_run(device, s, n_blocks, rec, pre_blocks);
   asym_stream_destroy(sv);
   if (rc != ASYM_OK) return rc;
-  std::vector<int> per(ASYM_MAX_XCDS, 0);
-  int agree = 0;
+  std::vector<int> per(ASYM_MAX_XCDS, 0), xs(n_blocks), blk(n_blocks);
   for (int b = 0; b < n_blocks; ++b) {
-    const int x = xccid((uint32_t)rec[4 * b]);
-    if (x < ASYM_MAX_XCDS) per[x] += 1;
-    if (x == b % t->n_xccs) ++agree;
+    blk[b] = b;
+    xs[b] = xccid((uint32_t)rec[4 * b]);
+    if (xs[b] < ASYM_MAX_XCDS) per[xs[b]] += 1;
   }
-  *rr_fraction = (double)agree / n_blocks;
+  dispatch_stats(blk.data(), xs.data(), n_blocks, t->n_xccs, class_fraction, rotation);
   if (blocks_per_xcd)
     for (int x = 0; x < ASYM_MAX_XCDS; ++x) blocks_per_xcd[x] = per[x];
   return ASYM_OK;
+}
+
+extern "C" int asym_dispatch_check(const asym_topology* topo, const uint32_t* mask,
+                                   double* rr_fraction, int* blocks_per_xcd) {
+  if (!rr_fraction) return asym::fail(ASYM_EINVAL, "dispatch check: null argument");
+  int rot = 0;
+  return dispatch_run(topo, mask, 0, rr_fraction, &rot, blocks_per_xcd);
+}
+
+extern "C" int asym_dispatch_probe(const asym_topology* topo, const uint32_t* mask, int pre_blocks,
+                                   double* class_fraction, int* rotation, int* blocks_per_xcd) {
+  if (!class_fraction || !rotation || pre_blocks < 0 || pre_blocks > (1 << 20))
+    return asym::fail(ASYM_EINVAL, "dispatch probe: bad argument");
+  return dispatch_run(topo, mask, pre_blocks, class_fraction, rotation, blocks_per_xcd);
 }

@@ -68,11 +68,17 @@ int build_topology(const int32_t* rec, int n, int n_cus_expected,
       t.cus[cu].mask_bit = b;
     }
   }
-  // dispatch agreement with round-robin: block b on XCC b mod n_xccs
-  int agree = 0;
-  for (int i = 0; i < n; ++i)
-    if (xccid((uint32_t)rec[4 * i]) == (rec[4 * i + 2] % n_xccs_expected)) ++agree;
-  t.rr_fraction = (double)agree / n;
+  // dispatch: how consistently each residue class of block indices (mod the
+  // XCD count) sits on one XCD
+  {
+    std::vector<int> blk(n), xs(n);
+    for (int i = 0; i < n; ++i) {
+      blk[i] = rec[4 * i + 2];
+      xs[i] = xccid((uint32_t)rec[4 * i]);
+    }
+    int rot = 0;
+    dispatch_stats(blk.data(), xs.data(), n, n_xccs_expected, &t.rr_fraction, &rot);
+  }
   // invariants against the device's own counts
   if (t.n_cus != n_cus_expected)
     return fail(ASYM_EINVARIANT, "topology: found " + std::to_string(t.n_cus) +
@@ -266,6 +272,26 @@ static std::string topology_json(const Topology& t) {
   }
   s += "}";
   return s;
+}
+
+void dispatch_stats(const int* block, const int* xcc, int n, int n_x, double* class_fraction, int* rotation) {
+  if (n < 1 || n_x < 1) {
+    *class_fraction = 0.0;
+    *rotation = 0;
+    return;
+  }
+  std::vector<std::vector<int>> cnt(n_x, std::vector<int>(ASYM_MAX_XCDS, 0));
+  std::vector<int> rot(n_x, 0);
+  for (int i = 0; i < n; ++i) {
+    const int x = xcc[i], b = block[i];
+    if (x < 0 || x >= ASYM_MAX_XCDS || b < 0) continue;
+    cnt[b % n_x][x] += 1;
+    if (x < n_x) rot[((x - b % n_x) % n_x + n_x) % n_x] += 1;
+  }
+  int best = 0;
+  for (int r = 0; r < n_x; ++r) best += *std::max_element(cnt[r].begin(), cnt[r].end());
+  *class_fraction = (double)best / n;
+  *rotation = (int)(std::max_element(rot.begin(), rot.end()) - rot.begin());
 }
 
 }  // namespace asym

@@ -61,9 +61,12 @@ def test_maskmap_probe(dev, topo):
 
 
 def test_dispatch_rule_on_cu_sets(dev, topo):
-    """Launches are dealt to XCDs round-robin by block index on the whole chip;
-    the same check on a random 128-CU set and on a striped set reports where
-    masked launches land (the aware GEMM relies on the rule for locality only)."""
+    """Launches are dealt to XCDs round-robin by block index on the whole chip
+    (every residue class of block indices on one XCD); the same check on a
+    random 128-CU set and on a striped set reports where masked launches land
+    (the aware schedules rely on the rule for locality only).  The XCD that
+    dealing starts on is reported for launches that follow launches of 0 to 13
+    workgroups."""
     n = asym.device_query(0)["n_cus"]
     rr, per = topo.dispatch_check(None)
     print("full", rr, per)
@@ -73,6 +76,12 @@ def test_dispatch_rule_on_cu_sets(dev, topo):
         rr, per = topo.dispatch_check(m)
         print(name, rr, per, topo.cuset_counts(m))
         assert 0.0 <= rr <= 1.0 and sum(per) == 4 * n
+    rots = {}
+    for pre in (0, 1, 3, 8, 13):
+        cf, rot, per = topo.dispatch_probe(pre)
+        rots[pre] = (round(cf, 4), rot)
+        assert cf == 1.0 and sum(per) == 4 * n
+    print("after a launch of k workgroups: (class share, rotation)", rots)
 
 
 def test_masked_gemm_bitwise(dev, topo):
@@ -180,3 +189,27 @@ def test_corun_prefill_decode(dev, topo):
                       asym.gemm_task(da, db, cd, 20, "aware", mask=dm, xcd_mask=0xC0)], topo)
     print("xcd-aligned", res)
     assert torch.equal(cp, ref_p) and torch.equal(cd, ref_d)
+
+
+def test_corun_gemm_with_read_tenant(dev, topo):
+    """A GEMM on a seeded random 128-CU set with the bandwidth-bound reader on
+    the complementary CUs: the GEMM's bits equal the GEMM run alone for every
+    mapping, the reader reports its passes and rate; a read task with no
+    passes, or with an XCD filter, is refused."""
+    A, B = workloads.make_inputs(workloads.COLOC)
+    Ad, Bd = A.to(dev), B.to(dev)
+    ref = asym.gemm(Ad, Bd)
+    torch.cuda.synchronize()
+    C = torch.empty_like(ref)
+    buf = torch.ones(256 << 20, dtype=torch.float32, device=dev)   # 1 GiB
+    mask = workloads.random_mask_bits(4, 1, 128)[0]
+    comp = [b for b in range(256) if b not in set(mask)]
+    for m in ("aware", "oblivious_grouped", "oblivious_rowmajor"):
+        res = asym.corun([asym.gemm_task(Ad, Bd, C, 5, m, mask=mask), asym.read_task(buf, 4, mask=comp)], topo)
+        print(m, res)
+        assert torch.equal(C, ref), m
+        assert res[1]["iters_done"] == 4 and res[1]["gbps"] > 100
+    with pytest.raises(asym.AsymError):
+        asym.corun([asym.gemm_task(Ad, Bd, C, 1, "aware", mask=mask), asym.read_task(buf, 0, mask=comp)], topo)
+    with pytest.raises(asym.AsymError):
+        asym.corun([asym.gemm_task(Ad, Bd, C, 1, "aware"), asym.read_task(buf, 1, xcd_mask=0x0F)], topo)

@@ -367,3 +367,21 @@ def test_grouped_schedule_rejects_bad_input(lib):
         asym.grouped_schedule_build([1, 1], 0, [32] * 8, asym.MAP_AWARE)
     with pytest.raises(asym.AsymError):
         asym.grouped_schedule_build([1, 1], 4, [0] * 8, asym.MAP_AWARE)
+
+
+def test_dispatch_share_counts_classes_not_the_start():
+    """The dispatch share is per residue class of block indices: dealing that
+    starts on another XCD (a rotation) still puts each class on one XCD and
+    scores 1; a class split over two XCDs scores the larger half.  Oracle and
+    library agree on both."""
+    lay = uniform_layout()
+    recs = fake_records(lay)
+    rotated = [[((r[0] & 0xF) + 3) % 8 | (r[0] & ~0xF), r[1], r[2], r[3]] for r in recs]
+    assert otopo.round_robin_fraction(rotated, 8) == 1.0
+    # the XCC field no longer matches the layout's CU records, so only the share is compared
+    split = [list(r) for r in recs]
+    cls0 = [r for r in split if r[2] % 8 == 0]
+    for r in cls0[: len(cls0) // 4]:
+        r[0] = (r[0] & ~0xF) | 1          # a quarter of class 0 moved to XCC 1
+    want = 1.0 - (len(cls0) // 4) / len(split)
+    assert abs(otopo.round_robin_fraction(split, 8) - want) < 1e-12
