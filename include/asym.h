@@ -600,9 +600,10 @@ int asym_gemm_set_small_m(int enable);
  * and V are read once.  A second launch merges the splits of each (request,
  * head) in split order.  Mapping: AWARE gives each XCD a share of the tasks
  * proportional to its CU count in the stream's CU set (and honours a
- * whole-XCD restriction); the oblivious mappings (both) hand out tasks
- * round-robin by workgroup, an equal share per XCD.  Every mapping gives the
- * same bits.  fp32 partials live in a per-stream library workspace, grown
+ * whole-XCD restriction); its workgroups read the XCD they run on and claim
+ * groups of 4 tasks from that XCD's share, then from the others; the
+ * oblivious mappings (both) hand out tasks round-robin by workgroup, an equal
+ * share per XCD.  Every mapping gives the same bits.  fp32 partials live in a per-stream library workspace, grown
  * (after a stream synchronisation) when a call needs more.  Asynchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_attn_decode_bf16(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,

@@ -22,11 +22,14 @@
 //
 // Assignment.  A task's bytes are read by exactly one wave, so there is no
 // cache reuse for a placement to exploit; what the topology decides is how
-// many tasks each XCD gets.  Workgroup i runs on XCD i mod n (round-robin
-// dispatch).  Oblivious: tasks 4i .. 4i+3 go to workgroup i, every XCD gets
-// the same share whatever its CU count.  Aware: each XCD's share of the task
-// list is proportional to its CU count in the stream's CU set, and XCD x's
-// workgroups i = x, x + n, ... take consecutive groups of 4 of its share.
+// many tasks each XCD gets.  Oblivious: tasks 4i .. 4i+3 go to workgroup i;
+// the hardware deals workgroups to XCDs round-robin, so every XCD gets the
+// same share whatever its CU count.  Aware: each XCD's share of the task list
+// is proportional to its CU count in the stream's CU set; a workgroup reads
+// the XCD it runs on (XCC_ID) and claims groups of 4 tasks of that XCD's share
+// from a counter, then of the other shares, until none are left (which XCD a
+// block index is dealt to is not fixed: the starting XCD differs between
+// streams, so claims, not block indices, decide).
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -37,6 +40,7 @@ namespace {
 constexpr int AD = 128;            // head dimension
 constexpr int AT_WAVES = 4;        // tasks per workgroup, one per wave
 constexpr uint32_t kAtOOB = 0x80000000u;
+constexpr int kClaimStride = 64;   // ints between claim counters: one 256-byte line each
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -49,6 +53,8 @@ struct AttnParams {
   float* part_o;       // [B][Hq][n_splits][128]
   float* part_ml;      // [B][Hq][n_splits][2]: max, sum
   const int* quota_off;  // aware: [n_x + 1] start of each XCD's share (tasks), null = oblivious
+  int* claim;            // aware: groups of 4 claimed from share y at claim[y * kClaimStride] (zero at launch)
+  uint32_t allow;        // aware: XCDs whose workgroups may work (the others leave)
   int B, Hq, Hkv, S, split, n_splits, tasks, n_x;
   float scale;
 };
@@ -210,25 +216,70 @@ __device__ void attn_task(const AttnParams& p, int task, float* __restrict__ sp)
 template <int G>
 __global__ void __launch_bounds__(64 * AT_WAVES) attn_decode_split(AttnParams p) {
   __shared__ float sp_all[AT_WAVES][256 + 16];
+  __shared__ int box[2];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  int task;
-  if (p.quota_off) {
-    const int x = blockIdx.x % p.n_x, j = blockIdx.x / p.n_x;
-    const int begin = p.quota_off[x], end = p.quota_off[x + 1];
-    task = begin + j * AT_WAVES + wave;
-    if (task >= end) return;
-  } else {
-    task = blockIdx.x * AT_WAVES + wave;
-    if (task >= p.tasks) return;
+  if (!p.quota_off) {
+    const int task = blockIdx.x * AT_WAVES + wave;
+    if (task < p.tasks) attn_task<G>(p, task, sp_all[wave]);
+    return;
   }
-  attn_task<G>(p, task, sp_all[wave]);
+  uint32_t xr;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xr));
+  const int own = (int)(xr & 0xFu);
+  if (own >= p.n_x || !((p.allow >> own) & 1u)) return;  // an XCD outside the set
+  // claims: own share first, then the others in turn.  Wave 0 reads every
+  // counter in one round trip and only adds to shares that still have groups;
+  // the loop ends when each counter has passed its share.
+  const int lane = threadIdx.x & 63;
+  for (;;) {
+    if (wave == 0) {
+      int rem = 0, y = 0, b0 = 0, b1 = 0;
+      if (lane < p.n_x) {
+        y = (own + lane) % p.n_x;
+        b0 = p.quota_off[y];
+        b1 = p.quota_off[y + 1];
+        const int taken = __hip_atomic_load(&p.claim[y * kClaimStride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        rem = (b1 - b0 + AT_WAVES - 1) / AT_WAVES - taken;
+      }
+      unsigned long long open = __ballot(lane < p.n_x && rem > 0);
+      int base = -1, end = 0;
+      while (open && base < 0) {
+        const int l = __builtin_ctzll(open);
+        open &= open - 1;
+        int got = -1;
+        if (lane == l) {
+          const int g = atomicAdd(&p.claim[y * kClaimStride], 1);
+          if (b0 + g * AT_WAVES < b1) got = b0 + g * AT_WAVES;
+        }
+        got = __shfl(got, l);
+        if (got >= 0) {
+          base = got;
+          end = __shfl(b1, l);
+        }
+      }
+      if (lane == 0) {
+        box[0] = base;
+        box[1] = end;
+      }
+    }
+    __syncthreads();
+    const int base = box[0], end = box[1];
+    __syncthreads();
+    if (base < 0) break;
+    if (base + wave < end) attn_task<G>(p, base + wave, sp_all[wave]);
+  }
 }
 
+
+
 // Merge of the splits of one (request, head) per wave, in split order.
+// It also clears the aware form's claim counters for the next split launch on
+// the stream (the split launch is complete when the merge runs).
 __global__ void __launch_bounds__(256) attn_decode_merge(const float* __restrict__ part_o,
                                                          const float* __restrict__ part_ml, int rows,
                                                          int n_splits, uint16_t* __restrict__ o,
-                                                         float* __restrict__ lse) {
+                                                         float* __restrict__ lse, int* claim, int n_claim) {
+  if (claim && blockIdx.x == 0 && (int)threadIdx.x < n_claim) claim[threadIdx.x * kClaimStride] = 0;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const int lane = threadIdx.x & 63;
@@ -261,6 +312,8 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
   p.part_o = a.part_o;
   p.part_ml = a.part_ml;
   p.quota_off = a.d_quota_off;
+  p.claim = a.d_claim;
+  p.allow = a.allow;
   p.B = a.B;
   p.Hq = a.Hq;
   p.Hkv = a.Hkv;
@@ -272,6 +325,8 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
   p.scale = a.scale;
   const int G = a.Hq / a.Hkv;
   const dim3 grid((unsigned)a.grid), block(64 * AT_WAVES);
+  if (a.d_quota_off && (!a.d_claim || a.n_x > 64))
+    return fail(ASYM_EINVAL, "attention: aware launch without claim counters");
   switch (G) {
     case 1: hipLaunchKernelGGL(attn_decode_split<1>, grid, block, 0, s, p); break;
     case 2: hipLaunchKernelGGL(attn_decode_split<2>, grid, block, 0, s, p); break;
@@ -283,11 +338,14 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
   ASYM_HIP(hipGetLastError());
   const int rows = a.B * a.Hq;
   hipLaunchKernelGGL(attn_decode_merge, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a.part_o, a.part_ml,
-                     rows, a.n_splits, static_cast<uint16_t*>(a.o), a.lse);
+                     rows, a.n_splits, static_cast<uint16_t*>(a.o), a.lse, a.d_quota_off ? a.d_claim : nullptr,
+                     a.n_x);
   ASYM_HIP(hipGetLastError());
   return ASYM_OK;
 }
 
 int attn_tasks_per_workgroup() { return AT_WAVES; }
+
+int attn_claim_ints() { return ASYM_MAX_XCDS * kClaimStride; }
 
 }  // namespace asym

@@ -85,6 +85,7 @@ struct Workspace {
   // offsets of recent aware plans (key: tasks, per-XCD slots), most recent first
   float* attn_buf = nullptr;
   size_t attn_bytes = 0;
+  int* attn_claim = nullptr;  // claim counters of the aware form, one 256-byte line each
   // small-M GEMM with a split K: fp32 partial tiles (grown on demand)
   float* sm_part = nullptr;
   size_t sm_part_bytes = 0;
@@ -369,6 +370,12 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   P->dynamic = false;
   for (int x = 0; x < t->n_xccs; ++x)
     if (per[x] < smax) P->dynamic = true;
+  // A whole-XCD restriction also takes claims: the static form's workers of
+  // XCD x are the workgroups with block index x mod n, which the hardware
+  // deals to one XCD but not always to XCD x (the XCD that dealing starts on
+  // differs between streams), so the static form could run the work on an
+  // XCD outside the set; claims read XCC_ID.
+  if (!cs.whole) P->dynamic = true;
   P->whole = cs.whole;
   P->per = std::move(per);
   P->slots = std::move(slots);
@@ -654,9 +661,12 @@ static int attn_plan(const asym_topology* topo_in, int B, int Hq, int Hkv, int S
   const int n_x = P->cs.t->n_xccs;
   if (mapping == ASYM_MAP_AWARE) {
     P->quota = largest_remainder_quotas(P->tasks, P->cs.slots);
+    // claiming workgroups loop until every share is taken: two per CU of the
+    // largest XCD on every XCD (the dealing is equal per XCD), but no more
+    // than the groups of the largest share
     int most = 0;
     for (int x = 0; x < n_x; ++x) most = std::max(most, (P->quota[x] + per_wg - 1) / per_wg);
-    P->grid = std::max(1, most * n_x);
+    P->grid = std::max(1, std::min(most, 2 * P->cs.smax) * n_x);
   } else {
     P->grid = (P->tasks + per_wg - 1) / per_wg;
   }
@@ -726,12 +736,21 @@ int attn_decode(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int
       ws->attn_off.insert(ws->attn_off.begin(), std::make_pair(std::move(key), dev_off));
     }
     d_off = ws->attn_off.front().second;
+    if (!ws->attn_claim) {
+      // zero once here; every aware launch's merge leaves them zero again
+      ASYM_HIP(hipMalloc(&ws->attn_claim, attn_claim_ints() * sizeof(int)));
+      ASYM_HIP(hipMemset(ws->attn_claim, 0, attn_claim_ints() * sizeof(int)));
+    }
   }
   AttnLaunch a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse;
   a.part_o = ws->attn_buf;
   a.part_ml = ws->attn_buf + (size_t)B * Hq * P.n_splits * 128;
   a.d_quota_off = d_off;
+  a.d_claim = ws->attn_claim;
+  a.allow = 0;
+  for (int x = 0; x < n_x; ++x)
+    if (P.cs.slots[x] > 0) a.allow |= 1u << x;
   a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.S = S;
   a.split = P.split; a.n_splits = P.n_splits;
   a.n_x = n_x; a.grid = P.grid;
@@ -829,6 +848,7 @@ void release_workspace(hipStream_t s) {
       hipFree(it->second.gemm_ctr);
       hipFree(it->second.copy_ctr);
       if (it->second.attn_buf) hipFree(it->second.attn_buf);
+      if (it->second.attn_claim) hipFree(it->second.attn_claim);
       if (it->second.sm_part) hipFree(it->second.sm_part);
       for (auto& t : it->second.attn_off) hipFree(t.second);
       for (auto& t : it->second.g_tables) {

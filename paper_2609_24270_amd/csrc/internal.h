@@ -114,11 +114,14 @@ struct AttnLaunch {
   float* part_o;              // [B][Hq][n_splits][128]
   float* part_ml;             // [B][Hq][n_splits][2]
   const int* d_quota_off;     // aware: device [n_x + 1]; null = oblivious
+  int* d_claim = nullptr;     // aware: claim counters, zero at launch (the merge clears them)
+  uint32_t allow = 0xFFFFFFFFu; // aware: XCDs whose workgroups work
   int B, Hq, Hkv, S, split, n_splits, n_x, grid;
   float scale;
 };
 int launch_attn_decode(const AttnLaunch& a, hipStream_t s);
 int attn_tasks_per_workgroup();
+int attn_claim_ints();  // ints of the aware form's claim counters
 
 int probe_identity_run(int device, hipStream_t s, int n_blocks,
                        std::vector<int32_t>& rec, int pre_blocks = 0);

@@ -174,6 +174,9 @@ def test_gemm_plan_full_sizes(dev):
             assert p["workers"] == 256 and p["workers_per_xcd"] == [32] * 8
             assert p["claims"] == 0
             assert p["grid"] == 256
+    # a whole-XCD restriction takes claims (workers read XCC_ID)
+    p = asym.gemm_plan(mapping="aware", M=8192, N=8192, K=8192, xcd_mask=0x0F)
+    assert p["claims"] == 1 and p["workers"] == 128 and p["workers_per_xcd"] == [32] * 4 + [0] * 4
     # the predicated path keeps the 256-wide tile
     p = asym.gemm_plan(mapping="aware", M=300, N=700, K=150)
     assert p["vector_path"] == 0 and p["tile_n"] == 256
