@@ -233,16 +233,20 @@ def prefill_decode(topo, dev, iters: int, halves):
     return out
 
 
+READ_TENANT_PASSES = 100   # about 27 ms at 4 TB/s: longer than 20 GEMM launches beside it
+
+
 def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gemm"):
     """GEMM 4096^3 (uniform[-1,1], seed 4) on 128-CU sets: n_masks seeded random
     choices of 128 mask bits (what a topology-oblivious allocator hands out) and
     the two whole-XCD halves (the measured affinity groups; each side lends the
     other one CU per XCD and works only on its own XCDs).  A second
-    tenant, the same GEMM, runs on the complementary 128 CUs for the whole
-    measurement (tenant "gemm"), or the bandwidth-bound reader making 40 passes
-    of a 1 GiB buffer (tenant "read", longer than the GEMM).  Per-set TFLOP/s of
-    the measured GEMM for each mapping, and the max/min spread over the random
-    sets."""
+    tenant, the same GEMM with three times the launches, runs on the
+    complementary 128 CUs (tenant "gemm"), or the bandwidth-bound reader making
+    READ_TENANT_PASSES passes of a 1 GiB buffer (tenant "read"), kept to its own
+    XCDs on the aligned halves.  Per-set TFLOP/s of the measured GEMM for each
+    mapping, the max/min spread over the random sets, and in how many runs the
+    tenant ended after the GEMM (so that it ran beside every launch)."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -256,10 +260,17 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gem
 
     def other(cus, xm=0):
         if tenant == "read":
-            return asym.read_task(rbuf, 40, mask=cus)
-        return asym.gemm_task(Ad, Bd, C2, iters + iters // 2, "aware", mask=cus, xcd_mask=xm)
+            return asym.read_task(rbuf, READ_TENANT_PASSES, mask=cus, xcd_mask=xm)
+        return asym.gemm_task(Ad, Bd, C2, 3 * iters, "aware", mask=cus, xcd_mask=xm)
     per = {m: [] for m in MAPPINGS}
     counts = []
+    runs, covered = 0, 0
+
+    def cover(r):
+        # the tenant was busy for the whole measurement when it ended last
+        nonlocal runs, covered
+        runs += 1
+        covered += r[1]["ms_total"] >= r[0]["ms_total"]
     for i, m in enumerate(masks):
         comp = [b for b in range(256) if b not in set(m)]
         counts.append(topo.cuset_counts(m))
@@ -269,17 +280,18 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gem
                 # the first set is run twice: its first run settles the clock
                 r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m), other(comp)], topo)
             per[mapping].append(r[0]["tflops"])
-    aligned = []
+            cover(r)
+    aligned, aligned_read = [], []
     for xm in halves:
         ma, mb = topo.cuset_split_xcds(xm)
-        if tenant == "read":
-            # the reader has no XCD filter: it runs on the other side's CUs only
-            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm), other(mb)], topo)
-        else:
-            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
-                            other(mb, 0xFF & ~xm)], topo)
+        r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
+                        other(mb, 0xFF & ~xm)], topo)
         aligned.append(round(r[0]["tflops"], 2))
+        aligned_read.append(round(r[1]["gbps"], 1))
+        cover(r)
     summ = {"tenant": tenant, "n_random_sets": n_masks, "iters": iters, "aligned_aware_tflops": aligned,
+            **({"aligned_reader_GBps": aligned_read} if tenant == "read" else {}),
+            "tenant_outlasted_gemm": f"{covered}/{runs}",
             "random_set_min_max_cus_per_xcd": [min(min(c) for c in counts), max(max(c) for c in counts)]}
     for mapping, v in per.items():
         summ[f"random_{mapping}"] = {"min": round(min(v), 2), "max": round(max(v), 2),

@@ -648,7 +648,9 @@ typedef struct asym_task {
   int M, N, K;     /* GEMM shape, dense row-major A, B ([N][K]), C */
   const void* A; const void* B; void* C;
   const void* src; void* dst; size_t n_bytes; /* copy; read: src and n_bytes
-                                                 (a multiple of 16) */
+                                                 (a multiple of 16, < 2^40) */
+  int grid;        /* read: workgroups; 0 = 8 per CU of the reading XCD with the
+                      most CUs, times the XCD count */
 } asym_task;
 
 typedef struct asym_task_result {
@@ -657,14 +659,23 @@ typedef struct asym_task_result {
   double tflops;      /* GEMM */
   double gbps;        /* copy: bytes read + written per second / 1e9; read: bytes read */
   int iters_done;
+  uint32_t checksum[4]; /* read: XOR of every 16-byte word read, over all passes
+                           (for an odd pass count, the XOR of the buffer's words
+                           when each was read once per pass) */
 } asym_task_result;
 
 /* Run tasks concurrently, each on its own stream (masked streams for partial
  * masks, unmasked streams with XCD filtering for whole-XCD sets).  All tasks
  * are released together; a copy task with iters <= 0 runs until every GEMM
  * task has finished (bounded at 100000 passes).  A read task makes `iters`
- * passes of a whole-buffer reader (256 workgroups per XCD, 16-byte loads,
- * bounded, no atomics): the bandwidth-bound tenant of the co-location study.
+ * passes of a whole-buffer reader (16-byte loads, bounded, no atomics): the
+ * bandwidth-bound tenant of the co-location study.  The buffer is cut into one
+ * slice per reading XCD, in proportion to the task's CUs there, and read by
+ * the workgroups that XCD is dealt.  A read task's xcd_mask keeps its reads
+ * on those XCDs (workgroups elsewhere, e.g. on CUs its mask lends it there,
+ * leave at once).  Every GEMM task is launched once, untimed, before the
+ * release, so that its one-time setup (workspace, schedule upload) does not
+ * wait for tasks already running.
  * Synchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_corun(const asym_topology* topo, const asym_task* tasks, int n_tasks,

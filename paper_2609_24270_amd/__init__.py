@@ -146,7 +146,7 @@ class Task(ctypes.Structure):
                 ("mapping", ctypes.c_int), ("M", ctypes.c_int), ("N", ctypes.c_int),
                 ("K", ctypes.c_int), ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
                 ("C", ctypes.c_void_p), ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p),
-                ("n_bytes", ctypes.c_size_t)]
+                ("n_bytes", ctypes.c_size_t), ("grid", ctypes.c_int)]
 
 
 class GemmPlanInfo(ctypes.Structure):
@@ -177,7 +177,7 @@ class AttnPlanInfo(ctypes.Structure):
 class TaskResult(ctypes.Structure):
     _fields_ = [("ms_total", ctypes.c_double), ("ms_per_iter", ctypes.c_double),
                 ("tflops", ctypes.c_double), ("gbps", ctypes.c_double),
-                ("iters_done", ctypes.c_int)]
+                ("iters_done", ctypes.c_int), ("checksum", ctypes.c_uint32 * 4)]
 
 
 _lib = None
@@ -801,9 +801,11 @@ def copy_task(dst, src, passes: int = 0, mask=None, xcd_mask: int = 0) -> Task:
     return t
 
 
-def read_task(src, passes: int, mask=None, xcd_mask: int = 0) -> Task:
-    """A bandwidth-bound co-runner: `passes` whole reads of the CUDA tensor src."""
+def read_task(src, passes: int, mask=None, xcd_mask: int = 0, grid: int = 0) -> Task:
+    """A bandwidth-bound co-runner: `passes` whole reads of the CUDA tensor src,
+    on `grid` workgroups (0: 8 per CU of its XCD with the most CUs, on every XCD)."""
     t = Task()
+    t.grid = grid
     t.kind = 2
     if mask is not None:
         m = mask_words(mask)
@@ -821,7 +823,10 @@ def corun(tasks: Sequence[Task], topo: Optional[Topology] = None) -> list:
     arr = (Task * n)(*tasks)
     res = (TaskResult * n)()
     _check(load_library().asym_corun(topo.handle if topo else None, arr, n, res))
-    return [{k: getattr(r, k) for k, _ in TaskResult._fields_} for r in res]
+    out = [{k: getattr(r, k) for k, _ in TaskResult._fields_} for r in res]
+    for d in out:
+        d["checksum"] = list(d["checksum"])
+    return out
 
 
 def last_error() -> str:

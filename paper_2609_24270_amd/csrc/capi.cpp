@@ -98,15 +98,24 @@ std::map<int, std::unique_ptr<Topology>> g_default_topo;
 
 }  // namespace
 
+// A stream's workspace, created at its first use.  Nothing here waits for
+// other streams: the counters are cleared by a kernel ordered on s (a blocking
+// hipMemset would run on the null stream, which waits for every other stream,
+// and so would hold a launch back until a co-running kernel ended).
 static int get_workspace(int device, hipStream_t s, Workspace** out) {
   auto key = std::make_pair(device, s);
   auto it = g_ws.find(key);
   if (it == g_ws.end()) {
     Workspace w;
     ASYM_HIP(hipMalloc(&w.gemm_ctr, 64 * sizeof(int)));
-    ASYM_HIP(hipMemset(w.gemm_ctr, 0, 64 * sizeof(int)));
     ASYM_HIP(hipMalloc(&w.copy_ctr, 4 * sizeof(unsigned long long)));
-    ASYM_HIP(hipMemset(w.copy_ctr, 0, 4 * sizeof(unsigned long long)));
+    int rc = launch_zero_words(w.gemm_ctr, 64, s);
+    if (rc == ASYM_OK) rc = launch_zero_words(w.copy_ctr, 8, s);
+    if (rc != ASYM_OK) {
+      (void)hipFree(w.gemm_ctr);
+      (void)hipFree(w.copy_ctr);
+      return rc;
+    }
     it = g_ws.emplace(key, w).first;
   }
   *out = &it->second;
@@ -154,8 +163,12 @@ static int current_device(int* dev) {
   return ASYM_OK;
 }
 
+// The device copy of a schedule, built and uploaded at its first use.  The
+// copies are ordered on the launch stream, and only that stream is waited for
+// (the host arrays are then free): a blocking hipMemcpy would wait for every
+// other stream too.
 static int upload_schedule(int device, int tiles_m, int tiles_n, int mapping,
-                           const std::vector<int>& slots, const DeviceSchedule** out) {
+                           const std::vector<int>& slots, hipStream_t stream, const DeviceSchedule** out) {
   ScheduleKey key{device, tiles_m, tiles_n, mapping, slots};
   auto it = g_schedules.find(key);
   if (it == g_schedules.end()) {
@@ -169,9 +182,11 @@ static int upload_schedule(int device, int tiles_m, int tiles_n, int mapping,
     ASYM_HIP(hipMalloc(&d.d_order, sizeof(int) * s.order.size()));
     ASYM_HIP(hipMalloc(&d.d_off, sizeof(int) * off.size()));
     ASYM_HIP(hipMalloc(&d.d_slots, sizeof(int) * sl.size()));
-    ASYM_HIP(hipMemcpy(d.d_order, s.order.data(), sizeof(int) * s.order.size(), hipMemcpyHostToDevice));
-    ASYM_HIP(hipMemcpy(d.d_off, off.data(), sizeof(int) * off.size(), hipMemcpyHostToDevice));
-    ASYM_HIP(hipMemcpy(d.d_slots, sl.data(), sizeof(int) * sl.size(), hipMemcpyHostToDevice));
+    ASYM_HIP(hipMemcpyAsync(d.d_order, s.order.data(), sizeof(int) * s.order.size(), hipMemcpyHostToDevice,
+                            stream));
+    ASYM_HIP(hipMemcpyAsync(d.d_off, off.data(), sizeof(int) * off.size(), hipMemcpyHostToDevice, stream));
+    ASYM_HIP(hipMemcpyAsync(d.d_slots, sl.data(), sizeof(int) * sl.size(), hipMemcpyHostToDevice, stream));
+    ASYM_HIP(hipStreamSynchronize(stream));
     it = g_schedules.emplace(key, d).first;
   }
   *out = &it->second;
@@ -422,7 +437,7 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
     return launch_gemm_small_m(sm, stream);
   }
   const DeviceSchedule* ds = nullptr;
-  rc = upload_schedule(P.device, P.tiles_m, P.tiles_n, mapping, P.slots, &ds);
+  rc = upload_schedule(P.device, P.tiles_m, P.tiles_n, mapping, P.slots, stream, &ds);
   if (rc != ASYM_OK) return rc;
   Workspace* ws = nullptr;
   rc = get_workspace(P.device, stream, &ws);
@@ -739,7 +754,8 @@ int attn_decode(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int
     if (!ws->attn_claim) {
       // zero once here; every aware launch's merge leaves them zero again
       ASYM_HIP(hipMalloc(&ws->attn_claim, attn_claim_ints() * sizeof(int)));
-      ASYM_HIP(hipMemset(ws->attn_claim, 0, attn_claim_ints() * sizeof(int)));
+      rc = launch_zero_words(ws->attn_claim, attn_claim_ints(), stream);
+      if (rc != ASYM_OK) return rc;
     }
   }
   AttnLaunch a;

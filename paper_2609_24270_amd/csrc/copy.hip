@@ -13,6 +13,8 @@
 // the counters, so back-to-back launches on one stream need no memset.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "internal.h"
 
 namespace asym {
@@ -83,6 +85,11 @@ copy_kernel(v4u* __restrict__ dst, const v4u* __restrict__ src, size_t n16, int 
   }
 }
 
+__global__ void zero_words_kernel(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
 __global__ void set_flag_kernel(int* flag, int v) {
   if (threadIdx.x == 0) __hip_atomic_store(flag, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
@@ -103,6 +110,16 @@ int launch_copy(void* dst, const void* src, size_t n_bytes, int passes, const in
 // The claim-loop copy kernel did not finish in two device runs whose cause is
 // not understood; it stays unreachable until the cause is shown.
 bool copy_kernel_enabled() { return false; }
+
+// Stream-ordered zero fill of n 4-byte words (a kernel, not a memset node, so
+// that it also behaves under graph capture).
+int launch_zero_words(void* p, size_t n, hipStream_t s) {
+  if (!p || !n) return ASYM_OK;
+  const int grid = (int)std::min<size_t>((n + 255) / 256, 1024);
+  hipLaunchKernelGGL(zero_words_kernel, dim3(grid), dim3(256), 0, s, static_cast<uint32_t*>(p), n);
+  ASYM_HIP(hipGetLastError());
+  return ASYM_OK;
+}
 
 int launch_set_flag(int* flag, int v, hipStream_t s) {
   hipLaunchKernelGGL(set_flag_kernel, dim3(1), dim3(64), 0, s, flag, v);

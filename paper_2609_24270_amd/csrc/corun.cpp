@@ -3,7 +3,8 @@
 // SM counts whose physical placement differs).  Each task gets its own stream:
 // a hardware CU-masked queue when the task names a CU mask, an unmasked queue
 // with the kernels' own XCD filter when it names whole XCDs.  Tasks are
-// enqueued back to back and timed with events on their own streams; a copy
+// enqueued back to back, after one untimed launch of each GEMM (its one-time
+// setup), and timed with events on their own streams; a copy
 // task with iters <= 0 keeps streaming until a device flag, raised on the
 // GEMM streams after their last launch, stops it.  A read task is the
 // bandwidth-bound co-runner that stays available while the copy kernel is
@@ -65,7 +66,6 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
     } else if (t.kind == 2) {
       if (!t.src || t.n_bytes < 16 || t.n_bytes % 16 || t.iters < 1)
         return fail(ASYM_EINVAL, "corun: a read task needs a source of a multiple of 16 bytes and iters >= 1");
-      if (t.xcd_mask) return fail(ASYM_EUNSUPPORTED, "corun: a read task runs on a CU mask, not an XCD filter");
     } else {
       return fail(ASYM_EINVAL, "corun: unknown task kind");
     }
@@ -85,19 +85,53 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
   int n_x = 0, dev = 0;
   ASYM_HIP(hipGetDevice(&dev));
   ASYM_HIP(hipDeviceGetAttribute(&n_x, hipDeviceAttributeNumberOfXccs, dev));
-  const int read_grid = asym::stream_read_grid(n_x);
+  // read tasks: the reading CUs per XCD (the task's mask, or every CU, less
+  // the XCDs its filter leaves out) and the grid
+  std::vector<std::vector<int>> read_cus(n_tasks);
+  std::vector<int> read_grid(n_tasks, 0);
   std::vector<void*> sink(n_tasks, nullptr);
-  for (int i = 0; i < n_tasks; ++i)
-    if (tasks[i].kind == 2) {
-      ASYM_HIP(hipMalloc(&sink[i], (size_t)read_grid * 256 * 16));
-      g.sinks.push_back(sink[i]);
+  for (int i = 0; i < n_tasks; ++i) {
+    const asym_task& t = tasks[i];
+    if (t.kind != 2) continue;
+    if (n_x < 1 || n_x > 16 || (t.xcd_mask >> n_x) != 0u)
+      return fail(ASYM_EINVAL, "corun: a read task's XCD filter names an XCD the device does not have");
+    if (t.grid < 0 || t.grid > (1 << 20)) return fail(ASYM_EINVAL, "corun: a read task's grid must be in [0, 2^20]");
+    std::vector<int>& cus = read_cus[i];
+    cus.assign(ASYM_MAX_XCDS, 0);
+    if (!mask_empty(t.mask)) {
+      int rc = asym_cuset_counts(topo, t.mask, cus.data());
+      if (rc != ASYM_OK) return rc;
+    } else if (topo) {
+      int rc = asym_topology_info(topo, nullptr, nullptr, cus.data(), nullptr);
+      if (rc != ASYM_OK) return rc;
+    } else {
+      int n_cus = 0;
+      ASYM_HIP(hipDeviceGetAttribute(&n_cus, hipDeviceAttributeMultiprocessorCount, dev));
+      for (int x = 0; x < n_x; ++x) cus[x] = n_cus / n_x;
     }
+    for (int x = 0; x < n_x; ++x)
+      if (t.xcd_mask && !((t.xcd_mask >> x) & 1u)) cus[x] = 0;
+    read_grid[i] = t.grid > 0 ? t.grid : asym::stream_read_grid(cus.data(), n_x);
+    ASYM_HIP(hipMalloc(&sink[i], (size_t)read_grid[i] * 256 * 16));
+    g.sinks.push_back(sink[i]);
+  }
   std::vector<hipEvent_t> ev0(n_tasks), ev1(n_tasks);
   for (int i = 0; i < n_tasks; ++i) {
     ASYM_HIP(hipEventCreate(&ev0[i]));
     g.events.push_back(ev0[i]);
     ASYM_HIP(hipEventCreate(&ev1[i]));
     g.events.push_back(ev1[i]);
+  }
+  // one untimed launch of every GEMM task on its own stream before the
+  // release: its first launch on a new stream or CU set does one-time setup
+  // (workspace, schedule upload) that waits on its stream, which must not
+  // happen while the other tasks already run
+  for (int i = 0; i < n_tasks; ++i) {
+    const asym_task& t = tasks[i];
+    if (t.kind != 0) continue;
+    int rc = asym::gemm_bf16(topo, t.M, t.N, t.K, t.A, t.K, t.B, t.K, ASYM_B_NK, t.C, t.N, t.mapping,
+                             t.xcd_mask, g.streams[i]);
+    if (rc != ASYM_OK) return rc;
   }
   ASYM_HIP(hipDeviceSynchronize());
 
@@ -110,7 +144,8 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
       hipStream_t s = g.streams[i];
       ASYM_HIP(hipEventRecord(ev0[i], s));
       if (t.kind == 2) {
-        int rc = asym::launch_stream_read(t.src, t.n_bytes, t.iters, sink[i], read_grid, s);
+        int rc = asym::launch_stream_read(t.src, t.n_bytes, t.iters, sink[i], read_grid[i], read_cus[i].data(),
+                                          n_x, s);
         if (rc != ASYM_OK) return rc;
       } else if (t.kind == 1) {
         const int passes = t.iters > 0 ? t.iters : 100000;
@@ -153,6 +188,9 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
       r.iters_done = t.iters;
       r.ms_per_iter = ms / t.iters;
       r.gbps = (double)t.n_bytes * t.iters / (ms * 1e-3) / 1e9;
+      std::vector<uint32_t> h((size_t)read_grid[i] * 256 * 4);
+      ASYM_HIP(hipMemcpy(h.data(), sink[i], sizeof(uint32_t) * h.size(), hipMemcpyDeviceToHost));
+      for (size_t w = 0; w < h.size(); ++w) r.checksum[w & 3] ^= h[w];
     }
   }
   // bytes moved by each copy: read back and clear the stream's byte counter

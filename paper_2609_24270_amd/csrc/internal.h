@@ -167,13 +167,17 @@ int analyze_interleave(const uint32_t* L, int n_x, int n_a, const uint64_t* offs
 
 // Bandwidth-bound co-runner: `passes` reads of a whole buffer (sink: grid x
 // 256 x 16 bytes).
-int stream_read_grid(int n_x);
-int launch_stream_read(const void* src, size_t n_bytes, int passes, void* sink, int grid, hipStream_t s);
+// reading CUs per XCD cus[n_x] (0 = no share) -> a grid whose workgroups all fit at once
+int stream_read_grid(const int* cus, int n_x);
+int launch_stream_read(const void* src, size_t n_bytes, int passes, void* sink, int grid, const int* cus,
+                       int n_x, hipStream_t s);
 
 int launch_copy(void* dst, const void* src, size_t n_bytes, int passes,
                 const int* stop_flag, uint32_t xcd_mask, int grid,
                 unsigned long long* ctr, hipStream_t s);
 int launch_set_flag(int* flag, int v, hipStream_t s);
+// zero n 4-byte words at p, ordered on stream s
+int launch_zero_words(void* p, size_t n, hipStream_t s);
 bool copy_kernel_enabled();
 int copy_bytes_take(hipStream_t s, unsigned long long* bytes);
 void release_workspace(hipStream_t s);

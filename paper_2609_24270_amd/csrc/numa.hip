@@ -48,14 +48,60 @@ chunk_read_kernel(const char* __restrict__ base, int chunk_log2, const uint32_t*
 }
 
 // Whole-buffer reader for a bandwidth-bound co-runner: `passes` passes over
-// n16 16-byte words, workgroup b taking words b * 256 + t, then a grid-wide
-// stride; bounded by the pass count, no atomics or barriers.
+// n16 16-byte words, bounded by the pass count, no atomics or barriers.  The
+// buffer is cut into one contiguous slice per reading XCD, sized in proportion
+// to the CUs the reader has there (sh.cus), in XCD order.  A workgroup reads
+// its XCC_ID: on an XCD with no share (outside the XCD filter, or no CUs) it
+// leaves at once after its sink store; otherwise the workgroups of its residue
+// class of block indices mod n_x (which the dispatcher deals to one XCD)
+// stride over that XCD's slice in blocks of 8 x 256 words, each lane keeping 8
+// independent 16-byte loads in flight.  If two classes shared an XCD, one
+// slice would be read twice and another not at all; every index stays inside
+// the buffer either way.
+struct ReadShares {
+  int cus[16];  // reading CUs per XCD, 0 where the reader has no share
+};
+
+constexpr int kReadUnroll = 8;
+
 __global__ void __launch_bounds__(kReadThreads)
-stream_read_kernel(const v4u* __restrict__ src, size_t n16, int passes, v4u* __restrict__ sink) {
+stream_read_kernel(const v4u* __restrict__ src, size_t n16, int passes, v4u* __restrict__ sink,
+                   ReadShares sh, int n_x) {
   v4u acc = {0u, 0u, 0u, 0u};
-  const size_t stride = (size_t)gridDim.x * kReadThreads;
-  for (int pass = 0; pass < passes; ++pass)
-    for (size_t i = (size_t)blockIdx.x * kReadThreads + threadIdx.x; i < n16; i += stride) acc ^= src[i];
+  uint32_t x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  x &= 0xFu;
+  unsigned before = 0, total = 0;
+  for (int y = 0; y < 16; ++y) {
+    before += y < (int)x ? (unsigned)sh.cus[y] : 0u;
+    total += (unsigned)sh.cus[y];
+  }
+  if (sh.cus[x] > 0 && total > 0) {
+    // n16 < 2^36 and the CU sums <= 1024: the products fit in 64 bits
+    const size_t lo = (size_t)((uint64_t)n16 * before / total);
+    const size_t hi = (size_t)((uint64_t)n16 * (before + (unsigned)sh.cus[x]) / total);
+    const unsigned cls = blockIdx.x % (unsigned)n_x;
+    const unsigned members = (gridDim.x - cls + (unsigned)n_x - 1u) / (unsigned)n_x;
+    constexpr size_t kBlock = (size_t)kReadUnroll * kReadThreads;
+    const size_t first = lo + (size_t)(blockIdx.x / (unsigned)n_x) * kBlock + threadIdx.x;
+    const size_t stride = (size_t)members * kBlock;
+    for (int pass = 0; pass < passes; ++pass)
+      for (size_t i = first; i < hi; i += stride) {
+        v4u v[kReadUnroll];
+        if (i + (size_t)(kReadUnroll - 1) * kReadThreads < hi) {
+#pragma unroll
+          for (int j = 0; j < kReadUnroll; ++j) v[j] = src[i + (size_t)j * kReadThreads];
+        } else {  // the slice's last block
+#pragma unroll
+          for (int j = 0; j < kReadUnroll; ++j) {
+            const size_t k = i + (size_t)j * kReadThreads;
+            v[j] = k < hi ? src[k] : v4u{0u, 0u, 0u, 0u};
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < kReadUnroll; ++j) acc ^= v[j];
+      }
+  }
   sink[(size_t)blockIdx.x * kReadThreads + threadIdx.x] = acc;
 }
 
@@ -300,13 +346,32 @@ int chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uint32_t
   return ASYM_OK;
 }
 
-int stream_read_grid(int n_x) { return n_x * kReadWorkersPerXcd; }
+// The reader's grid for reading CUs cus[x] per XCD: the same count w on every
+// XCD (workgroups are dealt round-robin), 8 workgroups of 4 waves per CU of
+// the XCD with the most reading CUs (its slice is the largest).  XCDs with
+// fewer CUs hold their workgroups in the queue until CUs free up; XCDs with no
+// share see theirs leave at once.
+int stream_read_grid(const int* cus, int n_x) {
+  int hi = 0;
+  for (int x = 0; x < n_x; ++x) hi = std::max(hi, cus[x]);
+  return n_x * std::max(1, 8 * hi);
+}
 
-int launch_stream_read(const void* src, size_t n_bytes, int passes, void* sink, int grid, hipStream_t s) {
-  if (!src || !sink || n_bytes < 16 || n_bytes % 16 || passes < 1 || grid < 1)
+int launch_stream_read(const void* src, size_t n_bytes, int passes, void* sink, int grid, const int* cus,
+                       int n_x, hipStream_t s) {
+  if (!src || !sink || !cus || n_bytes < 16 || n_bytes % 16 || (n_bytes >> 40) || passes < 1 || grid < 1 ||
+      n_x < 1 || n_x > 16)
     return fail(ASYM_EINVAL, "stream read: bad arguments");
+  ReadShares sh{};
+  int any = 0;
+  for (int x = 0; x < n_x; ++x) {
+    if (cus[x] < 0 || cus[x] > 64) return fail(ASYM_EINVAL, "stream read: bad CU count");
+    sh.cus[x] = cus[x];
+    any += cus[x];
+  }
+  if (!any) return fail(ASYM_EINVAL, "stream read: no reading CU");
   hipLaunchKernelGGL(stream_read_kernel, dim3(grid), dim3(kReadThreads), 0, s, static_cast<const v4u*>(src),
-                     n_bytes / 16, passes, static_cast<v4u*>(sink));
+                     n_bytes / 16, passes, static_cast<v4u*>(sink), sh, n_x);
   ASYM_HIP(hipGetLastError());
   return ASYM_OK;
 }

@@ -195,7 +195,7 @@ def test_corun_gemm_with_read_tenant(dev, topo):
     """A GEMM on a seeded random 128-CU set with the bandwidth-bound reader on
     the complementary CUs: the GEMM's bits equal the GEMM run alone for every
     mapping, the reader reports its passes and rate; a read task with no
-    passes, or with an XCD filter, is refused."""
+    passes, or with an XCD filter naming a missing XCD, is refused."""
     A, B = workloads.make_inputs(workloads.COLOC)
     Ad, Bd = A.to(dev), B.to(dev)
     ref = asym.gemm(Ad, Bd)
@@ -212,4 +212,39 @@ def test_corun_gemm_with_read_tenant(dev, topo):
     with pytest.raises(asym.AsymError):
         asym.corun([asym.gemm_task(Ad, Bd, C, 1, "aware", mask=mask), asym.read_task(buf, 0, mask=comp)], topo)
     with pytest.raises(asym.AsymError):
-        asym.corun([asym.gemm_task(Ad, Bd, C, 1, "aware"), asym.read_task(buf, 1, xcd_mask=0x0F)], topo)
+        asym.corun([asym.gemm_task(Ad, Bd, C, 1, "aware"), asym.read_task(buf, 1, xcd_mask=0x100)], topo)
+
+
+def test_read_tenant_covers_the_buffer(dev, topo):
+    """The reader's checksum (XOR of every 16-byte word it read) equals the XOR
+    of the buffer's words for an odd pass count: on a CU mask, on the whole
+    chip, and with an XCD filter (alone, and on the whole-XCD side of an
+    aligned split whose mask lends it one CU on each other XCD, beside a GEMM
+    restricted to the other side), on the default grid and on explicit ones
+    (more workgroups than the CUs hold; fewer than the XCDs).  A ragged size:
+    not a multiple of the per-XCD slices or of the grid's stride."""
+    n16 = (48 << 16) + 37
+    words = torch.randint(-2**31, 2**31 - 1, (n16 * 4,), dtype=torch.int32,
+                          generator=torch.Generator().manual_seed(5))
+    want = np.bitwise_xor.reduce(words.numpy().view(np.uint32).reshape(-1, 4), axis=0).tolist()
+    buf = words.to(dev)
+    A, B = workloads.make_inputs(workloads.COLOC)
+    Ad, Bd = A.to(dev), B.to(dev)
+    ref = asym.gemm(Ad, Bd)
+    torch.cuda.synchronize()
+    C = torch.empty_like(ref)
+    mask = workloads.random_mask_bits(4, 1, 128)[0]
+    comp = [b for b in range(256) if b not in set(mask)]
+    cases = [("masked", dict(mask=comp)), ("whole chip", {}), ("xcds 0xF0", dict(xcd_mask=0xF0)),
+             ("xcds 0x5A", dict(xcd_mask=0x5A)), ("masked, 3000 workgroups", dict(mask=comp, grid=3000)),
+             ("xcds 0x0F, 9 workgroups", dict(xcd_mask=0x0F, grid=9))]
+    for name, kw in cases:
+        r = asym.corun([asym.read_task(buf, 3, **kw)], topo)
+        print(name, r[0]["gbps"], [hex(v) for v in r[0]["checksum"]])
+        assert r[0]["checksum"] == want, name
+    for xm in (0x0F, 0xF0):
+        ma, mb = topo.cuset_split_xcds(xm)
+        r = asym.corun([asym.gemm_task(Ad, Bd, C, 5, "aware", mask=ma, xcd_mask=xm),
+                        asym.read_task(buf, 3, mask=mb, xcd_mask=0xFF & ~xm)], topo)
+        print("aligned", hex(xm), r)
+        assert r[1]["checksum"] == want and torch.equal(C, ref), hex(xm)
