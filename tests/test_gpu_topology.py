@@ -215,6 +215,25 @@ def test_corun_gemm_with_read_tenant(dev, topo):
         asym.corun([asym.gemm_task(Ad, Bd, C, 1, "aware"), asym.read_task(buf, 1, xcd_mask=0x100)], topo)
 
 
+def test_corun_tasks_overlap(dev, topo):
+    """Co-run tasks run at the same time: a short GEMM on a CU set not used
+    before (its schedule is built and uploaded inside the co-run) ends while a
+    reader about ten times longer still runs on the complementary CUs.  A
+    one-time setup that waited for every stream would start the GEMM only after
+    the reader ended."""
+    A, B = workloads.make_inputs(workloads.COLOC)
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
+    buf = torch.ones(256 << 20, dtype=torch.float32, device=dev)   # 1 GiB
+    for seed in (77, 78):
+        mask = workloads.random_mask_bits(seed, 1, 128)[0]
+        comp = [b for b in range(256) if b not in set(mask)]
+        res = asym.corun([asym.gemm_task(Ad, Bd, C, 3, "aware", mask=mask),
+                          asym.read_task(buf, 60, mask=comp)], topo)
+        print(seed, res)
+        assert res[0]["ms_total"] < 0.5 * res[1]["ms_total"], res
+
+
 def test_read_tenant_covers_the_buffer(dev, topo):
     """The reader's checksum (XOR of every 16-byte word it read) equals the XOR
     of the buffer's words for an odd pass count: on a CU mask, on the whole
