@@ -204,7 +204,7 @@ def prefill_decode(topo, dev, iters: int, halves):
     """Prefill GEMM 8192x4096x4096 on 192 CUs co-running with decode GEMM
     32x14336x4096 on the other 64, on XCD-aligned sets (6 XCDs / 2 XCDs, the
     decode pair taken from one affinity group) and on CU-striped sets (24 / 8
-    CUs of every XCD); aware mapping."""
+    CUs of every XCD); aware mapping; each also alone on its set."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -224,12 +224,19 @@ def prefill_decode(topo, dev, iters: int, halves):
                                               topo),
             "cu_striped": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=prefill),
                                               asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=decode)], topo)}
+    alone = {"xcd_aligned": (lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=pre_m, xcd_mask=pre_x)], topo),
+                             lambda: asym.corun([asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=dec_m, xcd_mask=dec_x)], topo)),
+             "cu_striped": (lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=prefill)], topo),
+                            lambda: asym.corun([asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=decode)], topo))}
     out = {}
     for _ in range(2):  # first round settles the clock; the second is kept
         for k, fn in runs.items():
             r = fn()
+            p_alone, d_alone = alone[k][0]()[0], alone[k][1]()[0]
             out[k] = {"prefill_ms": round(r[0]["ms_per_iter"], 4), "prefill_tflops": round(r[0]["tflops"], 2),
-                      "decode_ms": round(r[1]["ms_per_iter"], 4), "decode_tflops": round(r[1]["tflops"], 2)}
+                      "decode_ms": round(r[1]["ms_per_iter"], 4), "decode_tflops": round(r[1]["tflops"], 2),
+                      "prefill_alone_ms": round(p_alone["ms_per_iter"], 4),
+                      "decode_alone_ms": round(d_alone["ms_per_iter"], 4)}
     return out
 
 
@@ -245,8 +252,9 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gem
     complementary 128 CUs (tenant "gemm"), or the bandwidth-bound reader making
     READ_TENANT_PASSES passes of a 1 GiB buffer (tenant "read"), kept to its own
     XCDs on the aligned halves.  Per-set TFLOP/s of the measured GEMM for each
-    mapping, the max/min spread over the random sets, and in how many runs the
-    tenant ended after the GEMM (so that it ran beside every launch)."""
+    mapping, the max/min spread over the random sets, in how many runs the
+    tenant ended after the GEMM (so that it ran beside every launch), and the
+    same GEMM alone on the first random set and on the halves."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -281,9 +289,14 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gem
                 r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m), other(comp)], topo)
             per[mapping].append(r[0]["tflops"])
             cover(r)
-    aligned, aligned_read = [], []
+    m0 = masks[0]
+    alone = {mp: round(asym.corun([asym.gemm_task(Ad, Bd, C, iters, mp, mask=m0)], topo)[0]["tflops"], 2)
+             for mp in MAPPINGS}
+    aligned, aligned_read, aligned_alone = [], [], []
     for xm in halves:
         ma, mb = topo.cuset_split_xcds(xm)
+        aligned_alone.append(round(asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm)],
+                                              topo)[0]["tflops"], 2))
         r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
                         other(mb, 0xFF & ~xm)], topo)
         aligned.append(round(r[0]["tflops"], 2))
@@ -292,6 +305,7 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gem
     summ = {"tenant": tenant, "n_random_sets": n_masks, "iters": iters, "aligned_aware_tflops": aligned,
             **({"aligned_reader_GBps": aligned_read} if tenant == "read" else {}),
             "tenant_outlasted_gemm": f"{covered}/{runs}",
+            "alone_tflops": {"first_random_set": alone, "aligned_halves_aware": aligned_alone},
             "random_set_min_max_cus_per_xcd": [min(min(c) for c in counts), max(max(c) for c in counts)]}
     for mapping, v in per.items():
         summ[f"random_{mapping}"] = {"min": round(min(v), 2), "max": round(max(v), 2),
