@@ -5,15 +5,17 @@
 // the unit each block runs on, and giving it the tasks whose data is local to
 // that unit's partition, with work in proportion to each partition's units.
 // Here a task is a 256x256 output tile and the partition is the XCD (private
-// 4 MB L2).  On gfx950 the XCD a workgroup lands on is fixed by its launch
-// index: workgroups are dealt to the XCDs round-robin, which the identity
-// probe measures (every workgroup of a full-grid launch reports XCC_ID =
-// block index mod 8).  So the lookup costs nothing at run time: in AWARE mode
-// workgroup b is XCD (b mod n)'s (b / n)-th worker and runs that XCD's region
-// of the schedule with a stride of the XCD's worker count; workers beyond the
-// XCD's scheduled CU count leave at once.  No counters or atomics are
-// involved, and every tile is computed whatever the actual placement (which
-// decides only the L2 a tile is served from).  The OBLIVIOUS modes walk one
+// 4 MB L2).  On gfx950 workgroups are dealt to the XCDs round-robin by launch
+// index, so every residue class of block indices mod n lands on one XCD (the
+// identity probe measures this); which XCD a class lands on depends on where
+// the dealing starts, which has differed between streams.  Where the CU set
+// has the same count on every XCD, AWARE mode needs only the classes: workgroup
+// b is the (b / n)-th worker of region b mod n of the schedule and runs it with
+// a stride of the region's worker count.  A region's workers then share one
+// L2 whatever the rotation, no counters or atomics are involved, and every
+// tile is computed whatever the actual placement.  Where the XCD's identity
+// matters (unequal CU counts, a whole-XCD restriction) workgroups read XCC_ID
+// and claim tiles instead (dynamic form below).  The OBLIVIOUS modes walk one
 // shared order (tile i on workgroup i mod P), which is how a persistent GEMM
 // without topology knowledge runs.
 //
