@@ -77,7 +77,12 @@ def time_launches(fn, steps: int, stream):
     return total, sum(per) / len(per)
 
 
-def cpu_baseline(A, B, rows: int):
+def cpu_baseline(A, B, rows: int, C_gpu=None):
+    """The oracle timed on the host's cores over rows 0..rows-1 of the
+    problem.  When the GPU's output of the same problem is given, the oracle's
+    rows (computed anyway) also check it: the gate is max |C - R32| /
+    max(|R32|, rms(R32)) <= 2e-2 over every checked element, R32 being the
+    oracle's fp32 sum before rounding."""
     import numpy as np
     import torch
 
@@ -85,13 +90,24 @@ def cpu_baseline(A, B, rows: int):
     bits = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
     Ab, Bb = bits(A[:rows]), bits(B)
     t0 = time.perf_counter()
-    oracle.gemm_bf16(Ab, Bb, "nk", want_r32=False)
+    R, Co = oracle.gemm_bf16(Ab, Bb, "nk", want_r32=C_gpu is not None)
     dt = time.perf_counter() - t0
     flops = 2.0 * rows * B.shape[0] * B.shape[1]
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle", "seconds": dt,
-            "sample": f"rows 0..{rows - 1} of A against all of B (M={rows}, N={B.shape[0]}, K={B.shape[1]}), "
-                      f"{flops / 1e9:.1f} GFLOP"}
+    out = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+           "kind": "oracle", "seconds": dt,
+           "sample": f"rows 0..{rows - 1} of A against all of B (M={rows}, N={B.shape[0]}, K={B.shape[1]}), "
+                     f"{flops / 1e9:.1f} GFLOP"}
+    if C_gpu is None:
+        return out, None
+    Cg = bits(C_gpu[:rows])
+    g = (Cg.astype(np.uint32) << 16).view(np.float32).astype(np.float64)  # bf16 bits -> value
+    r = R.astype(np.float64)
+    rms = float(np.sqrt(np.mean(r * r)))
+    err = float(np.max(np.abs(g - r) / np.maximum(np.abs(r), rms)))
+    parity = {"checked": f"rows 0..{rows - 1}, every column ({rows * B.shape[0]} elements)",
+              "max_rel_err": err, "gate": 2e-2, "pass": err <= 2e-2,
+              "bitwise_equal_to_oracle_frac": float(np.mean(Cg == Co))}
+    return out, parity
 
 
 def settle(fns, seconds: float):
@@ -656,6 +672,7 @@ def main() -> int:
     head_mapping = args.mapping_only or "aware"
     fns = {m: (lambda m=m: asym.gemm(Ad, Bd, C, mapping=m, topo=topo, stream=stream)) for m in MAPPINGS}
     head = fns[head_mapping]
+    plan = asym.gemm_plan(Ad, Bd, C, mapping=head_mapping, topo=topo, stream=stream)
     for _ in range(args.warmup):
         head()
     settle([head], args.settle)
@@ -679,7 +696,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": "square bf16 GEMM M=N=K=8192, uniform[-1,1] seed 1, B [N,K], "
                                f"full GPU, {head_mapping} persistent mapping, topology probe first",
-                   "M": p.M, "N": p.N, "K": p.K, "mapping": head_mapping, "tile": "256x256, k-step 32"},
+                   "M": p.M, "N": p.N, "K": p.K, "mapping": head_mapping, "plan": plan},
         "pct_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
@@ -719,10 +736,15 @@ def main() -> int:
         line["partition_hash"] = summ
         if hres["n_groups"] == 2:
             line["numa_read_bw"] = numa_bw_study(dev, hres)
-    line["cpu_baseline"] = None if args.no_cpu else cpu_baseline(A, B, args.cpu_rows)
-    if line["cpu_baseline"]:
-        line["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v)
-                                for k, v in line["cpu_baseline"].items()}
+    if args.no_cpu:
+        line["cpu_baseline"] = None
+    else:
+        # the timed problem once more, so C holds the head mapping's output
+        head()
+        torch.cuda.synchronize()
+        cpu, parity = cpu_baseline(A, B, args.cpu_rows, C.cpu())
+        line["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cpu.items()}
+        line["parity_vs_oracle"] = parity
     print(json.dumps(line), flush=True)
     return 0
 

@@ -27,17 +27,19 @@
 // MFMA blocks, 256 fp32 accumulators per lane in AGPRs).
 //
 // Vector path (16-byte aligned operands, K a multiple of 8): k advances in
-// stages of 64 through a ring of two LDS slots (A and B, 256 rows x 128 bytes
-// each, 64 KiB per slot).  Operands go from HBM straight into LDS with
-// buffer_load_dwordx4 ... lds (no staging registers, no LDS write
-// instructions), eight lanes per whole 128-byte line; the loads for stage t+2
-// are issued during the second half of stage t, so a full stage of MFMA work
-// covers their latency.  Inside a row the eight 16-byte chunks are stored
-// XOR-swizzled by (row >> 1) & 7, which keeps the 16 rows read by one
-// ds_read_b128 free of bank conflicts.  MFMA fragments are double-buffered:
-// the next half-stage's fragments are read while the current half-stage's 64
-// MFMAs run.  One barrier per stage publishes the next slot; waits on the
-// loads are explicit, so the barrier does not drain the prefetch.
+// stages of 64 through LDS rings, three slots for A and two for B (32 KiB per
+// slot at the 256-wide tile, 160 KiB in all).  Operands go from HBM straight
+// into LDS with buffer_load_dwordx4 ... lds (no staging registers, no LDS
+// write instructions), eight lanes per whole 128-byte line; A's loads for
+// stage t+2 are issued during the first half of stage t and B's during the
+// second half, so MFMA work covers their latency.  Inside a row the eight
+// 16-byte chunks are stored XOR-swizzled by (row >> 1) & 7, which keeps the 16
+// rows read by one ds_read_b128 free of bank conflicts.  MFMA fragments are
+// double-buffered: the next half-stage's fragments are read while the current
+// half-stage's 64 MFMAs run.  One barrier per stage publishes the next stage;
+// waits on the loads are explicit, so the barrier does not drain the
+// prefetch.  Tiles 224 and 192 wide (7 and 6 B fragments per wave) exist for
+// shapes whose tile count fits the workers better at those widths.
 //
 // Generic path (any alignment or K): 256x256x64 tiles, register-staged
 // element loads into two padded LDS stages.
@@ -420,28 +422,41 @@ __device__ __forceinline__ void ring_load(const RingCtx& c, const StageOffsets& 
 // fragment G into `b` (B fragment G has no later use in this half-stage, so it
 // is replaced in place; the A fragments feed every group and are double
 // buffered).  Spreading the loads and reads keeps the MFMAs fed better than
-// bursts do.  `sa`/`sb` are the LDS addresses of the next half-stage's
-// fragment 0; `sa2` is A slot (t+2)'s byte offset.
+// bursts do.  The last group is different: nothing follows it in the
+// half-stage to cover a read issued after its MFMAs, and the next half-stage
+// starts by waiting for every read.  So the last B fragment is double
+// buffered (`bl`: HALF h computes with bl[h] and reads the next half-stage's
+// into bl[1 - h]) and the last group issues all its reads, and the remaining A
+// fragments of a tile narrower than 256, before its MFMAs.  `sa`/`sb` are the
+// LDS addresses of the next half-stage's fragment 0; `sa2` is A slot (t+2)'s
+// byte offset.
 template <int NBF, int G, int HALF>
 __device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets& o, int t, uint32_t sa2,
                                            f32x4 (&acc)[NBF][8], const bf16x8 (&ac)[8],
-                                           bf16x8 (&an)[8], bf16x8 (&b)[NBF], uint32_t sa,
-                                           uint32_t sb) {
+                                           bf16x8 (&an)[8], bf16x8 (&b)[NBF], bf16x8 (&bl)[2],
+                                           uint32_t sa, uint32_t sb) {
   constexpr int lo = HALF == 0 ? G * 8 / NBF : 8 + G, hi = HALF == 0 ? (G + 1) * 8 / NBF : 9 + G;
-  if constexpr (lo < hi) ring_load<NBF>(c, o, t + 2, sa2, lo);
+  if constexpr (G + 1 < NBF) {
+    if constexpr (lo < hi) ring_load<NBF>(c, o, t + 2, sa2, lo);
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
+    for (int mb = 0; mb < 4; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
 #pragma unroll
-  for (int j = lo + 1; j < hi; ++j) ring_load<NBF>(c, o, t + 2, sa2, j);
-  if constexpr (G < 8) lds_read_frag<G * 2048>(an[G], sa);
+    for (int j = lo + 1; j < hi; ++j) ring_load<NBF>(c, o, t + 2, sa2, j);
+    lds_read_frag<G * 2048>(an[G], sa);
 #pragma unroll
-  for (int mb = 4; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
-  lds_read_frag<G * 2048>(b[G], sb);
-  if constexpr (G + 1 == NBF) {
-    // fewer B fragments than A fragments: read the remaining A fragments
-    lds_read_frags_from<NBF>(an, sa);
+    for (int mb = 4; mb < 8; ++mb) mfma_acc(acc[G][mb], b[G], ac[mb]);
+    lds_read_frag<G * 2048>(b[G], sb);
+    ring_group<NBF, G + 1, HALF>(c, o, t, sa2, acc, ac, an, b, bl, sa, sb);
   } else {
-    ring_group<NBF, G + 1, HALF>(c, o, t, sa2, acc, ac, an, b, sa, sb);
+    if constexpr (lo < hi) ring_load<NBF>(c, o, t + 2, sa2, lo);
+    lds_read_frag<G * 2048>(bl[1 - HALF], sb);
+    lds_read_frags_from<G>(an, sa);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) mfma_acc(acc[G][mb], bl[HALF], ac[mb]);
+#pragma unroll
+    for (int j = lo + 1; j < hi; ++j) ring_load<NBF>(c, o, t + 2, sa2, j);
+#pragma unroll
+    for (int mb = 4; mb < 8; ++mb) mfma_acc(acc[G][mb], bl[HALF], ac[mb]);
   }
 }
 
@@ -459,16 +474,16 @@ __device__ __forceinline__ void ring_group(const RingCtx& c, const StageOffsets&
 template <int NBF>
 __device__ __forceinline__ void ring_stage(const RingCtx& c, int t, const uint32_t (&sa)[3],
                                            f32x4 (&acc)[NBF][8], bf16x8 (&a0)[8], bf16x8 (&a1)[8],
-                                           bf16x8 (&b)[NBF], const uint32_t (&ra)[2],
+                                           bf16x8 (&b)[NBF], bf16x8 (&bl)[2], const uint32_t (&ra)[2],
                                            const uint32_t (&rb)[2]) {
   const uint32_t sb0 = (uint32_t)(t & 1) * b_bytes<NBF>();
   const uint32_t sb1 = (uint32_t)((t + 1) & 1) * b_bytes<NBF>();
   const StageOffsets o = stage_offsets(c, t + 2);
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  ring_group<NBF, 0, 0>(c, o, t, sa[2], acc, a0, a1, b, ra[1] + sa[0], rb[1] + sb0);
+  ring_group<NBF, 0, 0>(c, o, t, sa[2], acc, a0, a1, b, bl, ra[1] + sa[0], rb[1] + sb0);
   asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
   lds_barrier();
-  ring_group<NBF, 0, 1>(c, o, t, sa[2], acc, a1, a0, b, ra[0] + sa[1], rb[0] + sb1);
+  ring_group<NBF, 0, 1>(c, o, t, sa[2], acc, a1, a0, b, bl, ra[0] + sa[1], rb[0] + sb1);
 }
 
 // An empty asm that redefines one column block's accumulators in AGPRs: the
@@ -561,17 +576,19 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   }
   asm volatile("s_waitcnt vmcnt(%0)" :: "n"(8 + NBF) : "memory");
   lds_barrier();
-  bf16x8 a0[8], a1[8], bf[NBF];
+  // (B fragments 0 .. NBF-2 in bf, the last one in bl[0]: see ring_group)
+  bf16x8 a0[8], a1[8], bf[NBF], bl[2];
   lds_read_frags_from<0>(a0, ra[0]);
   lds_read_frag<0>(bf[0], rb[0]); lds_read_frag<2048>(bf[1], rb[0]);
   lds_read_frag<4096>(bf[2], rb[0]); lds_read_frag<6144>(bf[3], rb[0]);
-  lds_read_frag<8192>(bf[4], rb[0]); lds_read_frag<10240>(bf[5], rb[0]);
-  if constexpr (NBF > 6) lds_read_frag<12288>(bf[6 % NBF], rb[0]);
-  if constexpr (NBF > 7) lds_read_frag<14336>(bf[7 % NBF], rb[0]);
+  lds_read_frag<8192>(bf[4], rb[0]);
+  if constexpr (NBF > 6) lds_read_frag<10240>(bf[5], rb[0]);
+  if constexpr (NBF > 7) lds_read_frag<12288>(bf[6 % NBF], rb[0]);
+  lds_read_frag<(NBF - 1) * 2048>(bl[0], rb[0]);
   // A slot offsets of stages t, t+1, t+2 (uniform, rotated each stage)
   uint32_t sa[3] = {0u, (uint32_t)A_BYTES, 2u * A_BYTES};
   for (int t = 0; t < KT; ++t) {
-    ring_stage<NBF>(c, t, sa, acc, a0, a1, bf, ra, rb);
+    ring_stage<NBF>(c, t, sa, acc, a0, a1, bf, bl, ra, rb);
     const uint32_t s0 = sa[0];
     sa[0] = sa[1];
     sa[1] = sa[2];
