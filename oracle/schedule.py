@@ -12,7 +12,14 @@ The tile order is the banded column-major walk: tile rows are cut into bands of
 `band` rows, each band is walked column by column, top to bottom.  AWARE shares
 every band out among the partitions: the band's walk is cut into contiguous
 runs of Hamilton-apportioned lengths, one per partition in index order, and a
-partition's list is its run of band 0, then of band 1, and so on.  The
+partition's list is its run of band 0, then of band 1, and so on.  A second
+reading of "tasks local to the partition" covers grids whose band holds fewer
+tiles than one round of every partition's workers (band * tiles_n < n * s): a
+band's runs would then be strips band rows by a few columns, taken from two or
+more bands at once.  With s workers on every partition the grid is instead cut
+into band x (s / band) blocks, numbered band by band and left to right, and
+block k goes to partition k mod n (each block's tiles column by column, top to
+bottom), where the blocks divide the grid and come out even.  The
 oblivious mappings hand order position i of the whole walk to workgroup
 i mod P, which round-robin dispatch places on partition (i mod P) mod n.
 
@@ -79,6 +86,40 @@ def aware_lists(tiles_m, tiles_n, slots, band):
             lists[x].extend(walk[pos:pos + qx])
             pos += qx
     return lists
+
+
+def block_deal_lists(tiles_m, tiles_n, slots, band):
+    """The block-dealing form of the aware lists (module docstring), or None
+    where it does not apply: unequal worker counts, a band that already holds
+    a round of every partition, or blocks that do not divide the grid or do
+    not come out even over the partitions."""
+    n = len(slots)
+    s = slots[0]
+    if s < 1 or any(w != s for w in slots):
+        return None
+    h = band
+    if h < 1 or s % h or tiles_m % h:
+        return None
+    c = s // h
+    if tiles_n % c or h * tiles_n >= n * s:
+        return None
+    if (tiles_m * tiles_n // s) % n:
+        return None
+    lists = [[] for _ in slots]
+    k = 0
+    for r0 in range(0, tiles_m, h):
+        for c0 in range(0, tiles_n, c):
+            lists[k % n].extend(r * tiles_n + cc for cc in range(c0, c0 + c) for r in range(r0, r0 + h))
+            k += 1
+    return lists
+
+
+def aware_lists_auto(tiles_m, tiles_n, slots):
+    """The aware lists with the band chosen by band_cost_choice: dealt blocks
+    where they apply, else the band runs."""
+    band = band_cost_choice(tiles_m, max(slots))
+    lists = block_deal_lists(tiles_m, tiles_n, slots, band)
+    return lists if lists is not None else aware_lists(tiles_m, tiles_n, slots, band)
 
 
 def aware_assignment(tiles_m, tiles_n, slots, band):

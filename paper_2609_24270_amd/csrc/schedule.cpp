@@ -22,6 +22,15 @@
 //                      form a compact block in its own L2, and all XCDs work in
 //                      the same band at the same time, so the band's A rows are
 //                      fetched from HBM once for all of them (memory-side cache).
+//                      Where a band holds fewer tiles than one round of
+//                      every XCD's workgroups (band * tiles_n < n * s, s the
+//                      same on every XCD), a band's runs would be strips a few
+//                      columns wide, taken from two bands at once.  The grid is
+//                      then cut into band x (s / band) blocks instead, numbered
+//                      band by band and left to right; block k goes to XCD
+//                      k mod n (where the blocks divide the grid and come out
+//                      even).  4096x4096 at 256^2 tiles: each XCD runs one
+//                      8x4 block, not two 8x2 strips.
 //   OBLIVIOUS_GROUPED: the banded order, tile i to workgroup i mod P; round-robin
 //                      dispatch then puts neighbouring tiles on different XCDs.
 //   OBLIVIOUS_ROWMAJOR: row-major order, tile i to workgroup i mod P.
@@ -117,7 +126,29 @@ int build_schedule(int tiles_m, int tiles_n, int n_xcds, const int* slots,
     }
   }
 
-  if (mapping == ASYM_MAP_AWARE) {
+  // the block-dealing form of the aware lists (auto band only)
+  bool blocks = mapping == ASYM_MAP_AWARE && band == 0 && slots[0] >= 1;
+  for (int x = 1; x < n_xcds && blocks; ++x) blocks = slots[x] == slots[0];
+  const int bh = blocks ? choose_band(tiles_m, smax) : 1;
+  const int bw = blocks ? slots[0] / bh : 1;
+  if (blocks)
+    blocks = slots[0] % bh == 0 && tiles_m % bh == 0 && tiles_n % bw == 0 &&
+             (int64_t)bh * tiles_n < (int64_t)n_xcds * slots[0] && (T / slots[0]) % n_xcds == 0;
+  if (blocks) {
+    std::vector<std::vector<int>> lists(n_xcds);
+    int k = 0;
+    for (int r0 = 0; r0 < tiles_m; r0 += bh)
+      for (int c0 = 0; c0 < tiles_n; c0 += bw, ++k)
+        for (int c = c0; c < c0 + bw; ++c)
+          for (int r = r0; r < r0 + bh; ++r) lists[k % n_xcds].push_back(r * tiles_n + c);
+    int o = 0;
+    for (int x = 0; x < n_xcds; ++x) {
+      std::copy(lists[x].begin(), lists[x].end(), s.order.begin() + o);
+      s.quota[x] = (int)lists[x].size();
+      o += s.quota[x];
+      s.off[x + 1] = o;
+    }
+  } else if (mapping == ASYM_MAP_AWARE) {
     // per band: apportion the band's tiles, cut the band's banded order into
     // one contiguous run per XCD; then concatenate each XCD's runs band by band
     const int h = band > 0 ? std::min(band, tiles_m) : choose_band(tiles_m, smax);

@@ -55,8 +55,9 @@ def test_schedule_matches_oracle(lib, tm, tn, slots):
     T = tm * tn
     band = osched.band_cost_choice(tm, max(slots))
     # aware: every band apportioned by Hamilton's method, lists band by band
+    # (or whole blocks dealt round-robin where a band is shorter than a round)
     order, off, quota = asym.schedule_build(tm, tn, slots, asym.MAP_AWARE)
-    lists = osched.aware_lists(tm, tn, slots, band)
+    lists = osched.aware_lists_auto(tm, tn, slots)
     assert quota == [len(lst) for lst in lists]
     assert order == [t for lst in lists for t in lst]
     assert off[0] == 0 and all(off[x + 1] - off[x] == quota[x] for x in range(len(slots)))
@@ -111,6 +112,31 @@ def test_aware_wave_blocks_are_compact():
     for x in range(8):
         mine = [t for t in first_wave if own[t] == x]
         assert len({t // 32 for t in mine}) + len({t % 32 for t in mine}) == 33
+
+
+def test_one_round_grid_deals_compact_blocks():
+    # 4096x4096 at 256^2 tiles (16 x 16 tiles, one round of 8 x 32 workers): an
+    # 8-row band holds 128 tiles, fewer than the 256 workers, so every XCD gets
+    # one whole 8 x 4 block (12 panels) instead of two 8 x 2 strips (18)
+    order, off, quota = asym.schedule_build(16, 16, [32] * 8, asym.MAP_AWARE)
+    assert quota == [32] * 8
+    blocks = set()
+    for x in range(8):
+        mine = order[off[x]:off[x + 1]]
+        rows = {t // 16 for t in mine}
+        cols = {t % 16 for t in mine}
+        assert len(rows) == 8 and len(cols) == 4 and max(cols) - min(cols) == 3
+        blocks.add((min(rows), min(cols)))
+    assert blocks == {(r, c) for r in (0, 8) for c in (0, 4, 8, 12)}
+    # block k (band by band, left to right) on XCD k mod 8
+    assert [min(order[off[x]:off[x + 1]]) for x in range(8)] == [0, 4, 8, 12, 128, 132, 136, 140]
+    # the band runs stay where a band holds a whole round (8192^3) or the
+    # counts are unequal
+    assert osched.block_deal_lists(32, 32, [32] * 8, 8) is None
+    assert osched.block_deal_lists(16, 16, [16, 10, 22, 16, 13, 19, 16, 16], 4) is None
+    # an explicit band keeps the band runs
+    order_b, _, _ = asym.schedule_build(16, 16, [32] * 8, asym.MAP_AWARE, band=8)
+    assert order_b == [t for lst in osched.aware_lists(16, 16, [32] * 8, 8) for t in lst]
 
 
 @pytest.mark.parametrize("args", [
