@@ -622,10 +622,10 @@ __device__ __forceinline__ void compute_tile_ring(const Params& pin, int tile, u
   // 4c .. 4c+3, c = lane / 16.  Blocks 2q and 2q+1 are paired by one
   // v_permlane16_swap per packed word, after which lane (r, c) holds 8
   // consecutive columns, 8 (c >> 1) .. +7 of block 2q + (c & 1): one 16-byte
-  // store per lane covers 16 rows x 32 columns, and the pairs of a 16-row block
-  // go out back to back, so every 128-byte line of C is written by four
-  // consecutive stores.  An odd last block (224-wide tiles) keeps the 8-byte
-  // layout.  Offsets: the lane's own one is a VGPR, the block's is uniform
+  // store per lane covers 16 rows x 32 columns (64 bytes of each row), so two
+  // stores, pairs q and q+1, fill a 128-byte line of C.  The order of the
+  // stores and their cache policy depend on the tile width (below).  An odd
+  // last block (224-wide tiles) keeps the 8-byte layout.  Offsets: the lane's own one is a VGPR, the block's is uniform
   // (scalar offset).  Rows past M fall outside the resource: stores dropped.
   // (the inputs pass through an opaque move so that nothing below is hoisted
   // out of the tile loop and kept live across the k-loop)
