@@ -110,6 +110,136 @@ def cpu_baseline(A, B, rows: int, C_gpu=None):
     return out, parity
 
 
+def full_parity(A, B, C_gpu) -> dict:
+    """Every output of one GPU product against the oracle (same gate as the
+    CPU-baseline leg): max |C - R32| / max(|R32|, rms(R32)) over all elements,
+    and the share bitwise equal to the oracle's rounded output."""
+    import numpy as np
+    import torch
+
+    import oracle
+    bits = lambda t: t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    t0 = time.perf_counter()
+    R, Co = oracle.gemm_bf16(bits(A), bits(B), "nk", want_r32=True)
+    dt = time.perf_counter() - t0
+    Cg = bits(C_gpu)
+    g = (Cg.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    r = R.astype(np.float64)
+    rms = float(np.sqrt(np.mean(r * r)))
+    err = float(np.max(np.abs(g - r) / np.maximum(np.abs(r), rms)))
+    return {"elements": int(Cg.size), "max_rel_err": float(f"{err:.4e}"), "gate": 2e-2, "pass": err <= 2e-2,
+            "bitwise_equal_to_oracle_frac": round(float(np.mean(Cg == Co)), 5), "oracle_s": round(dt, 2)}
+
+
+def config_parity(topo, dev, stream) -> dict:
+    """Full-output parity of every configuration's product, each launched the
+    way the studies time it: 512^3, the three decoder shapes (full GPU, aware);
+    prefill 8192x4096x4096 || decode 32x14336x4096 co-running on CU-striped
+    sets; 4096^3 on the first seeded random 128-CU set beside the 64 MiB copy
+    tenant (whose copy is checked too).  The 8192^3 headline is checked in the
+    CPU-baseline leg."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    out = {}
+    for p in (workloads.SQUARE_512,) + tuple(workloads.LLM_SHAPES):
+        A, B = workloads.make_inputs(p)
+        C = asym.gemm(A.to(dev), B.to(dev), topo=topo, stream=stream)
+        torch.cuda.synchronize()
+        out[p.name] = full_parity(A, B, C)
+    (pa, pb), (da, db) = workloads.make_pd_inputs()
+    pad, pbd, dad, dbd = pa.to(dev), pb.to(dev), da.to(dev), db.to(dev)
+    cp = torch.empty((pa.shape[0], pb.shape[0]), dtype=torch.bfloat16, device=dev)
+    cd = torch.empty((da.shape[0], db.shape[0]), dtype=torch.bfloat16, device=dev)
+    prefill = topo.cuset(192, asym.CUSET_STRIPED)
+    decode = [b for b in range(256) if b not in set(prefill)]
+    asym.corun([asym.gemm_task(pad, pbd, cp, 1, "aware", mask=prefill),
+                asym.gemm_task(dad, dbd, cd, 3, "aware", mask=decode)], topo)
+    out["prefill_8192x4096x4096_striped_corun"] = full_parity(pa, pb, cp)
+    out["decode_32x14336x4096_striped_corun"] = full_parity(da, db, cd)
+    del pad, pbd, dad, dbd, cp, cd
+    A, B = workloads.make_inputs(workloads.COLOC)
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
+    src = workloads.copy_source(workloads.COPY_BYTES // 2).to(dev)
+    dst = torch.zeros_like(src)
+    m = workloads.random_mask_bits(workloads.COLOC.seed, 1, 128)[0]
+    comp = [b for b in range(256) if b not in set(m)]
+    asym.corun([asym.gemm_task(Ad, Bd, C, 3, "aware", mask=m), asym.copy_task(dst, src, 8, mask=comp)], topo)
+    out["coloc_4096_random_set_copy_corun"] = full_parity(A, B, C)
+    out["coloc_4096_random_set_copy_corun"]["copy_tenant_exact"] = bool(torch.equal(dst, src))
+    out["all_pass"] = all(v["pass"] for v in out.values() if isinstance(v, dict)) and \
+        out["coloc_4096_random_set_copy_corun"]["copy_tenant_exact"]
+    return out
+
+
+def clock_power(summ: dict, achieved_tflops: float) -> dict:
+    """The sampler's figures and the MFMA fraction at the measured clock:
+    achieved / (256 CUs x 4096 flop/clk x sclk)."""
+    out = dict(summ)
+    f = summ.get("sclk_mhz_mean")
+    out["pct_peak_at_measured_clock"] = round(100.0 * achieved_tflops / (256 * 4096 * f * 1e6 / 1e12), 2) \
+        if f else None
+    return out
+
+
+class ClockPowerSampler:
+    """Shader clock and socket power read from the driver's hwmon files of the
+    GPU's PCI function, sampled by a thread every `period` seconds while it
+    runs (no GPU call).  Fields that cannot be read stay None."""
+
+    def __init__(self, pci_bus_id: str, period: float = 0.02):
+        import glob
+        import threading
+        self.period = period
+        self.files = {}
+        for d in sorted(glob.glob(f"/sys/bus/pci/devices/{pci_bus_id}/hwmon/hwmon*")):
+            for name in ("power1_average", "power1_input", "freq1_input", "power1_cap"):
+                f = os.path.join(d, name)
+                if os.path.exists(f) and name not in self.files:
+                    self.files[name] = f
+        self.samples = {k: [] for k in self.files}
+        self._stop = threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self, name):
+        try:
+            with open(self.files[name]) as f:
+                return float(f.read().split()[0])
+        except (OSError, ValueError, IndexError):
+            return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            for k in self.files:
+                if k == "power1_cap":
+                    continue
+                v = self._read(k)
+                if v is not None:
+                    self.samples[k].append(v)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._t.join()
+
+    def summary(self) -> dict:
+        mean = lambda v: sum(v) / len(v) if v else None
+        pw = self.samples.get("power1_average") or self.samples.get("power1_input") or []
+        fr = self.samples.get("freq1_input") or []
+        cap = self._read("power1_cap") if "power1_cap" in self.files else None
+        return {"sclk_mhz_mean": round(mean(fr) / 1e6, 1) if fr else None,
+                "power_w_mean": round(mean(pw) / 1e6, 1) if pw else None,
+                "power_cap_w": round(cap / 1e6, 1) if cap else None,
+                "samples": len(fr) or len(pw),
+                "source": ", ".join(sorted(self.files)) or "no hwmon file readable"}
+
+
 def settle(fns, seconds: float):
     """Untimed launches, round-robin over fns, for `seconds` of wall time: the
     chip's clock and power state move for a second or more after a burst of
@@ -259,18 +389,22 @@ def prefill_decode(topo, dev, iters: int, halves):
 READ_TENANT_PASSES = 100   # about 27 ms at 4 TB/s: longer than 20 GEMM launches beside it
 
 
-def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gemm"):
+def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "copy", repeats: int = 5):
     """GEMM 4096^3 (uniform[-1,1], seed 4) on 128-CU sets: n_masks seeded random
     choices of 128 mask bits (what a topology-oblivious allocator hands out) and
     the two whole-XCD halves (the measured affinity groups; each side lends the
-    other one CU per XCD and works only on its own XCDs).  A second
-    tenant, the same GEMM with three times the launches, runs on the
-    complementary 128 CUs (tenant "gemm"), or the bandwidth-bound reader making
-    READ_TENANT_PASSES passes of a 1 GiB buffer (tenant "read"), kept to its own
-    XCDs on the aligned halves.  Per-set TFLOP/s of the measured GEMM for each
-    mapping, the max/min spread over the random sets, in how many runs the
-    tenant ended after the GEMM (so that it ran beside every launch), and the
-    same GEMM alone on the first random set and on the halves."""
+    other one CU per XCD and works only on its own XCDs).  A second tenant runs
+    on the complementary 128 CUs: the 64 MiB bf16 streaming copy (tenant
+    "copy", Section 7.3's co-located tenant; its pass count is set from solo
+    runs so that it outlasts the GEMM), the same GEMM with three times the
+    launches ("gemm"), or the whole-buffer reader making READ_TENANT_PASSES
+    passes of 1 GiB ("read"), kept to its own XCDs on the aligned halves.
+    Each (set, mapping) is co-run `repeats` times in a row and its median
+    TFLOP/s kept; reported per mapping: the median, min and max of the per-set
+    medians and their max/min spread, the largest max/min within one set's
+    repeats, in how many runs the tenant ended after the GEMM (so that it ran
+    beside every launch), and the GEMM alone on the first random set and on
+    the halves (median of the repeats)."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -280,13 +414,31 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gem
     C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
     C2 = torch.empty_like(C)
     rbuf = torch.ones(256 << 20, dtype=torch.float32, device=dev) if tenant == "read" else None
+    src = workloads.copy_source(workloads.COPY_BYTES // 2).to(dev) if tenant == "copy" else None
+    dst = torch.empty_like(src) if tenant == "copy" else None
     masks = workloads.random_mask_bits(workloads.COLOC.seed, n_masks, 128)
+    med = lambda v: sorted(v)[len(v) // 2]
+    copy_passes = 0
+    if tenant == "copy":
+        # passes: 2x the solo GEMM's time over the slowest solo copy pass on a complement
+        m0 = masks[0]
+        g_ms = max(asym.corun([asym.gemm_task(Ad, Bd, C, iters, mp, mask=m0)], topo)[0]["ms_total"]
+                   for mp in MAPPINGS)
+        c_ms = 0.0
+        for m in masks[:4]:
+            comp = [b for b in range(256) if b not in set(m)]
+            c_ms = max(c_ms, asym.corun([asym.copy_task(dst, src, 10, mask=comp)], topo)[0]["ms_per_iter"])
+        copy_passes = max(10, int(2.0 * g_ms / max(c_ms, 1e-3)) + 1)
 
     def other(cus, xm=0):
         if tenant == "read":
             return asym.read_task(rbuf, READ_TENANT_PASSES, mask=cus, xcd_mask=xm)
+        if tenant == "copy":
+            return asym.copy_task(dst, src, copy_passes, mask=cus, xcd_mask=xm)
         return asym.gemm_task(Ad, Bd, C2, 3 * iters, "aware", mask=cus, xcd_mask=xm)
     per = {m: [] for m in MAPPINGS}
+    within = {m: 1.0 for m in MAPPINGS}
+    tenant_rate = []
     counts = []
     runs, covered = 0, 0
 
@@ -295,38 +447,53 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "gem
         nonlocal runs, covered
         runs += 1
         covered += r[1]["ms_total"] >= r[0]["ms_total"]
+    # settle: one untimed co-run on the first set
+    comp0 = [b for b in range(256) if b not in set(masks[0])]
+    asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=masks[0]), other(comp0)], topo)
     for i, m in enumerate(masks):
         comp = [b for b in range(256) if b not in set(m)]
         counts.append(topo.cuset_counts(m))
         for mapping in MAPPINGS:
-            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m), other(comp)], topo)
-            if i == 0 and not per[mapping]:
-                # the first set is run twice: its first run settles the clock
+            v = []
+            for _ in range(repeats):
                 r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mapping, mask=m), other(comp)], topo)
-            per[mapping].append(r[0]["tflops"])
-            cover(r)
+                v.append(r[0]["tflops"])
+                if tenant != "gemm":
+                    tenant_rate.append(r[1]["gbps"])
+                cover(r)
+            per[mapping].append(med(v))
+            within[mapping] = max(within[mapping], max(v) / min(v))
     m0 = masks[0]
-    alone = {mp: round(asym.corun([asym.gemm_task(Ad, Bd, C, iters, mp, mask=m0)], topo)[0]["tflops"], 2)
-             for mp in MAPPINGS}
-    aligned, aligned_read, aligned_alone = [], [], []
+    alone = {mp: round(med([asym.corun([asym.gemm_task(Ad, Bd, C, iters, mp, mask=m0)], topo)[0]["tflops"]
+                            for _ in range(repeats)]), 2) for mp in MAPPINGS}
+    aligned, aligned_rate, aligned_alone, aligned_within = [], [], [], []
     for xm in halves:
         ma, mb = topo.cuset_split_xcds(xm)
-        aligned_alone.append(round(asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm)],
-                                              topo)[0]["tflops"], 2))
-        r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
-                        other(mb, 0xFF & ~xm)], topo)
-        aligned.append(round(r[0]["tflops"], 2))
-        aligned_read.append(round(r[1]["gbps"], 1))
-        cover(r)
-    summ = {"tenant": tenant, "n_random_sets": n_masks, "iters": iters, "aligned_aware_tflops": aligned,
-            **({"aligned_reader_GBps": aligned_read} if tenant == "read" else {}),
+        aligned_alone.append(round(med([asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma,
+                                                                   xcd_mask=xm)], topo)[0]["tflops"]
+                                        for _ in range(repeats)]), 2))
+        v, rate = [], []
+        for _ in range(repeats):
+            r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, "aware", mask=ma, xcd_mask=xm),
+                            other(mb, 0xFF & ~xm)], topo)
+            v.append(r[0]["tflops"])
+            rate.append(r[1]["gbps"])
+            cover(r)
+        aligned.append(round(med(v), 2))
+        aligned_within.append(round(max(v) / min(v), 4))
+        aligned_rate.append(round(med(rate), 1))
+    summ = {"tenant": tenant, "n_random_sets": n_masks, "iters": iters, "repeats_per_set": repeats,
+            **({"copy_passes": copy_passes, "copy_bytes": workloads.COPY_BYTES} if tenant == "copy" else {}),
+            "aligned_aware_tflops": aligned, "aligned_within_set_max_min": aligned_within,
+            **({"aligned_tenant_GBps": aligned_rate,
+                "random_tenant_GBps_median": round(med(tenant_rate), 1)} if tenant != "gemm" else {}),
             "tenant_outlasted_gemm": f"{covered}/{runs}",
             "alone_tflops": {"first_random_set": alone, "aligned_halves_aware": aligned_alone},
             "random_set_min_max_cus_per_xcd": [min(min(c) for c in counts), max(max(c) for c in counts)]}
     for mapping, v in per.items():
-        summ[f"random_{mapping}"] = {"min": round(min(v), 2), "max": round(max(v), 2),
+        summ[f"random_{mapping}"] = {"median": round(med(v), 2), "min": round(min(v), 2), "max": round(max(v), 2),
                                      "spread": round(max(v) / min(v), 4),
-                                     "median": round(sorted(v)[len(v) // 2], 2)}
+                                     "within_set_max_min": round(within[mapping], 4)}
     return summ
 
 
@@ -610,13 +777,18 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa,attention",
+    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa,attention,parity",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
-                         "remote read bandwidth), attention (decode attention); 'none' for the "
-                         "headline only")
+                         "remote read bandwidth), attention (decode attention), parity (every "
+                         "configuration's product against the oracle, all outputs); 'none' for "
+                         "the headline only")
     ap.add_argument("--spread-masks", type=int, default=32)
+    ap.add_argument("--spread-tenants", default="copy",
+                    help="comma list of tenants for the CU-set spread study: copy (the 64 MiB "
+                         "streaming copy), gemm (a second GEMM), read (a whole-buffer reader)")
+    ap.add_argument("--spread-repeats", type=int, default=5)
     ap.add_argument("--focus", choices=FOCUS, default=None,
                     help="run only this workload (profiling runs); prints its own JSON line")
     ap.add_argument("--mapping-only", default=None,
@@ -675,8 +847,11 @@ def main() -> int:
     plan = asym.gemm_plan(Ad, Bd, C, mapping=head_mapping, topo=topo, stream=stream)
     for _ in range(args.warmup):
         head()
-    settle([head], args.settle)
-    total_ms, per_launch_ms = time_launches(head, args.steps, stream)
+    dinfo = asym.device_query(0)
+    sampler = ClockPowerSampler(dinfo["pci_bus_id"])
+    with sampler:
+        settle([head], args.settle)
+        total_ms, per_launch_ms = time_launches(head, args.steps, stream)
     ms_per_step = total_ms / args.steps
     tflops = p.flops / (ms_per_step * 1e-3) / 1e12
     achieved = p.flops / (per_launch_ms * 1e-3) / 1e12
@@ -698,6 +873,8 @@ def main() -> int:
                                f"full GPU, {head_mapping} persistent mapping, topology probe first",
                    "M": p.M, "N": p.N, "K": p.K, "mapping": head_mapping, "plan": plan},
         "pct_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
+        "clock_power": clock_power(sampler.summary(), achieved),
+        "device": {k: dinfo[k] for k in ("arch", "pci_bus_id", "compute_partition", "memory_partition")},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic()},
@@ -725,8 +902,9 @@ def main() -> int:
     if "pd" in studies:
         line["prefill_decode"] = prefill_decode(topo, dev, 10, halves)
     if "spread" in studies:
-        line["cu_set_spread"] = spread_study(topo, dev, args.spread_masks, 20, halves)
-        line["cu_set_spread_read_tenant"] = spread_study(topo, dev, args.spread_masks, 20, halves, "read")
+        for tenant in args.spread_tenants.split(","):
+            key = "cu_set_spread" if tenant == "copy" else f"cu_set_spread_{tenant}_tenant"
+            line[key] = spread_study(topo, dev, args.spread_masks, 20, halves, tenant, args.spread_repeats)
     if "grouped" in studies:
         line["grouped_gemm"] = grouped_study(dev, stream, range(1, 6), 8, 5)
     if "attention" in studies:
@@ -745,6 +923,8 @@ def main() -> int:
         cpu, parity = cpu_baseline(A, B, args.cpu_rows, C.cpu())
         line["cpu_baseline"] = {k: (round(v, 6) if isinstance(v, float) else v) for k, v in cpu.items()}
         line["parity_vs_oracle"] = parity
+        if args.probe != "identity" and "parity" in studies:
+            line["config_parity"] = config_parity(topo, dev, stream)
     print(json.dumps(line), flush=True)
     return 0
 

@@ -52,7 +52,9 @@ typedef enum asym_status {
   ASYM_EUNSUPPORTED = -3, /* valid request the library or device cannot serve */
   ASYM_ETIMEOUT = -4,     /* a watched device wait did not finish in time */
   ASYM_EINVARIANT = -5,   /* a topology map violates its exact invariants */
-  ASYM_ENOMEM = -6        /* host or device allocation failed */
+  ASYM_ENOMEM = -6,       /* host or device allocation failed */
+  ASYM_ENOCACHE = -7      /* no usable topology cache: missing, made on another chip
+                             or configuration, lacking a requested probe, or malformed */
 } asym_status;
 
 /* Tile-to-compute-unit mappings of the persistent GEMM (Section 7.1). */
@@ -76,7 +78,8 @@ typedef enum asym_mapping {
 /* Storage of the B operand of C = A . B. */
 typedef enum asym_b_layout {
   ASYM_B_NK = 0, /* B stored transposed, [N][ldb] row-major, K contiguous */
-  ASYM_B_KN = 1  /* B stored [K][ldb] row-major (not served: ASYM_EUNSUPPORTED) */
+  ASYM_B_KN = 1  /* B stored [K][ldb] row-major, N contiguous: transposed first
+                    (an exact copy into a library buffer), then as ASYM_B_NK */
 } asym_b_layout;
 
 /* What asym_probe_topology measures. */
@@ -95,7 +98,9 @@ typedef enum asym_cuset_policy {
   ASYM_CUSET_RANDOM = 3            /* seeded uniform choice among free CUs */
 } asym_cuset_policy;
 
-/* Device and partition-mode discovery. */
+/* Device and partition-mode discovery (Section 5.2: topology differs between
+ * chips of one product and between configurations, so every probe result is
+ * tied to the chip and mode it was measured on). */
 typedef struct asym_device_info {
   int n_cus;          /* hipDeviceAttributeMultiprocessorCount */
   int n_xccs;         /* hipDeviceAttributeNumberOfXccs */
@@ -106,6 +111,14 @@ typedef struct asym_device_info {
   int l2_bytes;       /* per XCD as reported by the runtime */
   size_t hbm_bytes;
   char arch[64];      /* gcnArchName, e.g. "gfx950:sramecc+:xnack-" */
+  char pci_bus_id[32];         /* "dddd:bb:dd.f", lower case */
+  char uuid[40];               /* the runtime's device UUID, 32 hex digits */
+  int runtime_version;         /* hipRuntimeGetVersion */
+  int driver_version;          /* hipDriverGetVersion */
+  char compute_partition[16];  /* the driver's current compute partition mode
+                                  (e.g. "SPX", "CPX"), "unknown" if not readable */
+  char memory_partition[16];   /* current memory partition mode (e.g. "NPS1"),
+                                  "unknown" if not readable */
 } asym_device_info;
 
 typedef struct asym_topology asym_topology; /* opaque, library-owned */
@@ -165,12 +178,26 @@ typedef struct asym_latency_summary {
 } asym_latency_summary;
 
 /* ---- device discovery -------------------------------------------------- */
-/* Fill *out from the HIP runtime.  Errors: ASYM_EINVAL (null out),
- * ASYM_EHIP. */
+/* Fill *out from the HIP runtime; the partition modes come from the driver's
+ * sysfs files of the device's PCI function (current_compute_partition,
+ * current_memory_partition), "unknown" where they cannot be read.
+ * Errors: ASYM_EINVAL (null out, no such device), ASYM_EHIP. */
 int asym_device_query(int device, asym_device_info* out);
+
+/* The key a probe result of `device` is cached under: one line naming the
+ * PCI bus id, UUID, runtime and driver versions, architecture, compute and
+ * memory partition modes and CU / XCD counts (Section 5.2: topology is per
+ * chip and per configuration).  *needed (nullable) receives the length + 1.
+ * Errors: ASYM_EINVAL (null or short buffer), ASYM_EHIP. */
+int asym_topology_cache_key(int device, char* buf, size_t len, size_t* needed);
 
 /* ---- topology probe (Section 5.1, Section 6.1, Appendix G) -------------- */
 /* Probe `device` and return a new topology map in *out.
+ * cache_path (nullable): a per-chip cache file.  If it holds a map made
+ * under this device's cache key (asym_topology_cache_key) with at least the
+ * requested probes, that map is returned without probing; otherwise the
+ * device is probed and the file is (re)written with the result (a failed
+ * write is not an error: the probed map is returned).
  * IDENTITY launches an oversubscribed kernel whose workgroups record
  * XCC_ID and HW_ID; the distinct (xcc, se, sh, cu) tuples, sorted, are the
  * CU records with dense indices 0..n-1.  MASKMAP launches the same kernel once
@@ -181,7 +208,24 @@ int asym_device_query(int device, asym_device_info* out);
  * counts summing to the device CU count, mask map a bijection); a violation
  * returns ASYM_EINVARIANT and no map.  Synchronous.
  * Errors: ASYM_EINVAL, ASYM_EHIP, ASYM_EINVARIANT, ASYM_ETIMEOUT. */
-int asym_probe_topology(int device, unsigned flags, asym_topology** out);
+int asym_probe_topology(int device, unsigned flags, const char* cache_path,
+                        asym_topology** out);
+
+/* Write `topo` to the cache file `path` (text: the key, the probes made,
+ * every CU record with its mask bit, the latency summary), replacing it
+ * atomically.  `key` (nullable) overrides the key the map was probed under
+ * (for maps built from records).  Host only.
+ * Errors: ASYM_EINVAL (null argument, unwritable path). */
+int asym_topology_save(const asym_topology* topo, const char* path, const char* key);
+
+/* Read a cache file written by asym_topology_save into a new map in *out,
+ * accepting it only if its key equals `key` and it holds every probe in
+ * `flags`; the map is checked against its exact invariants.  Host only.
+ * Errors: ASYM_EINVAL (null argument), ASYM_ENOCACHE (missing file, other
+ * key, missing probe, malformed file or broken invariant; the message says
+ * which). */
+int asym_topology_load(const char* path, const char* key, unsigned flags,
+                       asym_topology** out);
 
 /* Build a topology from raw identity records without a GPU (host only).
  * records: n_records rows of 4 int32 {xcc_id register, hw_id register,
@@ -499,8 +543,13 @@ int asym_grouped_schedule_build(int G, const int* tiles_m, int tiles_n, int n_xc
 /* ---- persistent bf16 GEMM (Section 7.1) --------------------------------- */
 /* C = A . B, bf16 inputs, fp32 accumulation, bf16 round-to-nearest-even
  * output.  A: [M][lda] row-major.  B: ASYM_B_NK, [N][ldb] row-major (the
- * logical B is its transpose).  C: [M][ldc] row-major.  Requires M, N, K >= 1,
- * lda >= K, ldb >= K, ldc >= N; 16-byte aligned pointers with lda, ldb, K
+ * logical B is its transpose; ldb >= K), or ASYM_B_KN, [K][ldb] row-major
+ * (ldb >= N): then B is first transposed, an exact copy on `stream` into a
+ * per-stream library buffer of N x K bf16 (grown after a stream
+ * synchronisation when a call needs more), and the product runs as for
+ * ASYM_B_NK, so both layouts of one logical B give bitwise the same C.
+ * C: [M][ldc] row-major.  Requires M, N, K >= 1,
+ * lda >= K, ldc >= N; 16-byte aligned pointers with lda, ldb, K
  * multiples of 8 and ldc a multiple of 4 take the vector path, anything else a
  * slower fully predicated path.  The CU set scheduled for is the stream's CU
  * mask (hipExtStreamGetCUMask) restricted to the XCDs in xcd_mask (bit x =
@@ -508,7 +557,11 @@ int asym_grouped_schedule_build(int G, const int* tiles_m, int tiles_n, int n_xc
  * NULL (a per-device identity probe made on first use is taken); a stream
  * with a partial CU mask needs a topology with a mask map.  Accumulation order
  * differs from a sequential sum but not between mappings: results are bitwise
- * identical across mappings, CU masks and runs.  Asynchronous on `stream`.
+ * identical across mappings, CU masks and runs.  (One exception: a product of
+ * at most 64 rows whose K the small-M kernel splits on the whole set runs on
+ * the persistent kernel under a whole-XCD restriction, and the two fp32 sums
+ * may differ in their last bits; see asym_gemm_set_small_m.)  Asynchronous on
+ * `stream`.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K,
                    const void* A, int lda, const void* B, int ldb,
@@ -561,6 +614,8 @@ typedef struct asym_gemm_plan_info {
                       than the device has CUs: K is cut into this many ranges, one
                       workgroup each, and a second launch adds the fp32 partial
                       tiles in range order (1 = no split) */
+  int b_transposed; /* 1: B is stored [K][N] and is transposed into the
+                       library's per-stream buffer before the product */
 } asym_gemm_plan_info;
 
 int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
@@ -585,7 +640,7 @@ int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
  * previous setting.  Not synchronised with launches in flight. */
 int asym_gemm_set_small_m(int enable);
 
-/* ---- decode attention (Section 7.1 attention workloads, decode; Appendix E) */
+/* ---- decode attention (Section 7.1 attention workloads, decode; Appendix F) */
 /* One query token per request against cached keys and values, with grouped
  * key/value heads: for request b and query head h, with g = h / (H_q / H_kv),
  *   O[b][h] = softmax_t(scale * q[b][h] . K[b][g][t]) . V[b][g][t]
@@ -629,28 +684,39 @@ int asym_attn_decode_plan(const asym_topology* topo, int B, int H_q, int H_kv, i
                           asym_attn_plan_info* out);
 
 /* ---- streaming copy and co-run (Sections 7.2, 7.3) ---------------------- */
-/* dst[i] = src[i] for n_bytes bytes (16-byte aligned, n_bytes a multiple of
- * 16), `passes` times over the buffer, with 16-byte accesses from every lane.
- * If stop_flag (device int, nullable) becomes nonzero the kernel ends after
- * the pass in progress; it always ends after `passes` passes.  On XCDs outside
- * xcd_mask (0 = all) workgroups exit at once.  Asynchronous.
- * Errors: ASYM_EINVAL, ASYM_EHIP. */
-int asym_copy_bf16(void* dst, const void* src, size_t n_bytes, int passes,
-                   const int* stop_flag, uint32_t xcd_mask, void* stream);
+/* The bandwidth-bound tenant of the co-location study (Section 7.3 runs a
+ * second tenant on the complementary units): dst[i] = src[i] for n_bytes
+ * bytes, `passes` times over the buffer, with 16-byte accesses from every lane
+ * (non-temporal).  dst and src: caller-owned device buffers, 16-byte aligned,
+ * not overlapping; n_bytes a nonzero multiple of 16, below 2^40; passes >= 1.
+ * The CU set is the stream's CU mask restricted to the XCDs in xcd_mask
+ * (0 = all), as for asym_gemm_bf16 (topo NULL: the per-device identity probe;
+ * a partial mask needs a topology with a mask map; a mask that leaves an XCD
+ * without a CU is refused).  The buffer is cut into one slice per XCD of the
+ * set, in proportion to its CUs there, copied by the workgroups the hardware
+ * deals to that XCD; workgroups on XCDs outside xcd_mask exit at once.  No
+ * atomics, no barriers: the copy always ends after `passes` passes.  If
+ * stop_flag (a device int, nullable) is nonzero when a wave starts a pass
+ * after its first, that wave ends there (it never extends the copy).
+ * Asynchronous on `stream`.
+ * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
+int asym_copy_bf16(const asym_topology* topo, void* dst, const void* src, size_t n_bytes,
+                   int passes, const int* stop_flag, uint32_t xcd_mask, void* stream);
 
 /* One task of a co-run: a GEMM or a streaming copy on its own CU set. */
 typedef struct asym_task {
   int kind;        /* 0 = GEMM, 1 = streaming copy, 2 = read (whole-buffer reader) */
   uint32_t mask[ASYM_MASK_WORDS]; /* CU-mask bits; all-zero = all CUs */
   uint32_t xcd_mask;              /* whole-XCD restriction, 0 = none */
-  int iters;       /* GEMM launches, or copy / read passes (reads: >= 1) */
+  int iters;       /* GEMM launches, or copy / read passes (>= 1) */
   int mapping;     /* GEMM mapping */
   int M, N, K;     /* GEMM shape, dense row-major A, B ([N][K]), C */
   const void* A; const void* B; void* C;
-  const void* src; void* dst; size_t n_bytes; /* copy; read: src and n_bytes
-                                                 (a multiple of 16, < 2^40) */
-  int grid;        /* read: workgroups; 0 = 8 per CU of the reading XCD with the
-                      most CUs, times the XCD count */
+  const void* src; void* dst; size_t n_bytes; /* copy: both (16-byte aligned,
+                                                 not overlapping); read: src; n_bytes
+                                                 a multiple of 16, < 2^40 */
+  int grid;        /* copy / read: workgroups; 0 = 8 per CU of the XCD of its set
+                      with the most CUs, times the XCD count */
 } asym_task;
 
 typedef struct asym_task_result {
@@ -665,18 +731,19 @@ typedef struct asym_task_result {
 } asym_task_result;
 
 /* Run tasks concurrently, each on its own stream (masked streams for partial
- * masks, unmasked streams with XCD filtering for whole-XCD sets).  All tasks
- * are released together; a copy task with iters <= 0 runs until every GEMM
- * task has finished (bounded at 100000 passes).  A read task makes `iters`
- * passes of a whole-buffer reader (16-byte loads, bounded, no atomics): the
- * bandwidth-bound tenant of the co-location study.  The buffer is cut into one
- * slice per reading XCD, in proportion to the task's CUs there, and read by
- * the workgroups that XCD is dealt.  A read task's xcd_mask keeps its reads
- * on those XCDs (workgroups elsewhere, e.g. on CUs its mask lends it there,
- * leave at once).  Every GEMM task is launched once, untimed, before the
- * release, so that its one-time setup (workspace, schedule upload) does not
- * wait for tasks already running.
- * Synchronous.
+ * masks, unmasked streams with XCD filtering for whole-XCD sets; Sections
+ * 7.2 and 7.3).  All tasks are released together.  A copy task makes `iters`
+ * passes of asym_copy_bf16 over its buffers and a read task `iters` passes of
+ * a whole-buffer reader (16-byte loads, no atomics); both cut their buffer
+ * into one slice per XCD of their set, in proportion to their CUs there, and
+ * an xcd_mask keeps their work on those XCDs (workgroups elsewhere, e.g. on
+ * CUs a split mask lends them there, leave at once).  No task is open-ended:
+ * a tenant that ran until the GEMMs ended could deadlock with a persistent
+ * GEMM whose workgroups dealt to the tenant's XCDs wait for its CUs, so a
+ * copy task with iters < 1 is refused; size the passes to outlast the GEMMs.
+ * Every GEMM task is launched once, untimed, before the release, so that its
+ * one-time setup (workspace, schedule upload) does not wait for tasks already
+ * running.  Synchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_corun(const asym_topology* topo, const asym_task* tasks, int n_tasks,
                asym_task_result* out);

@@ -2,7 +2,7 @@
 
 Section 7.1 runs attention kernels (multi-head and grouped-query attention) as
 full-GPU workloads, decode being one query token per request against a cached
-key/value sequence (Appendix E: S_q = 1, head dimension 128, 32 key/value
+key/value sequence (Appendix F: S_q = 1, head dimension 128, 32 key/value
 heads for multi-head and 8 for grouped-query attention).  What the kernel
 computes is the plain definition, written out here in float64 with numpy:
 

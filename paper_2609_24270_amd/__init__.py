@@ -22,7 +22,7 @@ MASK_WORDS = 8
 MAX_XCDS = 16
 MAX_CUS = MASK_WORDS * 32
 
-OK, EINVAL, EHIP, EUNSUPPORTED, ETIMEOUT, EINVARIANT, ENOMEM = 0, -1, -2, -3, -4, -5, -6
+OK, EINVAL, EHIP, EUNSUPPORTED, ETIMEOUT, EINVARIANT, ENOMEM, ENOCACHE = 0, -1, -2, -3, -4, -5, -6, -7
 MAP_AWARE, MAP_OBLIVIOUS_GROUPED, MAP_OBLIVIOUS_ROWMAJOR = 0, 1, 2
 MAPPINGS = {"aware": MAP_AWARE, "oblivious_grouped": MAP_OBLIVIOUS_GROUPED,
             "oblivious_rowmajor": MAP_OBLIVIOUS_ROWMAJOR}
@@ -32,7 +32,8 @@ CUSET_XCD_ALIGNED, CUSET_AFFINITY_ALIGNED, CUSET_STRIPED, CUSET_RANDOM = 0, 1, 2
 
 # Every function the C ABI exports (include/asym.h), in declaration order.
 EXPORTS = (
-    "asym_device_query", "asym_probe_topology", "asym_topology_from_records",
+    "asym_device_query", "asym_topology_cache_key", "asym_probe_topology",
+    "asym_topology_save", "asym_topology_load", "asym_topology_from_records",
     "asym_topology_free", "asym_topology_info", "asym_topology_cu",
     "asym_topology_dispatch", "asym_topology_latency", "asym_topology_json",
     "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
@@ -57,7 +58,10 @@ class DeviceInfo(ctypes.Structure):
                 ("n_cus_physical", ctypes.c_int), ("clock_khz", ctypes.c_int),
                 ("wall_clock_khz", ctypes.c_int), ("lds_bytes_per_cu", ctypes.c_int),
                 ("l2_bytes", ctypes.c_int), ("hbm_bytes", ctypes.c_size_t),
-                ("arch", ctypes.c_char * 64)]
+                ("arch", ctypes.c_char * 64), ("pci_bus_id", ctypes.c_char * 32),
+                ("uuid", ctypes.c_char * 40), ("runtime_version", ctypes.c_int),
+                ("driver_version", ctypes.c_int), ("compute_partition", ctypes.c_char * 16),
+                ("memory_partition", ctypes.c_char * 16)]
 
 
 class LatencyParams(ctypes.Structure):
@@ -155,7 +159,8 @@ class GemmPlanInfo(ctypes.Structure):
                 ("grid", ctypes.c_int), ("workers", ctypes.c_int),
                 ("claims", ctypes.c_int), ("vector_path", ctypes.c_int),
                 ("n_xcds", ctypes.c_int), ("workers_per_xcd", ctypes.c_int * MAX_XCDS),
-                ("small_m", ctypes.c_int), ("k_splits", ctypes.c_int)]
+                ("small_m", ctypes.c_int), ("k_splits", ctypes.c_int),
+                ("b_transposed", ctypes.c_int)]
 
     def to_dict(self) -> dict:
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "workers_per_xcd"}
@@ -197,7 +202,10 @@ def load_library(path: str = LIB_PATH):
     topo_p = ctypes.c_void_p
     sig = {
         "asym_device_query": (i, [i, ctypes.POINTER(DeviceInfo)]),
-        "asym_probe_topology": (i, [i, ctypes.c_uint, ctypes.POINTER(topo_p)]),
+        "asym_topology_cache_key": (i, [i, cp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
+        "asym_probe_topology": (i, [i, ctypes.c_uint, cp, ctypes.POINTER(topo_p)]),
+        "asym_topology_save": (i, [topo_p, cp, cp]),
+        "asym_topology_load": (i, [cp, cp, ctypes.c_uint, ctypes.POINTER(topo_p)]),
         "asym_topology_from_records": (i, [ctypes.POINTER(ctypes.c_int32), i, i, i,
                                            ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(topo_p)]),
         "asym_topology_free": (None, [topo_p]),
@@ -240,7 +248,7 @@ def load_library(path: str = LIB_PATH):
         "asym_gemm_set_small_m": (i, [i]),
         "asym_attn_decode_bf16": (i, [topo_p, i, i, i, i, i, vp, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
         "asym_attn_decode_plan": (i, [topo_p, i, i, i, i, i, i, i, u32, vp, ctypes.POINTER(AttnPlanInfo)]),
-        "asym_copy_bf16": (i, [vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
+        "asym_copy_bf16": (i, [topo_p, vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
         "asym_corun": (i, [topo_p, ctypes.POINTER(Task), i, ctypes.POINTER(TaskResult)]),
         "asym_last_error": (cp, []),
         "asym_version": (i, []),
@@ -286,8 +294,19 @@ def device_query(device: int = 0) -> dict:
     info = DeviceInfo()
     _check(load_library().asym_device_query(device, ctypes.byref(info)))
     d = {k: getattr(info, k) for k, _ in DeviceInfo._fields_}
-    d["arch"] = info.arch.decode()
+    for k in ("arch", "pci_bus_id", "uuid", "compute_partition", "memory_partition"):
+        d[k] = getattr(info, k).decode()
     return d
+
+
+def topology_cache_key(device: int = 0) -> str:
+    """The key probe results of `device` are cached under (chip and mode)."""
+    lib = load_library()
+    need = ctypes.c_size_t()
+    lib.asym_topology_cache_key(device, None, 0, ctypes.byref(need))
+    buf = ctypes.create_string_buffer(max(1, need.value))
+    _check(lib.asym_topology_cache_key(device, buf, need.value, ctypes.byref(need)))
+    return buf.value.decode()
 
 
 # ---- topology -----------------------------------------------------------
@@ -373,15 +392,29 @@ class Topology:
         _check(load_library().asym_cuset_split_xcds(self._h, xcd_mask_a, a, b))
         return mask_bits(a), mask_bits(b)
 
+    def save(self, path: str, key: Optional[str] = None) -> None:
+        """Write the map to a cache file (key: override the probe's own)."""
+        _check(load_library().asym_topology_save(self._h, path.encode(), key.encode() if key else None))
+
     def cuset_counts(self, bits: Sequence[int]) -> list:
         per = (ctypes.c_int * MAX_XCDS)()
         _check(load_library().asym_cuset_counts(self._h, mask_words(bits), per))
         return list(per)[: self.info()["n_xcds"]]
 
 
-def probe_topology(device: int = 0, flags: int = PROBE_IDENTITY) -> Topology:
+def probe_topology(device: int = 0, flags: int = PROBE_IDENTITY, cache_path: Optional[str] = None) -> Topology:
+    """Probe `device` (or reuse the map in cache_path when it was made on this
+    chip and configuration with at least these probes; else probe and write it)."""
     h = ctypes.c_void_p()
-    _check(load_library().asym_probe_topology(device, flags, ctypes.byref(h)))
+    _check(load_library().asym_probe_topology(device, flags, cache_path.encode() if cache_path else None,
+                                              ctypes.byref(h)))
+    return Topology(h.value)
+
+
+def topology_load(path: str, key: str, flags: int = PROBE_IDENTITY) -> Topology:
+    """A map from a cache file, if made under `key` with at least `flags`."""
+    h = ctypes.c_void_p()
+    _check(load_library().asym_topology_load(path.encode(), key.encode(), flags, ctypes.byref(h)))
     return Topology(h.value)
 
 
@@ -606,23 +639,27 @@ def _stream_ptr(stream):
 # ---- GEMM -----------------------------------------------------------------------
 
 def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mask: int = 0,
-         stream=None):
-    """C = A . B^T for bf16 CUDA tensors A [M,K] and B [N,K] (B's [N][K] storage).
+         stream=None, b_layout: str = "nk"):
+    """C = A . B for bf16 CUDA tensors: A [M,K]; B [N,K] when b_layout is "nk"
+    (its [N][K] storage: C = A . B^T of the tensor), or [K,N] when "kn".
 
-    Launches the persistent HIP kernel asynchronously on `stream` (default:
-    torch's current stream) and returns C.
+    Launches the HIP kernels asynchronously on `stream` (default: torch's
+    current stream) and returns C.
     """
     import torch
     if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16:
         raise TypeError("A and B must be bfloat16")
-    if A.dim() != 2 or B.dim() != 2 or A.shape[1] != B.shape[1]:
-        raise ValueError("A must be [M,K] and B [N,K]")
+    if b_layout not in ("nk", "kn"):
+        raise ValueError("b_layout must be 'nk' or 'kn'")
+    kn = b_layout == "kn"
+    if A.dim() != 2 or B.dim() != 2 or A.shape[1] != B.shape[0 if kn else 1]:
+        raise ValueError("A must be [M,K] and B [K,N]" if kn else "A must be [M,K] and B [N,K]")
     if not (A.is_cuda and B.is_cuda):
         raise ValueError("A and B must be on the GPU")
     if A.stride(1) != 1 or B.stride(1) != 1:
-        raise ValueError("A and B must be K-contiguous")
+        raise ValueError("A and B must be row-major (unit stride in their last dimension)")
     M, K = A.shape
-    N = B.shape[0]
+    N = B.shape[1] if kn else B.shape[0]
     if C is None:
         C = torch.empty((M, N), dtype=torch.bfloat16, device=A.device)
     if C.dtype != torch.bfloat16 or C.shape != (M, N) or C.stride(1) != 1:
@@ -630,7 +667,7 @@ def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mas
     mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
     _check(load_library().asym_gemm_bf16(
         topo.handle if topo else None, M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0),
-        ctypes.c_void_p(B.data_ptr()), B.stride(0), B_NK, ctypes.c_void_p(C.data_ptr()),
+        ctypes.c_void_p(B.data_ptr()), B.stride(0), B_KN if kn else B_NK, ctypes.c_void_p(C.data_ptr()),
         C.stride(0), mp, xcd_mask, _stream_ptr(stream)))
     return C
 
@@ -732,14 +769,15 @@ def set_small_m(enable: bool) -> bool:
 
 def gemm_plan(A=None, B=None, C=None, mapping="aware", topo: Optional[Topology] = None,
               xcd_mask: int = 0, stream=None, M: Optional[int] = None, N: Optional[int] = None,
-              K: Optional[int] = None) -> dict:
+              K: Optional[int] = None, b_layout: str = "nk") -> dict:
     """What gemm() would launch for these operands (or, given M, N, K alone,
     for dense 256-byte-aligned operands of that shape): tile shape and grid,
     workers in all and per XCD, static or claiming aware form, vector or
     predicated path.  Launches nothing."""
+    kn = b_layout == "kn"
     if A is not None:
         M, K = A.shape
-        N = B.shape[0]
+        N = B.shape[1] if kn else B.shape[0]
         pa, lda = A.data_ptr(), A.stride(0)
         pb, ldb = B.data_ptr(), B.stride(0)
         if C is not None:
@@ -749,22 +787,27 @@ def gemm_plan(A=None, B=None, C=None, mapping="aware", topo: Optional[Topology] 
     else:
         if M is None or N is None or K is None:
             raise ValueError("give A and B, or M, N and K")
-        pa, lda, pb, ldb, pc, ldc = 256, K, 256, K, 256, N
+        pa, lda, pb, ldb, pc, ldc = 256, K, 256, (N if kn else K), 256, N
     mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
     out = GemmPlanInfo()
     _check(load_library().asym_gemm_plan(
         topo.handle if topo else None, M, N, K, ctypes.c_void_p(pa), lda, ctypes.c_void_p(pb),
-        ldb, B_NK, ctypes.c_void_p(pc), ldc, mp, xcd_mask, _stream_ptr(stream), ctypes.byref(out)))
+        ldb, B_KN if kn else B_NK, ctypes.c_void_p(pc), ldc, mp, xcd_mask, _stream_ptr(stream),
+        ctypes.byref(out)))
     return out.to_dict()
 
 
 # ---- copy and co-run --------------------------------------------------------------
 
-def copy(dst, src, passes: int = 1, stop_flag=None, xcd_mask: int = 0, stream=None):
+def copy(dst, src, passes: int = 1, stop_flag=None, xcd_mask: int = 0, stream=None,
+         topo: Optional["Topology"] = None):
+    """`passes` streaming copies of the CUDA tensor src into dst (same byte
+    size) on `stream`'s CU set; stop_flag: an int32 CUDA tensor or None."""
     n = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() != n:
         raise ValueError("size mismatch")
     _check(load_library().asym_copy_bf16(
+        topo.handle if topo else None,
         ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), n, passes,
         ctypes.c_void_p(stop_flag.data_ptr()) if stop_flag is not None else None, xcd_mask,
         _stream_ptr(stream)))
@@ -787,9 +830,11 @@ def gemm_task(A, B, C, iters: int, mapping="aware", mask=None, xcd_mask: int = 0
     return t
 
 
-def copy_task(dst, src, passes: int = 0, mask=None, xcd_mask: int = 0) -> Task:
+def copy_task(dst, src, passes: int, mask=None, xcd_mask: int = 0, grid: int = 0) -> Task:
+    """The streaming-copy tenant: `passes` copies of src into dst."""
     t = Task()
     t.kind = 1
+    t.grid = grid
     if mask is not None:
         m = mask_words(mask)
         for w in range(MASK_WORDS):

@@ -19,9 +19,10 @@ OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libasym.so")
 ARCH = "gfx950"
 
-SOURCES = ["capi.cpp", "topology.cpp", "schedule.cpp", "corun.cpp", "affinity.cpp",
+SOURCES = ["capi.cpp", "topology.cpp", "topology_cache.cpp", "schedule.cpp", "corun.cpp", "affinity.cpp",
            "interleave.cpp",
-           "gemm.hip", "gemm_skinny.hip", "attn_decode.hip", "probe.hip", "latency.hip", "copy.hip", "numa.hip"]
+           "gemm.hip", "gemm_skinny.hip", "attn_decode.hip", "probe.hip", "latency.hip", "copy.hip", "numa.hip",
+           "transpose.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-function"]

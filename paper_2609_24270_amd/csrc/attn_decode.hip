@@ -1,5 +1,5 @@
 // Decode attention with grouped key/value heads (the attention workloads of
-// Section 7.1, decode case: one query token per request; Appendix E gives the
+// Section 7.1, decode case: one query token per request; Appendix F gives the
 // head dimension 128 and 32 or 8 key/value heads).
 //
 //   O[b, h] = softmax_t(scale * <q[b, h], K[b, g, t]>) . V[b, g, :],  g = h / G

@@ -3,6 +3,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <cctype>
+
 #include <algorithm>
 #include <cmath>
 #include <atomic>
@@ -71,7 +73,6 @@ constexpr size_t kGroupedCache = 8;
 // and the kernels leave their counters zeroed, so one block per stream does.
 struct Workspace {
   int* gemm_ctr = nullptr;                  // 64 ints (dynamic aware GEMM)
-  unsigned long long* copy_ctr = nullptr;   // 4 words
   // grouped GEMM: device copies of recent tile tables and schedules, most
   // recent first (a repeated call reuses its tables), and a pinned host
   // staging buffer with an event recorded after the copies out of it: the
@@ -89,6 +90,9 @@ struct Workspace {
   // small-M GEMM with a split K: fp32 partial tiles (grown on demand)
   float* sm_part = nullptr;
   size_t sm_part_bytes = 0;
+  // B stored [K][N]: its transpose, [N][K rounded up to 8] (grown on demand)
+  void* kn_buf = nullptr;
+  size_t kn_bytes = 0;
   std::vector<std::pair<std::vector<int>, int*>> attn_off;
 };
 
@@ -108,12 +112,9 @@ static int get_workspace(int device, hipStream_t s, Workspace** out) {
   if (it == g_ws.end()) {
     Workspace w;
     ASYM_HIP(hipMalloc(&w.gemm_ctr, 64 * sizeof(int)));
-    ASYM_HIP(hipMalloc(&w.copy_ctr, 4 * sizeof(unsigned long long)));
     int rc = launch_zero_words(w.gemm_ctr, 64, s);
-    if (rc == ASYM_OK) rc = launch_zero_words(w.copy_ctr, 8, s);
     if (rc != ASYM_OK) {
       (void)hipFree(w.gemm_ctr);
-      (void)hipFree(w.copy_ctr);
       return rc;
     }
     it = g_ws.emplace(key, w).first;
@@ -126,7 +127,7 @@ int default_topology(int device, const Topology** out) {
   auto it = g_default_topo.find(device);
   if (it == g_default_topo.end()) {
     asym_topology* t = nullptr;
-    int rc = asym_probe_topology(device, ASYM_PROBE_IDENTITY, &t);
+    int rc = asym_probe_topology(device, ASYM_PROBE_IDENTITY, nullptr, &t);
     if (rc != ASYM_OK) return rc;
     const Topology* tt = unwrap(t);
     g_default_topo[device] = std::make_unique<Topology>(*tt);
@@ -231,7 +232,11 @@ struct GemmPlan {
   bool vec_ab = false;  // A and B alone meet the vector-path alignment
   int bn = 0, tiles_m = 0, tiles_n = 0, grid = 0;
   int small_mb = 0;  // > 0: the small-M kernel with this many 16-row blocks
+  bool b_transposed = false;  // B stored [K][N]: transposed into a library buffer first
 };
+
+// Row pitch (elements) of the transposed copy of a [K][N] operand.
+static int kn_pitch(int K) { return (K + 7) / 8 * 8; }
 
 // The small-M kernel serves row tiles of at most 64 rows when A and B meet the
 // vector-path alignment (C may have any stride) and the GEMM runs on every XCD
@@ -271,9 +276,12 @@ int small_m_order(int mapping) {
 // adds the ranges' fp32 tiles in range order (the launch boundary makes the
 // partial tiles of every XCD visible; a hand-off inside the kernel needs
 // device-scope fences that write back and invalidate whole L2s, and measured
-// slower than no split).  The count
-// depends only on the shape and the device, not on the stream's CU set, so a
-// product has the same bits on every set.
+// slower than no split).  The count depends only on the shape and the device,
+// not on the stream's CU set, so a product has the same bits on every CU set
+// it runs on with the small-M kernel.  A whole-XCD restriction sends it to the
+// persistent kernel instead (one MFMA chain over all of K per output), whose
+// fp32 sums can differ in the last bits from a split product's; without a
+// split the two kernels agree bitwise.
 int small_m_ksplit(int M, int N, int K, int mb, int device_cus) {
   if (M > 64) return 1;
   const int tiles = (N + small_m_tile_cols() - 1) / small_m_tile_cols();
@@ -347,8 +355,17 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   if (M < 1 || N < 1 || K < 1) return fail(ASYM_EINVAL, "gemm: M, N, K must be >= 1");
   if (!A || !B || !C) return fail(ASYM_EINVAL, "gemm: null matrix pointer");
   if (lda < K || ldc < N) return fail(ASYM_EINVAL, "gemm: leading dimension too small");
-  if (b_layout == ASYM_B_KN) return fail(ASYM_EUNSUPPORTED, "gemm: B stored [K][N] is not served; store B as [N][K]");
-  if (b_layout != ASYM_B_NK) return fail(ASYM_EINVAL, "gemm: unknown B layout");
+  if (b_layout == ASYM_B_KN) {
+    // B stored [K][ldb]: the kernels read its transpose, written to a
+    // library buffer [N][kn_pitch(K)] (16-byte aligned rows); plan for that
+    if (ldb < N) return fail(ASYM_EINVAL, "gemm: leading dimension too small");
+    if ((int64_t)K * ldb * 2 >= (1ll << 40)) return fail(ASYM_EUNSUPPORTED, "gemm: B too large");
+    P->b_transposed = true;
+    ldb = kn_pitch(K);
+    B = reinterpret_cast<const void*>((uintptr_t)256);  // a 16-byte aligned stand-in for the buffer
+  } else if (b_layout != ASYM_B_NK) {
+    return fail(ASYM_EINVAL, "gemm: unknown B layout");
+  }
   if (ldb < K) return fail(ASYM_EINVAL, "gemm: leading dimension too small");
   if (mapping != ASYM_MAP_AWARE && mapping != ASYM_MAP_OBLIVIOUS_GROUPED &&
       mapping != ASYM_MAP_OBLIVIOUS_ROWMAJOR)
@@ -398,29 +415,78 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   return ASYM_OK;
 }
 
+// The small-M launch a plan asks for (everything but the partials buffer of
+// a split K, which the caller provides).
+static SmallMLaunch small_m_launch(const GemmPlan& P, const void* A, const void* B, void* C, int M, int N, int K,
+                                   int lda, int ldb, int ldc, int mapping) {
+  SmallMLaunch sm;
+  sm.A = A; sm.B = B; sm.C = C;
+  sm.M = M; sm.N = N; sm.K = K; sm.lda = lda; sm.ldb = ldb; sm.ldc = ldc;
+  sm.mb = P.small_mb;
+  sm.row_tiles = (M + 16 * P.small_mb - 1) / (16 * P.small_mb);
+  sm.order = small_m_order(mapping);
+  sm.n_x = P.t->n_xccs;
+  const int tiles_n = (N + small_m_tile_cols() - 1) / small_m_tile_cols();
+  sm.grid = small_m_grid(sm.row_tiles, tiles_n, sm.order, sm.n_x);
+  sm.ksplit = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
+  if (sm.ksplit > 1) sm.grid = (long long)tiles_n * sm.ksplit;
+  return sm;
+}
+
+// fp32 partial tiles of a split K: [column tiles][ranges][16 mb rows][64 columns]
+static size_t small_m_part_bytes(const SmallMLaunch& sm) {
+  const int tiles_n = (sm.N + small_m_tile_cols() - 1) / small_m_tile_cols();
+  return (size_t)tiles_n * sm.ksplit * 16 * sm.mb * 64 * sizeof(float);
+}
+
+static int gemm_bf16_locked(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
+                            const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
+                            uint32_t xcd_mask, hipStream_t stream);
+
 int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
               const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
               uint32_t xcd_mask, hipStream_t stream) {
   std::lock_guard<std::mutex> lock(g_mu);
+  if (b_layout != ASYM_B_KN)
+    return gemm_bf16_locked(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream);
+  // [K][N] storage: check everything first, then transpose B into the
+  // stream's buffer (an exact copy) and run the [N][K] path on it
+  GemmPlan P;
+  int rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
+  if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(P.device, stream, &ws);
+  if (rc != ASYM_OK) return rc;
+  const int ldt = kn_pitch(K);
+  const size_t need = (size_t)N * ldt * sizeof(uint16_t);
+  if (ws->kn_bytes < need) {
+    // a buffer in use by launches on this stream is freed after they finish
+    ASYM_HIP(hipStreamSynchronize(stream));
+    if (ws->kn_buf) ASYM_HIP(hipFree(ws->kn_buf));
+    ws->kn_buf = nullptr;
+    ws->kn_bytes = 0;
+    ASYM_HIP(hipMalloc(&ws->kn_buf, need));
+    ws->kn_bytes = need;
+  }
+  rc = launch_transpose_bf16(B, K, N, ldb, ws->kn_buf, ldt, stream);
+  if (rc != ASYM_OK) return rc;
+  return gemm_bf16_locked(topo_in, M, N, K, A, lda, ws->kn_buf, ldt, ASYM_B_NK, C, ldc, mapping, xcd_mask,
+                          stream);
+}
+
+static int gemm_bf16_locked(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
+                            const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
+                            uint32_t xcd_mask, hipStream_t stream) {
   GemmPlan P;
   int rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
   if (rc != ASYM_OK) return rc;
   if (P.small_mb) {
-    SmallMLaunch sm;
-    sm.A = A; sm.B = B; sm.C = C;
-    sm.M = M; sm.N = N; sm.K = K; sm.lda = lda; sm.ldb = ldb; sm.ldc = ldc;
-    sm.mb = P.small_mb;
-    sm.row_tiles = (M + 16 * P.small_mb - 1) / (16 * P.small_mb);
-    sm.order = small_m_order(mapping);
-    sm.n_x = P.t->n_xccs;
-    const int tiles_n = (N + small_m_tile_cols() - 1) / small_m_tile_cols();
-    sm.grid = small_m_grid(sm.row_tiles, tiles_n, sm.order, sm.n_x);
-    sm.ksplit = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
+    SmallMLaunch sm = small_m_launch(P, A, B, C, M, N, K, lda, ldb, ldc, mapping);
     if (sm.ksplit > 1) {
       Workspace* ws = nullptr;
       rc = get_workspace(P.device, stream, &ws);
       if (rc != ASYM_OK) return rc;
-      const size_t part_bytes = (size_t)tiles_n * sm.ksplit * 16 * P.small_mb * 64 * sizeof(float);
+      const size_t part_bytes = small_m_part_bytes(sm);
       if (ws->sm_part_bytes < part_bytes) {
         // a buffer in use by launches on this stream is freed after they finish
         ASYM_HIP(hipStreamSynchronize(stream));
@@ -432,7 +498,6 @@ int gemm_bf16(const asym_topology* topo_in, int M, int N, int K, const void* A, 
         ws->sm_part_bytes = pb;
       }
       sm.part = ws->sm_part;
-      sm.grid = (long long)tiles_n * sm.ksplit;
     }
     return launch_gemm_small_m(sm, stream);
   }
@@ -813,6 +878,7 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   if (rc != ASYM_OK) return rc;
   *out = asym_gemm_plan_info{};
   out->n_xcds = P.t->n_xccs;
+  out->b_transposed = P.b_transposed ? 1 : 0;
   out->vector_path = P.vec ? 1 : 0;
   if (P.small_mb) {
     out->vector_path = 1;
@@ -841,31 +907,16 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   return ASYM_OK;
 }
 
-// Bytes moved by copies on stream s since the last call; clears the count.
-int copy_bytes_take(hipStream_t s, unsigned long long* bytes) {
-  std::lock_guard<std::mutex> lock(g_mu);
-  int device = 0;
-  int rc = current_device(&device);
-  if (rc != ASYM_OK) return rc;
-  Workspace* ws = nullptr;
-  rc = get_workspace(device, s, &ws);
-  if (rc != ASYM_OK) return rc;
-  ASYM_HIP(hipStreamSynchronize(s));
-  ASYM_HIP(hipMemcpy(bytes, ws->copy_ctr + 2, sizeof(unsigned long long), hipMemcpyDeviceToHost));
-  ASYM_HIP(hipMemset(ws->copy_ctr + 2, 0, sizeof(unsigned long long)));
-  return ASYM_OK;
-}
-
 // Drop the workspace of a stream that is about to be destroyed.
 void release_workspace(hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_mu);
   for (auto it = g_ws.begin(); it != g_ws.end();) {
     if (it->first.second == s) {
       hipFree(it->second.gemm_ctr);
-      hipFree(it->second.copy_ctr);
       if (it->second.attn_buf) hipFree(it->second.attn_buf);
       if (it->second.attn_claim) hipFree(it->second.attn_claim);
       if (it->second.sm_part) hipFree(it->second.sm_part);
+      if (it->second.kn_buf) hipFree(it->second.kn_buf);
       for (auto& t : it->second.attn_off) hipFree(t.second);
       for (auto& t : it->second.g_tables) {
         hipFree(t.desc);
@@ -902,7 +953,17 @@ extern "C" int asym_device_query(int device, asym_device_info* out) {
   out->hbm_bytes = p.totalGlobalMem;
   std::strncpy(out->arch, p.gcnArchName, sizeof(out->arch) - 1);
   if (out->n_xccs < 1) out->n_xccs = 1;
-  return ASYM_OK;
+  char bus[sizeof(out->pci_bus_id)] = {0};
+  ASYM_HIP(hipDeviceGetPCIBusId(bus, (int)sizeof(bus) - 1, device));
+  for (size_t i = 0; i + 1 < sizeof(bus) && bus[i]; ++i) out->pci_bus_id[i] = (char)std::tolower((unsigned char)bus[i]);
+  hipUUID u;
+  ASYM_HIP(hipDeviceGetUuid(&u, device));
+  for (int i = 0; i < 16; ++i)
+    std::snprintf(out->uuid + 2 * i, 3, "%02x", (unsigned)(unsigned char)u.bytes[i]);
+  ASYM_HIP(hipRuntimeGetVersion(&out->runtime_version));
+  ASYM_HIP(hipDriverGetVersion(&out->driver_version));
+  return asym::read_partition_modes(out->pci_bus_id, out->compute_partition, out->memory_partition,
+                              sizeof(out->compute_partition));
 }
 
 extern "C" int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K, const void* A, int lda,
@@ -926,30 +987,28 @@ extern "C" int asym_gemm_plan(const asym_topology* topo, int M, int N, int K, co
                          static_cast<hipStream_t>(stream), out);
 }
 
-extern "C" int asym_copy_bf16(void* dst, const void* src, size_t n_bytes, int passes,
-                              const int* stop_flag, uint32_t xcd_mask, void* stream) {
+extern "C" int asym_copy_bf16(const asym_topology* topo, void* dst, const void* src, size_t n_bytes,
+                              int passes, const int* stop_flag, uint32_t xcd_mask, void* stream) {
   using namespace asym;
   if (!dst || !src) return fail(ASYM_EINVAL, "copy: null pointer");
   if (n_bytes == 0 || (n_bytes & 15u) || ((uintptr_t)dst & 15u) || ((uintptr_t)src & 15u))
     return fail(ASYM_EINVAL, "copy: size and pointers must be nonzero multiples of 16 bytes");
+  if (n_bytes >> 40) return fail(ASYM_EINVAL, "copy: at most 2^40 bytes");
   if (passes < 1) return fail(ASYM_EINVAL, "copy: passes must be >= 1");
-  if (!copy_kernel_enabled())
-    return fail(ASYM_EUNSUPPORTED,
-                "copy: the streaming-copy kernel is switched off: its launches did not finish on the "
-                "device and the cause has not been found yet");
+  const char* sp = static_cast<const char*>(src);
+  const char* dp = static_cast<const char*>(dst);
+  if (sp < dp + n_bytes && dp < sp + n_bytes) return fail(ASYM_EINVAL, "copy: source and destination overlap");
   hipStream_t s = static_cast<hipStream_t>(stream);
   std::lock_guard<std::mutex> lock(g_mu);
-  int device = 0;
-  int rc = current_device(&device);
+  // the stream's CU set, less the XCDs outside xcd_mask (their workgroups
+  // leave at once); a mask that leaves an XCD without a CU is refused, since
+  // the workgroups dealt there could never run
+  CuSet cs;
+  int rc = cu_set_for(topo, ASYM_MAP_AWARE, xcd_mask, s, "copy", &cs);
   if (rc != ASYM_OK) return rc;
-  const Topology* t = nullptr;
-  rc = default_topology(device, &t);
-  if (rc != ASYM_OK) return rc;
-  Workspace* ws = nullptr;
-  rc = get_workspace(device, s, &ws);
-  if (rc != ASYM_OK) return rc;
-  const int grid = 4 * t->n_cus;
-  return launch_copy(dst, src, n_bytes, passes, stop_flag, xcd_mask, grid, ws->copy_ctr, s);
+  const int n_x = cs.t->n_xccs;
+  return launch_copy(dst, src, n_bytes, passes, stop_flag, cs.slots.data(), n_x,
+                     copy_grid(cs.slots.data(), n_x), s);
 }
 
 extern "C" int asym_stream_create(const asym_topology* topo, const uint32_t* mask, void** out) {

@@ -4,11 +4,11 @@
 // a hardware CU-masked queue when the task names a CU mask, an unmasked queue
 // with the kernels' own XCD filter when it names whole XCDs.  Tasks are
 // enqueued back to back, after one untimed launch of each GEMM (its one-time
-// setup), and timed with events on their own streams; a copy
-// task with iters <= 0 keeps streaming until a device flag, raised on the
-// GEMM streams after their last launch, stops it.  A read task is the
-// bandwidth-bound co-runner that stays available while the copy kernel is
-// switched off: a fixed number of passes of a whole-buffer reader.
+// setup), and timed with events on their own streams.  The bandwidth-bound
+// tenants are a streaming copy and a whole-buffer reader, each a fixed number
+// of passes (no tenant runs "until the others end": a tenant that waits for a
+// persistent GEMM to finish, while that GEMM's workgroups dealt to the
+// tenant's XCDs wait for the tenant's CUs, never ends).
 #include <hip/hip_runtime.h>
 
 #include <cstring>
@@ -28,17 +28,15 @@ using asym::fail;
 
 namespace {
 
-struct Guard {  // releases streams, events, the flag and sinks on every exit path
+struct Guard {  // releases streams, events and sinks on every exit path
   std::vector<hipStream_t> streams;
   std::vector<hipEvent_t> events;
   std::vector<void*> sinks;
-  int* flag = nullptr;
   ~Guard() {
     for (hipStream_t s : streams) hipStreamSynchronize(s);
     for (hipEvent_t e : events) hipEventDestroy(e);
     for (hipStream_t s : streams) asym_stream_destroy(s);
     for (void* p : sinks) hipFree(p);
-    if (flag) hipFree(flag);
   }
 };
 
@@ -55,14 +53,23 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
   if (!tasks || !out || n_tasks < 1 || n_tasks > 16) return fail(ASYM_EINVAL, "corun: bad task list");
   std::memset(out, 0, sizeof(asym_task_result) * n_tasks);
   Guard g;
-  int n_gemm = 0;
   for (int i = 0; i < n_tasks; ++i) {
     const asym_task& t = tasks[i];
     if (t.kind == 0) {
       if (t.iters < 1 || !t.A || !t.B || !t.C) return fail(ASYM_EINVAL, "corun: bad GEMM task");
-      ++n_gemm;
     } else if (t.kind == 1) {
-      if (!t.src || !t.dst || t.n_bytes == 0) return fail(ASYM_EINVAL, "corun: bad copy task");
+      if (!t.src || !t.dst || t.n_bytes < 16 || t.n_bytes % 16)
+        return fail(ASYM_EINVAL, "corun: a copy task needs a source and destination of a multiple of 16 bytes");
+      const char* sp = static_cast<const char*>(t.src);
+      const char* dp = static_cast<const char*>(t.dst);
+      if (sp < dp + t.n_bytes && dp < sp + t.n_bytes)
+        return fail(ASYM_EINVAL, "corun: a copy task's source and destination overlap");
+      if (((uintptr_t)t.src & 15u) || ((uintptr_t)t.dst & 15u))
+        return fail(ASYM_EINVAL, "corun: a copy task's buffers must be 16-byte aligned");
+      if (t.iters < 1)
+        return fail(ASYM_EINVAL,
+                    "corun: a copy task runs a fixed number of passes (iters >= 1); an open-ended copy beside a "
+                    "persistent GEMM can deadlock (the GEMM's workgroups dealt to the copy's XCDs wait for its CUs)");
     } else if (t.kind == 2) {
       if (!t.src || t.n_bytes < 16 || t.n_bytes % 16 || t.iters < 1)
         return fail(ASYM_EINVAL, "corun: a read task needs a source of a multiple of 16 bytes and iters >= 1");
@@ -74,28 +81,21 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
     if (rc != ASYM_OK) return rc;
     g.streams.push_back(static_cast<hipStream_t>(s));
   }
-  bool open_copy = false;
-  for (int i = 0; i < n_tasks; ++i)
-    if (tasks[i].kind == 1 && tasks[i].iters <= 0) open_copy = true;
-  if (open_copy && n_gemm == 0) return fail(ASYM_EINVAL, "corun: an open-ended copy needs a GEMM task to end it");
-  if (open_copy) {
-    ASYM_HIP(hipMalloc(&g.flag, sizeof(int)));
-    ASYM_HIP(hipMemset(g.flag, 0, sizeof(int)));
-  }
   int n_x = 0, dev = 0;
   ASYM_HIP(hipGetDevice(&dev));
   ASYM_HIP(hipDeviceGetAttribute(&n_x, hipDeviceAttributeNumberOfXccs, dev));
-  // read tasks: the reading CUs per XCD (the task's mask, or every CU, less
-  // the XCDs its filter leaves out) and the grid
+  // copy and read tasks: the working CUs per XCD (the task's mask, or every
+  // CU, less the XCDs its filter leaves out) and the grid
   std::vector<std::vector<int>> read_cus(n_tasks);
   std::vector<int> read_grid(n_tasks, 0);
   std::vector<void*> sink(n_tasks, nullptr);
   for (int i = 0; i < n_tasks; ++i) {
     const asym_task& t = tasks[i];
-    if (t.kind != 2) continue;
+    if (t.kind != 1 && t.kind != 2) continue;
     if (n_x < 1 || n_x > 16 || (t.xcd_mask >> n_x) != 0u)
-      return fail(ASYM_EINVAL, "corun: a read task's XCD filter names an XCD the device does not have");
-    if (t.grid < 0 || t.grid > (1 << 20)) return fail(ASYM_EINVAL, "corun: a read task's grid must be in [0, 2^20]");
+      return fail(ASYM_EINVAL, "corun: a copy or read task's XCD filter names an XCD the device does not have");
+    if (t.grid < 0 || t.grid > (1 << 20))
+      return fail(ASYM_EINVAL, "corun: a copy or read task's grid must be in [0, 2^20]");
     std::vector<int>& cus = read_cus[i];
     cus.assign(ASYM_MAX_XCDS, 0);
     if (!mask_empty(t.mask)) {
@@ -111,6 +111,13 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
     }
     for (int x = 0; x < n_x; ++x)
       if (t.xcd_mask && !((t.xcd_mask >> x) & 1u)) cus[x] = 0;
+    int any = 0;
+    for (int x = 0; x < n_x; ++x) any += cus[x];
+    if (!any) return fail(ASYM_EINVAL, "corun: a copy or read task's XCD filter leaves it no CU");
+    if (t.kind == 1) {
+      read_grid[i] = t.grid > 0 ? t.grid : asym::copy_grid(cus.data(), n_x);
+      continue;
+    }
     read_grid[i] = t.grid > 0 ? t.grid : asym::stream_read_grid(cus.data(), n_x);
     ASYM_HIP(hipMalloc(&sink[i], (size_t)read_grid[i] * 256 * 16));
     g.sinks.push_back(sink[i]);
@@ -136,7 +143,6 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
   ASYM_HIP(hipDeviceSynchronize());
 
   // copies and reads first, so they are streaming when the GEMMs start
-  std::vector<unsigned long long*> copy_ctr(n_tasks, nullptr);
   for (int pass = 0; pass < 2; ++pass) {
     for (int i = 0; i < n_tasks; ++i) {
       const asym_task& t = tasks[i];
@@ -148,9 +154,8 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
                                           n_x, s);
         if (rc != ASYM_OK) return rc;
       } else if (t.kind == 1) {
-        const int passes = t.iters > 0 ? t.iters : 100000;
-        int rc = asym_copy_bf16(t.dst, t.src, t.n_bytes, passes, t.iters > 0 ? nullptr : g.flag,
-                                t.xcd_mask, s);
+        int rc = asym::launch_copy(t.dst, t.src, t.n_bytes, t.iters, nullptr, read_cus[i].data(), n_x,
+                                   read_grid[i], s);
         if (rc != ASYM_OK) return rc;
       } else {
         for (int it = 0; it < t.iters; ++it) {
@@ -161,17 +166,6 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
       }
       ASYM_HIP(hipEventRecord(ev1[i], s));
     }
-  }
-  if (open_copy) {
-    // raise the stop flag once every GEMM stream has drained: the last GEMM
-    // stream waits for the others' end events, then sets the flag
-    int last = -1;
-    for (int i = 0; i < n_tasks; ++i)
-      if (tasks[i].kind == 0) last = i;
-    for (int i = 0; i < n_tasks; ++i)
-      if (tasks[i].kind == 0 && i != last) ASYM_HIP(hipStreamWaitEvent(g.streams[last], ev1[i], 0));
-    int rc = asym::launch_set_flag(g.flag, 1, g.streams[last]);
-    if (rc != ASYM_OK) return rc;
   }
   for (int i = 0; i < n_tasks; ++i) ASYM_HIP(hipEventSynchronize(ev1[i]));
   for (int i = 0; i < n_tasks; ++i) {
@@ -184,6 +178,10 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
       r.iters_done = t.iters;
       r.ms_per_iter = ms / t.iters;
       r.tflops = 2.0 * t.M * t.N * (double)t.K * t.iters / (ms * 1e-3) / 1e12;
+    } else if (t.kind == 1) {
+      r.iters_done = t.iters;
+      r.ms_per_iter = ms / t.iters;
+      r.gbps = 2.0 * (double)t.n_bytes * t.iters / (ms * 1e-3) / 1e9;
     } else if (t.kind == 2) {
       r.iters_done = t.iters;
       r.ms_per_iter = ms / t.iters;
@@ -192,18 +190,6 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
       ASYM_HIP(hipMemcpy(h.data(), sink[i], sizeof(uint32_t) * h.size(), hipMemcpyDeviceToHost));
       for (size_t w = 0; w < h.size(); ++w) r.checksum[w & 3] ^= h[w];
     }
-  }
-  // bytes moved by each copy: read back and clear the stream's byte counter
-  for (int i = 0; i < n_tasks; ++i) {
-    if (tasks[i].kind != 1) continue;
-    unsigned long long bytes = 0;
-    int rc = asym::copy_bytes_take(g.streams[i], &bytes);
-    if (rc != ASYM_OK) return rc;
-    asym_task_result& r = out[i];
-    const double passes = (double)bytes / (double)tasks[i].n_bytes;
-    r.iters_done = (int)(passes + 0.5);
-    r.ms_per_iter = r.iters_done > 0 ? r.ms_total / passes : 0.0;
-    r.gbps = 2.0 * (double)bytes / (r.ms_total * 1e-3) / 1e9;
   }
   return ASYM_OK;
 }

@@ -37,7 +37,23 @@ struct Topology {
   double rr_fraction = -1.0;             // round-robin dispatch agreement
   bool has_latency = false;
   asym_latency_summary lat{};
+  unsigned flags = 0;                    // what was probed (asym_probe_flags)
+  std::string compute_partition = "unknown", memory_partition = "unknown";
+  std::string key;                       // chip and configuration it was probed on
 };
+
+// The chip and configuration a probe result belongs to (PCI bus id, UUID,
+// runtime and driver versions, architecture, partition modes, counts), as one
+// line of text; a cached topology is reused only under the same key.
+int device_key(int device, std::string* key, asym_device_info* info);
+// Cache file of a topology (text; host only).  load: ASYM_ENOCACHE with the
+// reason when the file is missing, made under another key, lacks a requested
+// probe, or is malformed or breaks an invariant.
+int topology_save(const Topology& t, const char* path);
+// The driver's current compute and memory partition modes of the PCI function
+// (sysfs), or "unknown"; each written as a C string of at most len bytes.
+int read_partition_modes(const char* pci_bus_id, char* compute, char* memory, size_t len);
+int topology_load(const char* path, const std::string& key, unsigned flags, Topology* out);
 
 // Fields of the HW_ID hardware register (GCN/CDNA layout).
 inline int hwid_cu(uint32_t h) { return (h >> 8) & 0xF; }
@@ -172,14 +188,16 @@ int stream_read_grid(const int* cus, int n_x);
 int launch_stream_read(const void* src, size_t n_bytes, int passes, void* sink, int grid, const int* cus,
                        int n_x, hipStream_t s);
 
-int launch_copy(void* dst, const void* src, size_t n_bytes, int passes,
-                const int* stop_flag, uint32_t xcd_mask, int grid,
-                unsigned long long* ctr, hipStream_t s);
-int launch_set_flag(int* flag, int v, hipStream_t s);
+// Streaming copy: `passes` passes of dst = src over n_bytes (a multiple of 16),
+// the buffer cut into per-XCD slices in proportion to cus[n_x] (0 = no slice);
+// stop_flag (nullable) is read before every pass after the first.
+int copy_grid(const int* cus, int n_x);
+int launch_copy(void* dst, const void* src, size_t n_bytes, int passes, const int* stop_flag,
+                const int* cus, int n_x, int grid, hipStream_t s);
+// dst[c][r] = src[r][c] (bf16; row pitches lds >= cols and ldd >= rows)
+int launch_transpose_bf16(const void* src, int rows, int cols, int lds, void* dst, int ldd, hipStream_t s);
 // zero n 4-byte words at p, ordered on stream s
 int launch_zero_words(void* p, size_t n, hipStream_t s);
-bool copy_kernel_enabled();
-int copy_bytes_take(hipStream_t s, unsigned long long* bytes);
 void release_workspace(hipStream_t s);
 
 // Stream CU mask -> CU set seen by the scheduler.

@@ -127,15 +127,27 @@ asym_topology* wrap_topology(Topology&& t);
 const Topology* unwrap(const asym_topology* p);
 }
 
-extern "C" int asym_probe_topology(int device, unsigned flags, asym_topology** out) {
+extern "C" int asym_probe_topology(int device, unsigned flags, const char* cache_path, asym_topology** out) {
   using namespace asym;
   if (!out) return fail(ASYM_EINVAL, "null out");
   *out = nullptr;
   if (flags & ~(unsigned)(ASYM_PROBE_IDENTITY | ASYM_PROBE_MASKMAP | ASYM_PROBE_LATENCY))
     return fail(ASYM_EINVAL, "probe: unknown flags");
+  // every probe includes the identity probe (the mask map and the latency
+  // probe are built on its CU records)
+  flags |= ASYM_PROBE_IDENTITY;
   asym_device_info info;
-  int rc = asym_device_query(device, &info);
+  std::string key;
+  int rc = device_key(device, &key, &info);
   if (rc != ASYM_OK) return rc;
+  if (cache_path) {
+    Topology cached;
+    if (topology_load(cache_path, key, flags, &cached) == ASYM_OK) {
+      cached.device = device;
+      *out = wrap_topology(std::move(cached));
+      return ASYM_OK;
+    }
+  }
   ASYM_HIP(hipSetDevice(device));
   if (info.n_cus > ASYM_MAX_CUS || info.n_xccs > ASYM_MAX_XCDS)
     return fail(ASYM_EUNSUPPORTED, "probe: device larger than the mask format");
@@ -165,6 +177,11 @@ extern "C" int asym_probe_topology(int device, unsigned flags, asym_topology** o
     rc = probe_latency_run(device, t);
     if (rc != ASYM_OK) return rc;
   }
+  t.flags = flags;
+  t.key = key;
+  t.compute_partition = info.compute_partition;
+  t.memory_partition = info.memory_partition;
+  if (cache_path) (void)topology_save(t, cache_path);  // a failed write leaves the probe result valid
   *out = wrap_topology(std::move(t));
   return ASYM_OK;
 }

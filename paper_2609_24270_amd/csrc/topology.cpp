@@ -228,6 +228,15 @@ static std::string topology_json(const Topology& t) {
   for (int x = 0; x < t.n_xccs; ++x) s += (x ? ", " : "") + std::to_string(t.cus_per_xcd[x]);
   s += "], \"has_maskmap\": ";
   s += t.has_maskmap ? "true" : "false";
+  s += ", \"probes\": " + std::to_string(t.flags);
+  s += ", \"compute_partition\": \"" + t.compute_partition + "\", \"memory_partition\": \"" +
+       t.memory_partition + "\"";
+  std::string k;  // the key as a JSON string (it holds no quote or backslash, but escape anyway)
+  for (char c : t.key) {
+    if (c == '"' || c == '\\') k += '\\';
+    k += c;
+  }
+  s += ", \"key\": \"" + k + "\"";
   s += ", \"cus\": [";
   for (size_t i = 0; i < t.cus.size(); ++i) {
     const CuRecord& c = t.cus[i];
@@ -312,6 +321,8 @@ extern "C" int asym_topology_from_records(const int32_t* records, int n_records,
   int rc = asym::build_topology(records, n_records, n_cus_expected, n_xccs_expected,
                                 mask_bit_record, t);
   if (rc != ASYM_OK) return rc;
+  t.flags = ASYM_PROBE_IDENTITY | (mask_bit_record ? ASYM_PROBE_MASKMAP : 0u);
+  t.key = "records";
   *out = new asym_topology{std::move(t)};
   return ASYM_OK;
 }

@@ -312,7 +312,7 @@ def planted_home_region(seed: int, n_pages: int, mask: int, n_verify: int = 64,
     return lat_of(pages), vo, lat_of(vo), home_of
 
 
-# Decode attention (Section 7.1 attention workloads; Appendix E): one query
+# Decode attention (Section 7.1 attention workloads; Appendix F): one query
 # token per request, head dimension 128, 32 query heads against 32 key/value
 # heads (multi-head) or 8 (grouped-query), batch 1..64, KV length from 512
 # doubling.  Recipe: one torch CPU generator per problem seeded `seed`, q then

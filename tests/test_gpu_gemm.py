@@ -57,9 +57,41 @@ def sampled_check(A, B, C, n_rows=128, n_cols=128, seed=0, exact=False):
 
 
 def test_device_query(dev):
+    """Device discovery: counts, the chip's identity and its partition modes
+    (recorded; SPX / NPS1 expected, "unknown" where the driver's files cannot
+    be read), and the cache key that ties a probe result to them."""
     d = asym.device_query(0)
     print(d)
     assert d["n_cus"] == 256 and d["n_xccs"] == 8 and d["arch"].startswith("gfx950")
+    assert len(d["uuid"]) == 32 and d["pci_bus_id"].count(":") == 2
+    assert d["compute_partition"] and d["memory_partition"]
+    key = asym.topology_cache_key(0)
+    print("cache key:", key)
+    for part in ("pci=" + d["pci_bus_id"], "uuid=" + d["uuid"], "compute=" + d["compute_partition"],
+                 "memory=" + d["memory_partition"], "cus=256", "xccs=8"):
+        assert part in key, part
+
+
+def test_topology_cache_on_the_device(dev, tmp_path):
+    """The first probe with a cache path probes and writes the file; the
+    second reuses it (no probe: same map, same key); a request for a probe the
+    file lacks probes again and rewrites it."""
+    import time
+    path = str(tmp_path / "topo_cache.txt")
+    t0 = time.perf_counter()
+    a = asym.probe_topology(0, asym.PROBE_IDENTITY, cache_path=path)
+    t1 = time.perf_counter()
+    b = asym.probe_topology(0, asym.PROBE_IDENTITY, cache_path=path)
+    t2 = time.perf_counter()
+    ja, jb = a.json(), b.json()
+    print("probe %.3f s, cached %.3f s; partitions %s / %s" % (t1 - t0, t2 - t1, ja["compute_partition"],
+                                                              ja["memory_partition"]))
+    assert ja["cus"] == jb["cus"] and ja["key"] == jb["key"] == asym.topology_cache_key(0)
+    assert ja["compute_partition"] == asym.device_query(0)["compute_partition"]
+    c = asym.probe_topology(0, asym.PROBE_IDENTITY | asym.PROBE_MASKMAP, cache_path=path)
+    assert c.json()["has_maskmap"]
+    d = asym.topology_load(path, asym.topology_cache_key(0), asym.PROBE_MASKMAP)
+    assert d.json()["cus"] == c.json()["cus"]
 
 
 @pytest.mark.parametrize("mapping", MAPS)
@@ -108,6 +140,32 @@ def test_gemm_strided_and_unaligned(dev):
     assert_gemm_close(bits(Cp[:, :N]), R)
     # the padding columns of C are untouched
     assert torch.all(Cp[:, N:].cpu() == 7.0)
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 512, 512), (300, 520, 264), (129, 1000, 77), (32, 4096, 4096),
+                                   (1000, 136, 2056)])
+def test_gemm_b_stored_kn_equals_nk(dev, M, N, K):
+    """B stored [K][N] (N contiguous) is transposed into the library's buffer
+    and gives bitwise the product of the same logical B stored [N][K], on the
+    persistent kernel (vector and predicated paths) and the small-M kernel;
+    a [K][N] operand with a leading dimension above N works too."""
+    A, B = workloads.make_inputs(workloads.make_problem(M, N, K, seed=31 + M + N + K))
+    Ad, Bd = A.to(dev), B.to(dev)
+    ref = asym.gemm(Ad, Bd)
+    Bkn = Bd.t().contiguous()
+    assert asym.gemm_plan(A=Ad, B=Bkn, b_layout="kn")["b_transposed"] == 1
+    assert asym.gemm_plan(A=Ad, B=Bd)["b_transposed"] == 0
+    for m in ("aware", "oblivious_rowmajor"):
+        C = asym.gemm(Ad, Bkn, mapping=m, b_layout="kn")
+        torch.cuda.synchronize()
+        assert torch.equal(C, ref), m
+    wide = torch.zeros((K, N + 24), dtype=torch.bfloat16, device=dev)
+    wide[:, :N] = Bkn
+    C = asym.gemm(Ad, wide[:, :N], b_layout="kn")
+    torch.cuda.synchronize()
+    assert torch.equal(C, ref)
+    R, _ = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    assert_gemm_close(bits(C), R, what=f"[K][N] {M}x{N}x{K}")
 
 
 def test_gemm_exact_integer_8192_sampled(dev):

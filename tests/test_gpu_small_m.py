@@ -229,3 +229,31 @@ def test_split_k_exact_integer_equals_persistent(dev):
         asym.set_small_m(prev)
     _, Co = oracle.gemm_bf16(bits(A), bits(B), "nk")
     assert np.array_equal(small, Co) and np.array_equal(pers, Co)
+
+
+def test_split_k_under_an_xcd_restriction(dev):
+    """32x4096x4096 splits K into ranges on the whole chip (small-M kernel);
+    under a whole-XCD restriction it runs on the persistent kernel, one MFMA
+    chain over K.  Both are within the tolerance of the oracle, and on
+    exact-integer inputs (exact fp32 sums in any order) both equal it bitwise;
+    on real-valued inputs the two may differ in the last bits, which the
+    library documents."""
+    for dist in ("llm", "int"):
+        p = workloads.make_problem(32, 4096, 4096, seed=12, dist=dist)
+        A, B = workloads.make_inputs(p)
+        Ad, Bd = A.to(dev), B.to(dev)
+        whole = asym.gemm_plan(A=Ad, B=Bd)
+        restricted = asym.gemm_plan(A=Ad, B=Bd, xcd_mask=0xC0)
+        assert whole["small_m"] == 1 and whole["k_splits"] == 4
+        assert restricted["small_m"] == 0 and restricted["claims"] == 1
+        C1 = bits(asym.gemm(Ad, Bd))
+        C2 = bits(asym.gemm(Ad, Bd, xcd_mask=0xC0))
+        torch.cuda.synchronize()
+        R, Co = oracle.gemm_bf16(bits(A), bits(B), "nk")
+        if dist == "int":
+            assert np.array_equal(C1, Co) and np.array_equal(C2, Co)
+        else:
+            e1 = assert_gemm_close(C1, R, what="whole chip, K split")
+            e2 = assert_gemm_close(C2, R, what="XCDs 6-7, persistent kernel")
+            print(f"32x4096x4096: split {e1:.3e}, restricted {e2:.3e}, "
+                  f"bitwise equal share {float(np.mean(C1 == C2)):.4f}")

@@ -111,29 +111,64 @@ def test_masked_gemm_bitwise(dev, topo):
         asym.gemm(Ad, Bd, mapping="oblivious_grouped", topo=topo, xcd_mask=0x0F)
 
 
-COPY_OFF = ("the streaming-copy kernel is switched off in libasym: two device runs of this test "
-            "did not finish and the cause has not been found; it stays off the GPU until it is")
-
-
-@pytest.mark.skip(reason=COPY_OFF)
-def test_copy_kernel(dev):
+def test_copy_kernel(dev, topo):
+    """The streaming copy on the whole chip, on whole-XCD filters and on a
+    CU-masked stream copies every byte, including a size that is not a whole
+    number of 16 KiB blocks per XCD; a stop flag raised before the launch ends
+    it after one pass; bad arguments are refused."""
     n = workloads.COPY_BYTES // 2
     src = workloads.copy_source(n).to(dev)
-    for xm, passes in ((0, 1), (0x3, 2), (0xF0, 3)):
+    for xm, passes in ((0, 1), (0x3, 2), (0xF0, 3), (0x81, 1)):
         dst = torch.zeros_like(src)
-        asym.copy(dst, src, passes=passes, xcd_mask=xm)
+        asym.copy(dst, src, passes=passes, xcd_mask=xm, topo=topo)
         torch.cuda.synchronize()
-        assert torch.equal(dst, src)
-    # a ragged size (not a multiple of the 64 KiB chunk)
+        assert torch.equal(dst, src), hex(xm)
     s2 = src[: 12345 * 8]
     d2 = torch.zeros_like(s2)
-    asym.copy(d2, s2)
+    asym.copy(d2, s2, topo=topo)
     torch.cuda.synchronize()
     assert torch.equal(d2, s2)
+    # a seeded random 128-CU set (9 to 23 CUs per XCD) on a masked stream
+    mask = workloads.random_mask_bits(4, 1, 128)[0]
+    s = asym.stream_create(topo, mask)
+    try:
+        dst = torch.zeros_like(src)
+        asym.copy(dst, src, passes=2, stream=s, topo=topo)
+        s.synchronize()
+        assert torch.equal(dst, src)
+    finally:
+        asym.stream_destroy(s)
+    def timed(fn):
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        fn()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1)
+    dst = torch.zeros_like(src)
+    t10 = timed(lambda: asym.copy(dst, src, passes=10, topo=topo))
+    flag = torch.ones(1, dtype=torch.int32, device=dev)
+    dst.zero_()
+    torch.cuda.synchronize()
+    t_flag = timed(lambda: asym.copy(dst, src, passes=1000, stop_flag=flag, topo=topo))
+    assert torch.equal(dst, src)
+    print("copy of 64 MiB: 10 passes %.3f ms; at most 1000 passes with the stop flag raised %.3f ms"
+          % (t10, t_flag))
+    assert t_flag < 3 * t10  # the flag ends it after its first pass (1000 passes: ~100 x t10)
+    with pytest.raises(asym.AsymError):
+        asym.copy(src[1:9], src[:8], topo=topo)      # misaligned source
+    with pytest.raises(asym.AsymError):
+        asym.copy(src[8:], src[:-8], topo=topo)      # overlapping buffers
+    with pytest.raises(asym.AsymError):
+        asym.copy(dst, src, passes=0, topo=topo)
 
 
-@pytest.mark.skip(reason=COPY_OFF)
 def test_corun_gemm_and_copy(dev, topo):
+    """A GEMM on a seeded random 128-CU set beside the 64 MiB copy tenant on
+    the complementary CUs, and on whole-XCD sides (split masks, each side
+    lending one CU per foreign XCD): the GEMM's bits equal its solo run and
+    the copy copies every byte; an open-ended copy task is refused."""
     A, B = workloads.make_inputs(workloads.COLOC)
     Ad, Bd = A.to(dev), B.to(dev)
     ref = asym.gemm(Ad, Bd)
@@ -144,23 +179,22 @@ def test_corun_gemm_and_copy(dev, topo):
     mask = workloads.random_mask_bits(4, 1, 128)[0]
     comp = [b for b in range(256) if b not in set(mask)]
     res = asym.corun([asym.gemm_task(Ad, Bd, C, 5, "aware", mask=mask),
-                      asym.copy_task(dst, src, 0, mask=comp)], topo)
+                      asym.copy_task(dst, src, 20, mask=comp)], topo)
     print(res)
     assert torch.equal(C, ref)
     assert torch.equal(dst, src)
-    assert res[0]["tflops"] > 0 and res[1]["gbps"] > 0 and res[1]["iters_done"] >= 1
-    # whole-XCD partitions through the kernels' XCD filter
-    res = asym.corun([asym.gemm_task(Ad, Bd, C, 5, "aware", xcd_mask=0x0F),
-                      asym.copy_task(dst, src, 0, xcd_mask=0xF0)], topo)
+    assert res[0]["tflops"] > 0 and res[1]["gbps"] > 0 and res[1]["iters_done"] == 20
+    ma, mb = topo.cuset_split_xcds(0x0F)
+    dst.zero_()
+    C.zero_()
+    res = asym.corun([asym.gemm_task(Ad, Bd, C, 5, "aware", mask=ma, xcd_mask=0x0F),
+                      asym.copy_task(dst, src, 20, mask=mb, xcd_mask=0xF0)], topo)
     print(res)
     assert torch.equal(C, ref)
-
-
-def test_copy_reports_switched_off(dev):
-    src = torch.zeros(1024, dtype=torch.bfloat16, device=dev)
-    with pytest.raises(asym.AsymError) as e:
-        asym.copy(torch.empty_like(src), src)
-    assert e.value.status == asym.EUNSUPPORTED
+    assert torch.equal(dst, src)
+    with pytest.raises(asym.AsymError):
+        asym.corun([asym.gemm_task(Ad, Bd, C, 1, "aware", mask=mask),
+                    asym.copy_task(dst, src, 0, mask=comp)], topo)
 
 
 def test_corun_prefill_decode(dev, topo):

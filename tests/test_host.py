@@ -326,15 +326,18 @@ def test_gemm_and_copy_argument_errors(lib):
         ((None, 0, 4, 4, P, 4, P, 4, 0, P, 4, 0, 0, None), asym.EINVAL),      # M = 0
         ((None, 4, 4, 4, None, 4, P, 4, 0, P, 4, 0, 0, None), asym.EINVAL),   # null A
         ((None, 4, 4, 8, P, 4, P, 8, 0, P, 4, 0, 0, None), asym.EINVAL),      # lda < K
-        ((None, 4, 4, 4, P, 4, P, 4, 1, P, 4, 0, 0, None), asym.EUNSUPPORTED),  # [K][N] B
+        ((None, 4, 8, 4, P, 4, P, 4, 1, P, 8, 0, 0, None), asym.EINVAL),      # [K][N] B, ldb < N
         ((None, 4, 4, 4, P, 4, P, 4, 7, P, 4, 0, 0, None), asym.EINVAL),      # bad layout
         ((None, 4, 4, 4, P, 4, P, 4, 0, P, 4, 9, 0, None), asym.EINVAL),      # bad mapping
     ]
     for args, want in cases:
         assert lib_.asym_gemm_bf16(*args) == want, args
         assert asym.last_error()
-    assert lib_.asym_copy_bf16(P, P, 24, 1, None, 0, None) == asym.EINVAL
-    assert lib_.asym_copy_bf16(P, P, 32, 0, None, 0, None) == asym.EINVAL
+    Q = ctypes.c_void_p(vp + 4096)
+    assert lib_.asym_copy_bf16(None, Q, P, 24, 1, None, 0, None) == asym.EINVAL     # size not 16k
+    assert lib_.asym_copy_bf16(None, Q, P, 32, 0, None, 0, None) == asym.EINVAL     # no pass
+    assert lib_.asym_copy_bf16(None, P, P, 32, 1, None, 0, None) == asym.EINVAL     # overlap
+    assert lib_.asym_copy_bf16(None, ctypes.c_void_p(vp + 8), P, 32, 1, None, 0, None) == asym.EINVAL
 
 
 def _grouped_cases():
@@ -411,3 +414,65 @@ def test_dispatch_share_counts_classes_not_the_start():
         r[0] = (r[0] & ~0xF) | 1          # a quarter of class 0 moved to XCC 1
     want = 1.0 - (len(cls0) // 4) / len(split)
     assert abs(otopo.round_robin_fraction(split, 8) - want) < 1e-12
+
+
+# -- per-chip topology cache ------------------------------------------------------------
+
+def test_topology_cache_round_trip_and_staleness(lib, tmp_path):
+    """A saved map loads back equal under its key, is refused under another key
+    (another chip or partition mode), when it lacks a requested probe, and
+    when the file is missing, truncated or edited to break an invariant."""
+    t, perm = _maskmap_topology(seed=5)
+    key = "pci=0000:0a:00.0 uuid=00ff hip=70200000 driver=70200000 arch=gfx950 compute=SPX memory=NPS1 cus=256 xccs=8"
+    path = str(tmp_path / "topo.txt")
+    t.save(path, key)
+    u = asym.topology_load(path, key, asym.PROBE_IDENTITY | asym.PROBE_MASKMAP)
+    ju, jt = u.json(), t.json()
+    assert ju["cus"] == jt["cus"] and ju["cus_per_xcd"] == jt["cus_per_xcd"] and ju["has_maskmap"]
+    assert ju["key"] == key and jt["key"] == "records"
+    assert [u.cu(i)["mask_bit"] for i in range(256)] == [t.cu(i)["mask_bit"] for i in range(256)]
+    assert u.cuset_counts(list(range(0, 256, 2))) == t.cuset_counts(list(range(0, 256, 2)))
+    # another chip, another partition mode
+    for other in (key.replace("0a:00.0", "0b:00.0"), key.replace("compute=SPX", "compute=CPX"),
+                  key.replace("memory=NPS1", "memory=NPS2")):
+        with pytest.raises(asym.AsymError) as e:
+            asym.topology_load(path, other, asym.PROBE_IDENTITY)
+        assert e.value.status == asym.ENOCACHE and "another key" in str(e.value)
+    # a probe the cached map does not hold
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_load(path, key, asym.PROBE_IDENTITY | asym.PROBE_LATENCY)
+    assert e.value.status == asym.ENOCACHE and "lacks" in str(e.value)
+    # missing file
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_load(str(tmp_path / "none.txt"), key)
+    assert e.value.status == asym.ENOCACHE
+    lines = open(path).read().splitlines()
+    # truncated
+    open(path, "w").write("\n".join(lines[:100]) + "\n")
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_load(path, key)
+    assert e.value.status == asym.ENOCACHE
+    # two CU lines made equal: the exact invariants reject the map
+    cu_lines = [i for i, l in enumerate(lines) if l.startswith("cu ")]
+    bad = list(lines)
+    f0 = bad[cu_lines[0]].split()
+    f1 = bad[cu_lines[1]].split()
+    bad[cu_lines[1]] = " ".join(f0[:5] + f1[5:])
+    open(path, "w").write("\n".join(bad) + "\n")
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_load(path, key)
+    assert e.value.status == asym.ENOCACHE and "invariant" in str(e.value)
+    # a mask bit used twice
+    bad = list(lines)
+    f1 = bad[cu_lines[1]].split()
+    bad[cu_lines[1]] = " ".join(f1[:5] + [bad[cu_lines[0]].split()[5]])
+    open(path, "w").write("\n".join(bad) + "\n")
+    with pytest.raises(asym.AsymError) as e:
+        asym.topology_load(path, key, asym.PROBE_IDENTITY | asym.PROBE_MASKMAP)
+    assert e.value.status == asym.ENOCACHE
+    # identity-only map: loads for identity requests only
+    plain = asym.topology_from_records(fake_records(uniform_layout()), 256, 8)
+    plain.save(path, key)
+    assert asym.topology_load(path, key).info()["cus_per_xcd"] == [32] * 8
+    with pytest.raises(asym.AsymError):
+        asym.topology_load(path, key, asym.PROBE_MASKMAP)
