@@ -588,6 +588,35 @@ int asym_gemm_grouped_bf16(const asym_topology* topo, int G, const int* M, int N
                            void* C, int ldc, int mapping, uint32_t xcd_mask,
                            void* stream);
 
+/* ---- GEMM without allocation ------------------------------------------- */
+/* For callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, harnesses that forbid the allocator): asym_gemm_bf16
+ * with the same arguments, numerics and kernels (bitwise the same C), but
+ * every device buffer that call keeps in its per-stream workspace (the tile
+ * schedule, the claim counters of the aware kernel's claiming form, the fp32
+ * partial tiles of a split K) sits in one fixed library array per GPU
+ * (asym_gemm_noalloc_limits: 5 MiB), held until the process ends.  It calls
+ * no allocator, device or pinned: a schedule the array does not hold yet is
+ * written into it by small kernels that carry it in their arguments.
+ * Limits: topo must be a probed topology (NULL is refused: the first-use
+ * probe would allocate); ASYM_B_KN is refused (it needs a transposed copy of
+ * B); at most asym_gemm_noalloc_limits' max_tiles output tiles (262016:
+ * e.g. M = N = 128000 at 256 x 256 tiles); split-K partials within
+ * max_partial_bytes (4 MiB, all a 256-CU device needs).
+ * Every call on one GPU shares the array and it keeps the last call's
+ * contents (the schedule is tracked on the host, the counters are cleared
+ * before each claiming launch): calls that overlap in time on one GPU, on any
+ * streams, race and must be serialised by the caller.  Asynchronous.
+ * Errors: those of asym_gemm_bf16, plus ASYM_EINVAL beyond the limits. */
+int asym_gemm_bf16_noalloc(const asym_topology* topo, int M, int N, int K,
+                           const void* A, int lda, const void* B, int ldb,
+                           int b_layout, void* C, int ldc, int mapping,
+                           uint32_t xcd_mask, void* stream);
+
+/* Size of the per-GPU array, the most output tiles a call may have, and the
+ * most bytes of split-K partials (all nullable).  Host only; always ASYM_OK. */
+int asym_gemm_noalloc_limits(size_t* scratch_bytes, int* max_tiles, size_t* max_partial_bytes);
+
 /* What asym_gemm_bf16 with the same arguments would launch, without
  * launching it or touching the matrices: the same checks and errors, the
  * output tile (tile_m x tile_n; the width is taken from 256, 224 and 192 to

@@ -42,7 +42,8 @@ EXPORTS = (
     "asym_dispatch_check", "asym_dispatch_probe", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
-    "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_plan", "asym_gemm_set_small_m",
+    "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_bf16_noalloc", "asym_gemm_noalloc_limits",
+    "asym_gemm_plan", "asym_gemm_set_small_m",
     "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
@@ -246,6 +247,8 @@ def load_library(path: str = LIB_PATH):
         "asym_gemm_plan": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp,
                                ctypes.POINTER(GemmPlanInfo)]),
         "asym_gemm_set_small_m": (i, [i]),
+        "asym_gemm_bf16_noalloc": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp]),
+        "asym_gemm_noalloc_limits": (i, [ctypes.POINTER(ctypes.c_size_t), ip, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_attn_decode_bf16": (i, [topo_p, i, i, i, i, i, vp, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
         "asym_attn_decode_plan": (i, [topo_p, i, i, i, i, i, i, i, u32, vp, ctypes.POINTER(AttnPlanInfo)]),
         "asym_copy_bf16": (i, [topo_p, vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
@@ -670,6 +673,39 @@ def gemm(A, B, C=None, mapping="aware", topo: Optional[Topology] = None, xcd_mas
         ctypes.c_void_p(B.data_ptr()), B.stride(0), B_KN if kn else B_NK, ctypes.c_void_p(C.data_ptr()),
         C.stride(0), mp, xcd_mask, _stream_ptr(stream)))
     return C
+
+
+def gemm_noalloc(A, B, C, topo: "Topology", mapping="aware", xcd_mask: int = 0, stream=None):
+    """gemm() through the entry point that allocates no device memory (its
+    schedule, counters and split-K partials sit in the library's fixed
+    per-GPU array): A [M,K], B [N,K], C [M,N] bf16 CUDA tensors, all given;
+    topo must be a probed topology.  Calls that overlap on one GPU race."""
+    import torch
+    if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16 or C.dtype != torch.bfloat16:
+        raise TypeError("A, B and C must be bfloat16")
+    if A.dim() != 2 or B.dim() != 2 or A.shape[1] != B.shape[1]:
+        raise ValueError("A must be [M,K] and B [N,K]")
+    if A.stride(1) != 1 or B.stride(1) != 1 or C.stride(1) != 1:
+        raise ValueError("A, B and C must be row-major")
+    M, K = A.shape
+    N = B.shape[0]
+    if tuple(C.shape) != (M, N):
+        raise ValueError("C must be [M,N]")
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    _check(load_library().asym_gemm_bf16_noalloc(
+        topo.handle if topo else None, M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0),
+        ctypes.c_void_p(B.data_ptr()), B.stride(0), B_NK, ctypes.c_void_p(C.data_ptr()),
+        C.stride(0), mp, xcd_mask, _stream_ptr(stream)))
+    return C
+
+
+def noalloc_limits() -> dict:
+    """The per-GPU array of gemm_noalloc: its size, the most output tiles and
+    the most split-K partial bytes a call may need."""
+    sb, pb = ctypes.c_size_t(), ctypes.c_size_t()
+    mt = ctypes.c_int()
+    _check(load_library().asym_gemm_noalloc_limits(ctypes.byref(sb), ctypes.byref(mt), ctypes.byref(pb)))
+    return {"scratch_bytes": sb.value, "max_tiles": mt.value, "max_partial_bytes": pb.value}
 
 
 def gemm_grouped(A, B, M: Sequence[int], C=None, mapping="aware", topo: Optional[Topology] = None,

@@ -523,6 +523,87 @@ static int gemm_bf16_locked(const asym_topology* topo_in, int M, int N, int K, c
   return launch_gemm(g, stream);
 }
 
+// ---- the GEMM without allocation: every buffer in the caller's scratch ------
+// Which schedule each device's scratch area holds (written by the last call
+// that needed a different one); guarded by g_mu.
+std::map<int, ScheduleKey> g_scratch_schedule;
+
+int gemm_noalloc_check(const asym_topology* topo_in, int M, int N, int b_layout) {
+  if (!topo_in)
+    return fail(ASYM_EINVAL, "gemm (no allocation): needs a probed topology (a first-use probe would allocate)");
+  if (b_layout == ASYM_B_KN)
+    return fail(ASYM_EUNSUPPORTED, "gemm (no allocation): B stored [K][N] needs a transposed copy; store B as [N][K]");
+  // every tile width is at most 256, so this bound holds before the plan picks one
+  if (M >= 1 && N >= 1 && (int64_t)((M + 255) / 256) * ((N + 255) / 256) > kScratchMaxTiles)
+    return fail(ASYM_EINVAL, "gemm (no allocation): more than " + std::to_string(kScratchMaxTiles) +
+                                 " output tiles; the scratch area holds no larger schedule");
+  return ASYM_OK;
+}
+
+int gemm_bf16_scratch(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda, const void* B,
+                      int ldb, int b_layout, void* C, int ldc, int mapping, uint32_t xcd_mask,
+                      hipStream_t stream, unsigned char* scratch, size_t bytes) {
+  int rc = gemm_noalloc_check(topo_in, M, N, b_layout);
+  if (rc != ASYM_OK) return rc;
+  if (!scratch || bytes < kScratchBytes) return fail(ASYM_EINVAL, "gemm (no allocation): scratch area too small");
+  std::lock_guard<std::mutex> lock(g_mu);
+  GemmPlan P;
+  rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
+  if (rc != ASYM_OK) return rc;
+  if (P.small_mb) {
+    SmallMLaunch sm = small_m_launch(P, A, B, C, M, N, K, lda, ldb, ldc, mapping);
+    if (sm.ksplit > 1) {
+      if (small_m_part_bytes(sm) > kScratchPartBytes)
+        return fail(ASYM_EINVAL, "gemm (no allocation): split-K partials exceed the scratch area");
+      sm.part = reinterpret_cast<float*>(scratch + kScratchPartOff);
+    }
+    return launch_gemm_small_m(sm, stream);
+  }
+  const int64_t T = (int64_t)P.tiles_m * P.tiles_n;
+  if (T > kScratchMaxTiles)
+    return fail(ASYM_EINVAL, "gemm (no allocation): more than " + std::to_string(kScratchMaxTiles) +
+                                 " output tiles; the scratch area holds no larger schedule");
+  int* d_ctr = reinterpret_cast<int*>(scratch + kScratchCtrOff);
+  int* d_off = reinterpret_cast<int*>(scratch + kScratchOffOff);
+  int* d_slots = reinterpret_cast<int*>(scratch + kScratchSlotsOff);
+  int* d_order = reinterpret_cast<int*>(scratch + kScratchOrderOff);
+  ScheduleKey key{P.device, P.tiles_m, P.tiles_n, mapping, P.slots};
+  auto it = g_scratch_schedule.find(P.device);
+  if (it == g_scratch_schedule.end() || it->second < key || key < it->second) {
+    if (it != g_scratch_schedule.end()) g_scratch_schedule.erase(it);
+    Schedule sch;
+    rc = build_schedule(P.tiles_m, P.tiles_n, (int)P.slots.size(), P.slots.data(), mapping, 0, sch);
+    if (rc != ASYM_OK) return rc;
+    std::vector<int> off(ASYM_MAX_XCDS + 1, sch.off.back()), sl(ASYM_MAX_XCDS, 0);
+    for (size_t x = 0; x < sch.off.size(); ++x) off[x] = sch.off[x];
+    for (size_t x = 0; x < P.slots.size(); ++x) sl[x] = P.slots[x];
+    rc = launch_put_words(d_off, off.data(), off.size(), stream);
+    if (rc == ASYM_OK) rc = launch_put_words(d_slots, sl.data(), sl.size(), stream);
+    if (rc == ASYM_OK) rc = launch_put_words(d_order, sch.order.data(), sch.order.size(), stream);
+    if (rc != ASYM_OK) return rc;
+    g_scratch_schedule[P.device] = key;
+  }
+  // the claiming form needs its counters at zero (its last workgroup leaves
+  // them so, but the area keeps whatever the last call on it left)
+  if (mapping == ASYM_MAP_AWARE && P.dynamic) {
+    rc = launch_zero_words(d_ctr, 64, stream);
+    if (rc != ASYM_OK) return rc;
+  }
+  GemmLaunch g;
+  g.A = A; g.B = B; g.C = C;
+  g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
+  g.mapping = mapping;
+  g.d_order = d_order; g.d_off = d_off; g.d_slots = d_slots;
+  g.tiles_m = P.tiles_m; g.tiles_n = P.tiles_n;
+  g.n_xccs = P.t->n_xccs;
+  g.grid = P.grid;
+  g.d_ctr = d_ctr;
+  g.dynamic = P.dynamic;
+  g.vec = P.vec;
+  g.bn = P.bn;
+  return launch_gemm(g, stream);
+}
+
 int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N, int K, const void* A,
                       int lda, const void* B, int ldb, void* C, int ldc, int mapping, uint32_t xcd_mask,
                       hipStream_t stream) {

@@ -73,6 +73,18 @@ copy_kernel(v4u* __restrict__ dst, const v4u* __restrict__ src, size_t n16, int 
   }
 }
 
+// Up to kPutWords 4-byte words carried in the kernel's arguments, written to
+// device memory: host data reaches the device without a staging buffer or a
+// copy engine (the runtime copies kernel arguments itself).
+constexpr int kPutWords = 960;
+struct PutWords {
+  int w[kPutWords];
+};
+
+__global__ void put_words_kernel(int* __restrict__ dst, int n, PutWords src) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = src.w[i];
+}
+
 __global__ void zero_words_kernel(uint32_t* p, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = 0u;
@@ -102,6 +114,21 @@ int launch_copy(void* dst, const void* src, size_t n_bytes, int passes, const in
   hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(kCopyThreads), 0, s, static_cast<v4u*>(dst),
                      static_cast<const v4u*>(src), n_bytes / 16, passes, stop_flag, sh, n_x);
   ASYM_HIP(hipGetLastError());
+  return ASYM_OK;
+}
+
+// dst[0 .. n) = host[0 .. n), ordered on stream s, through kernel arguments
+// (ceil(n / 960) launches).
+int launch_put_words(int* dst, const int* host, size_t n, hipStream_t s) {
+  if (!n) return ASYM_OK;
+  if (!dst || !host) return fail(ASYM_EINVAL, "put words: null pointer");
+  for (size_t i = 0; i < n; i += kPutWords) {
+    const int m = (int)std::min<size_t>(kPutWords, n - i);
+    PutWords w{};
+    for (int j = 0; j < m; ++j) w.w[j] = host[i + j];
+    hipLaunchKernelGGL(put_words_kernel, dim3(1), dim3(256), 0, s, dst + i, m, w);
+    ASYM_HIP(hipGetLastError());
+  }
   return ASYM_OK;
 }
 

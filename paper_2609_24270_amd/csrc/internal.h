@@ -198,6 +198,28 @@ int launch_copy(void* dst, const void* src, size_t n_bytes, int passes, const in
 int launch_transpose_bf16(const void* src, int rows, int cols, int lds, void* dst, int ldd, hipStream_t s);
 // zero n 4-byte words at p, ordered on stream s
 int launch_zero_words(void* p, size_t n, hipStream_t s);
+// dst[0 .. n) = host[0 .. n) (4-byte words), ordered on stream s, carried in
+// kernel arguments: no staging buffer, no allocation
+int launch_put_words(int* dst, const int* host, size_t n, hipStream_t s);
+
+// GEMM with every device buffer beyond A, B and C (tile schedule, claim
+// counters, split-K partials) in the caller's scratch area of `bytes` bytes
+// at device address `scratch` (layout below); allocates no device memory.
+// Calls that share one scratch area and overlap in time race.
+constexpr size_t kScratchCtrOff = 0;              // 64 ints: claim counters
+constexpr size_t kScratchOffOff = 256;            // ASYM_MAX_XCDS + 1 ints: region offsets
+constexpr size_t kScratchSlotsOff = 384;          // ASYM_MAX_XCDS ints: workers per XCD
+constexpr size_t kScratchOrderOff = 512;          // the tile order
+constexpr size_t kScratchPartOff = 1u << 20;      // fp32 partial tiles of a split K
+constexpr size_t kScratchPartBytes = 4u << 20;
+constexpr size_t kScratchBytes = kScratchPartOff + kScratchPartBytes;
+constexpr int kScratchMaxTiles = (int)((kScratchPartOff - kScratchOrderOff) / sizeof(int));
+// the checks that need no device: a topology given, [N][K] storage, a tile
+// count within the array's schedule
+int gemm_noalloc_check(const asym_topology* topo, int M, int N, int b_layout);
+int gemm_bf16_scratch(const asym_topology* topo, int M, int N, int K, const void* A, int lda, const void* B,
+                      int ldb, int b_layout, void* C, int ldc, int mapping, uint32_t xcd_mask,
+                      hipStream_t stream, unsigned char* scratch, size_t bytes);
 void release_workspace(hipStream_t s);
 
 // Stream CU mask -> CU set seen by the scheduler.

@@ -476,3 +476,25 @@ def test_topology_cache_round_trip_and_staleness(lib, tmp_path):
     assert asym.topology_load(path, key).info()["cus_per_xcd"] == [32] * 8
     with pytest.raises(asym.AsymError):
         asym.topology_load(path, key, asym.PROBE_MASKMAP)
+
+
+def test_noalloc_rejections_need_no_device(lib):
+    """The no-allocation GEMM refuses, before any device call, what its fixed
+    per-GPU array cannot serve: no topology (a first-use probe would
+    allocate), B stored [K][N] (a transposed copy would be needed), and more
+    output tiles than the array's schedule holds."""
+    import ctypes
+    lib_ = asym.load_library()
+    lim = asym.noalloc_limits()
+    assert lim["scratch_bytes"] == (5 << 20) and lim["max_tiles"] == ((1 << 20) - 512) // 4
+    assert lim["max_partial_bytes"] == 4 << 20
+    t = asym.topology_from_records(fake_records(uniform_layout()), 256, 8)
+    P = ctypes.c_void_p(0x1000)
+    assert lib_.asym_gemm_bf16_noalloc(None, 64, 64, 64, P, 64, P, 64, 0, P, 64, 0, 0, None) == asym.EINVAL
+    assert "topology" in asym.last_error()
+    assert lib_.asym_gemm_bf16_noalloc(t.handle, 64, 64, 64, P, 64, P, 64, 1, P, 64, 0, 0, None) == \
+        asym.EUNSUPPORTED
+    side = 131072  # 512 x 512 tiles of 256 > 262016
+    assert lib_.asym_gemm_bf16_noalloc(t.handle, side, side, 8, P, 8, P, 8, 0, P, side, 0, 0, None) == \
+        asym.EINVAL
+    assert "output tiles" in asym.last_error()
