@@ -199,6 +199,9 @@ class ClockPowerSampler:
                 f = os.path.join(d, name)
                 if os.path.exists(f) and name not in self.files:
                     self.files[name] = f
+        dpm = f"/sys/bus/pci/devices/{pci_bus_id}/pp_dpm_sclk"
+        if "freq1_input" not in self.files and os.path.exists(dpm):
+            self.files["pp_dpm_sclk"] = dpm
         self.samples = {k: [] for k in self.files}
         self._stop = threading.Event()
         self._t = threading.Thread(target=self._run, daemon=True)
@@ -206,7 +209,14 @@ class ClockPowerSampler:
     def _read(self, name):
         try:
             with open(self.files[name]) as f:
-                return float(f.read().split()[0])
+                text = f.read()
+            if name == "pp_dpm_sclk":
+                # the current level is the line marked '*', e.g. "1: 1950Mhz *"; in Hz like freq1_input
+                for ln in text.splitlines():
+                    if ln.rstrip().endswith("*"):
+                        return 1e6 * float(ln.split(":")[1].strip().lower().split("mhz")[0])
+                return None
+            return float(text.split()[0])
         except (OSError, ValueError, IndexError):
             return None
 
@@ -231,7 +241,7 @@ class ClockPowerSampler:
     def summary(self) -> dict:
         mean = lambda v: sum(v) / len(v) if v else None
         pw = self.samples.get("power1_average") or self.samples.get("power1_input") or []
-        fr = self.samples.get("freq1_input") or []
+        fr = self.samples.get("freq1_input") or self.samples.get("pp_dpm_sclk") or []
         cap = self._read("power1_cap") if "power1_cap" in self.files else None
         return {"sclk_mhz_mean": round(mean(fr) / 1e6, 1) if fr else None,
                 "power_w_mean": round(mean(pw) / 1e6, 1) if pw else None,
@@ -318,6 +328,27 @@ def llm_shapes(dev, stream, rounds: int):
         out[p.name] = {"M": p.M, "N": p.N, "K": p.K,
                        **{m: round(p.flops / (ms[m] * 1e-3) / 1e12, 2) for m in MAPPINGS}}
     return out
+
+
+def square_512(topo, dev, stream, launches: int = 50, rounds: int = 8):
+    """512^3 (uniform[-1,1], seed 0) on the full GPU: the three mappings, each
+    launch short enough that launches are queued behind a spin kernel and
+    averaged; 128 x 128 tiles (16 tiles)."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    A, B = workloads.make_inputs(workloads.SQUARE_512)
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.empty((512, 512), dtype=torch.bfloat16, device=dev)
+    fns = {m: (lambda m=m: asym.gemm(Ad, Bd, C, mapping=m, topo=topo, stream=stream)) for m in MAPPINGS}
+    for f in fns.values():
+        f()
+    ms = queued(fns, launches, rounds, stream)
+    plan = asym.gemm_plan(Ad, Bd, C, topo=topo, stream=stream)
+    return {"tile": [plan["tile_m"], plan["tile_n"]], "tiles": plan["tiles_m"] * plan["tiles_n"],
+            **{m: {"us": round(1e3 * ms[m], 2), "tflops": round(2 * 512 ** 3 / (ms[m] * 1e-3) / 1e12, 2)}
+               for m in MAPPINGS}}
 
 
 def decode_gemm(dev, stream, launches: int = 20, rounds: int = 5):
@@ -897,6 +928,7 @@ def main() -> int:
         line["context"] = {"torch_matmul_tflops": round(p.flops / (tot / 10 * 1e-3) / 1e12, 2)}
         del Bt
     if "llm" in studies:
+        line["square_512"] = square_512(topo, dev, stream)
         line["llm_shapes_tflops"] = llm_shapes(dev, stream, 20)
         line["decode_gemm"] = decode_gemm(dev, stream)
     if "pd" in studies:

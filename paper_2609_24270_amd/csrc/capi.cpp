@@ -230,7 +230,7 @@ struct GemmPlan {
   int total = 0, smax = 0;
   bool vec = false, dynamic = false, whole = true;
   bool vec_ab = false;  // A and B alone meet the vector-path alignment
-  int bn = 0, tiles_m = 0, tiles_n = 0, grid = 0;
+  int bn = 0, bm = 256, tiles_m = 0, tiles_n = 0, grid = 0;
   int small_mb = 0;  // > 0: the small-M kernel with this many 16-row blocks
   bool b_transposed = false;  // B stored [K][N]: transposed into a library buffer first
 };
@@ -351,7 +351,7 @@ static int cu_set_for(const asym_topology* topo_in, int mapping, uint32_t xcd_ma
 
 static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda,
                      const void* B, int ldb, int b_layout, const void* C, int ldc, int mapping,
-                     uint32_t xcd_mask, hipStream_t stream, GemmPlan* P) {
+                     uint32_t xcd_mask, hipStream_t stream, GemmPlan* P, bool small_tiles = true) {
   if (M < 1 || N < 1 || K < 1) return fail(ASYM_EINVAL, "gemm: M, N, K must be >= 1");
   if (!A || !B || !C) return fail(ASYM_EINVAL, "gemm: null matrix pointer");
   if (lda < K || ldc < N) return fail(ASYM_EINVAL, "gemm: leading dimension too small");
@@ -391,8 +391,17 @@ static int plan_gemm(const asym_topology* topo_in, int M, int N, int K, const vo
   P->smax = smax;
   P->vec = vec;
   P->vec_ab = vec_ab;
+  P->bm = (int)BMr;
   P->bn = vec ? choose_tile_width(M, N, total) : (int)BNr;
-  P->tiles_m = (int)((M + BMr - 1) / BMr);
+  // A product whose 256 x 256 tiles would leave three quarters of the workers
+  // idle takes 128 x 128 tiles on the register-staged path: four times the
+  // tiles, at most one round (512^3: 16 tiles instead of 4).  Each output is
+  // the same MFMA chain either way, so the bits do not change.
+  if (small_tiles && ((int64_t)(M + BMr - 1) / BMr) * ((N + BNr - 1) / BNr) * 4 <= total) {
+    P->bm = 128;
+    P->bn = 128;
+  }
+  P->tiles_m = (M + P->bm - 1) / P->bm;
   P->tiles_n = (N + P->bn - 1) / P->bn;
   P->grid = mapping == ASYM_MAP_AWARE ? t->n_xccs * smax : total;
   // The aware grid deals smax workgroups to every XCD.  Where an XCD has fewer
@@ -520,6 +529,7 @@ static int gemm_bf16_locked(const asym_topology* topo_in, int M, int N, int K, c
   g.dynamic = P.dynamic;
   g.vec = P.vec;
   g.bn = P.bn;
+  g.bm = P.bm;
   return launch_gemm(g, stream);
 }
 
@@ -601,6 +611,7 @@ int gemm_bf16_scratch(const asym_topology* topo_in, int M, int N, int K, const v
   g.dynamic = P.dynamic;
   g.vec = P.vec;
   g.bn = P.bn;
+  g.bm = P.bm;
   return launch_gemm(g, stream);
 }
 
@@ -636,7 +647,8 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   // (the weights: G * N rows of B)
   GemmPlan P;
   const int virt_m = (int)std::max<int64_t>(1, trows * gemm_tile_m());
-  int rc = plan_gemm(topo_in, virt_m, N, K, A, lda, B, ldb, ASYM_B_NK, C, ldc, mapping, xcd_mask, stream, &P);
+  int rc = plan_gemm(topo_in, virt_m, N, K, A, lda, B, ldb, ASYM_B_NK, C, ldc, mapping, xcd_mask, stream, &P,
+                     false);
   if (rc != ASYM_OK) return rc;
   const int max_rows = *std::max_element(Ms, Ms + G);
   long long wgs64 = 0;
@@ -975,7 +987,7 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
     out->small_m = 1;
     return ASYM_OK;
   }
-  out->tile_m = gemm_tile_m();
+  out->tile_m = P.bm;
   out->tile_n = P.bn;
   out->tiles_m = P.tiles_m;
   out->tiles_n = P.tiles_n;

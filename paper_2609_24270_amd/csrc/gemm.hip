@@ -85,7 +85,7 @@ struct TileGeom {
   int m0, rows, b0, n0;
 };
 
-__device__ __forceinline__ TileGeom tile_geom(const Params& p, int tile, int width) {
+__device__ __forceinline__ TileGeom tile_geom(const Params& p, int tile, int width, int height = BM) {
   TileGeom g;
   if (p.desc) {
     const int4 d = p.desc[tile];
@@ -95,8 +95,8 @@ __device__ __forceinline__ TileGeom tile_geom(const Params& p, int tile, int wid
     g.n0 = __builtin_amdgcn_readfirstlane(d.w);
   } else {
     const int tm = tile / p.tiles_n, tn = tile - tm * p.tiles_n;
-    g.m0 = tm * BM;
-    g.rows = min(BM, p.M - g.m0);
+    g.m0 = tm * height;
+    g.rows = min(height, p.M - g.m0);
     g.b0 = 0;
     g.n0 = tn * width;
   }
@@ -126,21 +126,21 @@ typedef unsigned v2u __attribute__((ext_vector_type(2)));
 // k >= K are sent out of range as well.  The per-thread part of the offset is
 // one VGPR (`vo`, row t/8 and chunk t%8 at k = 0); the row-block and k parts
 // are uniform and go in the scalar offset.
-template <bool VEC>
-__device__ __forceinline__ void load_tile(uint4 (&r)[8], __amdgpu_buffer_rsrc_t rs, int ld,
+template <bool VEC, int NR = 8>
+__device__ __forceinline__ void load_tile(uint4 (&r)[NR], __amdgpu_buffer_rsrc_t rs, int ld,
                                           uint32_t vo, int K, int k0) {
   const int kc = (threadIdx.x & 7) * 8;
   if constexpr (VEC) {
     const uint32_t v = k0 + kc < K ? vo : kOOB;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < NR; ++i) {
       const int so = (32 * i * ld + k0) * 2;
       const v4u x = __builtin_amdgcn_raw_buffer_load_b128(rs, v, so, 0);
       r[i] = make_uint4(x.x, x.y, x.z, x.w);
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < NR; ++i) {
       const int so = (32 * i * ld + k0) * 2;
       uint32_t w[4];
 #pragma unroll
@@ -155,11 +155,12 @@ __device__ __forceinline__ void load_tile(uint4 (&r)[8], __amdgpu_buffer_rsrc_t 
   }
 }
 
-__device__ __forceinline__ void store_tile(uint16_t* __restrict__ s, const uint4 (&r)[8]) {
+template <int NR = 8>
+__device__ __forceinline__ void store_tile(uint16_t* __restrict__ s, const uint4 (&r)[NR]) {
   const int t = threadIdx.x;
   const int kc = (t & 7) * 8;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < NR; ++i) {
     const int row = (t >> 3) + 32 * i;
     *reinterpret_cast<uint4*>(s + row * LDP + kc) = r[i];
   }
@@ -170,31 +171,39 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-template <bool VEC>
+// Register-staged path: tiles TE x TE (TE = 256, or 128 for products too
+// small to give every CU a 256-wide tile), 4 waves of TE/2 x TE/2, k-stages
+// of 64 in two padded LDS buffers.  Each output is the same chain of MFMAs as
+// on the vector path (k-stages in order, two 32-wide steps each), so every
+// tile size gives the same bits.
+template <bool VEC, int TE = 256>
 __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t* sA, uint16_t* sB) {
-  const TileGeom tg = tile_geom(p, tile, BN);
+  constexpr int TW = TE / 2;      // per-wave rows and columns
+  constexpr int FR = TW / 16;     // fragments per wave and dimension
+  constexpr int NR = TE / 32;     // rows per thread in the tile loads
+  const TileGeom tg = tile_geom(p, tile, TE, TE);
   const int m0 = tg.m0, n0 = tg.n0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int KT = (p.K + BK - 1) / BK;
 
-  f32x4 acc[8][8];
+  f32x4 acc[FR][FR];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < FR; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < FR; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int rows_a = tg.rows, rows_b = min(BN, p.N - n0);
+  const int rows_a = tg.rows, rows_b = min(TE, p.N - n0);
   const __amdgpu_buffer_rsrc_t rsa = make_rsrc(p.A + (size_t)m0 * p.lda, (uint32_t)rows_a * p.lda * 2u);
   const __amdgpu_buffer_rsrc_t rsb =
       make_rsrc(p.B + (size_t)(tg.b0 + n0) * p.ldb, (uint32_t)rows_b * p.ldb * 2u);
   const uint32_t voa = (uint32_t)((threadIdx.x >> 3) * p.lda + (threadIdx.x & 7) * 8) * 2u;
   const uint32_t vob = (uint32_t)((threadIdx.x >> 3) * p.ldb + (threadIdx.x & 7) * 8) * 2u;
-  uint4 ra[8], rb[8];
-  load_tile<VEC>(ra, rsa, p.lda, voa, p.K, 0);
-  load_tile<VEC>(rb, rsb, p.ldb, vob, p.K, 0);
-  store_tile(sA, ra);
-  store_tile(sB, rb);
+  uint4 ra[NR], rb[NR];
+  load_tile<VEC, NR>(ra, rsa, p.lda, voa, p.K, 0);
+  load_tile<VEC, NR>(rb, rsb, p.ldb, vob, p.K, 0);
+  store_tile<NR>(sA, ra);
+  store_tile<NR>(sB, rb);
   __syncthreads();
 
   const int lrow = lane & 15, lk = (lane >> 4) * 8;
@@ -202,28 +211,28 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
     const int cur = kt & 1;
     const bool more = kt + 1 < KT;
     if (more) {
-      load_tile<VEC>(ra, rsa, p.lda, voa, p.K, (kt + 1) * BK);
-      load_tile<VEC>(rb, rsb, p.ldb, vob, p.K, (kt + 1) * BK);
+      load_tile<VEC, NR>(ra, rsa, p.lda, voa, p.K, (kt + 1) * BK);
+      load_tile<VEC, NR>(rb, rsb, p.ldb, vob, p.K, (kt + 1) * BK);
     }
-    const uint16_t* a_s = sA + cur * (BM * LDP) + (wm * WM + lrow) * LDP + lk;
-    const uint16_t* b_s = sB + cur * (BN * LDP) + (wn * WN + lrow) * LDP + lk;
+    const uint16_t* a_s = sA + cur * (TE * LDP) + (wm * TW + lrow) * LDP + lk;
+    const uint16_t* b_s = sB + cur * (TE * LDP) + (wn * TW + lrow) * LDP + lk;
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8 xa[8], xb[8];
+      bf16x8 xa[FR], xb[FR];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < FR; ++i) {
         xa[i] = *reinterpret_cast<const bf16x8*>(a_s + i * 16 * LDP + ks * 32);
         xb[i] = *reinterpret_cast<const bf16x8*>(b_s + i * 16 * LDP + ks * 32);
       }
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb)
+      for (int nb = 0; nb < FR; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < 8; ++mb)
+        for (int mb = 0; mb < FR; ++mb)
           acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xb[nb], xa[mb], acc[nb][mb], 0, 0, 0);
     }
     if (more) {
-      store_tile(sA + (cur ^ 1) * (BM * LDP), ra);
-      store_tile(sB + (cur ^ 1) * (BN * LDP), rb);
+      store_tile<NR>(sA + (cur ^ 1) * (TE * LDP), ra);
+      store_tile<NR>(sB + (cur ^ 1) * (TE * LDP), rb);
     }
     __syncthreads();
   }
@@ -233,14 +242,14 @@ __device__ __forceinline__ void compute_tile(const Params& p, int tile, uint16_t
   const int rows_c = tg.rows;
   const __amdgpu_buffer_rsrc_t rsc = make_rsrc(p.C + (size_t)m0 * p.ldc, (uint32_t)rows_c * p.ldc * 2u);
 #pragma unroll
-  for (int nb = 0; nb < 8; ++nb) {
-    const int n = n0 + wn * WN + nb * 16 + (lane >> 4) * 4;
+  for (int nb = 0; nb < FR; ++nb) {
+    const int n = n0 + wn * TW + nb * 16 + (lane >> 4) * 4;
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
-      const int ml = wm * WM + mb * 16 + lrow;
+    for (int mb = 0; mb < FR; ++mb) {
+      const int ml = wm * TW + mb * 16 + lrow;
       const f32x4 v = acc[nb][mb];
       const uint32_t base = (uint32_t)(ml * p.ldc + n) * 2u;
-      if (VEC && n + 3 < p.N) {
+      if (VEC && n + 3 < p.N && ((((uintptr_t)p.C) & 7u) == 0) && (p.ldc % 4 == 0)) {
         v2u w;
         w.x = pack_bf16x2(v[0], v[1]);
         w.y = pack_bf16x2(v[2], v[3]);
@@ -741,13 +750,15 @@ __device__ __forceinline__ int steal_aware(const Params& p, int xcc, int q_lane)
   return -1;
 }
 
-template <bool VEC, int NBF>
+// TE = 0: the vector path's direct-to-LDS rings (256 x 32 NBF tiles);
+// otherwise the register-staged path with TE x TE tiles.
+template <bool VEC, int NBF, int TE>
 __device__ __forceinline__ void run_tile(const Params& p, int tile, unsigned char* lds, NextTile& nt) {
-  if constexpr (VEC) {
+  if constexpr (TE == 0) {
     compute_tile_ring<NBF>(p, tile, lds, nt);
   } else {
-    compute_tile<false>(p, tile, reinterpret_cast<uint16_t*>(lds),
-                        reinterpret_cast<uint16_t*>(lds) + 2 * BM * LDP);
+    compute_tile<VEC, TE>(p, tile, reinterpret_cast<uint16_t*>(lds),
+                          reinterpret_cast<uint16_t*>(lds) + 2 * TE * LDP);
     issue_next(nt);
   }
 }
@@ -763,10 +774,10 @@ __device__ __forceinline__ int read_box(const int* box) {
   return v;
 }
 
-template <bool VEC, int NBF>
+template <bool VEC, int NBF, int TE = 0>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 gemm_bf16_persistent(Params p) {
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[VEC ? RING_BYTES : 2 * (BM + BN) * LDP * 2];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[TE == 0 ? RING_BYTES : 2 * (2 * TE) * LDP * 2];
   int* const box = reinterpret_cast<int*>(lds);  // tile broadcast, used between tiles only
 
   // Static aware assignment: workgroup b belongs to XCD b mod n and is that
@@ -840,7 +851,7 @@ gemm_bf16_persistent(Params p) {
   }
   while (tile >= 0) {
     nt.i_next += nt.step;
-    run_tile<VEC, NBF>(p, tile, lds, nt);
+    run_tile<VEC, NBF, TE>(p, tile, lds, nt);
     if (threadIdx.x < 64) {
       const int nxt = take_next(p, nt, xcc, q_lane);
       if (lane == 0) box[0] = nxt;
@@ -873,8 +884,15 @@ int launch_gemm(const GemmLaunch& g, hipStream_t s) {
   p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots; p.ctr = g.d_ctr;
   p.dynamic = g.dynamic ? 1 : 0;
   p.desc = static_cast<const int4*>(g.d_desc);
-  if (!g.vec)
-    hipLaunchKernelGGL((gemm_bf16_persistent<false, 8>), dim3(g.grid), dim3(NT), 0, s, p);
+  if (g.bm == 128 && g.bn == 128) {
+    if (g.vec)
+      hipLaunchKernelGGL((gemm_bf16_persistent<true, 8, 128>), dim3(g.grid), dim3(NT), 0, s, p);
+    else
+      hipLaunchKernelGGL((gemm_bf16_persistent<false, 8, 128>), dim3(g.grid), dim3(NT), 0, s, p);
+  } else if (g.bm != 256) {
+    return fail(ASYM_EINVAL, "gemm: unsupported tile height");
+  } else if (!g.vec)
+    hipLaunchKernelGGL((gemm_bf16_persistent<false, 8, 256>), dim3(g.grid), dim3(NT), 0, s, p);
   else if (g.bn == 256)
     hipLaunchKernelGGL((gemm_bf16_persistent<true, 8>), dim3(g.grid), dim3(NT), 0, s, p);
   else if (g.bn == 224)

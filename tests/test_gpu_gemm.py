@@ -142,6 +142,24 @@ def test_gemm_strided_and_unaligned(dev):
     assert torch.all(Cp[:, N:].cpu() == 7.0)
 
 
+def test_gemm_128_tiles_equal_256_tiles_bitwise(dev):
+    """The 128 x 128 tiles of a small product give bitwise the outputs the
+    256 x 256 tiles give for the same rows and columns of a larger product
+    with the same K (each output is the same MFMA chain): on the vector path
+    (K multiple of 8) and on the predicated path (K = 1000 + 4)."""
+    for K, big in ((1024, 4096), (1004, 2304)):
+        A, B = workloads.make_inputs(workloads.make_problem(big, big, K, seed=K))
+        Ad, Bd = A.to(dev), B.to(dev)
+        assert asym.gemm_plan(Ad, Bd)["tile_m"] == 256
+        assert asym.gemm_plan(Ad[:512], Bd[:384])["tile_m"] == 128
+        C_big = asym.gemm(Ad, Bd)
+        C_small = asym.gemm(Ad[:512].contiguous(), Bd[:384].contiguous())
+        torch.cuda.synchronize()
+        assert torch.equal(C_small, C_big[:512, :384]), K
+        R, _ = oracle.gemm_bf16(bits(A[:512]), bits(B[:384]), "nk")
+        assert_gemm_close(bits(C_small), R, what=f"128 tiles, K={K}")
+
+
 @pytest.mark.parametrize("M,N,K", [(512, 512, 512), (300, 520, 264), (129, 1000, 77), (32, 4096, 4096),
                                    (1000, 136, 2056)])
 def test_gemm_b_stored_kn_equals_nk(dev, M, N, K):
@@ -200,7 +218,7 @@ def test_gemm_llm_shapes_sampled(dev, p):
 # leaves the persistent workers the fewest rounds of tiles.  With the aware
 # grid kept to XCD 0 (32 workers) and two tile rows, each width is the choice
 # for one of these shapes, every one with ragged M, N and K tails.
-WIDTH_CASES = [(256, 500, 4092, 328), (224, 500, 3548, 328), (192, 500, 700, 328)]
+WIDTH_CASES = [(256, 500, 4092, 328), (224, 500, 3548, 328), (192, 500, 1100, 328)]
 
 
 @pytest.mark.parametrize("width,M,N,K", WIDTH_CASES, ids=lambda v: str(v))
@@ -214,9 +232,10 @@ def test_gemm_tile_widths_elementwise(dev, width, M, N, K):
     C = run(Ad, Bd, "aware", xcd_mask=1)
     e = assert_gemm_close(bits(C), R, what=f"width {width} {M}x{N}x{K}")
     print(f"width {width} {M}x{N}x{K}: max rel err {e:.3e}")
-    # a different width over the whole chip gives the same bits
+    # other tiles over the whole chip (128 x 128: these products have too few
+    # 256-row tiles for 256 workers) give the same bits
     full = asym.gemm_plan(Ad, Bd, mapping="aware")
-    assert full["tile_n"] == 192 and full["workers"] == 256, full
+    assert (full["tile_m"], full["tile_n"]) == (128, 128) and full["workers"] == 256, full
     assert torch.equal(run(Ad, Bd, "aware"), C)
 
 
@@ -236,8 +255,16 @@ def test_gemm_plan_full_sizes(dev):
     p = asym.gemm_plan(mapping="aware", M=8192, N=8192, K=8192, xcd_mask=0x0F)
     assert p["claims"] == 1 and p["workers"] == 128 and p["workers_per_xcd"] == [32] * 4 + [0] * 4
     # the predicated path keeps the 256-wide tile
-    p = asym.gemm_plan(mapping="aware", M=300, N=700, K=150)
-    assert p["vector_path"] == 0 and p["tile_n"] == 256
+    p = asym.gemm_plan(mapping="aware", M=2304, N=2304, K=150)
+    assert p["vector_path"] == 0 and (p["tile_m"], p["tile_n"]) == (256, 256)
+    # products whose 256 x 256 tiles would leave 3/4 of the workers idle take 128 x 128 tiles
+    for (M, N, K) in ((512, 512, 512), (300, 700, 150), (2048, 2048, 1024), (129, 1000, 77)):
+        p = asym.gemm_plan(mapping="aware", M=M, N=N, K=K)
+        assert (p["tile_m"], p["tile_n"]) == (128, 128), (M, N, K, p)
+        assert (p["tiles_m"], p["tiles_n"]) == (-(-M // 128), -(-N // 128))
+    p = asym.gemm_plan(mapping="aware", M=512, N=512, K=512, xcd_mask=0x01)      # 32 workers
+    assert (p["tile_m"], p["tiles_m"], p["tiles_n"]) == (128, 4, 4)
+    assert asym.gemm_plan(mapping="aware", M=2304, N=2048, K=1024)["tile_m"] == 256
 
 
 def test_gemm_plan_rejects_like_launch(dev):
@@ -258,7 +285,7 @@ def test_gemm_plan_rejects_like_launch(dev):
 # The last three give each of the 32 workgroups two tiles (the rings run on
 # from one tile into the next), with K of 7 stages, of 2 (the fewest that run
 # on) and of 1 (each tile starts with its own prologue).
-STAGE_CASES = [(256, 500, 4092, 7), (224, 500, 3548, 5), (192, 500, 700, 8),
+STAGE_CASES = [(256, 500, 4092, 7), (224, 500, 3548, 5), (192, 500, 1100, 8),
                (256, 1000, 4092, 7), (256, 1000, 4092, 2), (256, 1000, 4092, 1)]
 
 
