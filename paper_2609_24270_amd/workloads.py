@@ -359,3 +359,54 @@ def make_attn_inputs_on(p: AttnProblem, device):
     k = torch.randn((p.B, p.Hkv, p.S, p.D), generator=g, device=device).to(torch.bfloat16)
     v = torch.randn((p.B, p.Hkv, p.S, p.D), generator=g, device=device).to(torch.bfloat16)
     return q, k, v
+
+
+# Multi-head latent attention, decode (Section 7.1 attention workloads;
+# Appendix F counts one compressed row of 512 + 64 values per token).  One
+# query token per request; query heads 16 (a tensor-parallel shard of a
+# 128-head model) or 128; each request caches one 576-wide row per token
+# (512 latent values, which are also the value, then 64 rotary key values).
+# Recipe: one torch CPU generator per problem seeded `seed`, q then the cache
+# drawn N(0, 1) in fp32 in their storage shapes and rounded to bf16.  Layout:
+# q [B, H_q, 576], cache [B, S_k, 576], O [B, H_q, 512].  The scale is
+# 1 / sqrt(192), the per-head query-key width before the projections are
+# absorbed (128 non-rotary + 64 rotary).  Working set 2 B S_k (512 + 64) bytes.
+MLA_D_QK = 576
+MLA_D_V = 512
+
+
+@dataclass(frozen=True)
+class MlaProblem:
+    name: str
+    B: int
+    Hq: int
+    S: int
+    seed: int = 7
+
+    @property
+    def kv_bytes(self) -> int:
+        return 2 * self.B * self.S * MLA_D_QK
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(192.0)
+
+
+def mla_problem(B: int, Hq: int, S: int, seed: int = 7) -> MlaProblem:
+    return MlaProblem(f"mla_decode_B{B}_H{Hq}_S{S}", B, Hq, S, seed=seed)
+
+
+def make_mla_inputs(p: MlaProblem):
+    """(q [B, H_q, 576], cache [B, S_k, 576]) bf16 CPU tensors."""
+    g = torch.Generator(device="cpu").manual_seed(p.seed)
+    q = torch.randn((p.B, p.Hq, MLA_D_QK), generator=g).to(torch.bfloat16)
+    kv = torch.randn((p.B, p.S, MLA_D_QK), generator=g).to(torch.bfloat16)
+    return q, kv
+
+
+def make_mla_inputs_on(p: MlaProblem, device):
+    """Same shapes and distribution drawn on `device` (timing runs at full size)."""
+    g = torch.Generator(device=device).manual_seed(p.seed)
+    q = torch.randn((p.B, p.Hq, MLA_D_QK), generator=g, device=device).to(torch.bfloat16)
+    kv = torch.randn((p.B, p.S, MLA_D_QK), generator=g, device=device).to(torch.bfloat16)
+    return q, kv
