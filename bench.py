@@ -732,7 +732,103 @@ def attention_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: 
     return {"configs": out, "random_128_cu_set_with_tenant": res}
 
 
-FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "chunk_read")
+def mla_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 3):
+    """Latent-attention decode (576-wide cache rows shared by all query heads):
+    16 and 128 query heads over batch and KV length, W = 2 B S_k (512 + 64)
+    bytes per time, aware and oblivious on the full GPU; then on CU sets with
+    unequal counts: the two I/O dies at 28 and 32 CUs per XCD (the analog of
+    the paper's 70/78-SM partitions), and a seeded random 128-CU set with the
+    same attention on the complementary CUs."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    out = {}
+    for Hq in (16, 128):
+        for B in (1, 16, 64):
+            for S in (4096, 32768):
+                p = workloads.mla_problem(B, Hq, S)
+                q, kv = workloads.make_mla_inputs_on(p, dev)
+                o = torch.empty((B, Hq, 512), dtype=torch.bfloat16, device=dev)
+                fns = {m: (lambda m=m: asym.mla_decode(q, kv, o, mapping=m, topo=topo, stream=stream))
+                       for m in ("aware", "oblivious_rowmajor")}
+                for f in fns.values():
+                    f()
+                ms = queued(fns, launches, rounds, stream)
+                flops = 2.0 * B * Hq * S * (576 + 512)
+                out[p.name] = {"W_GB": round(p.kv_bytes / 1e9, 4),
+                               **{f"{m}_us": round(1e3 * t, 2) for m, t in ms.items()},
+                               "aware_TBps_W": round(p.kv_bytes / (ms["aware"] * 1e-3) / 1e12, 3),
+                               "aware_tflops": round(flops / (ms["aware"] * 1e-3) / 1e12, 1),
+                               "speedup_vs_oblivious": round(ms["oblivious_rowmajor"] / ms["aware"], 4)}
+                del q, kv, o
+    torch.cuda.empty_cache()
+    uneven = {}
+    if masked:
+        # die-uneven set: 4 CUs taken off each XCD of the first I/O die (28 / 32 CUs per XCD)
+        g = topo.info()["group_of_xcd"]
+        die0 = [x for x in range(8) if (g[x] == 0 if g and min(g) >= 0 else x < 4)]
+        cus = topo.cus()
+        drop, seen = set(), {x: 0 for x in die0}
+        for c in cus:
+            if c["xcc"] in seen and seen[c["xcc"]] < 4:
+                drop.add(c["mask_bit"])
+                seen[c["xcc"]] += 1
+        die_mask = [c["mask_bit"] for c in cus if c["mask_bit"] not in drop]
+        for name, (B, Hq, S) in (("B64_H128_S8192", (64, 128, 8192)), ("B16_H16_S32768", (16, 16, 32768))):
+            p = workloads.mla_problem(B, Hq, S)
+            q, kv = workloads.make_mla_inputs_on(p, dev)
+            o = torch.empty((B, Hq, 512), dtype=torch.bfloat16, device=dev)
+            s = asym.stream_create(topo, die_mask)
+            try:
+                fns = {m: (lambda m=m: asym.mla_decode(q, kv, o, mapping=m, topo=topo, stream=s))
+                       for m in ("aware", "oblivious_rowmajor")}
+                for f in fns.values():
+                    f()
+                ms = queued(fns, launches, rounds, s)
+            finally:
+                asym.stream_destroy(s)
+            uneven[f"die_28_32_{name}"] = {"cus_per_xcd": topo.cuset_counts(die_mask),
+                                           **{f"{m}_us": round(1e3 * t, 2) for m, t in ms.items()},
+                                           "speedup_vs_oblivious": round(ms["oblivious_rowmajor"] / ms["aware"], 4)}
+            del q, kv, o
+        p = workloads.mla_problem(16, 128, 8192)
+        q, kv = workloads.make_mla_inputs_on(p, dev)
+        q2, kv2 = workloads.make_mla_inputs_on(p, dev)
+        o, o2 = torch.empty((16, 128, 512), dtype=torch.bfloat16, device=dev), \
+            torch.empty((16, 128, 512), dtype=torch.bfloat16, device=dev)
+        mask = workloads.random_mask_bits(workloads.COLOC.seed, 1, 128)[0]
+        comp = [b for b in range(256) if b not in set(mask)]
+        sa, sb = asym.stream_create(topo, mask), asym.stream_create(topo, comp)
+        res = {}
+        try:
+            for m in ("aware", "oblivious_rowmajor"):
+                f = lambda: asym.mla_decode(q, kv, o, mapping=m, topo=topo, stream=sa)
+                gg = lambda: asym.mla_decode(q2, kv2, o2, mapping="aware", topo=topo, stream=sb)
+                for _ in range(3):
+                    f(), gg()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(sa)
+                for _ in range(10):
+                    f()
+                    gg()
+                e1.record(sa)
+                torch.cuda.synchronize()
+                t = e0.elapsed_time(e1) / 10
+                res[m] = {"us": round(1e3 * t, 2), "TBps_W": round(p.kv_bytes / (t * 1e-3) / 1e12, 3)}
+            res["cus_per_xcd"] = topo.cuset_counts(mask)
+            res["workload"] = p.name
+        finally:
+            asym.stream_destroy(sa)
+            asym.stream_destroy(sb)
+        uneven["random_128_cu_set_with_tenant"] = res
+        del q, kv, q2, kv2, o, o2
+        torch.cuda.empty_cache()
+    return {"configs": out, "uneven_cu_sets": uneven}
+
+
+FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "chunk_read", "mla")
 
 
 def focus_run(name: str, dev, stream, launches: int) -> dict:
@@ -741,6 +837,7 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
       grouped_small_m  grouped GEMM (32 groups of ~20 rows) x (6144, 7168), seed 5
       attention_gqa    decode attention, grouped-query, B = 64, S_k = 32768
       chunk_read       strided read of a 16 GiB region in 8 KiB chunks, address order
+      mla              latent-attention decode, B = 64, H_q = 128, S_k = 8192 (aware)
     Reports the mean per launch (HIP events on the launch stream) and the
     algorithmic bytes each launch must read or write."""
     import torch
@@ -768,6 +865,13 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
         fn = lambda: asym.attn_decode(q, k, v, o, stream=stream)
         nbytes = p.kv_bytes + 2 * 2 * q.numel()
         kernel = "attn_decode_split<4> + attn_decode_merge"
+    elif name == "mla":
+        p = workloads.mla_problem(64, 128, 8192)
+        q, kv = workloads.make_mla_inputs_on(p, dev)
+        o = torch.empty((64, 128, 512), dtype=torch.bfloat16, device=dev)
+        fn = lambda: asym.mla_decode(q, kv, o, stream=stream)
+        nbytes = p.kv_bytes + 2 * q.numel() + 2 * o.numel()
+        kernel = "mla_decode_split + mla_decode_merge"
     elif name == "chunk_read":
         nb = 16 << 30
         raw = torch.empty(nb + (2 << 20), dtype=torch.uint8, device=dev)
@@ -808,11 +912,12 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa,attention,parity",
+    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa,attention,mla,parity",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
-                         "remote read bandwidth), attention (decode attention), parity (every "
+                         "remote read bandwidth), attention (decode attention), mla (latent-"
+                         "attention decode), parity (every "
                          "configuration's product against the oracle, all outputs); 'none' for "
                          "the headline only")
     ap.add_argument("--spread-masks", type=int, default=32)
@@ -941,6 +1046,8 @@ def main() -> int:
         line["grouped_gemm"] = grouped_study(dev, stream, range(1, 6), 8, 5)
     if "attention" in studies:
         line["decode_attention"] = attention_study(topo, dev, stream, args.probe != "identity")
+    if "mla" in studies:
+        line["mla_decode"] = mla_study(topo, dev, stream, args.probe != "identity")
     if "numa" in studies:
         summ, hres = interleave_summary(dev)
         line["partition_hash"] = summ

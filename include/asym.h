@@ -712,6 +712,57 @@ int asym_attn_decode_plan(const asym_topology* topo, int B, int H_q, int H_kv, i
                           int split_tokens, int mapping, uint32_t xcd_mask, void* stream,
                           asym_attn_plan_info* out);
 
+/* ---- multi-head latent attention, decode (Section 7.1; Appendix F) ---- */
+/* One query token per request against a compressed latent cache shared by
+ * all query heads (the decode form of multi-head latent attention, with the
+ * projections absorbed into the query; Appendix F counts one row of 512 + 64
+ * values per token).  For request b and query head h:
+ *   s_t = scale * <q[b][h], kv[b][t]>                  (576 values)
+ *   O[b][h] = sum_t softmax_t(s)_t * kv[b][t][0 .. 511]
+ *   lse[b][h] = log sum_t exp(s_t)                     (nullable output)
+ * Layout (contiguous, caller-owned device memory): q [B][H_q][576],
+ * kv [B][S_k][576] (per token: 512 latent values, which are also the value,
+ * then 64 rotary key values), O [B][H_q][512], all bf16; lse fp32 [B][H_q].
+ * H_q a multiple of 16 (at most 1024); q, kv and O 16-byte aligned; a
+ * request's cache below 2 GiB.
+ * The sequence is cut into splits of split_tokens tokens (0 = automatic: the
+ * longest of 1024, 512, ... 32 giving at least 2048 tasks; else a multiple
+ * of 32); a task is one (request, split, block of 16 query heads) on one wave
+ * of the matrix cores.  A second launch merges the splits of each (request,
+ * head) in split order.  Mapping: AWARE numbers the tasks request-split
+ * major, so the head blocks that read the same cache rows are consecutive,
+ * gives each XCD a share of that list in proportion to its CUs in the
+ * stream's CU set (honouring a whole-XCD restriction), and lets workgroups
+ * claim groups of 4 tasks from their XCD's share, then from the others: the
+ * rows cross into one XCD's L2 once.  The oblivious mappings (both) number
+ * them head-block major and hand out 4 per workgroup in order, so the head
+ * blocks of one split land on different XCDs and every XCD gets an equal
+ * share.  Every mapping gives the same bits.  fp32 partials live in a
+ * per-stream library workspace, grown (after a stream synchronisation) when a
+ * call needs more.  Asynchronous.
+ * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
+int asym_mla_decode_bf16(const asym_topology* topo, int B, int H_q, int S_k,
+                         const void* q, const void* kv, void* o, float* lse,
+                         float scale, int split_tokens, int mapping, uint32_t xcd_mask,
+                         void* stream);
+
+typedef struct asym_mla_plan_info {
+  int split_tokens;
+  int n_splits;
+  int head_blocks;         /* H_q / 16 */
+  int tasks;               /* B * n_splits * head_blocks */
+  int grid;                /* workgroups of the split launch */
+  int tasks_per_workgroup; /* one per wave */
+  int n_xcds;
+  int tasks_per_xcd[ASYM_MAX_XCDS];
+  size_t workspace_bytes;  /* fp32 partials: B * H_q * n_splits * 514 * 4 */
+} asym_mla_plan_info;
+
+/* What asym_mla_decode_bf16 would launch (no pointers needed; launches
+ * nothing).  Errors as asym_mla_decode_bf16. */
+int asym_mla_decode_plan(const asym_topology* topo, int B, int H_q, int S_k, int split_tokens,
+                         int mapping, uint32_t xcd_mask, void* stream, asym_mla_plan_info* out);
+
 /* ---- streaming copy and co-run (Sections 7.2, 7.3) ---------------------- */
 /* The bandwidth-bound tenant of the co-location study (Section 7.3 runs a
  * second tenant on the complementary units): dst[i] = src[i] for n_bytes

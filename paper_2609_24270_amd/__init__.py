@@ -44,7 +44,8 @@ EXPORTS = (
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
     "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_bf16_noalloc", "asym_gemm_noalloc_limits",
     "asym_gemm_plan", "asym_gemm_set_small_m",
-    "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
+    "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_mla_decode_bf16", "asym_mla_decode_plan",
+    "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
 
@@ -154,6 +155,18 @@ class Task(ctypes.Structure):
                 ("n_bytes", ctypes.c_size_t), ("grid", ctypes.c_int)]
 
 
+class MlaPlanInfo(ctypes.Structure):
+    _fields_ = [("split_tokens", ctypes.c_int), ("n_splits", ctypes.c_int), ("head_blocks", ctypes.c_int),
+                ("tasks", ctypes.c_int), ("grid", ctypes.c_int), ("tasks_per_workgroup", ctypes.c_int),
+                ("n_xcds", ctypes.c_int), ("tasks_per_xcd", ctypes.c_int * MAX_XCDS),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+    def to_dict(self) -> dict:
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "tasks_per_xcd"}
+        d["tasks_per_xcd"] = list(self.tasks_per_xcd)[:self.n_xcds]
+        return d
+
+
 class GemmPlanInfo(ctypes.Structure):
     _fields_ = [("tile_m", ctypes.c_int), ("tile_n", ctypes.c_int),
                 ("tiles_m", ctypes.c_int), ("tiles_n", ctypes.c_int),
@@ -251,6 +264,8 @@ def load_library(path: str = LIB_PATH):
         "asym_gemm_noalloc_limits": (i, [ctypes.POINTER(ctypes.c_size_t), ip, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_attn_decode_bf16": (i, [topo_p, i, i, i, i, i, vp, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
         "asym_attn_decode_plan": (i, [topo_p, i, i, i, i, i, i, i, u32, vp, ctypes.POINTER(AttnPlanInfo)]),
+        "asym_mla_decode_bf16": (i, [topo_p, i, i, i, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
+        "asym_mla_decode_plan": (i, [topo_p, i, i, i, i, i, u32, vp, ctypes.POINTER(MlaPlanInfo)]),
         "asym_copy_bf16": (i, [topo_p, vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
         "asym_corun": (i, [topo_p, ctypes.POINTER(Task), i, ctypes.POINTER(TaskResult)]),
         "asym_last_error": (cp, []),
@@ -830,6 +845,45 @@ def gemm_plan(A=None, B=None, C=None, mapping="aware", topo: Optional[Topology] 
         topo.handle if topo else None, M, N, K, ctypes.c_void_p(pa), lda, ctypes.c_void_p(pb),
         ldb, B_KN if kn else B_NK, ctypes.c_void_p(pc), ldc, mp, xcd_mask, _stream_ptr(stream),
         ctypes.byref(out)))
+    return out.to_dict()
+
+
+def mla_decode(q, kv, o=None, lse=None, scale: Optional[float] = None, split_tokens: int = 0,
+               mapping="aware", topo: Optional[Topology] = None, xcd_mask: int = 0, stream=None):
+    """Latent-attention decode: q [B, H_q, 576] and the cache kv [B, S_k, 576]
+    bf16 CUDA tensors (contiguous); returns O [B, H_q, 512] bf16 (and fills
+    lse [B, H_q] fp32 when given).  scale defaults to 1 / sqrt(192)."""
+    import math
+    import torch
+    if q.dtype != torch.bfloat16 or kv.dtype != torch.bfloat16:
+        raise TypeError("q and kv must be bfloat16")
+    if q.dim() != 3 or kv.dim() != 3 or q.shape[2] != 576 or kv.shape[2] != 576 or q.shape[0] != kv.shape[0]:
+        raise ValueError("q must be [B, H_q, 576] and kv [B, S_k, 576]")
+    if not (q.is_contiguous() and kv.is_contiguous()):
+        raise ValueError("q and kv must be contiguous")
+    B, Hq, _ = q.shape
+    S = kv.shape[1]
+    if o is None:
+        o = torch.empty((B, Hq, 512), dtype=torch.bfloat16, device=q.device)
+    if o.dtype != torch.bfloat16 or tuple(o.shape) != (B, Hq, 512) or not o.is_contiguous():
+        raise ValueError("o must be a contiguous bf16 [B, H_q, 512] tensor")
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hq) or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous fp32 [B, H_q] tensor")
+    sc = 1.0 / math.sqrt(192.0) if scale is None else float(scale)
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    _check(load_library().asym_mla_decode_bf16(
+        topo.handle if topo else None, B, Hq, S, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(kv.data_ptr()),
+        ctypes.c_void_p(o.data_ptr()), ctypes.c_void_p(lse.data_ptr()) if lse is not None else None, sc,
+        split_tokens, mp, xcd_mask, _stream_ptr(stream)))
+    return o
+
+
+def mla_decode_plan(B: int, Hq: int, S: int, split_tokens: int = 0, mapping="aware",
+                    topo: Optional[Topology] = None, xcd_mask: int = 0, stream=None) -> dict:
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    out = MlaPlanInfo()
+    _check(load_library().asym_mla_decode_plan(topo.handle if topo else None, B, Hq, S, split_tokens, mp,
+                                               xcd_mask, _stream_ptr(stream), ctypes.byref(out)))
     return out.to_dict()
 
 

@@ -22,7 +22,7 @@ ARCH = "gfx950"
 SOURCES = ["capi.cpp", "topology.cpp", "topology_cache.cpp", "schedule.cpp", "corun.cpp", "affinity.cpp",
            "interleave.cpp",
            "gemm.hip", "gemm_skinny.hip", "attn_decode.hip", "probe.hip", "latency.hip", "copy.hip", "numa.hip",
-           "transpose.hip", "noalloc.hip"]
+           "transpose.hip", "noalloc.hip", "mla_decode.hip"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-I", os.path.join(ROOT, "include"), "-Wall", "-Wno-unused-function"]

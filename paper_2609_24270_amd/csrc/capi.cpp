@@ -847,6 +847,70 @@ static int attn_plan(const asym_topology* topo_in, int B, int Hq, int Hkv, int S
   return ASYM_OK;
 }
 
+// The aware attention forms' per-XCD task offsets on the device (cached per
+// stream by CU counts, task count and kernel) and the claim counters, zeroed
+// at creation (every aware launch's merge leaves them zero again).
+static int aware_share_offsets(Workspace* ws, const CuSet& cs, const std::vector<int>& quota, int tasks, int kind,
+                               hipStream_t stream, int** d_off_out) {
+  const int n_x = cs.t->n_xccs;
+  std::vector<int> key(cs.slots);
+  key.push_back(tasks);
+  key.push_back(kind);
+  auto hit = std::find_if(ws->attn_off.begin(), ws->attn_off.end(),
+                          [&](const std::pair<std::vector<int>, int*>& e) { return e.first == key; });
+  if (hit != ws->attn_off.end()) {
+    std::rotate(ws->attn_off.begin(), hit, hit + 1);
+  } else {
+    if (ws->attn_off.size() >= 8) {
+      ASYM_HIP(hipStreamSynchronize(stream));
+      ASYM_HIP(hipFree(ws->attn_off.back().second));
+      ws->attn_off.pop_back();
+    }
+    int* dev_off = nullptr;
+    ASYM_HIP(hipMalloc(&dev_off, (ASYM_MAX_XCDS + 1) * sizeof(int)));
+    if (ws->g_pending) {
+      ASYM_HIP(hipEventSynchronize(ws->g_copied));
+      ws->g_pending = false;
+    }
+    if (ws->g_host_bytes < (ASYM_MAX_XCDS + 1) * sizeof(int)) {
+      if (ws->g_host) ASYM_HIP(hipHostFree(ws->g_host));
+      ws->g_host = nullptr;
+      ws->g_host_bytes = 0;
+      ASYM_HIP(hipHostMalloc(&ws->g_host, 64 << 10));
+      ws->g_host_bytes = 64 << 10;
+    }
+    if (!ws->g_copied) ASYM_HIP(hipEventCreateWithFlags(&ws->g_copied, hipEventDisableTiming));
+    int* h = static_cast<int*>(ws->g_host);
+    h[0] = 0;
+    for (int x = 0; x < n_x; ++x) h[x + 1] = h[x] + quota[x];
+    ASYM_HIP(hipMemcpyAsync(dev_off, h, (n_x + 1) * sizeof(int), hipMemcpyHostToDevice, stream));
+    ASYM_HIP(hipEventRecord(ws->g_copied, stream));
+    ws->g_pending = true;
+    ws->attn_off.insert(ws->attn_off.begin(), std::make_pair(std::move(key), dev_off));
+  }
+  *d_off_out = ws->attn_off.front().second;
+  if (!ws->attn_claim) {
+    ASYM_HIP(hipMalloc(&ws->attn_claim, attn_claim_ints() * sizeof(int)));
+    int rc = launch_zero_words(ws->attn_claim, attn_claim_ints(), stream);
+    if (rc != ASYM_OK) return rc;
+  }
+  return ASYM_OK;
+}
+
+// fp32 partials of the attention forms in the stream's buffer (grown after a
+// stream synchronisation: the old buffer may still be read by launches on it)
+static int attn_partials(Workspace* ws, size_t bytes_needed, hipStream_t stream) {
+  if (ws->attn_bytes >= bytes_needed) return ASYM_OK;
+  ASYM_HIP(hipStreamSynchronize(stream));
+  if (ws->attn_buf) ASYM_HIP(hipFree(ws->attn_buf));
+  ws->attn_buf = nullptr;
+  ws->attn_bytes = 0;
+  const size_t bytes = std::max<size_t>(bytes_needed, 1 << 20);
+  ASYM_HIP(hipMalloc(&ws->attn_buf, bytes));
+  ws->attn_bytes = bytes;
+  return ASYM_OK;
+}
+
 int attn_decode(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int D, const void* q, const void* k,
                 const void* v, void* o, float* lse, float scale, int split_in, int mapping, uint32_t xcd_mask,
                 hipStream_t stream) {
@@ -861,60 +925,13 @@ int attn_decode(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int
   Workspace* ws = nullptr;
   rc = get_workspace(P.cs.device, stream, &ws);
   if (rc != ASYM_OK) return rc;
-  if (ws->attn_bytes < P.ws_bytes) {
-    // the old buffer may still be read by launches on this stream
-    ASYM_HIP(hipStreamSynchronize(stream));
-    if (ws->attn_buf) ASYM_HIP(hipFree(ws->attn_buf));
-    ws->attn_buf = nullptr;
-    ws->attn_bytes = 0;
-    const size_t bytes = std::max<size_t>(P.ws_bytes, 1 << 20);
-    ASYM_HIP(hipMalloc(&ws->attn_buf, bytes));
-    ws->attn_bytes = bytes;
-  }
+  rc = attn_partials(ws, P.ws_bytes, stream);
+  if (rc != ASYM_OK) return rc;
   const int n_x = P.cs.t->n_xccs;
   int* d_off = nullptr;
   if (mapping == ASYM_MAP_AWARE) {
-    std::vector<int> key(P.cs.slots);
-    key.push_back(P.tasks);
-    auto hit = std::find_if(ws->attn_off.begin(), ws->attn_off.end(),
-                            [&](const std::pair<std::vector<int>, int*>& e) { return e.first == key; });
-    if (hit != ws->attn_off.end()) {
-      std::rotate(ws->attn_off.begin(), hit, hit + 1);
-    } else {
-      if (ws->attn_off.size() >= 8) {
-        ASYM_HIP(hipStreamSynchronize(stream));
-        ASYM_HIP(hipFree(ws->attn_off.back().second));
-        ws->attn_off.pop_back();
-      }
-      int* dev_off = nullptr;
-      ASYM_HIP(hipMalloc(&dev_off, (ASYM_MAX_XCDS + 1) * sizeof(int)));
-      if (ws->g_pending) {
-        ASYM_HIP(hipEventSynchronize(ws->g_copied));
-        ws->g_pending = false;
-      }
-      if (ws->g_host_bytes < (ASYM_MAX_XCDS + 1) * sizeof(int)) {
-        if (ws->g_host) ASYM_HIP(hipHostFree(ws->g_host));
-        ws->g_host = nullptr;
-        ws->g_host_bytes = 0;
-        ASYM_HIP(hipHostMalloc(&ws->g_host, 64 << 10));
-        ws->g_host_bytes = 64 << 10;
-      }
-      if (!ws->g_copied) ASYM_HIP(hipEventCreateWithFlags(&ws->g_copied, hipEventDisableTiming));
-      int* h = static_cast<int*>(ws->g_host);
-      h[0] = 0;
-      for (int x = 0; x < n_x; ++x) h[x + 1] = h[x] + P.quota[x];
-      ASYM_HIP(hipMemcpyAsync(dev_off, h, (n_x + 1) * sizeof(int), hipMemcpyHostToDevice, stream));
-      ASYM_HIP(hipEventRecord(ws->g_copied, stream));
-      ws->g_pending = true;
-      ws->attn_off.insert(ws->attn_off.begin(), std::make_pair(std::move(key), dev_off));
-    }
-    d_off = ws->attn_off.front().second;
-    if (!ws->attn_claim) {
-      // zero once here; every aware launch's merge leaves them zero again
-      ASYM_HIP(hipMalloc(&ws->attn_claim, attn_claim_ints() * sizeof(int)));
-      rc = launch_zero_words(ws->attn_claim, attn_claim_ints(), stream);
-      if (rc != ASYM_OK) return rc;
-    }
+    rc = aware_share_offsets(ws, P.cs, P.quota, P.tasks, 0, stream, &d_off);
+    if (rc != ASYM_OK) return rc;
   }
   AttnLaunch a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse;
@@ -953,6 +970,118 @@ int attn_decode_plan(const asym_topology* topo_in, int B, int Hq, int Hkv, int S
       out->tasks_per_xcd[x] = P.quota[x];
     } else {
       // workgroup i lands on XCD i mod n and holds tasks per_wg i .. per_wg i + per_wg - 1
+      long long c = 0;
+      for (int i = x; i < P.grid; i += out->n_xcds) c += std::min(per_wg, P.tasks - i * per_wg);
+      out->tasks_per_xcd[x] = (int)c;
+    }
+  }
+  return ASYM_OK;
+}
+
+// ---- multi-head latent attention, decode ------------------------------------
+static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int split_in, int mapping, uint32_t xcd_mask,
+                    hipStream_t stream, AttnPlan* P, int* hblocks) {
+  if (B < 1 || Hq < 1 || S < 1) return fail(ASYM_EINVAL, "mla: B, H_q, S_k must be >= 1");
+  if (Hq % 16) return fail(ASYM_EUNSUPPORTED, "mla: H_q must be a multiple of 16 (blocks of 16 query heads)");
+  if (Hq > 1024) return fail(ASYM_EUNSUPPORTED, "mla: at most 1024 query heads");
+  if ((int64_t)S * 576 * 2 >= (1ll << 31)) return fail(ASYM_EUNSUPPORTED, "mla: a request's cache must be below 2 GiB");
+  if (split_in < 0 || split_in % 32 || split_in > (1 << 20))
+    return fail(ASYM_EINVAL, "mla: split_tokens must be 0 (automatic) or a positive multiple of 32");
+  if (mapping != ASYM_MAP_AWARE && mapping != ASYM_MAP_OBLIVIOUS_GROUPED && mapping != ASYM_MAP_OBLIVIOUS_ROWMAJOR)
+    return fail(ASYM_EINVAL, "mla: unknown mapping");
+  int rc = cu_set_for(topo_in, mapping, xcd_mask, stream, "mla", &P->cs);
+  if (rc != ASYM_OK) return rc;
+  const int hb = Hq / 16;
+  int L = split_in;
+  if (!L) {
+    // the longest split (up to 1024 tokens) that still gives 2048 tasks
+    L = 1024;
+    while (L > 32 && (int64_t)B * hb * ((S + L - 1) / L) < 2048) L /= 2;
+  }
+  const int64_t n_splits = (S + L - 1) / L;
+  const int64_t tasks = (int64_t)B * hb * n_splits;
+  if (tasks > (1ll << 30)) return fail(ASYM_EINVAL, "mla: too many tasks");
+  P->split = L;
+  P->n_splits = (int)n_splits;
+  P->tasks = (int)tasks;
+  *hblocks = hb;
+  const int per_wg = mla_tasks_per_workgroup();
+  const int n_x = P->cs.t->n_xccs;
+  if (mapping == ASYM_MAP_AWARE) {
+    P->quota = largest_remainder_quotas(P->tasks, P->cs.slots);
+    // one 128 KiB workgroup fits per CU: one per CU of the largest XCD on
+    // every XCD (the dealing is equal per XCD), no more than the groups of
+    // the largest share
+    int most = 0;
+    for (int x = 0; x < n_x; ++x) most = std::max(most, (P->quota[x] + per_wg - 1) / per_wg);
+    P->grid = std::max(1, std::min(most, P->cs.smax) * n_x);
+  } else {
+    P->grid = (P->tasks + per_wg - 1) / per_wg;
+  }
+  P->ws_bytes = (size_t)B * Hq * n_splits * (512 + 2) * sizeof(float);
+  return ASYM_OK;
+}
+
+int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q, const void* kv, void* o, float* lse,
+               float scale, int split_in, int mapping, uint32_t xcd_mask, hipStream_t stream) {
+  if (!q || !kv || !o) return fail(ASYM_EINVAL, "mla: null pointer");
+  if (!aligned16(q) || !aligned16(kv) || !aligned16(o) || ((uintptr_t)lse & 3u))
+    return fail(ASYM_EINVAL, "mla: q, the cache and O must be 16-byte aligned, lse 4-byte aligned");
+  if (!std::isfinite(scale)) return fail(ASYM_EINVAL, "mla: scale must be finite");
+  std::lock_guard<std::mutex> lock(g_mu);
+  AttnPlan P;
+  int hblocks = 0;
+  int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks);
+  if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(P.cs.device, stream, &ws);
+  if (rc != ASYM_OK) return rc;
+  rc = attn_partials(ws, P.ws_bytes, stream);
+  if (rc != ASYM_OK) return rc;
+  const int n_x = P.cs.t->n_xccs;
+  int* d_off = nullptr;
+  if (mapping == ASYM_MAP_AWARE) {
+    rc = aware_share_offsets(ws, P.cs, P.quota, P.tasks, 1, stream, &d_off);
+    if (rc != ASYM_OK) return rc;
+  }
+  MlaLaunch a;
+  a.q = q; a.kv = kv; a.o = o; a.lse = lse;
+  a.part_o = ws->attn_buf;
+  a.part_ml = ws->attn_buf + (size_t)B * Hq * P.n_splits * 512;
+  a.d_quota_off = d_off;
+  a.d_claim = ws->attn_claim;
+  a.allow = 0;
+  for (int x = 0; x < n_x; ++x)
+    if (P.cs.slots[x] > 0) a.allow |= 1u << x;
+  a.B = B; a.Hq = Hq; a.S = S;
+  a.split = P.split; a.n_splits = P.n_splits;
+  a.n_x = n_x; a.grid = P.grid;
+  a.scale = scale;
+  return launch_mla_decode(a, stream);
+}
+
+int mla_decode_plan(const asym_topology* topo_in, int B, int Hq, int S, int split_in, int mapping, uint32_t xcd_mask,
+                    hipStream_t stream, asym_mla_plan_info* out) {
+  if (!out) return fail(ASYM_EINVAL, "mla plan: null output");
+  std::lock_guard<std::mutex> lock(g_mu);
+  AttnPlan P;
+  int hblocks = 0;
+  const int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks);
+  if (rc != ASYM_OK) return rc;
+  *out = asym_mla_plan_info{};
+  out->split_tokens = P.split;
+  out->n_splits = P.n_splits;
+  out->head_blocks = hblocks;
+  out->tasks = P.tasks;
+  out->grid = P.grid;
+  out->tasks_per_workgroup = mla_tasks_per_workgroup();
+  out->n_xcds = P.cs.t->n_xccs;
+  out->workspace_bytes = P.ws_bytes;
+  const int per_wg = mla_tasks_per_workgroup();
+  for (int x = 0; x < out->n_xcds && x < ASYM_MAX_XCDS; ++x) {
+    if (mapping == ASYM_MAP_AWARE) {
+      out->tasks_per_xcd[x] = P.quota[x];
+    } else {
       long long c = 0;
       for (int i = x; i < P.grid; i += out->n_xcds) c += std::min(per_wg, P.tasks - i * per_wg);
       out->tasks_per_xcd[x] = (int)c;
@@ -1143,6 +1272,19 @@ extern "C" int asym_version(void) { return 1; }
 
 extern "C" int asym_gemm_set_small_m(int enable) {
   return asym::g_small_m.exchange(enable != 0) ? 1 : 0;
+}
+
+extern "C" int asym_mla_decode_bf16(const asym_topology* topo, int B, int H_q, int S_k, const void* q,
+                                    const void* kv, void* o, float* lse, float scale, int split_tokens, int mapping,
+                                    uint32_t xcd_mask, void* stream) {
+  return asym::mla_decode(topo, B, H_q, S_k, q, kv, o, lse, scale, split_tokens, mapping, xcd_mask,
+                          static_cast<hipStream_t>(stream));
+}
+
+extern "C" int asym_mla_decode_plan(const asym_topology* topo, int B, int H_q, int S_k, int split_tokens,
+                                    int mapping, uint32_t xcd_mask, void* stream, asym_mla_plan_info* out) {
+  return asym::mla_decode_plan(topo, B, H_q, S_k, split_tokens, mapping, xcd_mask, static_cast<hipStream_t>(stream),
+                               out);
 }
 
 extern "C" int asym_attn_decode_bf16(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,

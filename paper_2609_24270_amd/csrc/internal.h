@@ -138,6 +138,22 @@ struct AttnLaunch {
 };
 int launch_attn_decode(const AttnLaunch& a, hipStream_t s);
 int attn_tasks_per_workgroup();
+
+// Multi-head latent attention, decode (576-wide cache rows, 512-wide values).
+struct MlaLaunch {
+  const void *q, *kv;
+  void* o;
+  float* lse;                 // nullable
+  float* part_o;              // [B][Hq][n_splits][512]
+  float* part_ml;             // [B][Hq][n_splits][2]
+  const int* d_quota_off;     // aware: device [n_x + 1]; null = oblivious
+  int* d_claim = nullptr;     // aware: claim counters, zero at launch (the merge clears them)
+  uint32_t allow = 0xFFFFFFFFu;
+  int B, Hq, S, split, n_splits, n_x, grid;
+  float scale;
+};
+int launch_mla_decode(const MlaLaunch& a, hipStream_t s);
+int mla_tasks_per_workgroup();
 int attn_claim_ints();  // ints of the aware form's claim counters
 
 int probe_identity_run(int device, hipStream_t s, int n_blocks,
