@@ -659,12 +659,33 @@ def numa_bw_study(dev, hash_res, rounds: int = 3, gib: int = 16):
         for k, (chunks, off) in cases.items():
             ms, _ = asym.chunk_read_bw(ptr, nbytes, chunk_log2, chunks, off, iters=5)
             acc[k] += len(chunks) * (1 << chunk_log2) / (ms * 1e-3) / 1e9
+    # latency as the bound: few workgroups per XCD, each reading one chunk at a
+    # time, over the first 2 GiB of the region (whole chip; local, remote and
+    # address-order lists of the same chunks)
+    import numpy as np
+    limit = (2 << 30) >> chunk_log2
+    low = {}
+    for name, mode in (("all", asym.CHUNKS_ALL), ("local", asym.CHUNKS_LOCAL), ("remote", asym.CHUNKS_REMOTE)):
+        chunks, off = asym.chunk_lists(homes, len(grp), grp, mode, 0)
+        segs = [np.asarray(chunks[off[x]:off[x + 1]]) for x in range(len(grp))]
+        segs = [g_[g_ < limit] for g_ in segs]
+        low[name] = (np.concatenate(segs).astype(np.uint32), np.cumsum([0] + [len(g_) for g_ in segs]))
+    lat = {}
+    for w in (1, 4, 16, 64, 256):
+        r = {}
+        for name, (chunks, off) in low.items():
+            ms, _ = asym.chunk_read_bw(ptr, nbytes, chunk_log2, chunks, off, iters=3, workers_per_xcd=w)
+            r[name] = round(len(chunks) * (1 << chunk_log2) / (ms * 1e-3) / 1e9, 1)
+        r["local_over_remote"] = round(r["local"] / r["remote"], 3)
+        r["local_over_all"] = round(r["local"] / r["all"], 3)
+        lat[f"workers_per_xcd_{w}"] = r
     del raw
     torch.cuda.empty_cache()
     return {"region_gib": gib, "chunk_bytes": 1 << chunk_log2, "rounds": rounds,
             "map": {k: info[k] for k in ("n_pages", "unclassified_pages", "chunk_share", "verify_classified",
                                          "verify_agree", "local_cycles", "remote_cycles")},
-            "GBps": {k: round(v / rounds, 1) for k, v in acc.items()}}
+            "GBps": {k: round(v / rounds, 1) for k, v in acc.items()},
+            "low_parallelism_GBps_first_2GiB": lat}
 
 
 def attention_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 3):
@@ -828,7 +849,7 @@ def mla_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 
     return {"configs": out, "uneven_cu_sets": uneven}
 
 
-FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "chunk_read", "mla")
+FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "chunk_read", "mla", "mla16", "copy")
 
 
 def focus_run(name: str, dev, stream, launches: int) -> dict:
@@ -838,6 +859,8 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
       attention_gqa    decode attention, grouped-query, B = 64, S_k = 32768
       chunk_read       strided read of a 16 GiB region in 8 KiB chunks, address order
       mla              latent-attention decode, B = 64, H_q = 128, S_k = 8192 (aware)
+      mla16            latent-attention decode, B = 64, H_q = 16, S_k = 32768 (aware)
+      copy             the streaming copy, 64 MiB, one pass, whole chip
     Reports the mean per launch (HIP events on the launch stream) and the
     algorithmic bytes each launch must read or write."""
     import torch
@@ -872,6 +895,19 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
         fn = lambda: asym.mla_decode(q, kv, o, stream=stream)
         nbytes = p.kv_bytes + 2 * q.numel() + 2 * o.numel()
         kernel = "mla_decode_split + mla_decode_merge"
+    elif name == "mla16":
+        p = workloads.mla_problem(64, 16, 32768)
+        q, kv = workloads.make_mla_inputs_on(p, dev)
+        o = torch.empty((64, 16, 512), dtype=torch.bfloat16, device=dev)
+        fn = lambda: asym.mla_decode(q, kv, o, stream=stream)
+        nbytes = p.kv_bytes + 2 * q.numel() + 2 * o.numel()
+        kernel = "mla_decode_split + mla_decode_merge"
+    elif name == "copy":
+        src = workloads.copy_source(workloads.COPY_BYTES // 2).to(dev)
+        dst = torch.empty_like(src)
+        fn = lambda: asym.copy(dst, src, passes=1, stream=stream)
+        nbytes = 2 * workloads.COPY_BYTES
+        kernel = "copy_kernel"
     elif name == "chunk_read":
         nb = 16 << 30
         raw = torch.empty(nb + (2 << 20), dtype=torch.uint8, device=dev)

@@ -467,8 +467,9 @@ int asym_chunk_lists(const int8_t* chunk_home, int n_chunks, int n_xcds, const i
  * chunks[off[x] .. off[x+1]) of the device range [base, base + bytes) (chunk
  * c at base + c << chunk_log2; every index must lie below bytes >> chunk_log2,
  * checked on the host), 16 bytes per lane, with 256 workgroups of 256 threads per
- * XCD (workgroup b runs on XCD b mod n_xcds: the dispatch rule the identity
- * probe checks).  Runs `iters` times on `stream` (NULL = null stream) between
+ * XCD (a workgroup reads the list of the XCD it runs on, XCC_ID, as one of the
+ * workers of its residue class of block indices mod n_xcds, which the hardware
+ * deals to one XCD).  Runs `iters` times on `stream` (NULL = null stream) between
  * two events and reports ms per iteration; checksum_out (nullable, 4 words)
  * receives the XOR of every 16-byte word read by one iteration.  chunks and
  * off are host arrays, copied to the device for the call; n_xcds must be the
@@ -478,6 +479,15 @@ int asym_chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uin
                        const int* off,
                        int n_xcds, int iters, void* stream, uint32_t* checksum_out,
                        double* ms_per_iter);
+
+/* The same reader with workers_per_xcd workgroups per XCD (1 .. 4096): few
+ * workers keep few loads in flight, so the time per chunk follows the
+ * latency of the memory the chunks live in (local or remote to the reading
+ * XCD's I/O die) rather than the bandwidth (Section 6.1 measures both).
+ * Errors: as asym_chunk_read_bw. */
+int asym_chunk_read(const void* base, size_t bytes, int chunk_log2, const uint32_t* chunks,
+                    const int* off, int n_xcds, int workers_per_xcd, int iters, void* stream,
+                    uint32_t* checksum_out, double* ms_per_iter);
 
 /* ---- CU sets and masked streams ----------------------------------------- */
 /* Choose n_cus compute units by `policy` among the CUs not in `exclude`

@@ -38,7 +38,7 @@ EXPORTS = (
     "asym_topology_dispatch", "asym_topology_latency", "asym_topology_json",
     "asym_latency_params_default", "asym_latency_probe", "asym_latency_analyze",
     "asym_interleave_params_default", "asym_interleave_probe", "asym_interleave_analyze",
-    "asym_home_map", "asym_home_map_analyze", "asym_chunk_lists", "asym_chunk_read_bw",
+    "asym_home_map", "asym_home_map_analyze", "asym_chunk_lists", "asym_chunk_read_bw", "asym_chunk_read",
     "asym_dispatch_check", "asym_dispatch_probe", "asym_cuset_split_xcds",
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
@@ -248,6 +248,8 @@ def load_library(path: str = LIB_PATH):
         "asym_chunk_lists": (i, [ctypes.POINTER(ctypes.c_int8), i, i, ip, u32, i, u32p, ip, ip]),
         "asym_chunk_read_bw": (i, [vp, ctypes.c_size_t, i, u32p, ip, i, i, vp, u32p,
                                    ctypes.POINTER(ctypes.c_double)]),
+        "asym_chunk_read": (i, [vp, ctypes.c_size_t, i, u32p, ip, i, i, i, vp, u32p,
+                                ctypes.POINTER(ctypes.c_double)]),
         "asym_topology_json": (i, [topo_p, cp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_cuset_make": (i, [topo_p, i, i, ctypes.c_uint64, u32p, u32p]),
         "asym_cuset_counts": (i, [topo_p, u32p, ip]),
@@ -579,18 +581,25 @@ def chunk_lists(homes, n_xcds: int, group_of_xcd, mode: int, xcd_mask: int = 0):
     return out[:n.value], off
 
 
-def chunk_read_bw(ptr: int, nbytes: int, chunk_log2: int, chunks, off, iters: int = 5, stream=None):
-    """Read the listed chunks of [ptr, ptr + nbytes) `iters` times; returns
-    (ms per iteration, XOR of every 16-byte word read as 4 uint32)."""
+def chunk_read_bw(ptr: int, nbytes: int, chunk_log2: int, chunks, off, iters: int = 5, stream=None,
+                  workers_per_xcd: Optional[int] = None):
+    """Read the listed chunks of [ptr, ptr + nbytes) `iters` times (256
+    workgroups per XCD, or workers_per_xcd); returns (ms per iteration, XOR of
+    every 16-byte word read as 4 uint32)."""
     import numpy as np
     c = np.ascontiguousarray(chunks, dtype=np.uint32)
     o = np.ascontiguousarray(off, dtype=np.int32)
     ms = ctypes.c_double()
     ck = np.zeros(4, dtype=np.uint32)
-    _check(load_library().asym_chunk_read_bw(
-        ctypes.c_void_p(ptr), nbytes, chunk_log2, c.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
-        o.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), o.shape[0] - 1, iters, _stream_ptr(stream),
-        ck.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), ctypes.byref(ms)))
+    cp_ = c.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+    op_ = o.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
+    ckp = ck.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+    if workers_per_xcd is None:
+        _check(load_library().asym_chunk_read_bw(ctypes.c_void_p(ptr), nbytes, chunk_log2, cp_, op_, o.shape[0] - 1,
+                                                 iters, _stream_ptr(stream), ckp, ctypes.byref(ms)))
+    else:
+        _check(load_library().asym_chunk_read(ctypes.c_void_p(ptr), nbytes, chunk_log2, cp_, op_, o.shape[0] - 1,
+                                              workers_per_xcd, iters, _stream_ptr(stream), ckp, ctypes.byref(ms)))
     return ms.value, ck
 
 

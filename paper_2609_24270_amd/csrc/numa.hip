@@ -29,20 +29,29 @@ typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
 // Each lane reads the 16-byte words at lane * 16 + j * 4096 of every chunk of
 // its workgroup's share; the XOR of what it read goes to sink[b * 256 + lane].
+// A workgroup reads the list of the XCD it runs on (XCC_ID) and strides over
+// it as the (b / n_x)-th of that XCD's workers: the workgroups of one residue
+// class of block indices, which the hardware deals to one XCD (if two classes
+// shared an XCD one list would be read twice and another not at all; every
+// index stays inside the lists either way).
 __global__ void __launch_bounds__(kReadThreads)
 chunk_read_kernel(const char* __restrict__ base, int chunk_log2, const uint32_t* __restrict__ chunks,
                   const int* __restrict__ off, int n_x, v4u* __restrict__ sink) {
   const int b = blockIdx.x;
-  const int x = b % n_x;
+  uint32_t xr;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xr));
+  const int x = (int)(xr & 0xFu);
   const int r = b / n_x;
   const int workers = gridDim.x / n_x;
-  const int i0 = off[x], i1 = off[x + 1];
-  const int words = 1 << (chunk_log2 - 12);  // 16-byte words per lane per chunk
   v4u acc = {0u, 0u, 0u, 0u};
-  for (int i = i0 + r; i < i1; i += workers) {
-    const v4u* p = reinterpret_cast<const v4u*>(base + ((size_t)chunks[i] << chunk_log2)) + threadIdx.x;
+  if (x < n_x) {
+    const int i0 = off[x], i1 = off[x + 1];
+    const int words = 1 << (chunk_log2 - 12);  // 16-byte words per lane per chunk
+    for (int i = i0 + r; i < i1; i += workers) {
+      const v4u* p = reinterpret_cast<const v4u*>(base + ((size_t)chunks[i] << chunk_log2)) + threadIdx.x;
 #pragma unroll 4
-    for (int j = 0; j < words; ++j) acc ^= p[(size_t)j * kReadThreads];
+      for (int j = 0; j < words; ++j) acc ^= p[(size_t)j * kReadThreads];
+    }
   }
   sink[(size_t)b * kReadThreads + threadIdx.x] = acc;
 }
@@ -292,11 +301,13 @@ int chunk_lists(const int8_t* home, int n_chunks, int n_x, const int* grp, uint3
 }
 
 int chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uint32_t* chunks, const int* off,
-                  int n_x, int iters, hipStream_t s, uint32_t* checksum, double* ms) {
+                  int n_x, int iters, hipStream_t s, uint32_t* checksum, double* ms, int workers_per_xcd) {
   if (!base || !chunks || !off || !ms) return fail(ASYM_EINVAL, "chunk read: null pointer");
   if (reinterpret_cast<uintptr_t>(base) % 16) return fail(ASYM_EINVAL, "chunk read: base must be 16-byte aligned");
   if (chunk_log2 < 12 || chunk_log2 > 21) return fail(ASYM_EINVAL, "chunk read: chunk_log2 must be in [12, 21]");
   if (iters < 1 || iters > 10000) return fail(ASYM_EINVAL, "chunk read: iters must be in [1, 10000]");
+  if (workers_per_xcd < 1 || workers_per_xcd > 4096)
+    return fail(ASYM_EINVAL, "chunk read: workers per XCD must be in [1, 4096]");
   int dev = 0, dev_x = 0;
   ASYM_HIP(hipGetDevice(&dev));
   ASYM_HIP(hipDeviceGetAttribute(&dev_x, hipDeviceAttributeNumberOfXccs, dev));
@@ -309,7 +320,7 @@ int chunk_read_bw(const void* base, size_t bytes, int chunk_log2, const uint32_t
   for (int i = 0; i < n; ++i)
     if (chunks[i] >= n_chunks) return fail(ASYM_EINVAL, "chunk read: chunk index beyond the range");
 
-  const int grid = n_x * kReadWorkersPerXcd;
+  const int grid = n_x * workers_per_xcd;
   Bufs b;
   ASYM_HIP(hipMalloc(&b.p[0], sizeof(uint32_t) * std::max(n, 1)));
   ASYM_HIP(hipMalloc(&b.p[1], sizeof(int) * (n_x + 1)));
@@ -406,5 +417,13 @@ extern "C" int asym_chunk_read_bw(const void* base, size_t bytes, int chunk_log2
                                   const int* off, int n_xcds, int iters, void* stream,
                                   uint32_t* checksum_out, double* ms_per_iter) {
   return asym::chunk_read_bw(base, bytes, chunk_log2, chunks, off, n_xcds, iters,
-                             static_cast<hipStream_t>(stream), checksum_out, ms_per_iter);
+                             static_cast<hipStream_t>(stream), checksum_out, ms_per_iter,
+                             asym::kReadWorkersPerXcd);
+}
+
+extern "C" int asym_chunk_read(const void* base, size_t bytes, int chunk_log2, const uint32_t* chunks,
+                               const int* off, int n_xcds, int workers_per_xcd, int iters, void* stream,
+                               uint32_t* checksum_out, double* ms_per_iter) {
+  return asym::chunk_read_bw(base, bytes, chunk_log2, chunks, off, n_xcds, iters,
+                             static_cast<hipStream_t>(stream), checksum_out, ms_per_iter, workers_per_xcd);
 }

@@ -66,6 +66,11 @@ def test_read_kernel_checksum_is_exact(dev, chunk_log2):
             want = _host_xor(words, chunk_log2, chunks)
             assert ck.tolist() == want.tolist(), (mode, xm)
             assert ms > 0
+            # few workers per XCD (each reads the list of the XCD it runs on)
+            for w in (1, 3):
+                _, ck = asym.chunk_read_bw(buf.data_ptr(), nbytes, chunk_log2, chunks, off, iters=1,
+                                           workers_per_xcd=w)
+                assert ck.tolist() == want.tolist(), (mode, xm, w)
 
 
 def test_read_kernel_rejects(dev):
