@@ -28,6 +28,7 @@ import json
 import os
 import sys
 import time
+from typing import Optional
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -377,6 +378,99 @@ def decode_gemm(dev, stream, launches: int = 20, rounds: int = 5):
                 "tflops": round(2 * 32 * 14336 * 4096 / (v * 1e-3) / 1e12, 2)} for k, v in out.items()}
 
 
+def pd_sets(topo, halves):
+    """The prefill / decode CU sets: 192 striped bits and the other 64; the
+    XCD-aligned split with the decode pair taken from one affinity group."""
+    import paper_2609_24270_amd as asym
+    prefill = topo.cuset(192, asym.CUSET_STRIPED)
+    decode = [b for b in range(256) if b not in set(prefill)]
+    grp = [x for x in range(8) if (halves[1] >> x) & 1]
+    dec_x = (1 << grp[-1]) | (1 << grp[-2])
+    pre_x = 0xFF & ~dec_x
+    pre_m, dec_m = topo.cuset_split_xcds(pre_x)
+    return prefill, decode, pre_x, dec_x, pre_m, dec_m
+
+
+def trace_summary(t: dict, khz: int, t0: Optional[int] = None) -> dict:
+    """Per-XCD summary of one traced GEMM launch; times in microseconds from
+    t0 (default: the first workgroup's start).  A CU is told apart by bits
+    8-15 of HW_ID (CU, shader array and engine numbers)."""
+    import numpy as np
+    t0 = int(t["start"].min()) if t0 is None else t0
+    rel = lambda v: (v.astype(np.int64) - t0) * (1e3 / khz)
+    st, ft, en = rel(t["start"]), rel(t["first_tile"]), rel(t["end"])
+    w = t["worked"] == 1
+    cu = (t["hw_id"] >> 8) & 0xFF
+    per = []
+    for x in range(8):
+        s = t["xcc"] == x
+        sw, ex = s & w, s & ~w
+        d = {"workgroups": int(s.sum()), "workers": int(sw.sum()), "tiles": int(t["tiles"][s].sum()),
+             "cus_used": int(len(np.unique(cu[s])))}
+        if sw.any():
+            d.update(last_start_us=round(float(st[sw].max()), 1), first_tile_by_us=round(float(ft[sw].max()), 1),
+                     first_end_us=round(float(en[sw].min()), 1), last_end_us=round(float(en[sw].max()), 1),
+                     us_per_tile=round(float(((en[sw] - ft[sw]) / t["tiles"][sw]).mean()), 2))
+        if ex.any():
+            d["exit_only_starts_us"] = [round(float(v), 1) for v in np.sort(st[ex])][:8]
+            d["exit_only_last_end_us"] = round(float(en[ex].max()), 1)
+        per.append(d)
+    worked = t["tiles"][w]
+    return {"grid": int(len(t["tiles"])), "first_start_us": round(float(st.min()), 1),
+            "span_us": round(float(en.max() - st.min()), 1), "last_end_us": round(float(en.max()), 1),
+            "tiles_per_worker": {int(k): int(v) for k, v in zip(*np.unique(worked, return_counts=True))},
+            "mean_us_per_tile": round(float(((en[w] - ft[w]) / worked).mean()), 2),
+            "per_xcd": per}
+
+
+def pd_trace(topo, dev, halves, launches: int = 10, traced: int = 4):
+    """The prefill GEMM 8192x4096x4096 alone, aware, on the XCD-aligned set
+    (6 XCDs, claiming form) and on the 192 striped CUs (static form), plus the
+    full chip: untraced ms per launch on the set's stream, then `traced`
+    traced launches queued back to back: the last one summarised per XCD and
+    the gaps between one launch's last workgroup end and the next launch's
+    first start."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    (pa, pb), _ = workloads.make_pd_inputs()
+    pa, pb = pa.to(dev), pb.to(dev)
+    cp = torch.empty((pa.shape[0], pb.shape[0]), dtype=torch.bfloat16, device=dev)
+    prefill, _, pre_x, _, pre_m, _ = pd_sets(topo, halves)
+    khz = asym.device_query(0)["wall_clock_khz"]
+    sets = {"xcd_aligned": (pre_m, pre_x), "cu_striped": (prefill, 0), "full_chip": (None, 0)}
+    out = {}
+    for name, (mask, xm) in sets.items():
+        s = asym.stream_create(topo, mask) if mask is not None else torch.cuda.current_stream()
+        try:
+            fn = lambda: asym.gemm(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s)
+            with torch.cuda.stream(s):
+                for _ in range(3):
+                    fn()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(s)
+                for _ in range(launches):
+                    fn()
+                e1.record(s)
+                s.synchronize()
+                ms = e0.elapsed_time(e1) / launches
+            asym.gemm_trace(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s)  # warm the traced kernel
+            ts = asym.gemm_trace(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s, launches=traced)
+            r = trace_summary(ts[-1], khz)
+            tick = 1e3 / khz
+            r["gaps_us"] = [round((int(b["start"].min()) - int(a["end"].max())) * tick, 1) for a, b in zip(ts, ts[1:])]
+            r["spans_us"] = [round((int(t["end"].max()) - int(t["start"].min())) * tick, 1) for t in ts]
+            r["ms_per_launch"] = round(ms, 4)
+            r["claims"] = ts[-1]["plan"]["claims"]
+            r["mask_cus_per_xcd"] = topo.cuset_counts(mask) if mask is not None else None
+            out[name] = r
+        finally:
+            if mask is not None:
+                asym.stream_destroy(s)
+    return out
+
+
 def prefill_decode(topo, dev, iters: int, halves):
     """Prefill GEMM 8192x4096x4096 on 192 CUs co-running with decode GEMM
     32x14336x4096 on the other 64, on XCD-aligned sets (6 XCDs / 2 XCDs, the
@@ -390,12 +484,7 @@ def prefill_decode(topo, dev, iters: int, halves):
     pa, pb, da, db = pa.to(dev), pb.to(dev), da.to(dev), db.to(dev)
     cp = torch.empty((pa.shape[0], pb.shape[0]), dtype=torch.bfloat16, device=dev)
     cd = torch.empty((da.shape[0], db.shape[0]), dtype=torch.bfloat16, device=dev)
-    prefill = topo.cuset(192, asym.CUSET_STRIPED)
-    decode = [b for b in range(256) if b not in set(prefill)]
-    grp = [x for x in range(8) if (halves[1] >> x) & 1]
-    dec_x = (1 << grp[-1]) | (1 << grp[-2])
-    pre_x = 0xFF & ~dec_x
-    pre_m, dec_m = topo.cuset_split_xcds(pre_x)
+    prefill, decode, pre_x, dec_x, pre_m, dec_m = pd_sets(topo, halves)
     runs = {"xcd_aligned": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=pre_m, xcd_mask=pre_x),
                                                asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=dec_m, xcd_mask=dec_x)],
                                               topo),
@@ -948,7 +1037,7 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,spread,grouped,numa,attention,mla,parity",
+    ap.add_argument("--studies", default="compare,llm,pd,pd_trace,spread,grouped,numa,attention,mla,parity",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
@@ -996,7 +1085,7 @@ def main() -> int:
         return 0
     studies = set() if args.mapping_only or args.studies == "none" else set(args.studies.split(","))
     if args.probe == "identity":
-        studies -= {"pd", "spread"}  # CU-masked sets need the mask map
+        studies -= {"pd", "pd_trace", "spread"}  # CU-masked sets need the mask map
     p = workloads.SQUARE_8192
     A, B = workloads.make_inputs(p)
     Ad, Bd = A.to(dev), B.to(dev)
@@ -1074,6 +1163,8 @@ def main() -> int:
         line["decode_gemm"] = decode_gemm(dev, stream)
     if "pd" in studies:
         line["prefill_decode"] = prefill_decode(topo, dev, 10, halves)
+    if "pd_trace" in studies:
+        line["prefill_trace"] = pd_trace(topo, dev, halves)
     if "spread" in studies:
         for tenant in args.spread_tenants.split(","):
             key = "cu_set_spread" if tenant == "copy" else f"cu_set_spread_{tenant}_tenant"

@@ -627,6 +627,36 @@ int asym_gemm_bf16_noalloc(const asym_topology* topo, int M, int N, int K,
  * most bytes of split-K partials (all nullable).  Host only; always ASYM_OK. */
 int asym_gemm_noalloc_limits(size_t* scratch_bytes, int* max_tiles, size_t* max_partial_bytes);
 
+/* ---- per-workgroup trace of the persistent GEMM ---------------------------- */
+/* One record per workgroup of a traced launch.  Times are the constant-rate
+ * clock read by s_memrealtime (asym_device_info.wall_clock_khz ticks per ms),
+ * comparable across XCDs. */
+typedef struct asym_wg_record {
+  uint64_t start;       /* the workgroup began */
+  uint64_t first_tile;  /* its first tile began (0: it computed none) */
+  uint64_t end;         /* it left */
+  uint32_t xcc;         /* XCC_ID it ran on */
+  uint32_t hw_id;       /* HW_ID register (SE, shader array, CU, SIMD, wave slot) */
+  uint32_t tiles;       /* tiles it computed */
+  uint32_t worked;      /* 1 if it computed a tile */
+} asym_wg_record;
+
+/* asym_gemm_bf16 on the persistent kernel, with every workgroup writing its
+ * record to records[block index] (caller-owned device memory, capacity
+ * entries): shows how a launch's workgroups are placed and when they start,
+ * work and leave (Section 7.1's persistent blocks; the per-CU timing the
+ * co-location studies of Sections 7.2 and 7.3 compare).  The traced kernels
+ * are separate instantiations of the same code; the bits of C are those of
+ * asym_gemm_bf16.  *n_records (host) receives the grid.  The small-M path
+ * and ASYM_B_KN are refused (ASYM_EUNSUPPORTED); capacity below the grid
+ * (asym_gemm_plan's grid) is refused (ASYM_EINVAL).  Asynchronous.
+ * Errors: those of asym_gemm_bf16. */
+int asym_gemm_bf16_trace(const asym_topology* topo, int M, int N, int K,
+                         const void* A, int lda, const void* B, int ldb,
+                         int b_layout, void* C, int ldc, int mapping,
+                         uint32_t xcd_mask, void* stream,
+                         asym_wg_record* records, int capacity, int* n_records);
+
 /* What asym_gemm_bf16 with the same arguments would launch, without
  * launching it or touching the matrices: the same checks and errors, the
  * output tile (tile_m x tile_n; the width is taken from 256, 224 and 192 to

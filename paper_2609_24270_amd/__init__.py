@@ -43,6 +43,7 @@ EXPORTS = (
     "asym_cuset_make", "asym_cuset_counts", "asym_stream_create",
     "asym_stream_destroy", "asym_schedule_build", "asym_grouped_schedule_build",
     "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_bf16_noalloc", "asym_gemm_noalloc_limits",
+    "asym_gemm_bf16_trace",
     "asym_gemm_plan", "asym_gemm_set_small_m",
     "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_mla_decode_bf16", "asym_mla_decode_plan",
     "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
@@ -263,6 +264,7 @@ def load_library(path: str = LIB_PATH):
                                ctypes.POINTER(GemmPlanInfo)]),
         "asym_gemm_set_small_m": (i, [i]),
         "asym_gemm_bf16_noalloc": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp]),
+        "asym_gemm_bf16_trace": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp, vp, i, ip]),
         "asym_gemm_noalloc_limits": (i, [ctypes.POINTER(ctypes.c_size_t), ip, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_attn_decode_bf16": (i, [topo_p, i, i, i, i, i, vp, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
         "asym_attn_decode_plan": (i, [topo_p, i, i, i, i, i, i, i, u32, vp, ctypes.POINTER(AttnPlanInfo)]),
@@ -721,6 +723,42 @@ def gemm_noalloc(A, B, C, topo: "Topology", mapping="aware", xcd_mask: int = 0, 
         ctypes.c_void_p(B.data_ptr()), B.stride(0), B_NK, ctypes.c_void_p(C.data_ptr()),
         C.stride(0), mp, xcd_mask, _stream_ptr(stream)))
     return C
+
+
+def gemm_trace(A, B, C, mapping="aware", topo: Optional["Topology"] = None, xcd_mask: int = 0, stream=None,
+               launches: int = 1):
+    """gemm() on the persistent kernel with one record per workgroup (the
+    40-byte asym_wg_record); returns a dict of numpy arrays indexed by block
+    index: start, first_tile, end (constant-rate clock ticks), xcc, hw_id,
+    tiles, worked, and the launch plan.  With launches > 1 the launches are
+    queued back to back, each with records of its own, and a list of such
+    dicts comes back.  Synchronises the stream."""
+    import numpy as np
+    import torch
+    M, K = A.shape
+    N = B.shape[0]
+    plan = gemm_plan(A, B, C, mapping=mapping, topo=topo, xcd_mask=xcd_mask, stream=stream)
+    grid = max(1, plan["grid"])
+    rec = torch.zeros((launches, grid, 10), dtype=torch.int32, device=A.device)
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    lib = load_library()
+    counts = []
+    for i in range(launches):
+        n = ctypes.c_int()
+        _check(lib.asym_gemm_bf16_trace(
+            topo.handle if topo else None, M, N, K, ctypes.c_void_p(A.data_ptr()), A.stride(0),
+            ctypes.c_void_p(B.data_ptr()), B.stride(0), B_NK, ctypes.c_void_p(C.data_ptr()), C.stride(0), mp,
+            xcd_mask, _stream_ptr(stream), ctypes.c_void_p(rec[i].data_ptr()), grid, ctypes.byref(n)))
+        counts.append(n.value)
+    (stream if stream is not None else torch.cuda.current_stream()).synchronize()
+    host = rec.cpu().numpy().view(np.uint32)
+    out = []
+    for i in range(launches):
+        r = host[i, : counts[i]]
+        u64 = lambda lo: r[:, lo].astype(np.uint64) | (r[:, lo + 1].astype(np.uint64) << np.uint64(32))
+        out.append({"start": u64(0), "first_tile": u64(2), "end": u64(4), "xcc": r[:, 6].copy(),
+                    "hw_id": r[:, 7].copy(), "tiles": r[:, 8].copy(), "worked": r[:, 9].copy(), "plan": plan})
+    return out[0] if launches == 1 else out
 
 
 def noalloc_limits() -> dict:

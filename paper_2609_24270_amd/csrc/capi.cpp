@@ -615,6 +615,42 @@ int gemm_bf16_scratch(const asym_topology* topo_in, int M, int N, int K, const v
   return launch_gemm(g, stream);
 }
 
+int gemm_bf16_trace(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda, const void* B,
+                    int ldb, int b_layout, void* C, int ldc, int mapping, uint32_t xcd_mask, hipStream_t stream,
+                    asym_wg_record* records, int capacity, int* n_records) {
+  if (!records || !n_records) return fail(ASYM_EINVAL, "gemm trace: null records");
+  if (b_layout == ASYM_B_KN) return fail(ASYM_EUNSUPPORTED, "gemm trace: B stored [K][N] is not traced");
+  std::lock_guard<std::mutex> lock(g_mu);
+  const bool prev = g_small_m.exchange(false);  // the persistent kernel, whatever the shape
+  GemmPlan P;
+  int rc = plan_gemm(topo_in, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask, stream, &P);
+  g_small_m.store(prev);
+  if (rc != ASYM_OK) return rc;
+  if (capacity < P.grid) return fail(ASYM_EINVAL, "gemm trace: capacity below the grid (" + std::to_string(P.grid) + ")");
+  const DeviceSchedule* ds = nullptr;
+  rc = upload_schedule(P.device, P.tiles_m, P.tiles_n, mapping, P.slots, stream, &ds);
+  if (rc != ASYM_OK) return rc;
+  Workspace* ws = nullptr;
+  rc = get_workspace(P.device, stream, &ws);
+  if (rc != ASYM_OK) return rc;
+  GemmLaunch g;
+  g.A = A; g.B = B; g.C = C;
+  g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
+  g.mapping = mapping;
+  g.d_order = ds->d_order; g.d_off = ds->d_off; g.d_slots = ds->d_slots;
+  g.tiles_m = P.tiles_m; g.tiles_n = P.tiles_n;
+  g.n_xccs = P.t->n_xccs;
+  g.grid = P.grid;
+  g.d_ctr = ws->gemm_ctr;
+  g.dynamic = P.dynamic;
+  g.vec = P.vec;
+  g.bn = P.bn;
+  g.bm = P.bm;
+  g.d_trace = records;
+  *n_records = P.grid;
+  return launch_gemm(g, stream);
+}
+
 int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N, int K, const void* A,
                       int lda, const void* B, int ldb, void* C, int ldc, int mapping, uint32_t xcd_mask,
                       hipStream_t stream) {
@@ -1193,6 +1229,14 @@ extern "C" int asym_gemm_bf16(const asym_topology* topo, int M, int N, int K, co
                               uint32_t xcd_mask, void* stream) {
   return asym::gemm_bf16(topo, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask,
                          static_cast<hipStream_t>(stream));
+}
+
+extern "C" int asym_gemm_bf16_trace(const asym_topology* topo, int M, int N, int K, const void* A, int lda,
+                                    const void* B, int ldb, int b_layout, void* C, int ldc, int mapping,
+                                    uint32_t xcd_mask, void* stream, asym_wg_record* records, int capacity,
+                                    int* n_records) {
+  return asym::gemm_bf16_trace(topo, M, N, K, A, lda, B, ldb, b_layout, C, ldc, mapping, xcd_mask,
+                               static_cast<hipStream_t>(stream), records, capacity, n_records);
 }
 
 extern "C" int asym_gemm_grouped_bf16(const asym_topology* topo, int G, const int* M, int N, int K,

@@ -74,6 +74,7 @@ struct Params {
   int* ctr;          // dynamic aware: [0,16) rank tickets, [16,32) tile counters, [32] exits
   int dynamic;       // aware mapping with claims instead of the static assignment
   const int4* desc;  // grouped GEMM: per tile {first row, rows, group's first B row, first column}
+  asym_wg_record* trace;  // traced launches: one record per workgroup (null otherwise)
 };
 
 // Where a tile lies.  Plain GEMM: tile = row-major index in the tile grid.
@@ -774,11 +775,36 @@ __device__ __forceinline__ int read_box(const int* box) {
   return v;
 }
 
-template <bool VEC, int NBF, int TE = 0>
+// Per-workgroup record of a traced launch (TRACE): the constant-rate clock
+// (s_memrealtime) when the workgroup starts, when its first tile starts and
+// when it leaves, the XCC and hardware IDs it ran on and how many tiles it
+// computed.  The traced kernels are separate instantiations, so the untraced
+// ones carry none of this.
+__device__ __forceinline__ unsigned long long wall_clock() { return __builtin_amdgcn_s_memrealtime(); }
+
+__device__ __forceinline__ void trace_record(const Params& p, unsigned long long t0, unsigned long long t_first,
+                                             int tiles, int worked) {
+  if (threadIdx.x != 0) return;
+  uint32_t xr, hw;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xr));
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+  asym_wg_record r;
+  r.start = t0;
+  r.first_tile = t_first;
+  r.end = wall_clock();
+  r.xcc = xr & 0xFu;
+  r.hw_id = hw;
+  r.tiles = (uint32_t)tiles;
+  r.worked = (uint32_t)worked;
+  p.trace[blockIdx.x] = r;
+}
+
+template <bool VEC, int NBF, int TE = 0, bool TRACE = false>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 gemm_bf16_persistent(Params p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[TE == 0 ? RING_BYTES : 2 * (2 * TE) * LDP * 2];
   int* const box = reinterpret_cast<int*>(lds);  // tile broadcast, used between tiles only
+  const unsigned long long t_start = TRACE ? wall_clock() : 0ull;
 
   // Static aware assignment: workgroup b belongs to XCD b mod n and is that
   // XCD's (b / n)-th persistent worker (the hardware deals workgroups to XCDs
@@ -817,7 +843,10 @@ gemm_bf16_persistent(Params p) {
   } else if (aware) {
     const int x = (int)blockIdx.x % p.n_xccs, r = (int)blockIdx.x / p.n_xccs;
     const int s_x = p.slots[x];
-    if (r >= s_x) return;  // the whole workgroup, before any barrier
+    if (r >= s_x) {  // the whole workgroup, before any barrier
+      if constexpr (TRACE) trace_record(p, t_start, 0ull, 0, 0);
+      return;
+    }
     nt.i_next = p.off[x] + r;
     nt.step = s_x;
     nt.end = p.off[x + 1];
@@ -849,8 +878,11 @@ gemm_bf16_persistent(Params p) {
   } else {
     tile = nt.i_next < nt.end ? __builtin_amdgcn_readfirstlane(p.order[nt.i_next]) : -1;
   }
+  const unsigned long long t_first = TRACE ? wall_clock() : 0ull;
+  int n_tiles_done = 0;
   while (tile >= 0) {
     nt.i_next += nt.step;
+    if constexpr (TRACE) ++n_tiles_done;
     run_tile<VEC, NBF, TE>(p, tile, lds, nt);
     if (threadIdx.x < 64) {
       const int nxt = take_next(p, nt, xcc, q_lane);
@@ -858,6 +890,7 @@ gemm_bf16_persistent(Params p) {
     }
     tile = read_box(box);
   }
+  if constexpr (TRACE) trace_record(p, t_start, t_first, n_tiles_done, n_tiles_done > 0);
   if (dyn && threadIdx.x == 0) {
     // the last workgroup to leave resets the counters for the next launch
     __threadfence();
@@ -867,6 +900,29 @@ gemm_bf16_persistent(Params p) {
       __threadfence();
     }
   }
+}
+
+template <bool TRACE>
+int launch_gemm_kind(const GemmLaunch& g, const Params& p, hipStream_t s) {
+  if (g.bm == 128 && g.bn == 128) {
+    if (g.vec)
+      hipLaunchKernelGGL((gemm_bf16_persistent<true, 8, 128, TRACE>), dim3(g.grid), dim3(NT), 0, s, p);
+    else
+      hipLaunchKernelGGL((gemm_bf16_persistent<false, 8, 128, TRACE>), dim3(g.grid), dim3(NT), 0, s, p);
+  } else if (g.bm != 256) {
+    return fail(ASYM_EINVAL, "gemm: unsupported tile height");
+  } else if (!g.vec)
+    hipLaunchKernelGGL((gemm_bf16_persistent<false, 8, 256, TRACE>), dim3(g.grid), dim3(NT), 0, s, p);
+  else if (g.bn == 256)
+    hipLaunchKernelGGL((gemm_bf16_persistent<true, 8, 0, TRACE>), dim3(g.grid), dim3(NT), 0, s, p);
+  else if (g.bn == 224)
+    hipLaunchKernelGGL((gemm_bf16_persistent<true, 7, 0, TRACE>), dim3(g.grid), dim3(NT), 0, s, p);
+  else if (g.bn == 192)
+    hipLaunchKernelGGL((gemm_bf16_persistent<true, 6, 0, TRACE>), dim3(g.grid), dim3(NT), 0, s, p);
+  else
+    return fail(ASYM_EINVAL, "gemm: unsupported tile width");
+  ASYM_HIP(hipGetLastError());
+  return ASYM_OK;
 }
 
 }  // namespace
@@ -884,25 +940,8 @@ int launch_gemm(const GemmLaunch& g, hipStream_t s) {
   p.order = g.d_order; p.off = g.d_off; p.slots = g.d_slots; p.ctr = g.d_ctr;
   p.dynamic = g.dynamic ? 1 : 0;
   p.desc = static_cast<const int4*>(g.d_desc);
-  if (g.bm == 128 && g.bn == 128) {
-    if (g.vec)
-      hipLaunchKernelGGL((gemm_bf16_persistent<true, 8, 128>), dim3(g.grid), dim3(NT), 0, s, p);
-    else
-      hipLaunchKernelGGL((gemm_bf16_persistent<false, 8, 128>), dim3(g.grid), dim3(NT), 0, s, p);
-  } else if (g.bm != 256) {
-    return fail(ASYM_EINVAL, "gemm: unsupported tile height");
-  } else if (!g.vec)
-    hipLaunchKernelGGL((gemm_bf16_persistent<false, 8, 256>), dim3(g.grid), dim3(NT), 0, s, p);
-  else if (g.bn == 256)
-    hipLaunchKernelGGL((gemm_bf16_persistent<true, 8>), dim3(g.grid), dim3(NT), 0, s, p);
-  else if (g.bn == 224)
-    hipLaunchKernelGGL((gemm_bf16_persistent<true, 7>), dim3(g.grid), dim3(NT), 0, s, p);
-  else if (g.bn == 192)
-    hipLaunchKernelGGL((gemm_bf16_persistent<true, 6>), dim3(g.grid), dim3(NT), 0, s, p);
-  else
-    return fail(ASYM_EINVAL, "gemm: unsupported tile width");
-  ASYM_HIP(hipGetLastError());
-  return ASYM_OK;
+  p.trace = static_cast<asym_wg_record*>(g.d_trace);
+  return g.d_trace ? launch_gemm_kind<true>(g, p, s) : launch_gemm_kind<false>(g, p, s);
 }
 
 int gemm_tile_m() { return BM; }

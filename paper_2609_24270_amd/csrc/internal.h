@@ -103,6 +103,7 @@ struct GemmLaunch {
   int bn;                      // tile width: 256, or 224 / 192 on the vector path; 128 with bm = 128
   int bm = 256;                // tile height: 256, or 128 (128 x 128 tiles, register-staged path)
   const void* d_desc = nullptr; // grouped GEMM: device int4 per tile {row, rows, group B row, column}
+  void* d_trace = nullptr;      // traced launch: device asym_wg_record per workgroup
 };
 int launch_gemm(const GemmLaunch& g, hipStream_t s);
 

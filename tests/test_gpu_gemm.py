@@ -307,3 +307,30 @@ def test_gemm_ring_stage_isolation(dev, width, M, N, KT):
             _, ref = oracle.gemm_bf16(bits(ta), bits(tb), "nk")
             C = run(ta.to(dev), tb.to(dev), "aware", xcd_mask=1)
             assert np.array_equal(bits(C), ref), f"width {width}: {which} stage {s} of {KT}"
+
+
+def test_gemm_trace_records(dev):
+    """The traced launch gives the bits of the untraced one and one record per
+    workgroup: every tile computed once in all, on the XCC each record names,
+    within the launch's time span; on the full chip (static aware form) every
+    worker computes its region's share; under a whole-XCD restriction only the
+    chosen XCDs' workgroups work."""
+    topo = asym.probe_topology(0, asym.PROBE_IDENTITY)
+    A, B = workloads.make_inputs(workloads.make_problem(4096, 4096, 1024, seed=77))
+    Ad, Bd = A.to(dev), B.to(dev)
+    ref = asym.gemm(Ad, Bd, topo=topo)
+    C = torch.zeros_like(ref)
+    t = asym.gemm_trace(Ad, Bd, C, topo=topo)
+    assert torch.equal(C, ref)
+    T = t["plan"]["tiles_m"] * t["plan"]["tiles_n"]
+    assert len(t["tiles"]) == t["plan"]["grid"] == 256 and int(t["tiles"].sum()) == T == 256
+    assert set(t["xcc"].tolist()) <= set(range(8)) and all(t["end"] >= t["start"])
+    assert all(t["tiles"][t["worked"] == 1] >= 1) and int(t["worked"].sum()) == 256
+    for x in range(8):
+        assert int(t["tiles"][t["xcc"] == x].sum()) == 32, x
+    C.zero_()
+    t = asym.gemm_trace(Ad, Bd, C, topo=topo, xcd_mask=0x0F)
+    assert torch.equal(C, ref)
+    assert int(t["tiles"].sum()) == 256 and set(t["xcc"][t["worked"] == 1].tolist()) <= {0, 1, 2, 3}
+    span = (int(t["end"].max()) - int(t["start"].min())) / (asym.device_query(0)["wall_clock_khz"] / 1e3)
+    print(f"traced 4096x4096x1024 on XCDs 0-3: {span:.1f} us from the first start to the last end")

@@ -168,9 +168,10 @@ def gemm_asm(tmp_path_factory):
     return out.read_text()
 
 
+@pytest.mark.parametrize("trace", [0, 1])
 @pytest.mark.parametrize("nbf", [8, 7, 6])
-def test_no_use_of_fragments_in_flight(gemm_asm, nbf):
-    kernel = f"_ZN4asym12_GLOBAL__N_120gemm_bf16_persistentILb1ELi{nbf}ELi0EEEvNS0_6ParamsE"
+def test_no_use_of_fragments_in_flight(gemm_asm, nbf, trace):
+    kernel = f"_ZN4asym12_GLOBAL__N_120gemm_bf16_persistentILb1ELi{nbf}ELi0ELb{trace}EEEvNS0_6ParamsE"
     v = inflight_violations(gemm_asm, kernel)
     assert not v, f"{len(v)} instructions touch fragment registers still being read, e.g. {v[:4]}"
 

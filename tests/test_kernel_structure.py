@@ -128,7 +128,7 @@ def test_gemm_tile_claim_is_published_in_its_own_loop(tmp):
     """The dynamic aware form claims tiles on per-XCD counters (offset 64 and
     up) inside the tile loop; every such claim must sit in the loop whose
     barrier publishes it.  No scalar-cache writes of any kind."""
-    body = function_body(asm_of("gemm.hip", tmp), "gemm_bf16_persistentILb1ELi8ELi0E")
+    body = function_body(asm_of("gemm.hip", tmp), "gemm_bf16_persistentILb1ELi8ELi0ELb0E")
     insts = annotate_loops(body)
     n = claims_published_in_their_loop(insts, r"^global_atomic_add v\d+, v\d+, v\d+, s\[\d+:\d+\]( offset:\d+)? sc0")
     assert n >= 1
