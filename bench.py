@@ -400,6 +400,8 @@ def trace_summary(t: dict, khz: int, t0: Optional[int] = None) -> dict:
     rel = lambda v: (v.astype(np.int64) - t0) * (1e3 / khz)
     st, ft, en = rel(t["start"]), rel(t["first_tile"]), rel(t["end"])
     w = t["worked"] == 1
+    live = np.maximum(1, (t["end"] - t["start"]).astype(np.int64))
+    mhz = t["cycles"].astype(np.float64) * khz / live / 1e3  # shader clock over each workgroup's life
     cu = (t["hw_id"] >> 8) & 0xFF
     per = []
     for x in range(8):
@@ -410,7 +412,9 @@ def trace_summary(t: dict, khz: int, t0: Optional[int] = None) -> dict:
         if sw.any():
             d.update(last_start_us=round(float(st[sw].max()), 1), first_tile_by_us=round(float(ft[sw].max()), 1),
                      first_end_us=round(float(en[sw].min()), 1), last_end_us=round(float(en[sw].max()), 1),
-                     us_per_tile=round(float(((en[sw] - ft[sw]) / t["tiles"][sw]).mean()), 2))
+                     us_per_tile=round(float(((en[sw] - ft[sw]) / t["tiles"][sw]).mean()), 2),
+                     clock_mhz=round(float(mhz[sw].mean()), 0))
+            d["kcycles_per_tile"] = round(d["us_per_tile"] * d["clock_mhz"] / 1e3, 1)
         if ex.any():
             d["exit_only_starts_us"] = [round(float(v), 1) for v in np.sort(st[ex])][:8]
             d["exit_only_last_end_us"] = round(float(en[ex].max()), 1)
@@ -420,16 +424,44 @@ def trace_summary(t: dict, khz: int, t0: Optional[int] = None) -> dict:
             "span_us": round(float(en.max() - st.min()), 1), "last_end_us": round(float(en.max()), 1),
             "tiles_per_worker": {int(k): int(v) for k, v in zip(*np.unique(worked, return_counts=True))},
             "mean_us_per_tile": round(float(((en[w] - ft[w]) / worked).mean()), 2),
+            "mean_clock_mhz": round(float(mhz[w].mean()), 0),
             "per_xcd": per}
 
 
-def pd_trace(topo, dev, halves, launches: int = 10, traced: int = 4):
+def array_balance(t: dict, topo, mask, khz: int) -> list:
+    """Per XCD and shader array (engine * 2 + array, from HW_ID): the mask's
+    CUs there, the workgroups that started within 5 us of the launch's first
+    start, and those that started later (they waited for a CU)."""
+    import numpy as np
+    cus = topo.json()["cus"]  # [xcc, se, sh, cu, mask bit]
+    bits = set(range(256)) if mask is None else set(mask)
+    arr = lambda se, sh: se * 2 + sh
+    n_arr = 1 + max(arr(c[1], c[2]) for c in cus)
+    rel = (t["start"].astype(np.int64) - int(t["start"].min())) * (1e3 / khz)
+    se, sh = (t["hw_id"] >> 13) & 0x7, (t["hw_id"] >> 12) & 0x1
+    out = []
+    for x in range(8):
+        m = [0] * n_arr
+        for c in cus:
+            if c[0] == x and c[4] in bits:
+                m[arr(c[1], c[2])] += 1
+        sel = t["xcc"] == x
+        early = [int(np.sum(sel & (rel < 5.0) & (arr(se, sh) == a))) for a in range(n_arr)]
+        late = [int(np.sum(sel & (rel >= 5.0) & (arr(se, sh) == a))) for a in range(n_arr)]
+        out.append({"mask_cus": m, "started_at_launch": early, "started_late": late})
+    return out
+
+
+def pd_trace(topo, dev, halves, launches: int = 10, traced: int = 4, warm_ms=(0, 20, 500)):
     """The prefill GEMM 8192x4096x4096 alone, aware, on the XCD-aligned set
     (6 XCDs, claiming form) and on the 192 striped CUs (static form), plus the
-    full chip: untraced ms per launch on the set's stream, then `traced`
-    traced launches queued back to back: the last one summarised per XCD and
-    the gaps between one launch's last workgroup end and the next launch's
-    first start."""
+    full chip: untraced ms per launch from the co-run executor (launched from
+    native code, as the co-run studies time it), then for each warm-up length
+    (ms of untraced launches queued just before, after 50 ms idle) `traced`
+    traced launches queued back to back.  Each warm-up gets the last traced
+    launch's span and mean shader clock; the longest one also its per-XCD
+    summary, the shader-array balance and the gaps between one launch's last
+    workgroup end and the next launch's first start."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -439,31 +471,30 @@ def pd_trace(topo, dev, halves, launches: int = 10, traced: int = 4):
     cp = torch.empty((pa.shape[0], pb.shape[0]), dtype=torch.bfloat16, device=dev)
     prefill, _, pre_x, _, pre_m, _ = pd_sets(topo, halves)
     khz = asym.device_query(0)["wall_clock_khz"]
+    tick = 1e3 / khz
     sets = {"xcd_aligned": (pre_m, pre_x), "cu_striped": (prefill, 0), "full_chip": (None, 0)}
     out = {}
     for name, (mask, xm) in sets.items():
+        asym.corun([asym.gemm_task(pa, pb, cp, 3, "aware", mask=mask, xcd_mask=xm)], topo)
+        ms = asym.corun([asym.gemm_task(pa, pb, cp, launches, "aware", mask=mask, xcd_mask=xm)], topo)[0]["ms_per_iter"]
         s = asym.stream_create(topo, mask) if mask is not None else torch.cuda.current_stream()
         try:
-            fn = lambda: asym.gemm(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s)
-            with torch.cuda.stream(s):
-                for _ in range(3):
-                    fn()
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record(s)
-                for _ in range(launches):
-                    fn()
-                e1.record(s)
-                s.synchronize()
-                ms = e0.elapsed_time(e1) / launches
-            asym.gemm_trace(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s)  # warm the traced kernel
-            ts = asym.gemm_trace(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s, launches=traced)
-            r = trace_summary(ts[-1], khz)
-            tick = 1e3 / khz
+            asym.gemm_trace(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s)  # load the traced kernel
+            warm = {}
+            for w in warm_ms:
+                time.sleep(0.05)
+                for _ in range(int(w / ms) if w else 0):
+                    asym.gemm(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s)
+                ts = asym.gemm_trace(pa, pb, cp, topo=topo, xcd_mask=xm, stream=s, launches=traced)
+                r = trace_summary(ts[-1], khz)
+                warm[w] = {"spans_us": [round((int(t["end"].max()) - int(t["start"].min())) * tick, 1) for t in ts],
+                           "clock_mhz": r["mean_clock_mhz"]}
             r["gaps_us"] = [round((int(b["start"].min()) - int(a["end"].max())) * tick, 1) for a, b in zip(ts, ts[1:])]
-            r["spans_us"] = [round((int(t["end"].max()) - int(t["start"].min())) * tick, 1) for t in ts]
+            r["after_warm_up_ms"] = warm
             r["ms_per_launch"] = round(ms, 4)
             r["claims"] = ts[-1]["plan"]["claims"]
             r["mask_cus_per_xcd"] = topo.cuset_counts(mask) if mask is not None else None
+            r["arrays"] = array_balance(ts[-1], topo, mask, khz)
             out[name] = r
         finally:
             if mask is not None:
@@ -471,11 +502,13 @@ def pd_trace(topo, dev, halves, launches: int = 10, traced: int = 4):
     return out
 
 
-def prefill_decode(topo, dev, iters: int, halves):
+def prefill_decode(topo, dev, iters: int, halves, warm: int = 0):
     """Prefill GEMM 8192x4096x4096 on 192 CUs co-running with decode GEMM
     32x14336x4096 on the other 64, on XCD-aligned sets (6 XCDs / 2 XCDs, the
     decode pair taken from one affinity group) and on CU-striped sets (24 / 8
-    CUs of every XCD); aware mapping; each also alone on its set."""
+    CUs of every XCD); aware mapping; each also alone on its set.  Every run
+    first runs `warm` times its timed launches untimed (warm = 100: about
+    300 ms), so the shader clock has risen under that run's own load."""
     import torch
 
     import paper_2609_24270_amd as asym
@@ -485,20 +518,15 @@ def prefill_decode(topo, dev, iters: int, halves):
     cp = torch.empty((pa.shape[0], pb.shape[0]), dtype=torch.bfloat16, device=dev)
     cd = torch.empty((da.shape[0], db.shape[0]), dtype=torch.bfloat16, device=dev)
     prefill, decode, pre_x, dec_x, pre_m, dec_m = pd_sets(topo, halves)
-    runs = {"xcd_aligned": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=pre_m, xcd_mask=pre_x),
-                                               asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=dec_m, xcd_mask=dec_x)],
-                                              topo),
-            "cu_striped": lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=prefill),
-                                              asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=decode)], topo)}
-    alone = {"xcd_aligned": (lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=pre_m, xcd_mask=pre_x)], topo),
-                             lambda: asym.corun([asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=dec_m, xcd_mask=dec_x)], topo)),
-             "cu_striped": (lambda: asym.corun([asym.gemm_task(pa, pb, cp, iters, "aware", mask=prefill)], topo),
-                            lambda: asym.corun([asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=decode)], topo))}
+    pre = lambda mask, xm: asym.gemm_task(pa, pb, cp, iters, "aware", mask=mask, xcd_mask=xm, warm_iters=warm * iters)
+    dec = lambda mask, xm: asym.gemm_task(da, db, cd, 3 * iters, "aware", mask=mask, xcd_mask=xm,
+                                          warm_iters=warm * 3 * iters)
+    sets = {"xcd_aligned": ((pre_m, pre_x), (dec_m, dec_x)), "cu_striped": ((prefill, 0), (decode, 0))}
     out = {}
     for _ in range(2):  # first round settles the clock; the second is kept
-        for k, fn in runs.items():
-            r = fn()
-            p_alone, d_alone = alone[k][0]()[0], alone[k][1]()[0]
+        for k, (ps, ds) in sets.items():
+            r = asym.corun([pre(*ps), dec(*ds)], topo)
+            p_alone, d_alone = asym.corun([pre(*ps)], topo)[0], asym.corun([dec(*ds)], topo)[0]
             out[k] = {"prefill_ms": round(r[0]["ms_per_iter"], 4), "prefill_tflops": round(r[0]["tflops"], 2),
                       "decode_ms": round(r[1]["ms_per_iter"], 4), "decode_tflops": round(r[1]["tflops"], 2),
                       "prefill_alone_ms": round(p_alone["ms_per_iter"], 4),
@@ -1162,7 +1190,8 @@ def main() -> int:
         line["llm_shapes_tflops"] = llm_shapes(dev, stream, 20)
         line["decode_gemm"] = decode_gemm(dev, stream)
     if "pd" in studies:
-        line["prefill_decode"] = prefill_decode(topo, dev, 10, halves)
+        line["prefill_decode"] = prefill_decode(topo, dev, 10, halves, warm=100)
+        line["prefill_decode_after_idle"] = prefill_decode(topo, dev, 10, halves, warm=0)
     if "pd_trace" in studies:
         line["prefill_trace"] = pd_trace(topo, dev, halves)
     if "spread" in studies:

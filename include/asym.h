@@ -639,6 +639,8 @@ typedef struct asym_wg_record {
   uint32_t hw_id;       /* HW_ID register (SE, shader array, CU, SIMD, wave slot) */
   uint32_t tiles;       /* tiles it computed */
   uint32_t worked;      /* 1 if it computed a tile */
+  uint64_t cycles;      /* shader-clock cycles (s_memtime) from start to end: with
+                           end - start, the mean clock of the CU it ran on */
 } asym_wg_record;
 
 /* asym_gemm_bf16 on the persistent kernel, with every workgroup writing its
@@ -647,8 +649,10 @@ typedef struct asym_wg_record {
  * work and leave (Section 7.1's persistent blocks; the per-CU timing the
  * co-location studies of Sections 7.2 and 7.3 compare).  The traced kernels
  * are separate instantiations of the same code; the bits of C are those of
- * asym_gemm_bf16.  *n_records (host) receives the grid.  The small-M path
- * and ASYM_B_KN are refused (ASYM_EUNSUPPORTED); capacity below the grid
+ * asym_gemm_bf16.  *n_records (host) receives the grid.  Every shape runs
+ * the persistent kernel (the small-M kernel has no traced form, so a product
+ * asym_gemm_bf16 would give to it gets the persistent kernel's bits);
+ * ASYM_B_KN is refused (ASYM_EUNSUPPORTED); capacity below the grid
  * (asym_gemm_plan's grid) is refused (ASYM_EINVAL).  Asynchronous.
  * Errors: those of asym_gemm_bf16. */
 int asym_gemm_bf16_trace(const asym_topology* topo, int M, int N, int K,
@@ -837,6 +841,9 @@ typedef struct asym_task {
                                                  a multiple of 16, < 2^40 */
   int grid;        /* copy / read: workgroups; 0 = 8 per CU of the XCD of its set
                       with the most CUs, times the XCD count */
+  int warm_iters;  /* untimed launches / passes queued right before the timed
+                      ones (>= 0), so the shader clock has settled under the
+                      co-run's own load when timing starts */
 } asym_task;
 
 typedef struct asym_task_result {
@@ -863,7 +870,12 @@ typedef struct asym_task_result {
  * copy task with iters < 1 is refused; size the passes to outlast the GEMMs.
  * Every GEMM task is launched once, untimed, before the release, so that its
  * one-time setup (workspace, schedule upload) does not wait for tasks already
- * running.  Synchronous.
+ * running.  With warm_iters > 0 on any task, every task first runs its
+ * warm_iters untimed (the caller sizes them to end together) and each
+ * stream's timed part waits for every task's warm-up to end: the shader clock
+ * rises over tens to hundreds of milliseconds of sustained load, so a short
+ * timed co-run straight after an idle host sync runs at a lower clock than
+ * the same co-run in steady state.  Synchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_corun(const asym_topology* topo, const asym_task* tasks, int n_tasks,
                asym_task_result* out);

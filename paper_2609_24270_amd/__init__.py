@@ -153,7 +153,7 @@ class Task(ctypes.Structure):
                 ("mapping", ctypes.c_int), ("M", ctypes.c_int), ("N", ctypes.c_int),
                 ("K", ctypes.c_int), ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
                 ("C", ctypes.c_void_p), ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p),
-                ("n_bytes", ctypes.c_size_t), ("grid", ctypes.c_int)]
+                ("n_bytes", ctypes.c_size_t), ("grid", ctypes.c_int), ("warm_iters", ctypes.c_int)]
 
 
 class MlaPlanInfo(ctypes.Structure):
@@ -728,18 +728,22 @@ def gemm_noalloc(A, B, C, topo: "Topology", mapping="aware", xcd_mask: int = 0, 
 def gemm_trace(A, B, C, mapping="aware", topo: Optional["Topology"] = None, xcd_mask: int = 0, stream=None,
                launches: int = 1):
     """gemm() on the persistent kernel with one record per workgroup (the
-    40-byte asym_wg_record); returns a dict of numpy arrays indexed by block
+    48-byte asym_wg_record); returns a dict of numpy arrays indexed by block
     index: start, first_tile, end (constant-rate clock ticks), xcc, hw_id,
-    tiles, worked, and the launch plan.  With launches > 1 the launches are
+    tiles, worked, cycles (shader clock, start to end), and the launch plan.  With launches > 1 the launches are
     queued back to back, each with records of its own, and a list of such
     dicts comes back.  Synchronises the stream."""
     import numpy as np
     import torch
     M, K = A.shape
     N = B.shape[0]
-    plan = gemm_plan(A, B, C, mapping=mapping, topo=topo, xcd_mask=xcd_mask, stream=stream)
+    prev = set_small_m(False)  # the plan of the persistent kernel, which the trace runs
+    try:
+        plan = gemm_plan(A, B, C, mapping=mapping, topo=topo, xcd_mask=xcd_mask, stream=stream)
+    finally:
+        set_small_m(prev)
     grid = max(1, plan["grid"])
-    rec = torch.zeros((launches, grid, 10), dtype=torch.int32, device=A.device)
+    rec = torch.zeros((launches, grid, 12), dtype=torch.int32, device=A.device)
     mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
     lib = load_library()
     counts = []
@@ -757,7 +761,8 @@ def gemm_trace(A, B, C, mapping="aware", topo: Optional["Topology"] = None, xcd_
         r = host[i, : counts[i]]
         u64 = lambda lo: r[:, lo].astype(np.uint64) | (r[:, lo + 1].astype(np.uint64) << np.uint64(32))
         out.append({"start": u64(0), "first_tile": u64(2), "end": u64(4), "xcc": r[:, 6].copy(),
-                    "hw_id": r[:, 7].copy(), "tiles": r[:, 8].copy(), "worked": r[:, 9].copy(), "plan": plan})
+                    "hw_id": r[:, 7].copy(), "tiles": r[:, 8].copy(), "worked": r[:, 9].copy(),
+                    "cycles": u64(10), "plan": plan})
     return out[0] if launches == 1 else out
 
 
@@ -951,8 +956,9 @@ def copy(dst, src, passes: int = 1, stop_flag=None, xcd_mask: int = 0, stream=No
     return dst
 
 
-def gemm_task(A, B, C, iters: int, mapping="aware", mask=None, xcd_mask: int = 0) -> Task:
+def gemm_task(A, B, C, iters: int, mapping="aware", mask=None, xcd_mask: int = 0, warm_iters: int = 0) -> Task:
     t = Task()
+    t.warm_iters = warm_iters
     t.kind = 0
     if mask is not None:
         m = mask_words(mask)
@@ -967,9 +973,11 @@ def gemm_task(A, B, C, iters: int, mapping="aware", mask=None, xcd_mask: int = 0
     return t
 
 
-def copy_task(dst, src, passes: int, mask=None, xcd_mask: int = 0, grid: int = 0) -> Task:
-    """The streaming-copy tenant: `passes` copies of src into dst."""
+def copy_task(dst, src, passes: int, mask=None, xcd_mask: int = 0, grid: int = 0, warm_passes: int = 0) -> Task:
+    """The streaming-copy tenant: `passes` copies of src into dst (after
+    `warm_passes` untimed ones)."""
     t = Task()
+    t.warm_iters = warm_passes
     t.kind = 1
     t.grid = grid
     if mask is not None:
@@ -983,10 +991,12 @@ def copy_task(dst, src, passes: int, mask=None, xcd_mask: int = 0, grid: int = 0
     return t
 
 
-def read_task(src, passes: int, mask=None, xcd_mask: int = 0, grid: int = 0) -> Task:
+def read_task(src, passes: int, mask=None, xcd_mask: int = 0, grid: int = 0, warm_passes: int = 0) -> Task:
     """A bandwidth-bound co-runner: `passes` whole reads of the CUDA tensor src,
-    on `grid` workgroups (0: 8 per CU of its XCD with the most CUs, on every XCD)."""
+    on `grid` workgroups (0: 8 per CU of its XCD with the most CUs, on every XCD),
+    after `warm_passes` untimed ones."""
     t = Task()
+    t.warm_iters = warm_passes
     t.grid = grid
     t.kind = 2
     if mask is not None:

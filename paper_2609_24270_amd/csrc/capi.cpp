@@ -615,6 +615,8 @@ int gemm_bf16_scratch(const asym_topology* topo_in, int M, int N, int K, const v
   return launch_gemm(g, stream);
 }
 
+static_assert(sizeof(asym_wg_record) == 48, "the trace record layout is part of the ABI");
+
 int gemm_bf16_trace(const asym_topology* topo_in, int M, int N, int K, const void* A, int lda, const void* B,
                     int ldb, int b_layout, void* C, int ldc, int mapping, uint32_t xcd_mask, hipStream_t stream,
                     asym_wg_record* records, int capacity, int* n_records) {

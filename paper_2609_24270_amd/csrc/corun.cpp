@@ -55,6 +55,7 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
   Guard g;
   for (int i = 0; i < n_tasks; ++i) {
     const asym_task& t = tasks[i];
+    if (t.warm_iters < 0) return fail(ASYM_EINVAL, "corun: warm_iters must be >= 0");
     if (t.kind == 0) {
       if (t.iters < 1 || !t.A || !t.B || !t.C) return fail(ASYM_EINVAL, "corun: bad GEMM task");
     } else if (t.kind == 1) {
@@ -122,13 +123,33 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
     ASYM_HIP(hipMalloc(&sink[i], (size_t)read_grid[i] * 256 * 16));
     g.sinks.push_back(sink[i]);
   }
-  std::vector<hipEvent_t> ev0(n_tasks), ev1(n_tasks);
+  bool warm = false;
+  for (int i = 0; i < n_tasks; ++i) warm |= tasks[i].warm_iters > 0;
+  std::vector<hipEvent_t> ev0(n_tasks), ev1(n_tasks), evw(n_tasks);
   for (int i = 0; i < n_tasks; ++i) {
     ASYM_HIP(hipEventCreate(&ev0[i]));
     g.events.push_back(ev0[i]);
     ASYM_HIP(hipEventCreate(&ev1[i]));
     g.events.push_back(ev1[i]);
+    ASYM_HIP(hipEventCreateWithFlags(&evw[i], hipEventDisableTiming));
+    g.events.push_back(evw[i]);
   }
+  // `n` launches (GEMM) or passes (copy, read) of task i on its stream
+  auto enqueue = [&](int i, int n) -> int {
+    const asym_task& t = tasks[i];
+    hipStream_t s = g.streams[i];
+    if (n < 1) return ASYM_OK;
+    if (t.kind == 2)
+      return asym::launch_stream_read(t.src, t.n_bytes, n, sink[i], read_grid[i], read_cus[i].data(), n_x, s);
+    if (t.kind == 1)
+      return asym::launch_copy(t.dst, t.src, t.n_bytes, n, nullptr, read_cus[i].data(), n_x, read_grid[i], s);
+    for (int it = 0; it < n; ++it) {
+      int rc = asym::gemm_bf16(topo, t.M, t.N, t.K, t.A, t.K, t.B, t.K, ASYM_B_NK, t.C, t.N, t.mapping,
+                               t.xcd_mask, s);
+      if (rc != ASYM_OK) return rc;
+    }
+    return ASYM_OK;
+  };
   // one untimed launch of every GEMM task on its own stream before the
   // release: its first launch on a new stream or CU set does one-time setup
   // (workspace, schedule upload) that waits on its stream, which must not
@@ -142,29 +163,29 @@ extern "C" int asym_corun(const asym_topology* topo, const asym_task* tasks, int
   }
   ASYM_HIP(hipDeviceSynchronize());
 
+  // warm-up: every task's untimed part, then each stream waits for all of
+  // them (no cycle: each stream records its event before its own waits)
+  if (warm) {
+    for (int pass = 0; pass < 2; ++pass)
+      for (int i = 0; i < n_tasks; ++i) {
+        if ((pass == 0) != (tasks[i].kind != 0)) continue;
+        int rc = enqueue(i, tasks[i].warm_iters);
+        if (rc != ASYM_OK) return rc;
+        ASYM_HIP(hipEventRecord(evw[i], g.streams[i]));
+      }
+    for (int i = 0; i < n_tasks; ++i)
+      for (int j = 0; j < n_tasks; ++j)
+        if (j != i) ASYM_HIP(hipStreamWaitEvent(g.streams[i], evw[j], 0));
+  }
   // copies and reads first, so they are streaming when the GEMMs start
   for (int pass = 0; pass < 2; ++pass) {
     for (int i = 0; i < n_tasks; ++i) {
       const asym_task& t = tasks[i];
       if ((pass == 0) != (t.kind != 0)) continue;
-      hipStream_t s = g.streams[i];
-      ASYM_HIP(hipEventRecord(ev0[i], s));
-      if (t.kind == 2) {
-        int rc = asym::launch_stream_read(t.src, t.n_bytes, t.iters, sink[i], read_grid[i], read_cus[i].data(),
-                                          n_x, s);
-        if (rc != ASYM_OK) return rc;
-      } else if (t.kind == 1) {
-        int rc = asym::launch_copy(t.dst, t.src, t.n_bytes, t.iters, nullptr, read_cus[i].data(), n_x,
-                                   read_grid[i], s);
-        if (rc != ASYM_OK) return rc;
-      } else {
-        for (int it = 0; it < t.iters; ++it) {
-          int rc = asym::gemm_bf16(topo, t.M, t.N, t.K, t.A, t.K, t.B, t.K, ASYM_B_NK, t.C, t.N,
-                                   t.mapping, t.xcd_mask, s);
-          if (rc != ASYM_OK) return rc;
-        }
-      }
-      ASYM_HIP(hipEventRecord(ev1[i], s));
+      ASYM_HIP(hipEventRecord(ev0[i], g.streams[i]));
+      int rc = enqueue(i, t.iters);
+      if (rc != ASYM_OK) return rc;
+      ASYM_HIP(hipEventRecord(ev1[i], g.streams[i]));
     }
   }
   for (int i = 0; i < n_tasks; ++i) ASYM_HIP(hipEventSynchronize(ev1[i]));

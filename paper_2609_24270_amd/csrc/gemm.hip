@@ -781,9 +781,10 @@ __device__ __forceinline__ int read_box(const int* box) {
 // computed.  The traced kernels are separate instantiations, so the untraced
 // ones carry none of this.
 __device__ __forceinline__ unsigned long long wall_clock() { return __builtin_amdgcn_s_memrealtime(); }
+__device__ __forceinline__ unsigned long long core_clock() { return __builtin_amdgcn_s_memtime(); }
 
-__device__ __forceinline__ void trace_record(const Params& p, unsigned long long t0, unsigned long long t_first,
-                                             int tiles, int worked) {
+__device__ __forceinline__ void trace_record(const Params& p, unsigned long long t0, unsigned long long c0,
+                                             unsigned long long t_first, int tiles, int worked) {
   if (threadIdx.x != 0) return;
   uint32_t xr, hw;
   asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xr));
@@ -792,6 +793,7 @@ __device__ __forceinline__ void trace_record(const Params& p, unsigned long long
   r.start = t0;
   r.first_tile = t_first;
   r.end = wall_clock();
+  r.cycles = core_clock() - c0;
   r.xcc = xr & 0xFu;
   r.hw_id = hw;
   r.tiles = (uint32_t)tiles;
@@ -805,6 +807,7 @@ gemm_bf16_persistent(Params p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[TE == 0 ? RING_BYTES : 2 * (2 * TE) * LDP * 2];
   int* const box = reinterpret_cast<int*>(lds);  // tile broadcast, used between tiles only
   const unsigned long long t_start = TRACE ? wall_clock() : 0ull;
+  const unsigned long long c_start = TRACE ? core_clock() : 0ull;
 
   // Static aware assignment: workgroup b belongs to XCD b mod n and is that
   // XCD's (b / n)-th persistent worker (the hardware deals workgroups to XCDs
@@ -844,7 +847,7 @@ gemm_bf16_persistent(Params p) {
     const int x = (int)blockIdx.x % p.n_xccs, r = (int)blockIdx.x / p.n_xccs;
     const int s_x = p.slots[x];
     if (r >= s_x) {  // the whole workgroup, before any barrier
-      if constexpr (TRACE) trace_record(p, t_start, 0ull, 0, 0);
+      if constexpr (TRACE) trace_record(p, t_start, c_start, 0ull, 0, 0);
       return;
     }
     nt.i_next = p.off[x] + r;
@@ -890,7 +893,7 @@ gemm_bf16_persistent(Params p) {
     }
     tile = read_box(box);
   }
-  if constexpr (TRACE) trace_record(p, t_start, t_first, n_tiles_done, n_tiles_done > 0);
+  if constexpr (TRACE) trace_record(p, t_start, c_start, t_first, n_tiles_done, n_tiles_done > 0);
   if (dyn && threadIdx.x == 0) {
     // the last workgroup to leave resets the counters for the next launch
     __threadfence();

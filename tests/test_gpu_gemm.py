@@ -328,9 +328,28 @@ def test_gemm_trace_records(dev):
     assert all(t["tiles"][t["worked"] == 1] >= 1) and int(t["worked"].sum()) == 256
     for x in range(8):
         assert int(t["tiles"][t["xcc"] == x].sum()) == 32, x
+    khz = asym.device_query(0)["wall_clock_khz"]
+    mhz = t["cycles"].astype(np.float64) * khz / np.maximum(1, (t["end"] - t["start"]).astype(np.int64)) / 1e3
+    assert np.all((mhz > 300) & (mhz < 2600)), (mhz.min(), mhz.max())  # the shader clock's range
     C.zero_()
     t = asym.gemm_trace(Ad, Bd, C, topo=topo, xcd_mask=0x0F)
     assert torch.equal(C, ref)
     assert int(t["tiles"].sum()) == 256 and set(t["xcc"][t["worked"] == 1].tolist()) <= {0, 1, 2, 3}
-    span = (int(t["end"].max()) - int(t["start"].min())) / (asym.device_query(0)["wall_clock_khz"] / 1e3)
+    span = (int(t["end"].max()) - int(t["start"].min())) / (khz / 1e3)
     print(f"traced 4096x4096x1024 on XCDs 0-3: {span:.1f} us from the first start to the last end")
+    ts = asym.gemm_trace(Ad, Bd, C, topo=topo, launches=3)
+    assert len(ts) == 3 and torch.equal(C, ref)
+    for a, b in zip(ts, ts[1:]):  # queued on one stream: a launch starts after the previous one ends
+        assert int(b["start"].min()) >= int(a["end"].max())
+    # the small-M kernel has no traced form: a 32-row product is traced on the
+    # persistent kernel and gives that kernel's bits
+    C32 = torch.empty((32, 4096), dtype=torch.bfloat16, device=dev)
+    t = asym.gemm_trace(Ad[:32], Bd, C32, topo=topo)
+    prev = asym.set_small_m(False)
+    try:
+        ref32 = asym.gemm(Ad[:32], Bd, topo=topo)
+    finally:
+        asym.set_small_m(prev)
+    torch.cuda.synchronize()
+    assert torch.equal(C32, ref32) and int(t["tiles"].sum()) == t["plan"]["tiles_m"] * t["plan"]["tiles_n"]
+    assert t["plan"]["small_m"] == 0

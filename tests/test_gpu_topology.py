@@ -223,6 +223,17 @@ def test_corun_prefill_decode(dev, topo):
                       asym.gemm_task(da, db, cd, 20, "aware", mask=dm, xcd_mask=0xC0)], topo)
     print("xcd-aligned", res)
     assert torch.equal(cp, ref_p) and torch.equal(cd, ref_d)
+    # with an untimed warm-up of every task first (the timed parts start
+    # together once all warm-ups are done): same bits, the timed iterations only
+    cp.zero_()
+    cd.zero_()
+    res = asym.corun([asym.gemm_task(pa, pb, cp, 3, "aware", mask=prefill, warm_iters=30),
+                      asym.gemm_task(da, db, cd, 20, "aware", mask=decode, warm_iters=200)], topo)
+    print("striped after warm-up", res)
+    assert torch.equal(cp, ref_p) and torch.equal(cd, ref_d)
+    assert res[0]["iters_done"] == 3 and res[1]["iters_done"] == 20 and res[0]["ms_total"] < 50
+    with pytest.raises(asym.AsymError):
+        asym.corun([asym.gemm_task(pa, pb, cp, 3, "aware", mask=prefill, warm_iters=-1)], topo)
 
 
 def test_corun_gemm_with_read_tenant(dev, topo):
