@@ -645,6 +645,53 @@ def spread_study(topo, dev, n_masks: int, iters: int, halves, tenant: str = "cop
     return summ
 
 
+def balanced_study(topo, dev, iters: int = 20, repeats: int = 5, warm: int = 10):
+    """Locality without balance: GEMM 4096^3 (uniform[-1,1], seed 4) on the
+    striped 128-CU and 192-CU sets (16 and 24 CUs of every XCD, so every
+    mapping gives each XCD the same work), alone and beside the 64 MiB
+    streaming copy on the complementary CUs; each mapping `repeats` times,
+    median kept, every co-run after `warm` times its launches (and a matching
+    share of copy passes) of untimed warm-up.  Any gap between the mappings is
+    what L2 locality is worth under the tenant's memory traffic."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    A, B = workloads.make_inputs(workloads.COLOC)
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.empty((A.shape[0], B.shape[0]), dtype=torch.bfloat16, device=dev)
+    src = workloads.copy_source(workloads.COPY_BYTES // 2).to(dev)
+    dst = torch.empty_like(src)
+    med = lambda v: sorted(v)[len(v) // 2]
+    out = {}
+    for n in (128, 192):
+        cus = topo.cuset(n, asym.CUSET_STRIPED)
+        comp = [b for b in range(256) if b not in set(cus)]
+        g_ms = max(asym.corun([asym.gemm_task(Ad, Bd, C, iters, mp, mask=cus)], topo)[0]["ms_total"]
+                   for mp in MAPPINGS)
+        c_ms = asym.corun([asym.copy_task(dst, src, 10, mask=comp)], topo)[0]["ms_per_iter"]
+        passes = max(10, int(2.0 * g_ms / max(c_ms, 1e-3)) + 1)
+        row = {"cus_per_xcd": topo.cuset_counts(cus), "copy_passes": passes}
+        for mp in MAPPINGS:
+            alone = [asym.corun([asym.gemm_task(Ad, Bd, C, iters, mp, mask=cus, warm_iters=warm * iters)],
+                                topo)[0]["tflops"] for _ in range(repeats)]
+            co, rate, covered = [], [], 0
+            for _ in range(repeats):
+                r = asym.corun([asym.gemm_task(Ad, Bd, C, iters, mp, mask=cus, warm_iters=warm * iters),
+                                asym.copy_task(dst, src, passes, mask=comp, warm_passes=warm * passes // 2)], topo)
+                co.append(r[0]["tflops"])
+                rate.append(r[1]["gbps"])
+                covered += r[1]["ms_total"] >= r[0]["ms_total"]
+            row[mp] = {"alone_tflops": round(med(alone), 2), "beside_copy_tflops": round(med(co), 2),
+                       "copy_GBps": round(med(rate), 1), "copy_outlasted_gemm": f"{covered}/{repeats}",
+                       "within_max_min": round(max(co) / min(co), 4)}
+        for mp in ("oblivious_grouped", "oblivious_rowmajor"):
+            row[f"aware_vs_{mp}"] = {k: round(row["aware"][k] / row[mp][k], 4)
+                                     for k in ("alone_tflops", "beside_copy_tflops")}
+        out[f"striped_{n}"] = row
+    return out
+
+
 def queued(fns: dict, launches: int, rounds: int, stream) -> dict:
     """Mean per-launch ms of each fn for kernels too short to time one launch
     at a time: each round first parks the stream on a spin kernel (about
@@ -1065,7 +1112,7 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,pd_trace,spread,grouped,numa,attention,mla,parity",
+    ap.add_argument("--studies", default="compare,llm,pd,pd_trace,spread,balanced,grouped,numa,attention,mla,parity",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
@@ -1113,7 +1160,7 @@ def main() -> int:
         return 0
     studies = set() if args.mapping_only or args.studies == "none" else set(args.studies.split(","))
     if args.probe == "identity":
-        studies -= {"pd", "pd_trace", "spread"}  # CU-masked sets need the mask map
+        studies -= {"pd", "pd_trace", "spread", "balanced"}  # CU-masked sets need the mask map
     p = workloads.SQUARE_8192
     A, B = workloads.make_inputs(p)
     Ad, Bd = A.to(dev), B.to(dev)
@@ -1198,6 +1245,8 @@ def main() -> int:
         for tenant in args.spread_tenants.split(","):
             key = "cu_set_spread" if tenant == "copy" else f"cu_set_spread_{tenant}_tenant"
             line[key] = spread_study(topo, dev, args.spread_masks, 20, halves, tenant, args.spread_repeats)
+    if "balanced" in studies:
+        line["balanced_sets"] = balanced_study(topo, dev)
     if "grouped" in studies:
         line["grouped_gemm"] = grouped_study(dev, stream, range(1, 6), 8, 5)
     if "attention" in studies:
