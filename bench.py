@@ -852,6 +852,69 @@ def numa_bw_study(dev, hash_res, rounds: int = 3, gib: int = 16):
             "low_parallelism_GBps_first_2GiB": lat}
 
 
+def placed_attention_study(dev, hres, topo, stream, launches: int = 20, rounds: int = 5):
+    """Decode attention (GQA 32 / 8 heads, head dim 128) over a paged cache
+    whose pages are placed by home (Appendix E): each task's pages homed on
+    the die of the XCD that owns the task (local), on the other die (remote),
+    or in address order (in order: pages alternate homes as the partition hash
+    deals them); the dense call beside them.  B = 1 and 4, S = 8192 and 32768,
+    on the whole chip and on one die's four XCDs (whole-XCD restriction).
+    Pages of 8 KiB are the chunks the home map measures."""
+    import numpy as np
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    grp = list(hres["group_of_xcd"])
+    g0 = sum(1 << x for x, g in enumerate(grp) if g == 0)
+    page = asym.PAGE_TOKENS * 128 * 2
+    out = {}
+    for B, S in ((1, 8192), (1, 32768), (4, 8192)):
+        p = workloads.AttnProblem(f"placed_B{B}_S{S}", B, 32, 8, S, seed=12)
+        q, k, v = workloads.make_attn_inputs_on(p, dev)
+        pph = -(-S // asym.PAGE_TOKENS)
+        n = B * 8 * pph
+        P = -(-(2 * n + 2048) // 256) * 256         # pool pages per pool, a whole number of 2 MiB pages
+        raw = torch.empty(2 * P * page + (2 << 20), dtype=torch.uint8, device=dev)
+        shift = (-raw.data_ptr()) % (2 << 20)
+        base = raw.data_ptr() + shift
+        info, homes = asym.home_map(base, 2 * P * page, hres["hash_mask"], 13, group_of_xcd=grp, passes=2,
+                                    n_verify=512, seed=7)
+        pools = raw[shift: shift + 2 * P * page].view(torch.bfloat16).view(2, P, asym.PAGE_TOKENS, 128)
+        row = {"kv_MB": round(p.kv_bytes / 1e6, 1), "pool_pages": P,
+               "map_agree": f"{info['verify_agree']}/{info['verify_classified']}"}
+        for where, xm in (("chip", 0), ("one_die", g0)):
+            plan = asym.attn_decode_plan(B, 32, 8, S, topo=topo, xcd_mask=xm)
+            tabs = {}
+            for name, pol in (("in_order", asym.PAGES_IN_ORDER), ("local", asym.PAGES_LOCAL),
+                              ("remote", asym.PAGES_REMOTE)):
+                kt = asym.attn_pages_place(plan, B, 8, S, P, pol, homes[:P], grp)
+                vt = asym.attn_pages_place(plan, B, 8, S, P, pol, homes[P:], grp)
+                tabs[name] = (torch.as_tensor(kt).to(dev), torch.as_tensor(vt).to(dev))
+            fns = {"dense": lambda: asym.attn_decode(q, k, v, topo=topo, xcd_mask=xm)}
+            outs = {}
+            for name, (kt, vt) in tabs.items():
+                pools[0].copy_(workloads.page_pool(k, kt, P))
+                pools[1].copy_(workloads.page_pool(v, vt, P))
+                o = asym.attn_decode_paged(q, pools[0], pools[1], kt, vt, S, topo=topo, xcd_mask=xm)
+                fns_one = {name: lambda kt=kt, vt=vt: asym.attn_decode_paged(q, pools[0], pools[1], kt, vt, S,
+                                                                              topo=topo, xcd_mask=xm)}
+                outs[name] = queued(fns_one, launches, rounds, stream)[name]
+                row.setdefault("bitwise_equal_to_dense", {})[f"{where}_{name}"] = bool(
+                    torch.equal(o, asym.attn_decode(q, k, v, topo=topo, xcd_mask=xm)))
+            outs["dense"] = queued(fns, launches, rounds, stream)["dense"]
+            r = {k_: {"us": round(1e3 * ms, 2), "GBps": round(p.kv_bytes / (ms * 1e-3) / 1e9, 1)}
+                 for k_, ms in outs.items()}
+            r["local_over_remote"] = round(outs["remote"] / outs["local"], 3)
+            r["local_over_in_order"] = round(outs["in_order"] / outs["local"], 3)
+            r["local_over_dense"] = round(outs["dense"] / outs["local"], 3)
+            row[where] = r
+        out[f"B{B}_S{S}"] = row
+        del raw, pools, q, k, v
+        torch.cuda.empty_cache()
+    return out
+
+
 def attention_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 3):
     """Decode attention (32 query heads, head dimension 128; grouped-query with
     8 key/value heads and multi-head with 32) over batch and KV length: the
@@ -1112,7 +1175,7 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,pd_trace,spread,balanced,grouped,numa,attention,mla,parity",
+    ap.add_argument("--studies", default="compare,llm,pd,pd_trace,spread,balanced,grouped,numa,placed,attention,mla,parity",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
@@ -1253,11 +1316,13 @@ def main() -> int:
         line["decode_attention"] = attention_study(topo, dev, stream, args.probe != "identity")
     if "mla" in studies:
         line["mla_decode"] = mla_study(topo, dev, stream, args.probe != "identity")
-    if "numa" in studies:
+    if "numa" in studies or "placed" in studies:
         summ, hres = interleave_summary(dev)
         line["partition_hash"] = summ
-        if hres["n_groups"] == 2:
+        if hres["n_groups"] == 2 and "numa" in studies:
             line["numa_read_bw"] = numa_bw_study(dev, hres)
+        if hres["n_groups"] == 2 and "placed" in studies:
+            line["placed_attention"] = placed_attention_study(dev, hres, topo, stream)
     if args.no_cpu:
         line["cpu_baseline"] = None
     else:

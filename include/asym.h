@@ -756,6 +756,44 @@ int asym_attn_decode_plan(const asym_topology* topo, int B, int H_q, int H_kv, i
                           int split_tokens, int mapping, uint32_t xcd_mask, void* stream,
                           asym_attn_plan_info* out);
 
+/* Paged form of asym_attn_decode_bf16 (Appendix E: memory remapping, here of
+ * the key/value cache).  K and V live in caller-owned pools of pool_pages
+ * pages of 8 KiB each, a page holding 32 consecutive tokens of one head
+ * ([pool_pages][32][128] bf16; pool_pages * 8 KiB at most 2 GiB); k_pages and
+ * v_pages (device int32 [B][H_kv][ceil(S_k / 32)]) give the pool page of each
+ * (request, head, 32-token page), the tokens past S_k in a head's last page
+ * being ignored.  Two table entries may name the same page; an entry outside
+ * [0, pool_pages) reads zeros or other bytes of the pool, never memory outside
+ * it (the pools are read through buffer descriptors sized to them).  Splits are
+ * at most 2048 tokens (0 = automatic).  Everything else, and the bits of O
+ * and lse, as asym_attn_decode_bf16 on the dense K and V the tables describe:
+ * the tables only change where each page's bytes are.
+ * Errors: those of asym_attn_decode_bf16. */
+int asym_attn_decode_paged_bf16(const asym_topology* topo, int B, int H_q, int H_kv, int S_k,
+                                const void* q, const void* k_pool, const void* v_pool,
+                                size_t pool_pages, const int32_t* k_pages, const int32_t* v_pages,
+                                void* o, float* lse, float scale, int split_tokens, int mapping,
+                                uint32_t xcd_mask, void* stream);
+
+/* Page placement for asym_attn_decode_paged_bf16 (Appendix E's placement by
+ * home: each task's pages in memory homed on the die of the XCD that reads
+ * them).  From a plan of the AWARE mapping (asym_attn_decode_plan: task t
+ * belongs to the XCD whose share, in XCD order, holds it), pool_home
+ * (pool_pages entries, the home group 0 / 1 of each pool page as
+ * asym_home_map gives it, -1 unknown; nullable for IN_ORDER) and
+ * group_of_xcd (n_xcds entries), fills pages (host int32
+ * [B][H_kv][ceil(S_k / 32)]):
+ *   ASYM_PAGES_IN_ORDER: page i of the table is pool page i (the dense layout);
+ *   ASYM_PAGES_LOCAL: the next unused pool page homed on the group of the XCD
+ *     that owns the task reading the page (its first token's task);
+ *   ASYM_PAGES_REMOTE: the same on the other group (the worst placement).
+ * Every table entry is a distinct pool page.  Host only.
+ * Errors: ASYM_EINVAL (inconsistent plan, too few pool pages of a group). */
+enum asym_page_policy { ASYM_PAGES_IN_ORDER = 0, ASYM_PAGES_LOCAL = 1, ASYM_PAGES_REMOTE = 2 };
+int asym_attn_pages_place(const asym_attn_plan_info* plan, int B, int H_kv, int S_k,
+                          const int8_t* pool_home, size_t pool_pages, const int* group_of_xcd,
+                          int policy, int32_t* pages);
+
 /* ---- multi-head latent attention, decode (Section 7.1; Appendix F) ---- */
 /* One query token per request against a compressed latent cache shared by
  * all query heads (the decode form of multi-head latent attention, with the

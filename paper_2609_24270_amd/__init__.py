@@ -45,7 +45,7 @@ EXPORTS = (
     "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_bf16_noalloc", "asym_gemm_noalloc_limits",
     "asym_gemm_bf16_trace",
     "asym_gemm_plan", "asym_gemm_set_small_m",
-    "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_mla_decode_bf16", "asym_mla_decode_plan",
+    "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_attn_decode_paged_bf16", "asym_attn_pages_place", "asym_mla_decode_bf16", "asym_mla_decode_plan",
     "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
@@ -268,6 +268,10 @@ def load_library(path: str = LIB_PATH):
         "asym_gemm_noalloc_limits": (i, [ctypes.POINTER(ctypes.c_size_t), ip, ctypes.POINTER(ctypes.c_size_t)]),
         "asym_attn_decode_bf16": (i, [topo_p, i, i, i, i, i, vp, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
         "asym_attn_decode_plan": (i, [topo_p, i, i, i, i, i, i, i, u32, vp, ctypes.POINTER(AttnPlanInfo)]),
+        "asym_attn_decode_paged_bf16": (i, [topo_p, i, i, i, i, vp, vp, vp, ctypes.c_size_t, vp, vp, vp, vp,
+                                            ctypes.c_float, i, i, u32, vp]),
+        "asym_attn_pages_place": (i, [ctypes.POINTER(AttnPlanInfo), i, i, i, ctypes.POINTER(ctypes.c_int8),
+                                      ctypes.c_size_t, ip, i, ctypes.POINTER(ctypes.c_int32)]),
         "asym_mla_decode_bf16": (i, [topo_p, i, i, i, vp, vp, vp, vp, ctypes.c_float, i, i, u32, vp]),
         "asym_mla_decode_plan": (i, [topo_p, i, i, i, i, i, u32, vp, ctypes.POINTER(MlaPlanInfo)]),
         "asym_copy_bf16": (i, [topo_p, vp, vp, ctypes.c_size_t, i, vp, u32, vp]),
@@ -854,6 +858,81 @@ def attn_decode(q, k, v, o=None, lse=None, scale: Optional[float] = None, split_
         ctypes.c_void_p(lse.data_ptr() if lse is not None else None), sc, split_tokens, mp, xcd_mask,
         _stream_ptr(stream)))
     return o
+
+
+PAGES_IN_ORDER, PAGES_LOCAL, PAGES_REMOTE = 0, 1, 2
+PAGE_TOKENS = 32  # tokens of one head per 8 KiB page of the paged cache
+
+
+def attn_decode_paged(q, k_pool, v_pool, k_pages, v_pages, S: int, o=None, lse=None, scale: Optional[float] = None,
+                      split_tokens: int = 0, mapping="aware", topo: Optional[Topology] = None, xcd_mask: int = 0,
+                      stream=None):
+    """Decode attention over a paged cache: q [B, H_q, 128] bf16; k_pool and
+    v_pool bf16 [pool_pages, 32, 128]; k_pages and v_pages int32 CUDA tensors
+    [B, H_kv, ceil(S / 32)] naming each (request, head, page)'s pool page.
+    Returns O [B, H_q, 128] bf16 (and fills lse when given), as attn_decode
+    on the dense K and V the tables describe."""
+    import math
+
+    import torch
+    if q.dtype != torch.bfloat16 or k_pool.dtype != torch.bfloat16 or v_pool.dtype != torch.bfloat16:
+        raise TypeError("q and the pools must be bfloat16")
+    if k_pages.dtype != torch.int32 or v_pages.dtype != torch.int32:
+        raise TypeError("page tables must be int32")
+    if not all(t.is_cuda and t.is_contiguous() for t in (q, k_pool, v_pool, k_pages, v_pages)):
+        raise ValueError("q, the pools and the tables must be contiguous GPU tensors")
+    if q.dim() != 3 or q.shape[2] != 128:
+        raise ValueError("q must be [B, H_q, 128]")
+    if k_pool.shape != v_pool.shape or k_pool.dim() != 3 or tuple(k_pool.shape[1:]) != (PAGE_TOKENS, 128):
+        raise ValueError("pools must be [pool_pages, 32, 128]")
+    B, Hq, _ = q.shape
+    if k_pages.dim() != 3 or k_pages.shape != v_pages.shape or k_pages.shape[0] != B \
+            or k_pages.shape[2] != (S + PAGE_TOKENS - 1) // PAGE_TOKENS:
+        raise ValueError("page tables must be [B, H_kv, ceil(S / 32)]")
+    Hkv = k_pages.shape[1]
+    if o is None:
+        o = torch.empty((B, Hq, 128), dtype=torch.bfloat16, device=q.device)
+    if o.dtype != torch.bfloat16 or tuple(o.shape) != (B, Hq, 128) or not o.is_contiguous():
+        raise ValueError("o must be a contiguous bf16 [B, H_q, 128] tensor")
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hq) or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous fp32 [B, H_q] tensor")
+    sc = 1.0 / math.sqrt(128) if scale is None else float(scale)
+    mp = MAPPINGS[mapping] if isinstance(mapping, str) else int(mapping)
+    _check(load_library().asym_attn_decode_paged_bf16(
+        topo.handle if topo else None, B, Hq, Hkv, S, ctypes.c_void_p(q.data_ptr()),
+        ctypes.c_void_p(k_pool.data_ptr()), ctypes.c_void_p(v_pool.data_ptr()), k_pool.shape[0],
+        ctypes.c_void_p(k_pages.data_ptr()), ctypes.c_void_p(v_pages.data_ptr()), ctypes.c_void_p(o.data_ptr()),
+        ctypes.c_void_p(lse.data_ptr() if lse is not None else None), sc, split_tokens, mp, xcd_mask,
+        _stream_ptr(stream)))
+    return o
+
+
+def attn_pages_place(plan: dict, B: int, Hkv: int, S: int, pool_pages: int, policy: int = PAGES_IN_ORDER,
+                     pool_home=None, group_of_xcd=None):
+    """Page table (numpy int32 [B, H_kv, ceil(S / 32)]) for attn_decode_paged
+    from an aware plan (attn_decode_plan) and the pool's page homes."""
+    import numpy as np
+    info = AttnPlanInfo()
+    for k, _ in AttnPlanInfo._fields_:
+        if k == "tasks_per_xcd":
+            for x, v in enumerate(plan["tasks_per_xcd"]):
+                info.tasks_per_xcd[x] = v
+        else:
+            setattr(info, k, plan[k])
+    pph = (S + PAGE_TOKENS - 1) // PAGE_TOKENS
+    out = np.zeros((B, Hkv, pph), dtype=np.int32)
+    home = None
+    if pool_home is not None:
+        home = np.ascontiguousarray(pool_home, dtype=np.int8)
+        if home.size < pool_pages:
+            raise ValueError("pool_home must have pool_pages entries")
+    grp = None
+    if group_of_xcd is not None:
+        grp = (ctypes.c_int * len(group_of_xcd))(*group_of_xcd)
+    _check(load_library().asym_attn_pages_place(
+        ctypes.byref(info), B, Hkv, S, home.ctypes.data_as(ctypes.POINTER(ctypes.c_int8)) if home is not None else None,
+        pool_pages, grp, policy, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
+    return out
 
 
 def attn_decode_plan(B: int, Hq: int, Hkv: int, S: int, D: int = 128, split_tokens: int = 0,

@@ -30,6 +30,17 @@
 // from a counter, then of the other shares, until none are left (which XCD a
 // block index is dealt to is not fixed: the starting XCD differs between
 // streams, so claims, not block indices, decide).
+//
+// Paged keys and values (the placed form, Appendix E's memory remapping).
+// The caller's K and V live in pools of 8 KiB pages (32 tokens of one head),
+// and an int32 table per pool gives the pool page of every (request, head,
+// 32-token page).  With the aware mapping each task's share, and so the XCD
+// that reads it, is known before launch; the table lets the caller put a
+// task's pages in memory homed on that XCD's die.  A task loads its split's
+// page numbers once (one per lane) and reads each block's page with a lane
+// read; a 16-token block never crosses a page.  The pools are read through
+// buffer descriptors sized to them, so a table entry past the pool reads
+// zeros or other pool bytes, never memory outside it.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -57,7 +68,13 @@ struct AttnParams {
   uint32_t allow;        // aware: XCDs whose workgroups may work (the others leave)
   int B, Hq, Hkv, S, split, n_splits, tasks, n_x;
   float scale;
+  int pages_per_head;    // paged form: ceil(S / 32)
+  const int* k_page;     // paged form: pool page of (request, head, page) [B][Hkv][pages_per_head]
+  const int* v_page;
+  uint32_t pool_bytes;   // each pool's size (at most 2^31, so the out-of-range offset reads zero)
 };
+
+constexpr int kPageTokens = 32;  // 8 KiB of one head's keys (or values)
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t at_rsrc(const void* base, uint32_t bytes) {
   const unsigned long long a = (unsigned long long)base;
@@ -70,8 +87,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t at_rsrc(const void* base, uint
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// One task on one wave.  G: query heads per key/value head (1 .. 16).
-template <int G>
+// One task on one wave.  G: query heads per key/value head (1 .. 16);
+// PAGED: K and V through the page tables.
+template <int G, bool PAGED>
 __device__ void attn_task(const AttnParams& p, int task, float* __restrict__ sp) {
   const int lane = threadIdx.x & 63;
   const int split = task % p.n_splits;
@@ -83,9 +101,30 @@ __device__ void attn_task(const AttnParams& p, int task, float* __restrict__ sp)
 
   // q rows of the G heads; rows past G read as zero
   const __amdgpu_buffer_rsrc_t rq = at_rsrc(p.q + ((size_t)b * p.Hq + (size_t)hk * G) * AD, G * AD * 2u);
-  const __amdgpu_buffer_rsrc_t rk = at_rsrc(p.k + (size_t)bh * p.S * AD, (uint32_t)p.S * AD * 2u);
-  const __amdgpu_buffer_rsrc_t rv = at_rsrc(p.v + (size_t)bh * p.S * AD, (uint32_t)p.S * AD * 2u);
+  const __amdgpu_buffer_rsrc_t rk =
+      PAGED ? at_rsrc(p.k, p.pool_bytes) : at_rsrc(p.k + (size_t)bh * p.S * AD, (uint32_t)p.S * AD * 2u);
+  const __amdgpu_buffer_rsrc_t rv =
+      PAGED ? at_rsrc(p.v, p.pool_bytes) : at_rsrc(p.v + (size_t)bh * p.S * AD, (uint32_t)p.S * AD * 2u);
   const int lr = lane & 15, lq = lane >> 4;
+  // paged: lane j holds the pool pages of the split's j-th page (at most 64)
+  const int p0 = t0 / kPageTokens;
+  int kpg = 0, vpg = 0;
+  if constexpr (PAGED) {
+    const int npg = (t1 - 1) / kPageTokens - p0 + 1;
+    if (lane < npg) {
+      const size_t e = (size_t)bh * p.pages_per_head + p0 + lane;
+      kpg = p.k_page[e];
+      vpg = p.v_page[e];
+    }
+  }
+  // byte offset of block blk's first row in its buffer
+  auto blk_off = [&](int blk, int pg) -> uint32_t {
+    const int bt = t0 + blk * 16;
+    if constexpr (PAGED)
+      return (uint32_t)__builtin_amdgcn_readlane(pg, bt / kPageTokens - p0) * (kPageTokens * AD * 2u) +
+             (uint32_t)(bt % kPageTokens) * (AD * 2u);
+    return (uint32_t)bt * (AD * 2u);
+  };
   bf16x8 qf[4];
 #pragma unroll
   for (int c = 0; c < 4; ++c)
@@ -103,17 +142,18 @@ __device__ void attn_task(const AttnParams& p, int task, float* __restrict__ sp)
 
   auto load_k = [&](int blk, bf16x8 (&kf)[4]) {
     const int tok = t0 + blk * 16 + lr;
-    const uint32_t base = tok < t1 ? (uint32_t)(tok * AD + lq * 8) * 2u : kAtOOB;
+    const uint32_t base = tok < t1 ? blk_off(blk, kpg) + (uint32_t)(lr * AD + lq * 8) * 2u : kAtOOB;
 #pragma unroll
     for (int c = 0; c < 4; ++c)
       kf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, base, 64 * c, 0));
   };
   auto load_v = [&](int blk, v4u (&vf)[4]) {
+    const uint32_t r0 = blk_off(blk, vpg);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int tok = t0 + blk * 16 + 4 * i + lq;
-      vf[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, tok < t1 ? (uint32_t)(tok * AD + lr * 8) * 2u : kAtOOB,
-                                                    0, 0);
+      vf[i] = __builtin_amdgcn_raw_buffer_load_b128(
+          rv, tok < t1 ? r0 + (uint32_t)((4 * i + lq) * AD + lr * 8) * 2u : kAtOOB, 0, 0);
     }
   };
 
@@ -213,14 +253,14 @@ __device__ void attn_task(const AttnParams& p, int task, float* __restrict__ sp)
   }
 }
 
-template <int G>
+template <int G, bool PAGED>
 __global__ void __launch_bounds__(64 * AT_WAVES) attn_decode_split(AttnParams p) {
   __shared__ float sp_all[AT_WAVES][256 + 16];
   __shared__ int box[2];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (!p.quota_off) {
     const int task = blockIdx.x * AT_WAVES + wave;
-    if (task < p.tasks) attn_task<G>(p, task, sp_all[wave]);
+    if (task < p.tasks) attn_task<G, PAGED>(p, task, sp_all[wave]);
     return;
   }
   uint32_t xr;
@@ -266,7 +306,7 @@ __global__ void __launch_bounds__(64 * AT_WAVES) attn_decode_split(AttnParams p)
     const int base = box[0], end = box[1];
     __syncthreads();
     if (base < 0) break;
-    if (base + wave < end) attn_task<G>(p, base + wave, sp_all[wave]);
+    if (base + wave < end) attn_task<G, PAGED>(p, base + wave, sp_all[wave]);
   }
 }
 
@@ -323,18 +363,33 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
   p.tasks = a.B * a.Hkv * a.n_splits;
   p.n_x = a.n_x;
   p.scale = a.scale;
+  p.k_page = a.k_page;
+  p.v_page = a.v_page;
+  p.pages_per_head = (a.S + kPageTokens - 1) / kPageTokens;
+  p.pool_bytes = a.pool_bytes;
   const int G = a.Hq / a.Hkv;
   const dim3 grid((unsigned)a.grid), block(64 * AT_WAVES);
   if (a.d_quota_off && (!a.d_claim || a.n_x > 64))
     return fail(ASYM_EINVAL, "attention: aware launch without claim counters");
+  const bool paged = a.k_page != nullptr;
+  if (paged && (!a.v_page || a.pool_bytes == 0 || a.pool_bytes > (1u << 31) || a.split > 64 * kPageTokens))
+    return fail(ASYM_EINVAL, "attention: a paged launch needs both tables, pools of at most 2 GiB, splits of <= 2048");
+#define ASYM_ATTN_CASE(g)                                                      \
+  case g:                                                                      \
+    if (paged)                                                                 \
+      hipLaunchKernelGGL((attn_decode_split<g, true>), grid, block, 0, s, p);  \
+    else                                                                       \
+      hipLaunchKernelGGL((attn_decode_split<g, false>), grid, block, 0, s, p); \
+    break;
   switch (G) {
-    case 1: hipLaunchKernelGGL(attn_decode_split<1>, grid, block, 0, s, p); break;
-    case 2: hipLaunchKernelGGL(attn_decode_split<2>, grid, block, 0, s, p); break;
-    case 4: hipLaunchKernelGGL(attn_decode_split<4>, grid, block, 0, s, p); break;
-    case 8: hipLaunchKernelGGL(attn_decode_split<8>, grid, block, 0, s, p); break;
-    case 16: hipLaunchKernelGGL(attn_decode_split<16>, grid, block, 0, s, p); break;
+    ASYM_ATTN_CASE(1)
+    ASYM_ATTN_CASE(2)
+    ASYM_ATTN_CASE(4)
+    ASYM_ATTN_CASE(8)
+    ASYM_ATTN_CASE(16)
     default: return fail(ASYM_EUNSUPPORTED, "attention: query heads per key/value head must be 1, 2, 4, 8 or 16");
   }
+#undef ASYM_ATTN_CASE
   ASYM_HIP(hipGetLastError());
   const int rows = a.B * a.Hq;
   hipLaunchKernelGGL(attn_decode_merge, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a.part_o, a.part_ml,
@@ -345,6 +400,8 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
 }
 
 int attn_tasks_per_workgroup() { return AT_WAVES; }
+
+int attn_page_tokens() { return kPageTokens; }
 
 int attn_claim_ints() { return ASYM_MAX_XCDS * kClaimStride; }
 

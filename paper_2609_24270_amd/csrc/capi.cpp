@@ -951,8 +951,20 @@ static int attn_partials(Workspace* ws, size_t bytes_needed, hipStream_t stream)
 
 int attn_decode(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int D, const void* q, const void* k,
                 const void* v, void* o, float* lse, float scale, int split_in, int mapping, uint32_t xcd_mask,
-                hipStream_t stream) {
+                hipStream_t stream, const int* k_pages = nullptr, const int* v_pages = nullptr,
+                size_t pool_pages = 0) {
   if (!q || !k || !v || !o) return fail(ASYM_EINVAL, "attention: null pointer");
+  const bool paged = k_pages || v_pages;
+  if (paged) {
+    if (!k_pages || !v_pages) return fail(ASYM_EINVAL, "paged attention: null page table");
+    if (((uintptr_t)k_pages & 3u) || ((uintptr_t)v_pages & 3u))
+      return fail(ASYM_EINVAL, "paged attention: page tables must be 4-byte aligned");
+    const size_t page_bytes = (size_t)attn_page_tokens() * 128 * 2;
+    if (pool_pages < 1 || pool_pages > ((size_t)1 << 31) / page_bytes)
+      return fail(ASYM_EINVAL, "paged attention: pool_pages must be in [1, 2 GiB / 8 KiB]");
+    if (split_in > 64 * attn_page_tokens())
+      return fail(ASYM_EINVAL, "paged attention: split_tokens must be at most 2048");
+  }
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || ((uintptr_t)o & 3u) || ((uintptr_t)lse & 3u))
     return fail(ASYM_EINVAL, "attention: q, K, V must be 16-byte aligned, O and lse 4-byte aligned");
   if (!std::isfinite(scale)) return fail(ASYM_EINVAL, "attention: scale must be finite");
@@ -984,6 +996,11 @@ int attn_decode(const asym_topology* topo_in, int B, int Hq, int Hkv, int S, int
   a.split = P.split; a.n_splits = P.n_splits;
   a.n_x = n_x; a.grid = P.grid;
   a.scale = scale;
+  if (paged) {
+    a.k_page = k_pages;
+    a.v_page = v_pages;
+    a.pool_bytes = (uint32_t)(pool_pages * (size_t)attn_page_tokens() * 128 * 2);
+  }
   return launch_attn_decode(a, stream);
 }
 
@@ -1339,6 +1356,16 @@ extern "C" int asym_attn_decode_bf16(const asym_topology* topo, int B, int H_q, 
                                      void* stream) {
   return asym::attn_decode(topo, B, H_q, H_kv, S_k, D, q, k, v, o, lse, scale, split_tokens, mapping, xcd_mask,
                            static_cast<hipStream_t>(stream));
+}
+
+extern "C" int asym_attn_decode_paged_bf16(const asym_topology* topo, int B, int H_q, int H_kv, int S_k,
+                                           const void* q, const void* k_pool, const void* v_pool, size_t pool_pages,
+                                           const int32_t* k_pages, const int32_t* v_pages, void* o, float* lse,
+                                           float scale, int split_tokens, int mapping, uint32_t xcd_mask,
+                                           void* stream) {
+  if (!k_pages || !v_pages) return asym::fail(ASYM_EINVAL, "paged attention: null page table");
+  return asym::attn_decode(topo, B, H_q, H_kv, S_k, 128, q, k_pool, v_pool, o, lse, scale, split_tokens, mapping,
+                           xcd_mask, static_cast<hipStream_t>(stream), k_pages, v_pages, pool_pages);
 }
 
 extern "C" int asym_attn_decode_plan(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,

@@ -136,9 +136,13 @@ struct AttnLaunch {
   uint32_t allow = 0xFFFFFFFFu; // aware: XCDs whose workgroups work
   int B, Hq, Hkv, S, split, n_splits, n_x, grid;
   float scale;
+  const int* k_page = nullptr;  // paged form: device tables [B][Hkv][ceil(S / 32)]; null = dense K, V
+  const int* v_page = nullptr;
+  uint32_t pool_bytes = 0;      // paged form: bytes of each pool (<= 2^31)
 };
 int launch_attn_decode(const AttnLaunch& a, hipStream_t s);
 int attn_tasks_per_workgroup();
+int attn_page_tokens();  // tokens per page of the paged form (8 KiB of one head)
 
 // Multi-head latent attention, decode (576-wide cache rows, 512-wide values).
 struct MlaLaunch {

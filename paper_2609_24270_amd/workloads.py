@@ -361,6 +361,22 @@ def make_attn_inputs_on(p: AttnProblem, device):
     return q, k, v
 
 
+def page_pool(x, table, pool_pages: int, fill: float = 0.0):
+    """The pool a paged cache reads: x [B, H_kv, S, 128] (keys or values) laid
+    out in 32-token pages at the pool pages `table` [B, H_kv, ceil(S / 32)]
+    names (int32, any device); the tail of a head's last page and every pool
+    page no entry names hold `fill`.  Returns bf16 [pool_pages, 32, 128] on
+    x's device."""
+    B, H, S, D = x.shape
+    pph = (S + 31) // 32
+    padded = torch.full((B, H, pph * 32, D), fill, dtype=x.dtype, device=x.device)
+    padded[:, :, :S] = x
+    pool = torch.full((pool_pages, 32, D), fill, dtype=x.dtype, device=x.device)
+    idx = torch.as_tensor(table, device=x.device).reshape(-1).long()
+    pool[idx] = padded.reshape(B * H * pph, 32, D)
+    return pool
+
+
 # Multi-head latent attention, decode (Section 7.1 attention workloads;
 # Appendix F counts one compressed row of 512 + 64 values per token).  One
 # query token per request; query heads 16 (a tensor-parallel shard of a
