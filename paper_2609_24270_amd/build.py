@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libasym.so")
 ARCH = "gfx950"
 
 SOURCES = ["capi.cpp", "topology.cpp", "topology_cache.cpp", "schedule.cpp", "corun.cpp", "affinity.cpp",
-           "interleave.cpp", "kv_place.cpp",
+           "interleave.cpp", "kv_place.cpp", "numa_host.cpp",
            "gemm.hip", "gemm_skinny.hip", "attn_decode.hip", "probe.hip", "latency.hip", "copy.hip", "numa.hip",
            "transpose.hip", "noalloc.hip", "mla_decode.hip"]
 

@@ -193,6 +193,10 @@ struct LatencyMeasure {
   uint64_t base_align = 0;         // out: largest power of two dividing the base address
 };
 int latency_measure(int device, LatencyMeasure& m);
+// home map analysis (numa_host.cpp): the homes of every chunk from the timed page and verification lines
+int home_map_analyze(const uint32_t* L, int n_x, int n_pages, const uint64_t* voffs, int n_verify,
+                     const int* grp, uint64_t hash_mask, int chunk_log2, double tie, int8_t* chunk_home,
+                     asym_home_map_info& info);
 // Affinity groups and home groups from HBM latencies [n_x][n_s] (host only);
 // home (nullable, n_s entries) receives each address's home group, -1 if tied.
 int analyze_latency(const uint32_t* lat, int n_x, int n_s, double threshold, double tie,
