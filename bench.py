@@ -378,6 +378,37 @@ def decode_gemm(dev, stream, launches: int = 20, rounds: int = 5):
                 "tflops": round(2 * 32 * 14336 * 4096 / (v * 1e-3) / 1e12, 2)} for k, v in out.items()}
 
 
+GRID_SHAPES = ((8192, 5120, 8192), (8192, 6656, 8192), (8192, 9216, 8192), (8192, 10240, 8192),
+               (6144, 6144, 8192), (8192, 8192, 8192))
+
+
+def grid_study(topo, dev, stream, launches: int = 20, settle_s: float = 1.0) -> list:
+    """Tile-column counts that are not multiples of 8 (so round-robin dealing
+    of a row-major order scatters each XCD's tiles): the three mappings,
+    interleaved, `launches` each after `settle_s` of settling launches; inputs
+    uniform[-1,1] from seed 1."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    from paper_2609_24270_amd import workloads
+    out = []
+    for (M, N, K) in GRID_SHAPES:
+        p = workloads.make_problem(M, N, K, seed=1)
+        A, B = workloads.make_inputs(p)
+        Ad, Bd = A.to(dev), B.to(dev)
+        C = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        fns = {m: (lambda m=m: asym.gemm(Ad, Bd, C, mapping=m, topo=topo, stream=stream)) for m in MAPPINGS}
+        plan = asym.gemm_plan(Ad, Bd, C, mapping="aware", topo=topo, stream=stream)
+        for f in fns.values():
+            f()
+        settle(list(fns.values()), settle_s)
+        ms = interleaved(fns, launches, stream)
+        out.append({"M": M, "N": N, "K": K, "tile_n": plan["tile_n"], "tiles": [plan["tiles_m"], plan["tiles_n"]],
+                    **{m: round(p.flops / (ms[m] * 1e-3) / 1e12, 1) for m in ms}})
+        del Ad, Bd, C
+    return out
+
+
 def pd_sets(topo, halves):
     """The prefill / decode CU sets: 192 striped bits and the other 64; the
     XCD-aligned split with the decode pair taken from one affinity group."""
@@ -693,23 +724,35 @@ def balanced_study(topo, dev, iters: int = 20, repeats: int = 5, warm: int = 10)
 
 
 def queued(fns: dict, launches: int, rounds: int, stream) -> dict:
-    """Mean per-launch ms of each fn for kernels too short to time one launch
-    at a time: each round first parks the stream on a spin kernel (about
-    3 ms), then queues `launches` back-to-back launches of every variant in
-    turn, each run bracketed by HIP events; the host finishes queueing before
-    the spin ends, so the events time the GPU alone, not the launch calls."""
+    """Mean per-launch ms of each fn for kernels too short to time from the
+    host: each round parks the stream on a spin kernel (about 8 ms) while the
+    host queues `launches` untimed launches of every variant in turn (the
+    clock recovers from the one-wave spin under them), then `launches`
+    back-to-back launches of each variant, each batch bracketed by HIP events
+    on the stream.  The order of the batches rotates from round to round and
+    the rounds are a multiple of the variant count, so every variant takes
+    every position equally often (a batch timed first after the spin runs in
+    another clock and power state than one timed last)."""
     import torch
     names = list(fns)
+    n = len(names)
+    rounds = -(-rounds // n) * n
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(stream)
-    torch.cuda._sleep(1 << 20)
-    b.record(stream)
+    with torch.cuda.stream(stream):
+        a.record(stream)
+        torch.cuda._sleep(1 << 20)
+        b.record(stream)
     torch.cuda.synchronize()
-    spin = int((1 << 20) * 3.0 / max(a.elapsed_time(b), 1e-3))
+    spin = int((1 << 20) * 8.0 / max(a.elapsed_time(b), 1e-3))
     evs = {k: [] for k in names}
-    for _ in range(rounds):
-        torch.cuda._sleep(spin)
-        for k in names:
+    for r in range(rounds):
+        order = names[r % n:] + names[:r % n]
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(spin)
+        for _ in range(launches):
+            for k in order:
+                fns[k]()
+        for k in order:
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             for _ in range(launches):
@@ -1175,7 +1218,7 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,llm,pd,pd_trace,spread,balanced,grouped,numa,placed,attention,mla,parity",
+    ap.add_argument("--studies", default="compare,grid,llm,pd,pd_trace,spread,balanced,grouped,numa,placed,attention,mla,parity",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
                          "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
@@ -1295,6 +1338,8 @@ def main() -> int:
         tot, per = time_launches(mm, 10, stream)
         line["context"] = {"torch_matmul_tflops": round(p.flops / (tot / 10 * 1e-3) / 1e12, 2)}
         del Bt
+    if "grid" in studies:
+        line["tile_grid_shapes"] = grid_study(topo, dev, stream)
     if "llm" in studies:
         line["square_512"] = square_512(topo, dev, stream)
         line["llm_shapes_tflops"] = llm_shapes(dev, stream, 20)

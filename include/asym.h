@@ -726,7 +726,7 @@ int asym_gemm_set_small_m(int enable);
  * longest of 1024, 512, ... 64 giving at least 2048 tasks); a task is one
  * (request, key/value head, split) and serves that head's query heads, so K
  * and V are read once.  A second launch merges the splits of each (request,
- * head) in split order.  Mapping: AWARE gives each XCD a share of the tasks
+ * head) in an order fixed by the split count.  Mapping: AWARE gives each XCD a share of the tasks
  * proportional to its CU count in the stream's CU set (and honours a
  * whole-XCD restriction); its workgroups read the XCD they run on and claim
  * groups of 4 tasks from that XCD's share, then from the others; the
@@ -808,10 +808,11 @@ int asym_attn_pages_place(const asym_attn_plan_info* plan, int B, int H_kv, int 
  * H_q a multiple of 16 (at most 1024); q, kv and O 16-byte aligned; a
  * request's cache below 2 GiB.
  * The sequence is cut into splits of split_tokens tokens (0 = automatic: the
- * longest of 1024, 512, ... 32 giving at least 2048 tasks; else a multiple
+ * longest of 1024, 512, ... 32 giving at least 1024 tasks, lengthened until
+ * there are at most 256 splits; else a multiple
  * of 32); a task is one (request, split, block of 16 query heads) on one wave
  * of the matrix cores.  A second launch merges the splits of each (request,
- * head) in split order.  Mapping: AWARE numbers the tasks request-split
+ * head) in an order fixed by the split count.  Mapping: AWARE numbers the tasks request-split
  * major, so the head blocks that read the same cache rows are consecutive,
  * gives each XCD a share of that list in proportion to its CUs in the
  * stream's CU set (honouring a whole-XCD restriction), and lets workgroups

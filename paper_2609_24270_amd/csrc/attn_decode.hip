@@ -17,7 +17,8 @@
 //     token index across rows, which an MFMA operand would need transposed);
 //   * the next block's K and V are in flight while a block is computed.
 // Each task writes its unnormalised output, max and sum (fp32); a second
-// kernel merges the splits of each (request, head) in split order, so the
+// kernel merges the splits of each (request, head) in an order fixed by the
+// split count (several waves per row when there are many splits), so the
 // result is the same for every assignment of tasks to workgroups.
 //
 // Assignment.  A task's bytes are read by exactly one wave, so there is no
@@ -44,6 +45,7 @@
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
+#include "split_merge.h"
 
 namespace asym {
 namespace {
@@ -312,34 +314,16 @@ __global__ void __launch_bounds__(64 * AT_WAVES) attn_decode_split(AttnParams p)
 
 
 
-// Merge of the splits of one (request, head) per wave, in split order.
-// It also clears the aware form's claim counters for the next split launch on
-// the stream (the split launch is complete when the merge runs).
-__global__ void __launch_bounds__(256) attn_decode_merge(const float* __restrict__ part_o,
-                                                         const float* __restrict__ part_ml, int rows,
-                                                         int n_splits, uint16_t* __restrict__ o,
-                                                         float* __restrict__ lse, int* claim, int n_claim) {
+// Merge of the splits of every (request, head) row (split_merge.h).  It also
+// clears the aware form's claim counters for the next split launch on the
+// stream (the split launch is complete when the merge runs).
+__global__ void __launch_bounds__(64 * kMergeWaves) attn_decode_merge(const float* __restrict__ part_o,
+                                                                      const float* __restrict__ part_ml, int rows,
+                                                                      int n_splits, int wpr, uint16_t* __restrict__ o,
+                                                                      float* __restrict__ lse, int* claim,
+                                                                      int n_claim) {
   if (claim && blockIdx.x == 0 && (int)threadIdx.x < n_claim) claim[threadIdx.x * kClaimStride] = 0;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const int lane = threadIdx.x & 63;
-  const float* ml = part_ml + (size_t)row * n_splits * 2;
-  float M = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml[2 * s]);
-  float L = 0.f, a0 = 0.f, a1 = 0.f;
-  for (int s = 0; s < n_splits; ++s) {
-    const float w = __expf(ml[2 * s] - M);
-    L = fmaf(ml[2 * s + 1], w, L);
-    const float* src = part_o + ((size_t)row * n_splits + s) * AD + 2 * lane;
-    a0 = fmaf(src[0], w, a0);
-    a1 = fmaf(src[1], w, a1);
-  }
-  const float inv = 1.f / L;
-  const __bf16 h0 = (__bf16)(a0 * inv), h1 = (__bf16)(a1 * inv);
-  const uint32_t packed = (uint32_t)__builtin_bit_cast(unsigned short, h0) |
-                          ((uint32_t)__builtin_bit_cast(unsigned short, h1) << 16);
-  reinterpret_cast<uint32_t*>(o + (size_t)row * AD)[lane] = packed;
-  if (lse && lane == 0) lse[row] = M + __logf(L);
+  merge_split_rows<AD>(part_o, part_ml, rows, n_splits, wpr, o, lse);
 }
 
 }  // namespace
@@ -392,9 +376,10 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
 #undef ASYM_ATTN_CASE
   ASYM_HIP(hipGetLastError());
   const int rows = a.B * a.Hq;
-  hipLaunchKernelGGL(attn_decode_merge, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a.part_o, a.part_ml,
-                     rows, a.n_splits, static_cast<uint16_t*>(a.o), a.lse, a.d_quota_off ? a.d_claim : nullptr,
-                     a.n_x);
+  const int wpr = merge_waves_per_row(a.n_splits), rows_per_wg = kMergeWaves / wpr;
+  hipLaunchKernelGGL(attn_decode_merge, dim3((unsigned)((rows + rows_per_wg - 1) / rows_per_wg)),
+                     dim3(64 * kMergeWaves), 0, s, a.part_o, a.part_ml, rows, a.n_splits, wpr,
+                     static_cast<uint16_t*>(a.o), a.lse, a.d_quota_off ? a.d_claim : nullptr, a.n_x);
   ASYM_HIP(hipGetLastError());
   return ASYM_OK;
 }

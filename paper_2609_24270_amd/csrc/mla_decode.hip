@@ -29,7 +29,8 @@
 //     output is rescaled only when a head's running maximum rises (a factor
 //     of exactly 1 is skipped, so the result is the same).
 // Each task writes its unnormalised output, max and sum (fp32); a second
-// kernel merges the splits of each (request, head) in split order, so the
+// kernel merges the splits of each (request, head) in an order fixed by the
+// split count (several waves per row when there are many splits), so the
 // result does not depend on which wave ran which task.
 //
 // Placement.  Tasks are numbered in one of two orders.  Aware: request-split
@@ -44,6 +45,7 @@
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
+#include "split_merge.h"
 
 namespace asym {
 namespace {
@@ -283,43 +285,15 @@ __global__ void __launch_bounds__(64 * MW) mla_decode_split(MlaParams p) {
   }
 }
 
-// Merge of the splits of one (request, head) per wave, in split order; also
+// Merge of the splits of every (request, head) row (split_merge.h); also
 // clears the aware form's claim counters (the split launch is complete).
-__global__ void __launch_bounds__(256) mla_decode_merge(const float* __restrict__ part_o,
-                                                        const float* __restrict__ part_ml, int rows, int n_splits,
-                                                        uint16_t* __restrict__ o, float* __restrict__ lse, int* claim,
-                                                        int n_claim) {
+__global__ void __launch_bounds__(64 * kMergeWaves) mla_decode_merge(const float* __restrict__ part_o,
+                                                                     const float* __restrict__ part_ml, int rows,
+                                                                     int n_splits, int wpr, uint16_t* __restrict__ o,
+                                                                     float* __restrict__ lse, int* claim,
+                                                                     int n_claim) {
   if (claim && blockIdx.x == 0 && (int)threadIdx.x < n_claim) claim[threadIdx.x * kMlClaimStride] = 0;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const int lane = threadIdx.x & 63;
-  const float* ml = part_ml + (size_t)row * n_splits * 2;
-  float M = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml[2 * s]);
-  float L = 0.f;
-  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < n_splits; ++s) {
-    const float w = __expf(ml[2 * s] - M);
-    L = fmaf(ml[2 * s + 1], w, L);
-    const float* src = part_o + ((size_t)row * n_splits + s) * MV + 8 * lane;
-    const f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
-    const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      a[e] = fmaf(x0[e], w, a[e]);
-      a[4 + e] = fmaf(x1[e], w, a[4 + e]);
-    }
-  }
-  const float inv = 1.f / L;
-  uint32_t packed[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const __bf16 lo = (__bf16)(a[2 * e] * inv), hi = (__bf16)(a[2 * e + 1] * inv);
-    packed[e] = (uint32_t)__builtin_bit_cast(unsigned short, lo) |
-                ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
-  }
-  *reinterpret_cast<v4u*>(o + (size_t)row * MV + 8 * lane) = v4u{packed[0], packed[1], packed[2], packed[3]};
-  if (lse && lane == 0) lse[row] = M + __logf(L);
+  merge_split_rows<MV>(part_o, part_ml, rows, n_splits, wpr, o, lse);
 }
 
 }  // namespace
@@ -347,8 +321,10 @@ int launch_mla_decode(const MlaLaunch& a, hipStream_t s) {
   hipLaunchKernelGGL(mla_decode_split, dim3((unsigned)a.grid), dim3(64 * MW), 0, s, p);
   ASYM_HIP(hipGetLastError());
   const int rows = a.B * a.Hq;
-  hipLaunchKernelGGL(mla_decode_merge, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a.part_o, a.part_ml, rows,
-                     a.n_splits, static_cast<uint16_t*>(a.o), a.lse, a.d_quota_off ? a.d_claim : nullptr, a.n_x);
+  const int wpr = merge_waves_per_row(a.n_splits), rows_per_wg = kMergeWaves / wpr;
+  hipLaunchKernelGGL(mla_decode_merge, dim3((unsigned)((rows + rows_per_wg - 1) / rows_per_wg)),
+                     dim3(64 * kMergeWaves), 0, s, a.part_o, a.part_ml, rows, a.n_splits, wpr,
+                     static_cast<uint16_t*>(a.o), a.lse, a.d_quota_off ? a.d_claim : nullptr, a.n_x);
   ASYM_HIP(hipGetLastError());
   return ASYM_OK;
 }
