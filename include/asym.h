@@ -605,14 +605,14 @@ int asym_gemm_grouped_bf16(const asym_topology* topo, int G, const int* M, int N
  * every device buffer that call keeps in its per-stream workspace (the tile
  * schedule, the claim counters of the aware kernel's claiming form, the fp32
  * partial tiles of a split K) sits in one fixed library array per GPU
- * (asym_gemm_noalloc_limits: 5 MiB), held until the process ends.  It calls
+ * (asym_gemm_noalloc_limits: 17 MiB), held until the process ends.  It calls
  * no allocator, device or pinned: a schedule the array does not hold yet is
  * written into it by small kernels that carry it in their arguments.
  * Limits: topo must be a probed topology (NULL is refused: the first-use
  * probe would allocate); ASYM_B_KN is refused (it needs a transposed copy of
  * B); at most asym_gemm_noalloc_limits' max_tiles output tiles (262016:
  * e.g. M = N = 128000 at 256 x 256 tiles); split-K partials within
- * max_partial_bytes (4 MiB, all a 256-CU device needs).
+ * max_partial_bytes (16 MiB, all a 256-CU device needs).
  * Every call on one GPU shares the array and it keeps the last call's
  * contents (the schedule is tracked on the host, the counters are cleared
  * before each claiming launch): calls that overlap in time on one GPU, on any

@@ -237,7 +237,7 @@ constexpr size_t kScratchOffOff = 256;            // ASYM_MAX_XCDS + 1 ints: reg
 constexpr size_t kScratchSlotsOff = 384;          // ASYM_MAX_XCDS ints: workers per XCD
 constexpr size_t kScratchOrderOff = 512;          // the tile order
 constexpr size_t kScratchPartOff = 1u << 20;      // fp32 partial tiles of a split K
-constexpr size_t kScratchPartBytes = 4u << 20;
+constexpr size_t kScratchPartBytes = 16u << 20;  // split K: fewer than 4 x CUs (tile, range) pairs of 16 KiB
 constexpr size_t kScratchBytes = kScratchPartOff + kScratchPartBytes;
 constexpr int kScratchMaxTiles = (int)((kScratchPartOff - kScratchOrderOff) / sizeof(int));
 // the checks that need no device: a topology given, [N][K] storage, a tile

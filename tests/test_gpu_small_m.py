@@ -244,7 +244,7 @@ def test_split_k_under_an_xcd_restriction(dev):
         Ad, Bd = A.to(dev), B.to(dev)
         whole = asym.gemm_plan(A=Ad, B=Bd)
         restricted = asym.gemm_plan(A=Ad, B=Bd, xcd_mask=0xC0)
-        assert whole["small_m"] == 1 and whole["k_splits"] == 4
+        assert whole["small_m"] == 1 and whole["k_splits"] == 8
         assert restricted["small_m"] == 0 and restricted["claims"] == 1
         C1 = bits(asym.gemm(Ad, Bd))
         C2 = bits(asym.gemm(Ad, Bd, xcd_mask=0xC0))
