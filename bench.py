@@ -1119,7 +1119,7 @@ def mla_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 
     return {"configs": out, "uneven_cu_sets": uneven}
 
 
-FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "chunk_read", "mla", "mla16", "copy")
+FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "attention_b1", "chunk_read", "mla", "mla16", "copy")
 
 
 def focus_run(name: str, dev, stream, launches: int) -> dict:
@@ -1127,6 +1127,7 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
       decode_gemm      small-M GEMM 32 x 14336 x 4096 (decode projection)
       grouped_small_m  grouped GEMM (32 groups of ~20 rows) x (6144, 7168), seed 5
       attention_gqa    decode attention, grouped-query, B = 64, S_k = 32768
+      attention_b1     decode attention, grouped-query, B = 1, S_k = 32768 (latency-bound)
       chunk_read       strided read of a 16 GiB region in 8 KiB chunks, address order
       mla              latent-attention decode, B = 64, H_q = 128, S_k = 8192 (aware)
       mla16            latent-attention decode, B = 64, H_q = 16, S_k = 32768 (aware)
@@ -1157,7 +1158,14 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
         o = torch.empty_like(q)
         fn = lambda: asym.attn_decode(q, k, v, o, stream=stream)
         nbytes = p.kv_bytes + 2 * 2 * q.numel()
-        kernel = "attn_decode_split<4> + attn_decode_merge"
+        kernel = "attn_decode_split<4, false> + attn_decode_merge"
+    elif name == "attention_b1":
+        p = workloads.attn_problem("gqa", 1, 32768)
+        q, k, v = workloads.make_attn_inputs_on(p, dev)
+        o = torch.empty_like(q)
+        fn = lambda: asym.attn_decode(q, k, v, o, stream=stream)
+        nbytes = p.kv_bytes + 2 * 2 * q.numel()
+        kernel = "attn_decode_split<4, false> + attn_decode_merge"
     elif name == "mla":
         p = workloads.mla_problem(64, 128, 8192)
         q, kv = workloads.make_mla_inputs_on(p, dev)

@@ -287,10 +287,12 @@ int small_m_ksplit(int M, int N, int K, int mb, int device_cus) {
   const int tiles = (N + small_m_tile_cols() - 1) / small_m_tile_cols();
   const int steps = (K + 31) / 32;
   const int u = mb == 4 ? 4 : 8;
-  if (tiles >= device_cus) return 1;
-  // about two workgroups per CU, in a power of two of ranges (measured on the
-  // decode shapes: 96 column tiles ran 18.6 us in 2 ranges, 15.4 us in 8; 224
-  // tiles 28.2 us unsplit, 27.1 us in 4), each range at least two stages
+  // only when the column tiles leave half the CUs idle, then about two
+  // workgroups per CU in a power of two of ranges, each at least two stages
+  // (measured on the decode shapes: 96 column tiles ran 18.6 us in 2 ranges
+  // and 15.4 us in 8; 224 tiles gained nothing, a 23.8 us split kernel plus a
+  // 4.5 us reduction against 28.7 us unsplit)
+  if (2 * tiles > device_cus) return 1;
   int ks = 1;
   while (ks < 8 && (long long)ks * tiles < 2ll * device_cus) ks *= 2;
   while (ks > 1 && ks * 2 * u > steps) ks /= 2;

@@ -42,7 +42,7 @@ SEQUENCE = [
     (512, 768, 256, "uniform", "aware", 0),             # smaller: 2 x 3 tiles
     (1024, 1536, 512, "llm", "aware", 0x0F),            # claiming form, counters used
     (300, 520, 264, "uniform", "aware", 0x0F),          # again, smaller (counters reused)
-    (32, 14336, 4096, "llm", "aware", 0),               # small-M decode projection, K in 4 ranges
+    (32, 6144, 4096, "llm", "aware", 0),                # small-M decode projection, K in 8 ranges
     (32, 4096, 4096, "llm", "aware", 0),                # small-M, K split into 8 ranges
     (24, 600, 2048, "llm", "aware", 0),                 # small-M, smaller split
     (700, 900, 640, "uniform", "oblivious_grouped", 0),  # oblivious orders
