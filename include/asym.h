@@ -811,12 +811,17 @@ int asym_attn_pages_place(const asym_attn_plan_info* plan, int B, int H_kv, int 
  * longest of 1024, 512, ... 32 giving at least 1024 tasks, lengthened until
  * there are at most 256 splits; else a multiple
  * of 32); a task is one (request, split, block of 16 query heads) on one wave
- * of the matrix cores.  A second launch merges the splits of each (request,
+ * of the matrix cores (wave form), or, when H_q is a multiple of 64, one
+ * (request, split, four blocks of 16 heads) on one workgroup whose four waves
+ * share each 16-token block of rows through LDS (workgroup form; the same
+ * arithmetic per head, so the same bits; asym_mla_set_workgroup_form).  A
+ * second launch merges the splits of each (request,
  * head) in an order fixed by the split count.  Mapping: AWARE numbers the tasks request-split
  * major, so the head blocks that read the same cache rows are consecutive,
  * gives each XCD a share of that list in proportion to its CUs in the
  * stream's CU set (honouring a whole-XCD restriction), and lets workgroups
- * claim groups of 4 tasks from their XCD's share, then from the others: the
+ * claim groups of 4 tasks (one task in the workgroup form) from their XCD's
+ * share, then from the others: the
  * rows cross into one XCD's L2 once.  The oblivious mappings (both) number
  * them head-block major and hand out 4 per workgroup in order, so the head
  * blocks of one split land on different XCDs and every XCD gets an equal
@@ -833,13 +838,21 @@ typedef struct asym_mla_plan_info {
   int split_tokens;
   int n_splits;
   int head_blocks;         /* H_q / 16 */
-  int tasks;               /* B * n_splits * head_blocks */
+  int tasks;               /* B * n_splits * head_blocks (wave form) or
+                              B * n_splits * head_blocks / 4 (workgroup form) */
   int grid;                /* workgroups of the split launch */
-  int tasks_per_workgroup; /* one per wave */
+  int tasks_per_workgroup; /* 4, one per wave (wave form); 1 (workgroup form) */
   int n_xcds;
   int tasks_per_xcd[ASYM_MAX_XCDS];
+  int workgroup_form;      /* 1: a task is 4 head blocks on one workgroup */
   size_t workspace_bytes;  /* fp32 partials: B * H_q * n_splits * 514 * 4 */
 } asym_mla_plan_info;
+
+/* Switch the workgroup form of asym_mla_decode_bf16 on or off for the
+ * process (default on; off runs every head count in the wave form, for
+ * comparison: the two give the same bits); returns the previous setting.
+ * Not synchronised with launches in flight. */
+int asym_mla_set_workgroup_form(int enable);
 
 /* What asym_mla_decode_bf16 would launch (no pointers needed; launches
  * nothing).  Errors as asym_mla_decode_bf16. */

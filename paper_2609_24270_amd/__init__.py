@@ -45,7 +45,7 @@ EXPORTS = (
     "asym_gemm_bf16", "asym_gemm_grouped_bf16", "asym_gemm_bf16_noalloc", "asym_gemm_noalloc_limits",
     "asym_gemm_bf16_trace",
     "asym_gemm_plan", "asym_gemm_set_small_m",
-    "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_attn_decode_paged_bf16", "asym_attn_pages_place", "asym_mla_decode_bf16", "asym_mla_decode_plan",
+    "asym_attn_decode_bf16", "asym_attn_decode_plan", "asym_attn_decode_paged_bf16", "asym_attn_pages_place", "asym_mla_decode_bf16", "asym_mla_decode_plan", "asym_mla_set_workgroup_form",
     "asym_copy_bf16", "asym_corun", "asym_last_error", "asym_version",
 )
 
@@ -160,7 +160,7 @@ class MlaPlanInfo(ctypes.Structure):
     _fields_ = [("split_tokens", ctypes.c_int), ("n_splits", ctypes.c_int), ("head_blocks", ctypes.c_int),
                 ("tasks", ctypes.c_int), ("grid", ctypes.c_int), ("tasks_per_workgroup", ctypes.c_int),
                 ("n_xcds", ctypes.c_int), ("tasks_per_xcd", ctypes.c_int * MAX_XCDS),
-                ("workspace_bytes", ctypes.c_size_t)]
+                ("workgroup_form", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t)]
 
     def to_dict(self) -> dict:
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "tasks_per_xcd"}
@@ -263,6 +263,7 @@ def load_library(path: str = LIB_PATH):
         "asym_gemm_plan": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp,
                                ctypes.POINTER(GemmPlanInfo)]),
         "asym_gemm_set_small_m": (i, [i]),
+        "asym_mla_set_workgroup_form": (i, [i]),
         "asym_gemm_bf16_noalloc": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp]),
         "asym_gemm_bf16_trace": (i, [topo_p, i, i, i, vp, i, vp, i, i, vp, i, i, u32, vp, vp, i, ip]),
         "asym_gemm_noalloc_limits": (i, [ctypes.POINTER(ctypes.c_size_t), ip, ctypes.POINTER(ctypes.c_size_t)]),
@@ -942,6 +943,12 @@ def attn_decode_plan(B: int, Hq: int, Hkv: int, S: int, D: int = 128, split_toke
     _check(load_library().asym_attn_decode_plan(topo.handle if topo else None, B, Hq, Hkv, S, D, split_tokens,
                                                 mp, xcd_mask, _stream_ptr(stream), ctypes.byref(out)))
     return out.to_dict()
+
+
+def set_mla_workgroup_form(enable: bool) -> bool:
+    """Switch the workgroup form of mla_decode (multiples of 64 heads) on or
+    off for the process; returns the previous setting."""
+    return bool(load_library().asym_mla_set_workgroup_form(1 if enable else 0))
 
 
 def set_small_m(enable: bool) -> bool:

@@ -31,7 +31,12 @@ DEVICE_ONLY = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 # Per-source extras.  gemm.hip: let the MFMA accumulators take the VGPR form, so
 # that the register allocator can keep 256 fp32 accumulators and two sets of
 # operand fragments without spilling (the AGPR-only form spills in the k-loop).
-EXTRA = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+# mla_decode.hip: in the AGPR form the 128 output accumulators, which the
+# online softmax rescales with vector instructions, were copied between AGPRs
+# and VGPRs every 16-token block (256 moves per block); in the VGPR form they
+# stay put.  attn_decode.hip: the same, 8 moves per task.
+_VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+EXTRA = {"gemm.hip": _VGPR_FORM, "mla_decode.hip": _VGPR_FORM, "attn_decode.hip": _VGPR_FORM}
 
 
 def hipcc() -> str:

@@ -243,6 +243,7 @@ static int kn_pitch(int K) { return (K + 7) / 8 * 8; }
 // of its CU set (a whole-XCD restriction needs
 // the persistent kernel, whose workers leave the excluded XCDs).
 std::atomic<bool> g_small_m{true};
+std::atomic<bool> g_mla_wg{true};  // latent-attention decode: the workgroup form for multiples of 64 heads
 
 // Up to 64 rows (per group) the small-M kernel always wins (measured: decode
 // projections and 20-row expert groups).  From 65 to kSmallMMaxRows rows it
@@ -1042,7 +1043,7 @@ int attn_decode_plan(const asym_topology* topo_in, int B, int Hq, int Hkv, int S
 
 // ---- multi-head latent attention, decode ------------------------------------
 static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int split_in, int mapping, uint32_t xcd_mask,
-                    hipStream_t stream, AttnPlan* P, int* hblocks) {
+                    hipStream_t stream, AttnPlan* P, int* hblocks, bool* wg_form) {
   if (B < 1 || Hq < 1 || S < 1) return fail(ASYM_EINVAL, "mla: B, H_q, S_k must be >= 1");
   if (Hq % 16) return fail(ASYM_EUNSUPPORTED, "mla: H_q must be a multiple of 16 (blocks of 16 query heads)");
   if (Hq > 1024) return fail(ASYM_EUNSUPPORTED, "mla: at most 1024 query heads");
@@ -1066,13 +1067,17 @@ static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
     while (L < 1024 && (S + L - 1) / L > 256) L *= 2;
   }
   const int64_t n_splits = (S + L - 1) / L;
-  const int64_t tasks = (int64_t)B * hb * n_splits;
+  // the workgroup form shares each block's rows among 4 head blocks (one
+  // task per workgroup); the wave form runs one head block per wave
+  const bool wg = g_mla_wg.load() && hb % mla_wg_head_blocks() == 0;
+  const int64_t tasks = (int64_t)B * n_splits * (wg ? hb / mla_wg_head_blocks() : hb);
   if (tasks > (1ll << 30)) return fail(ASYM_EINVAL, "mla: too many tasks");
   P->split = L;
   P->n_splits = (int)n_splits;
   P->tasks = (int)tasks;
   *hblocks = hb;
-  const int per_wg = mla_tasks_per_workgroup();
+  *wg_form = wg;
+  const int per_wg = wg ? 1 : mla_tasks_per_workgroup();
   const int n_x = P->cs.t->n_xccs;
   if (mapping == ASYM_MAP_AWARE) {
     P->quota = largest_remainder_quotas(P->tasks, P->cs.slots);
@@ -1098,7 +1103,8 @@ int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q
   std::lock_guard<std::mutex> lock(g_mu);
   AttnPlan P;
   int hblocks = 0;
-  int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks);
+  bool wg = false;
+  int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks, &wg);
   if (rc != ASYM_OK) return rc;
   Workspace* ws = nullptr;
   rc = get_workspace(P.cs.device, stream, &ws);
@@ -1108,7 +1114,7 @@ int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q
   const int n_x = P.cs.t->n_xccs;
   int* d_off = nullptr;
   if (mapping == ASYM_MAP_AWARE) {
-    rc = aware_share_offsets(ws, P.cs, P.quota, P.tasks, 1, stream, &d_off);
+    rc = aware_share_offsets(ws, P.cs, P.quota, P.tasks, wg ? 2 : 1, stream, &d_off);
     if (rc != ASYM_OK) return rc;
   }
   MlaLaunch a;
@@ -1124,6 +1130,7 @@ int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q
   a.split = P.split; a.n_splits = P.n_splits;
   a.n_x = n_x; a.grid = P.grid;
   a.scale = scale;
+  a.wg = wg;
   return launch_mla_decode(a, stream);
 }
 
@@ -1133,7 +1140,8 @@ int mla_decode_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
   std::lock_guard<std::mutex> lock(g_mu);
   AttnPlan P;
   int hblocks = 0;
-  const int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks);
+  bool wg = false;
+  const int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks, &wg);
   if (rc != ASYM_OK) return rc;
   *out = asym_mla_plan_info{};
   out->split_tokens = P.split;
@@ -1141,10 +1149,11 @@ int mla_decode_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
   out->head_blocks = hblocks;
   out->tasks = P.tasks;
   out->grid = P.grid;
-  out->tasks_per_workgroup = mla_tasks_per_workgroup();
+  const int per_wg = wg ? 1 : mla_tasks_per_workgroup();
+  out->tasks_per_workgroup = per_wg;
   out->n_xcds = P.cs.t->n_xccs;
+  out->workgroup_form = wg ? 1 : 0;
   out->workspace_bytes = P.ws_bytes;
-  const int per_wg = mla_tasks_per_workgroup();
   for (int x = 0; x < out->n_xcds && x < ASYM_MAX_XCDS; ++x) {
     if (mapping == ASYM_MAP_AWARE) {
       out->tasks_per_xcd[x] = P.quota[x];
@@ -1347,6 +1356,10 @@ extern "C" int asym_version(void) { return 1; }
 
 extern "C" int asym_gemm_set_small_m(int enable) {
   return asym::g_small_m.exchange(enable != 0) ? 1 : 0;
+}
+
+extern "C" int asym_mla_set_workgroup_form(int enable) {
+  return asym::g_mla_wg.exchange(enable != 0) ? 1 : 0;
 }
 
 extern "C" int asym_mla_decode_bf16(const asym_topology* topo, int B, int H_q, int S_k, const void* q,

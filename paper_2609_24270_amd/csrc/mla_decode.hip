@@ -19,15 +19,20 @@
 //     head, so the rescaling is a per-lane factor);
 //   * O^T (512 x 16 heads) += V^T . P^T on the matrix cores
 //     (v_mfma_f32_16x16x16_bf16): a lane's probabilities (4 consecutive
-//     tokens, one head) are already the B operand of that product, and V^T
-//     is written to a per-wave LDS tile from the key fragments already loaded
-//     (the latent part of the row is the value), so the rows are read from
-//     memory once; the tile's rows are padded to 40 bytes so that the four
-//     lane groups of a write land in different banks;
+//     tokens, one head) are already the B operand of that product; the
+//     values are written to a per-wave LDS tile as they are, one 16-byte
+//     store per key fragment already loaded (the latent part of the row is
+//     the value, so the rows are read from memory once), and the A operand
+//     V^T comes out of it through gfx950's transposing LDS read
+//     (ds_read_b64_tr_b16), one per 16 values; token rows are padded by 32
+//     bytes so that the reads of 16 rows spread over the banks;
 //   * 16-token blocks; the next block's rows go out as soon as a block's
 //     fragments are consumed (scores computed, values written), and the
-//     output is rescaled only when a head's running maximum rises (a factor
-//     of exactly 1 is skipped, so the result is the same).
+//     output is rescaled only when a head's block maximum exceeds the
+//     reference maximum by more than a fixed gap (the reference then follows;
+//     below the gap the stale reference keeps the result exact);
+//   * multiples of 64 heads run in the workgroup form instead: four waves on
+//     four head blocks share each block's rows through one LDS tile.
 // Each task writes its unnormalised output, max and sum (fp32); a second
 // kernel merges the splits of each (request, head) in an order fixed by the
 // split count (several waves per row when there are many splits), so the
@@ -56,8 +61,12 @@ constexpr int MW = 4;              // tasks per workgroup, one per wave
 constexpr int MT = 16;             // tokens per block
 constexpr int MSTEPS = MD / 32;    // 18 MFMA steps for the scores
 constexpr int VSTEPS = MV / 32;    // 16 of them cover the latent part
-constexpr int VT_ROW = 40;         // bytes of one V^T row: 16 tokens, padded
-constexpr int VT_BYTES = MV * VT_ROW;  // 20 KiB per wave
+constexpr int V_ROW = MV * 2 + 32;  // bytes of one token's values in the per-wave tile, padded
+constexpr int V_BYTES = MT * V_ROW;  // 16.5 KiB per wave
+constexpr int MG = 4;              // workgroup form: head blocks per workgroup, one per wave
+constexpr int K_ROW = MD * 2 + 32; // workgroup form: bytes of one token's row in the shared tile
+constexpr int K_BYTES = MT * K_ROW;  // 18.5 KiB per tile, two tiles
+constexpr int WG_CHUNKS = (MT * (MD / 8) + 64 * MG - 1) / (64 * MG);  // 16-byte loads per thread per block
 constexpr uint32_t kMlOOB = 0x80000000u;
 constexpr int kMlClaimStride = 64;  // ints between claim counters (256-byte lines)
 
@@ -108,24 +117,131 @@ __device__ __forceinline__ void mla_task_of(const MlaParams& p, bool aware, int 
   }
 }
 
+// ---- the arithmetic of one 16-token block, shared by both forms ----------
+// Scores S^T (16 tokens x 16 heads) = K . Q^T: lane (lr, lq) gets tokens
+// 4 lq .. 4 lq + 3 of the block, head lr.
+__device__ __forceinline__ f32x4 mla_scores(const bf16x8 (&kf)[MSTEPS], const bf16x8 (&qf)[MSTEPS]) {
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < MSTEPS; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[c], qf[c], s, 0, 0, 0);
+  return s;
+}
+
+// Online softmax of a block (tokens past t1 masked): updates the reference
+// max and the sum, rescales the output when some head's block maximum exceeds
+// its reference by more than kRescaleGap (the factor is exactly 1 elsewhere)
+// and returns the probabilities, relative to the reference, as the B operand
+// of P.V.  A reference below the true maximum leaves the result exact (the
+// output, the sum and the max that the merge receives all use it); it only
+// lets probabilities reach e^kRescaleGap, and saves the 128-multiply rescale
+// on most blocks (with the exact maximum, a random sequence raised some head's
+// maximum on about 60% of the blocks of a 1024-token split).
+constexpr float kRescaleGap = 8.f;
+__device__ __forceinline__ i16x4 mla_softmax(f32x4 s, int tok0, int t1, float scale, int lq, f32x4 (&o)[MV / 16],
+                                             float& m_run, float& l_part) {
+  float v[4];
+  float bm = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tok = tok0 + 4 * lq + i;
+    v[i] = tok < t1 ? s[i] * scale : -INFINITY;
+    bm = fmaxf(bm, v[i]);
+  }
+  bm = fmaxf(bm, __shfl_xor(bm, 16));
+  bm = fmaxf(bm, __shfl_xor(bm, 32));
+  // bm is finite (every block has a token); the first block always raises
+  const bool raise = bm > m_run + kRescaleGap;
+  const float m_new = raise ? bm : m_run;
+  const float alpha = raise ? __expf(m_run - m_new) : 1.f;
+  m_run = m_new;
+  float pr[4];
+  float ps = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    pr[i] = __expf(v[i] - m_new);
+    ps += pr[i];
+  }
+  l_part = l_part * alpha + ps;
+  i16x4 pb;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) pb[i] = __builtin_bit_cast(short, (__bf16)pr[i]);
+  if (__ballot(raise)) {
+#pragma unroll
+    for (int j = 0; j < MV / 16; ++j) o[j] *= alpha;
+  }
+  return pb;
+}
+
+// O^T (512 values x 16 heads) += V^T . P^T from a row-major tile (token rows
+// of `pitch` bytes, the latent values first).  The A operand
+// V^T[16 j + lr][4 lq .. 4 lq + 3] comes from a transposing read: in each
+// group of 16 lanes, result lane r takes element r % 4 of the 8 bytes that
+// lanes 4 i + r / 4 address, i = 0 .. 3; lane (lr, lq) addresses token
+// 4 lq + lr / 4, values 16 j + 4 (lr % 4) .. + 3.  In batches of 8, the next
+// batch's reads in flight while a batch's MFMAs run (an empty asm that takes a
+// whole batch keeps the compiler from placing each read next to its use).
+__device__ __forceinline__ void mla_pv(const unsigned char* tile, uint32_t pitch, i16x4 pb, int lr, int lq,
+                                       f32x4 (&o)[MV / 16]) {
+  const uint32_t tr0 = (uint32_t)(4 * lq + (lr >> 2)) * pitch + 8u * (lr & 3);
+  auto read_batch = [&](int jb, i16x4 (&a)[8]) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      a[u] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4*)(tile + tr0 + 32u * (jb + u)));
+  };
+  i16x4 ab[2][8];
+  read_batch(0, ab[0]);
+#pragma unroll
+  for (int jb = 0; jb < MV / 16; jb += 8) {
+    i16x4 (&cur)[8] = ab[(jb / 8) & 1];
+    asm volatile("" : "+v"(cur[0]), "+v"(cur[1]), "+v"(cur[2]), "+v"(cur[3]), "+v"(cur[4]), "+v"(cur[5]),
+                 "+v"(cur[6]), "+v"(cur[7]));
+    if (jb + 8 < MV / 16) read_batch(jb + 8, ab[((jb / 8) + 1) & 1]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) o[jb + u] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(cur[u], pb, o[jb + u], 0, 0, 0);
+  }
+}
+
+// The 16 query rows of head block hb (rows past H_q read as zero).
+__device__ __forceinline__ void mla_load_q(const MlaParams& p, int b, int hb, int lr, int lq, bf16x8 (&qf)[MSTEPS]) {
+  const int h0 = hb * 16;
+  const __amdgpu_buffer_rsrc_t rq =
+      ml_rsrc(p.q + ((size_t)b * p.Hq + h0) * MD, (uint32_t)min(16, p.Hq - h0) * MD * 2u);
+#pragma unroll
+  for (int c = 0; c < MSTEPS; ++c)
+    qf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rq, (uint32_t)(lr * MD + 32 * c + 8 * lq) * 2u, 0, 0));
+}
+
+// A task's unnormalised output, max and sum; lane (lr, lq) holds
+// O^T[16 j + 4 lq + i][head 16 hb + lr].
+__device__ __forceinline__ void mla_store(const MlaParams& p, int b, int split, int hb, int lr, int lq,
+                                          const f32x4 (&o)[MV / 16], float m_run, float l_part) {
+  l_part += __shfl_xor(l_part, 16);  // the four token groups of a head's sum
+  l_part += __shfl_xor(l_part, 32);
+  const int h = hb * 16 + lr;
+  if (h < p.Hq) {
+    const size_t row = ((size_t)b * p.Hq + h) * p.n_splits + split;
+    float* dst = p.part_o + row * MV + 4 * lq;
+#pragma unroll
+    for (int j = 0; j < MV / 16; ++j) *reinterpret_cast<f32x4*>(dst + 16 * j) = o[j];
+    if (lq == 0) {
+      p.part_ml[row * 2] = m_run;
+      p.part_ml[row * 2 + 1] = l_part;
+    }
+  }
+}
+
+// ---- wave form: one (request, split, head block) per wave ---------------
 __device__ void mla_task(const MlaParams& p, int b, int split, int hb, unsigned char* __restrict__ vt) {
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15, lq = lane >> 4;
   const int t0 = split * p.split;
   const int t1 = min(p.S, t0 + p.split);
   const int nblk = (t1 - t0 + MT - 1) / MT;
-
-  // the 16 query rows (rows past H_q are outside the resource and read as zero)
-  const int h0 = hb * 16;
-  const __amdgpu_buffer_rsrc_t rq =
-      ml_rsrc(p.q + ((size_t)b * p.Hq + h0) * MD, (uint32_t)min(16, p.Hq - h0) * MD * 2u);
   const __amdgpu_buffer_rsrc_t rk = ml_rsrc(p.kv + (size_t)b * p.S * MD, (uint32_t)p.S * MD * 2u);
   bf16x8 qf[MSTEPS];
-#pragma unroll
-  for (int c = 0; c < MSTEPS; ++c)
-    qf[c] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
-                                           rq, (uint32_t)(lr * MD + 32 * c + 8 * lq) * 2u, 0, 0));
-
+  mla_load_q(p, b, hb, lr, lq, qf);
   f32x4 o[MV / 16];
 #pragma unroll
   for (int j = 0; j < MV / 16; ++j) o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -142,82 +258,102 @@ __device__ void mla_task(const MlaParams& p, int b, int split, int hb, unsigned 
   };
   load_block(0);
   for (int blk = 0; blk < nblk; ++blk) {
-    // scores: lane (lr, lq) gets tokens 4 lq .. 4 lq + 3 of the block, head h0 + lr
-    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+    const f32x4 s = mla_scores(kf, qf);
+    // the latent values of the block into the tile as they are (row: token,
+    // 16 contiguous bytes per lane and step); this wave's reads of the
+    // previous block are complete (its LDS accesses run in order)
 #pragma unroll
-    for (int c = 0; c < MSTEPS; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[c], qf[c], s, 0, 0, 0);
-    // the latent values of the block into V^T (row: value index, column:
-    // token); this wave's reads of the previous block are complete (its LDS
-    // accesses run in order)
-#pragma unroll
-    for (int c = 0; c < VSTEPS; ++c) {
-      const v4u w = __builtin_bit_cast(v4u, kf[c]);
-      const uint32_t at = (uint32_t)(32 * c + 8 * lq) * VT_ROW + 2u * lr;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        *reinterpret_cast<uint16_t*>(vt + at + (2 * e) * VT_ROW) = (uint16_t)(w[e] & 0xFFFFu);
-        *reinterpret_cast<uint16_t*>(vt + at + (2 * e + 1) * VT_ROW) = (uint16_t)(w[e] >> 16);
-      }
-    }
+    for (int c = 0; c < VSTEPS; ++c)
+      *reinterpret_cast<v4u*>(vt + (uint32_t)lr * V_ROW + (uint32_t)(32 * c + 8 * lq) * 2u) =
+          __builtin_bit_cast(v4u, kf[c]);
     // the next block's rows go out now (the fragments are consumed)
     if (blk + 1 < nblk) load_block(blk + 1);
-    // mask tokens past the split, scale, block max per head
-    float v[4];
-    float bm = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int tok = t0 + blk * MT + 4 * lq + i;
-      v[i] = tok < t1 ? s[i] * p.scale : -INFINITY;
-      bm = fmaxf(bm, v[i]);
-    }
-    bm = fmaxf(bm, __shfl_xor(bm, 16));
-    bm = fmaxf(bm, __shfl_xor(bm, 32));
-    const float m_new = fmaxf(m_run, bm);  // finite: every block has a token
-    const float alpha = __expf(m_run - m_new);
-    m_run = m_new;
-    float pr[4];
-    float ps = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      pr[i] = __expf(v[i] - m_new);
-      ps += pr[i];
-    }
-    l_part = l_part * alpha + ps;
-    i16x4 pb;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pb[i] = __builtin_bit_cast(short, (__bf16)pr[i]);
-    // rescale only where some head's maximum rose (alpha is exactly 1 elsewhere)
-    if (__ballot(alpha != 1.f)) {
-#pragma unroll
-      for (int j = 0; j < MV / 16; ++j) o[j] *= alpha;
-    }
-    wave_sync();  // the V^T writes of every lane before any lane reads
-#pragma unroll
-    for (int j = 0; j < MV / 16; ++j) {
-      const i16x4 a = *reinterpret_cast<const i16x4*>(vt + (uint32_t)(16 * j + lr) * VT_ROW + 8u * lq);
-      o[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pb, o[j], 0, 0, 0);
-    }
+    const i16x4 pb = mla_softmax(s, t0 + blk * MT, t1, p.scale, lq, o, m_run, l_part);
+    wave_sync();  // the tile writes of every lane before any lane reads
+    mla_pv(vt, V_ROW, pb, lr, lq, o);
     wave_sync();  // every lane's reads of the tile before the next block's writes
   }
-  // the four token groups of a head's sum
-  l_part += __shfl_xor(l_part, 16);
-  l_part += __shfl_xor(l_part, 32);
-  // lane (lr, lq) holds O^T[16 j + 4 lq + i][head h0 + lr]
-  const int h = h0 + lr;
-  if (h < p.Hq) {
-    const size_t row = ((size_t)b * p.Hq + h) * p.n_splits + split;
-    float* dst = p.part_o + row * MV + 4 * lq;
+  mla_store(p, b, split, hb, lr, lq, o, m_run, l_part);
+}
+
+// ---- workgroup form: one (request, split, group of 4 head blocks) per
+// workgroup, wave w on head block 4 g + w.  Each block's rows are loaded
+// once per workgroup into a shared LDS tile (two tiles, with the loads of the
+// next two blocks in flight in registers) and read by all four waves: the
+// keys as score operands, the values through the transposing read.  The
+// arithmetic of each wave is that of the wave form, so the bits are the same.
+__device__ void mla_wg_task(const MlaParams& p, int b, int split, int hg, unsigned char* __restrict__ tiles) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15, lq = lane >> 4;
+  const int t0 = split * p.split;
+  const int t1 = min(p.S, t0 + p.split);
+  const int nblk = (t1 - t0 + MT - 1) / MT;
+  const int hb = hg * MG + wave;
+  const __amdgpu_buffer_rsrc_t rk = ml_rsrc(p.kv + (size_t)b * p.S * MD, (uint32_t)p.S * MD * 2u);
+  bf16x8 qf[MSTEPS];
+  mla_load_q(p, b, hb, lr, lq, qf);
+  f32x4 o[MV / 16];
 #pragma unroll
-    for (int j = 0; j < MV / 16; ++j) *reinterpret_cast<f32x4*>(dst + 16 * j) = o[j];
-    if (lq == 0) {
-      p.part_ml[row * 2] = m_run;
-      p.part_ml[row * 2 + 1] = l_part;
+  for (int j = 0; j < MV / 16; ++j) o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_part = 0.f;
+
+  // a block is 16 rows of 72 chunks of 16 bytes; thread t carries chunks
+  // t, t + 256, ... (tokens past the split read as zero)
+  auto gload = [&](int blk, v4u (&r)[WG_CHUNKS]) {
+#pragma unroll
+    for (int e = 0; e < WG_CHUNKS; ++e) {
+      const int c = threadIdx.x + 64 * MG * e;
+      const int tok = t0 + blk * MT + c / (MD / 8);
+      const bool in = c < MT * (MD / 8) && tok < t1;
+      r[e] = __builtin_amdgcn_raw_buffer_load_b128(
+          rk, in ? (uint32_t)(tok * MD + (c % (MD / 8)) * 8) * 2u : kMlOOB, 0, 0);
     }
+  };
+  auto swrite = [&](int buf, const v4u (&r)[WG_CHUNKS]) {
+#pragma unroll
+    for (int e = 0; e < WG_CHUNKS; ++e) {
+      const int c = threadIdx.x + 64 * MG * e;
+      if (c < MT * (MD / 8))
+        *reinterpret_cast<v4u*>(tiles + buf * K_BYTES + (uint32_t)(c / (MD / 8)) * K_ROW + (c % (MD / 8)) * 16u) =
+            r[e];
+    }
+  };
+  // at the top of an even iteration blk, rb holds block blk + 1 and ra block
+  // blk + 2 (odd: the other way round), and tile blk % 2 holds block blk
+  v4u ra[WG_CHUNKS], rb[WG_CHUNKS];
+  gload(0, ra);
+  if (nblk > 1) gload(1, rb);
+  swrite(0, ra);
+  if (nblk > 2) gload(2, ra);
+  __syncthreads();
+  for (int blk = 0; blk < nblk; ++blk) {
+    const unsigned char* tile = tiles + (blk & 1) * K_BYTES;
+    bf16x8 kf[MSTEPS];
+#pragma unroll
+    for (int c = 0; c < MSTEPS; ++c)
+      kf[c] = *reinterpret_cast<const bf16x8*>(tile + (uint32_t)lr * K_ROW + (uint32_t)(32 * c + 8 * lq) * 2u);
+    const f32x4 s = mla_scores(kf, qf);
+    const i16x4 pb = mla_softmax(s, t0 + blk * MT, t1, p.scale, lq, o, m_run, l_part);
+    mla_pv(tile, K_ROW, pb, lr, lq, o);
+    // block blk + 1 into the other tile (its last readers, block blk - 1,
+    // finished before the previous barrier), then block blk + 3's loads
+    if (blk + 1 < nblk) {
+      if (blk & 1) {
+        swrite(0, ra);
+        if (blk + 3 < nblk) gload(blk + 3, ra);
+      } else {
+        swrite(1, rb);
+        if (blk + 3 < nblk) gload(blk + 3, rb);
+      }
+    }
+    __syncthreads();
   }
+  mla_store(p, b, split, hb, lr, lq, o, m_run, l_part);
 }
 
 __global__ void __launch_bounds__(64 * MW) mla_decode_split(MlaParams p) {
-  __shared__ __attribute__((aligned(16))) unsigned char vt_all[MW][VT_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char vt_all[MW][V_BYTES];
   __shared__ int box[2];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -285,6 +421,76 @@ __global__ void __launch_bounds__(64 * MW) mla_decode_split(MlaParams p) {
   }
 }
 
+// Workgroup form: tasks (request, split, group of 4 head blocks), numbered
+// with the group fastest (aware) or group major (oblivious).  Oblivious: task
+// i on workgroup i.  Aware: claims of one task, own share first, then the
+// others, as in the wave form.
+__global__ void __launch_bounds__(64 * MG) mla_decode_split_wg(MlaParams p) {
+  __shared__ __attribute__((aligned(16))) unsigned char tiles[2 * K_BYTES];
+  __shared__ int box[1];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const bool aware = p.quota_off != nullptr;
+  const int groups = p.hblocks / MG;
+  int own = 0;
+  if (aware) {
+    uint32_t xr;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xr));
+    own = (int)(xr & 0xFu);
+    if (own >= p.n_x || !((p.allow >> own) & 1u)) return;  // an XCD outside the set
+  }
+  for (int round = 0;; ++round) {
+    int task;
+    if (!aware) {
+      if (round > 0 || (int)blockIdx.x >= p.tasks) break;
+      task = blockIdx.x;
+    } else {
+      if (wave == 0) {
+        int rem = 0, y = 0, b0 = 0, b1 = 0;
+        if (lane < p.n_x) {
+          y = (own + lane) % p.n_x;
+          b0 = p.quota_off[y];
+          b1 = p.quota_off[y + 1];
+          const int taken =
+              __hip_atomic_load(&p.claim[y * kMlClaimStride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          rem = (b1 - b0) - taken;
+        }
+        unsigned long long open = __ballot(lane < p.n_x && rem > 0);
+        int got_task = -1;
+        while (open && got_task < 0) {
+          const int l = __builtin_ctzll(open);
+          open &= open - 1;
+          int got = -1;
+          if (lane == l) {
+            const int g = atomicAdd(&p.claim[y * kMlClaimStride], 1);
+            if (b0 + g < b1) got = b0 + g;
+          }
+          got_task = __shfl(got, l);
+        }
+        if (lane == 0) box[0] = got_task;
+      }
+      __syncthreads();
+      task = box[0];
+      __syncthreads();
+      if (task < 0) break;
+    }
+    int b, split, hg;
+    if (aware) {
+      hg = task % groups;
+      const int r = task / groups;
+      split = r % p.n_splits;
+      b = r / p.n_splits;
+    } else {
+      const int bs = p.B * p.n_splits;
+      hg = task / bs;
+      const int r = task - hg * bs;
+      split = r % p.n_splits;
+      b = r / p.n_splits;
+    }
+    mla_wg_task(p, b, split, hg, tiles);
+  }
+}
+
 // Merge of the splits of every (request, head) row (split_merge.h); also
 // clears the aware form's claim counters (the split launch is complete).
 __global__ void __launch_bounds__(64 * kMergeWaves) mla_decode_merge(const float* __restrict__ part_o,
@@ -313,12 +519,16 @@ int launch_mla_decode(const MlaLaunch& a, hipStream_t s) {
   p.split = a.split;
   p.n_splits = a.n_splits;
   p.hblocks = (a.Hq + 15) / 16;
-  p.tasks = a.B * a.n_splits * p.hblocks;
+  if (a.wg && p.hblocks % MG) return fail(ASYM_EINVAL, "mla: the workgroup form needs a multiple of 64 heads");
+  p.tasks = a.B * a.n_splits * (a.wg ? p.hblocks / MG : p.hblocks);
   p.n_x = a.n_x;
   p.scale = a.scale;
   if (a.d_quota_off && (!a.d_claim || a.n_x > 64)) return fail(ASYM_EINVAL, "mla: aware launch without claim counters");
   if (a.grid < 1) return fail(ASYM_EINVAL, "mla: empty grid");
-  hipLaunchKernelGGL(mla_decode_split, dim3((unsigned)a.grid), dim3(64 * MW), 0, s, p);
+  if (a.wg)
+    hipLaunchKernelGGL(mla_decode_split_wg, dim3((unsigned)a.grid), dim3(64 * MG), 0, s, p);
+  else
+    hipLaunchKernelGGL(mla_decode_split, dim3((unsigned)a.grid), dim3(64 * MW), 0, s, p);
   ASYM_HIP(hipGetLastError());
   const int rows = a.B * a.Hq;
   const int wpr = merge_waves_per_row(a.n_splits), rows_per_wg = kMergeWaves / wpr;
@@ -330,5 +540,7 @@ int launch_mla_decode(const MlaLaunch& a, hipStream_t s) {
 }
 
 int mla_tasks_per_workgroup() { return MW; }
+
+int mla_wg_head_blocks() { return MG; }
 
 }  // namespace asym

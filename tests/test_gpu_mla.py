@@ -116,7 +116,11 @@ def test_mla_decode_paper_sizes_sampled(dev, B, Hq, S):
 
 def test_mla_plan_shares_and_rejections(dev, topo):
     full = asym.mla_decode_plan(16, 128, 32768, topo=topo)
-    assert full["head_blocks"] == 8 and full["tasks"] == 16 * 8 * full["n_splits"]
+    # 128 heads: the workgroup form, one task per (request, split, 4 head blocks)
+    assert full["head_blocks"] == 8 and full["workgroup_form"] == 1 and full["tasks_per_workgroup"] == 1
+    assert full["tasks"] == 16 * 2 * full["n_splits"]
+    small = asym.mla_decode_plan(16, 16, 32768, topo=topo)
+    assert small["workgroup_form"] == 0 and small["tasks"] == 16 * small["n_splits"]
     assert sum(full["tasks_per_xcd"]) == full["tasks"] and max(full["tasks_per_xcd"]) - min(full["tasks_per_xcd"]) <= 1
     mask = workloads.random_mask_bits(4, 1, 128)[0]
     counts = topo.cuset_counts(mask)
@@ -144,3 +148,42 @@ def test_mla_plan_shares_and_rejections(dev, topo):
     # misaligned output (2 bytes in): refused before any launch
     assert lib.asym_mla_decode_bf16(None, 1, 16, 8, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(kv.data_ptr()),
                                     ctypes.c_void_p(O.data_ptr() + 2), None, 0.1, 0, 0, 0, st) == asym.EINVAL
+
+
+@pytest.mark.parametrize("B,Hq,S,split", [(2, 64, 515, 0), (1, 128, 200, 0), (3, 128, 1000, 64), (1, 64, 17, 0),
+                                          (2, 192, 4111, 1024), (4, 128, 8192, 0)])
+def test_mla_workgroup_form_equals_wave_form_bitwise(dev, topo, B, Hq, S, split):
+    """At multiples of 64 heads the workgroup form (four head blocks sharing
+    each block of rows through LDS) gives the wave form's bits: the same
+    arithmetic per head, only the rows' path differs; on every mapping and on
+    a CU-masked stream.  The workgroup form's output is also checked against
+    the oracle on sampled heads."""
+    p = workloads.MlaProblem(f"wg{B}_{Hq}_{S}", B, Hq, S, seed=S + 3 * Hq)
+    q, kv = workloads.make_mla_inputs(p)
+    qd, kvd = q.to(dev), kv.to(dev)
+    lse_w, lse_g = (torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(2))
+    assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == 1
+    prev = asym.set_mla_workgroup_form(False)
+    try:
+        assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == 0
+        ref = asym.mla_decode(qd, kvd, lse=lse_w, split_tokens=split, topo=topo)
+        torch.cuda.synchronize()
+    finally:
+        asym.set_mla_workgroup_form(prev)
+    got = asym.mla_decode(qd, kvd, lse=lse_g, split_tokens=split, topo=topo)
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref) and torch.equal(lse_g, lse_w)
+    for m in MAPS[1:]:
+        O = asym.mla_decode(qd, kvd, split_tokens=split, mapping=m, topo=topo)
+        torch.cuda.synchronize()
+        assert torch.equal(O, ref), m
+    mask = workloads.random_mask_bits(4, 1, 128)[0]
+    s = asym.stream_create(topo, mask)
+    try:
+        O = asym.mla_decode(qd, kvd, split_tokens=split, topo=topo, stream=s)
+        s.synchronize()
+        assert torch.equal(O, ref), "masked"
+    finally:
+        asym.stream_destroy(s)
+    heads = sorted(set([0, Hq - 1, Hq // 2, 17 % Hq]))
+    check(q, kv, got, lse_g, p.scale, f"mla workgroup form B{B} H{Hq} S{S}", heads=heads)
