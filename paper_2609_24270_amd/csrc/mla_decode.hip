@@ -64,14 +64,17 @@ constexpr int VSTEPS = MV / 32;    // 16 of them cover the latent part
 constexpr int V_ROW = MV * 2 + 32;  // bytes of one token's values in the per-wave tile, padded
 constexpr int V_BYTES = MT * V_ROW;  // 16.5 KiB per wave
 constexpr int MG = 4;              // workgroup form: head blocks per workgroup, one per wave
+constexpr int MT2 = 32;            // workgroup form: tokens per block
 constexpr int K_ROW = MD * 2 + 32; // workgroup form: bytes of one token's row in the shared tile
-constexpr int K_BYTES = MT * K_ROW;  // 18.5 KiB per tile, two tiles
-constexpr int WG_CHUNKS = (MT * (MD / 8) + 64 * MG - 1) / (64 * MG);  // 16-byte loads per thread per block
+constexpr int K_BYTES = MT2 * K_ROW;  // 37 KiB per tile, two tiles
+constexpr int WG_CHUNKS = (MT2 * (MD / 8) + 64 * MG - 1) / (64 * MG);  // 16-byte loads per thread per block
+constexpr int KB = 6;              // workgroup form: score steps per batch of key-fragment reads
 constexpr uint32_t kMlOOB = 0x80000000u;
 constexpr int kMlClaimStride = 64;  // ints between claim counters (256-byte lines)
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
@@ -202,6 +205,81 @@ __device__ __forceinline__ void mla_pv(const unsigned char* tile, uint32_t pitch
   }
 }
 
+// The workgroup form's block of 32 tokens, as two 16-token halves: s0 and
+// s1 give lane (lr, lq) tokens 4 lq .. 4 lq + 3 and 16 + 4 lq .. 16 + 4 lq + 3
+// of head lr.  The softmax step is that of mla_softmax over the 32 tokens;
+// the probabilities come back as the B operand of a 32-deep product whose
+// k index 8 lq + i stands for the first group's token 4 lq + i (i < 4) and
+// the second group's token 16 + 4 lq + i - 4 (i >= 4).
+__device__ __forceinline__ bf16x8 mla_softmax32(f32x4 s0, f32x4 s1, int tok0, int t1, float scale, int lq,
+                                                f32x4 (&o)[MV / 16], float& m_run, float& l_part) {
+  float v[8];
+  float bm = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int tok = tok0 + (i < 4 ? 0 : 16) + 4 * lq + (i & 3);
+    v[i] = tok < t1 ? (i < 4 ? s0[i] : s1[i - 4]) * scale : -INFINITY;
+    bm = fmaxf(bm, v[i]);
+  }
+  bm = fmaxf(bm, __shfl_xor(bm, 16));
+  bm = fmaxf(bm, __shfl_xor(bm, 32));
+  // bm is finite (every block has a token); the first block always raises
+  const bool raise = bm > m_run + kRescaleGap;
+  const float m_new = raise ? bm : m_run;
+  const float alpha = raise ? __expf(m_run - m_new) : 1.f;
+  m_run = m_new;
+  float pr[8];
+  float ps = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    pr[i] = __expf(v[i] - m_new);
+    ps += pr[i];
+  }
+  l_part = l_part * alpha + ps;
+  bf16x8 pb;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) pb[i] = (__bf16)pr[i];
+  if (__ballot(raise)) {
+#pragma unroll
+    for (int j = 0; j < MV / 16; ++j) o[j] *= alpha;
+  }
+  return pb;
+}
+
+// O^T += V^T . P^T over a 32-token block of the shared tile with
+// v_mfma_f32_16x16x32_bf16: the A operand of lane (lr, lq) joins the
+// transposing reads of the two 16-row halves (values 16 j + lr, tokens
+// 4 lq .. 4 lq + 3 of each half), in the k order of mla_softmax32.  Batches of
+// 8 products, the next batch's 16 reads in flight while a batch runs.
+__device__ __forceinline__ void mla_pv32(const unsigned char* tile, bf16x8 pb, int lr, int lq, f32x4 (&o)[MV / 16]) {
+  const uint32_t tr0 = (uint32_t)(4 * lq + (lr >> 2)) * K_ROW + 8u * (lr & 3);
+  auto read_batch = [&](int jb, i16x4 (&a)[16]) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      a[2 * u] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4*)(tile + tr0 + 32u * (jb + u)));
+      a[2 * u + 1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4*)(tile + tr0 + 16u * K_ROW + 32u * (jb + u)));
+    }
+  };
+  i16x4 ab[2][16];
+  read_batch(0, ab[0]);
+#pragma unroll
+  for (int jb = 0; jb < MV / 16; jb += 8) {
+    i16x4 (&cur)[16] = ab[(jb / 8) & 1];
+    asm volatile("" : "+v"(cur[0]), "+v"(cur[1]), "+v"(cur[2]), "+v"(cur[3]), "+v"(cur[4]), "+v"(cur[5]),
+                 "+v"(cur[6]), "+v"(cur[7]), "+v"(cur[8]), "+v"(cur[9]), "+v"(cur[10]), "+v"(cur[11]),
+                 "+v"(cur[12]), "+v"(cur[13]), "+v"(cur[14]), "+v"(cur[15]));
+    if (jb + 8 < MV / 16) read_batch(jb + 8, ab[((jb / 8) + 1) & 1]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(cur[2 * u], cur[2 * u + 1], 0, 1, 2, 3,
+                                                                          4, 5, 6, 7));
+      o[jb + u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[jb + u], 0, 0, 0);
+    }
+  }
+}
+
 // The 16 query rows of head block hb (rows past H_q read as zero).
 __device__ __forceinline__ void mla_load_q(const MlaParams& p, int b, int hb, int lr, int lq, bf16x8 (&qf)[MSTEPS]) {
   const int h0 = hb * 16;
@@ -277,18 +355,20 @@ __device__ void mla_task(const MlaParams& p, int b, int split, int hb, unsigned 
 }
 
 // ---- workgroup form: one (request, split, group of 4 head blocks) per
-// workgroup, wave w on head block 4 g + w.  Each block's rows are loaded
-// once per workgroup into a shared LDS tile (two tiles, with the loads of the
-// next two blocks in flight in registers) and read by all four waves: the
-// keys as score operands, the values through the transposing read.  The
-// arithmetic of each wave is that of the wave form, so the bits are the same.
+// workgroup, wave w on head block 4 g + w.  Each 32-token block's rows are
+// loaded once per workgroup into a shared LDS tile (two tiles, the next
+// block's loads in flight in registers) and read by all four waves: the keys
+// as score operands (the two 16-row halves as two independent MFMA chains),
+// the values through the transposing read.  The softmax runs once per
+// 32 tokens and P.V takes 32-deep products, so this form rounds differently
+// from the wave form (16-token blocks); neither depends on the placement.
 __device__ void mla_wg_task(const MlaParams& p, int b, int split, int hg, unsigned char* __restrict__ tiles) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int lr = lane & 15, lq = lane >> 4;
   const int t0 = split * p.split;
   const int t1 = min(p.S, t0 + p.split);
-  const int nblk = (t1 - t0 + MT - 1) / MT;
+  const int nblk = (t1 - t0 + MT2 - 1) / MT2;
   const int hb = hg * MG + wave;
   const __amdgpu_buffer_rsrc_t rk = ml_rsrc(p.kv + (size_t)b * p.S * MD, (uint32_t)p.S * MD * 2u);
   bf16x8 qf[MSTEPS];
@@ -298,14 +378,14 @@ __device__ void mla_wg_task(const MlaParams& p, int b, int split, int hg, unsign
   for (int j = 0; j < MV / 16; ++j) o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_part = 0.f;
 
-  // a block is 16 rows of 72 chunks of 16 bytes; thread t carries chunks
+  // a block is 32 rows of 72 chunks of 16 bytes; thread t carries chunks
   // t, t + 256, ... (tokens past the split read as zero)
   auto gload = [&](int blk, v4u (&r)[WG_CHUNKS]) {
 #pragma unroll
     for (int e = 0; e < WG_CHUNKS; ++e) {
       const int c = threadIdx.x + 64 * MG * e;
-      const int tok = t0 + blk * MT + c / (MD / 8);
-      const bool in = c < MT * (MD / 8) && tok < t1;
+      const int tok = t0 + blk * MT2 + c / (MD / 8);
+      const bool in = c < MT2 * (MD / 8) && tok < t1;
       r[e] = __builtin_amdgcn_raw_buffer_load_b128(
           rk, in ? (uint32_t)(tok * MD + (c % (MD / 8)) * 8) * 2u : kMlOOB, 0, 0);
     }
@@ -314,38 +394,53 @@ __device__ void mla_wg_task(const MlaParams& p, int b, int split, int hg, unsign
 #pragma unroll
     for (int e = 0; e < WG_CHUNKS; ++e) {
       const int c = threadIdx.x + 64 * MG * e;
-      if (c < MT * (MD / 8))
+      if (c < MT2 * (MD / 8))
         *reinterpret_cast<v4u*>(tiles + buf * K_BYTES + (uint32_t)(c / (MD / 8)) * K_ROW + (c % (MD / 8)) * 16u) =
             r[e];
     }
   };
-  // at the top of an even iteration blk, rb holds block blk + 1 and ra block
-  // blk + 2 (odd: the other way round), and tile blk % 2 holds block blk
-  v4u ra[WG_CHUNKS], rb[WG_CHUNKS];
+  // at the top of iteration blk, tile blk % 2 holds block blk and the
+  // staging registers block blk + 1
+  v4u ra[WG_CHUNKS];
   gload(0, ra);
-  if (nblk > 1) gload(1, rb);
   swrite(0, ra);
-  if (nblk > 2) gload(2, ra);
+  if (nblk > 1) gload(1, ra);
   __syncthreads();
   for (int blk = 0; blk < nblk; ++blk) {
     const unsigned char* tile = tiles + (blk & 1) * K_BYTES;
-    bf16x8 kf[MSTEPS];
+    // scores of the two halves: key fragments of KB steps of both halves
+    // per batch, a batch's reads all issued (the empty asm) before the
+    // previous batch's MFMAs
+    const unsigned char* krow = tile + (uint32_t)lr * K_ROW + 16u * lq;
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    bf16x8 kf[2][2 * KB];
+    auto kread = [&](int c0, bf16x8 (&k)[2 * KB]) {
 #pragma unroll
-    for (int c = 0; c < MSTEPS; ++c)
-      kf[c] = *reinterpret_cast<const bf16x8*>(tile + (uint32_t)lr * K_ROW + (uint32_t)(32 * c + 8 * lq) * 2u);
-    const f32x4 s = mla_scores(kf, qf);
-    const i16x4 pb = mla_softmax(s, t0 + blk * MT, t1, p.scale, lq, o, m_run, l_part);
-    mla_pv(tile, K_ROW, pb, lr, lq, o);
-    // block blk + 1 into the other tile (its last readers, block blk - 1,
-    // finished before the previous barrier), then block blk + 3's loads
-    if (blk + 1 < nblk) {
-      if (blk & 1) {
-        swrite(0, ra);
-        if (blk + 3 < nblk) gload(blk + 3, ra);
-      } else {
-        swrite(1, rb);
-        if (blk + 3 < nblk) gload(blk + 3, rb);
+      for (int c = 0; c < KB; ++c) {
+        k[2 * c] = *reinterpret_cast<const bf16x8*>(krow + 64u * (c0 + c));
+        k[2 * c + 1] = *reinterpret_cast<const bf16x8*>(krow + 16u * K_ROW + 64u * (c0 + c));
       }
+    };
+    kread(0, kf[0]);
+#pragma unroll
+    for (int c0 = 0; c0 < MSTEPS; c0 += KB) {
+      bf16x8 (&k)[2 * KB] = kf[(c0 / KB) & 1];
+      asm volatile("" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]), "+v"(k[4]), "+v"(k[5]), "+v"(k[6]),
+                   "+v"(k[7]), "+v"(k[8]), "+v"(k[9]), "+v"(k[10]), "+v"(k[11]));
+      if (c0 + KB < MSTEPS) kread(c0 + KB, kf[((c0 / KB) + 1) & 1]);
+#pragma unroll
+      for (int c = 0; c < KB; ++c) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k[2 * c], qf[c0 + c], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k[2 * c + 1], qf[c0 + c], s1, 0, 0, 0);
+      }
+    }
+    const bf16x8 pb = mla_softmax32(s0, s1, t0 + blk * MT2, t1, p.scale, lq, o, m_run, l_part);
+    mla_pv32(tile, pb, lr, lq, o);
+    // block blk + 1 into the other tile (its last readers, block blk - 1,
+    // finished before the previous barrier), then block blk + 2's loads
+    if (blk + 1 < nblk) {
+      swrite((blk + 1) & 1, ra);
+      if (blk + 2 < nblk) gload(blk + 2, ra);
     }
     __syncthreads();
   }

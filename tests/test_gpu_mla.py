@@ -6,7 +6,8 @@ token, ragged 16-token blocks, one and many splits (automatic and forced),
 and 16 to 128 query heads; on sampled (request, head) pairs at the paper's
 sizes (long sequences, 128 heads).  Bitwise: every mapping, repeats, a
 CU-masked stream with unequal CUs per XCD and whole-XCD restrictions give the
-same bits.  The plan's task shares follow the CU counts; bad arguments are
+same bits; at multiples of 64 heads both the workgroup form and the wave
+form match the oracle.  The plan's task shares follow the CU counts; bad arguments are
 refused before any launch.
 """
 import numpy as np
@@ -151,13 +152,14 @@ def test_mla_plan_shares_and_rejections(dev, topo):
 
 
 @pytest.mark.parametrize("B,Hq,S,split", [(2, 64, 515, 0), (1, 128, 200, 0), (3, 128, 1000, 64), (1, 64, 17, 0),
-                                          (2, 192, 4111, 1024), (4, 128, 8192, 0)])
-def test_mla_workgroup_form_equals_wave_form_bitwise(dev, topo, B, Hq, S, split):
-    """At multiples of 64 heads the workgroup form (four head blocks sharing
-    each block of rows through LDS) gives the wave form's bits: the same
-    arithmetic per head, only the rows' path differs; on every mapping and on
-    a CU-masked stream.  The workgroup form's output is also checked against
-    the oracle on sampled heads."""
+                                          (2, 192, 4111, 1024), (4, 128, 8192, 0), (2, 64, 100, 32)])
+def test_mla_workgroup_form(dev, topo, B, Hq, S, split):
+    """At multiples of 64 heads the workgroup form runs (four head blocks
+    sharing each 32-token block of rows through LDS, one softmax step per 32
+    tokens, 32-deep P.V products).  It rounds differently from the wave form
+    (16-token blocks): both are checked against the oracle, on every head of
+    the small shapes and on sampled heads of the long ones, and the workgroup
+    form's bits are the same on every mapping and on a CU-masked stream."""
     p = workloads.MlaProblem(f"wg{B}_{Hq}_{S}", B, Hq, S, seed=S + 3 * Hq)
     q, kv = workloads.make_mla_inputs(p)
     qd, kvd = q.to(dev), kv.to(dev)
@@ -166,24 +168,24 @@ def test_mla_workgroup_form_equals_wave_form_bitwise(dev, topo, B, Hq, S, split)
     prev = asym.set_mla_workgroup_form(False)
     try:
         assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == 0
-        ref = asym.mla_decode(qd, kvd, lse=lse_w, split_tokens=split, topo=topo)
+        wave = asym.mla_decode(qd, kvd, lse=lse_w, split_tokens=split, topo=topo)
         torch.cuda.synchronize()
     finally:
         asym.set_mla_workgroup_form(prev)
     got = asym.mla_decode(qd, kvd, lse=lse_g, split_tokens=split, topo=topo)
     torch.cuda.synchronize()
-    assert torch.equal(got, ref) and torch.equal(lse_g, lse_w)
     for m in MAPS[1:]:
         O = asym.mla_decode(qd, kvd, split_tokens=split, mapping=m, topo=topo)
         torch.cuda.synchronize()
-        assert torch.equal(O, ref), m
+        assert torch.equal(O, got), m
     mask = workloads.random_mask_bits(4, 1, 128)[0]
     s = asym.stream_create(topo, mask)
     try:
         O = asym.mla_decode(qd, kvd, split_tokens=split, topo=topo, stream=s)
         s.synchronize()
-        assert torch.equal(O, ref), "masked"
+        assert torch.equal(O, got), "masked"
     finally:
         asym.stream_destroy(s)
-    heads = sorted(set([0, Hq - 1, Hq // 2, 17 % Hq]))
+    heads = None if B * Hq * S <= 200_000 else sorted(set([0, Hq - 1, Hq // 2, 17 % Hq]))
     check(q, kv, got, lse_g, p.scale, f"mla workgroup form B{B} H{Hq} S{S}", heads=heads)
+    check(q, kv, wave, lse_w, p.scale, f"mla wave form B{B} H{Hq} S{S}", heads=heads)
