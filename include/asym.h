@@ -811,12 +811,15 @@ int asym_attn_pages_place(const asym_attn_plan_info* plan, int B, int H_kv, int 
  * longest of 1024, 512, ... 32 giving at least 1024 tasks, lengthened until
  * there are at most 256 splits; else a multiple
  * of 32); a task is one (request, split, block of 16 query heads) on one wave
- * of the matrix cores (wave form), or, when H_q is a multiple of 64, one
- * (request, split, four blocks of 16 heads) on one workgroup whose four waves
- * share each 16-token block of rows through LDS (workgroup form; the same
- * arithmetic per head, so the same bits; asym_mla_set_workgroup_form).  A
- * second launch merges the splits of each (request,
- * head) in an order fixed by the split count.  Mapping: AWARE numbers the tasks request-split
+ * of the matrix cores (wave form, 16-token blocks), or, when H_q is a
+ * multiple of 64, one (request, split, four blocks of 16 heads) on one
+ * workgroup whose four waves share each 32-token block of rows through LDS
+ * (64-head form), or, when H_q is a multiple of 128 and those tasks number
+ * more than half the CUs of the set, one (request, split, eight blocks of 16
+ * heads) on one workgroup, two head blocks per wave (128-head form).  The two workgroup forms give the same bits (the same
+ * operations per head); the wave form, with a softmax step every 16 tokens,
+ * rounds differently (asym_mla_set_workgroup_form).  A second launch merges
+ * the splits of each (request, head) in an order fixed by the split count.  Mapping: AWARE numbers the tasks request-split
  * major, so the head blocks that read the same cache rows are consecutive,
  * gives each XCD a share of that list in proportion to its CUs in the
  * stream's CU set (honouring a whole-XCD restriction), and lets workgroups
@@ -838,21 +841,23 @@ typedef struct asym_mla_plan_info {
   int split_tokens;
   int n_splits;
   int head_blocks;         /* H_q / 16 */
-  int tasks;               /* B * n_splits * head_blocks (wave form) or
-                              B * n_splits * head_blocks / 4 (workgroup form) */
+  int tasks;               /* B * n_splits * head_blocks (wave form),
+                              B * n_splits * head_blocks / 4 or / 8 (64- and 128-head forms) */
   int grid;                /* workgroups of the split launch */
-  int tasks_per_workgroup; /* 4, one per wave (wave form); 1 (workgroup form) */
+  int tasks_per_workgroup; /* 4, one per wave (wave form); 1 (workgroup forms) */
   int n_xcds;
   int tasks_per_xcd[ASYM_MAX_XCDS];
-  int workgroup_form;      /* 1: a task is 4 head blocks on one workgroup */
+  int workgroup_form;      /* 0: wave form; 1: 64-head form; 2: 128-head form */
   size_t workspace_bytes;  /* fp32 partials: B * H_q * n_splits * 514 * 4 */
 } asym_mla_plan_info;
 
-/* Switch the workgroup form of asym_mla_decode_bf16 on or off for the
- * process (default on; off runs every head count in the wave form, for
- * comparison: the two give the same bits); returns the previous setting.
- * Not synchronised with launches in flight. */
-int asym_mla_set_workgroup_form(int enable);
+/* Which kernel forms asym_mla_decode_bf16 may take, for the process: 0 runs
+ * every head count in the wave form, 1 allows the 64-head form, 2 (the
+ * default) also the 128-head form where it has enough tasks, 3 the 128-head
+ * form wherever H_q is a multiple of 128; for comparisons.  Returns the
+ * previous level.  Not synchronised with launches in flight.
+ * Errors: ASYM_EINVAL (a level other than 0 to 3). */
+int asym_mla_set_workgroup_form(int level);
 
 /* What asym_mla_decode_bf16 would launch (no pointers needed; launches
  * nothing).  Errors as asym_mla_decode_bf16. */

@@ -945,10 +945,16 @@ def attn_decode_plan(B: int, Hq: int, Hkv: int, S: int, D: int = 128, split_toke
     return out.to_dict()
 
 
-def set_mla_workgroup_form(enable: bool) -> bool:
-    """Switch the workgroup form of mla_decode (multiples of 64 heads) on or
-    off for the process; returns the previous setting."""
-    return bool(load_library().asym_mla_set_workgroup_form(1 if enable else 0))
+def set_mla_workgroup_form(level) -> int:
+    """Which kernel forms mla_decode may take, for the process: 0 (or False)
+    the wave form only, 1 up to the 64-head workgroup form, 2 (or True, the
+    default) also the 128-head form where it has enough tasks, 3 the 128-head
+    form wherever the head count allows; returns the previous level."""
+    lvl = 2 if level is True else 0 if level is False else int(level)
+    prev = load_library().asym_mla_set_workgroup_form(lvl)
+    if prev < 0:
+        _check(prev)
+    return prev
 
 
 def set_small_m(enable: bool) -> bool:

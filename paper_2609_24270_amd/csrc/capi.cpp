@@ -243,7 +243,10 @@ static int kn_pitch(int K) { return (K + 7) / 8 * 8; }
 // of its CU set (a whole-XCD restriction needs
 // the persistent kernel, whose workers leave the excluded XCDs).
 std::atomic<bool> g_small_m{true};
-std::atomic<bool> g_mla_wg{true};  // latent-attention decode: the workgroup form for multiples of 64 heads
+// latent-attention decode: which kernel forms may run (0: waves only; 1: up to
+// the 64-head workgroup form; 2: also the 128-head form where it has enough
+// tasks; 3: the 128-head form wherever the head count allows)
+std::atomic<int> g_mla_form{2};
 
 // Up to 64 rows (per group) the small-M kernel always wins (measured: decode
 // projections and 20-row expert groups).  From 65 to kSmallMMaxRows rows it
@@ -1043,7 +1046,7 @@ int attn_decode_plan(const asym_topology* topo_in, int B, int Hq, int Hkv, int S
 
 // ---- multi-head latent attention, decode ------------------------------------
 static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int split_in, int mapping, uint32_t xcd_mask,
-                    hipStream_t stream, AttnPlan* P, int* hblocks, bool* wg_form) {
+                    hipStream_t stream, AttnPlan* P, int* hblocks, int* form_out) {
   if (B < 1 || Hq < 1 || S < 1) return fail(ASYM_EINVAL, "mla: B, H_q, S_k must be >= 1");
   if (Hq % 16) return fail(ASYM_EUNSUPPORTED, "mla: H_q must be a multiple of 16 (blocks of 16 query heads)");
   if (Hq > 1024) return fail(ASYM_EUNSUPPORTED, "mla: at most 1024 query heads");
@@ -1067,17 +1070,28 @@ static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
     while (L < 1024 && (S + L - 1) / L > 256) L *= 2;
   }
   const int64_t n_splits = (S + L - 1) / L;
-  // the workgroup form shares each block's rows among 4 head blocks (one
-  // task per workgroup); the wave form runs one head block per wave
-  const bool wg = g_mla_wg.load() && hb % mla_wg_head_blocks() == 0;
-  const int64_t tasks = (int64_t)B * n_splits * (wg ? hb / mla_wg_head_blocks() : hb);
+  // the workgroup forms share each block's rows among 4 or 8 head blocks
+  // (one task per workgroup); the wave form runs one head block per wave.
+  // The 128-head form does a task's blocks faster, but has half the 64-head
+  // form's tasks: it is taken when those tasks fill more than half the CU set
+  // (with fewer, the 64-head form finishes in one round of tasks on every CU;
+  // measured at one request, 128 heads, 32K tokens: 47.6 against 37.7 us)
+  const int allow = g_mla_form.load();
+  const int set_cus = P->cs.total;
+  const int64_t t128 = (int64_t)B * n_splits * (hb / mla_form_head_blocks(2));
+  const bool fits128 = hb % mla_form_head_blocks(2) == 0;
+  const int form = allow >= 3 && fits128                         ? 2
+                   : allow >= 2 && fits128 && 2 * t128 > set_cus ? 2
+                   : allow >= 1 && hb % mla_form_head_blocks(1) == 0 ? 1
+                                                                      : 0;
+  const int64_t tasks = (int64_t)B * n_splits * (hb / mla_form_head_blocks(form));
   if (tasks > (1ll << 30)) return fail(ASYM_EINVAL, "mla: too many tasks");
   P->split = L;
   P->n_splits = (int)n_splits;
   P->tasks = (int)tasks;
   *hblocks = hb;
-  *wg_form = wg;
-  const int per_wg = wg ? 1 : mla_tasks_per_workgroup();
+  *form_out = form;
+  const int per_wg = form ? 1 : mla_tasks_per_workgroup();
   const int n_x = P->cs.t->n_xccs;
   if (mapping == ASYM_MAP_AWARE) {
     P->quota = largest_remainder_quotas(P->tasks, P->cs.slots);
@@ -1103,8 +1117,8 @@ int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q
   std::lock_guard<std::mutex> lock(g_mu);
   AttnPlan P;
   int hblocks = 0;
-  bool wg = false;
-  int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks, &wg);
+  int form = 0;
+  int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks, &form);
   if (rc != ASYM_OK) return rc;
   Workspace* ws = nullptr;
   rc = get_workspace(P.cs.device, stream, &ws);
@@ -1114,7 +1128,7 @@ int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q
   const int n_x = P.cs.t->n_xccs;
   int* d_off = nullptr;
   if (mapping == ASYM_MAP_AWARE) {
-    rc = aware_share_offsets(ws, P.cs, P.quota, P.tasks, wg ? 2 : 1, stream, &d_off);
+    rc = aware_share_offsets(ws, P.cs, P.quota, P.tasks, 1 + form, stream, &d_off);
     if (rc != ASYM_OK) return rc;
   }
   MlaLaunch a;
@@ -1130,7 +1144,7 @@ int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q
   a.split = P.split; a.n_splits = P.n_splits;
   a.n_x = n_x; a.grid = P.grid;
   a.scale = scale;
-  a.wg = wg;
+  a.form = form;
   return launch_mla_decode(a, stream);
 }
 
@@ -1140,8 +1154,8 @@ int mla_decode_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
   std::lock_guard<std::mutex> lock(g_mu);
   AttnPlan P;
   int hblocks = 0;
-  bool wg = false;
-  const int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks, &wg);
+  int form = 0;
+  const int rc = mla_plan(topo_in, B, Hq, S, split_in, mapping, xcd_mask, stream, &P, &hblocks, &form);
   if (rc != ASYM_OK) return rc;
   *out = asym_mla_plan_info{};
   out->split_tokens = P.split;
@@ -1149,10 +1163,10 @@ int mla_decode_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
   out->head_blocks = hblocks;
   out->tasks = P.tasks;
   out->grid = P.grid;
-  const int per_wg = wg ? 1 : mla_tasks_per_workgroup();
+  const int per_wg = form ? 1 : mla_tasks_per_workgroup();
   out->tasks_per_workgroup = per_wg;
   out->n_xcds = P.cs.t->n_xccs;
-  out->workgroup_form = wg ? 1 : 0;
+  out->workgroup_form = form;
   out->workspace_bytes = P.ws_bytes;
   for (int x = 0; x < out->n_xcds && x < ASYM_MAX_XCDS; ++x) {
     if (mapping == ASYM_MAP_AWARE) {
@@ -1358,8 +1372,9 @@ extern "C" int asym_gemm_set_small_m(int enable) {
   return asym::g_small_m.exchange(enable != 0) ? 1 : 0;
 }
 
-extern "C" int asym_mla_set_workgroup_form(int enable) {
-  return asym::g_mla_wg.exchange(enable != 0) ? 1 : 0;
+extern "C" int asym_mla_set_workgroup_form(int level) {
+  if (level < 0 || level > 3) return asym::fail(ASYM_EINVAL, "mla: the form level must be 0, 1, 2 or 3");
+  return asym::g_mla_form.exchange(level);
 }
 
 extern "C" int asym_mla_decode_bf16(const asym_topology* topo, int B, int H_q, int S_k, const void* q,

@@ -156,11 +156,11 @@ struct MlaLaunch {
   uint32_t allow = 0xFFFFFFFFu;
   int B, Hq, S, split, n_splits, n_x, grid;
   float scale;
-  bool wg = false;            // workgroup form: a task is 4 head blocks on one workgroup
+  int form = 0;               // 0: a task is one head block on one wave; 1, 2: 4 or 8 head blocks on one workgroup
 };
 int launch_mla_decode(const MlaLaunch& a, hipStream_t s);
 int mla_tasks_per_workgroup();  // wave form: tasks (head blocks) per workgroup
-int mla_wg_head_blocks();       // workgroup form: head blocks per task
+int mla_form_head_blocks(int form);  // head blocks per task of a kernel form
 int attn_claim_ints();  // ints of the aware form's claim counters
 
 int probe_identity_run(int device, hipStream_t s, int n_blocks,

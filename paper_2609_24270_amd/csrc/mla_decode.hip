@@ -69,6 +69,13 @@ constexpr int K_ROW = MD * 2 + 32; // workgroup form: bytes of one token's row i
 constexpr int K_BYTES = MT2 * K_ROW;  // 37 KiB per tile, two tiles
 constexpr int WG_CHUNKS = (MT2 * (MD / 8) + 64 * MG - 1) / (64 * MG);  // 16-byte loads per thread per block
 constexpr int KB = 6;              // workgroup form: score steps per batch of key-fragment reads
+constexpr int MG2 = 8;             // 128-head form: head blocks per workgroup, two per wave
+constexpr int T2_ROWSLOTS = K_ROW / 16;  // 16-byte slots of a tile row (72 of them data)
+constexpr int T2_DMA = 10;         // 128-head form: 1 KiB direct-to-LDS loads per wave per block
+constexpr int T2_BYTES = 4 * T2_DMA * 1024;  // 40 KiB per tile (2368 slots used), three tiles
+constexpr int T2_TILES = 3;
+constexpr int KB2 = 3;             // 128-head form: score steps per batch of key-fragment reads
+static_assert(4 * T2_DMA * 64 >= MT2 * T2_ROWSLOTS, "a block's slots must fit the loads");
 constexpr uint32_t kMlOOB = 0x80000000u;
 constexpr int kMlClaimStride = 64;  // ints between claim counters (256-byte lines)
 
@@ -77,6 +84,10 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 struct MlaParams {
   const uint16_t* q;     // [B][Hq][576]
@@ -211,8 +222,10 @@ __device__ __forceinline__ void mla_pv(const unsigned char* tile, uint32_t pitch
 // the probabilities come back as the B operand of a 32-deep product whose
 // k index 8 lq + i stands for the first group's token 4 lq + i (i < 4) and
 // the second group's token 16 + 4 lq + i - 4 (i >= 4).
-__device__ __forceinline__ bf16x8 mla_softmax32(f32x4 s0, f32x4 s1, int tok0, int t1, float scale, int lq,
-                                                f32x4 (&o)[MV / 16], float& m_run, float& l_part) {
+// The probabilities and the statistics; `alpha` is the factor the output
+// takes when the wave's ballot of `raise` is set (exactly 1 on other lanes).
+__device__ __forceinline__ bf16x8 mla_softmax32_core(f32x4 s0, f32x4 s1, int tok0, int t1, float scale, int lq,
+                                                     float& m_run, float& l_part, float& alpha, bool& raise) {
   float v[8];
   float bm = -INFINITY;
 #pragma unroll
@@ -224,9 +237,9 @@ __device__ __forceinline__ bf16x8 mla_softmax32(f32x4 s0, f32x4 s1, int tok0, in
   bm = fmaxf(bm, __shfl_xor(bm, 16));
   bm = fmaxf(bm, __shfl_xor(bm, 32));
   // bm is finite (every block has a token); the first block always raises
-  const bool raise = bm > m_run + kRescaleGap;
+  raise = bm > m_run + kRescaleGap;
   const float m_new = raise ? bm : m_run;
-  const float alpha = raise ? __expf(m_run - m_new) : 1.f;
+  alpha = raise ? __expf(m_run - m_new) : 1.f;
   m_run = m_new;
   float pr[8];
   float ps = 0.f;
@@ -239,6 +252,14 @@ __device__ __forceinline__ bf16x8 mla_softmax32(f32x4 s0, f32x4 s1, int tok0, in
   bf16x8 pb;
 #pragma unroll
   for (int i = 0; i < 8; ++i) pb[i] = (__bf16)pr[i];
+  return pb;
+}
+
+__device__ __forceinline__ bf16x8 mla_softmax32(f32x4 s0, f32x4 s1, int tok0, int t1, float scale, int lq,
+                                                f32x4 (&o)[MV / 16], float& m_run, float& l_part) {
+  float alpha;
+  bool raise;
+  const bf16x8 pb = mla_softmax32_core(s0, s1, tok0, t1, scale, lq, m_run, l_part, alpha, raise);
   if (__ballot(raise)) {
 #pragma unroll
     for (int j = 0; j < MV / 16; ++j) o[j] *= alpha;
@@ -447,6 +468,199 @@ __device__ void mla_wg_task(const MlaParams& p, int b, int split, int hg, unsign
   mla_store(p, b, split, hb, lr, lq, o, m_run, l_part);
 }
 
+// ---- 128-head form: one (request, split, group of 8 head blocks) per
+// workgroup, wave w on head blocks 8 g + 2 w and 8 g + 2 w + 1.  Every key
+// fragment read from the tile feeds both head blocks' score chains and every
+// joined value fragment both P.V products, half the LDS reads per head of the
+// 64-head form.  The 256 output accumulators stay in AGPRs (inline-asm
+// MFMAs, with the wait states around their VALU accesses padded explicitly);
+// the rows go from memory straight into three LDS tiles (buffer_load ... lds,
+// two blocks ahead), so no registers stage them.  Per head the operations and
+// their order are those of the 64-head form, so the bits are the same.
+
+// buffer descriptor words (uniform) for the asm loads
+__device__ __forceinline__ i32x4 ml_rsrc_words(const void* base, uint32_t bytes) {
+  const unsigned long long a = (unsigned long long)base;
+  return i32x4{(int)__builtin_amdgcn_readfirstlane((uint32_t)a), (int)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)),
+               (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000};
+}
+
+// 16 bytes per lane from memory into LDS: lane L's bytes land at lds + 16 L.
+// The compiler does not see these loads; their completion is waited for
+// explicitly (ml_vmwait) before the barrier that publishes the tile.
+__device__ __forceinline__ void ml_dma16(uint32_t lds, i32x4 rs, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "s"(lds), "v"(voff), "s"(rs)
+               : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void ml_vmwait() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "i"(N) : "memory");
+}
+
+// acc += a . b with the accumulator in AGPRs
+__device__ __forceinline__ void ml_mfma_acc(f32x4& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// wait states between the asm MFMAs and vector accesses of their accumulators
+// (covers the longest dependency of the 16x16x32 shape)
+__device__ __forceinline__ void ml_mfma_fence() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+// the accumulators materialised in AGPRs at this point of the program
+__device__ __forceinline__ void ml_pin(f32x4 (&o)[2][MV / 16]) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int j = 0; j < MV / 16; ++j) asm volatile("" : "+a"(o[h][j]));
+}
+
+__device__ void mla_wg2_task(const MlaParams& p, int b, int split, int hg, unsigned char* __restrict__ tiles) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int lr = lane & 15, lq = lane >> 4;
+  const int t0 = split * p.split;
+  const int t1 = min(p.S, t0 + p.split);
+  const int nblk = (t1 - t0 + MT2 - 1) / MT2;
+  const int hb0 = hg * MG2 + 2 * wave;
+  // the request's rows; a split is a multiple of 32 tokens, so only the
+  // request's last block is partial and its rows past S_k read as zero
+  const i32x4 rk = ml_rsrc_words(p.kv + (size_t)b * p.S * MD, (uint32_t)p.S * MD * 2u);
+  bf16x8 qf[2][MSTEPS];
+  mla_load_q(p, b, hb0, lr, lq, qf[0]);
+  mla_load_q(p, b, hb0 + 1, lr, lq, qf[1]);
+  f32x4 o[2][MV / 16];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int j = 0; j < MV / 16; ++j) o[h][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  ml_pin(o);
+  ml_mfma_fence();
+  float m_run[2] = {-INFINITY, -INFINITY}, l_part[2] = {0.f, 0.f};
+
+  // load e of this wave fills slots 64 (w + 4 e) .. + 63 of the tile; slot s
+  // is row s / 74, 16-byte chunk s % 74 (chunks 72, 73 and slots past row 31
+  // are padding and read as zero)
+  uint32_t rel[T2_DMA];
+#pragma unroll
+  for (int e = 0; e < T2_DMA; ++e) {
+    const int sl = 64 * (wave + 4 * e) + lane;
+    const int row = sl / T2_ROWSLOTS, ch = sl - row * T2_ROWSLOTS;
+    rel[e] = (row < MT2 && ch < MD / 8) ? (uint32_t)(row * MD + ch * 8) * 2u : kMlOOB;
+  }
+  const uint32_t lds_base = (uint32_t)(size_t)tiles;  // a shared address's low word is its LDS address
+  const uint32_t lds0 = lds_base + 1024u * (uint32_t)wave;
+  auto dma = [&](int blk) {
+    const uint32_t base = (uint32_t)(t0 + blk * MT2) * (uint32_t)(MD * 2);
+    const uint32_t dst = lds0 + (uint32_t)(blk % T2_TILES) * (uint32_t)T2_BYTES;
+#pragma unroll
+    for (int e = 0; e < T2_DMA; ++e) ml_dma16(dst + 4096u * e, rk, rel[e] == kMlOOB ? kMlOOB : base + rel[e]);
+  };
+  dma(0);
+  if (nblk > 1) {
+    dma(1);
+    ml_vmwait<T2_DMA>();
+  } else {
+    ml_vmwait<0>();
+  }
+  __syncthreads();
+  const uint32_t tr0 = (uint32_t)(4 * lq + (lr >> 2)) * K_ROW + 8u * (lr & 3);
+  for (int blk = 0; blk < nblk; ++blk) {
+    // block blk + 2 into the tile block blk - 1 left (every wave passed the
+    // barrier after reading it)
+    if (blk + 2 < nblk) dma(blk + 2);
+    // the tile as an LDS address, so that the constant parts of the fragment
+    // addresses fold into the instructions' offsets
+    lds_u8* tile = reinterpret_cast<lds_u8*>((size_t)(lds_base + (uint32_t)(blk % T2_TILES) * (uint32_t)T2_BYTES));
+    // scores: s[h][half] for the two head blocks and the two 16-row halves
+    lds_u8* krow = tile + (uint32_t)lr * K_ROW + 16u * lq;
+    f32x4 sc[2][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) sc[h][0] = sc[h][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bf16x8 kf[2][2 * KB2];
+    auto kread = [&](int c0, bf16x8 (&k)[2 * KB2]) {
+#pragma unroll
+      for (int c = 0; c < KB2; ++c) {
+        k[2 * c] = *reinterpret_cast<lds_bf16x8*>(krow + 64u * (c0 + c));
+        k[2 * c + 1] = *reinterpret_cast<lds_bf16x8*>(krow + 16u * K_ROW + 64u * (c0 + c));
+      }
+    };
+    kread(0, kf[0]);
+#pragma unroll
+    for (int c0 = 0; c0 < MSTEPS; c0 += KB2) {
+      bf16x8 (&k)[2 * KB2] = kf[(c0 / KB2) & 1];
+      asm volatile("" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]), "+v"(k[4]), "+v"(k[5]));
+      if (c0 + KB2 < MSTEPS) kread(c0 + KB2, kf[((c0 / KB2) + 1) & 1]);
+#pragma unroll
+      for (int c = 0; c < KB2; ++c)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          sc[h][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k[2 * c], qf[h][c0 + c], sc[h][0], 0, 0, 0);
+          sc[h][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k[2 * c + 1], qf[h][c0 + c], sc[h][1], 0, 0, 0);
+        }
+    }
+    bf16x8 pb[2];
+    float alpha[2];
+    bool raise[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      pb[h] = mla_softmax32_core(sc[h][0], sc[h][1], t0 + blk * MT2, t1, p.scale, lq, m_run[h], l_part[h], alpha[h],
+                                 raise[h]);
+    if (__ballot(raise[0] || raise[1])) {
+      ml_mfma_fence();
+      // one accumulator at a time through 4 VGPRs: each read is ordered
+      // after the previous write-back by the empty asms
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < MV / 16; ++j) {
+          asm volatile("" : "+a"(o[h][j]));
+          f32x4 t = o[h][j];
+          asm volatile("" : "+v"(t));
+          t *= alpha[h];
+          o[h][j] = t;
+          asm volatile("" : "+a"(o[h][j]));
+        }
+    }
+    ml_mfma_fence();
+    // P.V: batches of 4 value tiles (8 transposing reads), each joined
+    // fragment used by both head blocks; the next batch's reads in flight
+    // while a batch's 8 MFMAs run
+    auto tread = [&](int jb, i16x4 (&a)[8]) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[2 * u] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(reinterpret_cast<lds_i16x4*>(tile + tr0 + 32u * (jb + u)));
+        a[2 * u + 1] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            reinterpret_cast<lds_i16x4*>(tile + tr0 + 16u * K_ROW + 32u * (jb + u)));
+      }
+    };
+    i16x4 ab[2][8];
+    tread(0, ab[0]);
+#pragma unroll
+    for (int jb = 0; jb < MV / 16; jb += 4) {
+      i16x4 (&cur)[8] = ab[(jb / 4) & 1];
+      asm volatile("" : "+v"(cur[0]), "+v"(cur[1]), "+v"(cur[2]), "+v"(cur[3]), "+v"(cur[4]), "+v"(cur[5]),
+                   "+v"(cur[6]), "+v"(cur[7]));
+      if (jb + 4 < MV / 16) tread(jb + 4, ab[((jb / 4) + 1) & 1]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(cur[2 * u], cur[2 * u + 1], 0, 1, 2, 3,
+                                                                            4, 5, 6, 7));
+        ml_mfma_acc(o[0][jb + u], a, pb[0]);
+        ml_mfma_acc(o[1][jb + u], a, pb[1]);
+      }
+    }
+    // block blk + 1 has landed (block blk + 2's loads may still be in flight)
+    if (blk + 2 < nblk)
+      ml_vmwait<T2_DMA>();
+    else
+      ml_vmwait<0>();
+    __syncthreads();
+  }
+  ml_mfma_fence();
+  mla_store(p, b, split, hb0, lr, lq, o[0], m_run[0], l_part[0]);
+  mla_store(p, b, split, hb0 + 1, lr, lq, o[1], m_run[1], l_part[1]);
+}
+
 __global__ void __launch_bounds__(64 * MW) mla_decode_split(MlaParams p) {
   __shared__ __attribute__((aligned(16))) unsigned char vt_all[MW][V_BYTES];
   __shared__ int box[2];
@@ -520,13 +734,14 @@ __global__ void __launch_bounds__(64 * MW) mla_decode_split(MlaParams p) {
 // with the group fastest (aware) or group major (oblivious).  Oblivious: task
 // i on workgroup i.  Aware: claims of one task, own share first, then the
 // others, as in the wave form.
-__global__ void __launch_bounds__(64 * MG) mla_decode_split_wg(MlaParams p) {
-  __shared__ __attribute__((aligned(16))) unsigned char tiles[2 * K_BYTES];
+template <int FORM>
+__global__ void __launch_bounds__(256) mla_decode_split_wg(MlaParams p) {
+  __shared__ __attribute__((aligned(1024))) unsigned char tiles[FORM == 2 ? T2_TILES * T2_BYTES : 2 * K_BYTES];
   __shared__ int box[1];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const bool aware = p.quota_off != nullptr;
-  const int groups = p.hblocks / MG;
+  const int groups = p.hblocks / (FORM == 2 ? MG2 : MG);
   int own = 0;
   if (aware) {
     uint32_t xr;
@@ -582,7 +797,10 @@ __global__ void __launch_bounds__(64 * MG) mla_decode_split_wg(MlaParams p) {
       split = r % p.n_splits;
       b = r / p.n_splits;
     }
-    mla_wg_task(p, b, split, hg, tiles);
+    if constexpr (FORM == 2)
+      mla_wg2_task(p, b, split, hg, tiles);
+    else
+      mla_wg_task(p, b, split, hg, tiles);
   }
 }
 
@@ -614,14 +832,18 @@ int launch_mla_decode(const MlaLaunch& a, hipStream_t s) {
   p.split = a.split;
   p.n_splits = a.n_splits;
   p.hblocks = (a.Hq + 15) / 16;
-  if (a.wg && p.hblocks % MG) return fail(ASYM_EINVAL, "mla: the workgroup form needs a multiple of 64 heads");
-  p.tasks = a.B * a.n_splits * (a.wg ? p.hblocks / MG : p.hblocks);
+  if (a.form < 0 || a.form > 2) return fail(ASYM_EINVAL, "mla: unknown kernel form");
+  const int per_task = mla_form_head_blocks(a.form);
+  if (p.hblocks % per_task) return fail(ASYM_EINVAL, "mla: the head count does not suit the kernel form");
+  p.tasks = a.B * a.n_splits * (p.hblocks / per_task);
   p.n_x = a.n_x;
   p.scale = a.scale;
   if (a.d_quota_off && (!a.d_claim || a.n_x > 64)) return fail(ASYM_EINVAL, "mla: aware launch without claim counters");
   if (a.grid < 1) return fail(ASYM_EINVAL, "mla: empty grid");
-  if (a.wg)
-    hipLaunchKernelGGL(mla_decode_split_wg, dim3((unsigned)a.grid), dim3(64 * MG), 0, s, p);
+  if (a.form == 2)
+    hipLaunchKernelGGL(mla_decode_split_wg<2>, dim3((unsigned)a.grid), dim3(256), 0, s, p);
+  else if (a.form == 1)
+    hipLaunchKernelGGL(mla_decode_split_wg<1>, dim3((unsigned)a.grid), dim3(256), 0, s, p);
   else
     hipLaunchKernelGGL(mla_decode_split, dim3((unsigned)a.grid), dim3(64 * MW), 0, s, p);
   ASYM_HIP(hipGetLastError());
@@ -636,6 +858,6 @@ int launch_mla_decode(const MlaLaunch& a, hipStream_t s) {
 
 int mla_tasks_per_workgroup() { return MW; }
 
-int mla_wg_head_blocks() { return MG; }
+int mla_form_head_blocks(int form) { return form == 2 ? MG2 : form == 1 ? MG : 1; }
 
 }  // namespace asym

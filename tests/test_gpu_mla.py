@@ -118,8 +118,15 @@ def test_mla_decode_paper_sizes_sampled(dev, B, Hq, S):
 def test_mla_plan_shares_and_rejections(dev, topo):
     full = asym.mla_decode_plan(16, 128, 32768, topo=topo)
     # 128 heads: the workgroup form, one task per (request, split, 4 head blocks)
-    assert full["head_blocks"] == 8 and full["workgroup_form"] == 1 and full["tasks_per_workgroup"] == 1
-    assert full["tasks"] == 16 * 2 * full["n_splits"]
+    assert full["head_blocks"] == 8 and full["workgroup_form"] == 2 and full["tasks_per_workgroup"] == 1
+    assert full["tasks"] == 16 * full["n_splits"]
+    h64 = asym.mla_decode_plan(16, 64, 32768, topo=topo)
+    assert h64["workgroup_form"] == 1 and h64["tasks"] == 16 * h64["n_splits"]
+    # the 128-head form only where its tasks outnumber half the CUs
+    one = asym.mla_decode_plan(1, 128, 32768, topo=topo)
+    assert one["workgroup_form"] == 1 and 2 * one["n_splits"] <= 256
+    wide = asym.mla_decode_plan(64, 128, 4096, topo=topo)
+    assert wide["workgroup_form"] == 2 and 2 * wide["tasks"] > 256
     small = asym.mla_decode_plan(16, 16, 32768, topo=topo)
     assert small["workgroup_form"] == 0 and small["tasks"] == 16 * small["n_splits"]
     assert sum(full["tasks_per_xcd"]) == full["tasks"] and max(full["tasks_per_xcd"]) - min(full["tasks_per_xcd"]) <= 1
@@ -152,40 +159,53 @@ def test_mla_plan_shares_and_rejections(dev, topo):
 
 
 @pytest.mark.parametrize("B,Hq,S,split", [(2, 64, 515, 0), (1, 128, 200, 0), (3, 128, 1000, 64), (1, 64, 17, 0),
-                                          (2, 192, 4111, 1024), (4, 128, 8192, 0), (2, 64, 100, 32)])
+                                          (2, 192, 4111, 1024), (4, 128, 8192, 0), (2, 64, 100, 32),
+                                          (2, 256, 333, 0), (1, 128, 31, 32), (2, 128, 4096, 32)])
 def test_mla_workgroup_form(dev, topo, B, Hq, S, split):
-    """At multiples of 64 heads the workgroup form runs (four head blocks
+    """At multiples of 64 heads a workgroup form runs (four head blocks
     sharing each 32-token block of rows through LDS, one softmax step per 32
-    tokens, 32-deep P.V products).  It rounds differently from the wave form
-    (16-token blocks): both are checked against the oracle, on every head of
-    the small shapes and on sampled heads of the long ones, and the workgroup
-    form's bits are the same on every mapping and on a CU-masked stream."""
+    tokens, 32-deep P.V products); at multiples of 128 the 128-head form (two
+    head blocks per wave, rows loaded straight into LDS), which gives the
+    64-head form's bits.  The workgroup forms round differently from the wave
+    form (16-token blocks): both are checked against the oracle, on every head
+    of the small shapes and on sampled heads of the long ones, and the
+    workgroup form's bits are the same on every mapping and on a CU-masked
+    stream."""
     p = workloads.MlaProblem(f"wg{B}_{Hq}_{S}", B, Hq, S, seed=S + 3 * Hq)
     q, kv = workloads.make_mla_inputs(p)
     qd, kvd = q.to(dev), kv.to(dev)
-    lse_w, lse_g = (torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(2))
-    assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == 1
-    prev = asym.set_mla_workgroup_form(False)
+    lse_w, lse_g, lse_1 = (torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(3))
+    form = 2 if Hq % 128 == 0 else 1
+    # level 3: the 128-head form wherever the head count allows (by default it
+    # runs only where its tasks fill the CU set, which these small shapes do not)
+    prev = asym.set_mla_workgroup_form(3)
     try:
+        assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == form
+        got = asym.mla_decode(qd, kvd, lse=lse_g, split_tokens=split, topo=topo)
+        torch.cuda.synchronize()
+        for m in MAPS[1:]:
+            O = asym.mla_decode(qd, kvd, split_tokens=split, mapping=m, topo=topo)
+            torch.cuda.synchronize()
+            assert torch.equal(O, got), m
+        mask = workloads.random_mask_bits(4, 1, 128)[0]
+        s = asym.stream_create(topo, mask)
+        try:
+            O = asym.mla_decode(qd, kvd, split_tokens=split, topo=topo, stream=s)
+            s.synchronize()
+            assert torch.equal(O, got), "masked"
+        finally:
+            asym.stream_destroy(s)
+        asym.set_mla_workgroup_form(1)
+        assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == 1
+        form1 = asym.mla_decode(qd, kvd, lse=lse_1, split_tokens=split, topo=topo)
+        torch.cuda.synchronize()
+        asym.set_mla_workgroup_form(0)
         assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == 0
         wave = asym.mla_decode(qd, kvd, lse=lse_w, split_tokens=split, topo=topo)
         torch.cuda.synchronize()
     finally:
         asym.set_mla_workgroup_form(prev)
-    got = asym.mla_decode(qd, kvd, lse=lse_g, split_tokens=split, topo=topo)
-    torch.cuda.synchronize()
-    for m in MAPS[1:]:
-        O = asym.mla_decode(qd, kvd, split_tokens=split, mapping=m, topo=topo)
-        torch.cuda.synchronize()
-        assert torch.equal(O, got), m
-    mask = workloads.random_mask_bits(4, 1, 128)[0]
-    s = asym.stream_create(topo, mask)
-    try:
-        O = asym.mla_decode(qd, kvd, split_tokens=split, topo=topo, stream=s)
-        s.synchronize()
-        assert torch.equal(O, got), "masked"
-    finally:
-        asym.stream_destroy(s)
+    assert torch.equal(got, form1) and torch.equal(lse_g, lse_1), "128-head form against the 64-head form"
     heads = None if B * Hq * S <= 200_000 else sorted(set([0, Hq - 1, Hq // 2, 17 % Hq]))
     check(q, kv, got, lse_g, p.scale, f"mla workgroup form B{B} H{Hq} S{S}", heads=heads)
     check(q, kv, wave, lse_w, p.scale, f"mla wave form B{B} H{Hq} S{S}", heads=heads)

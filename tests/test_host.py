@@ -498,3 +498,22 @@ def test_noalloc_rejections_need_no_device(lib):
     assert lib_.asym_gemm_bf16_noalloc(t.handle, side, side, 8, P, 8, P, 8, 0, P, side, 0, 0, None) == \
         asym.EINVAL
     assert "output tiles" in asym.last_error()
+
+
+def test_mla_form_level_switch(lib):
+    """The latent-attention kernel-form level round-trips (0 wave form only,
+    1 up to the 64-head form, 2 the default, 3 the 128-head form wherever it
+    fits) and other levels are refused without changing it."""
+    prev = asym.set_mla_workgroup_form(1)
+    try:
+        assert prev == 2
+        assert asym.set_mla_workgroup_form(False) == 1
+        assert asym.set_mla_workgroup_form(True) == 0
+        assert asym.set_mla_workgroup_form(3) == 2
+        assert lib.asym_mla_set_workgroup_form(4) == asym.EINVAL
+        assert lib.asym_mla_set_workgroup_form(-1) == asym.EINVAL
+        with pytest.raises(asym.AsymError):
+            asym.set_mla_workgroup_form(7)
+        assert asym.set_mla_workgroup_form(2) == 3
+    finally:
+        asym.set_mla_workgroup_form(prev)
