@@ -1069,7 +1069,7 @@ static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
     while (L > 32 && (int64_t)B * hb * ((S + L - 1) / L) < 1024) L /= 2;
     while (L < 1024 && (S + L - 1) / L > 256) L *= 2;
   }
-  const int64_t n_splits = (S + L - 1) / L;
+  int64_t n_splits = (S + L - 1) / L;
   // the workgroup forms share each block's rows among 4 or 8 head blocks
   // (one task per workgroup); the wave form runs one head block per wave.
   // The 128-head form does a task's blocks faster, but has half the 64-head
@@ -1084,6 +1084,16 @@ static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
                    : allow >= 2 && fits128 && 2 * t128 > set_cus ? 2
                    : allow >= 1 && hb % mla_form_head_blocks(1) == 0 ? 1
                                                                       : 0;
+  // a workgroup-form task is 4 or 8 head blocks: with automatic splits, they
+  // are lengthened (up to 8192 tokens) while at least two tasks per CU of
+  // the set remain.  The fp32 partials shrink with the split count (at B=64,
+  // 128 heads, 32K tokens: 537 MB for 32 splits, beyond the memory-side
+  // cache, against 134 MB for 8)
+  if (form != 0 && !split_in) {
+    const int64_t groups = hb / mla_form_head_blocks(form);
+    while (L < 8192 && (int64_t)B * ((S + 2 * L - 1) / (2 * L)) * groups >= 2ll * P->cs.total) L *= 2;
+    n_splits = (S + L - 1) / L;
+  }
   const int64_t tasks = (int64_t)B * n_splits * (hb / mla_form_head_blocks(form));
   if (tasks > (1ll << 30)) return fail(ASYM_EINVAL, "mla: too many tasks");
   P->split = L;
