@@ -74,7 +74,7 @@ constexpr int T2_ROWSLOTS = K_ROW / 16;  // 16-byte slots of a tile row (72 of t
 constexpr int T2_DMA = 10;         // 128-head form: 1 KiB direct-to-LDS loads per wave per block
 constexpr int T2_BYTES = 4 * T2_DMA * 1024;  // 40 KiB per tile (2368 slots used), three tiles
 constexpr int T2_TILES = 3;
-constexpr int KB2 = 3;             // 128-head form: score steps per batch of key-fragment reads
+constexpr int KB2 = 2;             // 128-head form: score steps per batch of key-fragment reads
 static_assert(4 * T2_DMA * 64 >= MT2 * T2_ROWSLOTS, "a block's slots must fit the loads");
 constexpr uint32_t kMlOOB = 0x80000000u;
 constexpr int kMlClaimStride = 64;  // ints between claim counters (256-byte lines)
@@ -131,6 +131,17 @@ __device__ __forceinline__ void mla_task_of(const MlaParams& p, bool aware, int 
   }
 }
 
+// The maximum over the four lanes l, l ^ 16, l ^ 32, l ^ 48: each row swap
+// (v_permlane16_swap, v_permlane32_swap) of a value with itself leaves every
+// lane the pair {x[l], x[l ^ 16]} (then ^ 32) in its two results; in the
+// vector unit, with no LDS round trip.  A maximum is exact in any order.
+__device__ __forceinline__ float ml_max4(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // ---- the arithmetic of one 16-token block, shared by both forms ----------
 // Scores S^T (16 tokens x 16 heads) = K . Q^T: lane (lr, lq) gets tokens
 // 4 lq .. 4 lq + 3 of the block, head lr.
@@ -161,8 +172,7 @@ __device__ __forceinline__ i16x4 mla_softmax(f32x4 s, int tok0, int t1, float sc
     v[i] = tok < t1 ? s[i] * scale : -INFINITY;
     bm = fmaxf(bm, v[i]);
   }
-  bm = fmaxf(bm, __shfl_xor(bm, 16));
-  bm = fmaxf(bm, __shfl_xor(bm, 32));
+  bm = ml_max4(bm);
   // bm is finite (every block has a token); the first block always raises
   const bool raise = bm > m_run + kRescaleGap;
   const float m_new = raise ? bm : m_run;
@@ -234,8 +244,7 @@ __device__ __forceinline__ bf16x8 mla_softmax32_core(f32x4 s0, f32x4 s1, int tok
     v[i] = tok < t1 ? (i < 4 ? s0[i] : s1[i - 4]) * scale : -INFINITY;
     bm = fmaxf(bm, v[i]);
   }
-  bm = fmaxf(bm, __shfl_xor(bm, 16));
-  bm = fmaxf(bm, __shfl_xor(bm, 32));
+  bm = ml_max4(bm);
   // bm is finite (every block has a token); the first block always raises
   raise = bm > m_run + kRescaleGap;
   const float m_new = raise ? bm : m_run;
@@ -571,12 +580,14 @@ __device__ void mla_wg2_task(const MlaParams& p, int b, int split, int hg, unsig
     // the tile as an LDS address, so that the constant parts of the fragment
     // addresses fold into the instructions' offsets
     lds_u8* tile = reinterpret_cast<lds_u8*>((size_t)(lds_base + (uint32_t)(blk % T2_TILES) * (uint32_t)T2_BYTES));
-    // scores: s[h][half] for the two head blocks and the two 16-row halves
+    // scores: s[h][half] for the two head blocks and the two 16-row halves;
+    // key fragments in batches of KB2 steps of both halves, three batches
+    // deep (a batch's reads issued two batches before its MFMAs)
     lds_u8* krow = tile + (uint32_t)lr * K_ROW + 16u * lq;
     f32x4 sc[2][2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) sc[h][0] = sc[h][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bf16x8 kf[2][2 * KB2];
+    bf16x8 kf[3][2 * KB2];
     auto kread = [&](int c0, bf16x8 (&k)[2 * KB2]) {
 #pragma unroll
       for (int c = 0; c < KB2; ++c) {
@@ -585,11 +596,13 @@ __device__ void mla_wg2_task(const MlaParams& p, int b, int split, int hg, unsig
       }
     };
     kread(0, kf[0]);
+    kread(KB2, kf[1]);
 #pragma unroll
     for (int c0 = 0; c0 < MSTEPS; c0 += KB2) {
-      bf16x8 (&k)[2 * KB2] = kf[(c0 / KB2) & 1];
-      asm volatile("" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]), "+v"(k[4]), "+v"(k[5]));
-      if (c0 + KB2 < MSTEPS) kread(c0 + KB2, kf[((c0 / KB2) + 1) & 1]);
+      bf16x8 (&k)[2 * KB2] = kf[(c0 / KB2) % 3];
+      static_assert(KB2 == 2, "the empty asm below names the batch's four fragments");
+      asm volatile("" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]));
+      if (c0 + 2 * KB2 < MSTEPS) kread(c0 + 2 * KB2, kf[((c0 / KB2) + 2) % 3]);
 #pragma unroll
       for (int c = 0; c < KB2; ++c)
 #pragma unroll
@@ -623,8 +636,8 @@ __device__ void mla_wg2_task(const MlaParams& p, int b, int split, int hg, unsig
     }
     ml_mfma_fence();
     // P.V: batches of 4 value tiles (8 transposing reads), each joined
-    // fragment used by both head blocks; the next batch's reads in flight
-    // while a batch's 8 MFMAs run
+    // fragment used by both head blocks; the next two batches' reads in
+    // flight while a batch's 8 MFMAs run
     auto tread = [&](int jb, i16x4 (&a)[8]) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -633,14 +646,15 @@ __device__ void mla_wg2_task(const MlaParams& p, int b, int split, int hg, unsig
             reinterpret_cast<lds_i16x4*>(tile + tr0 + 16u * K_ROW + 32u * (jb + u)));
       }
     };
-    i16x4 ab[2][8];
+    i16x4 ab[3][8];
     tread(0, ab[0]);
+    tread(4, ab[1]);
 #pragma unroll
     for (int jb = 0; jb < MV / 16; jb += 4) {
-      i16x4 (&cur)[8] = ab[(jb / 4) & 1];
+      i16x4 (&cur)[8] = ab[(jb / 4) % 3];
       asm volatile("" : "+v"(cur[0]), "+v"(cur[1]), "+v"(cur[2]), "+v"(cur[3]), "+v"(cur[4]), "+v"(cur[5]),
                    "+v"(cur[6]), "+v"(cur[7]));
-      if (jb + 4 < MV / 16) tread(jb + 4, ab[((jb / 4) + 1) & 1]);
+      if (jb + 8 < MV / 16) tread(jb + 8, ab[((jb / 4) + 2) % 3]);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(cur[2 * u], cur[2 * u + 1], 0, 1, 2, 3,
