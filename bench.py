@@ -1119,7 +1119,8 @@ def mla_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 
     return {"configs": out, "uneven_cu_sets": uneven}
 
 
-FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "attention_b1", "chunk_read", "mla", "mla16", "copy")
+FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "attention_b1", "chunk_read", "mla", "mla_long", "mla16",
+         "copy")
 
 
 def focus_run(name: str, dev, stream, launches: int) -> dict:
@@ -1130,6 +1131,7 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
       attention_b1     decode attention, grouped-query, B = 1, S_k = 32768 (latency-bound)
       chunk_read       strided read of a 16 GiB region in 8 KiB chunks, address order
       mla              latent-attention decode, B = 64, H_q = 128, S_k = 8192 (aware)
+      mla_long         latent-attention decode, B = 64, H_q = 128, S_k = 32768 (aware)
       mla16            latent-attention decode, B = 64, H_q = 16, S_k = 32768 (aware)
       copy             the streaming copy, 64 MiB, one pass, whole chip
     Reports the mean per launch (HIP events on the launch stream) and the
@@ -1166,13 +1168,13 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
         fn = lambda: asym.attn_decode(q, k, v, o, stream=stream)
         nbytes = p.kv_bytes + 2 * 2 * q.numel()
         kernel = "attn_decode_split<4, false> + attn_decode_merge"
-    elif name == "mla":
-        p = workloads.mla_problem(64, 128, 8192)
+    elif name in ("mla", "mla_long"):
+        p = workloads.mla_problem(64, 128, 8192 if name == "mla" else 32768)
         q, kv = workloads.make_mla_inputs_on(p, dev)
         o = torch.empty((64, 128, 512), dtype=torch.bfloat16, device=dev)
         fn = lambda: asym.mla_decode(q, kv, o, stream=stream)
         nbytes = p.kv_bytes + 2 * q.numel() + 2 * o.numel()
-        kernel = "mla_decode_split + mla_decode_merge"
+        kernel = "mla_decode_split_wg<2> + mla_decode_merge"
     elif name == "mla16":
         p = workloads.mla_problem(64, 16, 32768)
         q, kv = workloads.make_mla_inputs_on(p, dev)
