@@ -13,7 +13,12 @@ the next lgkmcnt(0).  The accumulators have the same problem with the
 inline-asm MFMAs that write them: reading them needs the wait states of the
 kernel's MFMA fence (`s_nop 7` x 3), which the compiler does not know about, so
 no instruction the compiler places may touch an accumulator register between
-an MFMA and the fence.
+an MFMA and the fence.  The other direction, an accumulator the compiler writes
+(zeroing, a rescale) and an inline-asm MFMA that then reads it, needs a few
+wait states too: every path from such a write to such an MFMA must carry at
+least `MIN_WRITE_TO_MFMA` of them.  Both checks also run over the latent-
+attention decode kernel whose 128-head form keeps its outputs in AGPRs
+through inline-asm MFMAs.
 """
 import os
 import re
@@ -156,16 +161,69 @@ def inflight_violations(asm: str, kernel: str):
     return v
 
 
-@pytest.fixture(scope="module")
-def gemm_asm(tmp_path_factory):
-    out = tmp_path_factory.mktemp("asm") / "gemm.s"
+def _compile(tmp_path_factory, src):
+    out = tmp_path_factory.mktemp("asm") / (src + ".s")
     cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"),
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
            "-mllvm", "-amdgpu-mfma-vgpr-form=1",
-           "--cuda-device-only", "-S", os.path.join(CSRC, "gemm.hip"), "-o", str(out)]
+           "--cuda-device-only", "-S", os.path.join(CSRC, src), "-o", str(out)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
     return out.read_text()
+
+
+@pytest.fixture(scope="module")
+def gemm_asm(tmp_path_factory):
+    return _compile(tmp_path_factory, "gemm.hip")
+
+
+@pytest.fixture(scope="module")
+def mla_asm(tmp_path_factory):
+    return _compile(tmp_path_factory, "mla_decode.hip")
+
+
+MLA_128 = "_ZN4asym12_GLOBAL__N_119mla_decode_split_wgILi2EEEvNS0_9MlaParamsE"
+MIN_WRITE_TO_MFMA = 4
+
+
+def write_to_mfma_violations(asm: str, kernel: str):
+    """Inline-asm MFMAs reached from a compiler-placed v_accvgpr_write by a
+    path of fewer than MIN_WRITE_TO_MFMA wait states (s_nop n counts n + 1,
+    any other instruction 1).  Dataflow over the control-flow graph: the
+    state is the fewest wait states since such a write on any path."""
+    blocks = blocks_of(asm, kernel)
+    succ = successors(blocks)
+    inf = 10 ** 9
+
+    def tr(block, ws, out=None):
+        for inst, is_asm in block["insts"]:
+            mn = inst.split()[0]
+            if is_asm and mn.startswith("v_mfma"):
+                if ws < MIN_WRITE_TO_MFMA and out is not None:
+                    out.append((block["label"], inst, ws))
+                ws = min(inf, ws + 1)
+            elif not is_asm and mn == "v_accvgpr_write_b32":
+                ws = 0
+            elif mn == "s_nop":
+                ws = min(inf, ws + int(inst.split()[1]) + 1)
+            else:
+                ws = min(inf, ws + 1)
+        return ws
+
+    ins = [inf] * len(blocks)
+    changed = True
+    while changed:
+        changed = False
+        for i, b in enumerate(blocks):
+            o = tr(b, ins[i])
+            for j in succ[i]:
+                if o < ins[j]:
+                    ins[j] = o
+                    changed = True
+    v = []
+    for i, b in enumerate(blocks):
+        tr(b, ins[i], v)
+    return v
 
 
 @pytest.mark.parametrize("trace", [0, 1])
@@ -174,6 +232,45 @@ def test_no_use_of_fragments_in_flight(gemm_asm, nbf, trace):
     kernel = f"_ZN4asym12_GLOBAL__N_120gemm_bf16_persistentILb1ELi{nbf}ELi0ELb{trace}EEEvNS0_6ParamsE"
     v = inflight_violations(gemm_asm, kernel)
     assert not v, f"{len(v)} instructions touch fragment registers still being read, e.g. {v[:4]}"
+
+
+def test_mla_outputs_fenced(mla_asm):
+    """The 128-head latent-attention kernel: no compiler-placed access of an
+    output accumulator between an asm MFMA and the fence."""
+    v = inflight_violations(mla_asm, MLA_128)
+    assert not v, f"{len(v)} accumulator accesses before the MFMA fence, e.g. {v[:4]}"
+
+
+@pytest.mark.parametrize("which", ["gemm8", "gemm7", "gemm6", "gemm8_trace", "mla128"])
+def test_accumulator_writes_reach_asm_mfmas_late_enough(gemm_asm, mla_asm, which):
+    if which == "mla128":
+        asm, kernel = mla_asm, MLA_128
+    else:
+        nbf, trace = int(which[4]), int(which.endswith("trace"))
+        asm, kernel = gemm_asm, f"_ZN4asym12_GLOBAL__N_120gemm_bf16_persistentILb1ELi{nbf}ELi0ELb{trace}EEEvNS0_6ParamsE"
+    v = write_to_mfma_violations(asm, kernel)
+    assert not v, f"{len(v)} asm MFMAs too soon after an accumulator write, e.g. {v[:3]}"
+
+
+def test_write_to_mfma_rule_sees_a_short_path():
+    """A write two instructions before an asm MFMA on one branch is flagged;
+    with a fence in between it is not."""
+    bad = """k:
+\tv_accvgpr_write_b32 a0, 0
+\ts_cbranch_scc1 .LBB0_2
+.LBB0_1:
+\ts_nop 7
+.LBB0_2:
+\t;;#ASMSTART
+\tv_mfma_f32_16x16x32_bf16 a[0:3], v[0:3], v[4:7], a[0:3]
+\t;;#ASMEND
+\ts_endpgm
+.Lfunc_end0:
+"""
+    v = write_to_mfma_violations(bad, "k")
+    assert len(v) == 1 and v[0][2] == 1
+    good = bad.replace("\ts_cbranch_scc1 .LBB0_2\n", "\ts_nop 7\n\ts_cbranch_scc1 .LBB0_2\n")
+    assert write_to_mfma_violations(good, "k") == []
 
 
 def test_checker_sees_a_planted_copy():
