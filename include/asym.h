@@ -680,9 +680,11 @@ typedef struct asym_gemm_plan_info {
   int vector_path;
   int n_xcds;
   int workers_per_xcd[ASYM_MAX_XCDS]; /* persistent kernel only (0 on the small-M path) */
-  int small_m;     /* 1: the small-M kernel (a plain launch of 64-column tiles,
-                      tile_m = 16, 32 or 64 rows, each wave 16 columns over all of K;
-                      grid = workgroups in the mapping's order) */
+  int small_m;     /* 1: the small-M kernel (a plain launch of column tiles of
+                      tile_n = 64 columns, or 8 to 56 for one unsplit row tile with
+                      fewer 64-column tiles than CUs; tile_m = 16, 32 or 64 rows,
+                      each wave 16 columns over all of K; grid = workgroups in the
+                      mapping's order) */
   int k_splits;    /* small-M kernel with one row tile and fewer 64-column tiles
                       than the device has CUs: K is cut into this many ranges, one
                       workgroup each, and a second launch adds the fp32 partial
@@ -705,9 +707,12 @@ int asym_gemm_plan(const asym_topology* topo, int M, int N, int K,
  * the row tiles that read one B panel one after another on one XCD (the panel
  * crosses into its L2 once), the oblivious orders put them on neighbouring
  * workgroups (column-major, different XCDs) or a row of tiles apart
- * (row-major).  Every order gives bitwise the same result.  Each workgroup computes 64 columns of C for all rows; each of its
- * four waves streams its 16 rows of B over all of K straight into MFMA
- * operands, with A shared through LDS.  This call
+ * (row-major).  Every order gives bitwise the same result.  Each workgroup
+ * computes 64 columns of C for all rows (a single unsplit row tile with fewer
+ * 64-column tiles than the device has CUs takes narrower tiles, a multiple of
+ * 8 columns giving about one per CU; the same bits); each of its four waves
+ * streams its 16 rows of B over all of K straight into MFMA operands, with A
+ * shared through LDS.  This call
  * switches the path on or off for the whole process (default on; off sends
  * such products to the persistent kernel, for comparison) and returns the
  * previous setting.  Not synchronised with launches in flight. */

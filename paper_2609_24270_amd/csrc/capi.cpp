@@ -303,6 +303,20 @@ int small_m_ksplit(int M, int N, int K, int mb, int device_cus) {
   return ks;
 }
 
+// A single unsplit row tile whose 64-column tiles number fewer than the CUs
+// narrows them, to the multiple of 8 columns that gives about one tile per CU:
+// each CU then reads at most that many columns of B, and a CU reads HBM at
+// about 20-24 GB/s at most (the decode projection 32 x 14336 x 4096: 224 tiles
+// of 64 columns leave 32 CUs idle; 256 of 56 use them all).  A narrower wave or
+// an idle one at a tile's edge is the same case as the product's edge, and each
+// output is still one wave's MFMA chain over all of K: the bits do not change.
+int small_m_cols(int N, int row_tiles, int ksplit, int device_cus) {
+  const int w = small_m_tile_cols();
+  if (row_tiles != 1 || ksplit != 1 || device_cus < 1) return w;
+  if ((N + w - 1) / w >= device_cus) return w;
+  return std::min(w, 8 * ((N + 8 * device_cus - 1) / (8 * device_cus)));
+}
+
 // The CU set a launch on `stream` may use: the device's topology (probed on
 // first use unless given), the stream's per-XCD CU counts, and the workers per
 // XCD after an optional whole-XCD restriction (one per CU).
@@ -446,9 +460,10 @@ static SmallMLaunch small_m_launch(const GemmPlan& P, const void* A, const void*
   sm.row_tiles = (M + 16 * P.small_mb - 1) / (16 * P.small_mb);
   sm.order = small_m_order(mapping);
   sm.n_x = P.t->n_xccs;
-  const int tiles_n = (N + small_m_tile_cols() - 1) / small_m_tile_cols();
-  sm.grid = small_m_grid(sm.row_tiles, tiles_n, sm.order, sm.n_x);
   sm.ksplit = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
+  sm.tile_cols = small_m_cols(N, sm.row_tiles, sm.ksplit, P.t->n_cus);
+  const int tiles_n = (N + sm.tile_cols - 1) / sm.tile_cols;
+  sm.grid = small_m_grid(sm.row_tiles, tiles_n, sm.order, sm.n_x);
   if (sm.ksplit > 1) sm.grid = (long long)tiles_n * sm.ksplit;
   return sm;
 }
@@ -1205,11 +1220,11 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
   if (P.small_mb) {
     out->vector_path = 1;
     out->tile_m = 16 * P.small_mb;
-    out->tile_n = small_m_tile_cols();
     out->tiles_m = (M + out->tile_m - 1) / out->tile_m;
+    out->k_splits = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
+    out->tile_n = small_m_cols(N, out->tiles_m, out->k_splits, P.t->n_cus);
     out->tiles_n = (N + out->tile_n - 1) / out->tile_n;
     out->grid = (int)small_m_grid(out->tiles_m, out->tiles_n, small_m_order(mapping), P.t->n_xccs);
-    out->k_splits = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
     if (out->k_splits > 1) out->grid = out->tiles_n * out->k_splits;
     out->workers = out->grid;
     out->claims = 0;

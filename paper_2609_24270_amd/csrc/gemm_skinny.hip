@@ -52,6 +52,7 @@ struct SkinnyParams {
   int order;          // plain GEMM: 0 aware, 1 column-major, 2 row-major
   int n_x;            // XCDs (workgroup i runs on XCD i mod n_x)
   const int4* desc;   // grouped: per workgroup {first row, rows, first B row, first column}; rows 0 = none
+  int tile_cols;      // plain GEMM: columns per column tile (a multiple of 8, at most 64; grouped: 64)
   int ksplit;         // plain GEMM, one row tile: K ranges per column tile (1 = none)
   float* part;        // ksplit > 1: fp32 partial tiles [column tile][range][16 MB][64]
 };
@@ -111,12 +112,13 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
     row0 = r * 16 * MB;
     rows = min(16 * MB, p.M - row0);
     brow0 = 0;
-    ncol0 = c * SK_COLS;
+    ncol0 = c * p.tile_cols;
     ctile = c;
   }
-  // this wave's 16 columns; a wave past N has an empty B range and stores nothing
+  // this wave's 16 columns (fewer at the tile's or the product's edge); a wave
+  // past either has an empty B range and stores nothing
   const int n0 = ncol0 + wave * 16;
-  const int cols = max(0, min(16, p.N - n0));
+  const int cols = max(0, min(16, min(p.N, ncol0 + p.tile_cols) - n0));
 
   // rows past the tile read as zero (outside the resource); a 16-byte chunk at
   // k >= K is sent out of range (K is a multiple of 8: a chunk is all inside
@@ -284,7 +286,11 @@ int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s) {
   p.lda = g.lda;
   p.ldb = g.ldb;
   p.ldc = g.ldc;
-  p.tiles_n = (g.N + SK_COLS - 1) / SK_COLS;
+  if (g.tile_cols < 8 || g.tile_cols > SK_COLS || g.tile_cols % 8 || (g.d_desc && g.tile_cols != SK_COLS) ||
+      (g.ksplit > 1 && g.tile_cols != SK_COLS))
+    return fail(ASYM_EINVAL, "small-M GEMM: column tiles of 8 to 64 columns (64 when grouped or split)");
+  p.tile_cols = g.tile_cols;
+  p.tiles_n = (g.N + g.tile_cols - 1) / g.tile_cols;
   p.row_tiles = g.row_tiles;
   p.order = g.order;
   p.n_x = g.n_x;

@@ -117,12 +117,14 @@ struct SmallMLaunch {
   int n_x = 8;                  // XCDs
   long long grid = 0;           // workgroups
   const void* d_desc = nullptr; // grouped: device int4 per workgroup {row, rows, B row, column}
+  int tile_cols = 64;           // columns per column tile: a multiple of 8 up to 64 (plain, unsplit)
   int ksplit = 1;               // plain, one row tile: K ranges per column tile
   float* part = nullptr;        // ksplit > 1: [column tiles][ksplit][16 mb][64] fp32
 };
 int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s);
 int small_m_blocks(int max_rows);  // 1, 2, 4, or 0 above 64 rows
-int small_m_tile_cols();
+int small_m_tile_cols();           // the widest column tile (64)
+int small_m_cols(int N, int row_tiles, int ksplit, int device_cus);  // the width a plain launch takes
 
 // Decode attention (head dimension 128).
 struct AttnLaunch {

@@ -257,3 +257,37 @@ def test_split_k_under_an_xcd_restriction(dev):
             e2 = assert_gemm_close(C2, R, what="XCDs 6-7, persistent kernel")
             print(f"32x4096x4096: split {e1:.3e}, restricted {e2:.3e}, "
                   f"bitwise equal share {float(np.mean(C1 == C2)):.4f}")
+
+
+@pytest.mark.parametrize("M,N,K,width", [(32, 14336, 4096, 56), (32, 10240, 4096, 40), (40, 3000, 200, 16)])
+def test_narrow_column_tiles(dev, M, N, K, width):
+    """A single unsplit row tile with fewer 64-column tiles than CUs takes
+    narrower tiles (a multiple of 8 columns, about one per CU; a wave of 8
+    columns or an idle one at the tile's edge).  On exact-integer inputs it
+    equals the oracle and the persistent kernel bitwise; on real-valued ones
+    every mapping gives the same bits and sampled columns match the oracle."""
+    ncu = asym.device_query(0)["n_cus"]
+    p = workloads.make_problem(M, N, K, seed=N + K, dist="int")
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    plan = asym.gemm_plan(A=Ad, B=Bd)
+    assert plan["small_m"] == 1 and plan["k_splits"] == 1, plan
+    if ncu == 256:
+        assert plan["tile_n"] == width and plan["tiles_n"] == (N + width - 1) // width, plan
+    small = bits(asym.gemm(Ad, Bd))
+    prev = asym.set_small_m(False)
+    try:
+        pers = bits(asym.gemm(Ad, Bd))
+    finally:
+        asym.set_small_m(prev)
+    _, Co = oracle.gemm_bf16(bits(A), bits(B), "nk")
+    assert np.array_equal(small, Co) and np.array_equal(pers, Co)
+    p = workloads.make_problem(M, N, K, seed=N + K + 1)
+    A, B = workloads.make_inputs(p)
+    Ad, Bd = A.to(dev), B.to(dev)
+    outs = [bits(asym.gemm(Ad, Bd, mapping=m)) for m in MAPS]
+    assert all(np.array_equal(outs[0], o) for o in outs[1:])
+    g = np.random.default_rng(N)
+    cols = np.unique(np.concatenate([g.choice(N, min(N, 400), replace=False), np.arange(N - width, N)]))
+    R, _ = oracle.gemm_bf16(bits(A), bits(B)[cols], "nk")
+    assert_gemm_close(outs[0][:, cols], R, what=f"{M}x{N}x{K} in {width}-column tiles")
