@@ -409,6 +409,39 @@ def grid_study(topo, dev, stream, launches: int = 20, settle_s: float = 1.0) -> 
     return out
 
 
+LARGE_SHAPES = ((16384, 16384, 16384), (16384, 15360, 16384), (12288, 12288, 12288))
+
+
+def large_study(topo, dev, stream, launches: int = 6, settle_s: float = 1.0) -> list:
+    """Products whose operands (384-512 MiB each) exceed the 256 MB memory-side
+    cache, so that L2 misses are served from HBM: the three mappings,
+    interleaved, `launches` each after `settle_s` of settling launches; inputs
+    uniform[-1, 1] drawn on the GPU from seed 1 (A, then B)."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    out = []
+    for (M, N, K) in LARGE_SHAPES:
+        g = torch.Generator(device=dev).manual_seed(1)
+        Ad = (torch.rand((M, K), generator=g, device=dev) * 2 - 1).to(torch.bfloat16)
+        Bd = (torch.rand((N, K), generator=g, device=dev) * 2 - 1).to(torch.bfloat16)
+        C = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        fns = {m: (lambda m=m: asym.gemm(Ad, Bd, C, mapping=m, topo=topo, stream=stream)) for m in MAPPINGS}
+        plan = asym.gemm_plan(Ad, Bd, C, mapping="aware", topo=topo, stream=stream)
+        for f in fns.values():
+            f()
+        settle(list(fns.values()), settle_s)
+        ms = interleaved(fns, launches, stream)
+        flops = 2.0 * M * N * K
+        out.append({"M": M, "N": N, "K": K, "tile_n": plan["tile_n"], "tiles": [plan["tiles_m"], plan["tiles_n"]],
+                    **{m: round(flops / (ms[m] * 1e-3) / 1e12, 1) for m in ms},
+                    "aware_vs_grouped": round(ms["oblivious_grouped"] / ms["aware"], 4),
+                    "aware_vs_rowmajor": round(ms["oblivious_rowmajor"] / ms["aware"], 4)})
+        del Ad, Bd, C
+        torch.cuda.empty_cache()
+    return out
+
+
 def pd_sets(topo, halves):
     """The prefill / decode CU sets: 192 striped bits and the other 64; the
     XCD-aligned split with the decode pair taken from one affinity group."""
@@ -1120,11 +1153,13 @@ def mla_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 
 
 
 FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "attention_b1", "chunk_read", "mla", "mla_long", "mla16",
-         "copy")
+         "copy", "gemm16k")
 
 
-def focus_run(name: str, dev, stream, launches: int) -> dict:
+def focus_run(name: str, dev, stream, launches: int, mapping: str = "aware") -> dict:
     """One workload launched `launches` times after 3 warm-ups (for profiler runs):
+      gemm16k          the persistent GEMM at 16384^3 (operands beyond the memory-side
+                       cache), in `mapping` (--mapping-only; default aware)
       decode_gemm      small-M GEMM 32 x 14336 x 4096 (decode projection)
       grouped_small_m  grouped GEMM (32 groups of ~20 rows) x (6144, 7168), seed 5
       attention_gqa    decode attention, grouped-query, B = 64, S_k = 32768
@@ -1188,6 +1223,15 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
         fn = lambda: asym.copy(dst, src, passes=1, stream=stream)
         nbytes = 2 * workloads.COPY_BYTES
         kernel = "copy_kernel"
+    elif name == "gemm16k":
+        n = 16384
+        g = torch.Generator(device=dev).manual_seed(1)
+        A = (torch.rand((n, n), generator=g, device=dev) * 2 - 1).to(torch.bfloat16)
+        B = (torch.rand((n, n), generator=g, device=dev) * 2 - 1).to(torch.bfloat16)
+        C = torch.empty((n, n), dtype=torch.bfloat16, device=dev)
+        fn = lambda: asym.gemm(A, B, C, mapping=mapping, stream=stream)
+        nbytes = 3 * 2 * n * n
+        kernel = f"gemm_bf16_persistent<true, 8, 0, false> ({mapping})"
     elif name == "chunk_read":
         nb = 16 << 30
         raw = torch.empty(nb + (2 << 20), dtype=torch.uint8, device=dev)
@@ -1208,6 +1252,9 @@ def focus_run(name: str, dev, stream, launches: int) -> dict:
         ms = sum(fn()[0] for _ in range(launches)) / launches
     else:
         ms = queued({"f": fn}, launches, 1, stream)["f"]
+    if name == "gemm16k":
+        return {"focus": name, "kernel": kernel, "launches": launches, "ms_per_launch": round(ms, 5),
+                "tflops": round(2.0 * 16384 ** 3 / (ms * 1e-3) / 1e12, 1), "compulsory_bytes": int(nbytes)}
     return {"focus": name, "kernel": kernel, "launches": launches, "ms_per_launch": round(ms, 5),
             "algorithmic_bytes": int(nbytes), "TBps": round(nbytes / (ms * 1e-3) / 1e12, 3)}
 
@@ -1228,9 +1275,10 @@ def main() -> int:
                          "queue interception does not survive CU-masked stream creation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy 10 times (scale for byte counters)")
-    ap.add_argument("--studies", default="compare,grid,llm,pd,pd_trace,spread,balanced,grouped,numa,placed,attention,mla,parity",
+    ap.add_argument("--studies", default="compare,grid,large,llm,pd,pd_trace,spread,balanced,grouped,numa,placed,attention,mla,parity",
                     help="comma list of extra studies: compare (interleaved mappings at 8192^3), "
-                         "llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
+                         "grid (tile-column counts not multiples of 8), large (operands beyond the "
+                         "memory-side cache, 12288^3 to 16384^3), llm (decoder shapes), pd (prefill || decode), spread (128-CU sets), "
                          "grouped (expert-layer grouped GEMMs), numa (partition hash and local / "
                          "remote read bandwidth), attention (decode attention), mla (latent-"
                          "attention decode), parity (every "
@@ -1272,7 +1320,8 @@ def main() -> int:
         print(json.dumps({"copy_calibration_bytes_each_way": src.numel() * 2, "launches": 10}))
         return 0
     if args.focus:
-        print(json.dumps(focus_run(args.focus, dev, torch.cuda.current_stream(), args.steps)), flush=True)
+        print(json.dumps(focus_run(args.focus, dev, torch.cuda.current_stream(), args.steps,
+                                   args.mapping_only or "aware")), flush=True)
         return 0
     studies = set() if args.mapping_only or args.studies == "none" else set(args.studies.split(","))
     if args.probe == "identity":
@@ -1350,6 +1399,8 @@ def main() -> int:
         del Bt
     if "grid" in studies:
         line["tile_grid_shapes"] = grid_study(topo, dev, stream)
+    if "large" in studies:
+        line["beyond_mall_shapes"] = large_study(topo, dev, stream)
     if "llm" in studies:
         line["square_512"] = square_512(topo, dev, stream)
         line["llm_shapes_tflops"] = llm_shapes(dev, stream, 20)
