@@ -409,7 +409,7 @@ def grid_study(topo, dev, stream, launches: int = 20, settle_s: float = 1.0) -> 
     return out
 
 
-LARGE_SHAPES = ((16384, 16384, 16384), (16384, 15360, 16384), (12288, 12288, 12288))
+LARGE_SHAPES = ((16384, 16384, 16384), (16384, 15360, 16384), (16384, 15616, 16384), (12288, 12288, 12288))
 
 
 def large_study(topo, dev, stream, launches: int = 6, settle_s: float = 1.0) -> list:
