@@ -169,8 +169,8 @@ def test_mla_workgroup_form(dev, topo, B, Hq, S, split):
     64-head form's bits.  The workgroup forms round differently from the wave
     form (16-token blocks): both are checked against the oracle, on every head
     of the small shapes and on sampled heads of the long ones, and the
-    workgroup form's bits are the same on every mapping and on a CU-masked
-    stream."""
+    workgroup form's bits are the same on every mapping, on a CU-masked
+    stream and under whole-XCD restrictions."""
     p = workloads.MlaProblem(f"wg{B}_{Hq}_{S}", B, Hq, S, seed=S + 3 * Hq)
     q, kv = workloads.make_mla_inputs(p)
     qd, kvd = q.to(dev), kv.to(dev)
@@ -195,6 +195,10 @@ def test_mla_workgroup_form(dev, topo, B, Hq, S, split):
             assert torch.equal(O, got), "masked"
         finally:
             asym.stream_destroy(s)
+        for xm in (0x0F, 0x81):
+            O = asym.mla_decode(qd, kvd, split_tokens=split, topo=topo, xcd_mask=xm)
+            torch.cuda.synchronize()
+            assert torch.equal(O, got), hex(xm)
         asym.set_mla_workgroup_form(1)
         assert asym.mla_decode_plan(B, Hq, S, split_tokens=split, topo=topo)["workgroup_form"] == 1
         form1 = asym.mla_decode(qd, kvd, lse=lse_1, split_tokens=split, topo=topo)

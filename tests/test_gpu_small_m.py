@@ -38,7 +38,7 @@ def dev():
 
 
 @pytest.mark.parametrize("M", [1, 5, 16, 17, 31, 32, 33, 48, 63, 64, 65, 100, 128, 200, 256])
-@pytest.mark.parametrize("N,K", [(1000, 72), (96, 1000), (257, 4104), (40, 264)])  # <= 2 row-tile WGs per CU
+@pytest.mark.parametrize("N,K", [(1000, 72), (96, 1000), (257, 4104), (40, 264), (1001, 72)])  # <= 2 row-tile WGs per CU
 def test_small_m_elementwise(dev, M, N, K):
     p = workloads.make_problem(M, N, K, seed=100 + M)
     A, B = workloads.make_inputs(p)
