@@ -1249,18 +1249,18 @@ void release_workspace(hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_mu);
   for (auto it = g_ws.begin(); it != g_ws.end();) {
     if (it->first.second == s) {
-      hipFree(it->second.gemm_ctr);
-      if (it->second.attn_buf) hipFree(it->second.attn_buf);
-      if (it->second.attn_claim) hipFree(it->second.attn_claim);
-      if (it->second.sm_part) hipFree(it->second.sm_part);
-      if (it->second.kn_buf) hipFree(it->second.kn_buf);
-      for (auto& t : it->second.attn_off) hipFree(t.second);
+      (void)hipFree(it->second.gemm_ctr);
+      if (it->second.attn_buf) (void)hipFree(it->second.attn_buf);
+      if (it->second.attn_claim) (void)hipFree(it->second.attn_claim);
+      if (it->second.sm_part) (void)hipFree(it->second.sm_part);
+      if (it->second.kn_buf) (void)hipFree(it->second.kn_buf);
+      for (auto& t : it->second.attn_off) (void)hipFree(t.second);
       for (auto& t : it->second.g_tables) {
-        hipFree(t.desc);
-        hipFree(t.sched);
+        (void)hipFree(t.desc);
+        (void)hipFree(t.sched);
       }
-      if (it->second.g_host) hipHostFree(it->second.g_host);
-      if (it->second.g_copied) hipEventDestroy(it->second.g_copied);
+      if (it->second.g_host) (void)hipHostFree(it->second.g_host);
+      if (it->second.g_copied) (void)hipEventDestroy(it->second.g_copied);
       it = g_ws.erase(it);
     } else {
       ++it;

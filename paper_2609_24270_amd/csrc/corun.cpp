@@ -33,10 +33,10 @@ struct Guard {  // releases streams, events and sinks on every exit path
   std::vector<hipEvent_t> events;
   std::vector<void*> sinks;
   ~Guard() {
-    for (hipStream_t s : streams) hipStreamSynchronize(s);
-    for (hipEvent_t e : events) hipEventDestroy(e);
+    for (hipStream_t s : streams) (void)hipStreamSynchronize(s);
+    for (hipEvent_t e : events) (void)hipEventDestroy(e);
     for (hipStream_t s : streams) asym_stream_destroy(s);
-    for (void* p : sinks) hipFree(p);
+    for (void* p : sinks) (void)hipFree(p);
   }
 };
 

@@ -69,7 +69,7 @@ int probe_identity_run(int device, hipStream_t s, int n_blocks, std::vector<int3
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   rec.assign(4 * (size_t)n_blocks, -1);
   if (e == hipSuccess) e = hipMemcpy(rec.data(), d, sizeof(int32_t) * 4 * (size_t)n_blocks, hipMemcpyDeviceToHost);
-  hipFree(d);
+  (void)hipFree(d);
   if (e != hipSuccess) return hip_fail(e, "identity probe");
   for (int i = 0; i < n_blocks; ++i)
     if (rec[4 * i + 2] != i) return fail(ASYM_EHIP, "identity probe: a workgroup left no record");
@@ -96,7 +96,7 @@ static int probe_maskmap(int device, const Topology& t, const std::vector<int32_
     ASYM_HIP(hipExtStreamCreateWithCUMask(&s, ASYM_MASK_WORDS, mask));
     std::vector<int32_t> rec;
     int rc = probe_identity_run(device, s, n_blocks, rec);
-    hipStreamDestroy(s);
+    (void)hipStreamDestroy(s);
     if (rc != ASYM_OK) return rc;
     std::set<Key> seen;
     for (int i = 0; i < n_blocks; ++i) {
@@ -157,7 +157,7 @@ extern "C" int asym_probe_topology(int device, unsigned flags, const char* cache
   ASYM_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
   std::vector<int32_t> rec;
   rc = probe_identity_run(device, s, n_blocks, rec);
-  hipStreamDestroy(s);
+  (void)hipStreamDestroy(s);
   if (rc != ASYM_OK) return rc;
   Topology t;
   rc = build_topology(rec.data(), n_blocks, info.n_cus, info.n_xccs, nullptr, t);
