@@ -100,11 +100,15 @@ def test_mla_decode_bitwise_across_mappings_masks_and_restrictions(dev, topo):
         asym.mla_decode(qd, kvd, mapping="oblivious_grouped", topo=topo, xcd_mask=0x0F)
 
 
-@pytest.mark.parametrize("B,Hq,S", [(16, 128, 32768), (64, 16, 8192), (4, 128, 65536)])
+@pytest.mark.parametrize("B,Hq,S", [(16, 128, 32768), (64, 16, 8192), (4, 128, 65536), (64, 128, 32768)])
 def test_mla_decode_paper_sizes_sampled(dev, B, Hq, S):
     p = workloads.mla_problem(B, Hq, S)
     q, kv = workloads.make_mla_inputs_on(p, dev)
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    plan = asym.mla_decode_plan(B, Hq, S)
+    if (B, Hq, S) == (64, 128, 32768) and asym.device_query(0)["n_cus"] == 256:
+        # the 128-head form with splits lengthened to 4096 tokens (two tasks per CU)
+        assert (plan["workgroup_form"], plan["split_tokens"], plan["n_splits"]) == (2, 4096, 8), plan
     O = asym.mla_decode(q, kv, lse=lse)
     torch.cuda.synchronize()
     g = np.random.default_rng(B + Hq)
