@@ -352,6 +352,44 @@ def square_512(topo, dev, stream, launches: int = 50, rounds: int = 8):
                for m in MAPPINGS}}
 
 
+DECODE_SHAPES = ((32, 4096, 4096), (64, 4096, 4096), (32, 6144, 4096), (32, 4096, 14336), (32, 14336, 4096),
+                 (32, 10240, 4096), (128, 4096, 4096), (128, 14336, 4096))
+
+
+def decode_projections(dev, stream, launches: int = 20, rounds: int = 5) -> list:
+    """Decode-time projections (M = 32 to 128 rows of activations against a
+    weight matrix) on the small-M kernel, with its plan (column-tile width,
+    K ranges), and on the persistent kernel (aware); weights N(0, 0.02) and
+    activations N(0, 1) drawn on the GPU from seed 3; the weight-streaming rate
+    2 N K / time."""
+    import torch
+
+    import paper_2609_24270_amd as asym
+    out = []
+    for (M, N, K) in DECODE_SHAPES:
+        g = torch.Generator(device=dev).manual_seed(3)
+        A = torch.randn((M, K), generator=g, device=dev).to(torch.bfloat16)
+        B = (torch.randn((N, K), generator=g, device=dev) * 0.02).to(torch.bfloat16)
+        C = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        plan = asym.gemm_plan(A, B, C)
+        f = lambda: asym.gemm(A, B, C, stream=stream)
+        f()
+        t = {"small_m": queued({"s": f}, launches, rounds, stream)["s"]}
+        prev = asym.set_small_m(False)
+        try:
+            f()
+            t["persistent"] = queued({"p": f}, launches, rounds, stream)["p"]
+        finally:
+            asym.set_small_m(prev)
+        wbytes = 2 * N * K
+        out.append({"M": M, "N": N, "K": K, "tile_n": plan["tile_n"], "tiles_n": plan["tiles_n"],
+                    "k_splits": plan["k_splits"],
+                    **{k: {"us": round(1e3 * v, 2), "weights_TBps": round(wbytes / (v * 1e-3) / 1e12, 3)}
+                       for k, v in t.items()}})
+        del A, B, C
+    return out
+
+
 def decode_gemm(dev, stream, launches: int = 20, rounds: int = 5):
     """Decode projection 32 x 14336 x 4096 (N(0,0.02) weights, N(0,1) activations)
     on the full GPU: the small-M kernel and the persistent kernel (aware), and
@@ -1405,6 +1443,7 @@ def main() -> int:
         line["square_512"] = square_512(topo, dev, stream)
         line["llm_shapes_tflops"] = llm_shapes(dev, stream, 20)
         line["decode_gemm"] = decode_gemm(dev, stream)
+        line["decode_projections"] = decode_projections(dev, stream)
     if "pd" in studies:
         line["prefill_decode"] = prefill_decode(topo, dev, 10, halves, warm=100)
         line["prefill_decode_after_idle"] = prefill_decode(topo, dev, 10, halves, warm=0)

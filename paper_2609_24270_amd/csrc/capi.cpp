@@ -303,18 +303,35 @@ int small_m_ksplit(int M, int N, int K, int mb, int device_cus) {
   return ks;
 }
 
-// A single unsplit row tile whose 64-column tiles number fewer than the CUs
-// narrows them, to the multiple of 8 columns that gives about one tile per CU:
-// each CU then reads at most that many columns of B, and a CU reads HBM at
-// about 20-24 GB/s at most (the decode projection 32 x 14336 x 4096: 224 tiles
-// of 64 columns leave 32 CUs idle; 256 of 56 use them all).  A narrower wave or
-// an idle one at a tile's edge is the same case as the product's edge, and each
-// output is still one wave's MFMA chain over all of K: the bits do not change.
-int small_m_cols(int N, int row_tiles, int ksplit, int device_cus) {
+// An unsplit product takes the column-tile width, a multiple of 8 up to 64,
+// that minimises what the busiest CU reads: ceil(workgroups / CUs) x (the
+// tile's 16 mb rows of A + its columns of B, per k), since a CU reads at about
+// 20-24 GB/s at most.  A narrower width is taken only when that saves at least
+// 7% over 64 columns (the widest on ties; measured: 32 x 14336 x 4096, 256
+// tiles of 56 columns instead of 224 of 64, 8% less read and 4% faster;
+// 32 x 10240 x 4096 in 40 columns, 1.08x; 128 x 4096 x 4096 in 32 columns,
+// 1.25x; 128 x 14336 x 4096 in 56 columns would save 6% and ran 1.4% slower).
+// A wave with no columns at a tile's edge computes nothing; a narrower wave is
+// the same case as the product's edge, and each output is still one wave's
+// MFMA chain over all of K: the bits do not change.
+int small_m_cols(int N, int mb, int row_tiles, int ksplit, int device_cus) {
   const int w = small_m_tile_cols();
-  if (row_tiles != 1 || ksplit != 1 || device_cus < 1) return w;
-  if ((N + w - 1) / w >= device_cus) return w;
-  return std::min(w, 8 * ((N + 8 * device_cus - 1) / (8 * device_cus)));
+  if (ksplit != 1 || device_cus < 1 || row_tiles < 1) return w;
+  auto cost = [&](int c) {
+    const long long wgs = (long long)row_tiles * ((N + c - 1) / c);
+    return (wgs + device_cus - 1) / device_cus * (16 * mb + c);
+  };
+  const long long wide = cost(w);
+  int best = w;
+  long long best_cost = wide;
+  for (int c = w - 8; c >= 8; c -= 8) {
+    const long long k = cost(c);
+    if (k < best_cost && k * 100 <= wide * 93) {
+      best_cost = k;
+      best = c;
+    }
+  }
+  return best;
 }
 
 // The CU set a launch on `stream` may use: the device's topology (probed on
@@ -461,7 +478,7 @@ static SmallMLaunch small_m_launch(const GemmPlan& P, const void* A, const void*
   sm.order = small_m_order(mapping);
   sm.n_x = P.t->n_xccs;
   sm.ksplit = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
-  sm.tile_cols = small_m_cols(N, sm.row_tiles, sm.ksplit, P.t->n_cus);
+  sm.tile_cols = small_m_cols(N, P.small_mb, sm.row_tiles, sm.ksplit, P.t->n_cus);
   const int tiles_n = (N + sm.tile_cols - 1) / sm.tile_cols;
   sm.grid = small_m_grid(sm.row_tiles, tiles_n, sm.order, sm.n_x);
   if (sm.ksplit > 1) sm.grid = (long long)tiles_n * sm.ksplit;
@@ -1222,7 +1239,7 @@ int gemm_plan(const asym_topology* topo_in, int M, int N, int K, const void* A, 
     out->tile_m = 16 * P.small_mb;
     out->tiles_m = (M + out->tile_m - 1) / out->tile_m;
     out->k_splits = small_m_ksplit(M, N, K, P.small_mb, P.t->n_cus);
-    out->tile_n = small_m_cols(N, out->tiles_m, out->k_splits, P.t->n_cus);
+    out->tile_n = small_m_cols(N, P.small_mb, out->tiles_m, out->k_splits, P.t->n_cus);
     out->tiles_n = (N + out->tile_n - 1) / out->tile_n;
     out->grid = (int)small_m_grid(out->tiles_m, out->tiles_n, small_m_order(mapping), P.t->n_xccs);
     if (out->k_splits > 1) out->grid = out->tiles_n * out->k_splits;

@@ -184,24 +184,27 @@ __global__ void __launch_bounds__(SK_THREADS) gemm_bf16_small_m(SkinnyParams p) 
 
   // stage s uses LDS buffer s % 2 and B registers b0 (even) / b1 (odd); the
   // loads of stage s + 1 are in flight while stage s is computed
+  // a wave with no columns (past the tile's or the product's edge) stages A
+  // and meets the barriers but loads no B and computes nothing
+  const bool busy = cols > 0;
   bf16x8 b0[U], b1[U];
   v4u ar[A_PER];
   a_load(0, ar);
   a_store(0, ar);
   if (stages > 1) a_load(1, ar);
-  b_load(0, b0);
+  if (busy) b_load(0, b0);
   __syncthreads();
   for (int st = 0; st < stages; st += 2) {
-    if (st + 1 < stages) b_load(st + 1, b1);
-    compute(0, b0);
+    if (busy && st + 1 < stages) b_load(st + 1, b1);
+    if (busy) compute(0, b0);
     if (st + 1 < stages) {
       a_store(1, ar);
       if (st + 2 < stages) a_load(st + 2, ar);
     }
     __syncthreads();
     if (st + 1 >= stages) break;
-    if (st + 2 < stages) b_load(st + 2, b0);
-    compute(1, b1);
+    if (busy && st + 2 < stages) b_load(st + 2, b0);
+    if (busy) compute(1, b1);
     if (st + 2 < stages) {
       a_store(0, ar);
       if (st + 3 < stages) a_load(st + 3, ar);

@@ -124,7 +124,7 @@ struct SmallMLaunch {
 int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s);
 int small_m_blocks(int max_rows);  // 1, 2, 4, or 0 above 64 rows
 int small_m_tile_cols();           // the widest column tile (64)
-int small_m_cols(int N, int row_tiles, int ksplit, int device_cus);  // the width a plain launch takes
+int small_m_cols(int N, int mb, int row_tiles, int ksplit, int device_cus);  // the width a plain launch takes
 
 // Decode attention (head dimension 128).
 struct AttnLaunch {

@@ -63,15 +63,17 @@ def test_plan_picks_the_kernel(dev):
     B = torch.zeros((14336, 4096), dtype=torch.bfloat16, device=dev)
     assert asym.gemm_plan(A=A, B=B)["small_m"] == 0 and asym.gemm_plan(A=A[:128], B=B)["small_m"] == 1
     p65 = plan(65)
-    assert (p65["tile_m"], p65["tiles_m"], p65["grid"]) == (64, 2, 16)      # aware: 8 columns x 2 rows
-    assert plan(65, mapping="oblivious_rowmajor")["grid"] == 16
+    # two 64-row tiles of 512 columns: 8-column tiles (64 x 2 workgroups, every CU
+    # reading at most 8 columns of B; the aware grid pads 64 to a multiple of 8)
+    assert (p65["tile_m"], p65["tiles_m"], p65["tile_n"], p65["grid"]) == (64, 2, 8, 128)
+    assert plan(65, mapping="oblivious_rowmajor")["grid"] == 128
     assert plan(32, K=4100)["small_m"] == 0                       # K not a multiple of 8
     assert plan(32, xcd_mask=0x0F)["small_m"] == 0                # whole-XCD restriction
     p = plan(32)
     # 8 column tiles on 256 CUs: K split into 8 ranges (128 k-steps, at least 16 per range)
     assert (p["tile_n"], p["tiles_n"], p["k_splits"], p["grid"], p["claims"]) == (64, 8, 8, 64, 0)
     assert plan(32, K=256)["k_splits"] == 1 and plan(65)["k_splits"] == 1
-    assert plan(200, mapping="aware")["grid"] == 32 and plan(200, mapping="oblivious_grouped")["grid"] == 32
+    assert plan(200, mapping="aware")["grid"] == 256 and plan(200, mapping="oblivious_grouped")["grid"] == 256
     prev = asym.set_small_m(False)
     try:
         assert plan(32)["small_m"] == 0
@@ -259,11 +261,12 @@ def test_split_k_under_an_xcd_restriction(dev):
                   f"bitwise equal share {float(np.mean(C1 == C2)):.4f}")
 
 
-@pytest.mark.parametrize("M,N,K,width", [(32, 14336, 4096, 56), (32, 10240, 4096, 40), (40, 3000, 200, 16)])
+@pytest.mark.parametrize("M,N,K,width", [(32, 14336, 4096, 56), (32, 10240, 4096, 40), (40, 3000, 200, 16),
+                                         (128, 4096, 4096, 32), (128, 14336, 4096, 64), (100, 1000, 72, 8)])
 def test_narrow_column_tiles(dev, M, N, K, width):
-    """A single unsplit row tile with fewer 64-column tiles than CUs takes
-    narrower tiles (a multiple of 8 columns, about one per CU; a wave of 8
-    columns or an idle one at the tile's edge).  On exact-integer inputs it
+    """An unsplit product takes the column-tile width (a multiple of 8 up to
+    64) that minimises the columns of B the busiest CU reads (a wave of 8
+    columns or an idle one at the tile's edge; one or more row tiles).  On exact-integer inputs it
     equals the oracle and the persistent kernel bitwise; on real-valued ones
     every mapping gives the same bits and sampled columns match the oracle."""
     ncu = asym.device_query(0)["n_cus"]
