@@ -735,13 +735,22 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
   long long wgs64 = 0;
   for (int g = 0; g < G; ++g) wgs64 += (long long)((Ms[g] + 63) / 64) * ((N + small_m_tile_cols() - 1) / small_m_tile_cols());
   const int small_mb = small_m_for(P, max_rows, wgs64);
-  const int tiles_n = small_mb ? (N + small_m_tile_cols() - 1) / small_m_tile_cols() : (N + P.bn - 1) / P.bn;
+  // the small-M path's column-tile width, by the rule of a plain product over
+  // all the groups' row tiles
+  int small_w = small_m_tile_cols();
+  if (small_mb) {
+    long long rts = 0;
+    for (int g = 0; g < G; ++g) rts += (Ms[g] + 16 * small_mb - 1) / (16 * small_mb);
+    small_w = small_m_cols(N, small_mb, (int)std::min<long long>(rts, 1 << 30), 1, P.t->n_cus);
+  }
+  const int tiles_n = small_mb ? (N + small_w - 1) / small_w : (N + P.bn - 1) / P.bn;
   Workspace* ws = nullptr;
   rc = get_workspace(P.device, stream, &ws);
   if (rc != ASYM_OK) return rc;
   std::vector<int> key(Ms, Ms + G);
   key.push_back(N);
   key.push_back(small_mb ? -small_mb : P.bn);
+  key.push_back(small_mb ? small_w : 0);
   key.push_back(mapping);
   key.insert(key.end(), P.slots.begin(), P.slots.end());
   auto hit = std::find_if(ws->g_tables.begin(), ws->g_tables.end(),
@@ -752,7 +761,7 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
     Schedule sch;
     std::vector<int4> small_desc;
     if (small_mb) {
-      // one workgroup per (group, row tile, 64-column tile), in the mapping's
+      // one workgroup per (group, row tile, column tile), in the mapping's
       // order; the aware order runs a column's row tiles one after another on
       // one XCD (each group's run padded to a multiple of the XCD count with
       // empty entries, so the XCD of an entry is its column mod n)
@@ -767,7 +776,7 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
             small_desc.push_back(int4{0, 0, 0, 0});
             return;
           }
-          small_desc.push_back(int4{row0 + r * tr, std::min(tr, Ms[g] - r * tr), g * N, c * small_m_tile_cols()});
+          small_desc.push_back(int4{row0 + r * tr, std::min(tr, Ms[g] - r * tr), g * N, c * small_w});
         };
         if (R > 0) {
           if (order == 0) {
@@ -853,6 +862,7 @@ int gemm_grouped_bf16(const asym_topology* topo_in, int G, const int* Ms, int N,
     sm.n_x = P.t->n_xccs;
     sm.grid = T;
     sm.d_desc = tb.desc;
+    sm.tile_cols = small_w;
     return launch_gemm_small_m(sm, stream);
   }
 

@@ -52,7 +52,7 @@ struct SkinnyParams {
   int order;          // plain GEMM: 0 aware, 1 column-major, 2 row-major
   int n_x;            // XCDs (workgroup i runs on XCD i mod n_x)
   const int4* desc;   // grouped: per workgroup {first row, rows, first B row, first column}; rows 0 = none
-  int tile_cols;      // plain GEMM: columns per column tile (a multiple of 8, at most 64; grouped: 64)
+  int tile_cols;      // columns per column tile (a multiple of 8, at most 64)
   int ksplit;         // plain GEMM, one row tile: K ranges per column tile (1 = none)
   float* part;        // ksplit > 1: fp32 partial tiles [column tile][range][16 MB][64]
 };
@@ -289,9 +289,8 @@ int launch_gemm_small_m(const SmallMLaunch& g, hipStream_t s) {
   p.lda = g.lda;
   p.ldb = g.ldb;
   p.ldc = g.ldc;
-  if (g.tile_cols < 8 || g.tile_cols > SK_COLS || g.tile_cols % 8 || (g.d_desc && g.tile_cols != SK_COLS) ||
-      (g.ksplit > 1 && g.tile_cols != SK_COLS))
-    return fail(ASYM_EINVAL, "small-M GEMM: column tiles of 8 to 64 columns (64 when grouped or split)");
+  if (g.tile_cols < 8 || g.tile_cols > SK_COLS || g.tile_cols % 8 || (g.ksplit > 1 && g.tile_cols != SK_COLS))
+    return fail(ASYM_EINVAL, "small-M GEMM: column tiles of 8 to 64 columns (64 when split)");
   p.tile_cols = g.tile_cols;
   p.tiles_n = (g.N + g.tile_cols - 1) / g.tile_cols;
   p.row_tiles = g.row_tiles;
