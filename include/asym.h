@@ -736,7 +736,11 @@ int asym_gemm_set_small_m(int enable);
  * whole-XCD restriction); its workgroups read the XCD they run on and claim
  * groups of 4 tasks from that XCD's share, then from the others; the
  * oblivious mappings (both) hand out tasks round-robin by workgroup, an equal
- * share per XCD.  Every mapping gives the same bits.  fp32 partials live in a per-stream library workspace, grown
+ * share per XCD.  On a CU set with equal CUs per XCD over every XCD, when each
+ * claiming workgroup would hold one group at most and splits are at most 128
+ * tokens, a dense AWARE call deals its groups round-robin as the oblivious
+ * mappings do (there the shares are equal and claims only cost their round
+ * trips); asym_attn_decode_plan reports it.  Every mapping gives the same bits.  fp32 partials live in a per-stream library workspace, grown
  * (after a stream synchronisation) when a call needs more.  Asynchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
 int asym_attn_decode_bf16(const asym_topology* topo, int B, int H_q, int H_kv, int S_k, int D,
@@ -753,6 +757,10 @@ typedef struct asym_attn_plan_info {
   int n_xcds;
   int tasks_per_xcd[ASYM_MAX_XCDS];
   size_t workspace_bytes;  /* fp32 partials: B * H_q * n_splits * 130 * 4 */
+  int dense_static;        /* AWARE: 1 if a dense call deals its groups statically
+                              (grid = ceil(tasks / tasks_per_workgroup), no claims;
+                              grid and tasks_per_xcd above are the claiming launch's,
+                              which paged calls always take) */
 } asym_attn_plan_info;
 
 /* What asym_attn_decode_bf16 would launch (no pointers needed; launches

@@ -186,7 +186,8 @@ class GemmPlanInfo(ctypes.Structure):
 class AttnPlanInfo(ctypes.Structure):
     _fields_ = [("split_tokens", ctypes.c_int), ("n_splits", ctypes.c_int), ("tasks", ctypes.c_int),
                 ("grid", ctypes.c_int), ("tasks_per_workgroup", ctypes.c_int), ("n_xcds", ctypes.c_int),
-                ("tasks_per_xcd", ctypes.c_int * MAX_XCDS), ("workspace_bytes", ctypes.c_size_t)]
+                ("tasks_per_xcd", ctypes.c_int * MAX_XCDS), ("workspace_bytes", ctypes.c_size_t),
+                ("dense_static", ctypes.c_int)]
 
     def to_dict(self) -> dict:
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "tasks_per_xcd"}
@@ -919,7 +920,7 @@ def attn_pages_place(plan: dict, B: int, Hkv: int, S: int, pool_pages: int, poli
             for x, v in enumerate(plan["tasks_per_xcd"]):
                 info.tasks_per_xcd[x] = v
         else:
-            setattr(info, k, plan[k])
+            setattr(info, k, plan.get(k, 0) if k == "dense_static" else plan[k])
     pph = (S + PAGE_TOKENS - 1) // PAGE_TOKENS
     out = np.zeros((B, Hkv, pph), dtype=np.int32)
     home = None

@@ -5,7 +5,9 @@ sequence tails, a single token, and every supported ratio of query to
 key/value heads; on sampled requests at the paper's sizes (32 query heads,
 8 or 32 key/value heads, head dimension 128, long sequences).  Bitwise: every
 mapping, repeats, a CU-masked stream with unequal CUs per XCD and a whole-XCD
-restriction give the same bits.  The plan's task counts follow the CU counts.
+restriction give the same bits (the aware mapping both claiming and, on short
+splits over the whole chip, dealing statically).  The plan's task counts follow
+the CU counts.
 """
 import math
 
@@ -126,6 +128,14 @@ def test_plan_and_rejects(dev):
     plan = asym.attn_decode_plan(64, 32, 8, 32768)
     assert plan["split_tokens"] == 1024 and plan["tasks"] == 64 * 8 * 32
     assert plan["workspace_bytes"] == 64 * 32 * 32 * 130 * 4
+    # dense aware calls deal statically only on a uniform set of every XCD, one
+    # group per claiming workgroup at most and splits of at most 128 tokens
+    assert asym.attn_decode_plan(16, 32, 8, 1024)["dense_static"] == 1
+    assert asym.attn_decode_plan(1, 32, 8, 8192)["dense_static"] == 1
+    assert asym.attn_decode_plan(16, 32, 8, 8192)["dense_static"] == 0  # 512-token splits
+    assert asym.attn_decode_plan(16, 32, 8, 1024, split_tokens=256)["dense_static"] == 0
+    assert asym.attn_decode_plan(16, 32, 8, 1024, xcd_mask=0x0F)["dense_static"] == 0
+    assert asym.attn_decode_plan(16, 32, 8, 1024, mapping="oblivious_grouped")["dense_static"] == 0
     for kw in (dict(D=64), dict(Hkv=3), dict(split_tokens=20), dict(S=0)):
         args = dict(B=1, Hq=32, Hkv=8, S=128)
         args.update(kw)
