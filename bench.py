@@ -794,16 +794,22 @@ def balanced_study(topo, dev, iters: int = 20, repeats: int = 5, warm: int = 10)
     return out
 
 
-def queued(fns: dict, launches: int, rounds: int, stream) -> dict:
+def queued(fns: dict, launches: int, rounds: int, stream, warm_ms: float = 40.0) -> dict:
     """Mean per-launch ms of each fn for kernels too short to time from the
-    host: each round parks the stream on a spin kernel (about 8 ms) while the
-    host queues `launches` untimed launches of every variant in turn (the
-    clock recovers from the one-wave spin under them), then `launches`
-    back-to-back launches of each variant, each batch bracketed by HIP events
-    on the stream.  The order of the batches rotates from round to round and
-    the rounds are a multiple of the variant count, so every variant takes
-    every position equally often (a batch timed first after the spin runs in
-    another clock and power state than one timed last)."""
+    host: each round parks the stream on a spin kernel while the host queues,
+    behind it, untimed launches of every variant in turn adding up to about
+    `warm_ms` of GPU work (at most 512 launches), then `launches` back-to-back
+    launches of each variant, each batch bracketed by HIP events on the
+    stream.  The chip's clock and power control settle only some 25-50 ms
+    after an idle spell such as the one-wave spin: launches 2-8 ms after it
+    ran up to 1.3x slower than 50 ms after it.  The spin lasts long enough for
+    the host to queue every launch of the round behind it, so that none waits
+    on the host.  The order of the batches rotates from round to round and the
+    rounds are a multiple of the variant count, so every variant takes every
+    position equally often."""
+    import math
+    import time
+
     import torch
     names = list(fns)
     n = len(names)
@@ -814,13 +820,26 @@ def queued(fns: dict, launches: int, rounds: int, stream) -> dict:
         torch.cuda._sleep(1 << 20)
         b.record(stream)
     torch.cuda.synchronize()
-    spin = int((1 << 20) * 8.0 / max(a.elapsed_time(b), 1e-3))
+    cycles_per_ms = (1 << 20) / max(a.elapsed_time(b), 1e-3)
+    # GPU time of one launch of every variant, and the host's cost of a launch
+    probe = 3
+    a.record(stream)
+    h0 = time.perf_counter()
+    for _ in range(probe):
+        for k in names:
+            fns[k]()
+    host_ms = (time.perf_counter() - h0) * 1e3 / (probe * n)
+    b.record(stream)
+    torch.cuda.synchronize()
+    cycle_ms = max(a.elapsed_time(b) / probe, 1e-3)
+    warm = max(launches, min(math.ceil(warm_ms / cycle_ms), max(launches, 512 // n)))
+    spin = int(cycles_per_ms * max(8.0, 1.5 * host_ms * n * (warm + launches) + 2.0))
     evs = {k: [] for k in names}
     for r in range(rounds):
         order = names[r % n:] + names[:r % n]
         with torch.cuda.stream(stream):
             torch.cuda._sleep(spin)
-        for _ in range(launches):
+        for _ in range(warm):
             for k in order:
                 fns[k]()
         for k in order:
@@ -1190,8 +1209,8 @@ def mla_study(topo, dev, stream, masked: bool, launches: int = 5, rounds: int = 
     return {"configs": out, "uneven_cu_sets": uneven}
 
 
-FOCUS = ("decode_gemm", "grouped_small_m", "attention_gqa", "attention_b1", "chunk_read", "mla", "mla_long", "mla16",
-         "copy", "gemm16k")
+FOCUS = ("decode_gemm", "grouped_small_m", "grouped_expert", "attention_gqa", "attention_b1", "chunk_read", "mla",
+         "mla_long", "mla16", "copy", "gemm16k")
 
 
 def focus_run(name: str, dev, stream, launches: int, mapping: str = "aware") -> dict:
@@ -1200,6 +1219,8 @@ def focus_run(name: str, dev, stream, launches: int, mapping: str = "aware") -> 
                        cache), in `mapping` (--mapping-only; default aware)
       decode_gemm      small-M GEMM 32 x 14336 x 4096 (decode projection)
       grouped_small_m  grouped GEMM (32 groups of ~20 rows) x (6144, 7168), seed 5
+      grouped_expert   grouped GEMM (6 groups of ~1024 rows) x (6144, 7168), seed 1, on
+                       the persistent kernel, in `mapping`
       attention_gqa    decode attention, grouped-query, B = 64, S_k = 32768
       attention_b1     decode attention, grouped-query, B = 1, S_k = 32768 (latency-bound)
       chunk_read       strided read of a 16 GiB region in 8 KiB chunks, address order
@@ -1227,6 +1248,13 @@ def focus_run(name: str, dev, stream, launches: int, mapping: str = "aware") -> 
         fn = lambda: asym.gemm_grouped(A, B, Ms, C, stream=stream)
         nbytes = p.working_set_bytes
         kernel = "gemm_bf16_small_m<2, 8>"
+    elif name == "grouped_expert":
+        p = workloads.grouped_problem(6, 1024, 6144, 7168, seed=1)
+        Ms, A, B = workloads.make_grouped_inputs_on(p, dev)
+        C = torch.empty((sum(Ms), p.N), dtype=torch.bfloat16, device=dev)
+        fn = lambda: asym.gemm_grouped(A, B, Ms, C, mapping=mapping, stream=stream)
+        nbytes = p.working_set_bytes
+        kernel = f"gemm_bf16_persistent (grouped, {mapping})"
     elif name == "attention_gqa":
         p = workloads.attn_problem("gqa", 64, 32768)
         q, k, v = workloads.make_attn_inputs_on(p, dev)
