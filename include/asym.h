@@ -842,7 +842,12 @@ int asym_attn_pages_place(const asym_attn_plan_info* plan, int B, int H_kv, int 
  * rows cross into one XCD's L2 once.  The oblivious mappings (both) number
  * them head-block major and hand out 4 per workgroup in order, so the head
  * blocks of one split land on different XCDs and every XCD gets an equal
- * share.  Every mapping gives the same bits.  fp32 partials live in a
+ * share.  When a (request, split) is a single task (no two tasks read the
+ * same rows), on a CU set with equal CUs per XCD over every XCD and with
+ * each claiming workgroup holding one group of tasks at most, an AWARE call
+ * deals its tasks as the oblivious mappings do (the numberings coincide
+ * there, and claims could move no work); asym_mla_decode_plan reports it.
+ * Every mapping gives the same bits.  fp32 partials live in a
  * per-stream library workspace, grown (after a stream synchronisation) when a
  * call needs more.  Asynchronous.
  * Errors: ASYM_EINVAL, ASYM_EUNSUPPORTED, ASYM_EHIP. */
@@ -863,6 +868,9 @@ typedef struct asym_mla_plan_info {
   int tasks_per_xcd[ASYM_MAX_XCDS];
   int workgroup_form;      /* 0: wave form; 1: 64-head form; 2: 128-head form */
   size_t workspace_bytes;  /* fp32 partials: B * H_q * n_splits * 514 * 4 */
+  int static_deal;         /* AWARE: 1 if the call deals its tasks statically
+                              (grid = ceil(tasks / tasks_per_workgroup), no claims;
+                              grid and tasks_per_xcd above are the claiming launch's) */
 } asym_mla_plan_info;
 
 /* Which kernel forms asym_mla_decode_bf16 may take, for the process: 0 runs

@@ -160,7 +160,8 @@ class MlaPlanInfo(ctypes.Structure):
     _fields_ = [("split_tokens", ctypes.c_int), ("n_splits", ctypes.c_int), ("head_blocks", ctypes.c_int),
                 ("tasks", ctypes.c_int), ("grid", ctypes.c_int), ("tasks_per_workgroup", ctypes.c_int),
                 ("n_xcds", ctypes.c_int), ("tasks_per_xcd", ctypes.c_int * MAX_XCDS),
-                ("workgroup_form", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t)]
+                ("workgroup_form", ctypes.c_int), ("workspace_bytes", ctypes.c_size_t),
+                ("static_deal", ctypes.c_int)]
 
     def to_dict(self) -> dict:
         d = {k: getattr(self, k) for k, _ in self._fields_ if k != "tasks_per_xcd"}

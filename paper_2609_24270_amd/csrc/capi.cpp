@@ -1171,6 +1171,17 @@ static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
     int most = 0;
     for (int x = 0; x < n_x; ++x) most = std::max(most, (P->quota[x] + per_wg - 1) / per_wg);
     P->grid = std::max(1, std::min(most, P->cs.smax) * n_x);
+    // When a (request, split) is one task (16 heads in the wave form, one
+    // head group in a workgroup form) no two tasks read the same rows; on a
+    // set with equal CUs on every XCD, with each claiming workgroup holding
+    // one group at most, the claims can then move no work either.  Such a
+    // call deals its tasks as the oblivious grid does (the two numberings
+    // coincide when a (request, split) is one task).  Measured on the full
+    // chip, claiming: 128 heads, B=64, S=4096 107.6 against 102.5 us; 16
+    // heads, B=1, S=32768 37.1 against 35.7.
+    bool uniform = P->cs.whole;
+    for (int x = 0; x < n_x; ++x) uniform = uniform && P->cs.slots[x] == P->cs.smax && P->cs.smax > 0;
+    P->dense_static = uniform && hb == mla_form_head_blocks(form) && most <= P->cs.smax;
   } else {
     P->grid = (P->tasks + per_wg - 1) / per_wg;
   }
@@ -1197,9 +1208,12 @@ int mla_decode(const asym_topology* topo_in, int B, int Hq, int S, const void* q
   if (rc != ASYM_OK) return rc;
   const int n_x = P.cs.t->n_xccs;
   int* d_off = nullptr;
-  if (mapping == ASYM_MAP_AWARE) {
+  if (mapping == ASYM_MAP_AWARE && !P.dense_static) {
     rc = aware_share_offsets(ws, P.cs, P.quota, P.tasks, 1 + form, stream, &d_off);
     if (rc != ASYM_OK) return rc;
+  } else if (mapping == ASYM_MAP_AWARE) {
+    const int per_wg = form ? 1 : mla_tasks_per_workgroup();
+    P.grid = (P.tasks + per_wg - 1) / per_wg;
   }
   MlaLaunch a;
   a.q = q; a.kv = kv; a.o = o; a.lse = lse;
@@ -1238,6 +1252,7 @@ int mla_decode_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
   out->n_xcds = P.cs.t->n_xccs;
   out->workgroup_form = form;
   out->workspace_bytes = P.ws_bytes;
+  out->static_deal = P.dense_static ? 1 : 0;
   for (int x = 0; x < out->n_xcds && x < ASYM_MAX_XCDS; ++x) {
     if (mapping == ASYM_MAP_AWARE) {
       out->tasks_per_xcd[x] = P.quota[x];

@@ -98,6 +98,24 @@ def test_mla_decode_bitwise_across_mappings_masks_and_restrictions(dev, topo):
         assert torch.equal(O, ref), hex(xm)
     with pytest.raises(asym.AsymError):
         asym.mla_decode(qd, kvd, mapping="oblivious_grouped", topo=topo, xcd_mask=0x0F)
+    # 16 heads (the wave form): the full chip's aware call deals statically,
+    # a masked stream and a whole-XCD restriction claim; the same bits
+    p = workloads.MlaProblem("bw16", 2, 16, 700, seed=12)
+    q, kv = workloads.make_mla_inputs(p)
+    qd, kvd = q.to(dev), kv.to(dev)
+    assert asym.mla_decode_plan(2, 16, 700, topo=topo)["static_deal"] == 1
+    ref = asym.mla_decode(qd, kvd, topo=topo)
+    torch.cuda.synchronize()
+    s = asym.stream_create(topo, mask)
+    try:
+        O = asym.mla_decode(qd, kvd, topo=topo, stream=s)
+        s.synchronize()
+        assert torch.equal(O, ref), "wave form, masked"
+    finally:
+        asym.stream_destroy(s)
+    O = asym.mla_decode(qd, kvd, topo=topo, xcd_mask=0x81)
+    torch.cuda.synchronize()
+    assert torch.equal(O, ref), "wave form, 0x81"
 
 
 @pytest.mark.parametrize("B,Hq,S", [(16, 128, 32768), (64, 16, 8192), (4, 128, 65536), (64, 128, 32768)])
@@ -133,6 +151,13 @@ def test_mla_plan_shares_and_rejections(dev, topo):
     assert wide["workgroup_form"] == 2 and 2 * wide["tasks"] > 256
     small = asym.mla_decode_plan(16, 16, 32768, topo=topo)
     assert small["workgroup_form"] == 0 and small["tasks"] == 16 * small["n_splits"]
+    # the static deal: one task per (request, split) and one claiming group per
+    # workgroup at most, on a set with equal CUs per XCD over every XCD
+    assert wide["static_deal"] == 1 and small["static_deal"] == 1
+    assert full["static_deal"] == 0  # 512 tasks: two per workgroup, the claims balance them
+    assert one["static_deal"] == 0  # two head groups per (request, split) share its rows
+    assert asym.mla_decode_plan(64, 128, 4096, topo=topo, xcd_mask=0x0F)["static_deal"] == 0
+    assert asym.mla_decode_plan(64, 128, 4096, mapping="oblivious_grouped", topo=topo)["static_deal"] == 0
     assert sum(full["tasks_per_xcd"]) == full["tasks"] and max(full["tasks_per_xcd"]) - min(full["tasks_per_xcd"]) <= 1
     mask = workloads.random_mask_bits(4, 1, 128)[0]
     counts = topo.cuset_counts(mask)
@@ -142,6 +167,7 @@ def test_mla_plan_shares_and_rejections(dev, topo):
         ob = asym.mla_decode_plan(16, 128, 32768, mapping="oblivious_rowmajor", topo=topo, stream=s)
     finally:
         asym.stream_destroy(s)
+    assert aw["static_deal"] == 0
     T = aw["tasks"]
     for x in range(8):
         assert abs(aw["tasks_per_xcd"][x] - T * counts[x] / 128) < 1.0, (x, aw, counts)
