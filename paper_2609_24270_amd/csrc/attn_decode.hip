@@ -317,13 +317,14 @@ __global__ void __launch_bounds__(64 * AT_WAVES) attn_decode_split(AttnParams p)
 // Merge of the splits of every (request, head) row (split_merge.h).  It also
 // clears the aware form's claim counters for the next split launch on the
 // stream (the split launch is complete when the merge runs).
+template <int CH>
 __global__ void __launch_bounds__(64 * kMergeWaves) attn_decode_merge(const float* __restrict__ part_o,
                                                                       const float* __restrict__ part_ml, int rows,
                                                                       int n_splits, int wpr, uint16_t* __restrict__ o,
                                                                       float* __restrict__ lse, int* claim,
                                                                       int n_claim) {
-  if (claim && blockIdx.x == 0 && (int)threadIdx.x < n_claim) claim[threadIdx.x * kClaimStride] = 0;
-  merge_split_rows<AD>(part_o, part_ml, rows, n_splits, wpr, o, lse);
+  if (claim && blockIdx.x == 0 && blockIdx.y == 0 && (int)threadIdx.x < n_claim) claim[threadIdx.x * kClaimStride] = 0;
+  merge_split_rows<AD, CH>(part_o, part_ml, rows, n_splits, wpr, o, lse);
 }
 
 }  // namespace
@@ -377,9 +378,12 @@ int launch_attn_decode(const AttnLaunch& a, hipStream_t s) {
   ASYM_HIP(hipGetLastError());
   const int rows = a.B * a.Hq;
   const int wpr = merge_waves_per_row(a.n_splits), rows_per_wg = kMergeWaves / wpr;
-  hipLaunchKernelGGL(attn_decode_merge, dim3((unsigned)((rows + rows_per_wg - 1) / rows_per_wg)),
-                     dim3(64 * kMergeWaves), 0, s, a.part_o, a.part_ml, rows, a.n_splits, wpr,
-                     static_cast<uint16_t*>(a.o), a.lse, a.d_quota_off ? a.d_claim : nullptr, a.n_x);
+  const int groups = (rows + rows_per_wg - 1) / rows_per_wg;
+  const int ch = merge_column_chunks(groups, AD / 64);
+  auto merge = ch == 2 ? attn_decode_merge<2> : attn_decode_merge<1>;
+  hipLaunchKernelGGL(merge, dim3((unsigned)groups, (unsigned)ch), dim3(64 * kMergeWaves), 0, s, a.part_o, a.part_ml,
+                     rows, a.n_splits, wpr, static_cast<uint16_t*>(a.o), a.lse, a.d_quota_off ? a.d_claim : nullptr,
+                     a.n_x);
   ASYM_HIP(hipGetLastError());
   return ASYM_OK;
 }

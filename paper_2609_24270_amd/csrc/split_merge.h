@@ -7,7 +7,11 @@
 // `wpr` waves work on one row (1, 2, 4, 8 or 16, from the split count): wave
 // j of a row takes splits j, j + wpr, j + 2 wpr, ... and eight of them at a
 // time, so that many partial loads are in flight; the waves' sums are added in
-// wave order.  The order depends only on the split count, so every assignment of
+// wave order.  A row's D columns may be cut into CH chunks, one per workgroup
+// (the grid's second dimension), so that rows with many splits are read by
+// more CUs; every workgroup of a row computes M and L the same way, and each
+// output element is summed over the same splits in the same order whatever
+// CH is.  The order depends only on the split count, so every assignment of
 // the splits to workgroups gives the same bits.
 #pragma once
 #include <hip/hip_runtime.h>
@@ -17,25 +21,54 @@
 namespace asym {
 namespace {
 
-constexpr int kMergeWaves = 16;  // waves per merge workgroup
+constexpr int kMergeWaves = 16;        // waves per merge workgroup
+constexpr int kMergeTargetGroups = 256;  // merge workgroups wanted (one per CU of the chip)
 
-// D: floats per row (128 or 512); lane l holds D / 64 consecutive values.
-template <int D>
+// a lane's values: a vector of N floats, or one float (an asm operand cannot
+// be a one-element vector)
+template <int N>
+struct MergeVec {
+  typedef float type __attribute__((ext_vector_type(N)));
+};
+template <>
+struct MergeVec<1> {
+  typedef float type;
+};
+template <int N>
+__device__ __forceinline__ float vget(const typename MergeVec<N>::type& v, int e) {
+  if constexpr (N == 1)
+    return v;
+  else
+    return v[e];
+}
+template <int N>
+__device__ __forceinline__ void vset(typename MergeVec<N>::type& v, int e, float f) {
+  if constexpr (N == 1)
+    v = f;
+  else
+    v[e] = f;
+}
+
+// D: floats per row (128 or 512), CH: column chunks per row; lane l holds
+// D / (64 CH) consecutive values of its chunk.
+template <int D, int CH>
 __device__ __forceinline__ void merge_split_rows(const float* __restrict__ part_o, const float* __restrict__ part_ml,
                                                  int rows, int n_splits, int wpr, uint16_t* __restrict__ o,
                                                  float* __restrict__ lse) {
-  constexpr int DPL = D / 64;
-  static_assert(DPL == 2 || DPL == 8, "rows of 128 or 512 values");
-  __shared__ float red[kMergeWaves][D];
+  constexpr int DC = D / CH;  // columns of this workgroup's chunk
+  constexpr int DPL = DC / 64;
+  static_assert(DPL == 1 || DPL == 2 || DPL == 4 || DPL == 8, "1 to 8 values per lane");
+  __shared__ float red[kMergeWaves][DC];
   __shared__ float red_m[kMergeWaves], red_l[kMergeWaves];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rows_per_wg = kMergeWaves / wpr;
   const int row = blockIdx.x * rows_per_wg + wave / wpr;
+  const int c0 = (int)blockIdx.y * DC + DPL * lane;  // this lane's first column
   const int sub = wave % wpr;
   const int lead = wave - sub;  // first wave of this row
   const bool valid = row < rows;
   const float* ml = part_ml + (size_t)(valid ? row : 0) * n_splits * 2;
-  const float* po = part_o + (size_t)(valid ? row : 0) * n_splits * D + DPL * lane;
+  const float* po = part_o + (size_t)(valid ? row : 0) * n_splits * D + c0;
 
   // the row's max over every split: the lanes of a wave read 64 of its
   // splits at a time, then the waves' maxima are combined
@@ -49,7 +82,7 @@ __device__ __forceinline__ void merge_split_rows(const float* __restrict__ part_
   float M = -INFINITY;
   for (int j = 0; j < wpr; ++j) M = fmaxf(M, red_m[lead + j]);
 
-  typedef float vrow __attribute__((ext_vector_type(DPL)));
+  typedef typename MergeVec<DPL>::type vrow;
   vrow acc = {};
   float L = 0.f;
   auto load = [&](int s, vrow& x, float2& q) {
@@ -60,7 +93,7 @@ __device__ __forceinline__ void merge_split_rows(const float* __restrict__ part_
     const float w = __expf(q.x - M);
     L = fmaf(q.y, w, L);
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = fmaf(x[e], w, acc[e]);
+    for (int e = 0; e < DPL; ++e) vset<DPL>(acc, e, fmaf(vget<DPL>(x, e), w, vget<DPL>(acc, e)));
   };
   if (valid) {
     int s = sub;
@@ -87,35 +120,41 @@ __device__ __forceinline__ void merge_split_rows(const float* __restrict__ part_
   }
   if (wpr > 1) {
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) red[wave][DPL * lane + e] = acc[e];
+    for (int e = 0; e < DPL; ++e) red[wave][DPL * lane + e] = vget<DPL>(acc, e);
     if (lane == 0) red_l[wave] = L;
   }
   __syncthreads();
   if (!valid || sub != 0) return;
   if (wpr > 1) {
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = red[lead][DPL * lane + e];
+    for (int e = 0; e < DPL; ++e) vset<DPL>(acc, e, red[lead][DPL * lane + e]);
     L = red_l[lead];
     for (int j = 1; j < wpr; ++j) {
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[e] += red[lead + j][DPL * lane + e];
+      for (int e = 0; e < DPL; ++e) vset<DPL>(acc, e, vget<DPL>(acc, e) + red[lead + j][DPL * lane + e]);
       L += red_l[lead + j];
     }
   }
   const float inv = 1.f / L;
-  uint32_t packed[DPL / 2];
+  uint16_t* dst = o + (size_t)row * D + c0;
+  if constexpr (DPL == 1) {
+    *dst = __builtin_bit_cast(unsigned short, (__bf16)(vget<DPL>(acc, 0) * inv));
+  } else {
+    uint32_t packed[DPL / 2];
 #pragma unroll
-  for (int e = 0; e < DPL / 2; ++e) {
-    const __bf16 lo = (__bf16)(acc[2 * e] * inv), hi = (__bf16)(acc[2 * e + 1] * inv);
-    packed[e] = (uint32_t)__builtin_bit_cast(unsigned short, lo) |
-                ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
+    for (int e = 0; e < DPL / 2; ++e) {
+      const __bf16 lo = (__bf16)(vget<DPL>(acc, 2 * e) * inv), hi = (__bf16)(vget<DPL>(acc, 2 * e + 1) * inv);
+      packed[e] = (uint32_t)__builtin_bit_cast(unsigned short, lo) |
+                  ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
+    }
+    if constexpr (DPL == 8)
+      *reinterpret_cast<uint4*>(dst) = uint4{packed[0], packed[1], packed[2], packed[3]};
+    else if constexpr (DPL == 4)
+      *reinterpret_cast<uint2*>(dst) = uint2{packed[0], packed[1]};
+    else
+      *reinterpret_cast<uint32_t*>(dst) = packed[0];
   }
-  uint16_t* dst = o + (size_t)row * D + DPL * lane;
-  if constexpr (DPL == 8)
-    *reinterpret_cast<uint4*>(dst) = uint4{packed[0], packed[1], packed[2], packed[3]};
-  else
-    *reinterpret_cast<uint32_t*>(dst) = packed[0];
-  if (lse && lane == 0) lse[row] = M + __logf(L);
+  if (lse && blockIdx.y == 0 && lane == 0) lse[row] = M + __logf(L);
 }
 
 // waves per row for a split count: enough that each wave merges about 8 splits
@@ -123,6 +162,14 @@ inline int merge_waves_per_row(int n_splits) {
   int w = 1;
   while (w < kMergeWaves && w * 8 < n_splits) w *= 2;
   return w;
+}
+
+// column chunks per row (a power of two, at most max_chunks): enough that the
+// merge's workgroups number about kMergeTargetGroups
+inline int merge_column_chunks(int row_groups, int max_chunks) {
+  int ch = 1;
+  while (ch < max_chunks && row_groups * ch < kMergeTargetGroups) ch *= 2;
+  return ch;
 }
 
 }  // namespace
