@@ -824,7 +824,8 @@ int asym_attn_pages_place(const asym_attn_plan_info* plan, int B, int H_kv, int 
  * longest of 1024, 512, ... 32 giving at least 1024 blocks of 16 heads times
  * splits, lengthened until there are at most 256 splits, and in the
  * workgroup forms further, up to 8192, while at least two tasks per CU of the
- * set remain; else a multiple of 32); a task is one (request, split, block of 16 query heads) on one wave
+ * set remain; a split of 1024 tokens or more is halved when that gives the
+ * 128-head form more tasks than half the set's CUs; else a multiple of 32); a task is one (request, split, block of 16 query heads) on one wave
  * of the matrix cores (wave form, 16-token blocks), or, when H_q is a
  * multiple of 64, one (request, split, four blocks of 16 heads) on one
  * workgroup whose four waves share each 32-token block of rows through LDS

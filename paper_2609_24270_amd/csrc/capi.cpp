@@ -1138,8 +1138,19 @@ static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
   // measured at one request, 128 heads, 32K tokens: 47.6 against 37.7 us)
   const int allow = g_mla_form.load();
   const int set_cus = P->cs.total;
-  const int64_t t128 = (int64_t)B * n_splits * (hb / mla_form_head_blocks(2));
+  int64_t t128 = (int64_t)B * n_splits * (hb / mla_form_head_blocks(2));
   const bool fits128 = hb % mla_form_head_blocks(2) == 0;
+  // An automatic split of 1024 tokens or more is halved when that gives the
+  // 128-head form more tasks than half the CU set (the rule below then takes
+  // it): 512-token splits keep its tasks long enough (measured at 128 heads,
+  // B=8, S=16384: 62.4 us against 73.0 in the 64-head form's 1024-token
+  // splits; B=32, S=4096: 65.5 against 73.8), shorter ones do not (B=16,
+  // S=4096: 49.0 in 256-token splits against 47.3 for the 64-head form's 512).
+  if (!split_in && allow == 2 && fits128 && L >= 1024 && 2 * t128 <= set_cus && 4 * t128 > set_cus) {
+    L /= 2;
+    n_splits = (S + L - 1) / L;
+    t128 = (int64_t)B * n_splits * (hb / mla_form_head_blocks(2));
+  }
   const int form = allow >= 3 && fits128                         ? 2
                    : allow >= 2 && fits128 && 2 * t128 > set_cus ? 2
                    : allow >= 1 && hb % mla_form_head_blocks(1) == 0 ? 1

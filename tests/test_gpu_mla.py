@@ -149,6 +149,12 @@ def test_mla_plan_shares_and_rejections(dev, topo):
     assert one["workgroup_form"] == 1 and 2 * one["n_splits"] <= 256
     wide = asym.mla_decode_plan(64, 128, 4096, topo=topo)
     assert wide["workgroup_form"] == 2 and 2 * wide["tasks"] > 256
+    # an automatic split of 1024 tokens is halved when that lets the 128-head
+    # form fill the chip; 512-token splits are not
+    mid = asym.mla_decode_plan(8, 128, 16384, topo=topo)
+    assert (mid["workgroup_form"], mid["split_tokens"], mid["tasks"]) == (2, 512, 256), mid
+    kept = asym.mla_decode_plan(16, 128, 4096, topo=topo)
+    assert (kept["workgroup_form"], kept["split_tokens"]) == (1, 512), kept
     small = asym.mla_decode_plan(16, 16, 32768, topo=topo)
     assert small["workgroup_form"] == 0 and small["tasks"] == 16 * small["n_splits"]
     # the static deal: one task per (request, split) and one claiming group per
