@@ -843,11 +843,10 @@ int asym_attn_pages_place(const asym_attn_plan_info* plan, int B, int H_kv, int 
  * rows cross into one XCD's L2 once.  The oblivious mappings (both) number
  * them head-block major and hand out 4 per workgroup in order, so the head
  * blocks of one split land on different XCDs and every XCD gets an equal
- * share.  When a (request, split) is a single task (no two tasks read the
- * same rows), on a CU set with equal CUs per XCD over every XCD and with
- * each claiming workgroup holding one group of tasks at most, an AWARE call
- * deals its tasks as the oblivious mappings do (the numberings coincide
- * there, and claims could move no work); asym_mla_decode_plan reports it.
+ * share.  On a CU set with equal CUs per XCD over every XCD, when each
+ * claiming workgroup would hold one group of tasks at most (every task runs
+ * at once and claims could move no work), an AWARE call deals its tasks as
+ * the oblivious mappings do; asym_mla_decode_plan reports it.
  * Every mapping gives the same bits.  fp32 partials live in a
  * per-stream library workspace, grown (after a stream synchronisation) when a
  * call needs more.  Asynchronous.

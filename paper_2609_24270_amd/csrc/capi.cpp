@@ -1182,17 +1182,18 @@ static int mla_plan(const asym_topology* topo_in, int B, int Hq, int S, int spli
     int most = 0;
     for (int x = 0; x < n_x; ++x) most = std::max(most, (P->quota[x] + per_wg - 1) / per_wg);
     P->grid = std::max(1, std::min(most, P->cs.smax) * n_x);
-    // When a (request, split) is one task (16 heads in the wave form, one
-    // head group in a workgroup form) no two tasks read the same rows; on a
-    // set with equal CUs on every XCD, with each claiming workgroup holding
-    // one group at most, the claims can then move no work either.  Such a
-    // call deals its tasks as the oblivious grid does (the two numberings
-    // coincide when a (request, split) is one task).  Measured on the full
-    // chip, claiming: 128 heads, B=64, S=4096 107.6 against 102.5 us; 16
-    // heads, B=1, S=32768 37.1 against 35.7.
+    // On a set with equal CUs on every XCD, with each claiming workgroup
+    // holding one group at most, the claims can move no work: every task runs
+    // at once, and the head groups of a split that could share its rows
+    // through one L2 read a working set the memory-side cache holds (so few
+    // tasks mean few requests and short splits).  Such a call deals its tasks
+    // as the oblivious grid does.  Measured on the full chip, claiming
+    // against dealing: 128 heads, B=64, S=4096 107.6 against 102.5 us; 16
+    // heads, B=1, S=32768 37.1 against 35.7; 128 heads (two head groups per
+    // split), B=1, S=32768 35.3 against 34.3.
     bool uniform = P->cs.whole;
     for (int x = 0; x < n_x; ++x) uniform = uniform && P->cs.slots[x] == P->cs.smax && P->cs.smax > 0;
-    P->dense_static = uniform && hb == mla_form_head_blocks(form) && most <= P->cs.smax;
+    P->dense_static = uniform && most <= P->cs.smax;
   } else {
     P->grid = (P->tasks + per_wg - 1) / per_wg;
   }
