@@ -118,7 +118,8 @@ def test_mla_decode_bitwise_across_mappings_masks_and_restrictions(dev, topo):
     assert torch.equal(O, ref), "wave form, 0x81"
 
 
-@pytest.mark.parametrize("B,Hq,S", [(16, 128, 32768), (64, 16, 8192), (4, 128, 65536), (64, 128, 32768)])
+@pytest.mark.parametrize("B,Hq,S", [(16, 128, 32768), (64, 16, 8192), (4, 128, 65536), (64, 128, 32768),
+                                    (8, 128, 16384), (1, 16, 32768)])
 def test_mla_decode_paper_sizes_sampled(dev, B, Hq, S):
     p = workloads.mla_problem(B, Hq, S)
     q, kv = workloads.make_mla_inputs_on(p, dev)
@@ -127,6 +128,12 @@ def test_mla_decode_paper_sizes_sampled(dev, B, Hq, S):
     if (B, Hq, S) == (64, 128, 32768) and asym.device_query(0)["n_cus"] == 256:
         # the 128-head form with splits lengthened to 4096 tokens (two tasks per CU)
         assert (plan["workgroup_form"], plan["split_tokens"], plan["n_splits"]) == (2, 4096, 8), plan
+    if (B, Hq, S) == (8, 128, 16384) and asym.device_query(0)["n_cus"] == 256:
+        # the automatic 1024-token split halved for the 128-head form
+        assert (plan["workgroup_form"], plan["split_tokens"]) == (2, 512), plan
+    if (B, Hq, S) == (1, 16, 32768):
+        # 256 splits: 16 waves per row, and the 16 rows' columns cut over 8 merge workgroups
+        assert plan["n_splits"] == 256, plan
     O = asym.mla_decode(q, kv, lse=lse)
     torch.cuda.synchronize()
     g = np.random.default_rng(B + Hq)
